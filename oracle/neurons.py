@@ -1,0 +1,75 @@
+"""Leaky integrate-and-fire neuron model (paper Sec. 2.1.3 names SimLIF and
+Sec. 3.2 / 5.2.1 its rate approximation; the paper defers the equations to Nengo,
+so they are stated here from the membrane equation dV/dt = (J - V) / tau_rc with
+threshold 1, reset 0 and an absolute refractory period tau_ref).
+
+Pins (tests/test_oracle_neurons.py):
+  lif_rate        closed form 1/(tau_ref - tau_rc ln(1 - 1/J)); printed values
+  lif_step        exact spike steps ceil(t_j / dt) for constant J; long-run rate
+  gain_bias       r(g + b) == max_rate and g * intercept + b == 1
+"""
+import numpy as np
+
+
+def lif_rate(J, tau_rc, tau_ref):
+    """Steady-state firing rate (Hz) of a LIF neuron driven by constant current J.
+
+    Time to climb from 0 to threshold 1 is tau_rc * ln(J / (J - 1)); one period
+    adds the refractory time.  Zero for J <= 1 (threshold never reached).
+    """
+    J = np.asarray(J, dtype=np.float64)
+    out = np.zeros_like(J)
+    m = J > 1.0
+    out[m] = 1.0 / (tau_ref + tau_rc * np.log1p(1.0 / (J[m] - 1.0)))
+    return out
+
+
+def gain_bias(max_rates, intercepts, tau_rc, tau_ref):
+    """Gain and bias so that a neuron starts firing at x = intercept and fires at
+    max_rate at x = 1 (radius 1): J(x) = gain * x + bias.
+
+    r(J_max) = max_rate gives J_max = 1 / (1 - exp((tau_ref - 1/max_rate) / tau_rc));
+    J(intercept) = 1 and J(1) = J_max fix the line.
+    """
+    max_rates = np.asarray(max_rates, dtype=np.float64)
+    intercepts = np.asarray(intercepts, dtype=np.float64)
+    j_max = 1.0 / -np.expm1((tau_ref - 1.0 / max_rates) / tau_rc)
+    gain = (j_max - 1.0) / (1.0 - intercepts)
+    bias = 1.0 - gain * intercepts
+    return gain, bias
+
+
+def lif_step(J, V, ref, dt, tau_rc, tau_ref, amplitude):
+    """One timestep of the spiking LIF model, elementwise; returns (s, V, ref).
+
+    V integrates exactly for the part of the step that is not refractory
+    (dt - ref, clipped to [0, dt]).  Crossing 1 (strictly) emits one spike of
+    height amplitude/dt; the crossing time is recovered from the overshoot by
+    inverting the exponential approach, so the refractory period is measured from
+    the crossing itself and not from the step boundary.  V is floored at 0.
+    """
+    J = np.asarray(J, dtype=np.float64)
+    V = np.array(V, dtype=np.float64, copy=True)
+    ref = np.array(ref, dtype=np.float64, copy=True)
+    integ = np.clip(dt - ref, 0.0, dt)
+    V = V - (J - V) * np.expm1(-integ / tau_rc)
+    ref = np.maximum(ref - dt, 0.0)
+    spiked = V > 1.0
+    since = np.zeros_like(V)
+    drive = J - 1.0
+    ok = spiked & (drive > 0.0)
+    q = np.zeros_like(V)
+    q[ok] = (V[ok] - 1.0) / drive[ok]
+    full = ok & (q >= 1.0)
+    part = ok & (q < 1.0)
+    since[full] = integ[full]
+    since[part] = np.minimum(-tau_rc * np.log1p(-q[part]), integ[part])
+    V = np.where(spiked, 0.0, np.maximum(V, 0.0))
+    ref = np.where(spiked, tau_ref - since, ref)
+    s = np.where(spiked, amplitude / dt, 0.0)
+    return s, V, ref
+
+
+def lif_rate_output(J, tau_rc, tau_ref, amplitude):
+    """Rate-mode neuron output: amplitude * r(J)."""
+    return amplitude * lif_rate(J, tau_rc, tau_ref)

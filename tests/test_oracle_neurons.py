@@ -1,0 +1,97 @@
+"""Pins for oracle/neurons.py against closed forms of the LIF model."""
+import math
+
+import numpy as np
+import pytest
+
+from oracle.neurons import gain_bias, lif_rate, lif_step
+
+TAU_RC, TAU_REF, DT = 0.02, 0.002, 0.001
+
+
+def test_rate_closed_form_values():
+    # r(J) = 1 / (tau_ref - tau_rc ln(1 - 1/J)); hand-evaluated:
+    # r(2) = 1/(0.002 + 0.02 ln 2)      = 63.0400 Hz
+    # r(5) = 1/(0.002 + 0.02 ln(5/4))   = 154.730 Hz
+    r = lif_rate(np.array([2.0, 5.0]), TAU_RC, TAU_REF)
+    assert r[0] == pytest.approx(63.0400, abs=5e-4)
+    assert r[1] == pytest.approx(154.730, abs=5e-3)
+
+
+def test_rate_matches_log_form_and_is_zero_below_threshold():
+    J = np.linspace(-3.0, 60.0, 2001)
+    r = lif_rate(J, TAU_RC, TAU_REF)
+    above = J > 1
+    ref = 1.0 / (TAU_REF - TAU_RC * np.log(1.0 - 1.0 / J[above]))
+    np.testing.assert_allclose(r[above], ref, rtol=1e-13)
+    assert np.all(r[~above] == 0.0)
+    assert np.all(np.diff(r[above]) > 0)          # monotone in J
+    assert r.max() < 1.0 / TAU_REF                 # refractory period caps the rate
+
+
+@pytest.mark.parametrize("J", [1.2, 2.0, 5.0, 40.0])
+def test_spike_steps_match_closed_form(J):
+    """Constant J from V = 0: crossing j happens at t_j = t1 + (j-1)(tau_ref + t1),
+    t1 = tau_rc ln(J/(J-1)); it is reported in step ceil(t_j / dt)."""
+    n_steps = 5000
+    V = np.zeros(1); ref = np.zeros(1)
+    steps = []
+    for k in range(1, n_steps + 1):
+        s, V, ref = lif_step(np.array([J]), V, ref, DT, TAU_RC, TAU_REF, 1.0)
+        if s[0] > 0:
+            assert s[0] == pytest.approx(1.0 / DT)
+            steps.append(k)
+    t1 = TAU_RC * math.log(J / (J - 1.0))
+    period = TAU_REF + t1
+    expect = []
+    j = 0
+    while True:
+        t = t1 + j * period
+        k = math.ceil(t / DT - 1e-9)
+        if k > n_steps:
+            break
+        expect.append(k)
+        j += 1
+    assert steps == expect
+    # long-run rate equals the rate curve
+    rate = len(steps) / (n_steps * DT)
+    assert rate == pytest.approx(lif_rate(np.array([J]), TAU_RC, TAU_REF)[0], rel=2e-3)
+
+
+@pytest.mark.parametrize("J", [-5.0, 0.0, 0.5, 1.0])
+def test_subthreshold_never_spikes_and_converges(J):
+    V = np.zeros(1); ref = np.zeros(1)
+    for _ in range(3000):
+        s, V, ref = lif_step(np.array([J]), V, ref, DT, TAU_RC, TAU_REF, 1.0)
+        assert s[0] == 0.0
+    assert V[0] == pytest.approx(max(J, 0.0), abs=1e-12)
+
+
+def test_partial_refractory_integrates_remaining_time():
+    # ref = 0.4 ms left: only 0.6 ms of integration this step
+    J = np.array([3.0]); V = np.array([0.0]); ref = np.array([0.0004])
+    s, V2, ref2 = lif_step(J, V, ref, DT, TAU_RC, TAU_REF, 1.0)
+    assert s[0] == 0.0 and ref2[0] == 0.0
+    assert V2[0] == pytest.approx(3.0 * (1 - math.exp(-0.0006 / TAU_RC)), rel=1e-14)
+    # fully refractory: no integration
+    s, V3, ref3 = lif_step(J, np.array([0.0]), np.array([0.0015]), DT, TAU_RC, TAU_REF, 1.0)
+    assert V3[0] == 0.0 and ref3[0] == pytest.approx(0.0005)
+
+
+def test_spike_sets_refractory_from_crossing_time():
+    # start just below threshold: crossing time inside the step is recoverable
+    J = np.array([2.0]); V0 = 0.99
+    s, V, ref = lif_step(J, np.array([V0]), np.array([0.0]), DT, TAU_RC, TAU_REF, 2.5)
+    t_cross = TAU_RC * math.log((J[0] - V0) / (J[0] - 1.0))
+    assert s[0] == pytest.approx(2.5 / DT)
+    assert V[0] == 0.0
+    assert ref[0] == pytest.approx(TAU_REF - (DT - t_cross), rel=1e-12)
+
+
+def test_gain_bias_invariants():
+    rng = np.random.default_rng(0)
+    m = rng.uniform(200, 400, 1000); c = rng.uniform(-0.99, 0.99, 1000)
+    g, b = gain_bias(m, c, TAU_RC, TAU_REF)
+    np.testing.assert_allclose(g * c + b, 1.0, rtol=0, atol=1e-12 * np.abs(g).max())
+    np.testing.assert_allclose(lif_rate(g + b, TAU_RC, TAU_REF), m, rtol=1e-12)
+    assert np.all(g > 0)
