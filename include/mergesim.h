@@ -1,0 +1,260 @@
+/*
+ * mergesim -- merged-operator spiking-network simulator for one MI355X (gfx950).
+ *
+ * C ABI.  Every entry point returns an ms_status (0 = MS_OK, negative = error)
+ * except the destroy functions and ms_last_error.  No C++ exception crosses this
+ * boundary.  On error, ms_last_error() returns a thread-local message describing
+ * the last failure of a call made on the calling thread.
+ *
+ * The operation follows the problem statement of the NengoDL paper
+ * (Rasmussen 2018):
+ *   - a model is a Network of Nodes, Ensembles, Connections and Probes
+ *     (Sec. 2.1.2); the builder lowers it to Signals and Operators (Sec. 2.1.3,
+ *     Fig. 2: a connection is DotInc -> synaptic filter -> Copy into the post);
+ *   - the simulator merges signals into base arrays and operators into groups,
+ *     plans the group order, sorts signals for contiguous reads and simplifies
+ *     special cases (Sec. 4.2, Alg. 1 and Alg. 2);
+ *   - run(n_steps) advances the simulation with per-node input feeds shaped
+ *     [minibatch][timesteps][dims] (Sec. 3.1); probes record one sample per
+ *     step, read back as [minibatch][timesteps][dims]; reset() restores the
+ *     initial state (Sec. 3.1).
+ *
+ * Ownership: the caller owns every array it passes in; the library copies model
+ * descriptions during the ms_model_add_* call and copies feeds during
+ * ms_sim_run_steps.  The library owns ms_model, ms_plan and ms_sim objects and
+ * every device buffer it allocates.  Probe reads copy into caller memory.
+ *
+ * Randomness: the library draws no random numbers; every random parameter
+ * (encoders, rates, intercepts, evaluation points, transforms) is an input.
+ *
+ * Precision: the build step (gains, biases, decoder solves) runs in double on
+ * the host; the simulation stores parameters and state in float32 on the GPU
+ * and accumulates products in float32.
+ */
+#ifndef MERGESIM_H
+#define MERGESIM_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef int32_t ms_status;
+
+#define MS_OK 0
+#define MS_E_INVALID (-1)   /* bad shape, id, range or option */
+#define MS_E_CYCLE (-2)     /* a cycle of connections without a synapse */
+#define MS_E_OOM (-3)       /* host or device allocation failed */
+#define MS_E_HIP (-4)       /* a HIP runtime call failed; message kept */
+#define MS_E_STATE (-5)     /* call not valid in the object's current state */
+#define MS_E_NUMERIC (-6)   /* decoder solve failed (matrix not positive definite) */
+
+typedef struct ms_model ms_model;
+typedef struct ms_plan ms_plan;
+typedef struct ms_sim ms_sim;
+
+/* Reference kinds used by connections and probes. */
+#define MS_REF_NODE 0     /* node output (pre) / passthrough node input (post) */
+#define MS_REF_ENS 1      /* decoded value (pre) / represented input (post)    */
+#define MS_REF_NEURONS 2  /* spike output (pre) / input current times gain (post) */
+
+#define MS_NEURON_LIF 0       /* spiking LIF, exact integration */
+#define MS_NEURON_LIF_RATE 1  /* LIF rate curve amplitude * r(J) */
+
+#define MS_FN_IDENTITY 0  /* decode x (d outputs) */
+#define MS_FN_PRODUCT 1   /* decode x0 * x1 (1 output, needs dims >= 2) */
+
+/* ------------------------------------------------------------------ model */
+
+/* Ensemble description (paper Sec. 2.1.2 "a group of neurons").
+ * encoders [n][d] row-major; either gains+biases [n] are given, or
+ * max_rates+intercepts [n] (then gain and bias are computed so that the
+ * neuron starts firing at intercept and fires at max_rate at x = 1).
+ * eval_points [M][d]: where decoders are fitted (needed only if something
+ * decodes from this ensemble without explicit decoders).
+ * tau_rc, tau_ref in seconds; amplitude scales the neuron output
+ * (spike height amplitude/dt, rate amplitude * r(J)). */
+typedef struct {
+  int32_t n_neurons;
+  int32_t dims;
+  int32_t neuron_type;          /* MS_NEURON_* */
+  double tau_rc, tau_ref, amplitude;
+  const double* encoders;       /* [n][d] */
+  const double* max_rates;      /* [n] or NULL if gains given */
+  const double* intercepts;     /* [n] or NULL if gains given */
+  const double* gains;          /* [n] or NULL */
+  const double* biases;         /* [n] or NULL */
+  int32_t n_eval_points;
+  const double* eval_points;    /* [M][d] or NULL */
+} ms_ensemble_desc;
+
+/* Connection description (paper Sec. 2.1.2 "Connection", Fig. 2).
+ * The value sent is v = T * pre[pre_start:pre_stop] (a start == stop == 0
+ * slice means the whole object).  Pre kinds: node output, an ensemble's decoded
+ * function (MS_FN_*, decoders solved on the ensemble's eval points unless
+ * explicit decoders [n][decoders_cols] are given), or an ensemble's spikes.
+ * T is a matrix [transform_rows][transform_cols] (rows = post slice size,
+ * cols = pre slice size) or, when transform_rows == 0, the scalar
+ * transform_scalar.  synapse_tau > 0 adds a lowpass filter (one-step delay);
+ * synapse_tau <= 0 delivers v within the same step.  Post kinds: a passthrough
+ * node, an ensemble's represented input, or an ensemble's neurons (added to the
+ * input current after multiplying by the neuron gains). */
+typedef struct {
+  int32_t pre_kind, pre_id, pre_start, pre_stop;
+  int32_t post_kind, post_id, post_start, post_stop;
+  int32_t function;             /* MS_FN_*, used when pre_kind == MS_REF_ENS */
+  const double* decoders;       /* explicit [n][decoders_cols] or NULL */
+  int32_t decoders_cols;
+  int32_t transform_rows, transform_cols;
+  const double* transform;      /* [rows][cols] or NULL for a scalar */
+  double transform_scalar;
+  double synapse_tau;           /* seconds; <= 0 means no synapse */
+} ms_connection_desc;
+
+/* Probe description (paper Sec. 3.1 sim.data[probe]).  Targets: node output,
+ * an ensemble's decoded identity, or spikes of neurons [start, stop) of an
+ * ensemble (start == stop == 0: all).  synapse_tau > 0 filters the probed
+ * value with a lowpass before recording. */
+typedef struct {
+  int32_t target_kind, target_id;
+  int32_t start, stop;
+  double synapse_tau;
+} ms_probe_desc;
+
+ms_status ms_model_create(ms_model** out);
+void ms_model_destroy(ms_model* model);
+
+/* A node of `size` outputs.  value == NULL: an input node whose output is
+ * supplied by a feed at every run call (zeros when no feed is given).
+ * value != NULL: a constant node (copied).  passthrough != 0: the node's output
+ * is the sum of its incoming connections in the same step (value ignored). */
+ms_status ms_model_add_node(ms_model* model, int32_t size, const double* value,
+                            int32_t passthrough, int32_t* id_out);
+ms_status ms_model_add_ensemble(ms_model* model, const ms_ensemble_desc* desc,
+                                int32_t* id_out);
+ms_status ms_model_add_connection(ms_model* model, const ms_connection_desc* desc,
+                                  int32_t* id_out);
+ms_status ms_model_add_probe(ms_model* model, const ms_probe_desc* desc, int32_t* id_out);
+
+/* ---------------------------------------------------------------- options */
+
+#define MS_PLANNER_GREEDY 0   /* schedule the largest ready group next (tree n = 1) */
+#define MS_PLANNER_TREE 1     /* bounded breadth-first tree search (Sec. 4.2.2) */
+
+#define MS_DRIVER_AUTO 0      /* library picks per model */
+#define MS_DRIVER_STEPS 1     /* one launch per merged group, stream-ordered */
+#define MS_DRIVER_GRAPH 2     /* hipGraph of `unroll` steps, replayed */
+#define MS_DRIVER_PERSISTENT 3 /* one launch per run: each workgroup owns batch
+                                  columns and executes every group of every step */
+
+typedef struct {
+  double dt;                  /* seconds, default 0.001 */
+  int32_t minibatch;          /* B >= 1, default 1 */
+  int32_t unroll;             /* steps per graph launch, default 10 */
+  int32_t planner;            /* MS_PLANNER_*, default TREE */
+  int32_t planner_depth;      /* tree search depth n, default 3 */
+  int32_t merge;              /* 0: one operator per group (no merging) */
+  int32_t sort;               /* 0: keep signals/operators in build order */
+  int32_t simplify;           /* 0: skip simplification */
+  int32_t driver;             /* MS_DRIVER_* */
+  int32_t device;             /* HIP device ordinal */
+  void* stream;               /* hipStream_t to run on, NULL = library-owned */
+  int64_t probe_capacity_steps; /* initial probe/feed staging capacity */
+} ms_sim_opts;
+
+/* Fill `opts` with the defaults listed above. */
+void ms_sim_opts_default(ms_sim_opts* opts);
+
+/* ------------------------------------------------------------------- plan */
+
+/* Host-only build + plan (no GPU needed): computes gains, biases and decoders
+ * in double, lowers the model to signals and operators, and runs merging,
+ * planning, sorting and simplification.  The plan is a snapshot; later edits of
+ * the model do not affect it. */
+ms_status ms_plan_create(const ms_model* model, const ms_sim_opts* opts, ms_plan** out);
+void ms_plan_destroy(ms_plan* plan);
+
+/* The plan as a JSON document (base arrays, signal placement, operator groups in
+ * execution order with their operators and index arrays).  Writes at most `cap`
+ * bytes including the terminating NUL; *len_out receives the full length
+ * (without NUL), so a call with cap == 0 sizes the buffer. */
+ms_status ms_plan_export_json(const ms_plan* plan, char* buf, int64_t cap, int64_t* len_out);
+
+#define MS_PARAM_GAIN 0       /* [n] */
+#define MS_PARAM_BIAS 1       /* [n] */
+#define MS_PARAM_DECODERS 2   /* [n][d_fn] for (ensemble, function) */
+
+/* Copy a built parameter (double, as computed by the build step) into `out`
+ * (capacity `cap` doubles); *n_out receives the element count. */
+ms_status ms_plan_get_param(const ms_plan* plan, int32_t which, int32_t ensemble,
+                            int32_t function, double* out, int64_t cap, int64_t* n_out);
+
+/* Copy parameter base array `base` (ids as in the JSON export; batched bases
+ * are rejected) as the float32 values the simulation uses: [rows][cols]
+ * row-major.  *n_out receives the element count; out == NULL sizes it. */
+ms_status ms_plan_export_base(const ms_plan* plan, int32_t base, float* out, int64_t cap,
+                              int64_t* n_out);
+
+/* -------------------------------------------------------------- simulator */
+
+ms_status ms_sim_create(const ms_model* model, const ms_sim_opts* opts, ms_sim** out);
+void ms_sim_destroy(ms_sim* sim);
+
+/* One input feed: data laid out [minibatch][n_steps][node size] float32;
+ * on_device != 0 means `data` is a device pointer on the simulator's device. */
+typedef struct {
+  int32_t node_id;
+  int32_t on_device;
+  const float* data;
+} ms_feed;
+
+/* Advance the simulation n_steps timesteps (paper Sec. 3.1 sim.run).  Steps
+ * continue from the current state; probes append.  Feeds for input nodes not
+ * listed read zeros.  Asynchronous with respect to the host unless a probe or
+ * state read follows; ms_sim_sync waits. */
+ms_status ms_sim_run_steps(ms_sim* sim, int64_t n_steps, const ms_feed* feeds, int32_t n_feeds);
+ms_status ms_sim_sync(ms_sim* sim);
+
+/* Number of steps recorded since creation or the last reset. */
+ms_status ms_sim_steps(const ms_sim* sim, int64_t* n_steps_out);
+
+/* Probe width (values per batch row per step). */
+ms_status ms_sim_probe_width(const ms_sim* sim, int32_t probe_id, int32_t* width_out);
+
+/* Copy probe `probe_id`'s record, [minibatch][steps][width] float32, into `out`
+ * (host memory unless out_on_device != 0).  cap_elems must be at least
+ * minibatch * steps * width. */
+ms_status ms_sim_probe_read(ms_sim* sim, int32_t probe_id, float* out, int64_t cap_elems,
+                            int32_t out_on_device);
+
+/* Restore the initial state (V = 0, refractory 0, filters 0) and clear probes
+ * (paper Sec. 3.1 sim.reset()). */
+ms_status ms_sim_reset(ms_sim* sim);
+
+/* State access for checkpoint/resume and injected-state tests.  Host buffers.
+ *   MS_STATE_VOLTAGE, MS_STATE_REFRACTORY: id = ensemble, [minibatch][n_neurons]
+ *   MS_STATE_SYNAPSE: id = connection with a synapse, [minibatch][post width]
+ *   MS_STATE_PROBE_SYNAPSE: id = probe with a synapse, [minibatch][width] */
+#define MS_STATE_VOLTAGE 0
+#define MS_STATE_REFRACTORY 1
+#define MS_STATE_SYNAPSE 2
+#define MS_STATE_PROBE_SYNAPSE 3
+ms_status ms_sim_get_state(ms_sim* sim, int32_t which, int32_t id, float* out, int64_t cap_elems);
+ms_status ms_sim_set_state(ms_sim* sim, int32_t which, int32_t id, const float* in, int64_t n_elems);
+
+/* Per-run timing of the last ms_sim_run_steps (HIP events on the simulator's
+ * stream around the simulation launches, excluding feed staging); ms. */
+ms_status ms_sim_last_run_ms(ms_sim* sim, double* ms_out);
+
+/* The driver actually used (MS_DRIVER_STEPS/GRAPH/PERSISTENT) and the number of
+ * merged groups executed per step. */
+ms_status ms_sim_info(const ms_sim* sim, int32_t* driver_out, int32_t* groups_per_step_out);
+
+const char* ms_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* MERGESIM_H */

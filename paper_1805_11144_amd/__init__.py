@@ -1,0 +1,13 @@
+"""mergesim: merged-operator spiking-network simulator for one MI355X.
+
+The simulation runs in ``libmergesim.so`` (hand-written HIP kernels for gfx950
+behind a C ABI, declared in include/mergesim.h).  This package is the thin
+Python binding: argument marshalling only.
+"""
+from .mergesim import (Model, Plan, Simulator, MergesimError, load_library, model_from_spec,
+                       DRIVER_AUTO, DRIVER_STEPS, DRIVER_GRAPH, DRIVER_PERSISTENT,
+                       PLANNER_GREEDY, PLANNER_TREE)
+
+__all__ = ["Model", "Plan", "Simulator", "MergesimError", "load_library", "model_from_spec",
+           "DRIVER_AUTO", "DRIVER_STEPS", "DRIVER_GRAPH", "DRIVER_PERSISTENT",
+           "PLANNER_GREEDY", "PLANNER_TREE"]

@@ -1,0 +1,235 @@
+// Host-side data structures of mergesim: the model description, the build
+// step's parameters, the signal/operator IR, the merged plan and its lowering
+// into per-group index arrays.  No HIP here: everything in this header runs on
+// the CPU and is testable without a GPU.
+#pragma once
+
+#include <cstdint>
+#include <map>
+#include <memory>
+#include <stdexcept>
+#include <string>
+#include <utility>
+#include <vector>
+
+#include "mergesim.h"
+
+namespace ms {
+
+// Error carrying an ms_status; caught at the C ABI boundary.
+struct Error : std::runtime_error {
+  ms_status code;
+  Error(ms_status c, const std::string& m) : std::runtime_error(m), code(c) {}
+};
+[[noreturn]] void fail(ms_status code, const std::string& msg);
+void set_last_error(const std::string& msg);
+
+// ------------------------------------------------------------------ model
+struct NodeDesc {
+  int32_t size = 0;
+  bool passthrough = false;
+  bool constant = false;          // value given
+  std::vector<double> value;      // [size]
+};
+
+struct EnsembleDesc {
+  int32_t n = 0, d = 0, neuron_type = MS_NEURON_LIF;
+  double tau_rc = 0.02, tau_ref = 0.002, amplitude = 1.0;
+  std::vector<double> encoders;   // [n*d]
+  std::vector<double> max_rates, intercepts, gains, biases;
+  int32_t n_eval = 0;
+  std::vector<double> eval_points;  // [M*d]
+};
+
+struct ConnDesc {
+  int32_t pre_kind = 0, pre_id = 0, pre_start = 0, pre_stop = 0;
+  int32_t post_kind = 0, post_id = 0, post_start = 0, post_stop = 0;
+  int32_t function = MS_FN_IDENTITY;
+  std::vector<double> decoders;   // explicit [n*cols] or empty
+  int32_t decoders_cols = 0;
+  int32_t t_rows = 0, t_cols = 0;
+  std::vector<double> transform;  // [rows*cols] or empty (scalar)
+  double t_scalar = 1.0;
+  double synapse = 0.0;           // <= 0: none
+};
+
+struct ProbeDesc {
+  int32_t kind = 0, id = 0, start = 0, stop = 0;
+  double synapse = 0.0;
+};
+
+struct Model {
+  std::vector<NodeDesc> nodes;
+  std::vector<EnsembleDesc> ens;
+  std::vector<ConnDesc> conns;
+  std::vector<ProbeDesc> probes;
+};
+
+// Size of the value a reference denotes (node output, decoded function,
+// neurons) -- used for validation of slices and transforms.
+int32_t function_size(int32_t fn, int32_t dims);
+
+// ------------------------------------------------------------------ build
+struct Built {
+  std::vector<std::vector<double>> gain, bias;          // per ensemble [n]
+  // decoders keyed by (ensemble, function): [n * d_fn]
+  std::map<std::pair<int32_t, int32_t>, std::vector<double>> decoders;
+};
+Built build_params(const Model& m);
+
+// --------------------------------------------------------------------- IR
+enum SigClass : int32_t { SC_BATCHED = 0, SC_PARAM = 1 };
+
+struct Signal {
+  std::string name;
+  int32_t rows = 0;
+  int32_t cols = 1;               // params: matrix width (1 for vectors)
+  SigClass cls = SC_BATCHED;
+  bool state = false;             // persists across steps (V, ref, filters)
+  std::vector<double> value;      // params: [rows*cols]
+  int32_t base = -1;              // base array id (assigned by the IR builder)
+};
+
+enum OpType : int32_t {
+  OP_FEED = 0,
+  OP_RESET = 1,
+  OP_COPY = 2,          // dst = src
+  OP_COPY_INC = 3,      // dst += src
+  OP_ELEM_INC = 4,      // dst += a (.) x
+  OP_DOT_INC = 5,       // dst += W x
+  OP_LIF = 6,
+  OP_LIF_RATE = 7,
+  OP_LOWPASS = 8,
+  OP_NTYPES = 9
+};
+const char* op_type_name(int32_t t);
+
+// A reference to rows [start, start+len) of a signal.
+struct SRef {
+  int32_t sig = -1;
+  int32_t start = 0;
+  int32_t len = 0;
+};
+
+struct Op {
+  OpType type;
+  std::string name;
+  SRef dst;            // RESET/COPY/COPY_INC/ELEM_INC/DOT_INC dst; LIF s; LOWPASS y
+  SRef src;            // COPY src; ELEM_INC x; DOT_INC x; LIF J; LOWPASS v
+  SRef a;              // ELEM_INC a (len 1 = broadcast scalar); DOT_INC W (rows M, cols K)
+  SRef V, ref;         // LIF state
+  int32_t node = -1;   // FEED: node id
+  std::vector<double> reset_value;  // RESET: [dst.len] (empty = zeros)
+  double tau_rc = 0, tau_ref = 0, amp = 0;  // LIF params
+  double coef_a = 0, coef_b = 0;            // LOWPASS y = coef_a y + coef_b v
+};
+
+struct BaseArray {
+  std::string name;   // "state", "vec", "mat<K>"
+  SigClass cls;
+  int32_t cols;
+};
+
+struct IR {
+  std::vector<Signal> sigs;
+  std::vector<Op> ops;
+  std::vector<BaseArray> bases;
+  // feed layout: fed nodes in id order, each [size] rows of the staging buffer
+  std::vector<int32_t> fed_nodes;       // node ids
+  std::vector<int32_t> feed_row_of_node;  // per node: first staging row or -1
+  int32_t feed_rows = 0;
+  std::vector<int32_t> node_size;       // per node
+  // probes: probed signal rows
+  struct ProbeSrc { SRef src; };
+  std::vector<ProbeSrc> probes;
+  // state signals for get/set state
+  std::vector<int32_t> ens_V, ens_ref;     // per ensemble signal id or -1
+  std::vector<int32_t> conn_y;             // per connection signal id or -1
+  std::vector<int32_t> probe_y;            // per probe signal id or -1
+};
+IR build_ir(const Model& m, const Built& b, double dt);
+void simplify_ir(IR& ir);
+
+// ------------------------------------------------------------------- plan
+struct PlanOpts {
+  int32_t planner = MS_PLANNER_TREE;
+  int32_t depth = 3;
+  bool merge = true, sort = true, simplify = true;
+};
+
+// One operand of a lowered group: rows in its base array, either a contiguous
+// range starting at `start` (idx empty) or an explicit index list.
+struct LOperand {
+  int32_t base = -1;
+  int64_t start = 0;
+  std::vector<int32_t> idx;
+  bool contiguous() const { return idx.empty(); }
+};
+
+struct LGroup {
+  OpType type;
+  std::vector<int32_t> ops;     // op ids in execution order
+  int64_t rows = 0;             // per-row work items (DOT_INC: number of ops)
+  // per-row operands (meaning depends on type, see lower_group)
+  LOperand dst, src, a, V, ref;
+  // CSR for increments with repeated destinations (COPY_INC / ELEM_INC):
+  // unique destinations `dst` (rows = number of unique), entries ptr[u]..ptr[u+1]
+  std::vector<int32_t> ptr;
+  // DOT_INC
+  int32_t M = 0, K = 0;
+  std::vector<int32_t> w_row, x_row, d_row;   // per op
+  // RESET values (empty: zeros)
+  std::vector<float> values;
+  // LIF / LIF_RATE parameters: uniform (size 1) or per row
+  std::vector<float> tau_rc, tau_ref, amp;
+  // LOWPASS coefficients: uniform (size 1) or per row
+  std::vector<float> ca, cb;
+  // FEED: staging rows per destination row
+  std::vector<int32_t> feed_rows;
+};
+
+struct Plan {
+  PlanOpts opts;
+  double dt = 0.001;
+  Built built;
+  IR ir;
+  std::vector<std::vector<int32_t>> groups;      // op ids per group, execution order
+  std::vector<int64_t> sig_offset;               // row offset of each signal in its base
+  std::vector<int64_t> base_rows;                // rows per base array
+  std::vector<int32_t> key_of_op;
+  std::vector<LGroup> lowered;
+  // probe lowering: source row (state base) per probe row; probe row offsets
+  std::vector<int32_t> probe_src_rows;
+  std::vector<int32_t> probe_row_offset;         // per probe, + total at end
+  std::vector<int32_t> probe_width;
+};
+
+std::unique_ptr<Plan> make_plan(const Model& m, double dt, const PlanOpts& o);
+std::string plan_to_json(const Plan& p);
+
+PlanOpts plan_opts_from(const ms_sim_opts* o);
+const Model& model_of(const ms_model* m);
+
+// Run f, converting exceptions into an ms_status and the thread-local message.
+template <class F>
+ms_status guarded(F&& f) {
+  try {
+    f();
+    return MS_OK;
+  } catch (const Error& e) {
+    set_last_error(e.what());
+    return e.code;
+  } catch (const std::bad_alloc&) {
+    set_last_error("host allocation failed");
+    return MS_E_OOM;
+  } catch (const std::exception& e) {
+    set_last_error(e.what());
+    return MS_E_INVALID;
+  }
+}
+
+// Planner internals exposed for tests through the JSON export.
+std::vector<std::vector<int32_t>> plan_groups(const IR& ir, const std::vector<int32_t>& key,
+                                              int32_t n_keys, const PlanOpts& o);
+
+}  // namespace ms

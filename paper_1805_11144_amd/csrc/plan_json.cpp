@@ -1,0 +1,105 @@
+// JSON export of a plan: base arrays, signal placement and the merged groups in
+// execution order with their lowered operands.  Used by tests to compare the
+// planner bit for bit with an independent implementation.
+#include <sstream>
+
+#include "host.hpp"
+
+namespace ms {
+
+namespace {
+
+void jstr(std::ostringstream& o, const std::string& s) {
+  o << '"';
+  for (char c : s) {
+    if (c == '"' || c == '\\') o << '\\';
+    o << c;
+  }
+  o << '"';
+}
+
+template <class T>
+void jarr(std::ostringstream& o, const std::vector<T>& v) {
+  o << '[';
+  for (size_t i = 0; i < v.size(); ++i) {
+    if (i) o << ',';
+    o << v[i];
+  }
+  o << ']';
+}
+
+void joperand(std::ostringstream& o, const LOperand& x) {
+  o << "{\"base\":" << x.base;
+  if (x.contiguous()) o << ",\"start\":" << x.start;
+  else { o << ",\"idx\":"; jarr(o, x.idx); }
+  o << '}';
+}
+
+}  // namespace
+
+std::string plan_to_json(const Plan& p) {
+  const IR& ir = p.ir;
+  std::ostringstream o;
+  o.precision(9);
+  o << "{\"bases\":[";
+  for (size_t b = 0; b < ir.bases.size(); ++b) {
+    if (b) o << ',';
+    o << "{\"name\":";
+    jstr(o, ir.bases[b].name);
+    o << ",\"rows\":" << p.base_rows[b] << ",\"cols\":" << ir.bases[b].cols << '}';
+  }
+  o << "],\"signals\":[";
+  for (size_t s = 0; s < ir.sigs.size(); ++s) {
+    if (s) o << ',';
+    o << "{\"name\":";
+    jstr(o, ir.sigs[s].name);
+    o << ",\"base\":" << ir.sigs[s].base << ",\"offset\":" << p.sig_offset[s]
+      << ",\"rows\":" << ir.sigs[s].rows << '}';
+  }
+  o << "],\"groups\":[";
+  for (size_t g = 0; g < p.lowered.size(); ++g) {
+    const LGroup& L = p.lowered[g];
+    if (g) o << ',';
+    o << "{\"type\":";
+    jstr(o, op_type_name(L.type));
+    o << ",\"key\":" << p.key_of_op[L.ops[0]] << ",\"ops\":[";
+    for (size_t k = 0; k < L.ops.size(); ++k) {
+      if (k) o << ',';
+      jstr(o, ir.ops[L.ops[k]].name);
+    }
+    o << "],\"rows\":" << L.rows;
+    if (L.type == OP_DOT_INC) {
+      o << ",\"M\":" << L.M << ",\"K\":" << L.K << ",\"w_row\":";
+      jarr(o, L.w_row);
+      o << ",\"x_row\":";
+      jarr(o, L.x_row);
+      o << ",\"d_row\":";
+      jarr(o, L.d_row);
+    } else {
+      o << ",\"dst\":";
+      joperand(o, L.dst);
+      if (L.src.base >= 0) { o << ",\"src\":"; joperand(o, L.src); }
+      if (L.a.base >= 0) { o << ",\"a\":"; joperand(o, L.a); }
+      if (L.V.base >= 0) { o << ",\"V\":"; joperand(o, L.V); }
+      if (L.ref.base >= 0) { o << ",\"ref\":"; joperand(o, L.ref); }
+      if (!L.ptr.empty()) { o << ",\"ptr\":"; jarr(o, L.ptr); }
+      if (!L.feed_rows.empty()) { o << ",\"feed_rows\":"; jarr(o, L.feed_rows); }
+      if (!L.values.empty()) { o << ",\"values\":"; jarr(o, L.values); }
+      if (!L.tau_rc.empty()) {
+        o << ",\"tau_rc\":"; jarr(o, L.tau_rc);
+        o << ",\"tau_ref\":"; jarr(o, L.tau_ref);
+        o << ",\"amp\":"; jarr(o, L.amp);
+      }
+      if (!L.ca.empty()) { o << ",\"ca\":"; jarr(o, L.ca); o << ",\"cb\":"; jarr(o, L.cb); }
+    }
+    o << '}';
+  }
+  o << "],\"probe_rows\":";
+  jarr(o, p.probe_src_rows);
+  o << ",\"probe_offsets\":";
+  jarr(o, p.probe_row_offset);
+  o << ",\"feed_rows\":" << ir.feed_rows << '}';
+  return o.str();
+}
+
+}  // namespace ms

@@ -1,0 +1,641 @@
+// Graph optimisations of the paper's Sec. 4.2: operator merging, planning
+// (greedy or bounded breadth-first tree search), signal/operator sorting
+// (Alg. 1 meta-block sorting, Alg. 2 signal/operator sorting) and the final
+// layout of signals in base arrays, followed by the lowering of every merged
+// group to index arrays the GPU kernels consume.
+//
+// Readings where the paper leaves details open:
+//  * dependencies: for every signal, the operators that set it run before those
+//    that increment it, which run before those that read it, which run before
+//    those that update it (Sec. 4.1.1: readers see a signal after all writes)
+//  * merge key: operator type, base array of every operand, and for DotInc the
+//    weight shape (M, K); neuron and filter parameters become per-row arrays
+//  * candidates of one planning step: for each key, all ready operators with
+//    that key; a plan's value is the number of operators it schedules in n
+//    steps; ties prefer the larger first group, then the lower key id (key ids
+//    in order of first appearance in the operator list)
+//  * read blocks: signals read by one group in one operand slot; block size =
+//    total elements; ties go to the lower id.  Alg. 1 filters keep the previous
+//    candidate set if a filter would empty it, and fall back to the lowest
+//    meta-block id.  Alg. 2 sorts operators by (position of the read signal,
+//    slice start), permutes signals only inside their meta-block, and makes at
+//    most 10 passes.
+#include <algorithm>
+#include <array>
+#include <climits>
+#include <numeric>
+#include <set>
+#include <tuple>
+
+#include "host.hpp"
+
+namespace ms {
+
+const char* op_type_name(int32_t t) {
+  static const char* n[] = {"Feed", "Reset", "Copy", "CopyInc", "ElementwiseInc",
+                            "DotInc", "SimLIF", "SimLIFRate", "Lowpass"};
+  return (t >= 0 && t < OP_NTYPES) ? n[t] : "?";
+}
+
+namespace {
+
+// Signals an operator reads, in slot order (the slots used for read blocks).
+std::vector<SRef> read_slots(const Op& o) {
+  switch (o.type) {
+    case OP_COPY:
+    case OP_COPY_INC: return {o.src};
+    case OP_ELEM_INC:
+    case OP_DOT_INC: return {o.a, o.src};
+    case OP_LIF: return {o.src, o.V, o.ref};
+    case OP_LIF_RATE: return {o.src};
+    case OP_LOWPASS: return {o.src, o.dst};
+    default: return {};
+  }
+}
+
+// sets / incs / reads / updates of batched signals
+void access(const Op& o, std::vector<int32_t>& sets, std::vector<int32_t>& incs,
+            std::vector<int32_t>& reads, std::vector<int32_t>& upds) {
+  sets.clear(); incs.clear(); reads.clear(); upds.clear();
+  switch (o.type) {
+    case OP_FEED:
+    case OP_RESET: sets.push_back(o.dst.sig); break;
+    case OP_COPY: sets.push_back(o.dst.sig); reads.push_back(o.src.sig); break;
+    case OP_COPY_INC: incs.push_back(o.dst.sig); reads.push_back(o.src.sig); break;
+    case OP_ELEM_INC:
+    case OP_DOT_INC: incs.push_back(o.dst.sig); reads.push_back(o.a.sig); reads.push_back(o.src.sig); break;
+    case OP_LIF: reads.push_back(o.src.sig); sets.push_back(o.dst.sig);
+      upds.push_back(o.V.sig); upds.push_back(o.ref.sig); break;
+    case OP_LIF_RATE: reads.push_back(o.src.sig); sets.push_back(o.dst.sig); break;
+    case OP_LOWPASS: reads.push_back(o.src.sig); upds.push_back(o.dst.sig); break;
+    default: break;
+  }
+}
+
+std::vector<int32_t> merge_key(const IR& ir, const Op& o) {
+  auto b = [&](const SRef& r) { return r.sig >= 0 ? ir.sigs[r.sig].base : -1; };
+  switch (o.type) {
+    case OP_FEED: return {OP_FEED};
+    case OP_RESET: return {OP_RESET, b(o.dst)};
+    case OP_COPY:
+    case OP_COPY_INC: return {o.type, b(o.dst), b(o.src)};
+    case OP_ELEM_INC: return {OP_ELEM_INC, b(o.dst), b(o.a), b(o.src)};
+    case OP_DOT_INC: return {OP_DOT_INC, b(o.dst), b(o.a), b(o.src), o.a.len, o.src.len};
+    case OP_LIF: return {OP_LIF, b(o.src), b(o.dst), b(o.V), b(o.ref)};
+    case OP_LIF_RATE: return {OP_LIF_RATE, b(o.src), b(o.dst)};
+    case OP_LOWPASS: return {OP_LOWPASS, b(o.dst), b(o.src)};
+    default: return {o.type};
+  }
+}
+
+struct Graph {
+  std::vector<std::vector<int32_t>> succ;
+  std::vector<int32_t> indeg;
+};
+
+Graph dependency_graph(const IR& ir) {
+  const int32_t no = (int32_t)ir.ops.size();
+  const int32_t ns = (int32_t)ir.sigs.size();
+  std::vector<std::array<std::vector<int32_t>, 4>> layers(ns);
+  std::vector<int32_t> s, i, r, u;
+  for (int32_t k = 0; k < no; ++k) {
+    access(ir.ops[k], s, i, r, u);
+    const std::vector<int32_t>* L[4] = {&s, &i, &r, &u};
+    for (int l = 0; l < 4; ++l)
+      for (int32_t sig : *L[l])
+        if (ir.sigs[sig].cls == SC_BATCHED) {
+          auto& v = layers[sig][l];
+          if (v.empty() || v.back() != k) v.push_back(k);
+        }
+  }
+  Graph g;
+  g.succ.assign(no, {});
+  g.indeg.assign(no, 0);
+  for (int32_t sig = 0; sig < ns; ++sig) {
+    if (layers[sig][0].size() > 1)
+      fail(MS_E_INVALID, "signal " + ir.sigs[sig].name + " is set by more than one operator");
+    const std::vector<int32_t>* prev = nullptr;
+    for (int l = 0; l < 4; ++l) {
+      const auto& cur = layers[sig][l];
+      if (cur.empty()) continue;
+      if (prev)
+        for (int32_t a : *prev)
+          for (int32_t bb : cur)
+            if (a != bb) { g.succ[a].push_back(bb); g.indeg[bb]++; }
+      prev = &cur;
+    }
+  }
+  // cycle check (Kahn)
+  std::vector<int32_t> deg = g.indeg, q;
+  for (int32_t k = 0; k < no; ++k) if (deg[k] == 0) q.push_back(k);
+  size_t seen = 0;
+  while (seen < q.size()) {
+    int32_t k = q[seen++];
+    for (int32_t t : g.succ[k]) if (--deg[t] == 0) q.push_back(t);
+  }
+  if ((int32_t)q.size() != no)
+    fail(MS_E_CYCLE, "the operator graph has a cycle (a loop of connections without a synapse)");
+  return g;
+}
+
+// ------------------------------------------------------------------ planner
+struct PlanSearch {
+  const Graph& g;
+  const std::vector<int32_t>& key;
+  std::vector<int32_t> indeg;
+  std::vector<std::vector<int32_t>> ready;   // per key
+
+  PlanSearch(const Graph& gg, const std::vector<int32_t>& k, int32_t nkeys)
+      : g(gg), key(k), indeg(gg.indeg), ready(nkeys) {
+    for (int32_t o = 0; o < (int32_t)indeg.size(); ++o)
+      if (indeg[o] == 0) ready[key[o]].push_back(o);
+  }
+
+  // schedule every ready op of key k; returns the scheduled list
+  std::vector<int32_t> apply(int32_t k) {
+    std::vector<int32_t> L;
+    L.swap(ready[k]);
+    for (int32_t o : L)
+      for (int32_t t : g.succ[o])
+        if (--indeg[t] == 0) ready[key[t]].push_back(t);
+    return L;
+  }
+  void undo(int32_t k, std::vector<int32_t>& L) {
+    for (auto it = L.rbegin(); it != L.rend(); ++it) {
+      const auto& sc = g.succ[*it];
+      for (auto jt = sc.rbegin(); jt != sc.rend(); ++jt) {
+        int32_t t = *jt;
+        if (indeg[t] == 0) ready[key[t]].pop_back();
+        ++indeg[t];
+      }
+    }
+    ready[k].swap(L);
+  }
+
+  int64_t best(int depth) {
+    if (depth <= 0) return 0;
+    int64_t v = 0;
+    for (int32_t k = 0; k < (int32_t)ready.size(); ++k) {
+      const int64_t sz = (int64_t)ready[k].size();
+      if (!sz) continue;
+      if (depth == 1) { v = std::max(v, sz); continue; }
+      auto L = apply(k);
+      v = std::max(v, sz + best(depth - 1));
+      undo(k, L);
+    }
+    return v;
+  }
+};
+
+}  // namespace
+
+std::vector<std::vector<int32_t>> plan_groups(const IR& ir, const std::vector<int32_t>& key,
+                                              int32_t n_keys, const PlanOpts& o) {
+  Graph g = dependency_graph(ir);
+  PlanSearch ps(g, key, n_keys);
+  const int depth = (o.planner == MS_PLANNER_GREEDY || !o.merge) ? 1 : std::max(1, o.depth);
+  std::vector<std::vector<int32_t>> groups;
+  size_t done = 0;
+  while (done < ir.ops.size()) {
+    int32_t best_k = -1;
+    int64_t best_v = -1, best_sz = -1;
+    for (int32_t k = 0; k < n_keys; ++k) {
+      const int64_t sz = (int64_t)ps.ready[k].size();
+      if (!sz) continue;
+      int64_t v = sz;
+      if (depth > 1) {
+        auto L = ps.apply(k);
+        v += ps.best(depth - 1);
+        ps.undo(k, L);
+      }
+      if (v > best_v || (v == best_v && sz > best_sz)) {
+        best_v = v; best_sz = sz; best_k = k;
+      }
+    }
+    if (best_k < 0) fail(MS_E_CYCLE, "planner stalled (cycle)");
+    auto L = ps.apply(best_k);
+    std::sort(L.begin(), L.end());
+    done += L.size();
+    groups.push_back(std::move(L));
+  }
+  return groups;
+}
+
+namespace {
+
+// ------------------------------------------------------------------ sorting
+struct Block {
+  int32_t group, slot, base;
+  int64_t size = 0;
+  std::vector<int32_t> sigs;          // distinct, first-occurrence order
+};
+
+struct SortState {
+  std::vector<std::vector<int32_t>> order;   // per base: signal ids
+  std::vector<int32_t> pos;                  // per signal: position in its base
+  void reindex(int32_t base) {
+    const auto& v = order[base];
+    for (int32_t i = 0; i < (int32_t)v.size(); ++i) pos[v[i]] = i;
+  }
+};
+
+void sort_plan(const IR& ir, std::vector<std::vector<int32_t>>& groups, SortState& st) {
+  const int32_t ns = (int32_t)ir.sigs.size(), nb = (int32_t)ir.bases.size();
+  // read blocks
+  std::vector<Block> blocks;
+  std::vector<std::vector<int32_t>> group_blocks(groups.size());
+  for (int32_t gi = 0; gi < (int32_t)groups.size(); ++gi) {
+    const Op& first = ir.ops[groups[gi][0]];
+    const size_t nslots = read_slots(first).size();
+    for (size_t sl = 0; sl < nslots; ++sl) {
+      Block b;
+      b.group = gi; b.slot = (int32_t)sl;
+      std::set<int32_t> seen;
+      for (int32_t oi : groups[gi]) {
+        int32_t sig = read_slots(ir.ops[oi])[sl].sig;
+        if (seen.insert(sig).second) {
+          b.sigs.push_back(sig);
+          b.size += (int64_t)ir.sigs[sig].rows * ir.sigs[sig].cols;
+        }
+      }
+      b.base = ir.sigs[b.sigs[0]].base;
+      group_blocks[gi].push_back((int32_t)blocks.size());
+      blocks.push_back(std::move(b));
+    }
+  }
+  const int32_t nblk = (int32_t)blocks.size();
+  // membership of each signal
+  std::vector<std::vector<int32_t>> member(ns);
+  for (int32_t bi = 0; bi < nblk; ++bi)
+    for (int32_t sig : blocks[bi].sigs) member[sig].push_back(bi);
+  // meta-blocks per base, first appearance in canonical signal order
+  std::map<std::pair<int32_t, std::vector<int32_t>>, int32_t> meta_id;
+  std::vector<std::vector<int32_t>> meta_sigs, meta_set;
+  std::vector<int32_t> meta_base;
+  std::vector<int32_t> meta_of(ns, -1);
+  for (int32_t sig = 0; sig < ns; ++sig) {
+    auto k = std::make_pair(ir.sigs[sig].base, member[sig]);
+    auto it = meta_id.find(k);
+    int32_t id;
+    if (it == meta_id.end()) {
+      id = (int32_t)meta_sigs.size();
+      meta_id[k] = id;
+      meta_sigs.push_back({});
+      meta_set.push_back(member[sig]);
+      meta_base.push_back(ir.sigs[sig].base);
+    } else {
+      id = it->second;
+    }
+    meta_sigs[id].push_back(sig);
+    meta_of[sig] = id;
+  }
+  auto bigger = [&](int32_t x, int32_t y) {   // block order: size desc, id asc
+    if (blocks[x].size != blocks[y].size) return blocks[x].size > blocks[y].size;
+    return x < y;
+  };
+  auto contains = [&](int32_t m, int32_t b) {
+    return std::binary_search(meta_set[m].begin(), meta_set[m].end(), b);
+  };
+  auto subset = [&](int32_t c, int32_t x) {   // set(c) within set(x)
+    return std::includes(meta_set[x].begin(), meta_set[x].end(), meta_set[c].begin(), meta_set[c].end());
+  };
+  auto hamming = [&](int32_t x, int32_t y) {
+    std::vector<int32_t> d;
+    std::set_symmetric_difference(meta_set[x].begin(), meta_set[x].end(), meta_set[y].begin(),
+                                  meta_set[y].end(), std::back_inserter(d));
+    return (int64_t)d.size();
+  };
+
+  // ---- Alg. 1, per base array
+  st.order.assign(nb, {});
+  st.pos.assign(ns, -1);
+  for (int32_t base = 0; base < nb; ++base) {
+    std::vector<int32_t> M;
+    for (int32_t m = 0; m < (int32_t)meta_sigs.size(); ++m) if (meta_base[m] == base) M.push_back(m);
+    std::vector<int32_t> bblocks;
+    for (int32_t bi = 0; bi < nblk; ++bi) if (blocks[bi].base == base) bblocks.push_back(bi);
+    std::vector<int32_t> S;
+    if (bblocks.empty()) {
+      S = M;
+    } else {
+      int32_t a = *std::min_element(bblocks.begin(), bblocks.end(), bigger);
+      int32_t c = -1;
+      for (int32_t m : M) if (contains(m, a)) { c = m; break; }
+      while (!M.empty()) {
+        std::vector<int32_t> X;
+        for (int32_t m : M) if (contains(m, a)) X.push_back(m);
+        if (X.empty()) {
+          X = M;
+          if (!meta_set[c].empty())
+            a = *std::min_element(meta_set[c].begin(), meta_set[c].end(), bigger);
+        }
+        std::vector<int32_t> Y;
+        for (int32_t x : X) if (subset(c, x)) Y.push_back(x);
+        if (Y.empty()) Y = X;
+        int64_t dmin = INT64_MAX;
+        for (int32_t y : Y) dmin = std::min(dmin, hamming(y, c));
+        std::vector<int32_t> Z;
+        for (int32_t y : Y) if (hamming(y, c) == dmin) Z.push_back(y);
+        if (Z.size() > 1) {
+          std::vector<int32_t> cb = meta_set[c];
+          std::sort(cb.begin(), cb.end(), bigger);
+          for (int32_t mb : cb) {
+            std::vector<int32_t> Z2;
+            for (int32_t z : Z) if (contains(z, mb)) Z2.push_back(z);
+            if (!Z2.empty()) Z.swap(Z2);
+            if (Z.size() == 1) break;
+          }
+        }
+        int32_t z = *std::min_element(Z.begin(), Z.end());
+        M.erase(std::find(M.begin(), M.end(), z));
+        S.push_back(z);
+        c = z;
+      }
+    }
+    for (int32_t m : S)
+      for (int32_t sig : meta_sigs[m]) st.order[base].push_back(sig);
+    st.reindex(base);
+  }
+
+  // ---- Alg. 2
+  std::vector<int32_t> sorted_blocks(nblk);
+  std::iota(sorted_blocks.begin(), sorted_blocks.end(), 0);
+  std::stable_sort(sorted_blocks.begin(), sorted_blocks.end(), [&](int32_t x, int32_t y) {
+    return blocks[x].size < blocks[y].size;
+  });
+  // meta-blocks containing each block
+  std::vector<std::vector<int32_t>> metas_of_block(nblk);
+  for (int32_t m = 0; m < (int32_t)meta_sigs.size(); ++m)
+    for (int32_t bi : meta_set[m]) metas_of_block[bi].push_back(m);
+  for (int pass = 0; pass < 10; ++pass) {
+    bool changed = false;
+    for (int32_t bi : sorted_blocks) {
+      const Block& b = blocks[bi];
+      std::vector<int32_t>& O = groups[b.group];
+      std::vector<int32_t> before = O;
+      std::stable_sort(O.begin(), O.end(), [&](int32_t x, int32_t y) {
+        const SRef rx = read_slots(ir.ops[x])[b.slot], ry = read_slots(ir.ops[y])[b.slot];
+        const int32_t px = st.pos[rx.sig], py = st.pos[ry.sig];
+        if (px != py) return px < py;
+        return rx.start < ry.start;
+      });
+      if (O != before) changed = true;
+      for (int32_t cbi : group_blocks[b.group]) {
+        const Block& cb = blocks[cbi];
+        // signals of cb in the new operator order
+        std::vector<int32_t> seq;
+        std::set<int32_t> seen;
+        for (int32_t oi : O) {
+          int32_t sig = read_slots(ir.ops[oi])[cb.slot].sig;
+          if (seen.insert(sig).second) seq.push_back(sig);
+        }
+        std::vector<int32_t> rank(0);
+        std::map<int32_t, int32_t> rk;
+        for (int32_t i = 0; i < (int32_t)seq.size(); ++i) rk[seq[i]] = i;
+        for (int32_t m : metas_of_block[cbi]) {
+          const auto& msigs = meta_sigs[m];
+          std::vector<int32_t> positions;
+          for (int32_t sig : msigs) positions.push_back(st.pos[sig]);
+          std::sort(positions.begin(), positions.end());
+          std::vector<int32_t> now(msigs.size());
+          for (size_t i = 0; i < positions.size(); ++i) now[i] = st.order[cb.base][positions[i]];
+          std::vector<int32_t> want = now;
+          std::stable_sort(want.begin(), want.end(), [&](int32_t x, int32_t y) { return rk[x] < rk[y]; });
+          if (want != now) {
+            changed = true;
+            for (size_t i = 0; i < positions.size(); ++i) {
+              st.order[cb.base][positions[i]] = want[i];
+              st.pos[want[i]] = positions[i];
+            }
+          }
+        }
+      }
+    }
+    if (!changed) break;
+  }
+}
+
+// ----------------------------------------------------------------- lowering
+LOperand make_operand(int32_t base, const std::vector<int32_t>& rows) {
+  LOperand o;
+  o.base = base;
+  bool contig = true;
+  for (size_t i = 1; i < rows.size(); ++i)
+    if (rows[i] != rows[0] + (int32_t)i) { contig = false; break; }
+  if (contig) {
+    o.start = rows.empty() ? 0 : rows[0];
+  } else {
+    o.idx = rows;
+  }
+  return o;
+}
+
+template <class T>
+std::vector<float> uniform_or_rows(const std::vector<T>& v) {
+  bool uni = true;
+  for (size_t i = 1; i < v.size(); ++i) if ((float)v[i] != (float)v[0]) { uni = false; break; }
+  std::vector<float> out;
+  if (uni && !v.empty()) out.push_back((float)v[0]);
+  else for (const T& x : v) out.push_back((float)x);
+  return out;
+}
+
+LGroup lower_group(const Plan& p, const std::vector<int32_t>& ops) {
+  const IR& ir = p.ir;
+  LGroup g;
+  g.type = ir.ops[ops[0]].type;
+  g.ops = ops;
+  auto row = [&](const SRef& r, int32_t i) { return (int32_t)(p.sig_offset[r.sig] + r.start + i); };
+  auto base = [&](const SRef& r) { return ir.sigs[r.sig].base; };
+  const Op& f = ir.ops[ops[0]];
+  switch (g.type) {
+    case OP_FEED: {
+      std::vector<int32_t> d, fr;
+      for (int32_t oi : ops) {
+        const Op& o = ir.ops[oi];
+        for (int32_t i = 0; i < o.dst.len; ++i) {
+          d.push_back(row(o.dst, i));
+          fr.push_back(ir.feed_row_of_node[o.node] + i);
+        }
+      }
+      g.rows = (int64_t)d.size();
+      g.dst = make_operand(base(f.dst), d);
+      g.feed_rows = fr;
+      break;
+    }
+    case OP_RESET: {
+      std::vector<int32_t> d;
+      std::vector<double> val;
+      bool any = false;
+      for (int32_t oi : ops) {
+        const Op& o = ir.ops[oi];
+        for (int32_t i = 0; i < o.dst.len; ++i) {
+          d.push_back(row(o.dst, i));
+          double v = o.reset_value.empty() ? 0.0 : o.reset_value[i];
+          any |= v != 0.0;
+          val.push_back(v);
+        }
+      }
+      g.rows = (int64_t)d.size();
+      g.dst = make_operand(base(f.dst), d);
+      if (any) for (double v : val) g.values.push_back((float)v);
+      break;
+    }
+    case OP_COPY: {
+      std::vector<int32_t> d, s;
+      for (int32_t oi : ops) {
+        const Op& o = ir.ops[oi];
+        for (int32_t i = 0; i < o.dst.len; ++i) { d.push_back(row(o.dst, i)); s.push_back(row(o.src, i)); }
+      }
+      g.rows = (int64_t)d.size();
+      g.dst = make_operand(base(f.dst), d);
+      g.src = make_operand(base(f.src), s);
+      break;
+    }
+    case OP_COPY_INC:
+    case OP_ELEM_INC: {
+      // entries in operator order; grouped by destination (first appearance)
+      std::vector<int32_t> ed, es, ea;
+      for (int32_t oi : ops) {
+        const Op& o = ir.ops[oi];
+        for (int32_t i = 0; i < o.dst.len; ++i) {
+          ed.push_back(row(o.dst, i));
+          es.push_back(row(o.src, i));
+          if (g.type == OP_ELEM_INC) ea.push_back(row(o.a, o.a.len == 1 ? 0 : i));
+        }
+      }
+      std::vector<int32_t> uniq;
+      std::map<int32_t, int32_t> uid;
+      std::vector<std::vector<int32_t>> ent;
+      for (int32_t e = 0; e < (int32_t)ed.size(); ++e) {
+        auto it = uid.find(ed[e]);
+        int32_t u;
+        if (it == uid.end()) { u = (int32_t)uniq.size(); uid[ed[e]] = u; uniq.push_back(ed[e]); ent.push_back({}); }
+        else u = it->second;
+        ent[u].push_back(e);
+      }
+      std::vector<int32_t> s2, a2;
+      g.ptr.push_back(0);
+      for (size_t u = 0; u < uniq.size(); ++u) {
+        for (int32_t e : ent[u]) { s2.push_back(es[e]); if (!ea.empty()) a2.push_back(ea[e]); }
+        g.ptr.push_back((int32_t)s2.size());
+      }
+      if (uniq.size() == ed.size()) g.ptr.clear();   // no repeated destination
+      g.rows = (int64_t)uniq.size();
+      g.dst = make_operand(base(f.dst), uniq);
+      g.src = make_operand(base(f.src), s2);
+      if (g.type == OP_ELEM_INC) g.a = make_operand(base(f.a), a2);
+      break;
+    }
+    case OP_DOT_INC: {
+      g.M = f.a.len;
+      g.K = f.src.len;
+      std::set<int32_t> dsts;
+      for (int32_t oi : ops) {
+        const Op& o = ir.ops[oi];
+        g.w_row.push_back((int32_t)p.sig_offset[o.a.sig] + o.a.start);
+        g.x_row.push_back(row(o.src, 0));
+        g.d_row.push_back(row(o.dst, 0));
+        if (!dsts.insert(o.dst.sig).second) fail(MS_E_INVALID, "DotInc group with repeated destination");
+      }
+      g.rows = (int64_t)ops.size();
+      g.a.base = base(f.a);
+      g.src.base = base(f.src);
+      g.dst.base = base(f.dst);
+      break;
+    }
+    case OP_LIF:
+    case OP_LIF_RATE: {
+      std::vector<int32_t> J, s, V, R;
+      std::vector<double> trc, tref, amp;
+      for (int32_t oi : ops) {
+        const Op& o = ir.ops[oi];
+        for (int32_t i = 0; i < o.src.len; ++i) {
+          J.push_back(row(o.src, i));
+          s.push_back(row(o.dst, i));
+          if (g.type == OP_LIF) { V.push_back(row(o.V, i)); R.push_back(row(o.ref, i)); }
+          trc.push_back(o.tau_rc); tref.push_back(o.tau_ref); amp.push_back(o.amp);
+        }
+      }
+      g.rows = (int64_t)J.size();
+      g.src = make_operand(base(f.src), J);
+      g.dst = make_operand(base(f.dst), s);
+      if (g.type == OP_LIF) { g.V = make_operand(base(f.V), V); g.ref = make_operand(base(f.ref), R); }
+      g.tau_rc = uniform_or_rows(trc);
+      g.tau_ref = uniform_or_rows(tref);
+      g.amp = uniform_or_rows(amp);
+      break;
+    }
+    case OP_LOWPASS: {
+      std::vector<int32_t> y, v;
+      std::vector<double> ca, cb;
+      for (int32_t oi : ops) {
+        const Op& o = ir.ops[oi];
+        for (int32_t i = 0; i < o.dst.len; ++i) {
+          y.push_back(row(o.dst, i)); v.push_back(row(o.src, i));
+          ca.push_back(o.coef_a); cb.push_back(o.coef_b);
+        }
+      }
+      g.rows = (int64_t)y.size();
+      g.dst = make_operand(base(f.dst), y);
+      g.src = make_operand(base(f.src), v);
+      g.ca = uniform_or_rows(ca);
+      g.cb = uniform_or_rows(cb);
+      break;
+    }
+    default: fail(MS_E_INVALID, "cannot lower operator type");
+  }
+  return g;
+}
+
+}  // namespace
+
+std::unique_ptr<Plan> make_plan(const Model& m, double dt, const PlanOpts& o) {
+  auto p = std::make_unique<Plan>();
+  p->opts = o;
+  p->dt = dt;
+  p->built = build_params(m);
+  p->ir = build_ir(m, p->built, dt);
+  if (o.simplify) simplify_ir(p->ir);
+  IR& ir = p->ir;
+  // merge keys in first-appearance order
+  std::map<std::vector<int32_t>, int32_t> kid;
+  p->key_of_op.resize(ir.ops.size());
+  int32_t nkeys = 0;
+  for (size_t k = 0; k < ir.ops.size(); ++k) {
+    if (!o.merge) { p->key_of_op[k] = nkeys++; continue; }
+    auto key = merge_key(ir, ir.ops[k]);
+    auto it = kid.find(key);
+    if (it == kid.end()) { kid[key] = nkeys; p->key_of_op[k] = nkeys++; }
+    else p->key_of_op[k] = it->second;
+  }
+  p->groups = plan_groups(ir, p->key_of_op, nkeys, o);
+  // layout
+  SortState st;
+  if (o.sort) {
+    sort_plan(ir, p->groups, st);
+  } else {
+    st.order.assign(ir.bases.size(), {});
+    st.pos.assign(ir.sigs.size(), -1);
+    for (int32_t s = 0; s < (int32_t)ir.sigs.size(); ++s) st.order[ir.sigs[s].base].push_back(s);
+  }
+  p->sig_offset.assign(ir.sigs.size(), 0);
+  p->base_rows.assign(ir.bases.size(), 0);
+  for (size_t b = 0; b < ir.bases.size(); ++b) {
+    int64_t off = 0;
+    for (int32_t s : st.order[b]) { p->sig_offset[s] = off; off += ir.sigs[s].rows; }
+    p->base_rows[b] = off;
+  }
+  for (const auto& g : p->groups) p->lowered.push_back(lower_group(*p, g));
+  // probes
+  p->probe_row_offset.push_back(0);
+  for (const auto& pr : ir.probes) {
+    for (int32_t i = 0; i < pr.src.len; ++i)
+      p->probe_src_rows.push_back((int32_t)(p->sig_offset[pr.src.sig] + pr.src.start + i));
+    p->probe_width.push_back(pr.src.len);
+    p->probe_row_offset.push_back((int32_t)p->probe_src_rows.size());
+  }
+  return p;
+}
+
+}  // namespace ms

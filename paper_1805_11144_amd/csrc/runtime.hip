@@ -1,0 +1,656 @@
+// GPU runtime of mergesim: device base arrays, the merged-group kernels, the
+// step drivers (stream-ordered launches, a hipGraph of `unroll` steps, and a
+// persistent per-batch-column kernel), feeds, probes and state access.
+//
+// Data layout in HBM (paper Sec. 4.2.1: signals are concatenated along the
+// first axis into base arrays):
+//   state  float [rows][B]  every batched signal, minibatch contiguous
+//   vec    float [rows]     per-row parameters (biases, gains, scalars)
+//   mat<K> float [rows][K]  weight matrices with K columns
+// Each merged group is one launch; a group's per-row operands are either a
+// contiguous row range (a "slice") or an int32 index list.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cmath>
+#include <cstring>
+#include <string>
+#include <vector>
+
+#include "host.hpp"
+#include "kernels.hpp"
+
+using namespace ms;
+
+#define HIPCHECK(expr)                                                                    \
+  do {                                                                                    \
+    hipError_t _e = (expr);                                                               \
+    if (_e != hipSuccess)                                                                 \
+      ms::fail(MS_E_HIP, std::string(#expr) + ": " + hipGetErrorString(_e));              \
+  } while (0)
+
+namespace {
+
+template <class T>
+T* dev_alloc(size_t n) {
+  if (n == 0) return nullptr;
+  void* p = nullptr;
+  hipError_t e = hipMalloc(&p, n * sizeof(T));
+  if (e != hipSuccess) fail(MS_E_OOM, std::string("hipMalloc failed: ") + hipGetErrorString(e));
+  return (T*)p;
+}
+
+// Host mirror of one lowered group, with device pointers.
+struct Launch {
+  int32_t type = 0;
+  int64_t rows = 0;
+  Opnd dst, src, a, V, ref;
+  const float* src_base = nullptr;   // base array of src (COPY*, ELEM_INC x)
+  bool src_bcast = false;            // src base is a parameter base (no batch axis)
+  const float* a_base = nullptr;     // ELEM_INC a / DOT_INC W base
+  const int32_t* ptr = nullptr;      // CSR offsets (repeated destinations) or null
+  const float* values = nullptr;     // RESET values or null (zeros)
+  int32_t M = 0, K = 0;
+  const int32_t* w_row = nullptr;
+  const int32_t* x_row = nullptr;
+  const int32_t* d_row = nullptr;
+  NeuronParams np{};
+  FilterParams fp{};
+  const int32_t* feed_rows = nullptr;
+};
+
+}  // namespace
+
+struct ms_sim {
+  std::unique_ptr<Plan> plan;
+  int32_t B = 1;
+  int32_t device = 0;
+  hipStream_t stream = nullptr;
+  bool own_stream = false;
+  int32_t driver = MS_DRIVER_STEPS;
+  int32_t unroll = 10;
+  float dt = 0.001f;
+  // device memory
+  std::vector<float*> base_ptr;      // per base id
+  float* state = nullptr;
+  size_t state_rows = 0;
+  Strides S{1, 1};                   // element (r, b) at r * S.rs + b * S.cs
+  int32_t* ipool = nullptr;
+  float* fpool = nullptr;
+  std::vector<Launch> launches;
+  int64_t* ctr = nullptr;            // [0] steps recorded since reset, [1] step within run
+  float* feed_stage = nullptr;       // [cap][feed_rows][B]
+  int64_t feed_cap = 0;
+  float* feed_tmp = nullptr;         // [B][T][size] upload buffer for host feeds
+  size_t feed_tmp_elems = 0;
+  float* probe_buf = nullptr;        // [cap][probe_rows][B]
+  int64_t probe_cap = 0;
+  int32_t probe_rows = 0;
+  const int32_t* probe_src = nullptr;
+  int64_t steps_total = 0;
+  // graph driver
+  hipGraphExec_t graph_exec = nullptr;
+  hipGraph_t graph = nullptr;
+  bool graph_valid = false;
+  hipEvent_t ev0 = nullptr, ev1 = nullptr;
+  double last_ms = 0.0;
+  // persistent driver
+  PersistentProgram prog{};
+  bool persistent_ok = false;
+};
+
+namespace {
+
+struct DeviceGuard {
+  int prev = 0;
+  explicit DeviceGuard(int dev) {
+    HIPCHECK(hipGetDevice(&prev));
+    if (prev != dev) HIPCHECK(hipSetDevice(dev));
+  }
+  ~DeviceGuard() {
+    int cur = 0;
+    if (hipGetDevice(&cur) == hipSuccess && cur != prev) (void)hipSetDevice(prev);
+  }
+};
+
+void destroy_graph(ms_sim* s) {
+  if (s->graph_exec) (void)hipGraphExecDestroy(s->graph_exec);
+  if (s->graph) (void)hipGraphDestroy(s->graph);
+  s->graph_exec = nullptr;
+  s->graph = nullptr;
+  s->graph_valid = false;
+}
+
+void free_sim(ms_sim* s) {
+  destroy_graph(s);
+  auto f = [](void* p) { if (p) (void)hipFree(p); };
+  f(s->state);
+  for (size_t b = 0; b < s->base_ptr.size(); ++b)
+    if (s->base_ptr[b] != s->state) f(s->base_ptr[b]);
+  f(s->ipool); f(s->fpool); f(s->ctr); f(s->feed_stage); f(s->feed_tmp); f(s->probe_buf);
+  f(s->prog.groups);
+  if (s->ev0) (void)hipEventDestroy(s->ev0);
+  if (s->ev1) (void)hipEventDestroy(s->ev1);
+  if (s->own_stream && s->stream) (void)hipStreamDestroy(s->stream);
+}
+
+// Pools of int32 and float arrays uploaded once; offsets resolved to pointers later.
+struct PoolBuilder {
+  std::vector<int32_t> ints;
+  std::vector<float> floats;
+  int64_t add_i(const std::vector<int32_t>& v) {
+    if (v.empty()) return -1;
+    int64_t off = (int64_t)ints.size();
+    ints.insert(ints.end(), v.begin(), v.end());
+    while (ints.size() % 64) ints.push_back(0);   // keep arrays 256-byte aligned
+    return off;
+  }
+  int64_t add_f(const std::vector<float>& v) {
+    if (v.empty()) return -1;
+    int64_t off = (int64_t)floats.size();
+    floats.insert(floats.end(), v.begin(), v.end());
+    while (floats.size() % 64) floats.push_back(0.f);
+    return off;
+  }
+};
+
+void setup_device(ms_sim* s) {
+  Plan& p = *s->plan;
+  const IR& ir = p.ir;
+  const int32_t B = s->B;
+  // ---- base arrays
+  s->base_ptr.assign(ir.bases.size(), nullptr);
+  for (size_t b = 0; b < ir.bases.size(); ++b) {
+    const BaseArray& ba = ir.bases[b];
+    if (ba.cls == SC_BATCHED) {
+      s->state_rows = (size_t)p.base_rows[b];
+      s->state = dev_alloc<float>(std::max<size_t>(1, s->state_rows * B));
+      s->base_ptr[b] = s->state;
+    } else {
+      const size_t n = (size_t)p.base_rows[b] * ba.cols;
+      std::vector<float> host(std::max<size_t>(1, n), 0.f);
+      for (size_t k = 0; k < ir.sigs.size(); ++k) {
+        const Signal& sg = ir.sigs[k];
+        if (sg.base != (int32_t)b) continue;
+        const size_t off = (size_t)p.sig_offset[k] * ba.cols;
+        for (size_t j = 0; j < sg.value.size(); ++j) host[off + j] = (float)sg.value[j];
+      }
+      s->base_ptr[b] = dev_alloc<float>(host.size());
+      HIPCHECK(hipMemcpy(s->base_ptr[b], host.data(), host.size() * sizeof(float), hipMemcpyHostToDevice));
+    }
+  }
+  if (!s->state) {
+    s->state = dev_alloc<float>(B);
+  }
+  // ---- lowered groups -> pools
+  PoolBuilder pb;
+  struct Offs { int64_t dst, src, a, V, ref, ptr, values, w, x, d, trc, tref, amp, ca, cb, feed; };
+  std::vector<Offs> offs;
+  for (const LGroup& g : p.lowered) {
+    Offs o{};
+    o.dst = pb.add_i(g.dst.idx); o.src = pb.add_i(g.src.idx); o.a = pb.add_i(g.a.idx);
+    o.V = pb.add_i(g.V.idx); o.ref = pb.add_i(g.ref.idx); o.ptr = pb.add_i(g.ptr);
+    o.w = pb.add_i(g.w_row); o.x = pb.add_i(g.x_row); o.d = pb.add_i(g.d_row);
+    o.feed = pb.add_i(g.feed_rows);
+    o.values = pb.add_f(g.values);
+    o.trc = g.tau_rc.size() > 1 ? pb.add_f(g.tau_rc) : -1;
+    o.tref = g.tau_ref.size() > 1 ? pb.add_f(g.tau_ref) : -1;
+    o.amp = g.amp.size() > 1 ? pb.add_f(g.amp) : -1;
+    o.ca = g.ca.size() > 1 ? pb.add_f(g.ca) : -1;
+    o.cb = g.cb.size() > 1 ? pb.add_f(g.cb) : -1;
+    offs.push_back(o);
+  }
+  const int64_t probe_off = pb.add_i(p.probe_src_rows);
+  s->ipool = dev_alloc<int32_t>(std::max<size_t>(1, pb.ints.size()));
+  s->fpool = dev_alloc<float>(std::max<size_t>(1, pb.floats.size()));
+  if (!pb.ints.empty())
+    HIPCHECK(hipMemcpy(s->ipool, pb.ints.data(), pb.ints.size() * 4, hipMemcpyHostToDevice));
+  if (!pb.floats.empty())
+    HIPCHECK(hipMemcpy(s->fpool, pb.floats.data(), pb.floats.size() * 4, hipMemcpyHostToDevice));
+  auto ip = [&](int64_t off) -> const int32_t* { return off < 0 ? nullptr : s->ipool + off; };
+  auto fp = [&](int64_t off) -> const float* { return off < 0 ? nullptr : s->fpool + off; };
+  auto opnd = [&](const LOperand& L, int64_t off) { return Opnd{ip(off), L.start}; };
+  for (size_t gi = 0; gi < p.lowered.size(); ++gi) {
+    const LGroup& g = p.lowered[gi];
+    const Offs& o = offs[gi];
+    Launch l;
+    l.type = g.type;
+    l.rows = g.rows;
+    l.dst = opnd(g.dst, o.dst);
+    l.src = opnd(g.src, o.src);
+    l.a = opnd(g.a, o.a);
+    l.V = opnd(g.V, o.V);
+    l.ref = opnd(g.ref, o.ref);
+    if (g.src.base >= 0) {
+      l.src_base = s->base_ptr[g.src.base];
+      l.src_bcast = ir.bases[g.src.base].cls != SC_BATCHED;
+    }
+    if (g.a.base >= 0) l.a_base = s->base_ptr[g.a.base];
+    l.ptr = ip(o.ptr);
+    l.values = fp(o.values);
+    l.M = g.M; l.K = g.K;
+    l.w_row = ip(o.w); l.x_row = ip(o.x); l.d_row = ip(o.d);
+    l.feed_rows = ip(o.feed);
+    if (g.type == OP_LIF || g.type == OP_LIF_RATE) {
+      l.np.tau_rc = g.tau_rc[0]; l.np.tau_ref = g.tau_ref[0]; l.np.amp = g.amp[0];
+      l.np.tau_rc_r = fp(o.trc); l.np.tau_ref_r = fp(o.tref); l.np.amp_r = fp(o.amp);
+    }
+    if (g.type == OP_LOWPASS) {
+      l.fp.a = g.ca[0]; l.fp.b = g.cb[0];
+      l.fp.a_r = fp(o.ca); l.fp.b_r = fp(o.cb);
+    }
+    s->launches.push_back(l);
+  }
+  s->probe_rows = (int32_t)p.probe_src_rows.size();
+  s->probe_src = ip(probe_off);
+  s->ctr = dev_alloc<int64_t>(2);
+  HIPCHECK(hipMemset(s->ctr, 0, 2 * sizeof(int64_t)));
+  HIPCHECK(hipMemset(s->state, 0, std::max<size_t>(1, s->state_rows) * B * sizeof(float)));
+}
+
+// -------------------------------------------------------------- launching
+constexpr int kBlock = 256;
+
+inline unsigned grid_for(int64_t n) { return (unsigned)std::max<int64_t>(1, (n + kBlock - 1) / kBlock); }
+
+void launch_group(ms_sim* s, const Launch& l) {
+  const int32_t B = s->B;
+  float* st = s->state;
+  const Strides S = s->S;
+  hipStream_t q = s->stream;
+  if (l.rows == 0) return;
+  const int64_t n = l.rows * B;
+  switch (l.type) {
+    case OP_FEED:
+      hipLaunchKernelGGL(k_feed, dim3(grid_for(n)), dim3(kBlock), 0, q, st, S, B, l.rows, l.dst,
+                         l.feed_rows, (const float*)s->feed_stage, s->plan->ir.feed_rows, s->ctr);
+      break;
+    case OP_RESET:
+      hipLaunchKernelGGL(k_reset, dim3(grid_for(n)), dim3(kBlock), 0, q, st, S, B, l.rows, l.dst, l.values);
+      break;
+    case OP_COPY:
+      hipLaunchKernelGGL(k_copy, dim3(grid_for(n)), dim3(kBlock), 0, q, st, S, B, l.rows, l.dst,
+                         l.src_base, l.src, (int)l.src_bcast);
+      break;
+    case OP_COPY_INC:
+      hipLaunchKernelGGL(k_copy_inc, dim3(grid_for(n)), dim3(kBlock), 0, q, st, S, B, l.rows, l.dst,
+                         l.src_base, l.src, (int)l.src_bcast, l.ptr);
+      break;
+    case OP_ELEM_INC:
+      hipLaunchKernelGGL(k_elem_inc, dim3(grid_for(n)), dim3(kBlock), 0, q, st, S, B, l.rows, l.dst,
+                         l.a_base, l.a, l.src_base, l.src, l.ptr);
+      break;
+    case OP_DOT_INC: {
+      if (l.K >= 64 && B <= 4) {
+        const int64_t waves = l.rows * (int64_t)l.M;
+        hipLaunchKernelGGL(k_dot_inc_wave, dim3(grid_for(waves * 64)), dim3(kBlock), 0, q, st, S, B, l.rows,
+                           l.M, l.K, l.a_base, l.w_row, l.x_row, l.d_row);
+      } else {
+        const int64_t work = l.rows * (int64_t)l.M * B;
+        hipLaunchKernelGGL(k_dot_inc, dim3(grid_for(work)), dim3(kBlock), 0, q, st, S, B, l.rows, l.M, l.K,
+                           l.a_base, l.w_row, l.x_row, l.d_row);
+      }
+      break;
+    }
+    case OP_LIF:
+      hipLaunchKernelGGL(k_lif, dim3(grid_for(n)), dim3(kBlock), 0, q, st, S, B, l.rows, l.src, l.dst,
+                         l.V, l.ref, l.np, s->dt);
+      break;
+    case OP_LIF_RATE:
+      hipLaunchKernelGGL(k_lif_rate, dim3(grid_for(n)), dim3(kBlock), 0, q, st, S, B, l.rows, l.src,
+                         l.dst, l.np);
+      break;
+    case OP_LOWPASS:
+      hipLaunchKernelGGL(k_lowpass, dim3(grid_for(n)), dim3(kBlock), 0, q, st, S, B, l.rows, l.dst,
+                         l.src, l.fp);
+      break;
+    default: fail(MS_E_INVALID, "unknown group type");
+  }
+}
+
+void launch_step(ms_sim* s) {
+  for (const Launch& l : s->launches) launch_group(s, l);
+  const int64_t n = (int64_t)s->probe_rows * s->B;
+  if (n > 0)
+    hipLaunchKernelGGL(k_probe, dim3(grid_for(n)), dim3(kBlock), 0, s->stream, (const float*)s->state,
+                       s->S, s->B, s->probe_rows, s->probe_src, s->probe_buf, s->ctr);
+  hipLaunchKernelGGL(k_advance, dim3(1), dim3(64), 0, s->stream, s->ctr);
+}
+
+void ensure_graph(ms_sim* s) {
+  if (s->graph_valid) return;
+  destroy_graph(s);
+  HIPCHECK(hipStreamBeginCapture(s->stream, hipStreamCaptureModeThreadLocal));
+  try {
+    for (int32_t u = 0; u < s->unroll; ++u) launch_step(s);
+  } catch (...) {
+    hipGraph_t g = nullptr;
+    (void)hipStreamEndCapture(s->stream, &g);
+    if (g) (void)hipGraphDestroy(g);
+    throw;
+  }
+  HIPCHECK(hipStreamEndCapture(s->stream, &s->graph));
+  HIPCHECK(hipGraphInstantiate(&s->graph_exec, s->graph, nullptr, nullptr, 0));
+  s->graph_valid = true;
+}
+
+void ensure_capacity(ms_sim* s, int64_t n_steps) {
+  const int32_t B = s->B;
+  const int32_t fr = s->plan->ir.feed_rows;
+  if (n_steps > s->feed_cap) {
+    int64_t cap = std::max<int64_t>(n_steps, s->feed_cap * 2);
+    if (s->feed_stage) HIPCHECK(hipFree(s->feed_stage));
+    s->feed_stage = dev_alloc<float>(std::max<size_t>(1, (size_t)cap * fr * B));
+    s->feed_cap = cap;
+    destroy_graph(s);
+    s->persistent_ok = false;
+  }
+  const int64_t need = s->steps_total + n_steps;
+  if (need > s->probe_cap) {
+    int64_t cap = std::max<int64_t>(need, s->probe_cap * 2);
+    float* nb = dev_alloc<float>(std::max<size_t>(1, (size_t)cap * s->probe_rows * B));
+    if (s->probe_buf) {
+      if (s->steps_total > 0)
+        HIPCHECK(hipMemcpyAsync(nb, s->probe_buf, (size_t)s->steps_total * s->probe_rows * B * 4,
+                                hipMemcpyDeviceToDevice, s->stream));
+      HIPCHECK(hipStreamSynchronize(s->stream));
+      HIPCHECK(hipFree(s->probe_buf));
+    }
+    s->probe_buf = nb;
+    s->probe_cap = cap;
+    destroy_graph(s);
+    s->persistent_ok = false;
+  }
+}
+
+void stage_feeds(ms_sim* s, int64_t n_steps, const ms_feed* feeds, int32_t n_feeds) {
+  const IR& ir = s->plan->ir;
+  const int32_t B = s->B;
+  const int32_t fr = ir.feed_rows;
+  if (fr == 0) return;
+  HIPCHECK(hipMemsetAsync(s->feed_stage, 0, (size_t)n_steps * fr * B * 4, s->stream));
+  for (int32_t i = 0; i < n_feeds; ++i) {
+    const ms_feed& f = feeds[i];
+    if (f.node_id < 0 || f.node_id >= (int32_t)ir.feed_row_of_node.size() || ir.feed_row_of_node[f.node_id] < 0)
+      fail(MS_E_INVALID, "feed for node " + std::to_string(f.node_id) + ", which is not an input node");
+    if (!f.data) fail(MS_E_INVALID, "feed data is NULL");
+    const int32_t nsize = ir.node_size[f.node_id];
+    const size_t elems = (size_t)B * n_steps * nsize;
+    const float* src = f.data;
+    if (!f.on_device) {
+      if (elems > s->feed_tmp_elems) {
+        HIPCHECK(hipStreamSynchronize(s->stream));
+        if (s->feed_tmp) HIPCHECK(hipFree(s->feed_tmp));
+        s->feed_tmp = dev_alloc<float>(elems);
+        s->feed_tmp_elems = elems;
+      }
+      HIPCHECK(hipMemcpyAsync(s->feed_tmp, f.data, elems * 4, hipMemcpyHostToDevice, s->stream));
+      src = s->feed_tmp;
+    }
+    const int64_t n = (int64_t)elems;
+    hipLaunchKernelGGL(k_stage_feed, dim3(grid_for(n)), dim3(kBlock), 0, s->stream, src, B, n_steps,
+                       nsize, s->feed_stage, fr, ir.feed_row_of_node[f.node_id]);
+    if (!f.on_device) HIPCHECK(hipStreamSynchronize(s->stream));   // feed_tmp reused
+  }
+}
+
+// Weight bytes read per step (every parameter base array).
+int64_t param_bytes(const Plan& p) {
+  int64_t n = 0;
+  for (size_t b = 0; b < p.ir.bases.size(); ++b)
+    if (p.ir.bases[b].cls != SC_BATCHED) n += p.base_rows[b] * p.ir.bases[b].cols * 4;
+  return n;
+}
+
+// Persistent per-column driver when one workgroup can hold a column's whole
+// step cheaply (small weights, modest state); launches otherwise.
+int32_t choose_driver(const Plan& p, int32_t B, int32_t requested) {
+  if (requested != MS_DRIVER_AUTO) return requested;
+  const int64_t rows = p.base_rows.empty() ? 0 : p.base_rows[0];
+  const int64_t wbytes = param_bytes(p);
+  if (wbytes <= (1 << 20) && rows <= (1 << 17) && (B >= 8 || rows <= 8192)) return MS_DRIVER_PERSISTENT;
+  return MS_DRIVER_GRAPH;
+}
+
+void setup_persistent(ms_sim* s) {
+  std::vector<GroupDesc> gd;
+  for (const Launch& l : s->launches) {
+    GroupDesc g{};
+    g.type = l.type; g.M = l.M; g.K = l.K; g.bcast = l.src_bcast ? 1 : 0; g.rows = l.rows;
+    g.dst = l.dst; g.src = l.src; g.a = l.a; g.V = l.V; g.ref = l.ref;
+    g.src_base = l.src_base; g.a_base = l.a_base; g.ptr = l.ptr; g.values = l.values;
+    g.w_row = l.w_row; g.x_row = l.x_row; g.d_row = l.d_row; g.feed_row = l.feed_rows;
+    g.np = l.np; g.fp = l.fp;
+    gd.push_back(g);
+  }
+  s->prog.n_groups = (int32_t)gd.size();
+  s->prog.groups = dev_alloc<GroupDesc>(std::max<size_t>(1, gd.size()));
+  if (!gd.empty())
+    HIPCHECK(hipMemcpy(s->prog.groups, gd.data(), gd.size() * sizeof(GroupDesc), hipMemcpyHostToDevice));
+}
+
+void run_persistent(ms_sim* s, int64_t n_steps) {
+  const int64_t rows = (int64_t)s->state_rows;
+  const int threads = rows <= 4096 ? 256 : 1024;
+  hipLaunchKernelGGL(k_persistent, dim3(s->B), dim3(threads), 0, s->stream, s->state, s->S, s->B,
+                     (const GroupDesc*)s->prog.groups, s->prog.n_groups, n_steps, s->dt,
+                     (const float*)s->feed_stage, s->plan->ir.feed_rows, s->probe_src, s->probe_rows,
+                     s->probe_buf, s->steps_total);
+  hipLaunchKernelGGL(k_set_ctr, dim3(1), dim3(64), 0, s->stream, s->ctr, s->steps_total + n_steps, n_steps);
+}
+
+}  // namespace
+
+extern "C" {
+
+ms_status ms_sim_create(const ms_model* model, const ms_sim_opts* opts, ms_sim** out) {
+  return guarded([&] {
+    if (!model || !out) fail(MS_E_INVALID, "NULL argument");
+    ms_sim_opts def;
+    ms_sim_opts_default(&def);
+    const ms_sim_opts* o = opts ? opts : &def;
+    if (!(o->dt > 0)) fail(MS_E_INVALID, "dt must be > 0");
+    if (o->minibatch < 1) fail(MS_E_INVALID, "minibatch must be >= 1");
+    if (o->unroll < 1) fail(MS_E_INVALID, "unroll must be >= 1");
+    if (o->driver < MS_DRIVER_AUTO || o->driver > MS_DRIVER_PERSISTENT) fail(MS_E_INVALID, "unknown driver");
+    int ndev = 0;
+    HIPCHECK(hipGetDeviceCount(&ndev));
+    if (o->device < 0 || o->device >= ndev) fail(MS_E_INVALID, "device ordinal out of range");
+    auto s = new ms_sim();
+    try {
+      s->B = o->minibatch;
+      s->device = o->device;
+      s->unroll = o->unroll;
+      s->dt = (float)o->dt;
+      s->plan = make_plan(model_of(model), o->dt, plan_opts_from(o));
+      DeviceGuard dg(s->device);
+      if (o->stream) {
+        s->stream = (hipStream_t)o->stream;
+      } else {
+        HIPCHECK(hipStreamCreateWithFlags(&s->stream, hipStreamNonBlocking));
+        s->own_stream = true;
+      }
+      HIPCHECK(hipEventCreate(&s->ev0));
+      HIPCHECK(hipEventCreate(&s->ev1));
+      s->driver = choose_driver(*s->plan, s->B, o->driver);
+      // persistent: one workgroup per batch column -> column-major state
+      s->S = s->driver == MS_DRIVER_PERSISTENT ? Strides{1, (int64_t)std::max<int64_t>(1, s->plan->base_rows.empty() ? 1 : s->plan->base_rows[0])}
+                                               : Strides{(int64_t)s->B, 1};
+      setup_device(s);
+      if (s->driver == MS_DRIVER_PERSISTENT) setup_persistent(s);
+      ensure_capacity(s, std::max<int64_t>(1, o->probe_capacity_steps));
+      HIPCHECK(hipStreamSynchronize(s->stream));
+    } catch (...) {
+      free_sim(s);
+      delete s;
+      throw;
+    }
+    *out = s;
+  });
+}
+
+void ms_sim_destroy(ms_sim* s) {
+  if (!s) return;
+  int prev = 0;
+  (void)hipGetDevice(&prev);
+  (void)hipSetDevice(s->device);
+  if (s->stream) (void)hipStreamSynchronize(s->stream);
+  free_sim(s);
+  (void)hipSetDevice(prev);
+  delete s;
+}
+
+ms_status ms_sim_run_steps(ms_sim* s, int64_t n_steps, const ms_feed* feeds, int32_t n_feeds) {
+  return guarded([&] {
+    if (!s) fail(MS_E_INVALID, "NULL sim");
+    if (n_steps < 0) fail(MS_E_INVALID, "n_steps must be >= 0");
+    if (n_feeds < 0 || (n_feeds > 0 && !feeds)) fail(MS_E_INVALID, "bad feeds");
+    if (n_steps == 0) return;
+    DeviceGuard dg(s->device);
+    ensure_capacity(s, n_steps);
+    stage_feeds(s, n_steps, feeds, n_feeds);
+    HIPCHECK(hipMemsetAsync(s->ctr + 1, 0, sizeof(int64_t), s->stream));
+    HIPCHECK(hipEventRecord(s->ev0, s->stream));
+    if (s->driver == MS_DRIVER_PERSISTENT) {
+      run_persistent(s, n_steps);
+    } else if (s->driver == MS_DRIVER_GRAPH) {
+      ensure_graph(s);
+      int64_t k = 0;
+      for (; k + s->unroll <= n_steps; k += s->unroll) HIPCHECK(hipGraphLaunch(s->graph_exec, s->stream));
+      for (; k < n_steps; ++k) launch_step(s);
+    } else {
+      for (int64_t k = 0; k < n_steps; ++k) launch_step(s);
+    }
+    HIPCHECK(hipGetLastError());
+    HIPCHECK(hipEventRecord(s->ev1, s->stream));
+    s->steps_total += n_steps;
+  });
+}
+
+ms_status ms_sim_sync(ms_sim* s) {
+  return guarded([&] {
+    if (!s) fail(MS_E_INVALID, "NULL sim");
+    DeviceGuard dg(s->device);
+    HIPCHECK(hipStreamSynchronize(s->stream));
+  });
+}
+
+ms_status ms_sim_last_run_ms(ms_sim* s, double* ms_out) {
+  return guarded([&] {
+    if (!s || !ms_out) fail(MS_E_INVALID, "NULL argument");
+    DeviceGuard dg(s->device);
+    HIPCHECK(hipEventSynchronize(s->ev1));
+    float ms = 0.f;
+    HIPCHECK(hipEventElapsedTime(&ms, s->ev0, s->ev1));
+    *ms_out = ms;
+  });
+}
+
+ms_status ms_sim_steps(const ms_sim* s, int64_t* out) {
+  return guarded([&] {
+    if (!s || !out) fail(MS_E_INVALID, "NULL argument");
+    *out = s->steps_total;
+  });
+}
+
+ms_status ms_sim_info(const ms_sim* s, int32_t* driver_out, int32_t* groups_out) {
+  return guarded([&] {
+    if (!s) fail(MS_E_INVALID, "NULL sim");
+    if (driver_out) *driver_out = s->driver;
+    if (groups_out) *groups_out = (int32_t)s->launches.size();
+  });
+}
+
+ms_status ms_sim_probe_width(const ms_sim* s, int32_t probe, int32_t* w) {
+  return guarded([&] {
+    if (!s || !w) fail(MS_E_INVALID, "NULL argument");
+    if (probe < 0 || probe >= (int32_t)s->plan->probe_width.size()) fail(MS_E_INVALID, "probe id out of range");
+    *w = s->plan->probe_width[probe];
+  });
+}
+
+ms_status ms_sim_probe_read(ms_sim* s, int32_t probe, float* out, int64_t cap, int32_t out_on_device) {
+  return guarded([&] {
+    if (!s || !out) fail(MS_E_INVALID, "NULL argument");
+    const Plan& p = *s->plan;
+    if (probe < 0 || probe >= (int32_t)p.probe_width.size()) fail(MS_E_INVALID, "probe id out of range");
+    const int32_t w = p.probe_width[probe];
+    const int64_t T = s->steps_total;
+    const int64_t n = (int64_t)s->B * T * w;
+    if (cap < n) fail(MS_E_INVALID, "probe output capacity too small");
+    if (n == 0) return;
+    DeviceGuard dg(s->device);
+    float* tmp = out_on_device ? out : dev_alloc<float>((size_t)n);
+    hipLaunchKernelGGL(k_probe_extract, dim3(grid_for(n)), dim3(kBlock), 0, s->stream,
+                       (const float*)s->probe_buf, s->B, T, s->probe_rows, p.probe_row_offset[probe], w, tmp);
+    hipError_t e = hipGetLastError();
+    if (e == hipSuccess && !out_on_device)
+      e = hipMemcpyAsync(out, tmp, (size_t)n * 4, hipMemcpyDeviceToHost, s->stream);
+    if (e == hipSuccess) e = hipStreamSynchronize(s->stream);
+    if (!out_on_device) (void)hipFree(tmp);
+    if (e != hipSuccess) fail(MS_E_HIP, std::string("probe read: ") + hipGetErrorString(e));
+  });
+}
+
+ms_status ms_sim_reset(ms_sim* s) {
+  return guarded([&] {
+    if (!s) fail(MS_E_INVALID, "NULL sim");
+    DeviceGuard dg(s->device);
+    HIPCHECK(hipMemsetAsync(s->state, 0, std::max<size_t>(1, s->state_rows) * s->B * 4, s->stream));
+    HIPCHECK(hipMemsetAsync(s->ctr, 0, 2 * sizeof(int64_t), s->stream));
+    HIPCHECK(hipStreamSynchronize(s->stream));
+    s->steps_total = 0;
+  });
+}
+
+static int32_t state_signal(const ms_sim* s, int32_t which, int32_t id) {
+  const IR& ir = s->plan->ir;
+  auto pick = [&](const std::vector<int32_t>& v) -> int32_t {
+    if (id < 0 || id >= (int32_t)v.size() || v[id] < 0) fail(MS_E_INVALID, "no such state for this id");
+    return v[id];
+  };
+  switch (which) {
+    case MS_STATE_VOLTAGE: return pick(ir.ens_V);
+    case MS_STATE_REFRACTORY: return pick(ir.ens_ref);
+    case MS_STATE_SYNAPSE: return pick(ir.conn_y);
+    case MS_STATE_PROBE_SYNAPSE: return pick(ir.probe_y);
+    default: fail(MS_E_INVALID, "unknown state kind");
+  }
+}
+
+ms_status ms_sim_get_state(ms_sim* s, int32_t which, int32_t id, float* out, int64_t cap) {
+  return guarded([&] {
+    if (!s || !out) fail(MS_E_INVALID, "NULL argument");
+    const int32_t sig = state_signal(s, which, id);
+    const int32_t rows = s->plan->ir.sigs[sig].rows;
+    const int64_t n = (int64_t)rows * s->B;
+    if (cap < n) fail(MS_E_INVALID, "state output capacity too small");
+    DeviceGuard dg(s->device);
+    std::vector<float> h(s->state_rows * s->B);
+    HIPCHECK(hipStreamSynchronize(s->stream));
+    HIPCHECK(hipMemcpy(h.data(), s->state, h.size() * 4, hipMemcpyDeviceToHost));
+    const int64_t r0 = s->plan->sig_offset[sig];
+    for (int32_t b = 0; b < s->B; ++b)
+      for (int32_t r = 0; r < rows; ++r) out[(size_t)b * rows + r] = h[(size_t)((r0 + r) * s->S.rs + b * s->S.cs)];
+  });
+}
+
+ms_status ms_sim_set_state(ms_sim* s, int32_t which, int32_t id, const float* in, int64_t n_elems) {
+  return guarded([&] {
+    if (!s || !in) fail(MS_E_INVALID, "NULL argument");
+    const int32_t sig = state_signal(s, which, id);
+    const int32_t rows = s->plan->ir.sigs[sig].rows;
+    const int64_t n = (int64_t)rows * s->B;
+    if (n_elems != n) fail(MS_E_INVALID, "state size mismatch");
+    DeviceGuard dg(s->device);
+    std::vector<float> h(s->state_rows * s->B);
+    HIPCHECK(hipStreamSynchronize(s->stream));
+    HIPCHECK(hipMemcpy(h.data(), s->state, h.size() * 4, hipMemcpyDeviceToHost));
+    const int64_t r0 = s->plan->sig_offset[sig];
+    for (int32_t b = 0; b < s->B; ++b)
+      for (int32_t r = 0; r < rows; ++r) h[(size_t)((r0 + r) * s->S.rs + b * s->S.cs)] = in[(size_t)b * rows + r];
+    HIPCHECK(hipMemcpy(s->state, h.data(), h.size() * 4, hipMemcpyHostToDevice));
+  });
+}
+
+}  // extern "C"

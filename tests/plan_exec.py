@@ -1,0 +1,221 @@
+"""Float64 CPU executor of an exported merged plan (test helper).
+
+It runs the library's plan -- base-array layout, merged groups in plan order,
+lowered index arrays and the float32 parameter values the GPU uses -- with
+numpy in float64.  Compared with the unmerged oracle (parameters rounded to
+float32), it checks that merging, planning, sorting, simplification and
+lowering do not change the model's output (paper Sec. 4.2), without a GPU.
+"""
+import numpy as np
+
+
+def _rows(op, n):
+    if op is None:
+        return None
+    if "idx" in op:
+        return np.asarray(op["idx"], np.int64)
+    return op["start"] + np.arange(n, dtype=np.int64)
+
+
+def _vec(v, n):
+    v = np.asarray(v, np.float64)
+    return np.broadcast_to(v, (n,)) if v.size == 1 else v
+
+
+def oracle_param(oracle, name):
+    """Value of a parameter signal, by its canonical name, from the oracle."""
+    owner, kind = name.split(".", 1)
+    i = int(owner[1:])
+    spec = oracle.spec
+    if owner[0] == "e":
+        if kind == "bias":
+            return oracle.bias[i]
+        if kind == "gain":
+            return oracle.gain[i]
+        if kind == "enc":
+            return oracle.enc[i]
+        if kind in ("Did", "Dprod"):
+            return oracle.dec[(i, "identity" if kind == "Did" else "product")].T
+    if owner[0] == "c":
+        if kind == "T":
+            return oracle.conn_T[i]
+        if kind == "t":
+            return np.array([oracle.conn_T[i]])
+        if kind == "D":
+            return oracle.conn_dec[i].T
+    if owner[0] == "n" and kind == "value":
+        return np.asarray(spec.nodes[i].value, np.float64)
+    raise KeyError(name)
+
+
+class PlanExecutor:
+    """params_from: an OracleSim whose (float32-rounded) parameters replace the
+    library's, so that only the plan itself is under test; None uses the
+    library's exported float32 parameters."""
+
+    def __init__(self, plan, spec, minibatch, params_from=None):
+        self.j = plan.json()
+        self.B = minibatch
+        self.spec = spec
+        self.bases = []
+        for bi, b in enumerate(self.j["bases"]):
+            if b["name"] == "state":
+                self.bases.append(None)
+                self.state_base = bi
+            elif params_from is None:
+                self.bases.append(plan.base(bi).astype(np.float64).reshape(b["rows"], b["cols"]))
+            else:
+                arr = np.zeros((b["rows"], b["cols"]))
+                for sg in self.j["signals"]:
+                    if sg["base"] == bi:
+                        v = np.asarray(oracle_param(params_from, sg["name"]), np.float64)
+                        arr[sg["offset"]:sg["offset"] + sg["rows"]] = v.reshape(sg["rows"], b["cols"])
+                self.bases.append(arr)
+        if params_from is not None:
+            self._replace_constants(params_from)
+        self.rows = self.j["bases"][self.state_base]["rows"]
+        self.fed = [i for i, n in enumerate(spec.nodes) if not n.passthrough and n.value is None]
+        self.dt = spec.dt
+        self.reset()
+
+    def _replace_constants(self, o):
+        """Reset values, neuron parameters and filter coefficients from the oracle."""
+        for g in self.j["groups"]:
+            if g["type"] == "Reset" and "values" in g:
+                rows = {sg["name"]: sg["rows"] for sg in self.j["signals"]}
+                dst = {"reset": "out", "resetx": "x", "resetid": "did", "resetprod": "dprod",
+                       "resetv": "v", "resetd": "xd"}
+                vals = []
+                for name in g["ops"]:
+                    owner, kind = name.split(".", 1)
+                    i = int(owner[1:])
+                    if kind == "bias":
+                        vals.append(o.bias[i])
+                    elif kind == "const":
+                        vals.append(np.asarray(self.spec.nodes[i].value, float))
+                    else:
+                        vals.append(np.zeros(rows[owner + "." + dst[kind]]))
+                g["values"] = np.concatenate(vals).tolist()
+            elif g["type"] in ("SimLIF", "SimLIFRate"):
+                cols = {"tau_rc": [], "tau_ref": [], "amp": []}
+                for name in g["ops"]:
+                    e = self.spec.ensembles[int(name.split(".")[0][1:])]
+                    for k in cols:
+                        cols[k].append(np.full(e.n_neurons, getattr(e, "amplitude" if k == "amp" else k)))
+                for k in cols:
+                    g[k] = np.concatenate(cols[k]).tolist()
+            elif g["type"] == "Lowpass":
+                ca, cb = [], []
+                for name in g["ops"]:
+                    owner = name.split(".")[0]
+                    i = int(owner[1:])
+                    a, b = (o.conn_a[i] if owner[0] == "c" else o.probe_a[i])
+                    w = (o.y[i] if owner[0] == "c" else o.yp[i]).shape[1]
+                    ca.append(np.full(w, a)); cb.append(np.full(w, b))
+                g["ca"] = np.concatenate(ca).tolist()
+                g["cb"] = np.concatenate(cb).tolist()
+
+    def reset(self):
+        self.st = np.zeros((self.rows, self.B))
+        self.records = []
+
+    def _src(self, base, rows):
+        if base == self.state_base:
+            return self.st[rows]
+        return np.broadcast_to(self.bases[base][rows, 0][:, None], (len(rows), self.B))
+
+    def step(self, feed_rows_values):
+        st = self.st
+        for g in self.j["groups"]:
+            t, n = g["type"], g["rows"]
+            if t == "Feed":
+                st[_rows(g["dst"], n)] = feed_rows_values[np.asarray(g["feed_rows"])]
+            elif t == "Reset":
+                d = _rows(g["dst"], n)
+                st[d] = _vec(g["values"], n)[:, None] if "values" in g else 0.0
+            elif t == "Copy":
+                st[_rows(g["dst"], n)] = self._src(g["src"]["base"], _rows(g["src"], n))
+            elif t in ("CopyInc", "ElementwiseInc"):
+                d = _rows(g["dst"], n)
+                if "ptr" in g:
+                    ptr = np.asarray(g["ptr"])
+                    m = ptr[-1]
+                    seg = np.repeat(np.arange(n), np.diff(ptr))
+                else:
+                    m = n
+                    seg = np.arange(n)
+                vals = self._src(g["src"]["base"], _rows(g["src"], m))
+                if t == "ElementwiseInc":
+                    vals = vals * self.bases[g["a"]["base"]][_rows(g["a"], m), 0][:, None]
+                acc = np.zeros((n, self.B))
+                np.add.at(acc, seg, vals)
+                st[d] += acc
+            elif t == "DotInc":
+                M, K = g["M"], g["K"]
+                # the weight base is found from the key of the group's first op via JSON
+                W = self.bases[self._weight_base(g)]
+                for w0, x0, d0 in zip(g["w_row"], g["x_row"], g["d_row"]):
+                    Wm = W[w0:w0 + M, :K] if W.shape[1] == K else W[w0:w0 + M * K, 0].reshape(M, K)
+                    st[d0:d0 + M] += Wm @ st[x0:x0 + K]
+            elif t in ("SimLIF", "SimLIFRate"):
+                J = st[_rows(g["src"], n)]
+                trc = _vec(g["tau_rc"], n)[:, None]
+                tref = _vec(g["tau_ref"], n)[:, None]
+                amp = _vec(g["amp"], n)[:, None]
+                if t == "SimLIFRate":
+                    out = np.zeros_like(J)
+                    m = J > 1
+                    r = np.zeros_like(J)
+                    r[m] = 1.0 / (np.broadcast_to(tref, J.shape)[m] +
+                                  np.broadcast_to(trc, J.shape)[m] * np.log1p(1.0 / (J[m] - 1.0)))
+                    out = amp * r
+                else:
+                    vr, rr = _rows(g["V"], n), _rows(g["ref"], n)
+                    V, ref = st[vr].copy(), st[rr].copy()
+                    dt = self.dt
+                    integ = np.clip(dt - ref, 0, dt)
+                    V = V - (J - V) * np.expm1(-integ / trc)
+                    ref = np.maximum(ref - dt, 0)
+                    spk = V > 1
+                    q = np.where(spk & (J > 1), (V - 1) / np.where(J > 1, J - 1, 1), 0.0)
+                    since = np.where(q >= 1, integ,
+                                     np.minimum(-trc * np.log1p(-np.minimum(q, 0.999999999999)), integ))
+                    since = np.where(spk & (J > 1), since, 0.0)
+                    st[vr] = np.where(spk, 0.0, np.maximum(V, 0.0))
+                    st[rr] = np.where(spk, tref - since, ref)
+                    out = np.where(spk, amp / dt, 0.0)
+                st[_rows(g["dst"], n)] = out
+            elif t == "Lowpass":
+                y, v = _rows(g["dst"], n), _rows(g["src"], n)
+                st[y] = _vec(g["ca"], n)[:, None] * st[y] + _vec(g["cb"], n)[:, None] * st[v]
+            else:
+                raise ValueError(t)
+        self.records.append(st[np.asarray(self.j["probe_rows"], np.int64)].copy())
+
+    def _weight_base(self, g):
+        sigs = self.j["signals"]
+        # weight signals are named like the op's owner with .enc/.D*/.T
+        name = g["ops"][0]
+        owner, kind = name.split(".", 1)
+        if kind == "enc":
+            wname = owner + ".enc"
+        elif kind.startswith("dec"):
+            wname = owner + ".D" + kind[3:]
+        else:   # transform
+            wname = owner + ".T"
+        for s in sigs:
+            if s["name"] == wname:
+                return s["base"]
+        raise KeyError(wname)
+
+    def run(self, n_steps, feeds):
+        for k in range(n_steps):
+            vals = np.concatenate([np.asarray(feeds[i][:, k, :], np.float64).T if i in feeds
+                                   else np.zeros((self.spec.nodes[i].size, self.B))
+                                   for i in self.fed], axis=0) if self.fed else np.zeros((0, self.B))
+            self.step(vals)
+
+    def data(self, probe):
+        off = self.j["probe_offsets"]
+        rec = np.stack(self.records, axis=0)        # [T, probe_rows, B]
+        return np.transpose(rec[:, off[probe]:off[probe + 1], :], (2, 0, 1))

@@ -1,0 +1,66 @@
+"""GPU parity: the HIP simulator against the float64 oracle on the same seeded
+inputs, through the C ABI.  Tolerances: rate mode max|gpu - oracle| /
+max|oracle| <= 1e-5 per probe; spiking mode spike flips <= 1e-4 of oracle spikes
+and filtered decoded probes within 1e-3 absolute."""
+import numpy as np
+import pytest
+
+import paper_1805_11144_amd as M
+from oracle.sim import OracleSim
+from synth import make_workload
+from tests.parity import flip_fraction, rel_err
+
+pytestmark = pytest.mark.gpu
+
+SMALL = {
+    "c1": dict(n_steps=200),
+    "c2": dict(n_steps=60, minibatch=3, n_neurons=20, n_eval=200),
+    "c3": dict(n_steps=30, minibatch=4, n_hidden=96, n_in=50),
+    "c4": dict(n_steps=60, minibatch=3, n_ens=6, n_neurons=40, n_eval=200),
+    "c5": dict(n_steps=40, n_ens=12, n_neurons=40, n_eval=200, n_input_targets=4, n_probed=3),
+}
+DRIVERS = {"steps": M.DRIVER_STEPS, "graph": M.DRIVER_GRAPH, "persistent": M.DRIVER_PERSISTENT}
+
+
+def run_gpu(w, **opts):
+    model = M.model_from_spec(w.spec)
+    with M.Simulator(model, minibatch=w.minibatch, **opts) as sim:
+        sim.run_steps(w.n_steps, w.feeds)
+        return [sim.data(p) for p in range(len(w.spec.probes))]
+
+
+def run_oracle(w):
+    ref = OracleSim(w.spec, minibatch=w.minibatch, param_dtype=np.float32)
+    ref.run_steps(w.n_steps, w.feeds)
+    return [ref.data(p) for p in range(len(w.spec.probes))]
+
+
+@pytest.mark.parametrize("driver", list(DRIVERS))
+@pytest.mark.parametrize("name", list(SMALL))
+def test_rate_mode_parity(name, driver):
+    w = make_workload(name, neuron_type="lif_rate", **SMALL[name])
+    got = run_gpu(w, driver=DRIVERS[driver], unroll=7)
+    exp = run_oracle(w)
+    for pi, (g, e) in enumerate(zip(got, exp)):
+        r = rel_err(g, e)
+        print(f"{name} {driver} probe {pi}: rel {r:.2e}")
+        assert r <= 1e-5, (name, driver, pi, r)
+
+
+@pytest.mark.parametrize("driver", list(DRIVERS))
+@pytest.mark.parametrize("name", list(SMALL))
+def test_spiking_mode_parity(name, driver):
+    w = make_workload(name, neuron_type="lif", **SMALL[name])
+    got = run_gpu(w, driver=DRIVERS[driver], unroll=7)
+    exp = run_oracle(w)
+    for pi, (g, e) in enumerate(zip(got, exp)):
+        p = w.spec.probes[pi]
+        if p.target[0] == "neurons":
+            f = flip_fraction(g, e)
+            print(f"{name} {driver} probe {pi}: flips {f:.2e} of {int((e > 0).sum())} spikes")
+            assert f <= 1e-4, (name, driver, pi, f)
+        else:
+            d = float(np.abs(g - e).max())
+            print(f"{name} {driver} probe {pi}: abs {d:.2e}")
+            if p.synapse is not None:
+                assert d <= 1e-3, (name, driver, pi, d)
