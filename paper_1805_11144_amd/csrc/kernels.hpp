@@ -26,7 +26,9 @@ __device__ __forceinline__ int64_t rowof(const Opnd& o, int64_t r) {
 
 struct NeuronParams {
   float tau_rc, tau_ref, amp;                     // uniform values
+  float full;                                     // expm1(-dt / tau_rc), uniform
   const float *tau_rc_r, *tau_ref_r, *amp_r;      // per-row values or null
+  const float* full_r;                            // per-row expm1(-dt / tau_rc) or null
 };
 
 struct FilterParams {
@@ -55,9 +57,11 @@ __device__ __forceinline__ void lif_item(float* st, const Strides& S, int64_t r,
   const float j = st[jv];
   float v = st[vv];
   float rf = st[rv];
-  // integrate exactly over the non-refractory part of the step
+  // integrate exactly over the non-refractory part of the step; a neuron that
+  // is not refractory integrates the whole step with the precomputed factor
   const float integ = fminf(fmaxf(dt - rf, 0.0f), dt);
-  v = v - (j - v) * expm1f(-integ / tau_rc);
+  const float e = rf <= 0.0f ? (np.full_r ? np.full_r[r] : np.full) : expm1f(-integ / tau_rc);
+  v = v - (j - v) * e;
   rf = fmaxf(rf - dt, 0.0f);
   float out = 0.0f;
   if (v > 1.0f) {
@@ -142,42 +146,42 @@ __device__ __forceinline__ void dot_row_item(float* st, const Strides& S, int64_
 }
 
 // ----------------------------------------------------------- launch kernels
+// Work items are (row, batch) pairs flattened as row * B + b; the host checks
+// that rows * B fits in 32 bits so the split uses 32-bit division.
 #define GRID_ITEM(n)                                                        \
-  const int64_t _i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;        \
-  if (_i >= (n)) return;
+  const uint32_t _i = blockIdx.x * blockDim.x + threadIdx.x;                \
+  if (_i >= (uint32_t)(n)) return;                                          \
+  const uint32_t _r = _i / (uint32_t)B, _b = _i - _r * (uint32_t)B;
 
 __global__ void k_reset(float* st, Strides S, int32_t B, int64_t rows, Opnd dst, const float* values) {
   GRID_ITEM(rows * B);
-  const int64_t r = _i / B, b = _i % B;
-  st[at(S, rowof(dst, r), b)] = values ? values[r] : 0.0f;
+  st[at(S, rowof(dst, _r), _b)] = values ? values[_r] : 0.0f;
 }
 
 __global__ void k_copy(float* st, Strides S, int32_t B, int64_t rows, Opnd dst, const float* src_base,
                        Opnd src, int bcast) {
   GRID_ITEM(rows * B);
-  const int64_t r = _i / B, b = _i % B;
-  st[at(S, rowof(dst, r), b)] = src_val(src_base, S, bcast, rowof(src, r), b);
+  st[at(S, rowof(dst, _r), _b)] = src_val(src_base, S, bcast, rowof(src, _r), _b);
 }
 
 __global__ void k_copy_inc(float* st, Strides S, int32_t B, int64_t rows, Opnd dst, const float* src_base,
                            Opnd src, int bcast, const int32_t* ptr) {
   GRID_ITEM(rows * B);
-  copy_inc_item(st, S, _i / B, _i % B, dst, src_base, src, bcast, ptr);
+  copy_inc_item(st, S, _r, _b, dst, src_base, src, bcast, ptr);
 }
 
 __global__ void k_elem_inc(float* st, Strides S, int32_t B, int64_t rows, Opnd dst, const float* a_base,
                            Opnd a, const float* x_base, Opnd x, const int32_t* ptr) {
   GRID_ITEM(rows * B);
-  elem_inc_item(st, S, _i / B, _i % B, dst, a_base, a, x_base, x, ptr);
+  elem_inc_item(st, S, _r, _b, dst, a_base, a, x_base, x, ptr);
 }
 
 // thread per (op, m, b)
 __global__ void k_dot_inc(float* st, Strides S, int32_t B, int64_t nops, int32_t M, int32_t K,
                           const float* W, const int32_t* w_row, const int32_t* x_row, const int32_t* d_row) {
   GRID_ITEM(nops * M * B);
-  const int64_t b = _i % B;
-  const int64_t t = _i / B;
-  dot_row_item(st, S, t / M, (int32_t)(t % M), b, K, W, w_row, x_row, d_row);
+  const uint32_t op = _r / (uint32_t)M;
+  dot_row_item(st, S, op, (int32_t)(_r - op * (uint32_t)M), _b, K, W, w_row, x_row, d_row);
 }
 
 // wave per (op, m): lanes split K, reduced across the wavefront; loops over b.
@@ -203,34 +207,32 @@ __global__ void k_dot_inc_wave(float* st, Strides S, int32_t B, int64_t nops, in
 __global__ void k_lif(float* st, Strides S, int32_t B, int64_t rows, Opnd J, Opnd s, Opnd V, Opnd R,
                       NeuronParams np, float dt) {
   GRID_ITEM(rows * B);
-  lif_item(st, S, _i / B, _i % B, J, s, V, R, np, dt);
+  lif_item(st, S, _r, _b, J, s, V, R, np, dt);
 }
 
 __global__ void k_lif_rate(float* st, Strides S, int32_t B, int64_t rows, Opnd J, Opnd s, NeuronParams np) {
   GRID_ITEM(rows * B);
-  lif_rate_item(st, S, _i / B, _i % B, J, s, np);
+  lif_rate_item(st, S, _r, _b, J, s, np);
 }
 
 __global__ void k_lowpass(float* st, Strides S, int32_t B, int64_t rows, Opnd y, Opnd v, FilterParams fp) {
   GRID_ITEM(rows * B);
-  lowpass_item(st, S, _i / B, _i % B, y, v, fp);
+  lowpass_item(st, S, _r, _b, y, v, fp);
 }
 
 // node output <- feed staging [step][feed_rows][B] at the run-relative step ctr[1]
 __global__ void k_feed(float* st, Strides S, int32_t B, int64_t rows, Opnd dst, const int32_t* feed_row,
                        const float* stage, int32_t feed_rows, const int64_t* ctr) {
   GRID_ITEM(rows * B);
-  const int64_t r = _i / B, b = _i % B;
   const int64_t t = ctr[1];
-  st[at(S, rowof(dst, r), b)] = stage[(t * feed_rows + feed_row[r]) * B + b];
+  st[at(S, rowof(dst, _r), _b)] = stage[(t * feed_rows + feed_row[_r]) * B + _b];
 }
 
 // probe buffer [step][probe_rows][B] at the absolute step ctr[0]
 __global__ void k_probe(const float* st, Strides S, int32_t B, int32_t rows, const int32_t* src, float* buf,
                         const int64_t* ctr) {
   GRID_ITEM((int64_t)rows * B);
-  const int64_t r = _i / B, b = _i % B;
-  buf[(ctr[0] * rows + r) * B + b] = st[at(S, src[r], b)];
+  buf[(ctr[0] * rows + _r) * B + _b] = st[at(S, src[_r], _b)];
 }
 
 __global__ void k_advance(int64_t* ctr) {
@@ -248,9 +250,13 @@ __global__ void k_set_ctr(int64_t* ctr, int64_t c0, int64_t c1) {
 }
 
 // feed [B][T][size] -> staging [T][feed_rows][B] rows [row0, row0+size)
+#define GRID_FLAT(n)                                                        \
+  const int64_t _i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;        \
+  if (_i >= (n)) return;
+
 __global__ void k_stage_feed(const float* src, int32_t B, int64_t T, int32_t size, float* stage,
                              int32_t feed_rows, int32_t row0) {
-  GRID_ITEM((int64_t)B * T * size);
+  GRID_FLAT((int64_t)B * T * size);
   const int64_t j = _i % size;
   const int64_t t = (_i / size) % T;
   const int64_t b = _i / (size * T);
@@ -260,7 +266,7 @@ __global__ void k_stage_feed(const float* src, int32_t B, int64_t T, int32_t siz
 // probe buffer [T][probe_rows][B] -> out [B][T][w] for rows [off, off+w)
 __global__ void k_probe_extract(const float* buf, int32_t B, int64_t T, int32_t probe_rows, int32_t off,
                                 int32_t w, float* out) {
-  GRID_ITEM((int64_t)B * T * w);
+  GRID_FLAT((int64_t)B * T * w);
   const int64_t j = _i % w;
   const int64_t t = (_i / w) % T;
   const int64_t b = _i / ((int64_t)w * T);
@@ -326,11 +332,12 @@ k_persistent(float* st, Strides S, int32_t B, const GroupDesc* groups, int32_t n
             elem_inc_item(st, S, r, b, G.dst, G.a_base, G.a, G.src_base, G.src, G.ptr);
           break;
         case ms::OP_DOT_INC: {
-          const int64_t total = rows * G.M;
+          const uint32_t total = (uint32_t)(rows * G.M);
+          const uint32_t M = (uint32_t)G.M;
           if (G.K >= 32) {
-            for (int64_t t = wave; t < total; t += nwaves) {
-              const int64_t op = t / G.M;
-              const int32_t m = (int32_t)(t % G.M);
+            for (uint32_t t = wave; t < total; t += nwaves) {
+              const uint32_t op = t / M;
+              const int32_t m = (int32_t)(t - op * M);
               const float* w = G.a_base + ((int64_t)G.w_row[op] + m) * G.K;
               const int64_t x0 = G.x_row[op];
               float acc = 0.0f;
@@ -339,8 +346,10 @@ k_persistent(float* st, Strides S, int32_t B, const GroupDesc* groups, int32_t n
               if (lane == 0) st[at(S, (int64_t)G.d_row[op] + m, b)] += acc;
             }
           } else {
-            for (int64_t t = tid; t < total; t += nt)
-              dot_row_item(st, S, t / G.M, (int32_t)(t % G.M), b, G.K, G.a_base, G.w_row, G.x_row, G.d_row);
+            for (uint32_t t = tid; t < total; t += nt) {
+              const uint32_t op = t / M;
+              dot_row_item(st, S, op, (int32_t)(t - op * M), b, G.K, G.a_base, G.w_row, G.x_row, G.d_row);
+            }
           }
           break;
         }

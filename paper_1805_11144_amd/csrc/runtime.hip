@@ -184,7 +184,7 @@ void setup_device(ms_sim* s) {
   }
   // ---- lowered groups -> pools
   PoolBuilder pb;
-  struct Offs { int64_t dst, src, a, V, ref, ptr, values, w, x, d, trc, tref, amp, ca, cb, feed; };
+  struct Offs { int64_t dst, src, a, V, ref, ptr, values, w, x, d, trc, tref, amp, ca, cb, feed, full; };
   std::vector<Offs> offs;
   for (const LGroup& g : p.lowered) {
     Offs o{};
@@ -194,6 +194,12 @@ void setup_device(ms_sim* s) {
     o.feed = pb.add_i(g.feed_rows);
     o.values = pb.add_f(g.values);
     o.trc = g.tau_rc.size() > 1 ? pb.add_f(g.tau_rc) : -1;
+    o.full = -1;
+    if (g.tau_rc.size() > 1) {
+      std::vector<float> full(g.tau_rc.size());
+      for (size_t k = 0; k < full.size(); ++k) full[k] = (float)std::expm1(-p.dt / (double)g.tau_rc[k]);
+      o.full = pb.add_f(full);
+    }
     o.tref = g.tau_ref.size() > 1 ? pb.add_f(g.tau_ref) : -1;
     o.amp = g.amp.size() > 1 ? pb.add_f(g.amp) : -1;
     o.ca = g.ca.size() > 1 ? pb.add_f(g.ca) : -1;
@@ -233,7 +239,9 @@ void setup_device(ms_sim* s) {
     l.feed_rows = ip(o.feed);
     if (g.type == OP_LIF || g.type == OP_LIF_RATE) {
       l.np.tau_rc = g.tau_rc[0]; l.np.tau_ref = g.tau_ref[0]; l.np.amp = g.amp[0];
+      l.np.full = (float)std::expm1(-p.dt / (double)g.tau_rc[0]);
       l.np.tau_rc_r = fp(o.trc); l.np.tau_ref_r = fp(o.tref); l.np.amp_r = fp(o.amp);
+      l.np.full_r = fp(o.full);
     }
     if (g.type == OP_LOWPASS) {
       l.fp.a = g.ca[0]; l.fp.b = g.cb[0];
@@ -255,6 +263,8 @@ inline unsigned grid_for(int64_t n) { return (unsigned)std::max<int64_t>(1, (n +
 
 void launch_group(ms_sim* s, const Launch& l) {
   const int32_t B = s->B;
+  if ((double)l.rows * (l.type == OP_DOT_INC ? l.M : 1) * B >= 4294967296.0)
+    fail(MS_E_INVALID, "merged group too large for 32-bit work-item indexing");
   float* st = s->state;
   const Strides S = s->S;
   hipStream_t q = s->stream;
