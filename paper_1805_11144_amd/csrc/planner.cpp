@@ -12,8 +12,10 @@
 //    weight shape (M, K); neuron and filter parameters become per-row arrays
 //  * candidates of one planning step: for each key, all ready operators with
 //    that key; a plan's value is the number of operators it schedules in n
-//    steps; ties prefer the larger first group, then the lower key id (key ids
-//    in order of first appearance in the operator list)
+//    steps, and among equal counts the plan that finishes in fewer steps (so
+//    an unbounded search returns a shortest plan); remaining ties prefer the
+//    larger first group, then the lower key id (key ids in order of first
+//    appearance in the operator list)
 //  * read blocks: signals read by one group in one operand slot; block size =
 //    total elements; ties go to the lower id.  Alg. 1 filters keep the previous
 //    candidate set if a filter would empty it, and fall back to the lowest
@@ -172,16 +174,29 @@ struct PlanSearch {
     ready[k].swap(L);
   }
 
-  int64_t best(int depth) {
-    if (depth <= 0) return 0;
-    int64_t v = 0;
+  // Best (operators scheduled, steps used) over all plans of at most `depth`
+  // steps from the current state: more operators first, then fewer steps
+  // (a plan that finishes everything early beats one that needs the horizon).
+  struct Val {
+    int64_t ops = 0, steps = 0;
+    bool better(const Val& o) const { return ops != o.ops ? ops > o.ops : steps < o.steps; }
+  };
+  Val best(int depth) {
+    Val v;
+    if (depth <= 0) return v;
     for (int32_t k = 0; k < (int32_t)ready.size(); ++k) {
       const int64_t sz = (int64_t)ready[k].size();
       if (!sz) continue;
-      if (depth == 1) { v = std::max(v, sz); continue; }
-      auto L = apply(k);
-      v = std::max(v, sz + best(depth - 1));
-      undo(k, L);
+      Val cand;
+      if (depth == 1) {
+        cand = Val{sz, 1};
+      } else {
+        auto L = apply(k);
+        Val rest = best(depth - 1);
+        undo(k, L);
+        cand = Val{sz + rest.ops, 1 + rest.steps};
+      }
+      if (cand.better(v) || v.steps == 0) v = cand;
     }
     return v;
   }
@@ -198,17 +213,19 @@ std::vector<std::vector<int32_t>> plan_groups(const IR& ir, const std::vector<in
   size_t done = 0;
   while (done < ir.ops.size()) {
     int32_t best_k = -1;
-    int64_t best_v = -1, best_sz = -1;
+    PlanSearch::Val best_v;
+    int64_t best_sz = -1;
     for (int32_t k = 0; k < n_keys; ++k) {
       const int64_t sz = (int64_t)ps.ready[k].size();
       if (!sz) continue;
-      int64_t v = sz;
+      PlanSearch::Val v{sz, 1};
       if (depth > 1) {
         auto L = ps.apply(k);
-        v += ps.best(depth - 1);
+        PlanSearch::Val rest = ps.best(depth - 1);
         ps.undo(k, L);
+        v = PlanSearch::Val{sz + rest.ops, 1 + rest.steps};
       }
-      if (v > best_v || (v == best_v && sz > best_sz)) {
+      if (best_k < 0 || v.better(best_v) || (!best_v.better(v) && sz > best_sz)) {
         best_v = v; best_sz = sz; best_k = k;
       }
     }

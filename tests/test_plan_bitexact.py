@@ -1,0 +1,58 @@
+"""The library's C++ planner against the independent reference planner: the
+exported plans (signal layout, merged groups, operator order, index arrays)
+must be identical."""
+import pytest
+
+import paper_1805_11144_amd as M
+from oracle import planner_ref as P
+from synth import make_workload
+
+CASES = {
+    "c1": dict(),
+    "c2": dict(n_steps=2, minibatch=1, n_neurons=20, n_eval=50),
+    "c3": dict(n_steps=2, minibatch=1, n_hidden=64, n_in=30),
+    "c4": dict(n_steps=2, minibatch=1, n_ens=12, n_neurons=30, n_eval=40),
+    "c5": dict(n_steps=2, n_ens=15, n_neurons=30, n_eval=40, n_input_targets=5, n_probed=4),
+}
+FLOAT_KEYS = {"values", "tau_rc", "tau_ref", "amp", "ca", "cb"}
+
+
+def _strip(plan):
+    plan = dict(plan)
+    plan["groups"] = [{k: v for k, v in g.items() if k not in FLOAT_KEYS} for g in plan["groups"]]
+    return plan
+
+
+OPTS = {
+    "tree3": (dict(), dict()),
+    "greedy": (dict(planner=M.PLANNER_GREEDY), dict(planner="greedy")),
+    "tree2_nosort": (dict(planner_depth=2, sort=False), dict(depth=2, sort=False)),
+    "nosimplify": (dict(simplify=False), dict(do_simplify=False)),
+    "nomerge": (dict(merge=False), dict(merge=False)),
+}
+
+
+@pytest.mark.parametrize("name", ["c1", "c2", "c3", "c4"])
+def test_full_size_plans_identical(name):
+    """Full benchmark-size models (default options)."""
+    w = make_workload(name)
+    got = _strip(M.Plan(M.model_from_spec(w.spec)).json())
+    exp = P.make_plan(w.spec)
+    assert got == {**exp, "groups": exp["groups"]}
+
+
+@pytest.mark.parametrize("opt", list(OPTS))
+@pytest.mark.parametrize("name", list(CASES))
+def test_plans_identical(name, opt):
+    w = make_workload(name, **CASES[name])
+    lib_opts, ref_opts = OPTS[opt]
+    got = _strip(M.Plan(M.model_from_spec(w.spec), **lib_opts).json())
+    exp = P.make_plan(w.spec, **ref_opts)
+    assert got["bases"] == exp["bases"]
+    assert got["signals"] == exp["signals"]
+    assert len(got["groups"]) == len(exp["groups"])
+    for g, e in zip(got["groups"], exp["groups"]):
+        assert g == e
+    assert got["probe_rows"] == exp["probe_rows"]
+    assert got["probe_offsets"] == exp["probe_offsets"]
+    assert got["feed_rows"] == exp["feed_rows"]
