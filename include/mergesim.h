@@ -157,6 +157,9 @@ typedef struct {
   int32_t merge;              /* 0: one operator per group (no merging) */
   int32_t sort;               /* 0: keep signals/operators in build order */
   int32_t simplify;           /* 0: skip simplification */
+  int32_t fuse;               /* 0: keep each ensemble's bias, encoder, neuron and
+                                 decoder operators separate (default 1: fuse them
+                                 into one operator per ensemble) */
   int32_t driver;             /* MS_DRIVER_* */
   int32_t device;             /* HIP device ordinal */
   void* stream;               /* hipStream_t to run on, NULL = library-owned */

@@ -32,9 +32,10 @@ from typing import Dict, List, Optional, Sequence, Tuple
 
 import numpy as np
 
-FEED, RESET, COPY, COPY_INC, ELEM_INC, DOT_INC, LIF, LIF_RATE, LOWPASS = range(9)
+FEED, RESET, COPY, COPY_INC, ELEM_INC, DOT_INC, LIF, LIF_RATE, LOWPASS, ENS = range(10)
 TYPE_NAMES = ["Feed", "Reset", "Copy", "CopyInc", "ElementwiseInc", "DotInc", "SimLIF",
-              "SimLIFRate", "Lowpass"]
+              "SimLIFRate", "Lowpass", "Ensemble"]
+MAX_FUSED_DECODED = 16
 
 
 @dataclass
@@ -65,6 +66,9 @@ class Op:
     ref: Optional[Ref] = None
     node: int = -1
     reset_value: Optional[np.ndarray] = None
+    bias: Optional[Ref] = None                 # fused ensemble: bias parameter
+    decs: list = field(default_factory=list)   # fused ensemble: [(D param, d output)]
+    lif: bool = True
 
 
 @dataclass
@@ -249,6 +253,83 @@ def simplify(ir: IR) -> None:
             o.type, o.src = RESET, None
 
 
+def fuse_ensembles(ir: IR) -> None:
+    """Replace each ensemble's bias, encoder, neuron and decoder operators by one
+    fused operator (an implementation choice for the GPU; the step computes the
+    same values).  Ensembles whose input current has other writers (neuron-space
+    connections) are left alone; decoders are fused only when their outputs
+    total at most MAX_FUSED_DECODED.  Spikes are kept only if something else
+    reads them."""
+    by_name = {o.name: k for k, o in enumerate(ir.ops)}
+    sig_by_name = {s.name: k for k, s in enumerate(ir.sigs)}
+    readers = {}
+    for o in ir.ops:
+        own_dec = o.type == DOT_INC and o.name.startswith("e") and ".dec" in o.name
+        if not own_dec:
+            for r in (o.src, o.a):
+                if r is not None:
+                    readers[r.sig] = readers.get(r.sig, 0) + 1
+    for r in ir.probes:
+        readers[r.sig] = readers.get(r.sig, 0) + 1
+    writers = {}
+    for o in ir.ops:
+        if o.dst is not None and o.type not in (LIF, LIF_RATE):
+            writers[o.dst.sig] = writers.get(o.dst.sig, 0) + 1
+    drop, fused = set(), {}
+    e = 0
+    while f"e{e}.bias" in by_name and f"e{e}.neurons" in by_name:
+        p = f"e{e}"
+        kb, kn = by_name[p + ".bias"], by_name[p + ".neurons"]
+        ke = by_name.get(p + ".enc")
+        neu = ir.ops[kn]
+        if writers.get(neu.src.sig, 0) == 1 + (ke is not None):
+            dec_ops = []
+            total = 0
+            for tag in ("id", "prod"):
+                if p + ".reset" + tag in by_name and p + ".dec" + tag in by_name:
+                    dec_ops.append((by_name[p + ".reset" + tag], by_name[p + ".dec" + tag]))
+                    total += ir.ops[by_name[p + ".dec" + tag]].dst.length
+            dec_ops.sort(key=lambda kk: kk[1])
+            fuse_dec = total <= MAX_FUSED_DECODED
+            f = Op(ENS, p + ".ens", V=neu.V, ref=neu.ref, lif=neu.type == LIF,
+                   bias=Ref(sig_by_name[p + ".bias"], 0, neu.src.length))
+            if ke is not None:
+                f.src, f.a = ir.ops[ke].src, ir.ops[ke].a
+            if fuse_dec:
+                f.decs = [(ir.ops[kd].a, ir.ops[kd].dst) for _, kd in dec_ops]
+            if readers.get(neu.dst.sig, 0) > 0 or not fuse_dec:
+                f.dst = neu.dst
+            drop |= {kb, kn} | ({ke} if ke is not None else set())
+            if fuse_dec:
+                drop |= {k for pair in dec_ops for k in pair}
+            fused[kb] = f
+        e += 1
+    if not fused:
+        return
+    ir.ops = [fused[k] if k in fused else o for k, o in enumerate(ir.ops)
+              if k in fused or k not in drop]
+    used = set()
+    for o in ir.ops:
+        for r in (o.dst, o.src, o.a, o.V, o.ref, o.bias):
+            if r is not None:
+                used.add(r.sig)
+        for D, d in o.decs:
+            used |= {D.sig, d.sig}
+    used |= {r.sig for r in ir.probes}
+    remap = {}
+    sigs = []
+    for k, sg in enumerate(ir.sigs):
+        if k in used:
+            remap[k] = len(sigs)
+            sigs.append(sg)
+    ir.sigs = sigs
+    rm = lambda r: None if r is None else Ref(remap[r.sig], r.start, r.length)
+    for o in ir.ops:
+        o.dst, o.src, o.a, o.V, o.ref, o.bias = map(rm, (o.dst, o.src, o.a, o.V, o.ref, o.bias))
+        o.decs = [(rm(D), rm(d)) for D, d in o.decs]
+    ir.probes = [rm(r) for r in ir.probes]
+
+
 # ------------------------------------------------------------- dependencies
 def accesses(o: Op):
     """(sets, incs, reads, updates) signal ids of an operator."""
@@ -267,6 +348,11 @@ def accesses(o: Op):
         return [o.dst.sig], [], [o.src.sig], []
     if t == LOWPASS:
         return [], [], [o.src.sig], [o.dst.sig]
+    if t == ENS:
+        sets = ([o.dst.sig] if o.dst is not None else []) + [d.sig for _, d in o.decs]
+        reads = [o.src.sig] if o.src is not None else []
+        upds = [o.V.sig, o.ref.sig] if o.V is not None else []
+        return sets, [], reads, upds
     raise ValueError(t)
 
 
@@ -311,6 +397,13 @@ def merge_key(ir: IR, o: Op):
         return (t, b(o.src), b(o.dst), b(o.V), b(o.ref))
     if t == LIF_RATE:
         return (t, b(o.src), b(o.dst))
+    if t == ENS:
+        bb = lambda r: -1 if r is None else ir.sigs[r.sig].base
+        key = (t, 0 if o.lif else 1, bb(o.src), bb(o.a), 0 if o.src is None else o.src.length,
+               bb(o.bias), bb(o.dst), bb(o.V), bb(o.ref))
+        for D, d in o.decs:
+            key += (bb(D), d.length, bb(d))
+        return key
     return (t, b(o.dst), b(o.src))
 
 
@@ -402,6 +495,10 @@ def read_refs(o: Op) -> List[Ref]:
         return [o.src]
     if t == LOWPASS:
         return [o.src, o.dst]
+    if t == ENS:
+        refs = ([o.src, o.a] if o.src is not None else []) + [o.bias]
+        refs += [o.V, o.ref] if o.V is not None else []
+        return refs + [D for D, _ in o.decs]
     return []
 
 
@@ -600,6 +697,19 @@ def lower_group(ir: IR, offset: Dict[int, int], g: List[int]) -> dict:
         out.update(rows=len(J), dst=_operand(base(o0.dst), S), src=_operand(base(o0.src), J))
         if t == LIF:
             out.update(V=_operand(base(o0.V), V), ref=_operand(base(o0.ref), R))
+    elif t == ENS:
+        ops = [ir.ops[oi] for oi in g]
+        rr = lambda r: -1 if r is None else row(r, 0)
+        bb = lambda r: -1 if r is None else ir.sigs[r.sig].base
+        out.update(rows=len(g), d=0 if o0.src is None else o0.src.length, neuron=0 if o0.lif else 1,
+                   enc_base=bb(o0.a), bias_base=bb(o0.bias), D_base=[bb(D) for D, _ in o0.decs],
+                   n=[o.bias.length for o in ops], x_row=[rr(o.src) for o in ops],
+                   enc_row=[-1 if o.a is None else offset[o.a.sig] for o in ops],
+                   bias_row=[rr(o.bias) for o in ops], V_row=[rr(o.V) for o in ops],
+                   ref_row=[rr(o.ref) for o in ops], s_row=[rr(o.dst) for o in ops],
+                   df=[d.length for _, d in o0.decs],
+                   D_row=[[offset[o.decs[k][0].sig] for o in ops] for k in range(len(o0.decs))],
+                   d_row=[[row(o.decs[k][1], 0) for o in ops] for k in range(len(o0.decs))])
     elif t == LOWPASS:
         y, v = [], []
         for oi in g:
@@ -610,12 +720,15 @@ def lower_group(ir: IR, offset: Dict[int, int], g: List[int]) -> dict:
     return out
 
 
-def make_plan(spec, planner="tree", depth=3, merge=True, sort=True, do_simplify=True) -> dict:
+def make_plan(spec, planner="tree", depth=3, merge=True, sort=True, do_simplify=True,
+              fuse=True) -> dict:
     """The whole pipeline; returns a dict shaped like the library's JSON export
     (without parameter values)."""
     ir = build_ir(spec)
     if do_simplify:
         simplify(ir)
+    if fuse:
+        fuse_ensembles(ir)
     key_ids: Dict[tuple, int] = {}
     keys = []
     for k, o in enumerate(ir.ops):

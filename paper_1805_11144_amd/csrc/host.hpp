@@ -100,8 +100,13 @@ enum OpType : int32_t {
   OP_LIF = 6,
   OP_LIF_RATE = 7,
   OP_LOWPASS = 8,
-  OP_NTYPES = 9
+  OP_ENS = 9,           // fused ensemble: J = bias + enc x; LIF; d_f = D_f s
+  OP_NTYPES = 10
 };
+
+// Fused decoders of one ensemble operator are limited to this many outputs in
+// total (they are accumulated in registers); larger ones stay separate.
+constexpr int32_t kMaxFusedDecoded = 16;
 const char* op_type_name(int32_t t);
 
 // A reference to rows [start, start+len) of a signal.
@@ -120,6 +125,10 @@ struct Op {
   SRef V, ref;         // LIF state
   int32_t node = -1;   // FEED: node id
   std::vector<double> reset_value;  // RESET: [dst.len] (empty = zeros)
+  SRef bias;                        // ENS: bias parameter [n]
+  std::vector<std::pair<SRef, SRef>> decs;  // ENS: (decoder param [d_f x n], output d_f)
+  int32_t ntype = 0;                // ENS: MS_NEURON_*
+  int32_t n = 0;                    // ENS: neurons
   double tau_rc = 0, tau_ref = 0, amp = 0;  // LIF params
   double coef_a = 0, coef_b = 0;            // LOWPASS y = coef_a y + coef_b v
 };
@@ -149,12 +158,13 @@ struct IR {
 };
 IR build_ir(const Model& m, const Built& b, double dt);
 void simplify_ir(IR& ir);
+void fuse_ensembles(IR& ir);
 
 // ------------------------------------------------------------------- plan
 struct PlanOpts {
   int32_t planner = MS_PLANNER_TREE;
   int32_t depth = 3;
-  bool merge = true, sort = true, simplify = true;
+  bool merge = true, sort = true, simplify = true, fuse = true;
 };
 
 // One operand of a lowered group: rows in its base array, either a contiguous
@@ -186,6 +196,14 @@ struct LGroup {
   std::vector<float> ca, cb;
   // FEED: staging rows per destination row
   std::vector<int32_t> feed_rows;
+  // ENS: per-op rows (x_row -1 when the ensemble has no decoded input, s_row -1
+  // when the spikes are not stored); decoder rows per fused function
+  int32_t ens_d = 0, ens_type = 0;
+  std::vector<int32_t> ens_n, ens_x, ens_enc, ens_bias, ens_V, ens_ref, ens_s;
+  std::vector<int32_t> ens_df;                       // per function
+  std::vector<std::vector<int32_t>> ens_D, ens_dd;   // [function][op]
+  std::vector<int32_t> ens_Dbase;                    // per function
+  int32_t ens_bias_base = -1;
 };
 
 struct Plan {

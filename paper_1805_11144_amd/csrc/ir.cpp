@@ -377,4 +377,108 @@ void simplify_ir(IR& ir) {
   }
 }
 
+// Fuse each ensemble's bias reset, encoder DotInc, neuron update and (when
+// small enough) its decoder resets and DotIncs into one ENS operator, so the
+// input current and, when nothing else reads them, the spikes never reach
+// memory.  Ensembles with neuron-space inputs keep their separate operators.
+// The fused operator takes the place of the ensemble's bias operator; signals
+// no operator or probe uses any more are dropped (order otherwise kept).
+void fuse_ensembles(IR& ir) {
+  std::map<std::string, int32_t> op_index;
+  for (int32_t k = 0; k < (int32_t)ir.ops.size(); ++k) op_index[ir.ops[k].name] = k;
+  auto find = [&](const std::string& n) -> int32_t {
+    auto it = op_index.find(n);
+    return it == op_index.end() ? -1 : it->second;
+  };
+  // readers of each signal other than decoder DotIncs of its own ensemble
+  std::vector<int32_t> other_readers(ir.sigs.size(), 0);
+  for (const Op& o : ir.ops) {
+    const bool own_dec = o.type == OP_DOT_INC && o.name.size() > 4 &&
+                         o.name.find(".dec") != std::string::npos && o.name[0] == 'e';
+    if (!own_dec) {
+      if (o.src.sig >= 0) other_readers[o.src.sig]++;
+      if (o.a.sig >= 0) other_readers[o.a.sig]++;
+    }
+  }
+  for (const auto& p : ir.probes) other_readers[p.src.sig]++;
+  std::vector<int32_t> writers(ir.sigs.size(), 0);
+  for (const Op& o : ir.ops)
+    if (o.dst.sig >= 0 && o.type != OP_LIF && o.type != OP_LIF_RATE) writers[o.dst.sig]++;
+  std::map<std::string, int32_t> sig_index;
+  for (int32_t k = 0; k < (int32_t)ir.sigs.size(); ++k) sig_index[ir.sigs[k].name] = k;
+  std::vector<char> drop(ir.ops.size(), 0);
+  std::vector<std::pair<int32_t, Op>> fused;   // (position, op)
+  for (int32_t e = 0;; ++e) {
+    const std::string p = "e" + std::to_string(e);
+    const int32_t kb = find(p + ".bias"), kn = find(p + ".neurons");
+    if (kb < 0 || kn < 0) break;
+    const Op& nop = ir.ops[kn];
+    const int32_t J = nop.src.sig;
+    // J must be written only by the bias op and the encoder op
+    const int32_t ke = find(p + ".enc");
+    if (writers[J] != 1 + (ke >= 0 ? 1 : 0)) continue;
+    Op f;
+    f.type = OP_ENS;
+    f.name = p + ".ens";
+    f.ntype = nop.type == OP_LIF ? MS_NEURON_LIF : MS_NEURON_LIF_RATE;
+    f.n = nop.src.len;
+    f.tau_rc = nop.tau_rc; f.tau_ref = nop.tau_ref; f.amp = nop.amp;
+    f.V = nop.V; f.ref = nop.ref;
+    f.bias = SRef{sig_index.at(p + ".bias"), 0, f.n};
+    if (ke >= 0) { f.src = ir.ops[ke].src; f.a = ir.ops[ke].a; }
+    // decoders
+    std::vector<int32_t> dec_ops;
+    int32_t total = 0;
+    for (const char* tag : {"id", "prod"}) {
+      const int32_t kr = find(p + ".reset" + tag), kd = find(p + ".dec" + tag);
+      if (kr >= 0 && kd >= 0) { dec_ops.push_back(kr); dec_ops.push_back(kd); total += ir.ops[kd].dst.len; }
+    }
+    // keep the function order of first use (operator order)
+    std::vector<int32_t> dec_pairs;
+    for (size_t k = 0; k + 1 < dec_ops.size(); k += 2) dec_pairs.push_back(dec_ops[k + 1]);
+    std::sort(dec_pairs.begin(), dec_pairs.end());
+    const bool fuse_dec = total <= kMaxFusedDecoded;
+    if (fuse_dec)
+      for (int32_t kd : dec_pairs) f.decs.push_back({ir.ops[kd].a, ir.ops[kd].dst});
+    // spikes stored only if something besides fused decoders reads them
+    const int32_t S = nop.dst.sig;
+    const bool s_needed = other_readers[S] > 0 || !fuse_dec;
+    if (s_needed) f.dst = nop.dst;
+    drop[kb] = 1; drop[kn] = 1;
+    if (ke >= 0) drop[ke] = 1;
+    if (fuse_dec)
+      for (int32_t k : dec_ops) drop[k] = 1;
+    fused.push_back({kb, f});
+  }
+  if (fused.empty()) return;
+  std::vector<Op> ops;
+  size_t fi = 0;
+  for (int32_t k = 0; k < (int32_t)ir.ops.size(); ++k) {
+    if (fi < fused.size() && fused[fi].first == k) { ops.push_back(fused[fi].second); ++fi; continue; }
+    if (!drop[k]) ops.push_back(ir.ops[k]);
+  }
+  ir.ops.swap(ops);
+  // drop signals nothing references any more
+  std::vector<char> used(ir.sigs.size(), 0);
+  auto mark = [&](const SRef& r) { if (r.sig >= 0) used[r.sig] = 1; };
+  for (const Op& o : ir.ops) {
+    mark(o.dst); mark(o.src); mark(o.a); mark(o.V); mark(o.ref); mark(o.bias);
+    for (const auto& d : o.decs) { mark(d.first); mark(d.second); }
+  }
+  for (const auto& p : ir.probes) mark(p.src);
+  std::vector<int32_t> remap(ir.sigs.size(), -1);
+  std::vector<Signal> sigs;
+  for (size_t s = 0; s < ir.sigs.size(); ++s)
+    if (used[s]) { remap[s] = (int32_t)sigs.size(); sigs.push_back(std::move(ir.sigs[s])); }
+  ir.sigs.swap(sigs);
+  auto rm = [&](SRef& r) { if (r.sig >= 0) r.sig = remap[r.sig]; };
+  for (Op& o : ir.ops) {
+    rm(o.dst); rm(o.src); rm(o.a); rm(o.V); rm(o.ref); rm(o.bias);
+    for (auto& d : o.decs) { rm(d.first); rm(d.second); }
+  }
+  for (auto& p : ir.probes) rm(p.src);
+  for (auto* v : {&ir.ens_V, &ir.ens_ref, &ir.conn_y, &ir.probe_y})
+    for (int32_t& x : *v) if (x >= 0) x = remap[x];
+}
+
 }  // namespace ms

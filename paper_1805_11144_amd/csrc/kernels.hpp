@@ -14,6 +14,16 @@
 
 #include <cstdint>
 
+// Pointers read out of device-resident descriptors are generic pointers to the
+// compiler; casting them back to the global address space turns flat memory
+// instructions (which also wait on LDS traffic) into global loads.
+template <class T>
+using gptr = const __attribute__((address_space(1))) T*;
+template <class T>
+__device__ __forceinline__ gptr<T> G(const T* p) {
+  return (gptr<T>)p;
+}
+
 // Row of the r-th work item of an operand: slice start + r, or idx[r].
 struct Opnd {
   const int32_t* idx;
@@ -21,7 +31,7 @@ struct Opnd {
 };
 
 __device__ __forceinline__ int64_t rowof(const Opnd& o, int64_t r) {
-  return o.idx ? (int64_t)o.idx[r] : o.start + r;
+  return o.idx ? (int64_t)G(o.idx)[r] : o.start + r;
 }
 
 struct NeuronParams {
@@ -47,37 +57,20 @@ __device__ __forceinline__ int64_t at(const Strides& s, int64_t r, int64_t b) {
 // --------------------------------------------------------- per-item bodies
 // Each body computes one (row, batch) work item of a merged group.
 
+__device__ __forceinline__ float neuron_update(int ntype, float j, float& v, float& rf, float tau_rc,
+                                               float tau_ref, float amp, float full, float dt,
+                                               float inv_tau);
+
 __device__ __forceinline__ void lif_item(float* st, const Strides& S, int64_t r, int64_t b,
                                          const Opnd& J, const Opnd& s, const Opnd& V, const Opnd& R,
                                          const NeuronParams& np, float dt) {
-  const float tau_rc = np.tau_rc_r ? np.tau_rc_r[r] : np.tau_rc;
-  const float tau_ref = np.tau_ref_r ? np.tau_ref_r[r] : np.tau_ref;
-  const float amp = np.amp_r ? np.amp_r[r] : np.amp;
+  const float tau_rc = np.tau_rc_r ? G(np.tau_rc_r)[r] : np.tau_rc;
+  const float tau_ref = np.tau_ref_r ? G(np.tau_ref_r)[r] : np.tau_ref;
+  const float amp = np.amp_r ? G(np.amp_r)[r] : np.amp;
+  const float full = np.full_r ? G(np.full_r)[r] : np.full;
   const int64_t jv = at(S, rowof(J, r), b), vv = at(S, rowof(V, r), b), rv = at(S, rowof(R, r), b);
-  const float j = st[jv];
-  float v = st[vv];
-  float rf = st[rv];
-  // integrate exactly over the non-refractory part of the step; a neuron that
-  // is not refractory integrates the whole step with the precomputed factor
-  const float integ = fminf(fmaxf(dt - rf, 0.0f), dt);
-  const float e = rf <= 0.0f ? (np.full_r ? np.full_r[r] : np.full) : expm1f(-integ / tau_rc);
-  v = v - (j - v) * e;
-  rf = fmaxf(rf - dt, 0.0f);
-  float out = 0.0f;
-  if (v > 1.0f) {
-    // time since the threshold crossing, from the overshoot
-    float since = 0.0f;
-    const float drive = j - 1.0f;
-    if (drive > 0.0f) {
-      const float q = (v - 1.0f) / drive;
-      since = q >= 1.0f ? integ : fminf(-tau_rc * log1pf(-q), integ);
-    }
-    v = 0.0f;
-    rf = tau_ref - since;
-    out = amp / dt;
-  } else {
-    v = fmaxf(v, 0.0f);
-  }
+  float v = st[vv], rf = st[rv];
+  const float out = neuron_update(0, st[jv], v, rf, tau_rc, tau_ref, amp, full, dt, 1.0f / tau_rc);
   st[vv] = v;
   st[rv] = rf;
   st[at(S, rowof(s, r), b)] = out;
@@ -85,9 +78,9 @@ __device__ __forceinline__ void lif_item(float* st, const Strides& S, int64_t r,
 
 __device__ __forceinline__ void lif_rate_item(float* st, const Strides& S, int64_t r, int64_t b,
                                               const Opnd& J, const Opnd& s, const NeuronParams& np) {
-  const float tau_rc = np.tau_rc_r ? np.tau_rc_r[r] : np.tau_rc;
-  const float tau_ref = np.tau_ref_r ? np.tau_ref_r[r] : np.tau_ref;
-  const float amp = np.amp_r ? np.amp_r[r] : np.amp;
+  const float tau_rc = np.tau_rc_r ? G(np.tau_rc_r)[r] : np.tau_rc;
+  const float tau_ref = np.tau_ref_r ? G(np.tau_ref_r)[r] : np.tau_ref;
+  const float amp = np.amp_r ? G(np.amp_r)[r] : np.amp;
   const float j = st[at(S, rowof(J, r), b)];
   float out = 0.0f;
   if (j > 1.0f) out = amp / (tau_ref + tau_rc * log1pf(1.0f / (j - 1.0f)));
@@ -96,15 +89,15 @@ __device__ __forceinline__ void lif_rate_item(float* st, const Strides& S, int64
 
 __device__ __forceinline__ void lowpass_item(float* st, const Strides& S, int64_t r, int64_t b,
                                              const Opnd& y, const Opnd& v, const FilterParams& fp) {
-  const float a = fp.a_r ? fp.a_r[r] : fp.a;
-  const float c = fp.b_r ? fp.b_r[r] : fp.b;
+  const float a = fp.a_r ? G(fp.a_r)[r] : fp.a;
+  const float c = fp.b_r ? G(fp.b_r)[r] : fp.b;
   const int64_t yi = at(S, rowof(y, r), b);
   st[yi] = a * st[yi] + c * st[at(S, rowof(v, r), b)];
 }
 
 __device__ __forceinline__ float src_val(const float* base, const Strides& S, int bcast, int64_t row,
                                          int64_t b) {
-  return bcast ? base[row] : base[at(S, row, b)];
+  return bcast ? G(base)[row] : base[at(S, row, b)];
 }
 
 // dst (+)= sum of src entries of unique destination u (ptr == null: one entry)
@@ -114,7 +107,7 @@ __device__ __forceinline__ void copy_inc_item(float* st, const Strides& S, int64
   const int64_t di = at(S, rowof(dst, u), b);
   float acc = st[di];
   if (ptr) {
-    for (int32_t e = ptr[u]; e < ptr[u + 1]; ++e) acc += src_val(src_base, S, bcast, rowof(src, e), b);
+    for (int32_t e = G(ptr)[u]; e < G(ptr)[u + 1]; ++e) acc += src_val(src_base, S, bcast, rowof(src, e), b);
   } else {
     acc += src_val(src_base, S, bcast, rowof(src, u), b);
   }
@@ -127,9 +120,9 @@ __device__ __forceinline__ void elem_inc_item(float* st, const Strides& S, int64
   const int64_t di = at(S, rowof(dst, u), b);
   float acc = st[di];
   if (ptr) {
-    for (int32_t e = ptr[u]; e < ptr[u + 1]; ++e) acc += a_base[rowof(a, e)] * x_base[at(S, rowof(x, e), b)];
+    for (int32_t e = G(ptr)[u]; e < G(ptr)[u + 1]; ++e) acc += G(a_base)[rowof(a, e)] * x_base[at(S, rowof(x, e), b)];
   } else {
-    acc += a_base[rowof(a, u)] * x_base[at(S, rowof(x, u), b)];
+    acc += G(a_base)[rowof(a, u)] * x_base[at(S, rowof(x, u), b)];
   }
   st[di] = acc;
 }
@@ -138,11 +131,177 @@ __device__ __forceinline__ void elem_inc_item(float* st, const Strides& S, int64
 __device__ __forceinline__ void dot_row_item(float* st, const Strides& S, int64_t op, int32_t m, int64_t b,
                                              int32_t K, const float* W, const int32_t* w_row,
                                              const int32_t* x_row, const int32_t* d_row) {
-  const float* w = W + ((int64_t)w_row[op] + m) * K;
-  const int64_t x0 = x_row[op];
+  gptr<float> w = G(W) + ((int64_t)G(w_row)[op] + m) * K;
+  const int64_t x0 = G(x_row)[op];
   float acc = 0.0f;
   for (int32_t k = 0; k < K; ++k) acc += w[k] * st[at(S, x0 + k, b)];
-  st[at(S, (int64_t)d_row[op] + m, b)] += acc;
+  st[at(S, (int64_t)G(d_row)[op] + m, b)] += acc;
+}
+
+// ------------------------------------------------------ fused ensemble ops
+// One merged group of fused ensemble operators.  Per op: n neurons, rows of its
+// represented input x (d rows, -1: none), gain-scaled encoders (row of the
+// [n x d] block in the encoder base), bias, state V / refractory, spikes (-1:
+// not stored) and, per fused function f, the decoder block [df[f] x n] and the
+// output rows.  Neuron parameters are uniform or per op.
+constexpr int kMaxFns = 2;
+constexpr int kMaxDec = 16;   // total decoded outputs of one fused op
+
+// Rows of one fused op, packed so a wavefront fetches them with one scalar load.
+struct EnsOp {
+  int32_t n, x, enc, bias, V, ref, s;
+  float inv_tau;                      // 1 / tau_rc
+  int32_t D[kMaxFns], d[kMaxFns];
+  float tau_rc, tau_ref, amp, full;   // neuron parameters of this op
+};
+
+struct EnsDesc {
+  int32_t d, ntype, nf, ndec;
+  int32_t df[kMaxFns];
+  const EnsOp* ops;
+  const float* enc;      // encoder base [rows][d]
+  const float* bias;     // bias base (vector)
+  const float* D[kMaxFns];  // decoder bases [rows][n]
+  int32_t Dcols[kMaxFns];   // row stride of each decoder base
+};
+
+// exp(x) - 1 for -1/16 <= x <= 0 (the partial-step integration factor):
+// degree-6 Taylor polynomial, truncation error below 1e-11 relative.
+__device__ __forceinline__ float expm1_small(float x) {
+  float p = 1.0f / 720.0f;
+  p = fmaf(p, x, 1.0f / 120.0f);
+  p = fmaf(p, x, 1.0f / 24.0f);
+  p = fmaf(p, x, 1.0f / 6.0f);
+  p = fmaf(p, x, 0.5f);
+  p = fmaf(p, x, 1.0f);
+  return p * x;
+}
+
+// LIF (or rate) update of one neuron for input current j; V, rf updated in place.
+// Spiking: exact integration over the non-refractory part of the step (the
+// whole-step factor `full` = expm1(-dt/tau_rc) is precomputed; a partial step
+// uses the polynomial above or expm1f), strict threshold 1, crossing time from
+// the overshoot (ln via the hardware logarithm: its error, about 1e-9 s, is
+// below the float32 resolution of the state), reset to 0, refractory period
+// measured from the crossing.  Rate: amplitude / (tau_ref + tau_rc log1p(1/(J-1))).
+__device__ __forceinline__ float neuron_update(int ntype, float j, float& v, float& rf, float tau_rc,
+                                               float tau_ref, float amp, float full, float dt,
+                                               float inv_tau) {
+  if (ntype != 0) {
+    return j > 1.0f ? amp / (tau_ref + tau_rc * log1pf(1.0f / (j - 1.0f))) : 0.0f;
+  }
+  const float integ = fminf(fmaxf(dt - rf, 0.0f), dt);
+  float e = full;
+  if (rf > 0.0f) {
+    const float x = -integ * inv_tau;
+    e = x >= -0.0625f ? expm1_small(x) : expm1f(x);
+  }
+  v = v - (j - v) * e;
+  rf = fmaxf(rf - dt, 0.0f);
+  if (v > 1.0f) {
+    float since = 0.0f;
+    const float drive = j - 1.0f;
+    if (drive > 0.0f) {
+      const float q = __fdividef(v - 1.0f, drive);
+      since = q >= 1.0f ? integ : fminf(-tau_rc * __logf(1.0f - q), integ);
+    }
+    v = 0.0f;
+    rf = tau_ref - since;
+    return amp / dt;
+  }
+  v = fmaxf(v, 0.0f);
+  return 0.0f;
+}
+
+// Sum over the 64 lanes of a wavefront, returned in every lane.  DPP moves
+// fold quads, half-rows and rows of 16 lanes; the four row sums are read with
+// readlane.  All lanes must be active.
+__device__ __forceinline__ float wave_sum(float x) {
+  int xi = __builtin_bit_cast(int, x);
+  x += __builtin_bit_cast(float, __builtin_amdgcn_mov_dpp(xi, 0xB1, 0xF, 0xF, true));   // quad [1,0,3,2]
+  xi = __builtin_bit_cast(int, x);
+  x += __builtin_bit_cast(float, __builtin_amdgcn_mov_dpp(xi, 0x4E, 0xF, 0xF, true));   // quad [2,3,0,1]
+  xi = __builtin_bit_cast(int, x);
+  x += __builtin_bit_cast(float, __builtin_amdgcn_mov_dpp(xi, 0x141, 0xF, 0xF, true));  // row_half_mirror
+  xi = __builtin_bit_cast(int, x);
+  x += __builtin_bit_cast(float, __builtin_amdgcn_mov_dpp(xi, 0x140, 0xF, 0xF, true));  // row_mirror
+  xi = __builtin_bit_cast(int, x);
+  return __builtin_bit_cast(float, __builtin_amdgcn_readlane(xi, 0)) +
+         __builtin_bit_cast(float, __builtin_amdgcn_readlane(xi, 16)) +
+         __builtin_bit_cast(float, __builtin_amdgcn_readlane(xi, 32)) +
+         __builtin_bit_cast(float, __builtin_amdgcn_readlane(xi, 48));
+}
+
+__device__ __forceinline__ EnsOp load_op(const EnsOp* ops, int op) {
+  gptr<int32_t> w = G(reinterpret_cast<const int32_t*>(ops + op));
+  EnsOp o;
+  o.n = w[0]; o.x = w[1]; o.enc = w[2]; o.bias = w[3]; o.V = w[4]; o.ref = w[5]; o.s = w[6];
+  o.inv_tau = __builtin_bit_cast(float, w[7]);
+  o.D[0] = w[8]; o.D[1] = w[9]; o.d[0] = w[10]; o.d[1] = w[11];
+  o.tau_rc = __builtin_bit_cast(float, w[12]);
+  o.tau_ref = __builtin_bit_cast(float, w[13]);
+  o.amp = __builtin_bit_cast(float, w[14]);
+  o.full = __builtin_bit_cast(float, w[15]);
+  return o;
+}
+
+// Decoded-output bucket: the smallest of 0, 1, 2, 4, 8, 16 that holds n outputs.
+__host__ __device__ __forceinline__ int dec_bucket(int n) {
+  return n <= 0 ? 0 : n <= 1 ? 1 : n <= 2 ? 2 : n <= 4 ? 4 : n <= 8 ? 8 : 16;
+}
+
+// One fused op, one batch column, processed by one wavefront (lanes over
+// neurons); NDEC >= total decoded outputs (extra slots repeat the last row and
+// are never stored).  The decoded outputs are reduced across the wavefront
+// and written by lane 0.  V/refractory/x/s/d live in `st` (strides S, column b).
+template <int NDEC>
+__device__ __forceinline__ void ens_op_wave_t(float* st, const Strides& S, int64_t b, const EnsDesc& E,
+                                              const EnsOp& o, int lane, float dt) {
+  const int d = E.d, ndec = E.ndec, df0 = E.df[0];
+  gptr<float> enc = G(E.enc) + (int64_t)o.enc * d;
+  gptr<float> bias = G(E.bias) + o.bias;
+  gptr<float> D0 = G(E.D[0]) + (int64_t)o.D[0] * E.Dcols[0];
+  gptr<float> D1 = G(E.D[E.nf > 1 ? 1 : 0]) + (int64_t)o.D[E.nf > 1 ? 1 : 0] * E.Dcols[E.nf > 1 ? 1 : 0];
+  const int64_t s0 = E.Dcols[0], s1 = E.Dcols[E.nf > 1 ? 1 : 0];
+  float acc[NDEC > 0 ? NDEC : 1];
+#pragma unroll
+  for (int q = 0; q < NDEC; ++q) acc[q] = 0.0f;
+  for (int r = lane; r < o.n; r += 64) {
+    float j = bias[r];
+    for (int k = 0; k < d; ++k) j += enc[(int64_t)r * d + k] * st[at(S, o.x + k, b)];
+    float v = 0.0f, rf = 0.0f;
+    if (E.ntype == 0) { v = st[at(S, o.V + r, b)]; rf = st[at(S, o.ref + r, b)]; }
+    const float sp = neuron_update(E.ntype, j, v, rf, o.tau_rc, o.tau_ref, o.amp, o.full, dt, o.inv_tau);
+    if (E.ntype == 0) { st[at(S, o.V + r, b)] = v; st[at(S, o.ref + r, b)] = rf; }
+    if (o.s >= 0) st[at(S, o.s + r, b)] = sp;
+#pragma unroll
+    for (int q = 0; q < NDEC; ++q) {
+      const int qq = q < ndec ? q : ndec - 1;
+      gptr<float> row = qq < df0 ? D0 + (int64_t)qq * s0 : D1 + (int64_t)(qq - df0) * s1;
+      acc[q] += row[r] * sp;
+    }
+  }
+#pragma unroll
+  for (int q = 0; q < NDEC; ++q) {
+    const float t = wave_sum(acc[q]);
+    if (lane == 0 && q < ndec) {
+      const int dr = q < df0 ? o.d[0] + q : o.d[1] + (q - df0);
+      st[at(S, dr, b)] = t;
+    }
+  }
+}
+
+__device__ __forceinline__ void ens_op_wave(float* st, const Strides& S, int64_t b, const EnsDesc& E, int op,
+                                            int lane, float dt) {
+  const EnsOp o = load_op(E.ops, op);
+  switch (dec_bucket(E.ndec)) {
+    case 0: ens_op_wave_t<0>(st, S, b, E, o, lane, dt); break;
+    case 1: ens_op_wave_t<1>(st, S, b, E, o, lane, dt); break;
+    case 2: ens_op_wave_t<2>(st, S, b, E, o, lane, dt); break;
+    case 4: ens_op_wave_t<4>(st, S, b, E, o, lane, dt); break;
+    case 8: ens_op_wave_t<8>(st, S, b, E, o, lane, dt); break;
+    default: ens_op_wave_t<16>(st, S, b, E, o, lane, dt); break;
+  }
 }
 
 // ----------------------------------------------------------- launch kernels
@@ -220,6 +379,87 @@ __global__ void k_lowpass(float* st, Strides S, int32_t B, int64_t rows, Opnd y,
   lowpass_item(st, S, _r, _b, y, v, fp);
 }
 
+// Fused ensembles, small minibatch: one workgroup per op; each wavefront takes
+// batch columns in turn (lanes over neurons).
+__global__ void __launch_bounds__(256) k_ens_rows(float* st, Strides S, int32_t B, EnsDesc E, float dt) {
+  const int op = blockIdx.x;
+  const int lane = threadIdx.x % 64, wave = threadIdx.x / 64, nw = blockDim.x / 64;
+  for (int64_t b = wave; b < B; b += nw) ens_op_wave(st, S, b, E, op, lane, dt);
+}
+
+// Fused ensembles, one wavefront per (op, batch column); for mid-size batches
+// and single-column ops with many neurons the grid covers ops x B wavefronts.
+__global__ void __launch_bounds__(256) k_ens_waves(float* st, Strides S, int32_t B, int32_t nops, EnsDesc E,
+                                                   float dt) {
+  const int64_t w = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) / 64;
+  const int lane = threadIdx.x % 64;
+  if (w >= (int64_t)nops * B) return;
+  ens_op_wave(st, S, w % B, E, (int)(w / B), lane, dt);
+}
+
+// Fused ensembles, large minibatch: one workgroup (4 wavefronts) per (op, tile
+// of 64 batch columns); lanes are batch columns, wavefronts split the neurons;
+// encoder and decoder weights are wavefront-uniform loads; decoded partial
+// sums are combined across wavefronts in LDS.
+template <int NDEC>
+__device__ __forceinline__ void ens_tile_t(float* st, const Strides& S, int32_t B, const EnsDesc& E, float dt,
+                                           float (*red)[kMaxDec][64]) {
+  const int op = blockIdx.x;
+  const int lane = threadIdx.x % 64, wave = threadIdx.x / 64;
+  const int64_t b = (int64_t)blockIdx.y * 64 + lane;
+  const bool live = b < B;
+  const EnsOp o = load_op(E.ops, op);
+  const int d = E.d, ndec = E.ndec, df0 = E.df[0];
+  gptr<float> enc = G(E.enc) + (int64_t)o.enc * d;
+  gptr<float> bias = G(E.bias) + o.bias;
+  gptr<float> D0 = G(E.D[0]) + (int64_t)o.D[0] * E.Dcols[0];
+  gptr<float> D1 = G(E.D[E.nf > 1 ? 1 : 0]) + (int64_t)o.D[E.nf > 1 ? 1 : 0] * E.Dcols[E.nf > 1 ? 1 : 0];
+  const int64_t s0 = E.Dcols[0], s1 = E.Dcols[E.nf > 1 ? 1 : 0];
+  const int64_t bb = live ? b : 0;
+  float acc[NDEC > 0 ? NDEC : 1];
+#pragma unroll
+  for (int q = 0; q < NDEC; ++q) acc[q] = 0.0f;
+  for (int r = wave; r < o.n; r += 4) {
+    float j = bias[r];
+    for (int k = 0; k < d; ++k) j += enc[(int64_t)r * d + k] * st[at(S, o.x + k, bb)];
+    float v = 0.0f, rf = 0.0f;
+    if (E.ntype == 0) { v = st[at(S, o.V + r, bb)]; rf = st[at(S, o.ref + r, bb)]; }
+    const float sp = neuron_update(E.ntype, j, v, rf, o.tau_rc, o.tau_ref, o.amp, o.full, dt, o.inv_tau);
+    if (live) {
+      if (E.ntype == 0) { st[at(S, o.V + r, b)] = v; st[at(S, o.ref + r, b)] = rf; }
+      if (o.s >= 0) st[at(S, o.s + r, b)] = sp;
+    }
+#pragma unroll
+    for (int q = 0; q < NDEC; ++q) {
+      const int qq = q < ndec ? q : ndec - 1;
+      gptr<float> row = qq < df0 ? D0 + (int64_t)qq * s0 : D1 + (int64_t)(qq - df0) * s1;
+      acc[q] += row[r] * sp;
+    }
+  }
+#pragma unroll
+  for (int q = 0; q < NDEC; ++q) red[wave][q][lane] = acc[q];
+  __syncthreads();
+  if (wave == 0 && live) {
+    for (int q = 0; q < ndec; ++q) {
+      const float t = red[0][q][lane] + red[1][q][lane] + red[2][q][lane] + red[3][q][lane];
+      const int dr = q < df0 ? o.d[0] + q : o.d[1] + (q - df0);
+      st[at(S, dr, b)] = t;
+    }
+  }
+}
+
+__global__ void __launch_bounds__(256) k_ens_tile(float* st, Strides S, int32_t B, EnsDesc E, float dt) {
+  __shared__ float red[4][kMaxDec][64];
+  switch (dec_bucket(E.ndec)) {
+    case 0: ens_tile_t<0>(st, S, B, E, dt, red); break;
+    case 1: ens_tile_t<1>(st, S, B, E, dt, red); break;
+    case 2: ens_tile_t<2>(st, S, B, E, dt, red); break;
+    case 4: ens_tile_t<4>(st, S, B, E, dt, red); break;
+    case 8: ens_tile_t<8>(st, S, B, E, dt, red); break;
+    default: ens_tile_t<16>(st, S, B, E, dt, red); break;
+  }
+}
+
 // node output <- feed staging [step][feed_rows][B] at the run-relative step ctr[1]
 __global__ void k_feed(float* st, Strides S, int32_t B, int64_t rows, Opnd dst, const int32_t* feed_row,
                        const float* stage, int32_t feed_rows, const int64_t* ctr) {
@@ -277,7 +517,9 @@ __global__ void k_probe_extract(const float* buf, int32_t B, int64_t T, int32_t 
 // A merged group as the persistent kernel sees it (device-resident array).
 struct GroupDesc {
   int32_t type;
-  int32_t M, K;
+  int32_t M, K, tpr;
+  const float* wt_base;    // DOT_INC: transposed weights
+  const int64_t* wt_off;   // DOT_INC: per-op offset of the [K][M] block
   int32_t bcast;
   int64_t rows;
   Opnd dst, src, a, V, ref;
@@ -291,6 +533,7 @@ struct GroupDesc {
   const int32_t* feed_row;
   NeuronParams np;
   FilterParams fp;
+  EnsDesc ens;
 };
 
 struct PersistentProgram {
@@ -301,73 +544,121 @@ struct PersistentProgram {
 // Every group of every step for one batch column per workgroup; groups are
 // separated by workgroup barriers (operators inside a group are independent by
 // construction, and groups run in plan order).  Probes record after each step.
+// LDS = true: the column's whole state is copied into LDS at the start, every
+// group works on LDS for all steps, and it is written back at the end.
+template <bool LDS>
 __global__ void __launch_bounds__(1024)
-k_persistent(float* st, Strides S, int32_t B, const GroupDesc* groups, int32_t ng, int64_t n_steps, float dt,
-             const float* stage, int32_t feed_rows, const int32_t* probe_src, int32_t probe_rows,
-             float* probe_buf, int64_t t0) {
-  const int64_t b = blockIdx.x;
+k_persistent(float* state, int64_t rows, int32_t B, const GroupDesc* groups, int32_t ng, int64_t n_steps,
+             float dt, const float* stage, int32_t feed_rows, const int32_t* probe_src, int32_t probe_rows,
+             float* probe_buf, int64_t t0, float* scratch_g, int64_t scratch_n) {
+  extern __shared__ float lds[];
+  const int64_t col = blockIdx.x;
   const int tid = threadIdx.x, nt = blockDim.x;
   const int lane = tid % warpSize, wave = tid / warpSize, nwaves = nt / warpSize;
+  // column-major state: column `col` occupies rows [col * rows, (col + 1) * rows)
+  float* gcol = state + col * rows;
+  float* st = LDS ? lds : gcol;
+  float* scratch = LDS ? lds + rows : scratch_g + col * scratch_n;
+  const Strides S{1, 0};
+  const int64_t b = 0;
+  if (LDS) {
+    for (int64_t r = tid; r < rows; r += nt) lds[r] = gcol[r];
+    __syncthreads();
+  }
   for (int64_t k = 0; k < n_steps; ++k) {
     for (int32_t g = 0; g < ng; ++g) {
-      const GroupDesc& G = groups[g];
-      const int64_t rows = G.rows;
+      const GroupDesc& G = groups[g];   // (::G is the address-space helper)
+      const int64_t nrow = G.rows;
       switch (G.type) {
         case ms::OP_FEED:
-          for (int64_t r = tid; r < rows; r += nt)
-            st[at(S, rowof(G.dst, r), b)] = stage[(k * feed_rows + G.feed_row[r]) * B + b];
+          for (int64_t r = tid; r < nrow; r += nt)
+            st[rowof(G.dst, r)] = stage[(k * feed_rows + ::G(G.feed_row)[r]) * B + col];
           break;
         case ms::OP_RESET:
-          for (int64_t r = tid; r < rows; r += nt) st[at(S, rowof(G.dst, r), b)] = G.values ? G.values[r] : 0.0f;
+          for (int64_t r = tid; r < nrow; r += nt) st[rowof(G.dst, r)] = G.values ? ::G(G.values)[r] : 0.0f;
           break;
         case ms::OP_COPY:
-          for (int64_t r = tid; r < rows; r += nt)
-            st[at(S, rowof(G.dst, r), b)] = src_val(G.src_base, S, G.bcast, rowof(G.src, r), b);
+          for (int64_t r = tid; r < nrow; r += nt)
+            st[rowof(G.dst, r)] = G.bcast ? ::G(G.src_base)[rowof(G.src, r)] : st[rowof(G.src, r)];
           break;
         case ms::OP_COPY_INC:
-          for (int64_t r = tid; r < rows; r += nt) copy_inc_item(st, S, r, b, G.dst, G.src_base, G.src, G.bcast, G.ptr);
+          for (int64_t r = tid; r < nrow; r += nt) {
+            const int64_t di = rowof(G.dst, r);
+            float acc = st[di];
+            if (G.ptr) {
+              for (int32_t e = ::G(G.ptr)[r]; e < ::G(G.ptr)[r + 1]; ++e)
+                acc += G.bcast ? ::G(G.src_base)[rowof(G.src, e)] : st[rowof(G.src, e)];
+            } else {
+              acc += G.bcast ? ::G(G.src_base)[rowof(G.src, r)] : st[rowof(G.src, r)];
+            }
+            st[di] = acc;
+          }
           break;
         case ms::OP_ELEM_INC:
-          for (int64_t r = tid; r < rows; r += nt)
-            elem_inc_item(st, S, r, b, G.dst, G.a_base, G.a, G.src_base, G.src, G.ptr);
+          for (int64_t r = tid; r < nrow; r += nt) {
+            const int64_t di = rowof(G.dst, r);
+            float acc = st[di];
+            if (G.ptr) {
+              for (int32_t e = ::G(G.ptr)[r]; e < ::G(G.ptr)[r + 1]; ++e)
+                acc += ::G(G.a_base)[rowof(G.a, e)] * st[rowof(G.src, e)];
+            } else {
+              acc += ::G(G.a_base)[rowof(G.a, r)] * st[rowof(G.src, r)];
+            }
+            st[di] = acc;
+          }
           break;
         case ms::OP_DOT_INC: {
-          const uint32_t total = (uint32_t)(rows * G.M);
-          const uint32_t M = (uint32_t)G.M;
-          if (G.K >= 32) {
-            for (uint32_t t = wave; t < total; t += nwaves) {
-              const uint32_t op = t / M;
-              const int32_t m = (int32_t)(t - op * M);
-              const float* w = G.a_base + ((int64_t)G.w_row[op] + m) * G.K;
-              const int64_t x0 = G.x_row[op];
+          // Weights are stored transposed per op ([K][M], G.wt_base) so that
+          // lanes over output rows read consecutive weights.  The K range is
+          // split into G.tpr parts; part-major work items keep lanes of a
+          // wavefront on consecutive rows; parts > 1 add their partial sums
+          // through the LDS scratch after the state.
+          const uint32_t M = (uint32_t)G.M, K = (uint32_t)G.K, tpr = (uint32_t)G.tpr;
+          const uint32_t total = (uint32_t)nrow * M;
+          const uint32_t chunk = (K + tpr - 1) / tpr;
+          for (uint32_t t = tid; t < total * tpr; t += (uint32_t)nt) {
+            const uint32_t part = t / total, rowi = t - part * total;
+            const uint32_t op = rowi / M, m = rowi - op * M;
+            gptr<float> w = ::G(G.wt_base) + (int64_t)::G(G.wt_off)[op];
+            const int64_t x0 = ::G(G.x_row)[op];
+            const uint32_t k0 = part * chunk, k1 = min(K, k0 + chunk);
+            float acc = 0.0f;
+            for (uint32_t kk = k0; kk < k1; ++kk) acc += w[(int64_t)kk * M + m] * st[x0 + kk];
+            if (tpr == 1) st[(int64_t)::G(G.d_row)[op] + m] += acc;
+            else scratch[t] = acc;
+          }
+          if (tpr > 1) {
+            __syncthreads();
+            for (uint32_t rowi = tid; rowi < total; rowi += (uint32_t)nt) {
+              const uint32_t op = rowi / M, m = rowi - op * M;
               float acc = 0.0f;
-              for (int32_t kk = lane; kk < G.K; kk += warpSize) acc += w[kk] * st[at(S, x0 + kk, b)];
-              for (int off = warpSize / 2; off > 0; off >>= 1) acc += __shfl_down(acc, off);
-              if (lane == 0) st[at(S, (int64_t)G.d_row[op] + m, b)] += acc;
-            }
-          } else {
-            for (uint32_t t = tid; t < total; t += nt) {
-              const uint32_t op = t / M;
-              dot_row_item(st, S, op, (int32_t)(t - op * M), b, G.K, G.a_base, G.w_row, G.x_row, G.d_row);
+              for (uint32_t p2 = 0; p2 < tpr; ++p2) acc += scratch[p2 * total + rowi];
+              st[(int64_t)::G(G.d_row)[op] + m] += acc;
             }
           }
           break;
         }
         case ms::OP_LIF:
-          for (int64_t r = tid; r < rows; r += nt) lif_item(st, S, r, b, G.src, G.dst, G.V, G.ref, G.np, dt);
+          for (int64_t r = tid; r < nrow; r += nt) lif_item(st, S, r, b, G.src, G.dst, G.V, G.ref, G.np, dt);
           break;
         case ms::OP_LIF_RATE:
-          for (int64_t r = tid; r < rows; r += nt) lif_rate_item(st, S, r, b, G.src, G.dst, G.np);
+          for (int64_t r = tid; r < nrow; r += nt) lif_rate_item(st, S, r, b, G.src, G.dst, G.np);
           break;
         case ms::OP_LOWPASS:
-          for (int64_t r = tid; r < rows; r += nt) lowpass_item(st, S, r, b, G.dst, G.src, G.fp);
+          for (int64_t r = tid; r < nrow; r += nt) lowpass_item(st, S, r, b, G.dst, G.src, G.fp);
+          break;
+        case ms::OP_ENS:
+          for (int op = wave; op < nrow; op += nwaves) ens_op_wave(st, S, b, G.ens, op, lane, dt);
           break;
         default: break;
       }
       __syncthreads();
     }
     for (int32_t r = tid; r < probe_rows; r += nt)
-      probe_buf[((t0 + k) * probe_rows + r) * B + b] = st[at(S, probe_src[r], b)];
+      probe_buf[((t0 + k) * probe_rows + r) * B + col] = st[::G(probe_src)[r]];
     __syncthreads();
+  }
+  if (LDS) {
+    for (int64_t r = tid; r < rows; r += nt) gcol[r] = lds[r];
   }
 }

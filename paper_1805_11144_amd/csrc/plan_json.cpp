@@ -68,7 +68,28 @@ std::string plan_to_json(const Plan& p) {
       jstr(o, ir.ops[L.ops[k]].name);
     }
     o << "],\"rows\":" << L.rows;
-    if (L.type == OP_DOT_INC) {
+    if (L.type == OP_ENS) {
+      o << ",\"d\":" << L.ens_d << ",\"neuron\":" << L.ens_type << ",\"enc_base\":" << L.a.base
+        << ",\"bias_base\":" << L.ens_bias_base << ",\"D_base\":";
+      jarr(o, L.ens_Dbase);
+      o << ",\"n\":";
+      jarr(o, L.ens_n);
+      o << ",\"x_row\":"; jarr(o, L.ens_x);
+      o << ",\"enc_row\":"; jarr(o, L.ens_enc);
+      o << ",\"bias_row\":"; jarr(o, L.ens_bias);
+      o << ",\"V_row\":"; jarr(o, L.ens_V);
+      o << ",\"ref_row\":"; jarr(o, L.ens_ref);
+      o << ",\"s_row\":"; jarr(o, L.ens_s);
+      o << ",\"df\":"; jarr(o, L.ens_df);
+      o << ",\"D_row\":[";
+      for (size_t k = 0; k < L.ens_D.size(); ++k) { if (k) o << ','; jarr(o, L.ens_D[k]); }
+      o << "],\"d_row\":[";
+      for (size_t k = 0; k < L.ens_dd.size(); ++k) { if (k) o << ','; jarr(o, L.ens_dd[k]); }
+      o << ']';
+      o << ",\"tau_rc\":"; jarr(o, L.tau_rc);
+      o << ",\"tau_ref\":"; jarr(o, L.tau_ref);
+      o << ",\"amp\":"; jarr(o, L.amp);
+    } else if (L.type == OP_DOT_INC) {
       o << ",\"M\":" << L.M << ",\"K\":" << L.K << ",\"w_row\":";
       jarr(o, L.w_row);
       o << ",\"x_row\":";

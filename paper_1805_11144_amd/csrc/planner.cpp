@@ -35,7 +35,7 @@ namespace ms {
 
 const char* op_type_name(int32_t t) {
   static const char* n[] = {"Feed", "Reset", "Copy", "CopyInc", "ElementwiseInc",
-                            "DotInc", "SimLIF", "SimLIFRate", "Lowpass"};
+                            "DotInc", "SimLIF", "SimLIFRate", "Lowpass", "Ensemble"};
   return (t >= 0 && t < OP_NTYPES) ? n[t] : "?";
 }
 
@@ -51,6 +51,14 @@ std::vector<SRef> read_slots(const Op& o) {
     case OP_LIF: return {o.src, o.V, o.ref};
     case OP_LIF_RATE: return {o.src};
     case OP_LOWPASS: return {o.src, o.dst};
+    case OP_ENS: {
+      std::vector<SRef> r;
+      if (o.src.sig >= 0) { r.push_back(o.src); r.push_back(o.a); }
+      r.push_back(o.bias);
+      if (o.V.sig >= 0) { r.push_back(o.V); r.push_back(o.ref); }
+      for (const auto& d : o.decs) r.push_back(d.first);
+      return r;
+    }
     default: return {};
   }
 }
@@ -70,6 +78,12 @@ void access(const Op& o, std::vector<int32_t>& sets, std::vector<int32_t>& incs,
       upds.push_back(o.V.sig); upds.push_back(o.ref.sig); break;
     case OP_LIF_RATE: reads.push_back(o.src.sig); sets.push_back(o.dst.sig); break;
     case OP_LOWPASS: reads.push_back(o.src.sig); upds.push_back(o.dst.sig); break;
+    case OP_ENS:
+      if (o.src.sig >= 0) reads.push_back(o.src.sig);
+      if (o.dst.sig >= 0) sets.push_back(o.dst.sig);
+      for (const auto& d : o.decs) sets.push_back(d.second.sig);
+      if (o.V.sig >= 0) { upds.push_back(o.V.sig); upds.push_back(o.ref.sig); }
+      break;
     default: break;
   }
 }
@@ -86,6 +100,12 @@ std::vector<int32_t> merge_key(const IR& ir, const Op& o) {
     case OP_LIF: return {OP_LIF, b(o.src), b(o.dst), b(o.V), b(o.ref)};
     case OP_LIF_RATE: return {OP_LIF_RATE, b(o.src), b(o.dst)};
     case OP_LOWPASS: return {OP_LOWPASS, b(o.dst), b(o.src)};
+    case OP_ENS: {
+      std::vector<int32_t> k = {OP_ENS, o.ntype, b(o.src), b(o.a), o.src.len, b(o.bias),
+                                b(o.dst), b(o.V), b(o.ref)};
+      for (const auto& d : o.decs) { k.push_back(b(d.first)); k.push_back(d.second.len); k.push_back(b(d.second)); }
+      return k;
+    }
     default: return {o.type};
   }
 }
@@ -600,6 +620,39 @@ LGroup lower_group(const Plan& p, const std::vector<int32_t>& ops) {
       g.cb = uniform_or_rows(cb);
       break;
     }
+    case OP_ENS: {
+      g.rows = (int64_t)ops.size();
+      g.ens_type = f.ntype;
+      g.ens_d = f.src.sig >= 0 ? f.src.len : 0;
+      for (const auto& d : f.decs) g.ens_df.push_back(d.second.len);
+      g.ens_D.assign(f.decs.size(), {});
+      g.ens_dd.assign(f.decs.size(), {});
+      std::vector<double> trc, tref, amp;
+      for (int32_t oi : ops) {
+        const Op& o = ir.ops[oi];
+        g.ens_n.push_back(o.n);
+        g.ens_x.push_back(o.src.sig >= 0 ? row(o.src, 0) : -1);
+        g.ens_enc.push_back(o.a.sig >= 0 ? (int32_t)p.sig_offset[o.a.sig] : -1);
+        g.ens_bias.push_back(row(o.bias, 0));
+        g.ens_V.push_back(o.V.sig >= 0 ? row(o.V, 0) : -1);
+        g.ens_ref.push_back(o.ref.sig >= 0 ? row(o.ref, 0) : -1);
+        g.ens_s.push_back(o.dst.sig >= 0 ? row(o.dst, 0) : -1);
+        for (size_t k = 0; k < o.decs.size(); ++k) {
+          g.ens_D[k].push_back((int32_t)p.sig_offset[o.decs[k].first.sig]);
+          g.ens_dd[k].push_back(row(o.decs[k].second, 0));
+        }
+        trc.push_back(o.tau_rc); tref.push_back(o.tau_ref); amp.push_back(o.amp);
+      }
+      // operand bases for the runtime
+      g.src.base = f.src.sig >= 0 ? base(f.src) : -1;
+      g.a.base = f.a.sig >= 0 ? base(f.a) : -1;
+      g.ens_bias_base = base(f.bias);
+      g.tau_rc = uniform_or_rows(trc);
+      g.tau_ref = uniform_or_rows(tref);
+      g.amp = uniform_or_rows(amp);
+      for (const auto& d : f.decs) g.ens_Dbase.push_back(base(d.first));
+      break;
+    }
     default: fail(MS_E_INVALID, "cannot lower operator type");
   }
   return g;
@@ -614,6 +667,7 @@ std::unique_ptr<Plan> make_plan(const Model& m, double dt, const PlanOpts& o) {
   p->built = build_params(m);
   p->ir = build_ir(m, p->built, dt);
   if (o.simplify) simplify_ir(p->ir);
+  if (o.fuse) fuse_ensembles(p->ir);
   IR& ir = p->ir;
   // merge keys in first-appearance order
   std::map<std::vector<int32_t>, int32_t> kid;

@@ -57,6 +57,7 @@ struct Launch {
   NeuronParams np{};
   FilterParams fp{};
   const int32_t* feed_rows = nullptr;
+  EnsDesc ens{};
 };
 
 }  // namespace
@@ -97,6 +98,12 @@ struct ms_sim {
   // persistent driver
   PersistentProgram prog{};
   bool persistent_ok = false;
+  size_t lds_limit = 0;              // dynamic LDS bytes one workgroup may use
+  int32_t persistent_threads = 256;  // workgroup size of the persistent kernel
+  int64_t scratch_n = 0;             // per-column scratch floats of the persistent kernel
+  float* scratch = nullptr;          // global scratch when state is not LDS-resident
+  std::vector<void*> extra_allocs;   // transposed weights and their offsets
+  std::vector<std::vector<float>> host_bases;   // host copies of parameter bases
 };
 
 namespace {
@@ -129,6 +136,8 @@ void free_sim(ms_sim* s) {
     if (s->base_ptr[b] != s->state) f(s->base_ptr[b]);
   f(s->ipool); f(s->fpool); f(s->ctr); f(s->feed_stage); f(s->feed_tmp); f(s->probe_buf);
   f(s->prog.groups);
+  f(s->scratch);
+  for (void* p : s->extra_allocs) f(p);
   if (s->ev0) (void)hipEventDestroy(s->ev0);
   if (s->ev1) (void)hipEventDestroy(s->ev1);
   if (s->own_stream && s->stream) (void)hipStreamDestroy(s->stream);
@@ -177,6 +186,8 @@ void setup_device(ms_sim* s) {
       }
       s->base_ptr[b] = dev_alloc<float>(host.size());
       HIPCHECK(hipMemcpy(s->base_ptr[b], host.data(), host.size() * sizeof(float), hipMemcpyHostToDevice));
+      if (s->host_bases.size() <= b) s->host_bases.resize(b + 1);
+      s->host_bases[b] = std::move(host);
     }
   }
   if (!s->state) {
@@ -193,18 +204,45 @@ void setup_device(ms_sim* s) {
     o.w = pb.add_i(g.w_row); o.x = pb.add_i(g.x_row); o.d = pb.add_i(g.d_row);
     o.feed = pb.add_i(g.feed_rows);
     o.values = pb.add_f(g.values);
-    o.trc = g.tau_rc.size() > 1 ? pb.add_f(g.tau_rc) : -1;
+    const bool per_row_params = g.type != OP_ENS;
+    o.trc = per_row_params && g.tau_rc.size() > 1 ? pb.add_f(g.tau_rc) : -1;
     o.full = -1;
-    if (g.tau_rc.size() > 1) {
+    if (per_row_params && g.tau_rc.size() > 1) {
       std::vector<float> full(g.tau_rc.size());
       for (size_t k = 0; k < full.size(); ++k) full[k] = (float)std::expm1(-p.dt / (double)g.tau_rc[k]);
       o.full = pb.add_f(full);
     }
-    o.tref = g.tau_ref.size() > 1 ? pb.add_f(g.tau_ref) : -1;
-    o.amp = g.amp.size() > 1 ? pb.add_f(g.amp) : -1;
+    o.tref = per_row_params && g.tau_ref.size() > 1 ? pb.add_f(g.tau_ref) : -1;
+    o.amp = per_row_params && g.amp.size() > 1 ? pb.add_f(g.amp) : -1;
     o.ca = g.ca.size() > 1 ? pb.add_f(g.ca) : -1;
     o.cb = g.cb.size() > 1 ? pb.add_f(g.cb) : -1;
     offs.push_back(o);
+  }
+  // packed per-op records of fused ensemble groups (EnsOp, 16 x 4 bytes each)
+  static_assert(sizeof(EnsOp) == 16 * 4, "EnsOp layout");
+  std::vector<int64_t> ens_off(p.lowered.size(), -1);
+  for (size_t gi = 0; gi < p.lowered.size(); ++gi) {
+    const LGroup& g = p.lowered[gi];
+    if (g.type != OP_ENS) continue;
+    std::vector<int32_t> rec;
+    for (size_t k = 0; k < g.ens_n.size(); ++k) {
+      EnsOp e{};
+      e.n = g.ens_n[k]; e.x = g.ens_x[k]; e.enc = g.ens_enc[k]; e.bias = g.ens_bias[k];
+      e.V = g.ens_V[k]; e.ref = g.ens_ref[k]; e.s = g.ens_s[k];
+      for (int f = 0; f < kMaxFns; ++f) {
+        e.D[f] = f < (int)g.ens_D.size() ? g.ens_D[f][k] : 0;
+        e.d[f] = f < (int)g.ens_dd.size() ? g.ens_dd[f][k] : 0;
+      }
+      const float trc = g.tau_rc.size() > 1 ? g.tau_rc[k] : g.tau_rc[0];
+      e.tau_rc = trc;
+      e.tau_ref = g.tau_ref.size() > 1 ? g.tau_ref[k] : g.tau_ref[0];
+      e.amp = g.amp.size() > 1 ? g.amp[k] : g.amp[0];
+      e.full = (float)std::expm1(-p.dt / (double)trc);
+      e.inv_tau = (float)(1.0 / (double)trc);
+      const int32_t* w = reinterpret_cast<const int32_t*>(&e);
+      rec.insert(rec.end(), w, w + 16);
+    }
+    ens_off[gi] = pb.add_i(rec);
   }
   const int64_t probe_off = pb.add_i(p.probe_src_rows);
   s->ipool = dev_alloc<int32_t>(std::max<size_t>(1, pb.ints.size()));
@@ -246,6 +284,20 @@ void setup_device(ms_sim* s) {
     if (g.type == OP_LOWPASS) {
       l.fp.a = g.ca[0]; l.fp.b = g.cb[0];
       l.fp.a_r = fp(o.ca); l.fp.b_r = fp(o.cb);
+    }
+    if (g.type == OP_ENS) {
+      EnsDesc& E = l.ens;
+      if ((int)g.ens_df.size() > kMaxFns) fail(MS_E_INVALID, "fused ensemble with too many decoded functions");
+      E.d = g.ens_d; E.ntype = g.ens_type; E.nf = (int32_t)g.ens_df.size(); E.ndec = 0;
+      for (int f = 0; f < E.nf; ++f) { E.df[f] = g.ens_df[f]; E.ndec += g.ens_df[f]; }
+      if (E.ndec > kMaxDec) fail(MS_E_INVALID, "fused ensemble decodes too many outputs");
+      for (int f = 0; f < E.nf; ++f) {
+        E.D[f] = s->base_ptr[g.ens_Dbase[f]];
+        E.Dcols[f] = ir.bases[g.ens_Dbase[f]].cols;
+      }
+      E.enc = g.a.base >= 0 ? s->base_ptr[g.a.base] : nullptr;
+      E.bias = s->base_ptr[g.ens_bias_base];
+      E.ops = reinterpret_cast<const EnsOp*>(s->ipool + ens_off[gi]);
     }
     s->launches.push_back(l);
   }
@@ -313,6 +365,16 @@ void launch_group(ms_sim* s, const Launch& l) {
     case OP_LOWPASS:
       hipLaunchKernelGGL(k_lowpass, dim3(grid_for(n)), dim3(kBlock), 0, q, st, S, B, l.rows, l.dst,
                          l.src, l.fp);
+      break;
+    case OP_ENS:
+      if (B >= 32) {
+        hipLaunchKernelGGL(k_ens_tile, dim3((unsigned)l.rows, (unsigned)((B + 63) / 64)), dim3(256), 0, q, st, S,
+                           B, l.ens, s->dt);
+      } else {
+        const int64_t waves = l.rows * B;
+        hipLaunchKernelGGL(k_ens_waves, dim3((unsigned)((waves + 3) / 4)), dim3(256), 0, q, st, S, B,
+                           (int32_t)l.rows, l.ens, s->dt);
+      }
       break;
     default: fail(MS_E_INVALID, "unknown group type");
   }
@@ -404,6 +466,12 @@ void stage_feeds(ms_sim* s, int64_t n_steps, const ms_feed* feeds, int32_t n_fee
   }
 }
 
+const std::vector<float>& host_param_base(ms_sim* s, int32_t base) {
+  if (base < 0 || base >= (int32_t)s->host_bases.size() || s->host_bases[base].empty())
+    fail(MS_E_INVALID, "parameter base not available on the host");
+  return s->host_bases[base];
+}
+
 // Weight bytes read per step (every parameter base array).
 int64_t param_bytes(const Plan& p) {
   int64_t n = 0;
@@ -423,16 +491,54 @@ int32_t choose_driver(const Plan& p, int32_t B, int32_t requested) {
 }
 
 void setup_persistent(ms_sim* s) {
+  s->persistent_threads = s->state_rows <= 4096 ? 256 : 1024;
   std::vector<GroupDesc> gd;
-  for (const Launch& l : s->launches) {
+  for (size_t gi = 0; gi < s->launches.size(); ++gi) {
+    const Launch& l = s->launches[gi];
     GroupDesc g{};
     g.type = l.type; g.M = l.M; g.K = l.K; g.bcast = l.src_bcast ? 1 : 0; g.rows = l.rows;
+    g.tpr = 1;
+    if (l.type == OP_DOT_INC) {
+      // transposed copy of every op's [M][K] block, [K][M], in one buffer
+      const int64_t blk = (int64_t)l.M * l.K;
+      std::vector<float> wt((size_t)(blk * l.rows));
+      std::vector<int64_t> off((size_t)l.rows);
+      std::vector<int32_t> wrow((size_t)l.rows);
+      HIPCHECK(hipMemcpy(wrow.data(), l.w_row, wrow.size() * 4, hipMemcpyDeviceToHost));
+      const LGroup& lg = s->plan->lowered[gi];
+      const std::vector<float>& host_w = host_param_base(s, lg.a.base);
+      const int64_t cols = s->plan->ir.bases[lg.a.base].cols;
+      for (int64_t op = 0; op < l.rows; ++op) {
+        off[op] = op * blk;
+        for (int32_t m = 0; m < l.M; ++m)
+          for (int32_t k = 0; k < l.K; ++k)
+            wt[(size_t)(op * blk + (int64_t)k * l.M + m)] =
+                host_w[(size_t)(((int64_t)wrow[op] + m) * cols + (cols == 1 ? 0 : k)) + (cols == 1 ? k : 0)];
+      }
+      float* dwt = dev_alloc<float>(std::max<size_t>(1, wt.size()));
+      int64_t* doff = dev_alloc<int64_t>(std::max<size_t>(1, off.size()));
+      HIPCHECK(hipMemcpy(dwt, wt.data(), wt.size() * 4, hipMemcpyHostToDevice));
+      HIPCHECK(hipMemcpy(doff, off.data(), off.size() * 8, hipMemcpyHostToDevice));
+      s->extra_allocs.push_back(dwt);
+      s->extra_allocs.push_back(doff);
+      g.wt_base = dwt;
+      g.wt_off = doff;
+      const int64_t out_rows = l.rows * (int64_t)l.M;
+      while (g.tpr < 64 && out_rows * g.tpr * 2 <= s->persistent_threads && g.tpr * 2 <= l.K) g.tpr *= 2;
+      s->scratch_n = std::max<int64_t>(s->scratch_n, out_rows * g.tpr);
+    }
     g.dst = l.dst; g.src = l.src; g.a = l.a; g.V = l.V; g.ref = l.ref;
     g.src_base = l.src_base; g.a_base = l.a_base; g.ptr = l.ptr; g.values = l.values;
     g.w_row = l.w_row; g.x_row = l.x_row; g.d_row = l.d_row; g.feed_row = l.feed_rows;
-    g.np = l.np; g.fp = l.fp;
+    g.np = l.np; g.fp = l.fp; g.ens = l.ens;
     gd.push_back(g);
   }
+  int lds_max = 0;
+  HIPCHECK(hipDeviceGetAttribute(&lds_max, hipDeviceAttributeMaxSharedMemoryPerBlock, s->device));
+  s->lds_limit = (size_t)lds_max;
+  if (s->lds_limit > 65536)
+    HIPCHECK(hipFuncSetAttribute((const void*)k_persistent<true>, hipFuncAttributeMaxDynamicSharedMemorySize,
+                                 (int)s->lds_limit));
   s->prog.n_groups = (int32_t)gd.size();
   s->prog.groups = dev_alloc<GroupDesc>(std::max<size_t>(1, gd.size()));
   if (!gd.empty())
@@ -440,12 +546,21 @@ void setup_persistent(ms_sim* s) {
 }
 
 void run_persistent(ms_sim* s, int64_t n_steps) {
-  const int64_t rows = (int64_t)s->state_rows;
-  const int threads = rows <= 4096 ? 256 : 1024;
-  hipLaunchKernelGGL(k_persistent, dim3(s->B), dim3(threads), 0, s->stream, s->state, s->S, s->B,
-                     (const GroupDesc*)s->prog.groups, s->prog.n_groups, n_steps, s->dt,
-                     (const float*)s->feed_stage, s->plan->ir.feed_rows, s->probe_src, s->probe_rows,
-                     s->probe_buf, s->steps_total);
+  const int64_t rows = (int64_t)std::max<size_t>(1, s->state_rows);
+  const int threads = s->persistent_threads;
+  const size_t lds = (size_t)(rows + s->scratch_n) * sizeof(float);
+  if (lds <= s->lds_limit) {
+    hipLaunchKernelGGL(k_persistent<true>, dim3(s->B), dim3(threads), lds, s->stream, s->state, rows, s->B,
+                       (const GroupDesc*)s->prog.groups, s->prog.n_groups, n_steps, s->dt,
+                       (const float*)s->feed_stage, s->plan->ir.feed_rows, s->probe_src, s->probe_rows,
+                       s->probe_buf, s->steps_total, s->scratch, s->scratch_n);
+  } else {
+    if (!s->scratch && s->scratch_n > 0) s->scratch = dev_alloc<float>((size_t)s->scratch_n * s->B);
+    hipLaunchKernelGGL(k_persistent<false>, dim3(s->B), dim3(threads), 0, s->stream, s->state, rows, s->B,
+                       (const GroupDesc*)s->prog.groups, s->prog.n_groups, n_steps, s->dt,
+                       (const float*)s->feed_stage, s->plan->ir.feed_rows, s->probe_src, s->probe_rows,
+                       s->probe_buf, s->steps_total, s->scratch, s->scratch_n);
+  }
   hipLaunchKernelGGL(k_set_ctr, dim3(1), dim3(64), 0, s->stream, s->ctr, s->steps_total + n_steps, n_steps);
 }
 

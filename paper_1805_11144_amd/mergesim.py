@@ -50,6 +50,7 @@ class ProbeDesc(C.Structure):
 class SimOpts(C.Structure):
     _fields_ = [("dt", C.c_double), ("minibatch", _i32), ("unroll", _i32), ("planner", _i32),
                 ("planner_depth", _i32), ("merge", _i32), ("sort", _i32), ("simplify", _i32),
+                ("fuse", _i32),
                 ("driver", _i32), ("device", _i32), ("stream", C.c_void_p),
                 ("probe_capacity_steps", _i64)]
 
@@ -232,13 +233,14 @@ def model_from_spec(spec) -> Model:
 
 
 def make_opts(dt=0.001, minibatch=1, unroll=10, planner=PLANNER_TREE, planner_depth=3, merge=True,
-              sort=True, simplify=True, driver=DRIVER_AUTO, device=0, stream=None,
+              sort=True, simplify=True, fuse=True, driver=DRIVER_AUTO, device=0, stream=None,
               probe_capacity_steps=1000) -> SimOpts:
     o = SimOpts()
     load_library().ms_sim_opts_default(C.byref(o))
     o.dt, o.minibatch, o.unroll = float(dt), int(minibatch), int(unroll)
     o.planner, o.planner_depth = int(planner), int(planner_depth)
     o.merge, o.sort, o.simplify = int(bool(merge)), int(bool(sort)), int(bool(simplify))
+    o.fuse = int(bool(fuse))
     o.driver, o.device = int(driver), int(device)
     o.stream = stream
     o.probe_capacity_steps = int(probe_capacity_steps)

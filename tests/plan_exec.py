@@ -17,6 +17,27 @@ def _rows(op, n):
     return op["start"] + np.arange(n, dtype=np.int64)
 
 
+def _lif(J, V, ref, dt, trc, tref, amp):
+    integ = np.clip(dt - ref, 0, dt)
+    V = V - (J - V) * np.expm1(-integ / trc)
+    ref = np.maximum(ref - dt, 0)
+    spk = V > 1
+    q = np.where(spk & (J > 1), (V - 1) / np.where(J > 1, J - 1, 1), 0.0)
+    since = np.where(q >= 1, integ, np.minimum(-trc * np.log1p(-np.minimum(q, 0.999999999999)), integ))
+    since = np.where(spk & (J > 1), since, 0.0)
+    V = np.where(spk, 0.0, np.maximum(V, 0.0))
+    ref = np.where(spk, tref - since, ref)
+    return np.where(spk, amp / dt, 0.0), V, ref
+
+
+def _rate(J, trc, tref, amp):
+    r = np.zeros_like(J)
+    m = J > 1
+    r[m] = 1.0 / (np.broadcast_to(tref, J.shape)[m] +
+                  np.broadcast_to(trc, J.shape)[m] * np.log1p(1.0 / (J[m] - 1.0)))
+    return amp * r
+
+
 def _vec(v, n):
     v = np.asarray(v, np.float64)
     return np.broadcast_to(v, (n,)) if v.size == 1 else v
@@ -104,6 +125,11 @@ class PlanExecutor:
                         cols[k].append(np.full(e.n_neurons, getattr(e, "amplitude" if k == "amp" else k)))
                 for k in cols:
                     g[k] = np.concatenate(cols[k]).tolist()
+            elif g["type"] == "Ensemble":
+                ens = [self.spec.ensembles[int(name.split(".")[0][1:])] for name in g["ops"]]
+                g["tau_rc"] = [e.tau_rc for e in ens]
+                g["tau_ref"] = [e.tau_ref for e in ens]
+                g["amp"] = [e.amplitude for e in ens]
             elif g["type"] == "Lowpass":
                 ca, cb = [], []
                 for name in g["ops"]:
@@ -185,6 +211,29 @@ class PlanExecutor:
                     st[rr] = np.where(spk, tref - since, ref)
                     out = np.where(spk, amp / dt, 0.0)
                 st[_rows(g["dst"], n)] = out
+            elif t == "Ensemble":
+                trc_all = _vec(g["tau_rc"], n); tref_all = _vec(g["tau_ref"], n)
+                amp_all = _vec(g["amp"], n)
+                for k in range(n):
+                    nn = g["n"][k]
+                    b0 = g["bias_row"][k]
+                    J = np.repeat(self.bases[g["bias_base"]][b0:b0 + nn, 0][:, None], self.B, axis=1)
+                    if g["x_row"][k] >= 0:
+                        d = g["d"]
+                        E = self.bases[g["enc_base"]][g["enc_row"][k]:g["enc_row"][k] + nn]
+                        J = J + E[:, :d] @ st[g["x_row"][k]:g["x_row"][k] + d]
+                    if g["neuron"] == 0:
+                        v0, r0 = g["V_row"][k], g["ref_row"][k]
+                        s_, st[v0:v0 + nn], st[r0:r0 + nn] = _lif(J, st[v0:v0 + nn].copy(),
+                                                                  st[r0:r0 + nn].copy(), self.dt,
+                                                                  trc_all[k], tref_all[k], amp_all[k])
+                    else:
+                        s_ = _rate(J, trc_all[k], tref_all[k], amp_all[k])
+                    if g["s_row"][k] >= 0:
+                        st[g["s_row"][k]:g["s_row"][k] + nn] = s_
+                    for f, df in enumerate(g["df"]):
+                        D = self.bases[g["D_base"][f]][g["D_row"][f][k]:g["D_row"][f][k] + df, :nn]
+                        st[g["d_row"][f][k]:g["d_row"][f][k] + df] = D @ s_
             elif t == "Lowpass":
                 y, v = _rows(g["dst"], n), _rows(g["src"], n)
                 st[y] = _vec(g["ca"], n)[:, None] * st[y] + _vec(g["cb"], n)[:, None] * st[v]

@@ -35,11 +35,12 @@ def run_oracle(w):
     return [ref.data(p) for p in range(len(w.spec.probes))]
 
 
+@pytest.mark.parametrize("fuse", [True, False])
 @pytest.mark.parametrize("driver", list(DRIVERS))
 @pytest.mark.parametrize("name", list(SMALL))
-def test_rate_mode_parity(name, driver):
+def test_rate_mode_parity(name, driver, fuse):
     w = make_workload(name, neuron_type="lif_rate", **SMALL[name])
-    got = run_gpu(w, driver=DRIVERS[driver], unroll=7)
+    got = run_gpu(w, driver=DRIVERS[driver], unroll=7, fuse=fuse)
     exp = run_oracle(w)
     for pi, (g, e) in enumerate(zip(got, exp)):
         r = rel_err(g, e)

@@ -29,6 +29,7 @@ OPTS = {
     "tree2_nosort": (dict(planner_depth=2, sort=False), dict(depth=2, sort=False)),
     "nosimplify": (dict(simplify=False), dict(do_simplify=False)),
     "nomerge": (dict(merge=False), dict(merge=False)),
+    "nofuse": (dict(fuse=False), dict(fuse=False)),
 }
 
 

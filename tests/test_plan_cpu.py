@@ -36,7 +36,7 @@ def test_build_params_match_oracle(name):
 @pytest.mark.parametrize("name", list(SMALL))
 @pytest.mark.parametrize("neuron_type", ["lif_rate", "lif"])
 @pytest.mark.parametrize("opts", [dict(), dict(planner=M.PLANNER_GREEDY), dict(sort=False),
-                                  dict(simplify=False), dict(merge=False)])
+                                  dict(simplify=False), dict(merge=False), dict(fuse=False)])
 def test_plan_execution_matches_oracle(name, neuron_type, opts):
     w = make_workload(name, neuron_type=neuron_type, **SMALL[name])
     plan = M.Plan(M.model_from_spec(w.spec), minibatch=w.minibatch, **opts)
