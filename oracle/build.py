@@ -15,6 +15,8 @@ Pins (tests/test_oracle_build.py): normal-equation residual; agreement with
 scipy.linalg.solve(assume_a='pos') and with numpy.linalg.lstsq on the stacked
 system [A; sqrt(lambda) I].
 """
+import os
+from concurrent.futures import ThreadPoolExecutor
 from dataclasses import dataclass, field
 from typing import Dict, Optional, Tuple
 
@@ -64,9 +66,8 @@ def ridge_decoders(A: np.ndarray, Y: np.ndarray, reg: float) -> np.ndarray:
     sigma = reg * A.max()
     lam = M * sigma * sigma
     G = A.T @ A + lam * np.eye(n)
-    L = np.linalg.cholesky(G)
-    Z = scipy.linalg.solve_triangular(L, A.T @ Y, lower=True)
-    return scipy.linalg.solve_triangular(L.T, Z, lower=False)
+    factor = scipy.linalg.cho_factor(G, lower=True, check_finite=False)
+    return scipy.linalg.cho_solve(factor, A.T @ Y, check_finite=False)
 
 
 SOLVER_REG = 0.1   # sigma = 0.1 * max activity
@@ -98,12 +99,34 @@ def build_params(spec, direct: frozenset = frozenset()) -> BuiltParams:
     for p in spec.probes:
         if p.target[0] == "ens":
             needed.append((p.target[1], "identity"))
+    todo = []
     for key in needed:
+        if key not in todo and key[0] not in direct:
+            todo.append(key)
+
+    def solve(key):
         ei, fn = key
-        if key in P.decoders or ei in direct:
-            continue
         ens = spec.ensembles[ei]
         X = np.asarray(ens.eval_points, np.float64)
         A = ensemble_activities(ens, P.gain[ei], P.bias[ei], X)
-        P.decoders[key] = ridge_decoders(A, function_targets(fn, X), SOLVER_REG)
+        return ridge_decoders(A, function_targets(fn, X), SOLVER_REG)
+
+    # ensembles are independent; solve them concurrently (numpy releases the GIL)
+    workers = min(len(todo), os.cpu_count() or 1) if len(todo) > 8 else 1
+    if workers > 1:
+        try:   # one BLAS thread per worker: parallelism comes from the ensembles
+            from threadpoolctl import threadpool_limits
+            limit = threadpool_limits(1)
+        except Exception:
+            limit = None
+        try:
+            with ThreadPoolExecutor(workers) as pool:
+                results = list(pool.map(solve, todo))
+        finally:
+            if limit is not None:
+                limit.restore_original_limits()
+    else:
+        results = [solve(k) for k in todo]
+    for key, D in zip(todo, results):
+        P.decoders[key] = D
     return P
