@@ -69,8 +69,10 @@ def _obj(ref):
 
 class OracleSim:
     def __init__(self, spec, minibatch: int = 1, param_dtype=np.float64,
-                 direct: frozenset = frozenset(), neuron_type: Optional[str] = None):
+                 direct: frozenset = frozenset(), neuron_type: Optional[str] = None,
+                 record_current: tuple = ()):
         self.spec = spec
+        self.record_current = tuple(record_current)
         self.B = int(minibatch)
         self.dt = float(spec.dt)
         self.direct = frozenset(direct)
@@ -148,6 +150,7 @@ class OracleSim:
                    for pi, p in enumerate(spec.probes) if p.synapse is not None}
         self.step = 0
         self.probe_data = {pi: [] for pi in range(len(spec.probes))}
+        self.current_rec = {i: ([], []) for i in self.record_current}
 
     def _post_width(self, c) -> int:
         if c.post_slice is not None:
@@ -225,6 +228,11 @@ class OracleSim:
                     out[obj] = None
                     continue
                 J = self.bias[i][None, :] + x @ self.enc[i].T + self.gain[i][None, :] * nin
+                if i in self.current_rec:
+                    scale = (np.abs(self.bias[i])[None, :] + np.abs(x) @ np.abs(self.enc[i]).T
+                             + np.abs(self.gain[i])[None, :] * np.abs(nin))
+                    self.current_rec[i][0].append(J.copy())
+                    self.current_rec[i][1].append(scale)
                 if self.neuron_type[i] == "lif":
                     s, self.V[i], self.ref[i] = lif_step(J, self.V[i], self.ref[i], self.dt,
                                                          ens.tau_rc, ens.tau_ref, ens.amplitude)
@@ -269,6 +277,13 @@ class OracleSim:
         if not d:
             return np.zeros((self.B, 0, self._probe_width(self.spec.probes[probe_index])))
         return np.stack(d, axis=1)
+
+    def current_data(self, ens: int):
+        """Input current J of an ensemble named in record_current, and the
+        magnitude of its terms |bias| + |x| |E|^T + |gain| |neuron input|, both
+        [B, steps_since_reset, n_neurons].  Recording changes no arithmetic."""
+        J, S = self.current_rec[ens]
+        return np.stack(J, axis=1), np.stack(S, axis=1)
 
     # -------------------------------------------------------------------- state
     def get_state(self):

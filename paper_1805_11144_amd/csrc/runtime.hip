@@ -728,6 +728,38 @@ ms_status ms_sim_reset(ms_sim* s) {
   });
 }
 
+// Copies one state signal between the device state and a host buffer laid out
+// [B][rows], touching only that signal's elements.  Row-major state (rs = B,
+// cs = 1) holds the signal as one block of rows*B floats; column-major state
+// (rs = 1) holds B columns of rows floats, cs floats apart.
+static void state_copy(ms_sim* s, int32_t sig, float* host, bool to_device) {
+  const int64_t rows = s->plan->ir.sigs[sig].rows, B = s->B;
+  const int64_t r0 = s->plan->sig_offset[sig];
+  DeviceGuard dg(s->device);
+  HIPCHECK(hipStreamSynchronize(s->stream));
+  if (s->S.cs == 1) {
+    if (s->S.rs != B) fail(MS_E_STATE, "unexpected state layout");
+    float* dev = s->state + r0 * B;
+    std::vector<float> h((size_t)(rows * B));
+    if (to_device) {
+      for (int64_t b = 0; b < B; ++b)
+        for (int64_t r = 0; r < rows; ++r) h[(size_t)(r * B + b)] = host[(size_t)(b * rows + r)];
+      HIPCHECK(hipMemcpy(dev, h.data(), h.size() * 4, hipMemcpyHostToDevice));
+    } else {
+      HIPCHECK(hipMemcpy(h.data(), dev, h.size() * 4, hipMemcpyDeviceToHost));
+      for (int64_t b = 0; b < B; ++b)
+        for (int64_t r = 0; r < rows; ++r) host[(size_t)(b * rows + r)] = h[(size_t)(r * B + b)];
+    }
+  } else {
+    if (s->S.rs != 1 || s->S.cs < r0 + rows) fail(MS_E_STATE, "unexpected state layout");
+    float* dev = s->state + r0;
+    if (to_device)
+      HIPCHECK(hipMemcpy2D(dev, s->S.cs * 4, host, rows * 4, rows * 4, B, hipMemcpyHostToDevice));
+    else
+      HIPCHECK(hipMemcpy2D(host, rows * 4, dev, s->S.cs * 4, rows * 4, B, hipMemcpyDeviceToHost));
+  }
+}
+
 static int32_t state_signal(const ms_sim* s, int32_t which, int32_t id) {
   const IR& ir = s->plan->ir;
   auto pick = [&](const std::vector<int32_t>& v) -> int32_t {
@@ -747,16 +779,8 @@ ms_status ms_sim_get_state(ms_sim* s, int32_t which, int32_t id, float* out, int
   return guarded([&] {
     if (!s || !out) fail(MS_E_INVALID, "NULL argument");
     const int32_t sig = state_signal(s, which, id);
-    const int32_t rows = s->plan->ir.sigs[sig].rows;
-    const int64_t n = (int64_t)rows * s->B;
-    if (cap < n) fail(MS_E_INVALID, "state output capacity too small");
-    DeviceGuard dg(s->device);
-    std::vector<float> h(s->state_rows * s->B);
-    HIPCHECK(hipStreamSynchronize(s->stream));
-    HIPCHECK(hipMemcpy(h.data(), s->state, h.size() * 4, hipMemcpyDeviceToHost));
-    const int64_t r0 = s->plan->sig_offset[sig];
-    for (int32_t b = 0; b < s->B; ++b)
-      for (int32_t r = 0; r < rows; ++r) out[(size_t)b * rows + r] = h[(size_t)((r0 + r) * s->S.rs + b * s->S.cs)];
+    if (cap < (int64_t)s->plan->ir.sigs[sig].rows * s->B) fail(MS_E_INVALID, "state output capacity too small");
+    state_copy(s, sig, out, false);
   });
 }
 
@@ -764,17 +788,8 @@ ms_status ms_sim_set_state(ms_sim* s, int32_t which, int32_t id, const float* in
   return guarded([&] {
     if (!s || !in) fail(MS_E_INVALID, "NULL argument");
     const int32_t sig = state_signal(s, which, id);
-    const int32_t rows = s->plan->ir.sigs[sig].rows;
-    const int64_t n = (int64_t)rows * s->B;
-    if (n_elems != n) fail(MS_E_INVALID, "state size mismatch");
-    DeviceGuard dg(s->device);
-    std::vector<float> h(s->state_rows * s->B);
-    HIPCHECK(hipStreamSynchronize(s->stream));
-    HIPCHECK(hipMemcpy(h.data(), s->state, h.size() * 4, hipMemcpyDeviceToHost));
-    const int64_t r0 = s->plan->sig_offset[sig];
-    for (int32_t b = 0; b < s->B; ++b)
-      for (int32_t r = 0; r < rows; ++r) h[(size_t)((r0 + r) * s->S.rs + b * s->S.cs)] = in[(size_t)b * rows + r];
-    HIPCHECK(hipMemcpy(s->state, h.data(), h.size() * 4, hipMemcpyHostToDevice));
+    if (n_elems != (int64_t)s->plan->ir.sigs[sig].rows * s->B) fail(MS_E_INVALID, "state size mismatch");
+    state_copy(s, sig, const_cast<float*>(in), true);
   });
 }
 

@@ -35,3 +35,37 @@ def unpaired_flips(got, exp):
         return a & m
     return int(np.count_nonzero(only_g & ~near(only_g, only_e)) +
                np.count_nonzero(only_e & ~near(only_e, only_g)))
+
+
+def lif_rate_inverse_ok(got, exp, J, scale, amp, tau_rc, tau_ref, rtol=1e-5):
+    """Backward-error check of a rate-mode neuron probe.
+
+    The rate r(J) has an unbounded slope at threshold (J -> 1+), and a neuron
+    whose intercept is close to the radius has a very large gain, so float32
+    rounding of J alone can move such a neuron's rate far beyond any forward
+    tolerance.  An element passes if it is within rtol * max|exp| of the oracle
+    (forward) or if it lies between amp*r(J - dJ) and amp*r(J + dJ) widened by
+    rtol * max|exp|, with dJ = rtol * scale: the GPU value is then the exact
+    rate of an input current that agrees with the oracle's to rtol relative to
+    the size of the current's terms.  Returns (n_forward_fail, n_fail)."""
+    from oracle.neurons import lif_rate
+    got = np.asarray(got, np.float64)
+    exp = np.asarray(exp, np.float64)
+    tol = rtol * max(np.abs(exp).max(initial=0.0), 1e-30)
+    fwd = np.abs(got - exp) <= tol
+    dJ = rtol * scale
+    lo = amp * lif_rate(J - dJ, tau_rc, tau_ref) - tol
+    hi = amp * lif_rate(J + dJ, tau_rc, tau_ref) + tol
+    ok = fwd | ((got >= lo) & (got <= hi))
+    return int((~fwd).sum()), int((~ok).sum())
+
+
+def lif_rate_spread(J, scale, amp, tau_rc, tau_ref, rtol=1e-5):
+    """Largest change of amp*r(J) over currents within rtol*scale of J: the part
+    of a rate neuron's output that float32 evaluation of its input current
+    leaves undetermined (see lif_rate_inverse_ok)."""
+    from oracle.neurons import lif_rate
+    r0 = lif_rate(J, tau_rc, tau_ref)
+    up = lif_rate(J + rtol * scale, tau_rc, tau_ref) - r0
+    dn = r0 - lif_rate(J - rtol * scale, tau_rc, tau_ref)
+    return amp * np.maximum(up, dn)

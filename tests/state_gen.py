@@ -18,13 +18,18 @@ def random_state(spec, B, seed):
     for ci, c in enumerate(spec.connections):
         if c.synapse is None:
             continue
-        if c.post_slice is not None:
-            w = c.post_slice[1] - c.post_slice[0]
-        elif c.post[0] == "node":
-            w = spec.nodes[c.post[1]].size
-        elif c.post[0] == "ens":
-            w = spec.ensembles[c.post[1]].dims
-        else:
-            w = spec.ensembles[c.post[1]].n_neurons
+        w = post_width(spec, c)
         st["y"][ci] = (0.3 * rng.standard_normal((B, w))).astype(np.float32)
     return st
+
+
+def post_width(spec, c):
+    """Width of the signal a connection writes into (its synapse state)."""
+    if c.post_slice is not None:
+        return c.post_slice[1] - c.post_slice[0]
+    kind, i = c.post
+    if kind == "node":
+        return spec.nodes[i].size
+    if kind == "ens":
+        return spec.ensembles[i].dims
+    return spec.ensembles[i].n_neurons

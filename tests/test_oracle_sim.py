@@ -227,3 +227,43 @@ def test_integrator_tracks_integral_with_neurons():
     t = np.arange(1, 1001) * DT
     target = 0.5 / (2 * np.pi) * (1 - np.cos(2 * np.pi * t))
     assert np.sqrt(np.mean((x - target) ** 2)) < 0.05
+
+
+def test_recorded_current_reproduces_rate_probe():
+    """The recorded input current J gives back the rate probe through the
+    closed-form rate, and the term scale bounds |J|."""
+    from oracle.neurons import lif_rate
+    from synth import make_workload
+    w = make_workload("c2", neuron_type="lif_rate", n_steps=20, minibatch=2, n_neurons=20,
+                      n_eval=100)
+    sim = OracleSim(w.spec, minibatch=2, record_current=(0, 1))
+    sim.run_steps(20, w.feeds)
+    for pi, p in enumerate(w.spec.probes):
+        if p.target[0] != "neurons":
+            continue
+        e = w.spec.ensembles[p.target[1]]
+        J, S = sim.current_data(p.target[1])
+        assert J.shape == sim.data(pi).shape
+        np.testing.assert_array_equal(sim.data(pi), e.amplitude * lif_rate(J, e.tau_rc, e.tau_ref))
+        assert np.all(S >= np.abs(J) * (1 - 1e-12))
+        assert (J > 1).any() and (J <= 1).any()
+
+
+def test_rate_backward_check_accepts_oracle_and_rejects_offsets():
+    """The backward-error check passes the oracle against itself and fails a
+    probe whose rates come from currents shifted well beyond the bound."""
+    from oracle.neurons import lif_rate
+    from synth import make_workload
+    from tests.parity import lif_rate_inverse_ok
+    w = make_workload("c2", neuron_type="lif_rate", n_steps=20, minibatch=2, n_neurons=20,
+                      n_eval=100)
+    sim = OracleSim(w.spec, minibatch=2, record_current=(0,))
+    sim.run_steps(20, w.feeds)
+    pi = next(i for i, p in enumerate(w.spec.probes) if p.target == ("neurons", 0))
+    e = w.spec.ensembles[0]
+    J, S = sim.current_data(0)
+    exp = sim.data(pi)
+    assert lif_rate_inverse_ok(exp, exp, J, S, e.amplitude, e.tau_rc, e.tau_ref) == (0, 0)
+    off = e.amplitude * lif_rate(J + 1e-3 * S, e.tau_rc, e.tau_ref)
+    nf, bad = lif_rate_inverse_ok(off, exp, J, S, e.amplitude, e.tau_rc, e.tau_ref)
+    assert bad > 0
