@@ -250,6 +250,30 @@ __host__ __device__ __forceinline__ int dec_bucket(int n) {
   return n <= 0 ? 0 : n <= 1 ? 1 : n <= 2 ? 2 : n <= 4 ? 4 : n <= 8 ? 8 : 16;
 }
 
+// Ensemble inputs up to this many dimensions are held in registers for the
+// whole neuron loop (they would otherwise be re-read for every neuron, since
+// the loop stores state through the same pointer).
+constexpr int kMaxXReg = 16;
+
+__device__ __forceinline__ void load_input(float (&xr)[kMaxXReg], const float* st, const Strides& S, int32_t x,
+                                           int64_t b, int d) {
+#pragma unroll
+  for (int k = 0; k < kMaxXReg; ++k) xr[k] = k < d ? st[at(S, x + k, b)] : 0.0f;
+}
+
+// J = bias + sum_k enc[k] x[k], accumulated in order k = 0..d-1.
+__device__ __forceinline__ float input_current(float j, gptr<float> enc, const float (&xr)[kMaxXReg],
+                                               const float* st, const Strides& S, int32_t x, int64_t b, int d) {
+  if (d <= kMaxXReg) {
+#pragma unroll
+    for (int k = 0; k < kMaxXReg; ++k)
+      if (k < d) j += enc[k] * xr[k];
+  } else {
+    for (int k = 0; k < d; ++k) j += enc[k] * st[at(S, x + k, b)];
+  }
+  return j;
+}
+
 // One fused op, one batch column, processed by one wavefront (lanes over
 // neurons); NDEC >= total decoded outputs (extra slots repeat the last row and
 // are never stored).  The decoded outputs are reduced across the wavefront
@@ -379,22 +403,65 @@ __global__ void k_lowpass(float* st, Strides S, int32_t B, int64_t rows, Opnd y,
   lowpass_item(st, S, _r, _b, y, v, fp);
 }
 
-// Fused ensembles, small minibatch: one workgroup per op; each wavefront takes
-// batch columns in turn (lanes over neurons).
-__global__ void __launch_bounds__(256) k_ens_rows(float* st, Strides S, int32_t B, EnsDesc E, float dt) {
+// Fused ensembles, small minibatch: one workgroup of 256 threads per (op,
+// batch column); threads over neurons.  Decoded partial sums are reduced
+// within each wavefront, then across the four wavefronts in LDS.
+template <int NDEC>
+__device__ __forceinline__ void ens_wg_t(float* st, const Strides& S, const EnsDesc& E, float dt,
+                                         float (*red)[kMaxDec]) {
   const int op = blockIdx.x;
-  const int lane = threadIdx.x % 64, wave = threadIdx.x / 64, nw = blockDim.x / 64;
-  for (int64_t b = wave; b < B; b += nw) ens_op_wave(st, S, b, E, op, lane, dt);
+  const int64_t b = blockIdx.y;
+  const int lane = threadIdx.x % 64, wave = threadIdx.x / 64;
+  const EnsOp o = load_op(E.ops, op);
+  const int d = E.d, ndec = E.ndec, df0 = E.df[0];
+  gptr<float> enc = G(E.enc) + (int64_t)o.enc * d;
+  gptr<float> bias = G(E.bias) + o.bias;
+  gptr<float> D0 = G(E.D[0]) + (int64_t)o.D[0] * E.Dcols[0];
+  gptr<float> D1 = G(E.D[E.nf > 1 ? 1 : 0]) + (int64_t)o.D[E.nf > 1 ? 1 : 0] * E.Dcols[E.nf > 1 ? 1 : 0];
+  const int64_t s0 = E.Dcols[0], s1 = E.Dcols[E.nf > 1 ? 1 : 0];
+  float acc[NDEC > 0 ? NDEC : 1];
+#pragma unroll
+  for (int q = 0; q < NDEC; ++q) acc[q] = 0.0f;
+  float xr[kMaxXReg];
+  load_input(xr, st, S, o.x, b, d);
+  for (int r = threadIdx.x; r < o.n; r += 256) {
+    const float j = input_current(bias[r], enc + (int64_t)r * d, xr, st, S, o.x, b, d);
+    float v = 0.0f, rf = 0.0f;
+    if (E.ntype == 0) { v = st[at(S, o.V + r, b)]; rf = st[at(S, o.ref + r, b)]; }
+    const float sp = neuron_update(E.ntype, j, v, rf, o.tau_rc, o.tau_ref, o.amp, o.full, dt, o.inv_tau);
+    if (E.ntype == 0) { st[at(S, o.V + r, b)] = v; st[at(S, o.ref + r, b)] = rf; }
+    if (o.s >= 0) st[at(S, o.s + r, b)] = sp;
+#pragma unroll
+    for (int q = 0; q < NDEC; ++q) {
+      const int qq = q < ndec ? q : ndec - 1;
+      gptr<float> row = qq < df0 ? D0 + (int64_t)qq * s0 : D1 + (int64_t)(qq - df0) * s1;
+      acc[q] += row[r] * sp;
+    }
+  }
+#pragma unroll
+  for (int q = 0; q < NDEC; ++q) {
+    const float t = wave_sum(acc[q]);
+    if (lane == 0) red[wave][q] = t;
+  }
+  __syncthreads();
+  const int q = threadIdx.x;
+  if (q < ndec) {
+    const float t = red[0][q] + red[1][q] + red[2][q] + red[3][q];
+    const int dr = q < df0 ? o.d[0] + q : o.d[1] + (q - df0);
+    st[at(S, dr, b)] = t;
+  }
 }
 
-// Fused ensembles, one wavefront per (op, batch column); for mid-size batches
-// and single-column ops with many neurons the grid covers ops x B wavefronts.
-__global__ void __launch_bounds__(256) k_ens_waves(float* st, Strides S, int32_t B, int32_t nops, EnsDesc E,
-                                                   float dt) {
-  const int64_t w = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) / 64;
-  const int lane = threadIdx.x % 64;
-  if (w >= (int64_t)nops * B) return;
-  ens_op_wave(st, S, w % B, E, (int)(w / B), lane, dt);
+__global__ void __launch_bounds__(256) k_ens_wg(float* st, Strides S, EnsDesc E, float dt) {
+  __shared__ float red[4][kMaxDec];
+  switch (dec_bucket(E.ndec)) {
+    case 0: ens_wg_t<0>(st, S, E, dt, red); break;
+    case 1: ens_wg_t<1>(st, S, E, dt, red); break;
+    case 2: ens_wg_t<2>(st, S, E, dt, red); break;
+    case 4: ens_wg_t<4>(st, S, E, dt, red); break;
+    case 8: ens_wg_t<8>(st, S, E, dt, red); break;
+    default: ens_wg_t<16>(st, S, E, dt, red); break;
+  }
 }
 
 // Fused ensembles, large minibatch: one workgroup (4 wavefronts) per (op, tile

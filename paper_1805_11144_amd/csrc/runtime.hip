@@ -371,9 +371,7 @@ void launch_group(ms_sim* s, const Launch& l) {
         hipLaunchKernelGGL(k_ens_tile, dim3((unsigned)l.rows, (unsigned)((B + 63) / 64)), dim3(256), 0, q, st, S,
                            B, l.ens, s->dt);
       } else {
-        const int64_t waves = l.rows * B;
-        hipLaunchKernelGGL(k_ens_waves, dim3((unsigned)((waves + 3) / 4)), dim3(256), 0, q, st, S, B,
-                           (int32_t)l.rows, l.ens, s->dt);
+        hipLaunchKernelGGL(k_ens_wg, dim3((unsigned)l.rows, (unsigned)B), dim3(256), 0, q, st, S, l.ens, s->dt);
       }
       break;
     default: fail(MS_E_INVALID, "unknown group type");
