@@ -222,6 +222,36 @@ struct Plan {
   std::vector<int32_t> probe_width;
 };
 
+// ------------------------------------------------- stage-major (window) schedule
+// A model whose operators form no cycle once every synapse update is taken as
+// an edge from one step to the next (feedforward chains and layers; every
+// recurrence is an element's own state: neuron voltage/refractory time, a
+// filter's output) can run stage by stage: each merged group over a whole
+// window of timesteps before the groups that depend on it.  Signals read by
+// other operators are then stored once per step of the window ("versioned":
+// [rows][(W+1)*B], block 0 holding the value carried in from the previous
+// window, block t+1 the value of window step t); neuron state stays in a
+// private [rows][B] array.
+struct WPhase {
+  LGroup g;               // lowered with window row numbering
+  int32_t level = 0;
+  int32_t src_blk = 1;    // src rows: 1 = this step's value, 0 = the previous step's
+  int32_t a_blk = 1;      // the same for a batched ElementwiseInc `a`
+};
+
+struct WindowPlan {
+  bool ok = false;
+  std::string why;                   // why the model cannot run stage by stage
+  std::vector<int64_t> sig_row;      // per signal: row in its window array (parameters: row in their base)
+  std::vector<char> priv;            // per signal: in the private array
+  int64_t rows_v = 0, rows_p = 0;
+  int32_t levels = 0;
+  std::vector<WPhase> phases;        // execution order
+  std::vector<int32_t> probe_rows;   // versioned rows of the probe sources, probe-row order
+};
+
+WindowPlan make_window_plan(const Plan& p);
+
 std::unique_ptr<Plan> make_plan(const Model& m, double dt, const PlanOpts& o);
 std::string plan_to_json(const Plan& p);
 

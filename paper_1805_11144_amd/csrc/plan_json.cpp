@@ -35,6 +35,64 @@ void joperand(std::ostringstream& o, const LOperand& x) {
   o << '}';
 }
 
+void jgroup(std::ostringstream& o, const Plan& p, const LGroup& L) {
+  const IR& ir = p.ir;
+  o << "{\"type\":";
+  jstr(o, op_type_name(L.type));
+  o << ",\"key\":" << p.key_of_op[L.ops[0]] << ",\"ops\":[";
+  for (size_t k = 0; k < L.ops.size(); ++k) {
+    if (k) o << ',';
+    jstr(o, ir.ops[L.ops[k]].name);
+  }
+  o << "],\"rows\":" << L.rows;
+  if (L.type == OP_ENS) {
+    o << ",\"d\":" << L.ens_d << ",\"neuron\":" << L.ens_type << ",\"enc_base\":" << L.a.base
+      << ",\"bias_base\":" << L.ens_bias_base << ",\"D_base\":";
+    jarr(o, L.ens_Dbase);
+    o << ",\"n\":";
+    jarr(o, L.ens_n);
+    o << ",\"x_row\":"; jarr(o, L.ens_x);
+    o << ",\"enc_row\":"; jarr(o, L.ens_enc);
+    o << ",\"bias_row\":"; jarr(o, L.ens_bias);
+    o << ",\"V_row\":"; jarr(o, L.ens_V);
+    o << ",\"ref_row\":"; jarr(o, L.ens_ref);
+    o << ",\"s_row\":"; jarr(o, L.ens_s);
+    o << ",\"df\":"; jarr(o, L.ens_df);
+    o << ",\"D_row\":[";
+    for (size_t k = 0; k < L.ens_D.size(); ++k) { if (k) o << ','; jarr(o, L.ens_D[k]); }
+    o << "],\"d_row\":[";
+    for (size_t k = 0; k < L.ens_dd.size(); ++k) { if (k) o << ','; jarr(o, L.ens_dd[k]); }
+    o << ']';
+    o << ",\"tau_rc\":"; jarr(o, L.tau_rc);
+    o << ",\"tau_ref\":"; jarr(o, L.tau_ref);
+    o << ",\"amp\":"; jarr(o, L.amp);
+  } else if (L.type == OP_DOT_INC) {
+    o << ",\"M\":" << L.M << ",\"K\":" << L.K << ",\"w_row\":";
+    jarr(o, L.w_row);
+    o << ",\"x_row\":";
+    jarr(o, L.x_row);
+    o << ",\"d_row\":";
+    jarr(o, L.d_row);
+  } else {
+    o << ",\"dst\":";
+    joperand(o, L.dst);
+    if (L.src.base >= 0) { o << ",\"src\":"; joperand(o, L.src); }
+    if (L.a.base >= 0) { o << ",\"a\":"; joperand(o, L.a); }
+    if (L.V.base >= 0) { o << ",\"V\":"; joperand(o, L.V); }
+    if (L.ref.base >= 0) { o << ",\"ref\":"; joperand(o, L.ref); }
+    if (!L.ptr.empty()) { o << ",\"ptr\":"; jarr(o, L.ptr); }
+    if (!L.feed_rows.empty()) { o << ",\"feed_rows\":"; jarr(o, L.feed_rows); }
+    if (!L.values.empty()) { o << ",\"values\":"; jarr(o, L.values); }
+    if (!L.tau_rc.empty()) {
+      o << ",\"tau_rc\":"; jarr(o, L.tau_rc);
+      o << ",\"tau_ref\":"; jarr(o, L.tau_ref);
+      o << ",\"amp\":"; jarr(o, L.amp);
+    }
+    if (!L.ca.empty()) { o << ",\"ca\":"; jarr(o, L.ca); o << ",\"cb\":"; jarr(o, L.cb); }
+  }
+  o << '}';
+}
+
 }  // namespace
 
 std::string plan_to_json(const Plan& p) {
@@ -58,68 +116,37 @@ std::string plan_to_json(const Plan& p) {
   }
   o << "],\"groups\":[";
   for (size_t g = 0; g < p.lowered.size(); ++g) {
-    const LGroup& L = p.lowered[g];
     if (g) o << ',';
-    o << "{\"type\":";
-    jstr(o, op_type_name(L.type));
-    o << ",\"key\":" << p.key_of_op[L.ops[0]] << ",\"ops\":[";
-    for (size_t k = 0; k < L.ops.size(); ++k) {
-      if (k) o << ',';
-      jstr(o, ir.ops[L.ops[k]].name);
-    }
-    o << "],\"rows\":" << L.rows;
-    if (L.type == OP_ENS) {
-      o << ",\"d\":" << L.ens_d << ",\"neuron\":" << L.ens_type << ",\"enc_base\":" << L.a.base
-        << ",\"bias_base\":" << L.ens_bias_base << ",\"D_base\":";
-      jarr(o, L.ens_Dbase);
-      o << ",\"n\":";
-      jarr(o, L.ens_n);
-      o << ",\"x_row\":"; jarr(o, L.ens_x);
-      o << ",\"enc_row\":"; jarr(o, L.ens_enc);
-      o << ",\"bias_row\":"; jarr(o, L.ens_bias);
-      o << ",\"V_row\":"; jarr(o, L.ens_V);
-      o << ",\"ref_row\":"; jarr(o, L.ens_ref);
-      o << ",\"s_row\":"; jarr(o, L.ens_s);
-      o << ",\"df\":"; jarr(o, L.ens_df);
-      o << ",\"D_row\":[";
-      for (size_t k = 0; k < L.ens_D.size(); ++k) { if (k) o << ','; jarr(o, L.ens_D[k]); }
-      o << "],\"d_row\":[";
-      for (size_t k = 0; k < L.ens_dd.size(); ++k) { if (k) o << ','; jarr(o, L.ens_dd[k]); }
-      o << ']';
-      o << ",\"tau_rc\":"; jarr(o, L.tau_rc);
-      o << ",\"tau_ref\":"; jarr(o, L.tau_ref);
-      o << ",\"amp\":"; jarr(o, L.amp);
-    } else if (L.type == OP_DOT_INC) {
-      o << ",\"M\":" << L.M << ",\"K\":" << L.K << ",\"w_row\":";
-      jarr(o, L.w_row);
-      o << ",\"x_row\":";
-      jarr(o, L.x_row);
-      o << ",\"d_row\":";
-      jarr(o, L.d_row);
-    } else {
-      o << ",\"dst\":";
-      joperand(o, L.dst);
-      if (L.src.base >= 0) { o << ",\"src\":"; joperand(o, L.src); }
-      if (L.a.base >= 0) { o << ",\"a\":"; joperand(o, L.a); }
-      if (L.V.base >= 0) { o << ",\"V\":"; joperand(o, L.V); }
-      if (L.ref.base >= 0) { o << ",\"ref\":"; joperand(o, L.ref); }
-      if (!L.ptr.empty()) { o << ",\"ptr\":"; jarr(o, L.ptr); }
-      if (!L.feed_rows.empty()) { o << ",\"feed_rows\":"; jarr(o, L.feed_rows); }
-      if (!L.values.empty()) { o << ",\"values\":"; jarr(o, L.values); }
-      if (!L.tau_rc.empty()) {
-        o << ",\"tau_rc\":"; jarr(o, L.tau_rc);
-        o << ",\"tau_ref\":"; jarr(o, L.tau_ref);
-        o << ",\"amp\":"; jarr(o, L.amp);
-      }
-      if (!L.ca.empty()) { o << ",\"ca\":"; jarr(o, L.ca); o << ",\"cb\":"; jarr(o, L.cb); }
-    }
-    o << '}';
+    jgroup(o, p, p.lowered[g]);
   }
   o << "],\"probe_rows\":";
   jarr(o, p.probe_src_rows);
   o << ",\"probe_offsets\":";
   jarr(o, p.probe_row_offset);
-  o << ",\"feed_rows\":" << ir.feed_rows << '}';
+  o << ",\"feed_rows\":" << ir.feed_rows;
+  const WindowPlan w = make_window_plan(p);
+  o << ",\"window\":{\"ok\":" << (w.ok ? "true" : "false") << ",\"why\":";
+  jstr(o, w.why);
+  if (w.ok) {
+    o << ",\"levels\":" << w.levels << ",\"rows_v\":" << w.rows_v << ",\"rows_p\":" << w.rows_p
+      << ",\"sig_row\":";
+    jarr(o, w.sig_row);
+    std::vector<int> pv(w.priv.begin(), w.priv.end());
+    o << ",\"priv\":";
+    jarr(o, pv);
+    o << ",\"probe_rows\":";
+    jarr(o, w.probe_rows);
+    o << ",\"phases\":[";
+    for (size_t k = 0; k < w.phases.size(); ++k) {
+      if (k) o << ',';
+      o << "{\"level\":" << w.phases[k].level << ",\"src_blk\":" << w.phases[k].src_blk
+        << ",\"a_blk\":" << w.phases[k].a_blk << ",\"group\":";
+      jgroup(o, p, w.phases[k].g);
+      o << '}';
+    }
+    o << ']';
+  }
+  o << "}}";
   return o.str();
 }
 

@@ -477,12 +477,13 @@ std::vector<float> uniform_or_rows(const std::vector<T>& v) {
   return out;
 }
 
-LGroup lower_group(const Plan& p, const std::vector<int32_t>& ops) {
-  const IR& ir = p.ir;
+// Lowers the operators `ops` of one merged group to row lists, with signal rows
+// taken from `sig_offset` (row of each signal's first element in its base).
+LGroup lower_group_at(const IR& ir, const std::vector<int64_t>& sig_offset, const std::vector<int32_t>& ops) {
   LGroup g;
   g.type = ir.ops[ops[0]].type;
   g.ops = ops;
-  auto row = [&](const SRef& r, int32_t i) { return (int32_t)(p.sig_offset[r.sig] + r.start + i); };
+  auto row = [&](const SRef& r, int32_t i) { return (int32_t)(sig_offset[r.sig] + r.start + i); };
   auto base = [&](const SRef& r) { return ir.sigs[r.sig].base; };
   const Op& f = ir.ops[ops[0]];
   switch (g.type) {
@@ -570,7 +571,7 @@ LGroup lower_group(const Plan& p, const std::vector<int32_t>& ops) {
       std::set<int32_t> dsts;
       for (int32_t oi : ops) {
         const Op& o = ir.ops[oi];
-        g.w_row.push_back((int32_t)p.sig_offset[o.a.sig] + o.a.start);
+        g.w_row.push_back((int32_t)sig_offset[o.a.sig] + o.a.start);
         g.x_row.push_back(row(o.src, 0));
         g.d_row.push_back(row(o.dst, 0));
         if (!dsts.insert(o.dst.sig).second) fail(MS_E_INVALID, "DotInc group with repeated destination");
@@ -632,13 +633,13 @@ LGroup lower_group(const Plan& p, const std::vector<int32_t>& ops) {
         const Op& o = ir.ops[oi];
         g.ens_n.push_back(o.n);
         g.ens_x.push_back(o.src.sig >= 0 ? row(o.src, 0) : -1);
-        g.ens_enc.push_back(o.a.sig >= 0 ? (int32_t)p.sig_offset[o.a.sig] : -1);
+        g.ens_enc.push_back(o.a.sig >= 0 ? (int32_t)sig_offset[o.a.sig] : -1);
         g.ens_bias.push_back(row(o.bias, 0));
         g.ens_V.push_back(o.V.sig >= 0 ? row(o.V, 0) : -1);
         g.ens_ref.push_back(o.ref.sig >= 0 ? row(o.ref, 0) : -1);
         g.ens_s.push_back(o.dst.sig >= 0 ? row(o.dst, 0) : -1);
         for (size_t k = 0; k < o.decs.size(); ++k) {
-          g.ens_D[k].push_back((int32_t)p.sig_offset[o.decs[k].first.sig]);
+          g.ens_D[k].push_back((int32_t)sig_offset[o.decs[k].first.sig]);
           g.ens_dd[k].push_back(row(o.decs[k].second, 0));
         }
         trc.push_back(o.tau_rc); tref.push_back(o.tau_ref); amp.push_back(o.amp);
@@ -658,7 +659,128 @@ LGroup lower_group(const Plan& p, const std::vector<int32_t>& ops) {
   return g;
 }
 
+LGroup lower_group(const Plan& p, const std::vector<int32_t>& ops) { return lower_group_at(p.ir, p.sig_offset, ops); }
+
 }  // namespace
+
+// Stage-major schedule.  Per batched signal: the operators that set it run
+// before those that increment it, which run before those that read it (all
+// within a step); a signal that is updated (filter output) is read as the
+// previous step's value, so its updater runs, for the whole window, before its
+// readers.  Levels are longest paths in that graph; each level's operators run
+// as the plan's merged groups restricted to the level.
+WindowPlan make_window_plan(const Plan& p) {
+  const IR& ir = p.ir;
+  WindowPlan w;
+  const int32_t no = (int32_t)ir.ops.size(), ns = (int32_t)ir.sigs.size();
+  auto batched = [&](int32_t sg) { return sg >= 0 && ir.sigs[sg].cls == SC_BATCHED; };
+  std::vector<std::vector<int32_t>> S(ns), I(ns), R(ns), U(ns);
+  std::vector<int32_t> s_, i_, r_, u_;
+  for (int32_t k = 0; k < no; ++k) {
+    access(ir.ops[k], s_, i_, r_, u_);
+    const std::vector<int32_t>* src[4] = {&s_, &i_, &r_, &u_};
+    std::vector<std::vector<int32_t>>* dst[4] = {&S, &I, &R, &U};
+    for (int l = 0; l < 4; ++l)
+      for (int32_t sg : *src[l])
+        if (batched(sg)) {
+          auto& v = (*dst[l])[sg];
+          if (v.empty() || v.back() != k) v.push_back(k);
+        }
+  }
+  w.priv.assign(ns, 0);
+  for (const Op& o : ir.ops)
+    if ((o.type == OP_LIF || o.type == OP_ENS) && o.V.sig >= 0) { w.priv[o.V.sig] = 1; w.priv[o.ref.sig] = 1; }
+  auto refuse = [&](const std::string& why) { w.ok = false; w.why = why; return w; };
+  for (int32_t sg = 0; sg < ns; ++sg) {
+    if (!batched(sg)) continue;
+    if (w.priv[sg]) {
+      if (U[sg].size() != 1 || !S[sg].empty() || !I[sg].empty() || !R[sg].empty())
+        return refuse("neuron state " + ir.sigs[sg].name + " is accessed by other operators");
+      continue;
+    }
+    if (!U[sg].empty() && (!S[sg].empty() || !I[sg].empty() || U[sg].size() > 1))
+      return refuse("signal " + ir.sigs[sg].name + " is both updated and written");
+    if (U[sg].empty() && S[sg].empty() && !I[sg].empty())
+      return refuse("signal " + ir.sigs[sg].name + " accumulates across steps");
+  }
+  for (const auto& pr : ir.probes)
+    if (w.priv[pr.src.sig]) return refuse("a probe reads neuron state");
+  // graph: ops, then three ordering points per signal (after set, after
+  // increments, after update)
+  const int32_t nn = no + 3 * ns;
+  std::vector<std::vector<int32_t>> succ(nn);
+  for (int32_t sg = 0; sg < ns; ++sg) {
+    if (!batched(sg) || w.priv[sg]) continue;
+    const int32_t AS = no + 3 * sg, AI = AS + 1, AU = AS + 2;
+    for (int32_t k : S[sg]) succ[k].push_back(AS);
+    succ[AS].push_back(AI);
+    for (int32_t k : I[sg]) { succ[AS].push_back(k); succ[k].push_back(AI); }
+    if (!U[sg].empty()) {
+      for (int32_t k : U[sg]) succ[k].push_back(AU);
+      for (int32_t k : R[sg]) if (k != U[sg][0]) succ[AU].push_back(k);
+    } else {
+      for (int32_t k : R[sg]) succ[AI].push_back(k);
+    }
+  }
+  std::vector<int32_t> indeg(nn, 0), dist(nn, 0);
+  for (int32_t u = 0; u < nn; ++u) for (int32_t v : succ[u]) indeg[v]++;
+  std::vector<int32_t> q;
+  for (int32_t u = 0; u < nn; ++u) if (indeg[u] == 0) q.push_back(u);
+  size_t head = 0;
+  while (head < q.size()) {
+    const int32_t u = q[head++];
+    const int32_t fin = dist[u] + (u < no ? 1 : 0);
+    for (int32_t v : succ[u]) {
+      dist[v] = std::max(dist[v], fin);
+      if (--indeg[v] == 0) q.push_back(v);
+    }
+  }
+  if ((int32_t)q.size() != nn) return refuse("a cycle through synapse updates (recurrent connections)");
+  // window rows: batched signals in layout order, private ones in their own array
+  w.sig_row = p.sig_offset;
+  std::vector<int32_t> order;
+  for (int32_t sg = 0; sg < ns; ++sg) if (batched(sg)) order.push_back(sg);
+  std::stable_sort(order.begin(), order.end(), [&](int32_t a, int32_t b) { return p.sig_offset[a] < p.sig_offset[b]; });
+  for (int32_t sg : order) {
+    if (w.priv[sg]) { w.sig_row[sg] = w.rows_p; w.rows_p += ir.sigs[sg].rows; }
+    else { w.sig_row[sg] = w.rows_v; w.rows_v += ir.sigs[sg].rows; }
+  }
+  // phases
+  int32_t maxl = 0;
+  for (int32_t k = 0; k < no; ++k) maxl = std::max(maxl, dist[k]);
+  w.levels = no ? maxl + 1 : 0;
+  auto blk = [&](int32_t k, const SRef& r) {
+    if (!batched(r.sig) || w.priv[r.sig] || U[r.sig].empty()) return 1;
+    return U[r.sig][0] == k ? 1 : 0;
+  };
+  for (int32_t L = 0; L <= maxl && no; ++L) {
+    for (const auto& grp : p.groups) {
+      std::map<std::pair<int32_t, int32_t>, std::vector<int32_t>> parts;
+      std::vector<std::pair<int32_t, int32_t>> part_order;
+      for (int32_t k : grp) {
+        if (dist[k] != L) continue;
+        const Op& o = ir.ops[k];
+        const int32_t sb = o.src.sig >= 0 ? blk(k, o.src) : 1;
+        const int32_t ab = (o.type == OP_ELEM_INC && batched(o.a.sig)) ? blk(k, o.a) : 1;
+        auto key = std::make_pair(sb, ab);
+        if (!parts.count(key)) part_order.push_back(key);
+        parts[key].push_back(k);
+      }
+      for (const auto& key : part_order) {
+        WPhase ph;
+        ph.g = lower_group_at(ir, w.sig_row, parts[key]);
+        ph.level = L;
+        ph.src_blk = key.first;
+        ph.a_blk = key.second;
+        w.phases.push_back(std::move(ph));
+      }
+    }
+  }
+  for (const auto& pr : ir.probes)
+    for (int32_t i = 0; i < pr.src.len; ++i) w.probe_rows.push_back((int32_t)(w.sig_row[pr.src.sig] + pr.src.start + i));
+  w.ok = true;
+  return w;
+}
 
 std::unique_ptr<Plan> make_plan(const Model& m, double dt, const PlanOpts& o) {
   auto p = std::make_unique<Plan>();

@@ -93,15 +93,17 @@ class PlanExecutor:
                         arr[sg["offset"]:sg["offset"] + sg["rows"]] = v.reshape(sg["rows"], b["cols"])
                 self.bases.append(arr)
         if params_from is not None:
-            self._replace_constants(params_from)
+            self._replace_constants(params_from, self.j["groups"])
+            if self.j.get("window", {}).get("ok"):
+                self._replace_constants(params_from, [ph["group"] for ph in self.j["window"]["phases"]])
         self.rows = self.j["bases"][self.state_base]["rows"]
         self.fed = [i for i, n in enumerate(spec.nodes) if not n.passthrough and n.value is None]
         self.dt = spec.dt
         self.reset()
 
-    def _replace_constants(self, o):
+    def _replace_constants(self, o, groups):
         """Reset values, neuron parameters and filter coefficients from the oracle."""
-        for g in self.j["groups"]:
+        for g in groups:
             if g["type"] == "Reset" and "values" in g:
                 rows = {sg["name"]: sg["rows"] for sg in self.j["signals"]}
                 dst = {"reset": "out", "resetx": "x", "resetid": "did", "resetprod": "dprod",
@@ -145,101 +147,90 @@ class PlanExecutor:
         self.st = np.zeros((self.rows, self.B))
         self.records = []
 
-    def _src(self, base, rows):
+    def _src(self, arr, base, rows):
         if base == self.state_base:
-            return self.st[rows]
+            return arr[rows]
         return np.broadcast_to(self.bases[base][rows, 0][:, None], (len(rows), self.B))
 
     def step(self, feed_rows_values):
         st = self.st
         for g in self.j["groups"]:
-            t, n = g["type"], g["rows"]
-            if t == "Feed":
-                st[_rows(g["dst"], n)] = feed_rows_values[np.asarray(g["feed_rows"])]
-            elif t == "Reset":
-                d = _rows(g["dst"], n)
-                st[d] = _vec(g["values"], n)[:, None] if "values" in g else 0.0
-            elif t == "Copy":
-                st[_rows(g["dst"], n)] = self._src(g["src"]["base"], _rows(g["src"], n))
-            elif t in ("CopyInc", "ElementwiseInc"):
-                d = _rows(g["dst"], n)
-                if "ptr" in g:
-                    ptr = np.asarray(g["ptr"])
-                    m = ptr[-1]
-                    seg = np.repeat(np.arange(n), np.diff(ptr))
-                else:
-                    m = n
-                    seg = np.arange(n)
-                vals = self._src(g["src"]["base"], _rows(g["src"], m))
-                if t == "ElementwiseInc":
-                    vals = vals * self.bases[g["a"]["base"]][_rows(g["a"], m), 0][:, None]
-                acc = np.zeros((n, self.B))
-                np.add.at(acc, seg, vals)
-                st[d] += acc
-            elif t == "DotInc":
-                M, K = g["M"], g["K"]
-                # the weight base is found from the key of the group's first op via JSON
-                W = self.bases[self._weight_base(g)]
-                for w0, x0, d0 in zip(g["w_row"], g["x_row"], g["d_row"]):
-                    Wm = W[w0:w0 + M, :K] if W.shape[1] == K else W[w0:w0 + M * K, 0].reshape(M, K)
-                    st[d0:d0 + M] += Wm @ st[x0:x0 + K]
-            elif t in ("SimLIF", "SimLIFRate"):
-                J = st[_rows(g["src"], n)]
-                trc = _vec(g["tau_rc"], n)[:, None]
-                tref = _vec(g["tau_ref"], n)[:, None]
-                amp = _vec(g["amp"], n)[:, None]
-                if t == "SimLIFRate":
-                    out = np.zeros_like(J)
-                    m = J > 1
-                    r = np.zeros_like(J)
-                    r[m] = 1.0 / (np.broadcast_to(tref, J.shape)[m] +
-                                  np.broadcast_to(trc, J.shape)[m] * np.log1p(1.0 / (J[m] - 1.0)))
-                    out = amp * r
-                else:
-                    vr, rr = _rows(g["V"], n), _rows(g["ref"], n)
-                    V, ref = st[vr].copy(), st[rr].copy()
-                    dt = self.dt
-                    integ = np.clip(dt - ref, 0, dt)
-                    V = V - (J - V) * np.expm1(-integ / trc)
-                    ref = np.maximum(ref - dt, 0)
-                    spk = V > 1
-                    q = np.where(spk & (J > 1), (V - 1) / np.where(J > 1, J - 1, 1), 0.0)
-                    since = np.where(q >= 1, integ,
-                                     np.minimum(-trc * np.log1p(-np.minimum(q, 0.999999999999)), integ))
-                    since = np.where(spk & (J > 1), since, 0.0)
-                    st[vr] = np.where(spk, 0.0, np.maximum(V, 0.0))
-                    st[rr] = np.where(spk, tref - since, ref)
-                    out = np.where(spk, amp / dt, 0.0)
-                st[_rows(g["dst"], n)] = out
-            elif t == "Ensemble":
-                trc_all = _vec(g["tau_rc"], n); tref_all = _vec(g["tau_ref"], n)
-                amp_all = _vec(g["amp"], n)
-                for k in range(n):
-                    nn = g["n"][k]
-                    b0 = g["bias_row"][k]
-                    J = np.repeat(self.bases[g["bias_base"]][b0:b0 + nn, 0][:, None], self.B, axis=1)
-                    if g["x_row"][k] >= 0:
-                        d = g["d"]
-                        E = self.bases[g["enc_base"]][g["enc_row"][k]:g["enc_row"][k] + nn]
-                        J = J + E[:, :d] @ st[g["x_row"][k]:g["x_row"][k] + d]
-                    if g["neuron"] == 0:
-                        v0, r0 = g["V_row"][k], g["ref_row"][k]
-                        s_, st[v0:v0 + nn], st[r0:r0 + nn] = _lif(J, st[v0:v0 + nn].copy(),
-                                                                  st[r0:r0 + nn].copy(), self.dt,
-                                                                  trc_all[k], tref_all[k], amp_all[k])
-                    else:
-                        s_ = _rate(J, trc_all[k], tref_all[k], amp_all[k])
-                    if g["s_row"][k] >= 0:
-                        st[g["s_row"][k]:g["s_row"][k] + nn] = s_
-                    for f, df in enumerate(g["df"]):
-                        D = self.bases[g["D_base"][f]][g["D_row"][f][k]:g["D_row"][f][k] + df, :nn]
-                        st[g["d_row"][f][k]:g["d_row"][f][k] + df] = D @ s_
-            elif t == "Lowpass":
-                y, v = _rows(g["dst"], n), _rows(g["src"], n)
-                st[y] = _vec(g["ca"], n)[:, None] * st[y] + _vec(g["cb"], n)[:, None] * st[v]
-            else:
-                raise ValueError(t)
+            self.exec_group(g, st, st, st, st, feed_rows_values)
         self.records.append(st[np.asarray(self.j["probe_rows"], np.int64)].copy())
+
+    def exec_group(self, g, cur, src, prev, pa, feed_rows_values):
+        """One merged group for one step.  cur: this step's values (written);
+        src: where the group's batched inputs are read; prev: the previous
+        step's values (a filter's own output); pa: neuron state.  In the
+        time-major layout all four are the same array."""
+        t, n = g["type"], g["rows"]
+        if t == "Feed":
+            cur[_rows(g["dst"], n)] = feed_rows_values[np.asarray(g["feed_rows"])]
+        elif t == "Reset":
+            d = _rows(g["dst"], n)
+            cur[d] = _vec(g["values"], n)[:, None] if "values" in g else 0.0
+        elif t == "Copy":
+            cur[_rows(g["dst"], n)] = self._src(src, g["src"]["base"], _rows(g["src"], n))
+        elif t in ("CopyInc", "ElementwiseInc"):
+            d = _rows(g["dst"], n)
+            if "ptr" in g:
+                ptr = np.asarray(g["ptr"])
+                m = ptr[-1]
+                seg = np.repeat(np.arange(n), np.diff(ptr))
+            else:
+                m = n
+                seg = np.arange(n)
+            vals = self._src(src, g["src"]["base"], _rows(g["src"], m))
+            if t == "ElementwiseInc":
+                vals = vals * self.bases[g["a"]["base"]][_rows(g["a"], m), 0][:, None]
+            acc = np.zeros((n, self.B))
+            np.add.at(acc, seg, vals)
+            cur[d] += acc
+        elif t == "DotInc":
+            M, K = g["M"], g["K"]
+            W = self.bases[self._weight_base(g)]
+            for w0, x0, d0 in zip(g["w_row"], g["x_row"], g["d_row"]):
+                Wm = W[w0:w0 + M, :K] if W.shape[1] == K else W[w0:w0 + M * K, 0].reshape(M, K)
+                cur[d0:d0 + M] += Wm @ src[x0:x0 + K]
+        elif t in ("SimLIF", "SimLIFRate"):
+            J = src[_rows(g["src"], n)]
+            trc = _vec(g["tau_rc"], n)[:, None]
+            tref = _vec(g["tau_ref"], n)[:, None]
+            amp = _vec(g["amp"], n)[:, None]
+            if t == "SimLIFRate":
+                out = _rate(J, trc, tref, amp)
+            else:
+                vr, rr = _rows(g["V"], n), _rows(g["ref"], n)
+                out, pa[vr], pa[rr] = _lif(J, pa[vr].copy(), pa[rr].copy(), self.dt, trc, tref, amp)
+            cur[_rows(g["dst"], n)] = out
+        elif t == "Ensemble":
+            trc_all = _vec(g["tau_rc"], n); tref_all = _vec(g["tau_ref"], n)
+            amp_all = _vec(g["amp"], n)
+            for k in range(n):
+                nn = g["n"][k]
+                b0 = g["bias_row"][k]
+                J = np.repeat(self.bases[g["bias_base"]][b0:b0 + nn, 0][:, None], self.B, axis=1)
+                if g["x_row"][k] >= 0:
+                    d = g["d"]
+                    E = self.bases[g["enc_base"]][g["enc_row"][k]:g["enc_row"][k] + nn]
+                    J = J + E[:, :d] @ src[g["x_row"][k]:g["x_row"][k] + d]
+                if g["neuron"] == 0:
+                    v0, r0 = g["V_row"][k], g["ref_row"][k]
+                    s_, pa[v0:v0 + nn], pa[r0:r0 + nn] = _lif(J, pa[v0:v0 + nn].copy(),
+                                                              pa[r0:r0 + nn].copy(), self.dt,
+                                                              trc_all[k], tref_all[k], amp_all[k])
+                else:
+                    s_ = _rate(J, trc_all[k], tref_all[k], amp_all[k])
+                if g["s_row"][k] >= 0:
+                    cur[g["s_row"][k]:g["s_row"][k] + nn] = s_
+                for f, df in enumerate(g["df"]):
+                    D = self.bases[g["D_base"][f]][g["D_row"][f][k]:g["D_row"][f][k] + df, :nn]
+                    cur[g["d_row"][f][k]:g["d_row"][f][k] + df] = D @ s_
+        elif t == "Lowpass":
+            y, v = _rows(g["dst"], n), _rows(g["src"], n)
+            cur[y] = _vec(g["ca"], n)[:, None] * prev[y] + _vec(g["cb"], n)[:, None] * src[v]
+        else:
+            raise ValueError(t)
 
     def _weight_base(self, g):
         sigs = self.j["signals"]
@@ -268,3 +259,45 @@ class PlanExecutor:
         off = self.j["probe_offsets"]
         rec = np.stack(self.records, axis=0)        # [T, probe_rows, B]
         return np.transpose(rec[:, off[probe]:off[probe + 1], :], (2, 0, 1))
+
+
+class WindowExecutor(PlanExecutor):
+    """Runs the library's stage-major schedule (the plan's "window" section):
+    every phase over a whole window of steps before the next phase, with
+    versioned signals [rows][W+1][B] (block 0: carried in; block t+1: window
+    step t) and neuron state in a private [rows][B] array."""
+
+    def __init__(self, plan, spec, minibatch, window, params_from=None):
+        super().__init__(plan, spec, minibatch, params_from)
+        self.w = self.j["window"]
+        assert self.w["ok"], self.w["why"]
+        self.W = window
+        self.reset()
+
+    def reset(self):
+        super().reset()
+        if getattr(self, "w", None) is None:
+            return
+        self.va = np.zeros((self.w["rows_v"], self.W + 1, self.B))
+        self.pa = np.zeros((self.w["rows_p"], self.B))
+
+    def run(self, n_steps, feeds):
+        vals_all = []
+        for k in range(n_steps):
+            vals_all.append(np.concatenate([np.asarray(feeds[i][:, k, :], np.float64).T if i in feeds
+                                            else np.zeros((self.spec.nodes[i].size, self.B))
+                                            for i in self.fed], axis=0) if self.fed
+                            else np.zeros((0, self.B)))
+        pr = np.asarray(self.w["probe_rows"], np.int64)
+        t0 = 0
+        while t0 < n_steps:
+            tw = min(self.W, n_steps - t0)
+            for ph in self.w["phases"]:
+                g = ph["group"]
+                for t in range(tw):
+                    self.exec_group(g, self.va[:, t + 1], self.va[:, t + ph["src_blk"]], self.va[:, t],
+                                    self.pa, vals_all[t0 + t])
+            for t in range(tw):
+                self.records.append(self.va[pr, t + 1].copy())
+            self.va[:, 0] = self.va[:, tw]
+            t0 += tw
