@@ -107,7 +107,7 @@ def main():
     ap.add_argument("--steps", type=int, default=5)
     ap.add_argument("--warmup", type=int, default=2)
     ap.add_argument("--config", default="c2", choices=sorted(WORKLOADS))
-    ap.add_argument("--driver", default="auto", choices=["auto", "steps", "graph", "persistent"])
+    ap.add_argument("--driver", default="auto", choices=["auto", "steps", "graph", "persistent", "window"])
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-budget", type=float, default=15.0)
     args = ap.parse_args()
@@ -123,7 +123,7 @@ def main():
     w = make_workload(args.config)
     model = M.model_from_spec(w.spec)
     driver = {"auto": M.DRIVER_AUTO, "steps": M.DRIVER_STEPS, "graph": M.DRIVER_GRAPH,
-              "persistent": M.DRIVER_PERSISTENT}[args.driver]
+              "persistent": M.DRIVER_PERSISTENT, "window": M.DRIVER_WINDOW}[args.driver]
     dev = torch.device("cuda:0")
     t_build = time.perf_counter()
     sim = M.Simulator(model, minibatch=w.minibatch, driver=driver, unroll=20,
@@ -159,7 +159,7 @@ def main():
     roofline = {"bound": "hbm", "achieved": round(achieved_gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
                 "frac": round(achieved_gbs / HBM_PEAK_GBS, 4), "traffic": None,
                 "kernel": {1: "per-group kernels", 2: "per-group kernels (hipGraph)",
-                           3: "k_persistent"}.get(info["driver"], "?"),
+                           3: "k_persistent", 4: "stage-major window kernels"}.get(info["driver"], "?"),
                 "launch_ms": round(launch_ms, 4), "bytes_per_launch": int(bytes_run)}
     out = {
         "metric": "neuron-timesteps/sec (x minibatch) on 1 MI355X",
@@ -168,7 +168,7 @@ def main():
         "scaling": "weak", "vs_baseline": None, "dtype": "f32", "data": "synthetic",
         "config": {"workload": WORKLOADS[args.config], "name": args.config, "neurons": w.n_neurons,
                    "timesteps": w.n_steps, "minibatch": w.minibatch,
-                   "driver": {1: "steps", 2: "graph", 3: "persistent"}.get(info["driver"]),
+                   "driver": {1: "steps", 2: "graph", 3: "persistent", 4: "window"}.get(info["driver"]),
                    "groups_per_step": info["groups_per_step"], "build_s": round(t_build, 2)},
         "roofline": roofline,
     }

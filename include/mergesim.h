@@ -147,6 +147,14 @@ ms_status ms_model_add_probe(ms_model* model, const ms_probe_desc* desc, int32_t
 #define MS_DRIVER_GRAPH 2     /* hipGraph of `unroll` steps, replayed */
 #define MS_DRIVER_PERSISTENT 3 /* one launch per run: each workgroup owns batch
                                   columns and executes every group of every step */
+#define MS_DRIVER_WINDOW 4    /* stage-major: each merged group runs over a window of
+                                 steps before the groups that depend on it.  Only for
+                                 models with no recurrence other than each neuron's and
+                                 filter's own state (feedforward layers and chains; the
+                                 one-step synapse delay separates the stages); other
+                                 models get MS_E_INVALID with the reason.  Same results
+                                 as the time-major drivers: every operator still sees
+                                 exactly the values of its own step (Sec. 4.1). */
 
 typedef struct {
   double dt;                  /* seconds, default 0.001 */
@@ -250,8 +258,8 @@ ms_status ms_sim_set_state(ms_sim* sim, int32_t which, int32_t id, const float* 
  * stream around the simulation launches, excluding feed staging); ms. */
 ms_status ms_sim_last_run_ms(ms_sim* sim, double* ms_out);
 
-/* The driver actually used (MS_DRIVER_STEPS/GRAPH/PERSISTENT) and the number of
- * merged groups executed per step. */
+/* The driver actually used (MS_DRIVER_STEPS/GRAPH/PERSISTENT/WINDOW) and the
+ * number of merged groups executed per step (WINDOW: launches per window). */
 ms_status ms_sim_info(const ms_sim* sim, int32_t* driver_out, int32_t* groups_per_step_out);
 
 const char* ms_last_error(void);

@@ -5,9 +5,9 @@ behind a C ABI, declared in include/mergesim.h).  This package is the thin
 Python binding: argument marshalling only.
 """
 from .mergesim import (Model, Plan, Simulator, MergesimError, load_library, model_from_spec,
-                       DRIVER_AUTO, DRIVER_STEPS, DRIVER_GRAPH, DRIVER_PERSISTENT,
+                       DRIVER_AUTO, DRIVER_STEPS, DRIVER_GRAPH, DRIVER_PERSISTENT, DRIVER_WINDOW,
                        PLANNER_GREEDY, PLANNER_TREE)
 
 __all__ = ["Model", "Plan", "Simulator", "MergesimError", "load_library", "model_from_spec",
-           "DRIVER_AUTO", "DRIVER_STEPS", "DRIVER_GRAPH", "DRIVER_PERSISTENT",
+           "DRIVER_AUTO", "DRIVER_STEPS", "DRIVER_GRAPH", "DRIVER_PERSISTENT", "DRIVER_WINDOW",
            "PLANNER_GREEDY", "PLANNER_TREE"]

@@ -1,0 +1,256 @@
+// Stage-major (window) kernels: one launch runs a merged group for every step
+// of a window of T timesteps.
+//
+// Versioned signals live in `va`: element (row, block k, batch column b) at
+// va[row * vs + k * B + b] with vs = (W + 1) * B; block 0 holds the value
+// carried in from the previous window, block t + 1 the value of window step t.
+// An operand read at block offset `blk` = 1 sees this step's value, 0 the
+// previous step's (a filter output read before its update).  Neuron state
+// (voltage, refractory time) lives in `pa` as [rows][B].
+//
+// Groups without a recurrence (feeds, resets, copies, increments, products,
+// rate neurons) are time-parallel: one work item per (row, step, column), the
+// (step, column) pair flattened as c = t * B + b so that block t + blk of a row
+// is va[row * vs + blk * B + c].  Filters and spiking neurons carry their
+// state through the window in registers, one work item per (row, column).
+#pragma once
+
+#include "kernels.hpp"
+
+struct WView {
+  float* va;
+  int64_t vs;      // row stride of va, (W + 1) * B
+  int32_t B;
+  int32_t T;       // steps of this window
+};
+
+__device__ __forceinline__ int64_t vat(const WView& w, int64_t row, int64_t c) { return row * w.vs + c; }
+
+// Work item i of rows x (T * B): row and flattened (step, column) index.  The
+// host checks that rows * T * B fits in 32 bits.
+#define W_ITEM(rows)                                                           \
+  const uint32_t _i = blockIdx.x * blockDim.x + threadIdx.x;                   \
+  const uint32_t _tb = (uint32_t)w.T * (uint32_t)w.B;                          \
+  if (_i >= (uint32_t)(rows) * _tb) return;                                    \
+  const uint32_t _r = _i / _tb, _c = _i - _r * _tb;
+
+__device__ __forceinline__ float w_src(const WView& w, const float* param, int bcast, int64_t row, int blk,
+                                       uint32_t c) {
+  return bcast ? G(param)[row] : w.va[vat(w, row, (int64_t)blk * w.B + c)];
+}
+
+// node rows <- staged feed [step][feed_rows][B] at run step t0 + t
+__global__ void k_w_feed(WView w, int64_t rows, Opnd dst, const int32_t* feed_row, const float* stage,
+                         int32_t feed_rows, int64_t t0) {
+  W_ITEM(rows);
+  const uint32_t t = _c / (uint32_t)w.B, b = _c - t * (uint32_t)w.B;
+  w.va[vat(w, rowof(dst, _r), w.B + _c)] = stage[((t0 + t) * feed_rows + G(feed_row)[_r]) * w.B + b];
+}
+
+__global__ void k_w_reset(WView w, int64_t rows, Opnd dst, const float* values) {
+  W_ITEM(rows);
+  w.va[vat(w, rowof(dst, _r), w.B + _c)] = values ? G(values)[_r] : 0.0f;
+}
+
+__global__ void k_w_copy(WView w, int64_t rows, Opnd dst, const float* param, Opnd src, int bcast, int sblk) {
+  W_ITEM(rows);
+  w.va[vat(w, rowof(dst, _r), w.B + _c)] = w_src(w, param, bcast, rowof(src, _r), sblk, _c);
+}
+
+// dst += sum of the src entries of unique destination u (ptr == null: one entry)
+__global__ void k_w_copy_inc(WView w, int64_t rows, Opnd dst, const float* param, Opnd src, int bcast, int sblk,
+                             const int32_t* ptr) {
+  W_ITEM(rows);
+  const int64_t di = vat(w, rowof(dst, _r), w.B + _c);
+  float acc = w.va[di];
+  if (ptr) {
+    for (int32_t e = G(ptr)[_r]; e < G(ptr)[_r + 1]; ++e) acc += w_src(w, param, bcast, rowof(src, e), sblk, _c);
+  } else {
+    acc += w_src(w, param, bcast, rowof(src, _r), sblk, _c);
+  }
+  w.va[di] = acc;
+}
+
+// dst += a (.) x, entries grouped by destination as in k_w_copy_inc
+__global__ void k_w_elem_inc(WView w, int64_t rows, Opnd dst, const float* a_param, Opnd a, int a_bcast, int ablk,
+                             const float* x_param, Opnd x, int x_bcast, int xblk, const int32_t* ptr) {
+  W_ITEM(rows);
+  const int64_t di = vat(w, rowof(dst, _r), w.B + _c);
+  float acc = w.va[di];
+  if (ptr) {
+    for (int32_t e = G(ptr)[_r]; e < G(ptr)[_r + 1]; ++e)
+      acc += w_src(w, a_param, a_bcast, rowof(a, e), ablk, _c) * w_src(w, x_param, x_bcast, rowof(x, e), xblk, _c);
+  } else {
+    acc += w_src(w, a_param, a_bcast, rowof(a, _r), ablk, _c) * w_src(w, x_param, x_bcast, rowof(x, _r), xblk, _c);
+  }
+  w.va[di] = acc;
+}
+
+// dst[m] += W[m, :] . x for every op, output row and (step, column)
+__global__ void k_w_dot(WView w, int64_t nops, int32_t M, int32_t K, const float* Wt, const int32_t* w_row,
+                        const int32_t* x_row, const int32_t* d_row, int xblk) {
+  W_ITEM(nops * M);
+  const uint32_t op = _r / (uint32_t)M, m = _r - op * (uint32_t)M;
+  gptr<float> wr = G(Wt) + ((int64_t)G(w_row)[op] + m) * K;
+  const int64_t x0 = G(x_row)[op];
+  const int64_t xc = (int64_t)xblk * w.B + _c;
+  float acc = 0.0f;
+  for (int32_t k = 0; k < K; ++k) acc += wr[k] * w.va[vat(w, x0 + k, xc)];
+  w.va[vat(w, (int64_t)G(d_row)[op] + m, w.B + _c)] += acc;
+}
+
+__global__ void k_w_lif_rate(WView w, int64_t rows, Opnd J, Opnd s, NeuronParams np, int jblk) {
+  W_ITEM(rows);
+  const float tau_rc = np.tau_rc_r ? G(np.tau_rc_r)[_r] : np.tau_rc;
+  const float tau_ref = np.tau_ref_r ? G(np.tau_ref_r)[_r] : np.tau_ref;
+  const float amp = np.amp_r ? G(np.amp_r)[_r] : np.amp;
+  const float j = w.va[vat(w, rowof(J, _r), (int64_t)jblk * w.B + _c)];
+  float out = 0.0f;
+  if (j > 1.0f) out = amp / (tau_ref + tau_rc * log1pf(1.0f / (j - 1.0f)));
+  w.va[vat(w, rowof(s, _r), w.B + _c)] = out;
+}
+
+// Work item per (row, column): state carried through the window.
+#define W_ROWCOL(rows)                                                         \
+  const uint32_t _i = blockIdx.x * blockDim.x + threadIdx.x;                   \
+  if (_i >= (uint32_t)(rows) * (uint32_t)w.B) return;                          \
+  const uint32_t _r = _i / (uint32_t)w.B, _b = _i - _r * (uint32_t)w.B;
+
+__global__ void k_w_lif(WView w, int64_t rows, Opnd J, Opnd s, Opnd V, Opnd R, float* pa, NeuronParams np,
+                        float dt, int jblk) {
+  W_ROWCOL(rows);
+  const float tau_rc = np.tau_rc_r ? G(np.tau_rc_r)[_r] : np.tau_rc;
+  const float tau_ref = np.tau_ref_r ? G(np.tau_ref_r)[_r] : np.tau_ref;
+  const float amp = np.amp_r ? G(np.amp_r)[_r] : np.amp;
+  const float full = np.full_r ? G(np.full_r)[_r] : np.full;
+  const int64_t vi = rowof(V, _r) * w.B + _b, ri = rowof(R, _r) * w.B + _b;
+  float v = pa[vi], rf = pa[ri];
+  const int64_t jr = rowof(J, _r) * w.vs + (int64_t)jblk * w.B + _b;
+  const int64_t sr = rowof(s, _r) * w.vs + w.B + _b;
+  for (int32_t t = 0; t < w.T; ++t) {
+    const float j = w.va[jr + (int64_t)t * w.B];
+    w.va[sr + (int64_t)t * w.B] = neuron_update(0, j, v, rf, tau_rc, tau_ref, amp, full, dt, 1.0f / tau_rc);
+  }
+  pa[vi] = v;
+  pa[ri] = rf;
+}
+
+// y(t) = a y(t - 1) + b v(t) through the window; y(-1) is block 0
+__global__ void k_w_lowpass(WView w, int64_t rows, Opnd y, Opnd v, FilterParams fp, int vblk) {
+  W_ROWCOL(rows);
+  const float a = fp.a_r ? G(fp.a_r)[_r] : fp.a;
+  const float c = fp.b_r ? G(fp.b_r)[_r] : fp.b;
+  const int64_t yr = rowof(y, _r) * w.vs + _b;
+  const int64_t vr = rowof(v, _r) * w.vs + (int64_t)vblk * w.B + _b;
+  float yv = w.va[yr];
+  for (int32_t t = 0; t < w.T; ++t) {
+    yv = a * yv + c * w.va[vr + (int64_t)t * w.B];
+    w.va[yr + (int64_t)(t + 1) * w.B] = yv;
+  }
+}
+
+// probe buffer [step][probe_rows][B] <- block t + 1 of the probed rows
+__global__ void k_w_probe(WView w, const int32_t* src, int32_t probe_rows, float* buf, int64_t step0) {
+  W_ITEM(probe_rows);
+  const uint32_t t = _c / (uint32_t)w.B, b = _c - t * (uint32_t)w.B;
+  buf[((step0 + t) * probe_rows + _r) * w.B + b] = w.va[vat(w, G(src)[_r], w.B + _c)];
+}
+
+// block 0 <- block T for every row (the values the next window starts from)
+__global__ void k_w_carry(WView w, int64_t rows) {
+  W_ROWCOL(rows);
+  const int64_t r0 = (int64_t)_r * w.vs + _b;
+  w.va[r0] = w.va[r0 + (int64_t)w.T * w.B];
+}
+
+// ------------------------------------------------- fused ensembles over a window
+// One workgroup per (op, batch column); thread tid owns neurons tid + j*blockDim
+// (j < NPT), whose voltage, refractory time, bias and encoder row stay in
+// registers for the whole window.  The window is processed in sub-windows of
+// `ts_max` steps: the sub-window's inputs x are staged in LDS, every thread
+// advances its neurons through the sub-window and leaves their outputs in LDS
+// (no synchronisation between steps: a neuron depends only on its own past),
+// then the decoded outputs of all sub-window steps are formed as dot products
+// over the neurons and written, with the spikes if they are stored.
+template <int NPT>
+__global__ void __launch_bounds__(1024) k_w_ens(WView w, float* pa, EnsDesc E, float dt, int32_t nmax,
+                                                int32_t ts_max, int xblk) {
+  extern __shared__ float lds[];
+  const int op = blockIdx.x;
+  const int64_t b = blockIdx.y;
+  const int tid = threadIdx.x, nthr = blockDim.x;
+  const EnsOp o = load_op(E.ops, op);
+  const int d = o.x >= 0 ? E.d : 0, ndec = E.ndec, df0 = E.df[0];
+  float* X = lds;                          // [ts_max][d]
+  float* Sb = lds + (int64_t)ts_max * E.d;  // [ts_max][nmax]
+  gptr<float> enc = G(E.enc) + (int64_t)o.enc * E.d;
+  gptr<float> bias = G(E.bias) + o.bias;
+  gptr<float> D0 = G(E.D[0]) + (int64_t)o.D[0] * E.Dcols[0];
+  gptr<float> D1 = G(E.D[E.nf > 1 ? 1 : 0]) + (int64_t)o.D[E.nf > 1 ? 1 : 0] * E.Dcols[E.nf > 1 ? 1 : 0];
+  const int64_t s0 = E.Dcols[0], s1 = E.Dcols[E.nf > 1 ? 1 : 0];
+  const bool spiking = E.ntype == 0;
+  float v[NPT], rf[NPT], bj[NPT], er[NPT][kMaxXReg];
+#pragma unroll
+  for (int j = 0; j < NPT; ++j) {
+    const int r = tid + j * nthr;
+    const bool live = r < o.n;
+    v[j] = (live && spiking) ? pa[(o.V + r) * (int64_t)w.B + b] : 0.0f;
+    rf[j] = (live && spiking) ? pa[(o.ref + r) * (int64_t)w.B + b] : 0.0f;
+    bj[j] = live ? bias[r] : 0.0f;
+#pragma unroll
+    for (int k = 0; k < kMaxXReg; ++k) er[j][k] = (live && k < d) ? enc[(int64_t)r * E.d + k] : 0.0f;
+  }
+  for (int32_t t0 = 0; t0 < w.T; t0 += ts_max) {
+    const int ts = min(ts_max, w.T - t0);
+    for (int i = tid; i < ts * d; i += nthr) {
+      const int s = i / d, k = i - s * d;
+      X[s * E.d + k] = w.va[(int64_t)(o.x + k) * w.vs + (int64_t)(t0 + s + xblk) * w.B + b];
+    }
+    __syncthreads();
+#pragma unroll
+    for (int j = 0; j < NPT; ++j) {
+      const int r = tid + j * nthr;
+      if (r < o.n) {
+        for (int s = 0; s < ts; ++s) {
+          float jc = bj[j];
+          if (d <= kMaxXReg) {
+#pragma unroll
+            for (int k = 0; k < kMaxXReg; ++k)
+              if (k < d) jc += er[j][k] * X[s * E.d + k];
+          } else {
+            for (int k = 0; k < d; ++k) jc += enc[(int64_t)r * E.d + k] * X[s * E.d + k];
+          }
+          Sb[(int64_t)s * nmax + r] =
+              neuron_update(E.ntype, jc, v[j], rf[j], o.tau_rc, o.tau_ref, o.amp, o.full, dt, o.inv_tau);
+        }
+      }
+    }
+    __syncthreads();
+    for (int i = tid; i < ndec * ts; i += nthr) {
+      const int q = i / ts, s = i - q * ts;
+      gptr<float> row = q < df0 ? D0 + (int64_t)q * s0 : D1 + (int64_t)(q - df0) * s1;
+      const float* sp = Sb + (int64_t)s * nmax;
+      float acc = 0.0f;
+      for (int r = 0; r < o.n; ++r) acc += row[r] * sp[r];
+      const int dr = q < df0 ? o.d[0] + q : o.d[1] + (q - df0);
+      w.va[(int64_t)dr * w.vs + (int64_t)(t0 + s + 1) * w.B + b] = acc;
+    }
+    if (o.s >= 0) {
+      for (int i = tid; i < ts * o.n; i += nthr) {
+        const int s = i / o.n, r = i - s * o.n;
+        w.va[(int64_t)(o.s + r) * w.vs + (int64_t)(t0 + s + 1) * w.B + b] = Sb[(int64_t)s * nmax + r];
+      }
+    }
+    __syncthreads();
+  }
+  if (spiking) {
+#pragma unroll
+    for (int j = 0; j < NPT; ++j) {
+      const int r = tid + j * nthr;
+      if (r < o.n) {
+        pa[(o.V + r) * (int64_t)w.B + b] = v[j];
+        pa[(o.ref + r) * (int64_t)w.B + b] = rf[j];
+      }
+    }
+  }
+}

@@ -19,6 +19,7 @@
 
 #include "host.hpp"
 #include "kernels.hpp"
+#include "kernels_window.hpp"
 
 using namespace ms;
 
@@ -58,6 +59,11 @@ struct Launch {
   FilterParams fp{};
   const int32_t* feed_rows = nullptr;
   EnsDesc ens{};
+  bool a_bcast = true;               // ELEM_INC a is a parameter base
+  // window driver
+  int32_t src_blk = 1, a_blk = 1;    // block offsets of src / a (1: this step, 0: previous step)
+  int32_t nmax = 0, npt = 1, nthr = 64, ts = 16;   // fused-ensemble launch shape
+  size_t lds = 0;
 };
 
 }  // namespace
@@ -102,7 +108,15 @@ struct ms_sim {
   int32_t persistent_threads = 256;  // workgroup size of the persistent kernel
   int64_t scratch_n = 0;             // per-column scratch floats of the persistent kernel
   float* scratch = nullptr;          // global scratch when state is not LDS-resident
-  std::vector<void*> extra_allocs;   // transposed weights and their offsets
+  std::vector<void*> extra_allocs;   // transposed weights and their offsets, extra pools
+  // window driver
+  std::unique_ptr<WindowPlan> wplan;
+  std::vector<Launch> wl;            // phases in execution order
+  float* va = nullptr;               // versioned signals [rows_v][(W+1)*B]
+  float* pa = nullptr;               // neuron state [rows_p][B]
+  int32_t W = 0;                     // steps per window
+  int64_t vs = 0;                    // row stride of va
+  const int32_t* wprobe_src = nullptr;
   std::vector<std::vector<float>> host_bases;   // host copies of parameter bases
 };
 
@@ -137,6 +151,7 @@ void free_sim(ms_sim* s) {
   f(s->ipool); f(s->fpool); f(s->ctr); f(s->feed_stage); f(s->feed_tmp); f(s->probe_buf);
   f(s->prog.groups);
   f(s->scratch);
+  f(s->va); f(s->pa);
   for (void* p : s->extra_allocs) f(p);
   if (s->ev0) (void)hipEventDestroy(s->ev0);
   if (s->ev1) (void)hipEventDestroy(s->ev1);
@@ -162,6 +177,129 @@ struct PoolBuilder {
     return off;
   }
 };
+
+// Lowered groups -> launch records (index and parameter arrays uploaded into
+// pools owned by the simulator); `extra_ints` is uploaded alongside and its
+// device address returned in *extra_ptr.
+void build_launches(ms_sim* s, const std::vector<LGroup>& groups, std::vector<Launch>& out,
+                    const std::vector<int32_t>& extra_ints, const int32_t** extra_ptr) {
+  Plan& p = *s->plan;
+  const IR& ir = p.ir;
+  // ---- lowered groups -> pools
+  PoolBuilder pb;
+  struct Offs { int64_t dst, src, a, V, ref, ptr, values, w, x, d, trc, tref, amp, ca, cb, feed, full; };
+  std::vector<Offs> offs;
+  for (const LGroup& g : groups) {
+    Offs o{};
+    o.dst = pb.add_i(g.dst.idx); o.src = pb.add_i(g.src.idx); o.a = pb.add_i(g.a.idx);
+    o.V = pb.add_i(g.V.idx); o.ref = pb.add_i(g.ref.idx); o.ptr = pb.add_i(g.ptr);
+    o.w = pb.add_i(g.w_row); o.x = pb.add_i(g.x_row); o.d = pb.add_i(g.d_row);
+    o.feed = pb.add_i(g.feed_rows);
+    o.values = pb.add_f(g.values);
+    const bool per_row_params = g.type != OP_ENS;
+    o.trc = per_row_params && g.tau_rc.size() > 1 ? pb.add_f(g.tau_rc) : -1;
+    o.full = -1;
+    if (per_row_params && g.tau_rc.size() > 1) {
+      std::vector<float> full(g.tau_rc.size());
+      for (size_t k = 0; k < full.size(); ++k) full[k] = (float)std::expm1(-p.dt / (double)g.tau_rc[k]);
+      o.full = pb.add_f(full);
+    }
+    o.tref = per_row_params && g.tau_ref.size() > 1 ? pb.add_f(g.tau_ref) : -1;
+    o.amp = per_row_params && g.amp.size() > 1 ? pb.add_f(g.amp) : -1;
+    o.ca = g.ca.size() > 1 ? pb.add_f(g.ca) : -1;
+    o.cb = g.cb.size() > 1 ? pb.add_f(g.cb) : -1;
+    offs.push_back(o);
+  }
+  // packed per-op records of fused ensemble groups (EnsOp, 16 x 4 bytes each)
+  static_assert(sizeof(EnsOp) == 16 * 4, "EnsOp layout");
+  std::vector<int64_t> ens_off(groups.size(), -1);
+  for (size_t gi = 0; gi < groups.size(); ++gi) {
+    const LGroup& g = groups[gi];
+    if (g.type != OP_ENS) continue;
+    std::vector<int32_t> rec;
+    for (size_t k = 0; k < g.ens_n.size(); ++k) {
+      EnsOp e{};
+      e.n = g.ens_n[k]; e.x = g.ens_x[k]; e.enc = g.ens_enc[k]; e.bias = g.ens_bias[k];
+      e.V = g.ens_V[k]; e.ref = g.ens_ref[k]; e.s = g.ens_s[k];
+      for (int f = 0; f < kMaxFns; ++f) {
+        e.D[f] = f < (int)g.ens_D.size() ? g.ens_D[f][k] : 0;
+        e.d[f] = f < (int)g.ens_dd.size() ? g.ens_dd[f][k] : 0;
+      }
+      const float trc = g.tau_rc.size() > 1 ? g.tau_rc[k] : g.tau_rc[0];
+      e.tau_rc = trc;
+      e.tau_ref = g.tau_ref.size() > 1 ? g.tau_ref[k] : g.tau_ref[0];
+      e.amp = g.amp.size() > 1 ? g.amp[k] : g.amp[0];
+      e.full = (float)std::expm1(-p.dt / (double)trc);
+      e.inv_tau = (float)(1.0 / (double)trc);
+      const int32_t* w = reinterpret_cast<const int32_t*>(&e);
+      rec.insert(rec.end(), w, w + 16);
+    }
+    ens_off[gi] = pb.add_i(rec);
+  }
+  const int64_t extra_off = pb.add_i(extra_ints);
+  int32_t* ipool = dev_alloc<int32_t>(std::max<size_t>(1, pb.ints.size()));
+  float* fpool = dev_alloc<float>(std::max<size_t>(1, pb.floats.size()));
+  s->extra_allocs.push_back(ipool);
+  s->extra_allocs.push_back(fpool);
+  if (!pb.ints.empty())
+    HIPCHECK(hipMemcpy(ipool, pb.ints.data(), pb.ints.size() * 4, hipMemcpyHostToDevice));
+  if (!pb.floats.empty())
+    HIPCHECK(hipMemcpy(fpool, pb.floats.data(), pb.floats.size() * 4, hipMemcpyHostToDevice));
+  auto ip = [&](int64_t off) -> const int32_t* { return off < 0 ? nullptr : ipool + off; };
+  auto fp = [&](int64_t off) -> const float* { return off < 0 ? nullptr : fpool + off; };
+  *extra_ptr = ip(extra_off);
+  auto opnd = [&](const LOperand& L, int64_t off) { return Opnd{ip(off), L.start}; };
+  for (size_t gi = 0; gi < groups.size(); ++gi) {
+    const LGroup& g = groups[gi];
+    const Offs& o = offs[gi];
+    Launch l;
+    l.type = g.type;
+    l.rows = g.rows;
+    l.dst = opnd(g.dst, o.dst);
+    l.src = opnd(g.src, o.src);
+    l.a = opnd(g.a, o.a);
+    l.V = opnd(g.V, o.V);
+    l.ref = opnd(g.ref, o.ref);
+    if (g.src.base >= 0) {
+      l.src_base = s->base_ptr[g.src.base];
+      l.src_bcast = ir.bases[g.src.base].cls != SC_BATCHED;
+    }
+    if (g.a.base >= 0) {
+      l.a_base = s->base_ptr[g.a.base];
+      l.a_bcast = ir.bases[g.a.base].cls != SC_BATCHED;
+    }
+    l.ptr = ip(o.ptr);
+    l.values = fp(o.values);
+    l.M = g.M; l.K = g.K;
+    l.w_row = ip(o.w); l.x_row = ip(o.x); l.d_row = ip(o.d);
+    l.feed_rows = ip(o.feed);
+    if (g.type == OP_LIF || g.type == OP_LIF_RATE) {
+      l.np.tau_rc = g.tau_rc[0]; l.np.tau_ref = g.tau_ref[0]; l.np.amp = g.amp[0];
+      l.np.full = (float)std::expm1(-p.dt / (double)g.tau_rc[0]);
+      l.np.tau_rc_r = fp(o.trc); l.np.tau_ref_r = fp(o.tref); l.np.amp_r = fp(o.amp);
+      l.np.full_r = fp(o.full);
+    }
+    if (g.type == OP_LOWPASS) {
+      l.fp.a = g.ca[0]; l.fp.b = g.cb[0];
+      l.fp.a_r = fp(o.ca); l.fp.b_r = fp(o.cb);
+    }
+    if (g.type == OP_ENS) {
+      EnsDesc& E = l.ens;
+      if ((int)g.ens_df.size() > kMaxFns) fail(MS_E_INVALID, "fused ensemble with too many decoded functions");
+      E.d = g.ens_d; E.ntype = g.ens_type; E.nf = (int32_t)g.ens_df.size(); E.ndec = 0;
+      for (int f = 0; f < E.nf; ++f) { E.df[f] = g.ens_df[f]; E.ndec += g.ens_df[f]; }
+      if (E.ndec > kMaxDec) fail(MS_E_INVALID, "fused ensemble decodes too many outputs");
+      for (int f = 0; f < E.nf; ++f) {
+        E.D[f] = s->base_ptr[g.ens_Dbase[f]];
+        E.Dcols[f] = ir.bases[g.ens_Dbase[f]].cols;
+      }
+      E.enc = g.a.base >= 0 ? s->base_ptr[g.a.base] : nullptr;
+      E.bias = s->base_ptr[g.ens_bias_base];
+      E.ops = reinterpret_cast<const EnsOp*>(ipool + ens_off[gi]);
+    }
+    out.push_back(l);
+  }
+}
 
 void setup_device(ms_sim* s) {
   Plan& p = *s->plan;
@@ -193,116 +331,8 @@ void setup_device(ms_sim* s) {
   if (!s->state) {
     s->state = dev_alloc<float>(B);
   }
-  // ---- lowered groups -> pools
-  PoolBuilder pb;
-  struct Offs { int64_t dst, src, a, V, ref, ptr, values, w, x, d, trc, tref, amp, ca, cb, feed, full; };
-  std::vector<Offs> offs;
-  for (const LGroup& g : p.lowered) {
-    Offs o{};
-    o.dst = pb.add_i(g.dst.idx); o.src = pb.add_i(g.src.idx); o.a = pb.add_i(g.a.idx);
-    o.V = pb.add_i(g.V.idx); o.ref = pb.add_i(g.ref.idx); o.ptr = pb.add_i(g.ptr);
-    o.w = pb.add_i(g.w_row); o.x = pb.add_i(g.x_row); o.d = pb.add_i(g.d_row);
-    o.feed = pb.add_i(g.feed_rows);
-    o.values = pb.add_f(g.values);
-    const bool per_row_params = g.type != OP_ENS;
-    o.trc = per_row_params && g.tau_rc.size() > 1 ? pb.add_f(g.tau_rc) : -1;
-    o.full = -1;
-    if (per_row_params && g.tau_rc.size() > 1) {
-      std::vector<float> full(g.tau_rc.size());
-      for (size_t k = 0; k < full.size(); ++k) full[k] = (float)std::expm1(-p.dt / (double)g.tau_rc[k]);
-      o.full = pb.add_f(full);
-    }
-    o.tref = per_row_params && g.tau_ref.size() > 1 ? pb.add_f(g.tau_ref) : -1;
-    o.amp = per_row_params && g.amp.size() > 1 ? pb.add_f(g.amp) : -1;
-    o.ca = g.ca.size() > 1 ? pb.add_f(g.ca) : -1;
-    o.cb = g.cb.size() > 1 ? pb.add_f(g.cb) : -1;
-    offs.push_back(o);
-  }
-  // packed per-op records of fused ensemble groups (EnsOp, 16 x 4 bytes each)
-  static_assert(sizeof(EnsOp) == 16 * 4, "EnsOp layout");
-  std::vector<int64_t> ens_off(p.lowered.size(), -1);
-  for (size_t gi = 0; gi < p.lowered.size(); ++gi) {
-    const LGroup& g = p.lowered[gi];
-    if (g.type != OP_ENS) continue;
-    std::vector<int32_t> rec;
-    for (size_t k = 0; k < g.ens_n.size(); ++k) {
-      EnsOp e{};
-      e.n = g.ens_n[k]; e.x = g.ens_x[k]; e.enc = g.ens_enc[k]; e.bias = g.ens_bias[k];
-      e.V = g.ens_V[k]; e.ref = g.ens_ref[k]; e.s = g.ens_s[k];
-      for (int f = 0; f < kMaxFns; ++f) {
-        e.D[f] = f < (int)g.ens_D.size() ? g.ens_D[f][k] : 0;
-        e.d[f] = f < (int)g.ens_dd.size() ? g.ens_dd[f][k] : 0;
-      }
-      const float trc = g.tau_rc.size() > 1 ? g.tau_rc[k] : g.tau_rc[0];
-      e.tau_rc = trc;
-      e.tau_ref = g.tau_ref.size() > 1 ? g.tau_ref[k] : g.tau_ref[0];
-      e.amp = g.amp.size() > 1 ? g.amp[k] : g.amp[0];
-      e.full = (float)std::expm1(-p.dt / (double)trc);
-      e.inv_tau = (float)(1.0 / (double)trc);
-      const int32_t* w = reinterpret_cast<const int32_t*>(&e);
-      rec.insert(rec.end(), w, w + 16);
-    }
-    ens_off[gi] = pb.add_i(rec);
-  }
-  const int64_t probe_off = pb.add_i(p.probe_src_rows);
-  s->ipool = dev_alloc<int32_t>(std::max<size_t>(1, pb.ints.size()));
-  s->fpool = dev_alloc<float>(std::max<size_t>(1, pb.floats.size()));
-  if (!pb.ints.empty())
-    HIPCHECK(hipMemcpy(s->ipool, pb.ints.data(), pb.ints.size() * 4, hipMemcpyHostToDevice));
-  if (!pb.floats.empty())
-    HIPCHECK(hipMemcpy(s->fpool, pb.floats.data(), pb.floats.size() * 4, hipMemcpyHostToDevice));
-  auto ip = [&](int64_t off) -> const int32_t* { return off < 0 ? nullptr : s->ipool + off; };
-  auto fp = [&](int64_t off) -> const float* { return off < 0 ? nullptr : s->fpool + off; };
-  auto opnd = [&](const LOperand& L, int64_t off) { return Opnd{ip(off), L.start}; };
-  for (size_t gi = 0; gi < p.lowered.size(); ++gi) {
-    const LGroup& g = p.lowered[gi];
-    const Offs& o = offs[gi];
-    Launch l;
-    l.type = g.type;
-    l.rows = g.rows;
-    l.dst = opnd(g.dst, o.dst);
-    l.src = opnd(g.src, o.src);
-    l.a = opnd(g.a, o.a);
-    l.V = opnd(g.V, o.V);
-    l.ref = opnd(g.ref, o.ref);
-    if (g.src.base >= 0) {
-      l.src_base = s->base_ptr[g.src.base];
-      l.src_bcast = ir.bases[g.src.base].cls != SC_BATCHED;
-    }
-    if (g.a.base >= 0) l.a_base = s->base_ptr[g.a.base];
-    l.ptr = ip(o.ptr);
-    l.values = fp(o.values);
-    l.M = g.M; l.K = g.K;
-    l.w_row = ip(o.w); l.x_row = ip(o.x); l.d_row = ip(o.d);
-    l.feed_rows = ip(o.feed);
-    if (g.type == OP_LIF || g.type == OP_LIF_RATE) {
-      l.np.tau_rc = g.tau_rc[0]; l.np.tau_ref = g.tau_ref[0]; l.np.amp = g.amp[0];
-      l.np.full = (float)std::expm1(-p.dt / (double)g.tau_rc[0]);
-      l.np.tau_rc_r = fp(o.trc); l.np.tau_ref_r = fp(o.tref); l.np.amp_r = fp(o.amp);
-      l.np.full_r = fp(o.full);
-    }
-    if (g.type == OP_LOWPASS) {
-      l.fp.a = g.ca[0]; l.fp.b = g.cb[0];
-      l.fp.a_r = fp(o.ca); l.fp.b_r = fp(o.cb);
-    }
-    if (g.type == OP_ENS) {
-      EnsDesc& E = l.ens;
-      if ((int)g.ens_df.size() > kMaxFns) fail(MS_E_INVALID, "fused ensemble with too many decoded functions");
-      E.d = g.ens_d; E.ntype = g.ens_type; E.nf = (int32_t)g.ens_df.size(); E.ndec = 0;
-      for (int f = 0; f < E.nf; ++f) { E.df[f] = g.ens_df[f]; E.ndec += g.ens_df[f]; }
-      if (E.ndec > kMaxDec) fail(MS_E_INVALID, "fused ensemble decodes too many outputs");
-      for (int f = 0; f < E.nf; ++f) {
-        E.D[f] = s->base_ptr[g.ens_Dbase[f]];
-        E.Dcols[f] = ir.bases[g.ens_Dbase[f]].cols;
-      }
-      E.enc = g.a.base >= 0 ? s->base_ptr[g.a.base] : nullptr;
-      E.bias = s->base_ptr[g.ens_bias_base];
-      E.ops = reinterpret_cast<const EnsOp*>(s->ipool + ens_off[gi]);
-    }
-    s->launches.push_back(l);
-  }
+  build_launches(s, p.lowered, s->launches, p.probe_src_rows, &s->probe_src);
   s->probe_rows = (int32_t)p.probe_src_rows.size();
-  s->probe_src = ip(probe_off);
   s->ctr = dev_alloc<int64_t>(2);
   HIPCHECK(hipMemset(s->ctr, 0, 2 * sizeof(int64_t)));
   HIPCHECK(hipMemset(s->state, 0, std::max<size_t>(1, s->state_rows) * B * sizeof(float)));
@@ -478,10 +508,13 @@ int64_t param_bytes(const Plan& p) {
   return n;
 }
 
-// Persistent per-column driver when one workgroup can hold a column's whole
-// step cheaply (small weights, modest state); launches otherwise.
+// Stage-major when the model has no recurrence beyond each neuron's and filter's
+// own state; otherwise the persistent per-column driver when one workgroup can
+// hold a column's whole step cheaply (small weights, modest state), else
+// launches.
 int32_t choose_driver(const Plan& p, int32_t B, int32_t requested) {
   if (requested != MS_DRIVER_AUTO) return requested;
+  if (make_window_plan(p).ok) return MS_DRIVER_WINDOW;
   const int64_t rows = p.base_rows.empty() ? 0 : p.base_rows[0];
   const int64_t wbytes = param_bytes(p);
   if (wbytes <= (1 << 20) && rows <= (1 << 17) && (B >= 8 || rows <= 8192)) return MS_DRIVER_PERSISTENT;
@@ -562,6 +595,136 @@ void run_persistent(ms_sim* s, int64_t n_steps) {
   hipLaunchKernelGGL(k_set_ctr, dim3(1), dim3(64), 0, s->stream, s->ctr, s->steps_total + n_steps, n_steps);
 }
 
+// ------------------------------------------------------------ window driver
+constexpr double kWindowBytes = 8.0 * (1 << 30);   // budget for the versioned signals
+constexpr int32_t kMaxWindow = 1024;
+
+// Launch shape of a fused-ensemble phase: threads cover the largest op's
+// neurons (at most 4 per thread), LDS holds a sub-window of inputs and outputs.
+void ens_shape(ms_sim* s, Launch& l, const LGroup& g) {
+  int32_t nmax = 1;
+  for (int32_t n : g.ens_n) nmax = std::max(nmax, n);
+  l.nmax = nmax;
+  l.nthr = (int32_t)std::min<int64_t>(1024, ((int64_t)nmax + 63) / 64 * 64);
+  l.npt = (nmax + l.nthr - 1) / l.nthr;
+  if (l.npt > 4) fail(MS_E_INVALID, "ensemble too large for the window driver (more than 4096 neurons)");
+  if (l.npt == 3) l.npt = 4;
+  const int64_t per_step = (int64_t)l.ens.d + nmax;
+  l.ts = (int32_t)std::min<int64_t>(16, (int64_t)(s->lds_limit / 4) / std::max<int64_t>(1, per_step));
+  if (l.ts < 1) fail(MS_E_INVALID, "ensemble too large for the window driver's LDS staging");
+  l.lds = (size_t)l.ts * per_step * sizeof(float);
+}
+
+void setup_window(ms_sim* s) {
+  WindowPlan& w = *s->wplan;
+  const int32_t B = s->B;
+  if (B > 65535) fail(MS_E_INVALID, "minibatch too large for the window driver");
+  int lds_max = 0;
+  HIPCHECK(hipDeviceGetAttribute(&lds_max, hipDeviceAttributeMaxSharedMemoryPerBlock, s->device));
+  s->lds_limit = (size_t)lds_max;
+  const double per_step = (double)std::max<int64_t>(1, w.rows_v) * B * sizeof(float);
+  s->W = (int32_t)std::max<double>(1.0, std::min<double>(kMaxWindow, std::floor(kWindowBytes / per_step) - 1));
+  s->vs = (int64_t)(s->W + 1) * B;
+  s->va = dev_alloc<float>((size_t)std::max<int64_t>(1, w.rows_v) * s->vs);
+  s->pa = dev_alloc<float>((size_t)std::max<int64_t>(1, w.rows_p) * B);
+  std::vector<LGroup> groups;
+  for (const WPhase& ph : w.phases) groups.push_back(ph.g);
+  build_launches(s, groups, s->wl, w.probe_rows, &s->wprobe_src);
+  for (size_t k = 0; k < s->wl.size(); ++k) {
+    Launch& l = s->wl[k];
+    l.src_blk = w.phases[k].src_blk;
+    l.a_blk = w.phases[k].a_blk;
+    if (l.type == OP_ENS) {
+      ens_shape(s, l, w.phases[k].g);
+    }
+  }
+  if (s->lds_limit > 65536) {
+    HIPCHECK(hipFuncSetAttribute((const void*)k_w_ens<1>, hipFuncAttributeMaxDynamicSharedMemorySize, (int)s->lds_limit));
+    HIPCHECK(hipFuncSetAttribute((const void*)k_w_ens<2>, hipFuncAttributeMaxDynamicSharedMemorySize, (int)s->lds_limit));
+    HIPCHECK(hipFuncSetAttribute((const void*)k_w_ens<4>, hipFuncAttributeMaxDynamicSharedMemorySize, (int)s->lds_limit));
+  }
+  HIPCHECK(hipMemset(s->va, 0, (size_t)std::max<int64_t>(1, w.rows_v) * s->vs * sizeof(float)));
+  HIPCHECK(hipMemset(s->pa, 0, (size_t)std::max<int64_t>(1, w.rows_p) * B * sizeof(float)));
+}
+
+inline unsigned grid_items(double n) {
+  if (n >= 4294967296.0) fail(MS_E_INVALID, "window phase too large for 32-bit work-item indexing");
+  return (unsigned)std::max<int64_t>(1, ((int64_t)n + kBlock - 1) / kBlock);
+}
+
+void launch_phase(ms_sim* s, const Launch& l, int32_t T, int64_t t0) {
+  if (l.rows == 0) return;
+  const WView w{s->va, s->vs, s->B, T};
+  const double tb = (double)T * s->B;
+  hipStream_t q = s->stream;
+  switch (l.type) {
+    case OP_FEED:
+      hipLaunchKernelGGL(k_w_feed, dim3(grid_items(l.rows * tb)), dim3(kBlock), 0, q, w, l.rows, l.dst, l.feed_rows,
+                         (const float*)s->feed_stage, s->plan->ir.feed_rows, t0);
+      break;
+    case OP_RESET:
+      hipLaunchKernelGGL(k_w_reset, dim3(grid_items(l.rows * tb)), dim3(kBlock), 0, q, w, l.rows, l.dst, l.values);
+      break;
+    case OP_COPY:
+      hipLaunchKernelGGL(k_w_copy, dim3(grid_items(l.rows * tb)), dim3(kBlock), 0, q, w, l.rows, l.dst,
+                         l.src_base, l.src, (int)l.src_bcast, l.src_blk);
+      break;
+    case OP_COPY_INC:
+      hipLaunchKernelGGL(k_w_copy_inc, dim3(grid_items(l.rows * tb)), dim3(kBlock), 0, q, w, l.rows, l.dst,
+                         l.src_base, l.src, (int)l.src_bcast, l.src_blk, l.ptr);
+      break;
+    case OP_ELEM_INC:
+      hipLaunchKernelGGL(k_w_elem_inc, dim3(grid_items(l.rows * tb)), dim3(kBlock), 0, q, w, l.rows, l.dst,
+                         l.a_base, l.a, (int)l.a_bcast, l.a_blk, l.src_base, l.src, (int)l.src_bcast, l.src_blk,
+                         l.ptr);
+      break;
+    case OP_DOT_INC:
+      hipLaunchKernelGGL(k_w_dot, dim3(grid_items((double)l.rows * l.M * tb)), dim3(kBlock), 0, q, w, l.rows, l.M,
+                         l.K, l.a_base, l.w_row, l.x_row, l.d_row, l.src_blk);
+      break;
+    case OP_LIF:
+      hipLaunchKernelGGL(k_w_lif, dim3(grid_items((double)l.rows * s->B)), dim3(kBlock), 0, q, w, l.rows, l.src,
+                         l.dst, l.V, l.ref, s->pa, l.np, s->dt, l.src_blk);
+      break;
+    case OP_LIF_RATE:
+      hipLaunchKernelGGL(k_w_lif_rate, dim3(grid_items(l.rows * tb)), dim3(kBlock), 0, q, w, l.rows, l.src, l.dst,
+                         l.np, l.src_blk);
+      break;
+    case OP_LOWPASS:
+      hipLaunchKernelGGL(k_w_lowpass, dim3(grid_items((double)l.rows * s->B)), dim3(kBlock), 0, q, w, l.rows,
+                         l.dst, l.src, l.fp, l.src_blk);
+      break;
+    case OP_ENS: {
+      const dim3 grid((unsigned)l.rows, (unsigned)s->B);
+      if (l.npt == 1)
+        hipLaunchKernelGGL(k_w_ens<1>, grid, dim3(l.nthr), l.lds, q, w, s->pa, l.ens, s->dt, l.nmax, l.ts, l.src_blk);
+      else if (l.npt == 2)
+        hipLaunchKernelGGL(k_w_ens<2>, grid, dim3(l.nthr), l.lds, q, w, s->pa, l.ens, s->dt, l.nmax, l.ts, l.src_blk);
+      else
+        hipLaunchKernelGGL(k_w_ens<4>, grid, dim3(l.nthr), l.lds, q, w, s->pa, l.ens, s->dt, l.nmax, l.ts, l.src_blk);
+      break;
+    }
+    default: fail(MS_E_INVALID, "unknown group type");
+  }
+}
+
+void run_window(ms_sim* s, int64_t n_steps) {
+  const WindowPlan& w = *s->wplan;
+  for (int64_t t0 = 0; t0 < n_steps; t0 += s->W) {
+    const int32_t T = (int32_t)std::min<int64_t>(s->W, n_steps - t0);
+    for (const Launch& l : s->wl) launch_phase(s, l, T, t0);
+    const WView v{s->va, s->vs, s->B, T};
+    const int32_t pr = (int32_t)w.probe_rows.size();
+    if (pr > 0)
+      hipLaunchKernelGGL(k_w_probe, dim3(grid_items((double)pr * T * s->B)), dim3(kBlock), 0, s->stream, v,
+                         s->wprobe_src, pr, s->probe_buf, s->steps_total + t0);
+    if (w.rows_v > 0)
+      hipLaunchKernelGGL(k_w_carry, dim3(grid_items((double)w.rows_v * s->B)), dim3(kBlock), 0, s->stream, v,
+                         w.rows_v);
+  }
+  hipLaunchKernelGGL(k_set_ctr, dim3(1), dim3(64), 0, s->stream, s->ctr, s->steps_total + n_steps, n_steps);
+}
+
 }  // namespace
 
 extern "C" {
@@ -575,7 +738,7 @@ ms_status ms_sim_create(const ms_model* model, const ms_sim_opts* opts, ms_sim**
     if (!(o->dt > 0)) fail(MS_E_INVALID, "dt must be > 0");
     if (o->minibatch < 1) fail(MS_E_INVALID, "minibatch must be >= 1");
     if (o->unroll < 1) fail(MS_E_INVALID, "unroll must be >= 1");
-    if (o->driver < MS_DRIVER_AUTO || o->driver > MS_DRIVER_PERSISTENT) fail(MS_E_INVALID, "unknown driver");
+    if (o->driver < MS_DRIVER_AUTO || o->driver > MS_DRIVER_WINDOW) fail(MS_E_INVALID, "unknown driver");
     int ndev = 0;
     HIPCHECK(hipGetDeviceCount(&ndev));
     if (o->device < 0 || o->device >= ndev) fail(MS_E_INVALID, "device ordinal out of range");
@@ -599,8 +762,13 @@ ms_status ms_sim_create(const ms_model* model, const ms_sim_opts* opts, ms_sim**
       // persistent: one workgroup per batch column -> column-major state
       s->S = s->driver == MS_DRIVER_PERSISTENT ? Strides{1, (int64_t)std::max<int64_t>(1, s->plan->base_rows.empty() ? 1 : s->plan->base_rows[0])}
                                                : Strides{(int64_t)s->B, 1};
+      if (s->driver == MS_DRIVER_WINDOW) {
+        s->wplan = std::make_unique<WindowPlan>(make_window_plan(*s->plan));
+        if (!s->wplan->ok) fail(MS_E_INVALID, "the window driver cannot run this model: " + s->wplan->why);
+      }
       setup_device(s);
       if (s->driver == MS_DRIVER_PERSISTENT) setup_persistent(s);
+      if (s->driver == MS_DRIVER_WINDOW) setup_window(s);
       ensure_capacity(s, std::max<int64_t>(1, o->probe_capacity_steps));
       HIPCHECK(hipStreamSynchronize(s->stream));
     } catch (...) {
@@ -636,6 +804,8 @@ ms_status ms_sim_run_steps(ms_sim* s, int64_t n_steps, const ms_feed* feeds, int
     HIPCHECK(hipEventRecord(s->ev0, s->stream));
     if (s->driver == MS_DRIVER_PERSISTENT) {
       run_persistent(s, n_steps);
+    } else if (s->driver == MS_DRIVER_WINDOW) {
+      run_window(s, n_steps);
     } else if (s->driver == MS_DRIVER_GRAPH) {
       ensure_graph(s);
       int64_t k = 0;
@@ -680,7 +850,7 @@ ms_status ms_sim_info(const ms_sim* s, int32_t* driver_out, int32_t* groups_out)
   return guarded([&] {
     if (!s) fail(MS_E_INVALID, "NULL sim");
     if (driver_out) *driver_out = s->driver;
-    if (groups_out) *groups_out = (int32_t)s->launches.size();
+    if (groups_out) *groups_out = (int32_t)(s->driver == MS_DRIVER_WINDOW ? s->wl.size() : s->launches.size());
   });
 }
 
@@ -720,6 +890,8 @@ ms_status ms_sim_reset(ms_sim* s) {
     if (!s) fail(MS_E_INVALID, "NULL sim");
     DeviceGuard dg(s->device);
     HIPCHECK(hipMemsetAsync(s->state, 0, std::max<size_t>(1, s->state_rows) * s->B * 4, s->stream));
+    if (s->va) HIPCHECK(hipMemsetAsync(s->va, 0, (size_t)std::max<int64_t>(1, s->wplan->rows_v) * s->vs * 4, s->stream));
+    if (s->pa) HIPCHECK(hipMemsetAsync(s->pa, 0, (size_t)std::max<int64_t>(1, s->wplan->rows_p) * s->B * 4, s->stream));
     HIPCHECK(hipMemsetAsync(s->ctr, 0, 2 * sizeof(int64_t), s->stream));
     HIPCHECK(hipStreamSynchronize(s->stream));
     s->steps_total = 0;
@@ -735,6 +907,25 @@ static void state_copy(ms_sim* s, int32_t sig, float* host, bool to_device) {
   const int64_t r0 = s->plan->sig_offset[sig];
   DeviceGuard dg(s->device);
   HIPCHECK(hipStreamSynchronize(s->stream));
+  if (s->driver == MS_DRIVER_WINDOW) {
+    // block 0 of a versioned signal (the value the next window starts from), or
+    // the private neuron state
+    const WindowPlan& w = *s->wplan;
+    const int64_t row = w.sig_row[sig];
+    float* dev = w.priv[sig] ? s->pa + row * B : s->va + row * s->vs;
+    const size_t pitch = (size_t)(w.priv[sig] ? B : s->vs) * 4;
+    std::vector<float> h((size_t)(rows * B));
+    if (to_device) {
+      for (int64_t b = 0; b < B; ++b)
+        for (int64_t r = 0; r < rows; ++r) h[(size_t)(r * B + b)] = host[(size_t)(b * rows + r)];
+      HIPCHECK(hipMemcpy2D(dev, pitch, h.data(), B * 4, B * 4, rows, hipMemcpyHostToDevice));
+    } else {
+      HIPCHECK(hipMemcpy2D(h.data(), B * 4, dev, pitch, B * 4, rows, hipMemcpyDeviceToHost));
+      for (int64_t b = 0; b < B; ++b)
+        for (int64_t r = 0; r < rows; ++r) host[(size_t)(b * rows + r)] = h[(size_t)(r * B + b)];
+    }
+    return;
+  }
   if (s->S.cs == 1) {
     if (s->S.rs != B) fail(MS_E_STATE, "unexpected state layout");
     float* dev = s->state + r0 * B;

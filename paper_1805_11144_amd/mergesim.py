@@ -17,7 +17,7 @@ REF_NODE, REF_ENS, REF_NEURONS = 0, 1, 2
 NEURON_LIF, NEURON_LIF_RATE = 0, 1
 FN_IDENTITY, FN_PRODUCT = 0, 1
 PLANNER_GREEDY, PLANNER_TREE = 0, 1
-DRIVER_AUTO, DRIVER_STEPS, DRIVER_GRAPH, DRIVER_PERSISTENT = 0, 1, 2, 3
+DRIVER_AUTO, DRIVER_STEPS, DRIVER_GRAPH, DRIVER_PERSISTENT, DRIVER_WINDOW = 0, 1, 2, 3, 4
 PARAM_GAIN, PARAM_BIAS, PARAM_DECODERS = 0, 1, 2
 STATE_VOLTAGE, STATE_REFRACTORY, STATE_SYNAPSE, STATE_PROBE_SYNAPSE = 0, 1, 2, 3
 

@@ -19,7 +19,14 @@ SMALL = {
     "c4": dict(n_steps=60, minibatch=3, n_ens=6, n_neurons=40, n_eval=200),
     "c5": dict(n_steps=40, n_ens=12, n_neurons=40, n_eval=200, n_input_targets=4, n_probed=3),
 }
-DRIVERS = {"steps": M.DRIVER_STEPS, "graph": M.DRIVER_GRAPH, "persistent": M.DRIVER_PERSISTENT}
+DRIVERS = {"steps": M.DRIVER_STEPS, "graph": M.DRIVER_GRAPH, "persistent": M.DRIVER_PERSISTENT,
+           "window": M.DRIVER_WINDOW}
+RECURRENT = {"c1", "c5"}     # the window driver refuses these (checked below)
+
+
+def skip_unsupported(name, driver):
+    if driver == "window" and name in RECURRENT:
+        pytest.skip("recurrent model: the stage-major window driver does not apply")
 
 
 def run_gpu(w, **opts):
@@ -39,6 +46,7 @@ def run_oracle(w):
 @pytest.mark.parametrize("driver", list(DRIVERS))
 @pytest.mark.parametrize("name", list(SMALL))
 def test_rate_mode_parity(name, driver, fuse):
+    skip_unsupported(name, driver)
     w = make_workload(name, neuron_type="lif_rate", **SMALL[name])
     got = run_gpu(w, driver=DRIVERS[driver], unroll=7, fuse=fuse)
     exp = run_oracle(w)
@@ -55,6 +63,7 @@ def test_spiking_mode_parity(name, driver):
     signature of float32-vs-float64 rounding at the threshold) and rare; the
     1e-4 flip bound itself is asserted at full sizes, where the spike count can
     resolve it."""
+    skip_unsupported(name, driver)
     w = make_workload(name, neuron_type="lif", **SMALL[name])
     got = run_gpu(w, driver=DRIVERS[driver], unroll=7)
     exp = run_oracle(w)
@@ -68,3 +77,10 @@ def test_spiking_mode_parity(name, driver):
         else:
             d = float(np.abs(g - e).max())
             print(f"{name} {driver} probe {pi}: abs {d:.2e}")
+
+
+@pytest.mark.parametrize("name", sorted(RECURRENT))
+def test_window_driver_refuses_recurrent_models(name):
+    w = make_workload(name, **SMALL[name])
+    with pytest.raises(M.MergesimError, match="cycle"):
+        M.Simulator(M.model_from_spec(w.spec), minibatch=w.minibatch, driver=M.DRIVER_WINDOW)

@@ -12,7 +12,8 @@ from tests.state_gen import random_state
 
 pytestmark = pytest.mark.gpu
 
-DRIVERS = {"steps": M.DRIVER_STEPS, "graph": M.DRIVER_GRAPH, "persistent": M.DRIVER_PERSISTENT}
+DRIVERS = {"steps": M.DRIVER_STEPS, "graph": M.DRIVER_GRAPH, "persistent": M.DRIVER_PERSISTENT,
+           "window": M.DRIVER_WINDOW}
 C2S = dict(n_steps=40, minibatch=4, n_neurons=30, n_eval=200)
 
 
@@ -37,7 +38,8 @@ def test_minibatch_equals_sequential_runs_with_reset(driver):
 
 @pytest.mark.parametrize("driver", list(DRIVERS))
 def test_split_runs_reset_and_determinism(driver):
-    w = make_workload("c1", n_steps=300)
+    w = make_workload("c1", n_steps=300) if driver != "window" else \
+        make_workload("c4", n_steps=300, minibatch=2, n_ens=4, n_neurons=40, n_eval=100)
     with sim_for(w, driver=DRIVERS[driver], unroll=7) as a:
         a.run_steps(300, w.feeds)
         whole = [a.data(p) for p in range(2)]
@@ -118,3 +120,18 @@ def test_injected_state_rate_parity(name):
     got, exp = run_injected(w, st, 100)
     for g, e in zip(got, exp):
         assert rel_err(g, e) <= 1e-5
+
+
+@pytest.mark.parametrize("K", [1, 10])
+@pytest.mark.parametrize("name", ["c2", "c4"])
+def test_injected_state_window_driver(name, K):
+    """The stage-major driver from the same seeded state as the oracle."""
+    w = make_workload(name, neuron_type="lif", **INJECT[name])
+    st = random_state(w.spec, w.minibatch, seed=300 + K)
+    got, exp = run_injected(w, st, K, driver=M.DRIVER_WINDOW)
+    for pi, (g, e) in enumerate(zip(got, exp)):
+        p = w.spec.probes[pi]
+        if p.target[0] == "neurons":
+            assert unpaired_flips(g, e) == 0 and flip_fraction(g, e) <= 1e-4
+        elif p.synapse is not None:
+            assert float(np.abs(g - e).max()) <= 1e-3
