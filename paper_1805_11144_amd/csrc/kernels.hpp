@@ -213,6 +213,28 @@ __device__ __forceinline__ float neuron_update(int ntype, float j, float& v, flo
   return 0.0f;
 }
 
+// Branch-free form of the spiking update above for dt / tau_rc <= 1/16 (the
+// partial-step factor always comes from the polynomial): the same formulas,
+// with every path computed and the results selected, so that lanes whose
+// neurons spike or sit in their refractory period do not serialise the
+// wavefront.  Returns the neuron output (amp_dt = amplitude / dt or 0).
+__device__ __forceinline__ float lif_update_bf(float j, float& v, float& rf, float tau_rc, float tau_ref,
+                                               float amp_dt, float full, float dt, float inv_tau) {
+  const float integ = fminf(fmaxf(dt - rf, 0.0f), dt);
+  const float ep = expm1_small(-integ * inv_tau);
+  const float e = rf > 0.0f ? ep : full;
+  v = v - (j - v) * e;
+  rf = fmaxf(rf - dt, 0.0f);
+  const float drive = j - 1.0f;
+  const float q = __fdividef(v - 1.0f, drive);
+  const float lg = fminf(-tau_rc * __logf(1.0f - q), integ);
+  const float since = drive > 0.0f ? (q >= 1.0f ? integ : lg) : 0.0f;
+  const bool spk = v > 1.0f;
+  v = spk ? 0.0f : fmaxf(v, 0.0f);
+  rf = spk ? tau_ref - since : rf;
+  return spk ? amp_dt : 0.0f;
+}
+
 // Sum over the 64 lanes of a wavefront, returned in every lane.  DPP moves
 // fold quads, half-rows and rows of 16 lanes; the four row sums are read with
 // readlane.  All lanes must be active.

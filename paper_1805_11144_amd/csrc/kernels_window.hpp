@@ -127,9 +127,18 @@ __global__ void k_w_lif(WView w, int64_t rows, Opnd J, Opnd s, Opnd V, Opnd R, f
   float v = pa[vi], rf = pa[ri];
   const int64_t jr = rowof(J, _r) * w.vs + (int64_t)jblk * w.B + _b;
   const int64_t sr = rowof(s, _r) * w.vs + w.B + _b;
-  for (int32_t t = 0; t < w.T; ++t) {
-    const float j = w.va[jr + (int64_t)t * w.B];
-    w.va[sr + (int64_t)t * w.B] = neuron_update(0, j, v, rf, tau_rc, tau_ref, amp, full, dt, 1.0f / tau_rc);
+  const float inv_tau = 1.0f / tau_rc;
+  if (dt * inv_tau <= 0.0625f) {
+    const float amp_dt = amp / dt;
+    for (int32_t t = 0; t < w.T; ++t) {
+      const float j = w.va[jr + (int64_t)t * w.B];
+      w.va[sr + (int64_t)t * w.B] = lif_update_bf(j, v, rf, tau_rc, tau_ref, amp_dt, full, dt, inv_tau);
+    }
+  } else {
+    for (int32_t t = 0; t < w.T; ++t) {
+      const float j = w.va[jr + (int64_t)t * w.B];
+      w.va[sr + (int64_t)t * w.B] = neuron_update(0, j, v, rf, tau_rc, tau_ref, amp, full, dt, inv_tau);
+    }
   }
   pa[vi] = v;
   pa[ri] = rf;
@@ -143,7 +152,20 @@ __global__ void k_w_lowpass(WView w, int64_t rows, Opnd y, Opnd v, FilterParams 
   const int64_t yr = rowof(y, _r) * w.vs + _b;
   const int64_t vr = rowof(v, _r) * w.vs + (int64_t)vblk * w.B + _b;
   float yv = w.va[yr];
-  for (int32_t t = 0; t < w.T; ++t) {
+  // inputs of 8 steps are loaded before they are consumed, so the loads of a
+  // chunk are in flight together; the recurrence itself is one FMA per step
+  int32_t t = 0;
+  for (; t + 8 <= w.T; t += 8) {
+    float vin[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) vin[u] = w.va[vr + (int64_t)(t + u) * w.B];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      yv = a * yv + c * vin[u];
+      w.va[yr + (int64_t)(t + u + 1) * w.B] = yv;
+    }
+  }
+  for (; t < w.T; ++t) {
     yv = a * yv + c * w.va[vr + (int64_t)t * w.B];
     w.va[yr + (int64_t)(t + 1) * w.B] = yv;
   }
@@ -167,28 +189,38 @@ __global__ void k_w_carry(WView w, int64_t rows) {
 // One workgroup per (op, batch column); thread tid owns neurons tid + j*blockDim
 // (j < NPT), whose voltage, refractory time, bias and encoder row stay in
 // registers for the whole window.  The window is processed in sub-windows of
-// `ts_max` steps: the sub-window's inputs x are staged in LDS, every thread
-// advances its neurons through the sub-window and leaves their outputs in LDS
-// (no synchronisation between steps: a neuron depends only on its own past),
-// then the decoded outputs of all sub-window steps are formed as dot products
-// over the neurons and written, with the spikes if they are stored.
+// `ts_max` (<= 16) steps: the sub-window's inputs x are staged in LDS, every
+// thread advances its neurons through the sub-window and leaves their outputs
+// in LDS (no synchronisation between steps: a neuron depends only on its own
+// past), then the decoded outputs of all sub-window steps, a [ndec x n] by
+// [n x ts] product, are formed on MFMA (v_mfma_f32_16x16x4f32: A lane l row
+// l%16, k l/16; B lane l k l/16, column l%16; result register v row
+// 4(l/16) + v, column l%16).  Each wavefront takes every nw-th group of four
+// neurons, keeps its decoder fragments in registers for the whole window, and
+// the wavefronts' partial 16 x 16 tiles are summed in LDS.
+typedef float mfma_f4x __attribute__((ext_vector_type(4)));
+constexpr int kEnsDecCache = 16;   // MFMA k-steps whose decoder fragments stay in registers
+
 template <int NPT>
 __global__ void __launch_bounds__(1024) k_w_ens(WView w, float* pa, EnsDesc E, float dt, int32_t nmax,
                                                 int32_t ts_max, int xblk) {
   extern __shared__ float lds[];
   const int op = blockIdx.x;
   const int64_t b = blockIdx.y;
-  const int tid = threadIdx.x, nthr = blockDim.x;
+  const int tid = threadIdx.x, nthr = blockDim.x, lane = tid % 64, wave = tid / 64, nw = nthr / 64;
   const EnsOp o = load_op(E.ops, op);
   const int d = o.x >= 0 ? E.d : 0, ndec = E.ndec, df0 = E.df[0];
-  float* X = lds;                          // [ts_max][d]
-  float* Sb = lds + (int64_t)ts_max * E.d;  // [ts_max][nmax]
+  float* X = lds;                                  // [ts_max][E.d]
+  float* Sb = X + (int64_t)ts_max * E.d;           // [ts_max][nmax]
+  float* red = Sb + (int64_t)ts_max * nmax;        // [nw][16][16]
   gptr<float> enc = G(E.enc) + (int64_t)o.enc * E.d;
   gptr<float> bias = G(E.bias) + o.bias;
   gptr<float> D0 = G(E.D[0]) + (int64_t)o.D[0] * E.Dcols[0];
   gptr<float> D1 = G(E.D[E.nf > 1 ? 1 : 0]) + (int64_t)o.D[E.nf > 1 ? 1 : 0] * E.Dcols[E.nf > 1 ? 1 : 0];
   const int64_t s0 = E.Dcols[0], s1 = E.Dcols[E.nf > 1 ? 1 : 0];
   const bool spiking = E.ntype == 0;
+  const bool bf = spiking && dt * o.inv_tau <= 0.0625f;   // branch-free spiking update applies
+  const float amp_dt = o.amp / dt;
   float v[NPT], rf[NPT], bj[NPT], er[NPT][kMaxXReg];
 #pragma unroll
   for (int j = 0; j < NPT; ++j) {
@@ -200,6 +232,18 @@ __global__ void __launch_bounds__(1024) k_w_ens(WView w, float* pa, EnsDesc E, f
 #pragma unroll
     for (int k = 0; k < kMaxXReg; ++k) er[j][k] = (live && k < d) ? enc[(int64_t)r * E.d + k] : 0.0f;
   }
+  // decoder fragment of this lane for MFMA k-step ks: row q = lane % 16,
+  // neuron r = 4 * (wave + nw * ks) + lane / 16
+  const int qa = lane % 16;
+  gptr<float> drow = qa < df0 ? D0 + (int64_t)qa * s0 : D1 + (int64_t)(qa - df0) * s1;
+  const int ksteps = (o.n + 4 * nw - 1) / (4 * nw);
+  auto dfrag = [&](int ks) {
+    const int r = 4 * (wave + nw * ks) + lane / 16;
+    return (qa < ndec && r < o.n) ? drow[r] : 0.0f;
+  };
+  float dA[kEnsDecCache];
+#pragma unroll
+  for (int ks = 0; ks < kEnsDecCache; ++ks) dA[ks] = (ndec > 0 && ks < ksteps) ? dfrag(ks) : 0.0f;
   for (int32_t t0 = 0; t0 < w.T; t0 += ts_max) {
     const int ts = min(ts_max, w.T - t0);
     for (int i = tid; i < ts * d; i += nthr) {
@@ -221,19 +265,35 @@ __global__ void __launch_bounds__(1024) k_w_ens(WView w, float* pa, EnsDesc E, f
             for (int k = 0; k < d; ++k) jc += enc[(int64_t)r * E.d + k] * X[s * E.d + k];
           }
           Sb[(int64_t)s * nmax + r] =
-              neuron_update(E.ntype, jc, v[j], rf[j], o.tau_rc, o.tau_ref, o.amp, o.full, dt, o.inv_tau);
+              bf ? lif_update_bf(jc, v[j], rf[j], o.tau_rc, o.tau_ref, amp_dt, o.full, dt, o.inv_tau)
+                 : neuron_update(E.ntype, jc, v[j], rf[j], o.tau_rc, o.tau_ref, o.amp, o.full, dt, o.inv_tau);
         }
       }
     }
     __syncthreads();
-    for (int i = tid; i < ndec * ts; i += nthr) {
-      const int q = i / ts, s = i - q * ts;
-      gptr<float> row = q < df0 ? D0 + (int64_t)q * s0 : D1 + (int64_t)(q - df0) * s1;
-      const float* sp = Sb + (int64_t)s * nmax;
-      float acc = 0.0f;
-      for (int r = 0; r < o.n; ++r) acc += row[r] * sp[r];
-      const int dr = q < df0 ? o.d[0] + q : o.d[1] + (q - df0);
-      w.va[(int64_t)dr * w.vs + (int64_t)(t0 + s + 1) * w.B + b] = acc;
+    if (ndec > 0) {
+      mfma_f4x acc = {0.0f, 0.0f, 0.0f, 0.0f};
+      const int sb = lane % 16;
+      for (int ks = 0; ks < ksteps; ++ks) {
+        const int r = 4 * (wave + nw * ks) + lane / 16;
+        float a = 0.0f;
+#pragma unroll
+        for (int c = 0; c < kEnsDecCache; ++c)
+          if (c == ks) a = dA[c];
+        if (ks >= kEnsDecCache) a = dfrag(ks);
+        const float bb = (sb < ts && r < o.n) ? Sb[(int64_t)sb * nmax + r] : 0.0f;
+        acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a, bb, acc, 0, 0, 0);
+      }
+#pragma unroll
+      for (int q = 0; q < 4; ++q) red[(wave * 16 + 4 * (lane / 16) + q) * 16 + sb] = acc[q];
+      __syncthreads();
+      for (int i = tid; i < ndec * ts; i += nthr) {
+        const int q = i / ts, s = i - q * ts;
+        float sum = 0.0f;
+        for (int u = 0; u < nw; ++u) sum += red[(u * 16 + q) * 16 + s];
+        const int dr = q < df0 ? o.d[0] + q : o.d[1] + (q - df0);
+        w.va[(int64_t)dr * w.vs + (int64_t)(t0 + s + 1) * w.B + b] = sum;
+      }
     }
     if (o.s >= 0) {
       for (int i = tid; i < ts * o.n; i += nthr) {
@@ -252,5 +312,62 @@ __global__ void __launch_bounds__(1024) k_w_ens(WView w, float* pa, EnsDesc E, f
         pa[(o.ref + r) * (int64_t)w.B + b] = rf[j];
       }
     }
+  }
+}
+
+// ------------------------------------------------- products on fp32 MFMA
+// dst[m][c] += sum_k W[m][k] x[k][c] for every op of a merged DotInc group and
+// every (step, column) c of the window: per op a dense M x K by K x (T*B)
+// product.  Workgroup tile 64 x 64 (M x columns), K in slices of 16 staged in
+// LDS; each of the four wavefronts owns a 32 x 32 quarter and accumulates it
+// with v_mfma_f32_32x32x2f32 (A lane l: row l%32, k l/32; B lane l: k l/32,
+// column l%32; result register v: row 8(v/4) + 4(l/32) + v%4, column l%32).
+typedef float mfma_f16x __attribute__((ext_vector_type(16)));
+
+constexpr int kGemmBM = 64, kGemmBN = 64, kGemmBK = 16;
+
+__global__ void __launch_bounds__(256) k_w_gemm(WView w, int32_t M, int32_t K, int32_t mtiles, const float* Wt,
+                                                const int32_t* w_row, const int32_t* x_row, const int32_t* d_row,
+                                                int xblk) {
+  __shared__ float As[kGemmBK][kGemmBM + 4];
+  __shared__ float Bs[kGemmBK][kGemmBN + 4];
+  const int64_t N = (int64_t)w.T * w.B;
+  const int op = blockIdx.y / mtiles, mt = blockIdx.y - op * mtiles;
+  const int64_t m0 = (int64_t)mt * kGemmBM, c0 = (int64_t)blockIdx.x * kGemmBN;
+  const int tid = threadIdx.x, lane = tid % 64, wave = tid / 64;
+  const int wm = wave / 2, wn = wave % 2;
+  gptr<float> A = G(Wt) + (int64_t)G(w_row)[op] * K;
+  const float* X = w.va + (int64_t)G(x_row)[op] * w.vs + (int64_t)xblk * w.B;
+  float* C = w.va + (int64_t)G(d_row)[op] * w.vs + w.B;
+  mfma_f16x acc;
+#pragma unroll
+  for (int v = 0; v < 16; ++v) acc[v] = 0.0f;
+  for (int32_t k0 = 0; k0 < K; k0 += kGemmBK) {
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const int idx = tid + q * 256;
+      const int mm = idx / kGemmBK, kk = idx % kGemmBK;
+      const int64_t m = m0 + mm;
+      const int32_t k = k0 + kk;
+      As[kk][mm] = (m < M && k < K) ? A[m * K + k] : 0.0f;
+      const int kb = idx / kGemmBN, jj = idx % kGemmBN;
+      const int32_t kx = k0 + kb;
+      const int64_t c = c0 + jj;
+      Bs[kb][jj] = (kx < K && c < N) ? X[(int64_t)kx * w.vs + c] : 0.0f;
+    }
+    __syncthreads();
+#pragma unroll
+    for (int kk = 0; kk < kGemmBK; kk += 2) {
+      const float a = As[kk + lane / 32][wm * 32 + lane % 32];
+      const float b = Bs[kk + lane / 32][wn * 32 + lane % 32];
+      acc = __builtin_amdgcn_mfma_f32_32x32x2f32(a, b, acc, 0, 0, 0);
+    }
+    __syncthreads();
+  }
+#pragma unroll
+  for (int v = 0; v < 16; ++v) {
+    const int64_t m = m0 + wm * 32 + 8 * (v / 4) + 4 * (lane / 32) + (v % 4);
+    const int64_t c = c0 + wn * 32 + lane % 32;
+    if (m < M && c < N) C[m * w.vs + c] += acc[v];
   }
 }

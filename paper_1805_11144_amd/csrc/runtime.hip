@@ -610,9 +610,35 @@ void ens_shape(ms_sim* s, Launch& l, const LGroup& g) {
   if (l.npt > 4) fail(MS_E_INVALID, "ensemble too large for the window driver (more than 4096 neurons)");
   if (l.npt == 3) l.npt = 4;
   const int64_t per_step = (int64_t)l.ens.d + nmax;
-  l.ts = (int32_t)std::min<int64_t>(16, (int64_t)(s->lds_limit / 4) / std::max<int64_t>(1, per_step));
+  const int64_t red = (int64_t)(l.nthr / 64) * 256;   // per-wavefront 16 x 16 decode partials
+  l.ts = (int32_t)std::min<int64_t>(16, ((int64_t)(s->lds_limit / 4) - red) / std::max<int64_t>(1, per_step));
   if (l.ts < 1) fail(MS_E_INVALID, "ensemble too large for the window driver's LDS staging");
-  l.lds = (size_t)l.ts * per_step * sizeof(float);
+  l.lds = (size_t)(l.ts * per_step + red) * sizeof(float);
+}
+
+// Steps per window for a run of n_steps: as many as the run needs, up to the
+// memory budget; the versioned array is reallocated (keeping block 0, the
+// carried state) when a longer window is wanted.  Blocks 1..W are always
+// written before they are read; block 0 starts at zero.
+void ensure_window(ms_sim* s, int64_t n_steps) {
+  const WindowPlan& w = *s->wplan;
+  const int32_t B = s->B;
+  const double per_step = (double)std::max<int64_t>(1, w.rows_v) * B * sizeof(float);
+  const int64_t cap = (int64_t)std::max<double>(1.0, std::min<double>(kMaxWindow, std::floor(kWindowBytes / per_step) - 1));
+  const int32_t want = (int32_t)std::min<int64_t>(cap, std::max<int64_t>(1, n_steps));
+  if (s->va && want <= s->W) return;
+  const int64_t rows = std::max<int64_t>(1, w.rows_v);
+  const int64_t vs = (int64_t)(want + 1) * B;
+  float* nva = dev_alloc<float>((size_t)rows * vs);
+  HIPCHECK(hipMemsetAsync(nva, 0, (size_t)rows * vs * sizeof(float), s->stream));
+  if (s->va) {
+    HIPCHECK(hipMemcpy2DAsync(nva, vs * 4, s->va, s->vs * 4, (size_t)B * 4, rows, hipMemcpyDeviceToDevice, s->stream));
+    HIPCHECK(hipStreamSynchronize(s->stream));
+    HIPCHECK(hipFree(s->va));
+  }
+  s->va = nva;
+  s->W = want;
+  s->vs = vs;
 }
 
 void setup_window(ms_sim* s) {
@@ -622,11 +648,8 @@ void setup_window(ms_sim* s) {
   int lds_max = 0;
   HIPCHECK(hipDeviceGetAttribute(&lds_max, hipDeviceAttributeMaxSharedMemoryPerBlock, s->device));
   s->lds_limit = (size_t)lds_max;
-  const double per_step = (double)std::max<int64_t>(1, w.rows_v) * B * sizeof(float);
-  s->W = (int32_t)std::max<double>(1.0, std::min<double>(kMaxWindow, std::floor(kWindowBytes / per_step) - 1));
-  s->vs = (int64_t)(s->W + 1) * B;
-  s->va = dev_alloc<float>((size_t)std::max<int64_t>(1, w.rows_v) * s->vs);
   s->pa = dev_alloc<float>((size_t)std::max<int64_t>(1, w.rows_p) * B);
+  ensure_window(s, 1);
   std::vector<LGroup> groups;
   for (const WPhase& ph : w.phases) groups.push_back(ph.g);
   build_launches(s, groups, s->wl, w.probe_rows, &s->wprobe_src);
@@ -643,7 +666,6 @@ void setup_window(ms_sim* s) {
     HIPCHECK(hipFuncSetAttribute((const void*)k_w_ens<2>, hipFuncAttributeMaxDynamicSharedMemorySize, (int)s->lds_limit));
     HIPCHECK(hipFuncSetAttribute((const void*)k_w_ens<4>, hipFuncAttributeMaxDynamicSharedMemorySize, (int)s->lds_limit));
   }
-  HIPCHECK(hipMemset(s->va, 0, (size_t)std::max<int64_t>(1, w.rows_v) * s->vs * sizeof(float)));
   HIPCHECK(hipMemset(s->pa, 0, (size_t)std::max<int64_t>(1, w.rows_p) * B * sizeof(float)));
 }
 
@@ -679,8 +701,17 @@ void launch_phase(ms_sim* s, const Launch& l, int32_t T, int64_t t0) {
                          l.ptr);
       break;
     case OP_DOT_INC:
-      hipLaunchKernelGGL(k_w_dot, dim3(grid_items((double)l.rows * l.M * tb)), dim3(kBlock), 0, q, w, l.rows, l.M,
-                         l.K, l.a_base, l.w_row, l.x_row, l.d_row, l.src_blk);
+      if (l.K >= 16) {
+        const int32_t mtiles = (l.M + kGemmBM - 1) / kGemmBM;
+        const double ntiles = std::ceil(tb / kGemmBN);
+        if (ntiles >= 2147483648.0 || (double)mtiles * l.rows > 65535.0)
+          fail(MS_E_INVALID, "window product too large for the GEMM grid");
+        hipLaunchKernelGGL(k_w_gemm, dim3((unsigned)ntiles, (unsigned)(mtiles * l.rows)), dim3(256), 0, q, w, l.M,
+                           l.K, mtiles, l.a_base, l.w_row, l.x_row, l.d_row, l.src_blk);
+      } else {
+        hipLaunchKernelGGL(k_w_dot, dim3(grid_items((double)l.rows * l.M * tb)), dim3(kBlock), 0, q, w, l.rows,
+                           l.M, l.K, l.a_base, l.w_row, l.x_row, l.d_row, l.src_blk);
+      }
       break;
     case OP_LIF:
       hipLaunchKernelGGL(k_w_lif, dim3(grid_items((double)l.rows * s->B)), dim3(kBlock), 0, q, w, l.rows, l.src,
@@ -710,6 +741,7 @@ void launch_phase(ms_sim* s, const Launch& l, int32_t T, int64_t t0) {
 
 void run_window(ms_sim* s, int64_t n_steps) {
   const WindowPlan& w = *s->wplan;
+  ensure_window(s, n_steps);
   for (int64_t t0 = 0; t0 < n_steps; t0 += s->W) {
     const int32_t T = (int32_t)std::min<int64_t>(s->W, n_steps - t0);
     for (const Launch& l : s->wl) launch_phase(s, l, T, t0);
@@ -890,7 +922,8 @@ ms_status ms_sim_reset(ms_sim* s) {
     if (!s) fail(MS_E_INVALID, "NULL sim");
     DeviceGuard dg(s->device);
     HIPCHECK(hipMemsetAsync(s->state, 0, std::max<size_t>(1, s->state_rows) * s->B * 4, s->stream));
-    if (s->va) HIPCHECK(hipMemsetAsync(s->va, 0, (size_t)std::max<int64_t>(1, s->wplan->rows_v) * s->vs * 4, s->stream));
+    if (s->va)   // block 0 (the carried state); the other blocks are written before they are read
+      HIPCHECK(hipMemset2DAsync(s->va, s->vs * 4, 0, (size_t)s->B * 4, std::max<int64_t>(1, s->wplan->rows_v), s->stream));
     if (s->pa) HIPCHECK(hipMemsetAsync(s->pa, 0, (size_t)std::max<int64_t>(1, s->wplan->rows_p) * s->B * 4, s->stream));
     HIPCHECK(hipMemsetAsync(s->ctr, 0, 2 * sizeof(int64_t), s->stream));
     HIPCHECK(hipStreamSynchronize(s->stream));
