@@ -237,6 +237,7 @@ struct WPhase {
   int32_t level = 0;
   int32_t src_blk = 1;    // src rows: 1 = this step's value, 0 = the previous step's
   int32_t a_blk = 1;      // the same for a batched ElementwiseInc `a`
+  bool exclusive = false; // no other phase of its level writes a signal it writes
 };
 
 struct WindowPlan {

@@ -186,33 +186,42 @@ __global__ void k_w_carry(WView w, int64_t rows) {
 }
 
 // ------------------------------------------------- fused ensembles over a window
-// One workgroup per (op, batch column); thread tid owns neurons tid + j*blockDim
-// (j < NPT), whose voltage, refractory time, bias and encoder row stay in
-// registers for the whole window.  The window is processed in sub-windows of
-// `ts_max` (<= 16) steps: the sub-window's inputs x are staged in LDS, every
-// thread advances its neurons through the sub-window and leaves their outputs
-// in LDS (no synchronisation between steps: a neuron depends only on its own
-// past), then the decoded outputs of all sub-window steps, a [ndec x n] by
-// [n x ts] product, are formed on MFMA (v_mfma_f32_16x16x4f32: A lane l row
-// l%16, k l/16; B lane l k l/16, column l%16; result register v row
-// 4(l/16) + v, column l%16).  Each wavefront takes every nw-th group of four
-// neurons, keeps its decoder fragments in registers for the whole window, and
-// the wavefronts' partial 16 x 16 tiles are summed in LDS.
+// One workgroup per (op, batch column), for the whole window, in sub-windows
+// of ts_max steps (a multiple of 16).  Per sub-window:
+//   1. input currents J = E x + bias for all the sub-window's steps on MFMA
+//      (v_mfma_f32_16x16x4f32; A lane l: row l%16, k l/16; B lane l: k l/16,
+//      column l%16; result register v: row 4(l/16) + v, column l%16), with
+//      16-neuron tiles spread over the wavefronts, written to LDS as [step][neuron];
+//   2. every thread advances its own neurons (voltage and refractory time in
+//      registers for the whole window) through the sub-window, overwriting
+//      each J in LDS with the neuron's output -- no synchronisation between
+//      steps, since a neuron depends only on its own past;
+//   3. decoded outputs, [ndec x n] by [n x ts], on MFMA: each wavefront takes
+//      every nw-th group of four neurons (its decoder fragments stay in
+//      registers for the whole window) and the partial 16 x 16 tiles are
+//      summed in LDS.
+// The next sub-window's inputs are fetched into registers before step 1 and
+// stored to LDS after it, so their latency overlaps the work.
 typedef float mfma_f4x __attribute__((ext_vector_type(4)));
-constexpr int kEnsDecCache = 16;   // MFMA k-steps whose decoder fragments stay in registers
+constexpr int kEnsDecCache = 16;   // decoder k-steps whose fragments stay in registers
+constexpr int kEnsEncCache = 16;   // encoder fragments kept in registers
+constexpr int kEnsXPre = 4;        // prefetched input values per thread
 
 template <int NPT>
-__global__ void __launch_bounds__(1024) k_w_ens(WView w, float* pa, EnsDesc E, float dt, int32_t nmax,
+__global__ void __launch_bounds__(512) k_w_ens(WView w, float* pa, EnsDesc E, float dt, int32_t nmax,
                                                 int32_t ts_max, int xblk) {
   extern __shared__ float lds[];
   const int op = blockIdx.x;
   const int64_t b = blockIdx.y;
   const int tid = threadIdx.x, nthr = blockDim.x, lane = tid % 64, wave = tid / 64, nw = nthr / 64;
   const EnsOp o = load_op(E.ops, op);
+  const int n = o.n;
   const int d = o.x >= 0 ? E.d : 0, ndec = E.ndec, df0 = E.df[0];
-  float* X = lds;                                  // [ts_max][E.d]
-  float* Sb = X + (int64_t)ts_max * E.d;           // [ts_max][nmax]
-  float* red = Sb + (int64_t)ts_max * nmax;        // [nw][16][16]
+  const int dp = E.d > 0 ? E.d : 1;
+  const int ctiles = ts_max / 16;
+  float* X = lds;                                   // [ts_max][dp]
+  float* Jb = X + ts_max * dp;                      // [ts_max][nmax]: currents, then outputs
+  float* red = Jb + (int64_t)ts_max * nmax;         // [nw][ctiles][16][16]
   gptr<float> enc = G(E.enc) + (int64_t)o.enc * E.d;
   gptr<float> bias = G(E.bias) + o.bias;
   gptr<float> D0 = G(E.D[0]) + (int64_t)o.D[0] * E.Dcols[0];
@@ -221,84 +230,152 @@ __global__ void __launch_bounds__(1024) k_w_ens(WView w, float* pa, EnsDesc E, f
   const bool spiking = E.ntype == 0;
   const bool bf = spiking && dt * o.inv_tau <= 0.0625f;   // branch-free spiking update applies
   const float amp_dt = o.amp / dt;
-  float v[NPT], rf[NPT], bj[NPT], er[NPT][kMaxXReg];
+  const float* xsrc = w.va + (int64_t)(o.x >= 0 ? o.x : 0) * w.vs + (int64_t)xblk * w.B + b;
+  // neuron state
+  float v[NPT], rf[NPT];
 #pragma unroll
   for (int j = 0; j < NPT; ++j) {
     const int r = tid + j * nthr;
-    const bool live = r < o.n;
-    v[j] = (live && spiking) ? pa[(o.V + r) * (int64_t)w.B + b] : 0.0f;
-    rf[j] = (live && spiking) ? pa[(o.ref + r) * (int64_t)w.B + b] : 0.0f;
-    bj[j] = live ? bias[r] : 0.0f;
-#pragma unroll
-    for (int k = 0; k < kMaxXReg; ++k) er[j][k] = (live && k < d) ? enc[(int64_t)r * E.d + k] : 0.0f;
+    const bool live = spiking && r < n;
+    v[j] = live ? pa[(int64_t)(o.V + r) * w.B + b] : 0.0f;
+    rf[j] = live ? pa[(int64_t)(o.ref + r) * w.B + b] : 0.0f;
   }
-  // decoder fragment of this lane for MFMA k-step ks: row q = lane % 16,
-  // neuron r = 4 * (wave + nw * ks) + lane / 16
+  // encoder fragments: tile t = wave + nw * i, k-step kk; row r = 16 t + lane%16, k = 4 kk + lane/16
+  const int ntile = (n + 15) / 16, tpw = (ntile - wave + nw - 1) / nw, kd = (d + 3) / 4;
+  auto efrag = [&](int i, int kk) {
+    const int r = 16 * (wave + nw * i) + lane % 16, k = 4 * kk + lane / 16;
+    return (r < n && k < d) ? enc[(int64_t)r * E.d + k] : 0.0f;
+  };
+  float eA[kEnsEncCache];
+#pragma unroll
+  for (int c = 0; c < kEnsEncCache; ++c) {
+    const int i = kd > 0 ? c / kd : 0, kk = kd > 0 ? c % kd : 0;
+    eA[c] = (kd > 0 && i < tpw) ? efrag(i, kk) : 0.0f;
+  }
+  // decoder fragments: k-step ks, row q = lane%16, neuron r = 4 (wave + nw ks) + lane/16
   const int qa = lane % 16;
   gptr<float> drow = qa < df0 ? D0 + (int64_t)qa * s0 : D1 + (int64_t)(qa - df0) * s1;
-  const int ksteps = (o.n + 4 * nw - 1) / (4 * nw);
+  const int ksteps = (n + 4 * nw - 1) / (4 * nw);
   auto dfrag = [&](int ks) {
     const int r = 4 * (wave + nw * ks) + lane / 16;
-    return (qa < ndec && r < o.n) ? drow[r] : 0.0f;
+    return (qa < ndec && r < n) ? drow[r] : 0.0f;
   };
   float dA[kEnsDecCache];
 #pragma unroll
-  for (int ks = 0; ks < kEnsDecCache; ++ks) dA[ks] = (ndec > 0 && ks < ksteps) ? dfrag(ks) : 0.0f;
+  for (int c = 0; c < kEnsDecCache; ++c) dA[c] = (ndec > 0 && c < ksteps) ? dfrag(c) : 0.0f;
+  // first sub-window's inputs
+  {
+    const int ts = min(ts_max, w.T);
+    for (int i = tid; i < ts * d; i += nthr) {
+      const int st = i / d, k = i - st * d;
+      X[st * dp + k] = xsrc[(int64_t)k * w.vs + (int64_t)st * w.B];
+    }
+  }
+  __syncthreads();
   for (int32_t t0 = 0; t0 < w.T; t0 += ts_max) {
     const int ts = min(ts_max, w.T - t0);
-    for (int i = tid; i < ts * d; i += nthr) {
-      const int s = i / d, k = i - s * d;
-      X[s * E.d + k] = w.va[(int64_t)(o.x + k) * w.vs + (int64_t)(t0 + s + xblk) * w.B + b];
+    // 0. fetch the next sub-window's inputs
+    const int32_t t1 = t0 + ts_max;
+    const int tsn = t1 < w.T ? min(ts_max, w.T - t1) : 0;
+    float xpre[kEnsXPre];
+#pragma unroll
+    for (int c = 0; c < kEnsXPre; ++c) {
+      const int i = tid + c * nthr;
+      float val = 0.0f;
+      if (i < tsn * d) {
+        const int st = i / d, k = i - st * d;
+        val = xsrc[(int64_t)k * w.vs + (int64_t)(t1 + st) * w.B];
+      }
+      xpre[c] = val;
     }
-    __syncthreads();
+    // 1. J = E x + bias
+    for (int i = 0; i < tpw; ++i) {
+      const int tile = wave + nw * i;
+      float bb[4];
 #pragma unroll
-    for (int j = 0; j < NPT; ++j) {
-      const int r = tid + j * nthr;
-      if (r < o.n) {
-        for (int s = 0; s < ts; ++s) {
-          float jc = bj[j];
-          if (d <= kMaxXReg) {
+      for (int u = 0; u < 4; ++u) {
+        const int r = 16 * tile + 4 * (lane / 16) + u;
+        bb[u] = r < n ? bias[r] : 0.0f;
+      }
+      for (int ct = 0; ct < ctiles; ++ct) {
+        mfma_f4x acc = {0.0f, 0.0f, 0.0f, 0.0f};
+        const int sc = 16 * ct + lane % 16;
+        for (int kk = 0; kk < kd; ++kk) {
+          const int c = i * kd + kk;
+          float a = 0.0f;
 #pragma unroll
-            for (int k = 0; k < kMaxXReg; ++k)
-              if (k < d) jc += er[j][k] * X[s * E.d + k];
-          } else {
-            for (int k = 0; k < d; ++k) jc += enc[(int64_t)r * E.d + k] * X[s * E.d + k];
+          for (int cc = 0; cc < kEnsEncCache; ++cc)
+            if (cc == c) a = eA[cc];
+          if (c >= kEnsEncCache) a = efrag(i, kk);
+          const int k = 4 * kk + lane / 16;
+          const float xb = (sc < ts && k < d) ? X[sc * dp + k] : 0.0f;
+          acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a, xb, acc, 0, 0, 0);
+        }
+        if (sc < ts) {
+#pragma unroll
+          for (int u = 0; u < 4; ++u) {
+            const int r = 16 * tile + 4 * (lane / 16) + u;
+            if (r < n) Jb[sc * nmax + r] = acc[u] + bb[u];
           }
-          Sb[(int64_t)s * nmax + r] =
-              bf ? lif_update_bf(jc, v[j], rf[j], o.tau_rc, o.tau_ref, amp_dt, o.full, dt, o.inv_tau)
-                 : neuron_update(E.ntype, jc, v[j], rf[j], o.tau_rc, o.tau_ref, o.amp, o.full, dt, o.inv_tau);
         }
       }
     }
     __syncthreads();
-    if (ndec > 0) {
-      mfma_f4x acc = {0.0f, 0.0f, 0.0f, 0.0f};
-      const int sb = lane % 16;
-      for (int ks = 0; ks < ksteps; ++ks) {
-        const int r = 4 * (wave + nw * ks) + lane / 16;
-        float a = 0.0f;
+    // next inputs into LDS (every read of this sub-window's X is done)
 #pragma unroll
-        for (int c = 0; c < kEnsDecCache; ++c)
-          if (c == ks) a = dA[c];
-        if (ks >= kEnsDecCache) a = dfrag(ks);
-        const float bb = (sb < ts && r < o.n) ? Sb[(int64_t)sb * nmax + r] : 0.0f;
-        acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a, bb, acc, 0, 0, 0);
-      }
-#pragma unroll
-      for (int q = 0; q < 4; ++q) red[(wave * 16 + 4 * (lane / 16) + q) * 16 + sb] = acc[q];
-      __syncthreads();
-      for (int i = tid; i < ndec * ts; i += nthr) {
-        const int q = i / ts, s = i - q * ts;
-        float sum = 0.0f;
-        for (int u = 0; u < nw; ++u) sum += red[(u * 16 + q) * 16 + s];
-        const int dr = q < df0 ? o.d[0] + q : o.d[1] + (q - df0);
-        w.va[(int64_t)dr * w.vs + (int64_t)(t0 + s + 1) * w.B + b] = sum;
+    for (int c = 0; c < kEnsXPre; ++c) {
+      const int i = tid + c * nthr;
+      if (i < tsn * d) {
+        const int st = i / d, k = i - st * d;
+        X[st * dp + k] = xpre[c];
       }
     }
+    // 2. neurons through the sub-window
+#pragma unroll
+    for (int j = 0; j < NPT; ++j) {
+      const int r = tid + j * nthr;
+      if (r < n) {
+        for (int st = 0; st < ts; ++st) {
+          float* cell = Jb + st * nmax + r;
+          const float jc = *cell;
+          *cell = bf ? lif_update_bf(jc, v[j], rf[j], o.tau_rc, o.tau_ref, amp_dt, o.full, dt, o.inv_tau)
+                     : neuron_update(E.ntype, jc, v[j], rf[j], o.tau_rc, o.tau_ref, o.amp, o.full, dt, o.inv_tau);
+        }
+      }
+    }
+    __syncthreads();
+    // 3. decoded outputs
+    if (ndec > 0) {
+      for (int ct = 0; ct < ctiles; ++ct) {
+        mfma_f4x acc = {0.0f, 0.0f, 0.0f, 0.0f};
+        const int sc = 16 * ct + lane % 16;
+        for (int ks = 0; ks < ksteps; ++ks) {
+          const int r = 4 * (wave + nw * ks) + lane / 16;
+          float a = 0.0f;
+#pragma unroll
+          for (int cc = 0; cc < kEnsDecCache; ++cc)
+            if (cc == ks) a = dA[cc];
+          if (ks >= kEnsDecCache) a = dfrag(ks);
+          const float sb = (sc < ts && r < n) ? Jb[sc * nmax + r] : 0.0f;
+          acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a, sb, acc, 0, 0, 0);
+        }
+#pragma unroll
+        for (int u = 0; u < 4; ++u)
+          red[((wave * ctiles + ct) * 16 + 4 * (lane / 16) + u) * 16 + lane % 16] = acc[u];
+      }
+    }
+    __syncthreads();
+    for (int i = tid; i < ndec * ts; i += nthr) {
+      const int q = i / ts, st = i - q * ts;
+      float sum = 0.0f;
+      for (int u = 0; u < nw; ++u) sum += red[((u * ctiles + st / 16) * 16 + q) * 16 + st % 16];
+      const int dr = q < df0 ? o.d[0] + q : o.d[1] + (q - df0);
+      w.va[(int64_t)dr * w.vs + (int64_t)(t0 + st + 1) * w.B + b] = sum;
+    }
     if (o.s >= 0) {
-      for (int i = tid; i < ts * o.n; i += nthr) {
-        const int s = i / o.n, r = i - s * o.n;
-        w.va[(int64_t)(o.s + r) * w.vs + (int64_t)(t0 + s + 1) * w.B + b] = Sb[(int64_t)s * nmax + r];
+      for (int i = tid; i < ts * n; i += nthr) {
+        const int st = i / n, r = i - st * n;
+        w.va[(int64_t)(o.s + r) * w.vs + (int64_t)(t0 + st + 1) * w.B + b] = Jb[st * nmax + r];
       }
     }
     __syncthreads();
@@ -307,9 +384,9 @@ __global__ void __launch_bounds__(1024) k_w_ens(WView w, float* pa, EnsDesc E, f
 #pragma unroll
     for (int j = 0; j < NPT; ++j) {
       const int r = tid + j * nthr;
-      if (r < o.n) {
-        pa[(o.V + r) * (int64_t)w.B + b] = v[j];
-        pa[(o.ref + r) * (int64_t)w.B + b] = rf[j];
+      if (r < n) {
+        pa[(int64_t)(o.V + r) * w.B + b] = v[j];
+        pa[(int64_t)(o.ref + r) * w.B + b] = rf[j];
       }
     }
   }

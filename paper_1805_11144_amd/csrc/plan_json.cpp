@@ -140,7 +140,8 @@ std::string plan_to_json(const Plan& p) {
     for (size_t k = 0; k < w.phases.size(); ++k) {
       if (k) o << ',';
       o << "{\"level\":" << w.phases[k].level << ",\"src_blk\":" << w.phases[k].src_blk
-        << ",\"a_blk\":" << w.phases[k].a_blk << ",\"group\":";
+        << ",\"a_blk\":" << w.phases[k].a_blk << ",\"exclusive\":" << (w.phases[k].exclusive ? "true" : "false")
+        << ",\"group\":";
       jgroup(o, p, w.phases[k].g);
       o << '}';
     }

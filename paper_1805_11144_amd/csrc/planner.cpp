@@ -776,6 +776,27 @@ WindowPlan make_window_plan(const Plan& p) {
       }
     }
   }
+  // phases of a level may run concurrently only if their written signals are disjoint
+  for (size_t a = 0; a < w.phases.size();) {
+    size_t e = a;
+    while (e < w.phases.size() && w.phases[e].level == w.phases[a].level) ++e;
+    std::map<int32_t, int32_t> writers;
+    std::vector<std::set<int32_t>> wsets(e - a);
+    for (size_t k = a; k < e; ++k) {
+      for (int32_t op : w.phases[k].g.ops) {
+        access(ir.ops[op], s_, i_, r_, u_);
+        for (const auto* L : {&s_, &i_, &u_})
+          for (int32_t sg : *L) if (batched(sg)) wsets[k - a].insert(sg);
+      }
+      for (int32_t sg : wsets[k - a]) writers[sg]++;
+    }
+    for (size_t k = a; k < e; ++k) {
+      bool ex = true;
+      for (int32_t sg : wsets[k - a]) ex = ex && writers[sg] == 1;
+      w.phases[k].exclusive = ex;
+    }
+    a = e;
+  }
   for (const auto& pr : ir.probes)
     for (int32_t i = 0; i < pr.src.len; ++i) w.probe_rows.push_back((int32_t)(w.sig_row[pr.src.sig] + pr.src.start + i));
   w.ok = true;

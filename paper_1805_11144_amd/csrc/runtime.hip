@@ -117,6 +117,9 @@ struct ms_sim {
   int32_t W = 0;                     // steps per window
   int64_t vs = 0;                    // row stride of va
   const int32_t* wprobe_src = nullptr;
+  static constexpr int kSide = 3;    // extra streams for independent phases of one level
+  hipStream_t side[kSide] = {};
+  hipEvent_t side_ev[kSide + 1] = {};
   std::vector<std::vector<float>> host_bases;   // host copies of parameter bases
 };
 
@@ -155,6 +158,10 @@ void free_sim(ms_sim* s) {
   for (void* p : s->extra_allocs) f(p);
   if (s->ev0) (void)hipEventDestroy(s->ev0);
   if (s->ev1) (void)hipEventDestroy(s->ev1);
+  for (int k = 0; k < ms_sim::kSide; ++k)
+    if (s->side[k]) (void)hipStreamDestroy(s->side[k]);
+  for (int k = 0; k <= ms_sim::kSide; ++k)
+    if (s->side_ev[k]) (void)hipEventDestroy(s->side_ev[k]);
   if (s->own_stream && s->stream) (void)hipStreamDestroy(s->stream);
 }
 
@@ -605,15 +612,22 @@ void ens_shape(ms_sim* s, Launch& l, const LGroup& g) {
   int32_t nmax = 1;
   for (int32_t n : g.ens_n) nmax = std::max(nmax, n);
   l.nmax = nmax;
-  l.nthr = (int32_t)std::min<int64_t>(1024, ((int64_t)nmax + 63) / 64 * 64);
+  l.nthr = (int32_t)std::min<int64_t>(512, ((int64_t)nmax + 63) / 64 * 64);
   l.npt = (nmax + l.nthr - 1) / l.nthr;
-  if (l.npt > 4) fail(MS_E_INVALID, "ensemble too large for the window driver (more than 4096 neurons)");
-  if (l.npt == 3) l.npt = 4;
-  const int64_t per_step = (int64_t)l.ens.d + nmax;
-  const int64_t red = (int64_t)(l.nthr / 64) * 256;   // per-wavefront 16 x 16 decode partials
-  l.ts = (int32_t)std::min<int64_t>(16, ((int64_t)(s->lds_limit / 4) - red) / std::max<int64_t>(1, per_step));
-  if (l.ts < 1) fail(MS_E_INVALID, "ensemble too large for the window driver's LDS staging");
-  l.lds = (size_t)(l.ts * per_step + red) * sizeof(float);
+  if (l.npt > 8) fail(MS_E_INVALID, "ensemble too large for the window driver (more than 4096 neurons)");
+  l.npt = l.npt <= 1 ? 1 : l.npt <= 2 ? 2 : l.npt <= 4 ? 4 : 8;
+  const int64_t nw = l.nthr / 64, dp = std::max<int32_t>(1, l.ens.d);
+  // sub-window: the longest (a multiple of 16, at most 64 steps) that keeps
+  // about 16 wavefronts per CU resident within the CU's LDS; the prefetched
+  // inputs must fit the per-thread registers
+  auto bytes = [&](int64_t ts) { return (ts * (dp + nmax) + nw * (ts / 16) * 256) * (int64_t)sizeof(float); };
+  const int64_t wgs = std::max<int64_t>(1, 16 / nw);
+  int64_t ts = 64;
+  while (ts > 16 && (bytes(ts) * wgs > (int64_t)s->lds_limit || ts * l.ens.d > (int64_t)kEnsXPre * l.nthr)) ts -= 16;
+  if (bytes(ts) > (int64_t)s->lds_limit || ts * l.ens.d > (int64_t)kEnsXPre * l.nthr)
+    fail(MS_E_INVALID, "ensemble too large for the window driver's LDS staging");
+  l.ts = (int32_t)ts;
+  l.lds = (size_t)bytes(ts);
 }
 
 // Steps per window for a run of n_steps: as many as the run needs, up to the
@@ -650,6 +664,8 @@ void setup_window(ms_sim* s) {
   s->lds_limit = (size_t)lds_max;
   s->pa = dev_alloc<float>((size_t)std::max<int64_t>(1, w.rows_p) * B);
   ensure_window(s, 1);
+  for (int k = 0; k < ms_sim::kSide; ++k) HIPCHECK(hipStreamCreateWithFlags(&s->side[k], hipStreamNonBlocking));
+  for (int k = 0; k <= ms_sim::kSide; ++k) HIPCHECK(hipEventCreateWithFlags(&s->side_ev[k], hipEventDisableTiming));
   std::vector<LGroup> groups;
   for (const WPhase& ph : w.phases) groups.push_back(ph.g);
   build_launches(s, groups, s->wl, w.probe_rows, &s->wprobe_src);
@@ -665,6 +681,7 @@ void setup_window(ms_sim* s) {
     HIPCHECK(hipFuncSetAttribute((const void*)k_w_ens<1>, hipFuncAttributeMaxDynamicSharedMemorySize, (int)s->lds_limit));
     HIPCHECK(hipFuncSetAttribute((const void*)k_w_ens<2>, hipFuncAttributeMaxDynamicSharedMemorySize, (int)s->lds_limit));
     HIPCHECK(hipFuncSetAttribute((const void*)k_w_ens<4>, hipFuncAttributeMaxDynamicSharedMemorySize, (int)s->lds_limit));
+    HIPCHECK(hipFuncSetAttribute((const void*)k_w_ens<8>, hipFuncAttributeMaxDynamicSharedMemorySize, (int)s->lds_limit));
   }
   HIPCHECK(hipMemset(s->pa, 0, (size_t)std::max<int64_t>(1, w.rows_p) * B * sizeof(float)));
 }
@@ -674,11 +691,10 @@ inline unsigned grid_items(double n) {
   return (unsigned)std::max<int64_t>(1, ((int64_t)n + kBlock - 1) / kBlock);
 }
 
-void launch_phase(ms_sim* s, const Launch& l, int32_t T, int64_t t0) {
+void launch_phase(ms_sim* s, const Launch& l, int32_t T, int64_t t0, hipStream_t q) {
   if (l.rows == 0) return;
   const WView w{s->va, s->vs, s->B, T};
   const double tb = (double)T * s->B;
-  hipStream_t q = s->stream;
   switch (l.type) {
     case OP_FEED:
       hipLaunchKernelGGL(k_w_feed, dim3(grid_items(l.rows * tb)), dim3(kBlock), 0, q, w, l.rows, l.dst, l.feed_rows,
@@ -731,8 +747,10 @@ void launch_phase(ms_sim* s, const Launch& l, int32_t T, int64_t t0) {
         hipLaunchKernelGGL(k_w_ens<1>, grid, dim3(l.nthr), l.lds, q, w, s->pa, l.ens, s->dt, l.nmax, l.ts, l.src_blk);
       else if (l.npt == 2)
         hipLaunchKernelGGL(k_w_ens<2>, grid, dim3(l.nthr), l.lds, q, w, s->pa, l.ens, s->dt, l.nmax, l.ts, l.src_blk);
-      else
+      else if (l.npt == 4)
         hipLaunchKernelGGL(k_w_ens<4>, grid, dim3(l.nthr), l.lds, q, w, s->pa, l.ens, s->dt, l.nmax, l.ts, l.src_blk);
+      else
+        hipLaunchKernelGGL(k_w_ens<8>, grid, dim3(l.nthr), l.lds, q, w, s->pa, l.ens, s->dt, l.nmax, l.ts, l.src_blk);
       break;
     }
     default: fail(MS_E_INVALID, "unknown group type");
@@ -744,7 +762,29 @@ void run_window(ms_sim* s, int64_t n_steps) {
   ensure_window(s, n_steps);
   for (int64_t t0 = 0; t0 < n_steps; t0 += s->W) {
     const int32_t T = (int32_t)std::min<int64_t>(s->W, n_steps - t0);
-    for (const Launch& l : s->wl) launch_phase(s, l, T, t0);
+    // phases of one level are independent: spread them over the side streams
+    for (size_t a = 0; a < s->wl.size();) {
+      size_t e = a + 1;
+      while (e < s->wl.size() && w.phases[e].level == w.phases[a].level) ++e;
+      if (e - a == 1) {
+        launch_phase(s, s->wl[a], T, t0, s->stream);
+      } else {
+        const int used = (int)std::min<size_t>(ms_sim::kSide, e - a - 1);
+        HIPCHECK(hipEventRecord(s->side_ev[ms_sim::kSide], s->stream));
+        for (int k = 0; k < used; ++k) HIPCHECK(hipStreamWaitEvent(s->side[k], s->side_ev[ms_sim::kSide], 0));
+        size_t rr = 0;   // exclusive phases round-robin over the streams; the rest in order on the main stream
+        for (size_t i = a; i < e; ++i) {
+          if (!w.phases[i].exclusive) { launch_phase(s, s->wl[i], T, t0, s->stream); continue; }
+          const size_t slot = rr++ % (size_t)(used + 1);
+          launch_phase(s, s->wl[i], T, t0, slot == 0 ? s->stream : s->side[slot - 1]);
+        }
+        for (int k = 0; k < used; ++k) {
+          HIPCHECK(hipEventRecord(s->side_ev[k], s->side[k]));
+          HIPCHECK(hipStreamWaitEvent(s->stream, s->side_ev[k], 0));
+        }
+      }
+      a = e;
+    }
     const WView v{s->va, s->vs, s->B, T};
     const int32_t pr = (int32_t)w.probe_rows.size();
     if (pr > 0)
