@@ -186,42 +186,41 @@ __global__ void k_w_carry(WView w, int64_t rows) {
 }
 
 // ------------------------------------------------- fused ensembles over a window
-// One workgroup per (op, batch column), for the whole window, in sub-windows
-// of ts_max steps (a multiple of 16).  Per sub-window:
-//   1. input currents J = E x + bias for all the sub-window's steps on MFMA
-//      (v_mfma_f32_16x16x4f32; A lane l: row l%16, k l/16; B lane l: k l/16,
-//      column l%16; result register v: row 4(l/16) + v, column l%16), with
-//      16-neuron tiles spread over the wavefronts, written to LDS as [step][neuron];
-//   2. every thread advances its own neurons (voltage and refractory time in
-//      registers for the whole window) through the sub-window, overwriting
-//      each J in LDS with the neuron's output -- no synchronisation between
-//      steps, since a neuron depends only on its own past;
-//   3. decoded outputs, [ndec x n] by [n x ts], on MFMA: each wavefront takes
-//      every nw-th group of four neurons (its decoder fragments stay in
-//      registers for the whole window) and the partial 16 x 16 tiles are
-//      summed in LDS.
+// One workgroup per (op, group of cpw batch columns), for the whole window, in
+// sub-windows of ts steps (a multiple of 16).  A thread slot g = tid + j*blockDim
+// (j < NPT) owns neuron g % nmax of column g / nmax; its voltage and refractory
+// time stay in registers for the whole window.  The "columns" of the two
+// products below are the (batch column, step) pairs c*ts + s of a sub-window.
+// Per sub-window:
+//   1. input currents J = E x + bias on MFMA (v_mfma_f32_16x16x4f32; A lane l:
+//      row l%16, k l/16; B lane l: k l/16, column l%16; result register v:
+//      row 4(l/16) + v, column l%16), one (16-neuron tile, 16-column tile)
+//      unit per wavefront at a time, written to LDS as [column][neuron];
+//   2. every slot advances its neuron through the sub-window, overwriting each
+//      J in LDS with the neuron's output -- no synchronisation between steps,
+//      since a neuron depends only on its own past;
+//   3. decoded outputs, [ndec x n] by [n x columns], on MFMA: units are
+//      (16-column tile, chunk of neurons), partial tiles summed in LDS.
 // The next sub-window's inputs are fetched into registers before step 1 and
 // stored to LDS after it, so their latency overlaps the work.
 typedef float mfma_f4x __attribute__((ext_vector_type(4)));
-constexpr int kEnsDecCache = 16;   // decoder k-steps whose fragments stay in registers
-constexpr int kEnsEncCache = 16;   // encoder fragments kept in registers
 constexpr int kEnsXPre = 4;        // prefetched input values per thread
 
 template <int NPT>
 __global__ void __launch_bounds__(512) k_w_ens(WView w, float* pa, EnsDesc E, float dt, int32_t nmax,
-                                                int32_t ts_max, int xblk) {
+                                               int32_t ts, int32_t cpw, int32_t kch, int xblk) {
   extern __shared__ float lds[];
   const int op = blockIdx.x;
-  const int64_t b = blockIdx.y;
+  const int b0 = blockIdx.y * cpw;
   const int tid = threadIdx.x, nthr = blockDim.x, lane = tid % 64, wave = tid / 64, nw = nthr / 64;
   const EnsOp o = load_op(E.ops, op);
   const int n = o.n;
   const int d = o.x >= 0 ? E.d : 0, ndec = E.ndec, df0 = E.df[0];
   const int dp = E.d > 0 ? E.d : 1;
-  const int ctiles = ts_max / 16;
-  float* X = lds;                                   // [ts_max][dp]
-  float* Jb = X + ts_max * dp;                      // [ts_max][nmax]: currents, then outputs
-  float* red = Jb + (int64_t)ts_max * nmax;         // [nw][ctiles][16][16]
+  const int ncol = cpw * ts, ctiles = ncol / 16;
+  float* X = lds;                                   // [ncol][dp]
+  float* Jb = X + ncol * dp;                        // [ncol][nmax]: currents, then outputs
+  float* red = Jb + (int64_t)ncol * nmax;           // [ctiles][kch][16][16]
   gptr<float> enc = G(E.enc) + (int64_t)o.enc * E.d;
   gptr<float> bias = G(E.bias) + o.bias;
   gptr<float> D0 = G(E.D[0]) + (int64_t)o.D[0] * E.Dcols[0];
@@ -230,94 +229,58 @@ __global__ void __launch_bounds__(512) k_w_ens(WView w, float* pa, EnsDesc E, fl
   const bool spiking = E.ntype == 0;
   const bool bf = spiking && dt * o.inv_tau <= 0.0625f;   // branch-free spiking update applies
   const float amp_dt = o.amp / dt;
-  const float* xsrc = w.va + (int64_t)(o.x >= 0 ? o.x : 0) * w.vs + (int64_t)xblk * w.B + b;
-  // neuron state
+  const float* xsrc = w.va + (int64_t)(o.x >= 0 ? o.x : 0) * w.vs + (int64_t)xblk * w.B;
+  // neuron state of this thread's slots
   float v[NPT], rf[NPT];
 #pragma unroll
   for (int j = 0; j < NPT; ++j) {
-    const int r = tid + j * nthr;
-    const bool live = spiking && r < n;
-    v[j] = live ? pa[(int64_t)(o.V + r) * w.B + b] : 0.0f;
-    rf[j] = live ? pa[(int64_t)(o.ref + r) * w.B + b] : 0.0f;
+    const int g = tid + j * nthr, c = g / nmax, r = g - c * nmax;
+    const bool live = spiking && c < cpw && b0 + c < w.B && r < n;
+    v[j] = live ? pa[(int64_t)(o.V + r) * w.B + b0 + c] : 0.0f;
+    rf[j] = live ? pa[(int64_t)(o.ref + r) * w.B + b0 + c] : 0.0f;
   }
-  // encoder fragments: tile t = wave + nw * i, k-step kk; row r = 16 t + lane%16, k = 4 kk + lane/16
-  const int ntile = (n + 15) / 16, tpw = (ntile - wave + nw - 1) / nw, kd = (d + 3) / 4;
-  auto efrag = [&](int i, int kk) {
-    const int r = 16 * (wave + nw * i) + lane % 16, k = 4 * kk + lane / 16;
-    return (r < n && k < d) ? enc[(int64_t)r * E.d + k] : 0.0f;
+  auto stage_x = [&](int i, int32_t tb, int tsv) -> float {   // input value i of the sub-window at tb
+    const int col = i / d, k = i - col * d, c = col / ts, st = col - c * ts;
+    return (st < tsv && b0 + c < w.B) ? xsrc[(int64_t)k * w.vs + (int64_t)(tb + st) * w.B + b0 + c] : 0.0f;
   };
-  float eA[kEnsEncCache];
-#pragma unroll
-  for (int c = 0; c < kEnsEncCache; ++c) {
-    const int i = kd > 0 ? c / kd : 0, kk = kd > 0 ? c % kd : 0;
-    eA[c] = (kd > 0 && i < tpw) ? efrag(i, kk) : 0.0f;
-  }
-  // decoder fragments: k-step ks, row q = lane%16, neuron r = 4 (wave + nw ks) + lane/16
-  const int qa = lane % 16;
-  gptr<float> drow = qa < df0 ? D0 + (int64_t)qa * s0 : D1 + (int64_t)(qa - df0) * s1;
-  const int ksteps = (n + 4 * nw - 1) / (4 * nw);
-  auto dfrag = [&](int ks) {
-    const int r = 4 * (wave + nw * ks) + lane / 16;
-    return (qa < ndec && r < n) ? drow[r] : 0.0f;
-  };
-  float dA[kEnsDecCache];
-#pragma unroll
-  for (int c = 0; c < kEnsDecCache; ++c) dA[c] = (ndec > 0 && c < ksteps) ? dfrag(c) : 0.0f;
-  // first sub-window's inputs
   {
-    const int ts = min(ts_max, w.T);
-    for (int i = tid; i < ts * d; i += nthr) {
-      const int st = i / d, k = i - st * d;
-      X[st * dp + k] = xsrc[(int64_t)k * w.vs + (int64_t)st * w.B];
+    const int tsv = min(ts, w.T);
+    for (int i = tid; i < ncol * d; i += nthr) {
+      const int col = i / d, k = i - col * d;
+      X[col * dp + k] = stage_x(i, 0, tsv);
     }
   }
   __syncthreads();
-  for (int32_t t0 = 0; t0 < w.T; t0 += ts_max) {
-    const int ts = min(ts_max, w.T - t0);
+  const int ntile = (n + 15) / 16, kd = (d + 3) / 4;
+  const int qa = lane % 16;
+  gptr<float> drow = qa < df0 ? D0 + (int64_t)qa * s0 : D1 + (int64_t)(qa - df0) * s1;
+  const int ksteps = (n + 4 * kch - 1) / (4 * kch);
+  for (int32_t t0 = 0; t0 < w.T; t0 += ts) {
+    const int tsv = min(ts, w.T - t0);
     // 0. fetch the next sub-window's inputs
-    const int32_t t1 = t0 + ts_max;
-    const int tsn = t1 < w.T ? min(ts_max, w.T - t1) : 0;
+    const int32_t t1 = t0 + ts;
+    const int tsn = t1 < w.T ? min(ts, w.T - t1) : 0;
     float xpre[kEnsXPre];
 #pragma unroll
     for (int c = 0; c < kEnsXPre; ++c) {
       const int i = tid + c * nthr;
-      float val = 0.0f;
-      if (i < tsn * d) {
-        const int st = i / d, k = i - st * d;
-        val = xsrc[(int64_t)k * w.vs + (int64_t)(t1 + st) * w.B];
-      }
-      xpre[c] = val;
+      xpre[c] = (tsn > 0 && i < ncol * d) ? stage_x(i, t1, tsn) : 0.0f;
     }
     // 1. J = E x + bias
-    for (int i = 0; i < tpw; ++i) {
-      const int tile = wave + nw * i;
-      float bb[4];
-#pragma unroll
-      for (int u = 0; u < 4; ++u) {
-        const int r = 16 * tile + 4 * (lane / 16) + u;
-        bb[u] = r < n ? bias[r] : 0.0f;
+    for (int u = wave; u < ntile * ctiles; u += nw) {
+      const int nt = u / ctiles, ct = u - nt * ctiles;
+      const int col = 16 * ct + lane % 16;
+      mfma_f4x acc = {0.0f, 0.0f, 0.0f, 0.0f};
+      for (int kk = 0; kk < kd; ++kk) {
+        const int ra = 16 * nt + lane % 16, k = 4 * kk + lane / 16;
+        const float a = (ra < n && k < d) ? enc[(int64_t)ra * E.d + k] : 0.0f;
+        const float xb = k < d ? X[col * dp + k] : 0.0f;
+        acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a, xb, acc, 0, 0, 0);
       }
-      for (int ct = 0; ct < ctiles; ++ct) {
-        mfma_f4x acc = {0.0f, 0.0f, 0.0f, 0.0f};
-        const int sc = 16 * ct + lane % 16;
-        for (int kk = 0; kk < kd; ++kk) {
-          const int c = i * kd + kk;
-          float a = 0.0f;
 #pragma unroll
-          for (int cc = 0; cc < kEnsEncCache; ++cc)
-            if (cc == c) a = eA[cc];
-          if (c >= kEnsEncCache) a = efrag(i, kk);
-          const int k = 4 * kk + lane / 16;
-          const float xb = (sc < ts && k < d) ? X[sc * dp + k] : 0.0f;
-          acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a, xb, acc, 0, 0, 0);
-        }
-        if (sc < ts) {
-#pragma unroll
-          for (int u = 0; u < 4; ++u) {
-            const int r = 16 * tile + 4 * (lane / 16) + u;
-            if (r < n) Jb[sc * nmax + r] = acc[u] + bb[u];
-          }
-        }
+      for (int q = 0; q < 4; ++q) {
+        const int r = 16 * nt + 4 * (lane / 16) + q;
+        if (r < n) Jb[col * nmax + r] = acc[q] + bias[r];
       }
     }
     __syncthreads();
@@ -325,18 +288,24 @@ __global__ void __launch_bounds__(512) k_w_ens(WView w, float* pa, EnsDesc E, fl
 #pragma unroll
     for (int c = 0; c < kEnsXPre; ++c) {
       const int i = tid + c * nthr;
-      if (i < tsn * d) {
-        const int st = i / d, k = i - st * d;
-        X[st * dp + k] = xpre[c];
+      if (tsn > 0 && i < ncol * d) {
+        const int col = i / d, k = i - col * d;
+        X[col * dp + k] = xpre[c];
+      }
+    }
+    if (tsn > 0) {   // inputs beyond the prefetch registers
+      for (int i = tid + kEnsXPre * nthr; i < ncol * d; i += nthr) {
+        const int col = i / d, k = i - col * d;
+        X[col * dp + k] = stage_x(i, t1, tsn);
       }
     }
     // 2. neurons through the sub-window
 #pragma unroll
     for (int j = 0; j < NPT; ++j) {
-      const int r = tid + j * nthr;
-      if (r < n) {
-        for (int st = 0; st < ts; ++st) {
-          float* cell = Jb + st * nmax + r;
+      const int g = tid + j * nthr, c = g / nmax, r = g - c * nmax;
+      if (c < cpw && b0 + c < w.B && r < n) {
+        float* cell = Jb + (int64_t)c * ts * nmax + r;
+        for (int st = 0; st < tsv; ++st, cell += nmax) {
           const float jc = *cell;
           *cell = bf ? lif_update_bf(jc, v[j], rf[j], o.tau_rc, o.tau_ref, amp_dt, o.full, dt, o.inv_tau)
                      : neuron_update(E.ntype, jc, v[j], rf[j], o.tau_rc, o.tau_ref, o.amp, o.full, dt, o.inv_tau);
@@ -346,36 +315,35 @@ __global__ void __launch_bounds__(512) k_w_ens(WView w, float* pa, EnsDesc E, fl
     __syncthreads();
     // 3. decoded outputs
     if (ndec > 0) {
-      for (int ct = 0; ct < ctiles; ++ct) {
+      for (int u = wave; u < ctiles * kch; u += nw) {
+        const int ct = u / kch, kc = u - ct * kch;
+        const int col = 16 * ct + lane % 16;
         mfma_f4x acc = {0.0f, 0.0f, 0.0f, 0.0f};
-        const int sc = 16 * ct + lane % 16;
         for (int ks = 0; ks < ksteps; ++ks) {
-          const int r = 4 * (wave + nw * ks) + lane / 16;
-          float a = 0.0f;
-#pragma unroll
-          for (int cc = 0; cc < kEnsDecCache; ++cc)
-            if (cc == ks) a = dA[cc];
-          if (ks >= kEnsDecCache) a = dfrag(ks);
-          const float sb = (sc < ts && r < n) ? Jb[sc * nmax + r] : 0.0f;
+          const int r = 4 * (kc + kch * ks) + lane / 16;
+          const float a = (qa < ndec && r < n) ? drow[r] : 0.0f;
+          const float sb = r < n ? Jb[col * nmax + r] : 0.0f;
           acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a, sb, acc, 0, 0, 0);
         }
 #pragma unroll
-        for (int u = 0; u < 4; ++u)
-          red[((wave * ctiles + ct) * 16 + 4 * (lane / 16) + u) * 16 + lane % 16] = acc[u];
+        for (int q = 0; q < 4; ++q) red[(u * 16 + 4 * (lane / 16) + q) * 16 + lane % 16] = acc[q];
       }
     }
     __syncthreads();
-    for (int i = tid; i < ndec * ts; i += nthr) {
-      const int q = i / ts, st = i - q * ts;
-      float sum = 0.0f;
-      for (int u = 0; u < nw; ++u) sum += red[((u * ctiles + st / 16) * 16 + q) * 16 + st % 16];
-      const int dr = q < df0 ? o.d[0] + q : o.d[1] + (q - df0);
-      w.va[(int64_t)dr * w.vs + (int64_t)(t0 + st + 1) * w.B + b] = sum;
+    for (int i = tid; i < ndec * ncol; i += nthr) {
+      const int q = i / ncol, col = i - q * ncol, c = col / ts, st = col - c * ts;
+      if (st < tsv && b0 + c < w.B) {
+        float sum = 0.0f;
+        for (int kc = 0; kc < kch; ++kc) sum += red[(((col / 16) * kch + kc) * 16 + q) * 16 + col % 16];
+        const int dr = q < df0 ? o.d[0] + q : o.d[1] + (q - df0);
+        w.va[(int64_t)dr * w.vs + (int64_t)(t0 + st + 1) * w.B + b0 + c] = sum;
+      }
     }
     if (o.s >= 0) {
-      for (int i = tid; i < ts * n; i += nthr) {
-        const int st = i / n, r = i - st * n;
-        w.va[(int64_t)(o.s + r) * w.vs + (int64_t)(t0 + st + 1) * w.B + b] = Jb[st * nmax + r];
+      for (int i = tid; i < ncol * n; i += nthr) {
+        const int col = i / n, r = i - col * n, c = col / ts, st = col - c * ts;
+        if (st < tsv && b0 + c < w.B)
+          w.va[(int64_t)(o.s + r) * w.vs + (int64_t)(t0 + st + 1) * w.B + b0 + c] = Jb[col * nmax + r];
       }
     }
     __syncthreads();
@@ -383,10 +351,10 @@ __global__ void __launch_bounds__(512) k_w_ens(WView w, float* pa, EnsDesc E, fl
   if (spiking) {
 #pragma unroll
     for (int j = 0; j < NPT; ++j) {
-      const int r = tid + j * nthr;
-      if (r < n) {
-        pa[(int64_t)(o.V + r) * w.B + b] = v[j];
-        pa[(int64_t)(o.ref + r) * w.B + b] = rf[j];
+      const int g = tid + j * nthr, c = g / nmax, r = g - c * nmax;
+      if (c < cpw && b0 + c < w.B && r < n) {
+        pa[(int64_t)(o.V + r) * w.B + b0 + c] = v[j];
+        pa[(int64_t)(o.ref + r) * w.B + b0 + c] = rf[j];
       }
     }
   }

@@ -62,7 +62,7 @@ struct Launch {
   bool a_bcast = true;               // ELEM_INC a is a parameter base
   // window driver
   int32_t src_blk = 1, a_blk = 1;    // block offsets of src / a (1: this step, 0: previous step)
-  int32_t nmax = 0, npt = 1, nthr = 64, ts = 16;   // fused-ensemble launch shape
+  int32_t nmax = 0, npt = 1, nthr = 64, ts = 16, cpw = 1, kch = 1;   // fused-ensemble launch shape
   size_t lds = 0;
 };
 
@@ -612,21 +612,30 @@ void ens_shape(ms_sim* s, Launch& l, const LGroup& g) {
   int32_t nmax = 1;
   for (int32_t n : g.ens_n) nmax = std::max(nmax, n);
   l.nmax = nmax;
-  l.nthr = (int32_t)std::min<int64_t>(512, ((int64_t)nmax + 63) / 64 * 64);
-  l.npt = (nmax + l.nthr - 1) / l.nthr;
+  // batch columns per workgroup: fill up to 512 threads with whole columns
+  l.cpw = (int32_t)std::max<int64_t>(1, std::min<int64_t>(s->B, 512 / nmax));
+  l.nthr = (int32_t)std::min<int64_t>(512, ((int64_t)nmax * l.cpw + 63) / 64 * 64);
+  l.npt = (int32_t)(((int64_t)nmax * l.cpw + l.nthr - 1) / l.nthr);
   if (l.npt > 8) fail(MS_E_INVALID, "ensemble too large for the window driver (more than 4096 neurons)");
   l.npt = l.npt <= 1 ? 1 : l.npt <= 2 ? 2 : l.npt <= 4 ? 4 : 8;
   const int64_t nw = l.nthr / 64, dp = std::max<int32_t>(1, l.ens.d);
   // sub-window: the longest (a multiple of 16, at most 64 steps) that keeps
-  // about 16 wavefronts per CU resident within the CU's LDS; the prefetched
-  // inputs must fit the per-thread registers
-  auto bytes = [&](int64_t ts) { return (ts * (dp + nmax) + nw * (ts / 16) * 256) * (int64_t)sizeof(float); };
-  const int64_t wgs = std::max<int64_t>(1, 16 / nw);
+  // about 32 wavefronts per CU resident within the CU's LDS and whose inputs
+  // fit the per-thread prefetch registers (if none does, 16 steps, the rest of
+  // the inputs loaded without prefetch); decoder products split the neurons
+  // into kch chunks so that there are about as many units as wavefronts
+  auto kch_of = [&](int64_t ts) { return std::max<int64_t>(1, nw / std::max<int64_t>(1, l.cpw * ts / 16)); };
+  auto bytes = [&](int64_t ts) {
+    const int64_t ncol = l.cpw * ts;
+    return (ncol * (dp + nmax) + (ncol / 16) * kch_of(ts) * 256) * (int64_t)sizeof(float);
+  };
+  const int64_t wgs = std::max<int64_t>(1, 32 / nw);
   int64_t ts = 64;
-  while (ts > 16 && (bytes(ts) * wgs > (int64_t)s->lds_limit || ts * l.ens.d > (int64_t)kEnsXPre * l.nthr)) ts -= 16;
-  if (bytes(ts) > (int64_t)s->lds_limit || ts * l.ens.d > (int64_t)kEnsXPre * l.nthr)
-    fail(MS_E_INVALID, "ensemble too large for the window driver's LDS staging");
+  while (ts > 16 && (bytes(ts) * wgs > (int64_t)s->lds_limit || l.cpw * ts * l.ens.d > (int64_t)kEnsXPre * l.nthr))
+    ts -= 16;
+  if (bytes(ts) > (int64_t)s->lds_limit) fail(MS_E_INVALID, "ensemble too large for the window driver's LDS staging");
   l.ts = (int32_t)ts;
+  l.kch = (int32_t)kch_of(ts);
   l.lds = (size_t)bytes(ts);
 }
 
@@ -742,15 +751,15 @@ void launch_phase(ms_sim* s, const Launch& l, int32_t T, int64_t t0, hipStream_t
                          l.dst, l.src, l.fp, l.src_blk);
       break;
     case OP_ENS: {
-      const dim3 grid((unsigned)l.rows, (unsigned)s->B);
+      const dim3 grid((unsigned)l.rows, (unsigned)((s->B + l.cpw - 1) / l.cpw));
       if (l.npt == 1)
-        hipLaunchKernelGGL(k_w_ens<1>, grid, dim3(l.nthr), l.lds, q, w, s->pa, l.ens, s->dt, l.nmax, l.ts, l.src_blk);
+        hipLaunchKernelGGL(k_w_ens<1>, grid, dim3(l.nthr), l.lds, q, w, s->pa, l.ens, s->dt, l.nmax, l.ts, l.cpw, l.kch, l.src_blk);
       else if (l.npt == 2)
-        hipLaunchKernelGGL(k_w_ens<2>, grid, dim3(l.nthr), l.lds, q, w, s->pa, l.ens, s->dt, l.nmax, l.ts, l.src_blk);
+        hipLaunchKernelGGL(k_w_ens<2>, grid, dim3(l.nthr), l.lds, q, w, s->pa, l.ens, s->dt, l.nmax, l.ts, l.cpw, l.kch, l.src_blk);
       else if (l.npt == 4)
-        hipLaunchKernelGGL(k_w_ens<4>, grid, dim3(l.nthr), l.lds, q, w, s->pa, l.ens, s->dt, l.nmax, l.ts, l.src_blk);
+        hipLaunchKernelGGL(k_w_ens<4>, grid, dim3(l.nthr), l.lds, q, w, s->pa, l.ens, s->dt, l.nmax, l.ts, l.cpw, l.kch, l.src_blk);
       else
-        hipLaunchKernelGGL(k_w_ens<8>, grid, dim3(l.nthr), l.lds, q, w, s->pa, l.ens, s->dt, l.nmax, l.ts, l.src_blk);
+        hipLaunchKernelGGL(k_w_ens<8>, grid, dim3(l.nthr), l.lds, q, w, s->pa, l.ens, s->dt, l.nmax, l.ts, l.cpw, l.kch, l.src_blk);
       break;
     }
     default: fail(MS_E_INVALID, "unknown group type");
