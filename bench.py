@@ -80,6 +80,42 @@ def gemm_flops_per_step(w):
     return f
 
 
+LIF_FLOPS = 21    # exact-integration LIF step, operations per neuron-step
+RATE_FLOPS = 7    # rate LIF
+FP32_MFMA_PEAK_TFLOPS = 157.3
+
+
+def ensemble_work_per_step(w):
+    """(flops, bytes) of the fused ensemble operators in one timestep: per
+    neuron and batch row the encoders (2d), bias (1), neuron update and fused
+    decoders (2 per decoded dimension); bytes as a time-major pass moves them
+    (parameters once, V/refractory state read and written, inputs and decoded
+    outputs)."""
+    spec, B = w.spec, w.minibatch
+    ndec = {}
+    for c in spec.connections:
+        if c.pre[0] == "ens" and c.decoders is None:
+            e = spec.ensembles[c.pre[1]]
+            ndec.setdefault(c.pre[1], {})[c.function] = 1 if c.function == "product" else e.dims
+    for p in spec.probes:
+        if p.target[0] == "ens":
+            ndec.setdefault(p.target[1], {})["identity"] = spec.ensembles[p.target[1]].dims
+    flops = byts = 0
+    for i, e in enumerate(spec.ensembles):
+        nd = sum(ndec.get(i, {}).values())
+        nf = LIF_FLOPS if e.neuron_type == "lif" else RATE_FLOPS
+        flops += e.n_neurons * B * (2 * e.dims + 1 + nf + 2 * nd)
+        byts += 4 * e.n_neurons * (e.dims + 1 + nd) + 4 * B * (e.dims + nd)
+        if e.neuron_type == "lif":
+            byts += 16 * e.n_neurons * B
+    return flops, byts
+
+
+def dot_flops_per_step(plan_json, B):
+    """GEMM flops of the merged DotInc groups (2 M K per op and batch row)."""
+    return sum(2 * g["M"] * g["K"] * len(g["w_row"]) * B for g in plan_json["groups"] if g["type"] == "DotInc")
+
+
 def cpu_baseline(w, budget_s=15.0):
     """Time the float64 oracle on a bounded sample of the same workload."""
     from oracle.sim import OracleSim
@@ -101,6 +137,127 @@ def cpu_baseline(w, budget_s=15.0):
                       f"float64 numpy, {dt:.1f} s"}
 
 
+def measure_roofline(M, model, w, sim, info, feeds):
+    """Roofline of the dominant kernel, timed with HIP events on the stream it
+    runs on (one extra run with per-launch timing; the plain-launch driver
+    stands in for the hipGraph driver, whose kernels are the same)."""
+    T = w.n_steps
+    drv = info["driver"]
+    if drv == M.DRIVER_PERSISTENT:
+        ms = sim.last_run_ms()
+        b = compulsory_bytes_per_step(w) * T
+        ach = b / (ms * 1e-3) / 1e9
+        return {"bound": "hbm", "achieved": round(ach, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                "frac": round(ach / HBM_PEAK_GBS, 4), "traffic": None, "kernel": "k_persistent",
+                "launch_ms": round(ms, 4), "launches": 1, "work_per_launch": int(b)}
+    tsim = sim if drv in (M.DRIVER_WINDOW, M.DRIVER_STEPS) else \
+        M.Simulator(model, minibatch=w.minibatch, driver=M.DRIVER_STEPS, probe_capacity_steps=T)
+    tsim.set_timing(True)
+    tsim.reset()
+    tsim.run_steps(T, feeds)
+    times = {t: tsim.kernel_time(t) for t in range(10)}
+    tsim.set_timing(False)
+    if tsim is not sim:
+        tsim.close()
+    top = max(times, key=lambda t: times[t][0])
+    ms, n = times[top]
+    window = drv == M.DRIVER_WINDOW
+    if top == M.mergesim.OP_ENSEMBLE:
+        flops, byts = ensemble_work_per_step(w)
+        if window:    # state stays on chip across the window: arithmetic bounds it
+            work, bound, peak, unit = flops * T, "alu", FP32_VALU_PEAK_TFLOPS, "TFLOP/s"
+            kernel = "k_w_ens"
+        else:
+            work, bound, peak, unit = byts * T, "hbm", HBM_PEAK_GBS, "GB/s"
+            kernel = "k_ens_wg" if w.minibatch < 32 else "k_ens_tile"
+    elif top == M.mergesim.OP_DOT_INC:
+        work = dot_flops_per_step(M.Plan(model, minibatch=w.minibatch).json(), w.minibatch) * T
+        bound, peak, unit = "mfma", FP32_MFMA_PEAK_TFLOPS, "TFLOP/s"
+        kernel = "k_w_gemm" if window else "k_dot_inc"
+    else:
+        work, bound, peak, unit = compulsory_bytes_per_step(w) * T, "hbm", HBM_PEAK_GBS, "GB/s"
+        kernel = f"op type {top}"
+    scale = 1e12 if unit == "TFLOP/s" else 1e9
+    ach = work / (ms * 1e-3) / scale
+    return {"bound": bound, "achieved": round(ach, 3), "peak": peak, "unit": unit,
+            "frac": round(ach / peak, 4), "traffic": stored_traffic(kernel, w.name),
+            "kernel": kernel, "launch_ms": round(ms / max(n, 1), 4), "launches": n,
+            "work_per_launch": int(work / max(n, 1))}
+
+
+def stored_traffic(kernel, workload):
+    """HBM bytes per launch from the committed counter summary of this kernel
+    and workload, if it was taken from the current kernel sources."""
+    path = os.path.join(ROOT, "profiles", f"{kernel}_{workload}_traffic.json")
+    if not os.path.exists(path):
+        return None
+    with open(path) as f:
+        rec = json.load(f)
+    return rec["bytes_per_launch"] if rec.get("source_sha") == source_sha() else None
+
+
+def source_sha():
+    import hashlib
+    h = hashlib.sha256()
+    csrc = os.path.join(ROOT, "paper_1805_11144_amd", "csrc")
+    for name in sorted(os.listdir(csrc)):
+        if name.endswith((".hpp", ".hip", ".cpp")):
+            with open(os.path.join(csrc, name), "rb") as f:
+                h.update(f.read())
+    return h.hexdigest()[:16]
+
+
+COPY_PROBE_BYTES = 256 << 20
+
+
+def _counter_rows(d):
+    import csv
+    import glob
+    rows = []
+    for path in glob.glob(os.path.join(d, "**", "*counter_collection*.csv"), recursive=True):
+        with open(path) as f:
+            rows += list(csv.DictReader(f))
+    if not rows:
+        raise SystemExit(f"no counter_collection csv under {d}")
+    return rows
+
+
+def _per_dispatch(rows, counter):
+    """kernel name -> list of per-dispatch counter values (bytes)."""
+    out = {}
+    for r in rows:
+        if r.get("Counter_Name") != counter:
+            continue
+        out.setdefault(r["Kernel_Name"], []).append(float(r["Counter_Value"]) * 1024.0)   # KiB -> B
+    return out
+
+
+def summarize_traffic(args):
+    """Per-launch HBM bytes of a kernel from FETCH_SIZE and WRITE_SIZE runs, each
+    scaled by what the same counter reads for the 256 MiB calibration copy."""
+    res = {}
+    for kind, d, counter in (("fetch", args.summarize_traffic[0], "FETCH_SIZE"),
+                             ("write", args.summarize_traffic[1], "WRITE_SIZE")):
+        per = _per_dispatch(_counter_rows(d), counter)
+        copies = [v for k, vals in per.items() if "copyBuffer" in k for v in vals]
+        if not copies:
+            raise SystemExit("calibration copy not found (run the profiled bench with --copy-probe)")
+        scale = COPY_PROBE_BYTES / max(copies)
+        vals = [v for k, vs in per.items() if k.split("(")[0].split("<")[0].strip().endswith(args.kernel) or
+                k.startswith(args.kernel) or (" " + args.kernel) in k for v in vs]
+        if not vals:
+            raise SystemExit(f"kernel {args.kernel} not found in {d}")
+        res[kind] = {"raw_bytes_per_launch": sum(vals) / len(vals), "scale": scale, "launches": len(vals),
+                     "bytes_per_launch": scale * sum(vals) / len(vals)}
+    rec = {"kernel": args.kernel, "workload": args.config,
+           "bytes_per_launch": int(res["fetch"]["bytes_per_launch"] + res["write"]["bytes_per_launch"]),
+           "fetch": res["fetch"], "write": res["write"], "source_sha": source_sha(), "command": args.command}
+    path = os.path.join(ROOT, "profiles", f"{args.kernel}_{args.config}_traffic.json")
+    with open(path, "w") as f:
+        json.dump(rec, f, indent=1)
+    print(json.dumps(rec))
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -110,7 +267,16 @@ def main():
     ap.add_argument("--driver", default="auto", choices=["auto", "steps", "graph", "persistent", "window"])
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-budget", type=float, default=15.0)
+    ap.add_argument("--copy-probe", action="store_true",
+                    help="copy 256 MiB device to device before timing (calibrates HBM counters)")
+    ap.add_argument("--summarize-traffic", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
+                    help="turn two rocprofv3 --pmc runs (FETCH_SIZE, WRITE_SIZE) into profiles/<kernel>_<config>_traffic.json")
+    ap.add_argument("--kernel", default="k_w_ens", help="kernel name prefix for --summarize-traffic")
+    ap.add_argument("--command", default="", help="profiling command recorded by --summarize-traffic")
     args = ap.parse_args()
+    if args.summarize_traffic:
+        summarize_traffic(args)
+        return
     if args.gpus != 1:
         print(json.dumps({"error": "this build runs on one GPU; --gpus must be 1"}))
         sys.exit(2)
@@ -130,6 +296,11 @@ def main():
                       probe_capacity_steps=w.n_steps)
     t_build = time.perf_counter() - t_build
     feeds = {i: torch.from_numpy(f).to(dev) for i, f in w.feeds.items()}
+    if args.copy_probe:
+        src = torch.ones(COPY_PROBE_BYTES // 4, dtype=torch.float32, device=dev)
+        dst = torch.empty_like(src)
+        dst.copy_(src)
+        del src, dst
     torch.cuda.synchronize()
 
     def one_run():
@@ -153,14 +324,7 @@ def main():
     neuron_steps = w.n_neurons * w.n_steps * w.minibatch
     value = neuron_steps / (elapsed / args.steps)
     info = sim.info()
-    launch_ms = float(np.mean(kernel_ms))
-    bytes_run = compulsory_bytes_per_step(w) * w.n_steps
-    achieved_gbs = bytes_run / (launch_ms * 1e-3) / 1e9
-    roofline = {"bound": "hbm", "achieved": round(achieved_gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                "frac": round(achieved_gbs / HBM_PEAK_GBS, 4), "traffic": None,
-                "kernel": {1: "per-group kernels", 2: "per-group kernels (hipGraph)",
-                           3: "k_persistent", 4: "stage-major window kernels"}.get(info["driver"], "?"),
-                "launch_ms": round(launch_ms, 4), "bytes_per_launch": int(bytes_run)}
+    roofline = measure_roofline(M, model, w, sim, info, feeds)
     out = {
         "metric": "neuron-timesteps/sec (x minibatch) on 1 MI355X",
         "value": value, "unit": "neuron-timesteps/s", "n_gpus": 1, "steps": args.steps,
@@ -169,7 +333,8 @@ def main():
         "config": {"workload": WORKLOADS[args.config], "name": args.config, "neurons": w.n_neurons,
                    "timesteps": w.n_steps, "minibatch": w.minibatch,
                    "driver": {1: "steps", 2: "graph", 3: "persistent", 4: "window"}.get(info["driver"]),
-                   "groups_per_step": info["groups_per_step"], "build_s": round(t_build, 2)},
+                   "launches_per_window" if info["driver"] == M.DRIVER_WINDOW else "groups_per_step":
+                       info["groups_per_step"], "build_s": round(t_build, 2)},
         "roofline": roofline,
     }
     if not args.no_cpu_baseline:

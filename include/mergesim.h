@@ -262,6 +262,28 @@ ms_status ms_sim_last_run_ms(ms_sim* sim, double* ms_out);
  * number of merged groups executed per step (WINDOW: launches per window). */
 ms_status ms_sim_info(const ms_sim* sim, int32_t* driver_out, int32_t* groups_per_step_out);
 
+/* Merged operator types (the groups a plan is made of, paper Sec. 4.2). */
+#define MS_OP_FEED 0
+#define MS_OP_RESET 1
+#define MS_OP_COPY 2
+#define MS_OP_COPY_INC 3
+#define MS_OP_ELEMENTWISE_INC 4
+#define MS_OP_DOT_INC 5
+#define MS_OP_LIF 6
+#define MS_OP_LIF_RATE 7
+#define MS_OP_LOWPASS 8
+#define MS_OP_ENSEMBLE 9  /* fused bias + encoders + neurons + decoders of an ensemble */
+
+/* Per-kernel timing for measurement.  With timing on (on != 0), every kernel
+ * launch of a merged group is bracketed by HIP events recorded on the stream
+ * the launch runs on; ms_sim_kernel_time then returns the summed duration in
+ * ms and the number of launches of operator type `op_type` (MS_OP_*) during
+ * the last ms_sim_run_steps call (it waits for that call to finish).  Only the
+ * WINDOW and STEPS drivers time individual launches (MS_E_STATE otherwise).
+ * Timing adds event records to every launch: leave it off for throughput runs. */
+ms_status ms_sim_set_timing(ms_sim* sim, int32_t on);
+ms_status ms_sim_kernel_time(ms_sim* sim, int32_t op_type, double* ms_out, int64_t* launches_out);
+
 const char* ms_last_error(void);
 
 #ifdef __cplusplus

@@ -208,7 +208,8 @@ constexpr int kEnsXPre = 4;        // prefetched input values per thread
 
 template <int NPT>
 __global__ void __launch_bounds__(512) k_w_ens(WView w, float* pa, EnsDesc E, float dt, int32_t nmax,
-                                               int32_t ts, int32_t cpw, int32_t kch, int xblk) {
+                                               int32_t ts, int32_t cpw, int32_t kch, int xblk, int enc_lds,
+                                               int dec_lds) {
   extern __shared__ float lds[];
   const int op = blockIdx.x;
   const int b0 = blockIdx.y * cpw;
@@ -221,6 +222,9 @@ __global__ void __launch_bounds__(512) k_w_ens(WView w, float* pa, EnsDesc E, fl
   float* X = lds;                                   // [ncol][dp]
   float* Jb = X + ncol * dp;                        // [ncol][nmax]: currents, then outputs
   float* red = Jb + (int64_t)ncol * nmax;           // [ctiles][kch][16][16]
+  float* Bl = red + ctiles * kch * 256;             // [nmax] biases, [nmax][dp] encoders (enc_lds)
+  float* El = Bl + nmax;
+  float* Dl = El + (enc_lds ? nmax * dp : 0);       // [ndec][nmax] decoders (dec_lds)
   gptr<float> enc = G(E.enc) + (int64_t)o.enc * E.d;
   gptr<float> bias = G(E.bias) + o.bias;
   gptr<float> D0 = G(E.D[0]) + (int64_t)o.D[0] * E.Dcols[0];
@@ -250,6 +254,15 @@ __global__ void __launch_bounds__(512) k_w_ens(WView w, float* pa, EnsDesc E, fl
       X[col * dp + k] = stage_x(i, 0, tsv);
     }
   }
+  // per-op constants: biases always, encoders and decoders when they fit
+  for (int r = tid; r < n; r += nthr) Bl[r] = bias[r];
+  if (enc_lds)
+    for (int i = tid; i < n * d; i += nthr) El[(i / d) * dp + i % d] = enc[(int64_t)i];
+  if (dec_lds)
+    for (int i = tid; i < ndec * n; i += nthr) {
+      const int q = i / n, r = i - q * n;
+      Dl[q * nmax + r] = (q < df0 ? D0 + (int64_t)q * s0 : D1 + (int64_t)(q - df0) * s1)[r];
+    }
   __syncthreads();
   const int ntile = (n + 15) / 16, kd = (d + 3) / 4;
   const int qa = lane % 16;
@@ -273,14 +286,14 @@ __global__ void __launch_bounds__(512) k_w_ens(WView w, float* pa, EnsDesc E, fl
       mfma_f4x acc = {0.0f, 0.0f, 0.0f, 0.0f};
       for (int kk = 0; kk < kd; ++kk) {
         const int ra = 16 * nt + lane % 16, k = 4 * kk + lane / 16;
-        const float a = (ra < n && k < d) ? enc[(int64_t)ra * E.d + k] : 0.0f;
+        const float a = (ra < n && k < d) ? (enc_lds ? El[ra * dp + k] : enc[(int64_t)ra * E.d + k]) : 0.0f;
         const float xb = k < d ? X[col * dp + k] : 0.0f;
         acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a, xb, acc, 0, 0, 0);
       }
 #pragma unroll
       for (int q = 0; q < 4; ++q) {
         const int r = 16 * nt + 4 * (lane / 16) + q;
-        if (r < n) Jb[col * nmax + r] = acc[q] + bias[r];
+        if (r < n) Jb[col * nmax + r] = acc[q] + Bl[r];
       }
     }
     __syncthreads();
@@ -305,10 +318,14 @@ __global__ void __launch_bounds__(512) k_w_ens(WView w, float* pa, EnsDesc E, fl
       const int g = tid + j * nthr, c = g / nmax, r = g - c * nmax;
       if (c < cpw && b0 + c < w.B && r < n) {
         float* cell = Jb + (int64_t)c * ts * nmax + r;
-        for (int st = 0; st < tsv; ++st, cell += nmax) {
-          const float jc = *cell;
-          *cell = bf ? lif_update_bf(jc, v[j], rf[j], o.tau_rc, o.tau_ref, amp_dt, o.full, dt, o.inv_tau)
-                     : neuron_update(E.ntype, jc, v[j], rf[j], o.tau_rc, o.tau_ref, o.amp, o.full, dt, o.inv_tau);
+        if (bf) {
+          for (int st = 0; st < tsv; ++st)
+            cell[st * nmax] = lif_update_bf(cell[st * nmax], v[j], rf[j], o.tau_rc, o.tau_ref, amp_dt, o.full, dt,
+                                            o.inv_tau);
+        } else {
+          for (int st = 0; st < tsv; ++st)
+            cell[st * nmax] = neuron_update(E.ntype, cell[st * nmax], v[j], rf[j], o.tau_rc, o.tau_ref, o.amp,
+                                            o.full, dt, o.inv_tau);
         }
       }
     }
@@ -321,7 +338,7 @@ __global__ void __launch_bounds__(512) k_w_ens(WView w, float* pa, EnsDesc E, fl
         mfma_f4x acc = {0.0f, 0.0f, 0.0f, 0.0f};
         for (int ks = 0; ks < ksteps; ++ks) {
           const int r = 4 * (kc + kch * ks) + lane / 16;
-          const float a = (qa < ndec && r < n) ? drow[r] : 0.0f;
+          const float a = (qa < ndec && r < n) ? (dec_lds ? Dl[qa * nmax + r] : drow[r]) : 0.0f;
           const float sb = r < n ? Jb[col * nmax + r] : 0.0f;
           acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a, sb, acc, 0, 0, 0);
         }

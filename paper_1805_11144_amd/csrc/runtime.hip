@@ -63,6 +63,7 @@ struct Launch {
   // window driver
   int32_t src_blk = 1, a_blk = 1;    // block offsets of src / a (1: this step, 0: previous step)
   int32_t nmax = 0, npt = 1, nthr = 64, ts = 16, cpw = 1, kch = 1;   // fused-ensemble launch shape
+  int32_t enc_lds = 0, dec_lds = 0;
   size_t lds = 0;
 };
 
@@ -117,6 +118,11 @@ struct ms_sim {
   int32_t W = 0;                     // steps per window
   int64_t vs = 0;                    // row stride of va
   const int32_t* wprobe_src = nullptr;
+  // per-launch timing (ms_sim_set_timing)
+  bool timing = false;
+  std::vector<hipEvent_t> tev;       // event pool, pairs
+  std::vector<int32_t> ttype;        // op type of each recorded pair
+  size_t tn = 0;                     // pairs recorded in the last run
   static constexpr int kSide = 3;    // extra streams for independent phases of one level
   hipStream_t side[kSide] = {};
   hipEvent_t side_ev[kSide + 1] = {};
@@ -158,6 +164,7 @@ void free_sim(ms_sim* s) {
   for (void* p : s->extra_allocs) f(p);
   if (s->ev0) (void)hipEventDestroy(s->ev0);
   if (s->ev1) (void)hipEventDestroy(s->ev1);
+  for (hipEvent_t e : s->tev) (void)hipEventDestroy(e);
   for (int k = 0; k < ms_sim::kSide; ++k)
     if (s->side[k]) (void)hipStreamDestroy(s->side[k]);
   for (int k = 0; k <= ms_sim::kSide; ++k)
@@ -350,6 +357,28 @@ constexpr int kBlock = 256;
 
 inline unsigned grid_for(int64_t n) { return (unsigned)std::max<int64_t>(1, (n + kBlock - 1) / kBlock); }
 
+// Timing brackets around one launch of type `type` on stream q (no-ops unless
+// timing is on).
+void time_begin(ms_sim* s, int32_t type, hipStream_t q) {
+  if (!s->timing) return;
+  if (2 * (s->tn + 1) > s->tev.size()) {
+    for (int k = 0; k < 2; ++k) {
+      hipEvent_t e = nullptr;
+      HIPCHECK(hipEventCreate(&e));
+      s->tev.push_back(e);
+    }
+  }
+  if (s->ttype.size() <= s->tn) s->ttype.resize(s->tn + 1);
+  s->ttype[s->tn] = type;
+  HIPCHECK(hipEventRecord(s->tev[2 * s->tn], q));
+}
+
+void time_end(ms_sim* s, hipStream_t q) {
+  if (!s->timing) return;
+  HIPCHECK(hipEventRecord(s->tev[2 * s->tn + 1], q));
+  ++s->tn;
+}
+
 void launch_group(ms_sim* s, const Launch& l) {
   const int32_t B = s->B;
   if ((double)l.rows * (l.type == OP_DOT_INC ? l.M : 1) * B >= 4294967296.0)
@@ -416,7 +445,12 @@ void launch_group(ms_sim* s, const Launch& l) {
 }
 
 void launch_step(ms_sim* s) {
-  for (const Launch& l : s->launches) launch_group(s, l);
+  for (const Launch& l : s->launches) {
+    const bool t = s->driver == MS_DRIVER_STEPS && l.rows > 0;
+    if (t) time_begin(s, l.type, s->stream);
+    launch_group(s, l);
+    if (t) time_end(s, s->stream);
+  }
   const int64_t n = (int64_t)s->probe_rows * s->B;
   if (n > 0)
     hipLaunchKernelGGL(k_probe, dim3(grid_for(n)), dim3(kBlock), 0, s->stream, (const float*)s->state,
@@ -625,9 +659,14 @@ void ens_shape(ms_sim* s, Launch& l, const LGroup& g) {
   // the inputs loaded without prefetch); decoder products split the neurons
   // into kch chunks so that there are about as many units as wavefronts
   auto kch_of = [&](int64_t ts) { return std::max<int64_t>(1, nw / std::max<int64_t>(1, l.cpw * ts / 16)); };
+  // per-op constants staged in LDS: biases always; encoders and decoders when
+  // small (otherwise they are read through the caches)
+  l.enc_lds = (int64_t)nmax * dp * 4 <= 16384 ? 1 : 0;
+  l.dec_lds = (int64_t)l.ens.ndec * nmax * 4 <= 16384 ? 1 : 0;
+  const int64_t consts = nmax + (l.enc_lds ? (int64_t)nmax * dp : 0) + (l.dec_lds ? (int64_t)l.ens.ndec * nmax : 0);
   auto bytes = [&](int64_t ts) {
     const int64_t ncol = l.cpw * ts;
-    return (ncol * (dp + nmax) + (ncol / 16) * kch_of(ts) * 256) * (int64_t)sizeof(float);
+    return (ncol * (dp + nmax) + (ncol / 16) * kch_of(ts) * 256 + consts) * (int64_t)sizeof(float);
   };
   const int64_t wgs = std::max<int64_t>(1, 32 / nw);
   int64_t ts = 64;
@@ -753,17 +792,24 @@ void launch_phase(ms_sim* s, const Launch& l, int32_t T, int64_t t0, hipStream_t
     case OP_ENS: {
       const dim3 grid((unsigned)l.rows, (unsigned)((s->B + l.cpw - 1) / l.cpw));
       if (l.npt == 1)
-        hipLaunchKernelGGL(k_w_ens<1>, grid, dim3(l.nthr), l.lds, q, w, s->pa, l.ens, s->dt, l.nmax, l.ts, l.cpw, l.kch, l.src_blk);
+        hipLaunchKernelGGL(k_w_ens<1>, grid, dim3(l.nthr), l.lds, q, w, s->pa, l.ens, s->dt, l.nmax, l.ts, l.cpw, l.kch, l.src_blk, l.enc_lds, l.dec_lds);
       else if (l.npt == 2)
-        hipLaunchKernelGGL(k_w_ens<2>, grid, dim3(l.nthr), l.lds, q, w, s->pa, l.ens, s->dt, l.nmax, l.ts, l.cpw, l.kch, l.src_blk);
+        hipLaunchKernelGGL(k_w_ens<2>, grid, dim3(l.nthr), l.lds, q, w, s->pa, l.ens, s->dt, l.nmax, l.ts, l.cpw, l.kch, l.src_blk, l.enc_lds, l.dec_lds);
       else if (l.npt == 4)
-        hipLaunchKernelGGL(k_w_ens<4>, grid, dim3(l.nthr), l.lds, q, w, s->pa, l.ens, s->dt, l.nmax, l.ts, l.cpw, l.kch, l.src_blk);
+        hipLaunchKernelGGL(k_w_ens<4>, grid, dim3(l.nthr), l.lds, q, w, s->pa, l.ens, s->dt, l.nmax, l.ts, l.cpw, l.kch, l.src_blk, l.enc_lds, l.dec_lds);
       else
-        hipLaunchKernelGGL(k_w_ens<8>, grid, dim3(l.nthr), l.lds, q, w, s->pa, l.ens, s->dt, l.nmax, l.ts, l.cpw, l.kch, l.src_blk);
+        hipLaunchKernelGGL(k_w_ens<8>, grid, dim3(l.nthr), l.lds, q, w, s->pa, l.ens, s->dt, l.nmax, l.ts, l.cpw, l.kch, l.src_blk, l.enc_lds, l.dec_lds);
       break;
     }
     default: fail(MS_E_INVALID, "unknown group type");
   }
+}
+
+void timed_phase(ms_sim* s, const Launch& l, int32_t T, int64_t t0, hipStream_t q) {
+  if (l.rows == 0) return;
+  time_begin(s, l.type, q);
+  launch_phase(s, l, T, t0, q);
+  time_end(s, q);
 }
 
 void run_window(ms_sim* s, int64_t n_steps) {
@@ -776,16 +822,16 @@ void run_window(ms_sim* s, int64_t n_steps) {
       size_t e = a + 1;
       while (e < s->wl.size() && w.phases[e].level == w.phases[a].level) ++e;
       if (e - a == 1) {
-        launch_phase(s, s->wl[a], T, t0, s->stream);
+        timed_phase(s, s->wl[a], T, t0, s->stream);
       } else {
         const int used = (int)std::min<size_t>(ms_sim::kSide, e - a - 1);
         HIPCHECK(hipEventRecord(s->side_ev[ms_sim::kSide], s->stream));
         for (int k = 0; k < used; ++k) HIPCHECK(hipStreamWaitEvent(s->side[k], s->side_ev[ms_sim::kSide], 0));
         size_t rr = 0;   // exclusive phases round-robin over the streams; the rest in order on the main stream
         for (size_t i = a; i < e; ++i) {
-          if (!w.phases[i].exclusive) { launch_phase(s, s->wl[i], T, t0, s->stream); continue; }
+          if (!w.phases[i].exclusive) { timed_phase(s, s->wl[i], T, t0, s->stream); continue; }
           const size_t slot = rr++ % (size_t)(used + 1);
-          launch_phase(s, s->wl[i], T, t0, slot == 0 ? s->stream : s->side[slot - 1]);
+          timed_phase(s, s->wl[i], T, t0, slot == 0 ? s->stream : s->side[slot - 1]);
         }
         for (int k = 0; k < used; ++k) {
           HIPCHECK(hipEventRecord(s->side_ev[k], s->side[k]));
@@ -882,6 +928,7 @@ ms_status ms_sim_run_steps(ms_sim* s, int64_t n_steps, const ms_feed* feeds, int
     ensure_capacity(s, n_steps);
     stage_feeds(s, n_steps, feeds, n_feeds);
     HIPCHECK(hipMemsetAsync(s->ctr + 1, 0, sizeof(int64_t), s->stream));
+    s->tn = 0;
     HIPCHECK(hipEventRecord(s->ev0, s->stream));
     if (s->driver == MS_DRIVER_PERSISTENT) {
       run_persistent(s, n_steps);
@@ -917,6 +964,35 @@ ms_status ms_sim_last_run_ms(ms_sim* s, double* ms_out) {
     float ms = 0.f;
     HIPCHECK(hipEventElapsedTime(&ms, s->ev0, s->ev1));
     *ms_out = ms;
+  });
+}
+
+ms_status ms_sim_set_timing(ms_sim* s, int32_t on) {
+  return guarded([&] {
+    if (!s) fail(MS_E_INVALID, "NULL sim");
+    s->timing = on != 0;
+  });
+}
+
+ms_status ms_sim_kernel_time(ms_sim* s, int32_t op_type, double* ms_out, int64_t* launches_out) {
+  return guarded([&] {
+    if (!s || !ms_out) fail(MS_E_INVALID, "NULL argument");
+    if (op_type < 0 || op_type >= OP_NTYPES) fail(MS_E_INVALID, "unknown operator type");
+    if (s->driver != MS_DRIVER_WINDOW && s->driver != MS_DRIVER_STEPS)
+      fail(MS_E_STATE, "per-kernel timing needs the WINDOW or STEPS driver");
+    DeviceGuard dg(s->device);
+    HIPCHECK(hipEventSynchronize(s->ev1));
+    double total = 0.0;
+    int64_t count = 0;
+    for (size_t k = 0; k < s->tn; ++k) {
+      if (s->ttype[k] != op_type) continue;
+      float ms = 0.f;
+      HIPCHECK(hipEventElapsedTime(&ms, s->tev[2 * k], s->tev[2 * k + 1]));
+      total += ms;
+      ++count;
+    }
+    *ms_out = total;
+    if (launches_out) *launches_out = count;
   });
 }
 

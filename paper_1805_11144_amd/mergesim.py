@@ -20,6 +20,8 @@ PLANNER_GREEDY, PLANNER_TREE = 0, 1
 DRIVER_AUTO, DRIVER_STEPS, DRIVER_GRAPH, DRIVER_PERSISTENT, DRIVER_WINDOW = 0, 1, 2, 3, 4
 PARAM_GAIN, PARAM_BIAS, PARAM_DECODERS = 0, 1, 2
 STATE_VOLTAGE, STATE_REFRACTORY, STATE_SYNAPSE, STATE_PROBE_SYNAPSE = 0, 1, 2, 3
+(OP_FEED, OP_RESET, OP_COPY, OP_COPY_INC, OP_ELEMENTWISE_INC, OP_DOT_INC, OP_LIF, OP_LIF_RATE, OP_LOWPASS,
+ OP_ENSEMBLE) = range(10)
 
 _dp = C.POINTER(C.c_double)
 _fp = C.POINTER(C.c_float)
@@ -92,6 +94,8 @@ _SIGNATURES = [
     ("ms_sim_get_state", [C.c_void_p, _i32, _i32, _fp, _i64], _i32),
     ("ms_sim_set_state", [C.c_void_p, _i32, _i32, _fp, _i64], _i32),
     ("ms_sim_last_run_ms", [C.c_void_p, C.POINTER(C.c_double)], _i32),
+    ("ms_sim_set_timing", [C.c_void_p, _i32], _i32),
+    ("ms_sim_kernel_time", [C.c_void_p, _i32, C.POINTER(C.c_double), C.POINTER(_i64)], _i32),
     ("ms_sim_info", [C.c_void_p, C.POINTER(_i32), C.POINTER(_i32)], _i32),
     ("ms_last_error", [], C.c_char_p),
 ]
@@ -377,6 +381,15 @@ class Simulator:
         v = C.c_double()
         _check(self._lib.ms_sim_last_run_ms(self.handle, C.byref(v)))
         return v.value
+
+    def set_timing(self, on: bool) -> None:
+        _check(self._lib.ms_sim_set_timing(self.handle, 1 if on else 0))
+
+    def kernel_time(self, op_type: int):
+        """(summed ms, launches) of operator type op_type (OP_*) in the last run."""
+        ms, n = C.c_double(), _i64()
+        _check(self._lib.ms_sim_kernel_time(self.handle, int(op_type), C.byref(ms), C.byref(n)))
+        return ms.value, n.value
 
     def info(self):
         d, g = _i32(), _i32()
