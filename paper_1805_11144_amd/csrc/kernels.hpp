@@ -165,6 +165,8 @@ struct EnsDesc {
   int32_t Dcols[kMaxFns];   // row stride of each decoder base
 };
 
+constexpr float kLn2 = 0.6931471805599453f;
+
 // exp(x) - 1 for -1/16 <= x <= 0 (the partial-step integration factor):
 // degree-6 Taylor polynomial, truncation error below 1e-11 relative.
 __device__ __forceinline__ float expm1_small(float x) {
@@ -181,9 +183,10 @@ __device__ __forceinline__ float expm1_small(float x) {
 // Spiking: exact integration over the non-refractory part of the step (the
 // whole-step factor `full` = expm1(-dt/tau_rc) is precomputed; a partial step
 // uses the polynomial above or expm1f), strict threshold 1, crossing time from
-// the overshoot (ln via the hardware logarithm: its error, about 1e-9 s, is
-// below the float32 resolution of the state), reset to 0, refractory period
-// measured from the crossing.  Rate: amplitude / (tau_ref + tau_rc log1p(1/(J-1))).
+// the overshoot (the hardware reciprocal and base-2 logarithm, v_rcp_f32 and
+// v_log_f32, each within about one ulp: the crossing time is off by at most a
+// few 1e-9 s, some 1e-6 of a step), reset to 0, refractory period measured from
+// the crossing.  Rate: amplitude / (tau_ref + tau_rc log1p(1/(J-1))).
 __device__ __forceinline__ float neuron_update(int ntype, float j, float& v, float& rf, float tau_rc,
                                                float tau_ref, float amp, float full, float dt,
                                                float inv_tau) {
@@ -202,8 +205,8 @@ __device__ __forceinline__ float neuron_update(int ntype, float j, float& v, flo
     float since = 0.0f;
     const float drive = j - 1.0f;
     if (drive > 0.0f) {
-      const float q = __fdividef(v - 1.0f, drive);
-      since = q >= 1.0f ? integ : fminf(-tau_rc * __logf(1.0f - q), integ);
+      const float q = (v - 1.0f) * __builtin_amdgcn_rcpf(drive);
+      since = q >= 1.0f ? integ : fminf(-tau_rc * kLn2 * __builtin_amdgcn_logf(1.0f - q), integ);
     }
     v = 0.0f;
     rf = tau_ref - since;
@@ -226,8 +229,8 @@ __device__ __forceinline__ float lif_update_bf(float j, float& v, float& rf, flo
   v = v - (j - v) * e;
   rf = fmaxf(rf - dt, 0.0f);
   const float drive = j - 1.0f;
-  const float q = __fdividef(v - 1.0f, drive);
-  const float lg = fminf(-tau_rc * __logf(1.0f - q), integ);
+  const float q = (v - 1.0f) * __builtin_amdgcn_rcpf(drive);
+  const float lg = fminf(-tau_rc * kLn2 * __builtin_amdgcn_logf(1.0f - q), integ);
   const float since = drive > 0.0f ? (q >= 1.0f ? integ : lg) : 0.0f;
   const bool spk = v > 1.0f;
   v = spk ? 0.0f : fmaxf(v, 0.0f);

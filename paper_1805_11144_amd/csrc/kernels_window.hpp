@@ -357,10 +357,12 @@ __global__ void __launch_bounds__(512) k_w_ens(WView w, float* pa, EnsDesc E, fl
       }
     }
     if (o.s >= 0) {
+      // neuron outputs: adjacent lanes take adjacent batch columns, then steps,
+      // so that a wavefront's stores fall into few cache lines
       for (int i = tid; i < ncol * n; i += nthr) {
-        const int col = i / n, r = i - col * n, c = col / ts, st = col - c * ts;
+        const int r = i / ncol, rem = i - r * ncol, st = rem / cpw, c = rem - st * cpw;
         if (st < tsv && b0 + c < w.B)
-          w.va[(int64_t)(o.s + r) * w.vs + (int64_t)(t0 + st + 1) * w.B + b0 + c] = Jb[col * nmax + r];
+          w.va[(int64_t)(o.s + r) * w.vs + (int64_t)(t0 + st + 1) * w.B + b0 + c] = Jb[(c * ts + st) * nmax + r];
       }
     }
     __syncthreads();
