@@ -160,6 +160,7 @@ struct EnsDesc {
   int32_t df[kMaxFns];
   const EnsOp* ops;
   const float* enc;      // encoder base [rows][d]
+  const float* encT;     // the same encoders with each op's block stored [d][n] (or null)
   const float* bias;     // bias base (vector)
   const float* D[kMaxFns];  // decoder bases [rows][n]
   int32_t Dcols[kMaxFns];   // row stride of each decoder base
@@ -449,8 +450,19 @@ __device__ __forceinline__ void ens_wg_t(float* st, const Strides& S, const EnsD
   for (int q = 0; q < NDEC; ++q) acc[q] = 0.0f;
   float xr[kMaxXReg];
   load_input(xr, st, S, o.x, b, d);
+  // with the transposed copy, encoder k of adjacent neurons is adjacent in memory
+  gptr<float> encT = G(E.encT) + (int64_t)o.enc * d;
+  const bool tr = E.encT != nullptr && d <= kMaxXReg;
   for (int r = threadIdx.x; r < o.n; r += 256) {
-    const float j = input_current(bias[r], enc + (int64_t)r * d, xr, st, S, o.x, b, d);
+    float j;
+    if (tr) {
+      j = bias[r];
+#pragma unroll
+      for (int k = 0; k < kMaxXReg; ++k)
+        if (k < d) j += encT[(int64_t)k * o.n + r] * xr[k];
+    } else {
+      j = input_current(bias[r], enc + (int64_t)r * d, xr, st, S, o.x, b, d);
+    }
     float v = 0.0f, rf = 0.0f;
     if (E.ntype == 0) { v = st[at(S, o.V + r, b)]; rf = st[at(S, o.ref + r, b)]; }
     const float sp = neuron_update(E.ntype, j, v, rf, o.tau_rc, o.tau_ref, o.amp, o.full, dt, o.inv_tau);

@@ -192,6 +192,8 @@ struct PoolBuilder {
   }
 };
 
+const std::vector<float>& host_param_base(ms_sim* s, int32_t base);
+
 // Lowered groups -> launch records (index and parameter arrays uploaded into
 // pools owned by the simulator); `extra_ints` is uploaded alongside and its
 // device address returned in *extra_ptr.
@@ -308,6 +310,21 @@ void build_launches(ms_sim* s, const std::vector<LGroup>& groups, std::vector<La
         E.Dcols[f] = ir.bases[g.ens_Dbase[f]].cols;
       }
       E.enc = g.a.base >= 0 ? s->base_ptr[g.a.base] : nullptr;
+      if (g.a.base >= 0 && g.ens_d > 0 && s->B < 32) {
+        // per-op transposed encoder blocks for the lanes-over-neurons kernel
+        const std::vector<float>& he = host_param_base(s, g.a.base);
+        std::vector<float> t(he.size(), 0.0f);
+        const int64_t d = g.ens_d;
+        for (size_t k = 0; k < g.ens_n.size(); ++k) {
+          const int64_t e0 = g.ens_enc[k], n = g.ens_n[k];
+          for (int64_t r = 0; r < n; ++r)
+            for (int64_t q = 0; q < d; ++q) t[(size_t)(e0 * d + q * n + r)] = he[(size_t)((e0 + r) * d + q)];
+        }
+        float* dt_ = dev_alloc<float>(std::max<size_t>(1, t.size()));
+        HIPCHECK(hipMemcpy(dt_, t.data(), t.size() * 4, hipMemcpyHostToDevice));
+        s->extra_allocs.push_back(dt_);
+        E.encT = dt_;
+      }
       E.bias = s->base_ptr[g.ens_bias_base];
       E.ops = reinterpret_cast<const EnsOp*>(ipool + ens_off[gi]);
     }
