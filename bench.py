@@ -273,6 +273,11 @@ def main():
                     help="turn two rocprofv3 --pmc runs (FETCH_SIZE, WRITE_SIZE) into profiles/<kernel>_<config>_traffic.json")
     ap.add_argument("--kernel", default="k_w_ens", help="kernel name prefix for --summarize-traffic")
     ap.add_argument("--command", default="", help="profiling command recorded by --summarize-traffic")
+    ap.add_argument("--timesteps", type=int, default=0,
+                    help="override the workload's timesteps (counter passes: per-launch traffic of a "
+                         "time-major kernel does not depend on the run length)")
+    ap.add_argument("--counters-run", action="store_true",
+                    help="one untimed run for a rocprofv3 --pmc pass (with --copy-probe); prints no JSON")
     args = ap.parse_args()
     if args.summarize_traffic:
         summarize_traffic(args)
@@ -286,7 +291,7 @@ def main():
     import paper_1805_11144_amd as M
     from synth import make_workload
 
-    w = make_workload(args.config)
+    w = make_workload(args.config, **({"n_steps": args.timesteps} if args.timesteps else {}))
     model = M.model_from_spec(w.spec)
     driver = {"auto": M.DRIVER_AUTO, "steps": M.DRIVER_STEPS, "graph": M.DRIVER_GRAPH,
               "persistent": M.DRIVER_PERSISTENT, "window": M.DRIVER_WINDOW}[args.driver]
@@ -307,6 +312,11 @@ def main():
         sim.reset()
         sim.run_steps(w.n_steps, feeds)
 
+    if args.counters_run:
+        one_run()
+        sim.sync()
+        torch.cuda.synchronize()
+        return
     for _ in range(args.warmup):
         one_run()
     sim.sync()

@@ -454,26 +454,36 @@ __device__ __forceinline__ void ens_wg_t(float* st, const Strides& S, const EnsD
   gptr<float> encT = G(E.encT) + (int64_t)o.enc * d;
   const bool tr = E.encT != nullptr && d <= kMaxXReg;
   for (int r = threadIdx.x; r < o.n; r += 256) {
-    float j;
+    // every load of this neuron is issued before any arithmetic or store: the
+    // encoders with the index clamped to d - 1 (the extra terms meet xr[k] = 0),
+    // the bias, the state and the decoder entries
+    float ev[kMaxXReg], dv[NDEC > 0 ? NDEC : 1];
     if (tr) {
-      j = bias[r];
 #pragma unroll
-      for (int k = 0; k < kMaxXReg; ++k)
-        if (k < d) j += encT[(int64_t)k * o.n + r] * xr[k];
-    } else {
-      j = input_current(bias[r], enc + (int64_t)r * d, xr, st, S, o.x, b, d);
+      for (int k = 0; k < kMaxXReg; ++k) ev[k] = encT[(int64_t)(k < d ? k : d - 1) * o.n + r];
     }
+    const float bj = bias[r];
     float v = 0.0f, rf = 0.0f;
     if (E.ntype == 0) { v = st[at(S, o.V + r, b)]; rf = st[at(S, o.ref + r, b)]; }
-    const float sp = neuron_update(E.ntype, j, v, rf, o.tau_rc, o.tau_ref, o.amp, o.full, dt, o.inv_tau);
-    if (E.ntype == 0) { st[at(S, o.V + r, b)] = v; st[at(S, o.ref + r, b)] = rf; }
-    if (o.s >= 0) st[at(S, o.s + r, b)] = sp;
 #pragma unroll
     for (int q = 0; q < NDEC; ++q) {
       const int qq = q < ndec ? q : ndec - 1;
       gptr<float> row = qq < df0 ? D0 + (int64_t)qq * s0 : D1 + (int64_t)(qq - df0) * s1;
-      acc[q] += row[r] * sp;
+      dv[q] = row[r];
     }
+    float j;
+    if (tr) {
+      j = bj;
+#pragma unroll
+      for (int k = 0; k < kMaxXReg; ++k) j += ev[k] * xr[k];
+    } else {
+      j = input_current(bj, enc + (int64_t)r * d, xr, st, S, o.x, b, d);
+    }
+    const float sp = neuron_update(E.ntype, j, v, rf, o.tau_rc, o.tau_ref, o.amp, o.full, dt, o.inv_tau);
+    if (E.ntype == 0) { st[at(S, o.V + r, b)] = v; st[at(S, o.ref + r, b)] = rf; }
+    if (o.s >= 0) st[at(S, o.s + r, b)] = sp;
+#pragma unroll
+    for (int q = 0; q < NDEC; ++q) acc[q] += dv[q] * sp;
   }
 #pragma unroll
   for (int q = 0; q < NDEC; ++q) {
