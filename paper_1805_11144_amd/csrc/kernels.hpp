@@ -134,7 +134,21 @@ __device__ __forceinline__ void dot_row_item(float* st, const Strides& S, int64_
   gptr<float> w = G(W) + ((int64_t)G(w_row)[op] + m) * K;
   const int64_t x0 = G(x_row)[op];
   float acc = 0.0f;
-  for (int32_t k = 0; k < K; ++k) acc += w[k] * st[at(S, x0 + k, b)];
+  if ((K & 3) == 0) {
+    // weight rows are 16-byte aligned when K is a multiple of 4: four at a time
+    typedef float f4v __attribute__((ext_vector_type(4)));
+    const __attribute__((address_space(1))) f4v* w4 = (const __attribute__((address_space(1))) f4v*)w;
+    for (int32_t k4 = 0; k4 < K / 4; ++k4) {
+      const f4v wv = w4[k4];
+      const int64_t k = 4 * (int64_t)k4;
+      acc += wv[0] * st[at(S, x0 + k, b)];
+      acc += wv[1] * st[at(S, x0 + k + 1, b)];
+      acc += wv[2] * st[at(S, x0 + k + 2, b)];
+      acc += wv[3] * st[at(S, x0 + k + 3, b)];
+    }
+  } else {
+    for (int32_t k = 0; k < K; ++k) acc += w[k] * st[at(S, x0 + k, b)];
+  }
   st[at(S, (int64_t)G(d_row)[op] + m, b)] += acc;
 }
 
