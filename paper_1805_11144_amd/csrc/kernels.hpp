@@ -622,13 +622,26 @@ __global__ void k_set_ctr(int64_t* ctr, int64_t c0, int64_t c1) {
   const int64_t _i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;        \
   if (_i >= (n)) return;
 
-__global__ void k_stage_feed(const float* src, int32_t B, int64_t T, int32_t size, float* stage,
-                             int32_t feed_rows, int32_t row0) {
-  GRID_FLAT((int64_t)B * T * size);
-  const int64_t j = _i % size;
-  const int64_t t = (_i / size) % T;
-  const int64_t b = _i / (size * T);
-  stage[(t * feed_rows + row0 + j) * B + b] = src[_i];
+// feed [B][T][size] -> staging [T][feed_rows][B] at rows row0..row0+size: per
+// step a [B x size] -> [size x B] transpose through a 32 x 33 LDS tile, so that
+// both the reads (along size) and the writes (along B) are coalesced.
+// Grid (ceil(size/32), ceil(B/32), steps of this chunk), block 32 x 8; steps
+// t_off + blockIdx.z.
+__global__ void __launch_bounds__(256) k_stage_feed(const float* src, int32_t B, int64_t T, int32_t size,
+                                                    float* stage, int32_t feed_rows, int32_t row0, int64_t t_off) {
+  __shared__ float tile[32][33];
+  const int64_t t = t_off + blockIdx.z;
+  const int j0 = blockIdx.x * 32, b0 = blockIdx.y * 32;
+  const int tx = threadIdx.x, ty = threadIdx.y;
+  for (int r = ty; r < 32; r += 8) {
+    const int b = b0 + r, j = j0 + tx;
+    if (b < B && j < size) tile[r][tx] = src[((int64_t)b * T + t) * size + j];
+  }
+  __syncthreads();
+  for (int r = ty; r < 32; r += 8) {
+    const int j = j0 + r, b = b0 + tx;
+    if (j < size && b < B) stage[(t * feed_rows + row0 + j) * B + b] = tile[tx][r];
+  }
 }
 
 // probe buffer [T][probe_rows][B] -> out [B][T][w] for rows [off, off+w)

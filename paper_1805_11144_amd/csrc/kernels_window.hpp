@@ -435,3 +435,125 @@ __global__ void __launch_bounds__(256) k_w_gemm(WView w, int32_t M, int32_t K, i
     if (m < M && c < N) C[m * w.vs + c] += acc[v];
   }
 }
+
+// Larger products: workgroup tile 128 x 128, K in slices of 16, double-buffered
+// LDS; each of the four wavefronts owns a 64 x 64 quarter as 2 x 2 blocks of
+// v_mfma_f32_32x32x2f32.  The next slice is fetched into registers (four
+// float4 per thread) while the current one is multiplied.  Used when K and B
+// are multiples of 4 (so rows of W and of x are 16-byte aligned).
+constexpr int kG2M = 128, kG2N = 128, kG2K = 16;
+
+__global__ void __launch_bounds__(256) k_w_gemm2(WView w, int32_t M, int32_t K, int32_t mtiles, const float* Wt,
+                                                 const int32_t* w_row, const int32_t* x_row, const int32_t* d_row,
+                                                 int xblk) {
+  typedef float f4v __attribute__((ext_vector_type(4)));
+  __shared__ float As[2][kG2K][kG2M + 4];
+  __shared__ float Bs[2][kG2K][kG2N + 4];
+  const int64_t N = (int64_t)w.T * w.B;
+  const int op = blockIdx.y / mtiles, mt = blockIdx.y - op * mtiles;
+  const int64_t m0 = (int64_t)mt * kG2M, c0 = (int64_t)blockIdx.x * kG2N;
+  const int tid = threadIdx.x, lane = tid % 64, wave = tid / 64;
+  const int wm = wave / 2, wn = wave % 2;
+  gptr<float> A = G(Wt) + (int64_t)G(w_row)[op] * K;
+  const float* X = w.va + (int64_t)G(x_row)[op] * w.vs + (int64_t)xblk * w.B;
+  float* C = w.va + (int64_t)G(d_row)[op] * w.vs + w.B;
+  // fetch assignment: A slice 128 x 16 = 512 float4 (row mm, k4), B slice 16 x 128 = 512 float4 (k, col4)
+  f4v ra[2], rb[2];
+  auto fetch = [&](int32_t k0) {
+#pragma unroll
+    for (int q = 0; q < 2; ++q) {
+      const int idx = tid + q * 256;
+      const int mm = idx / 4, k4 = idx % 4;
+      const int64_t m = m0 + mm;
+      const int32_t k = k0 + 4 * k4;
+      f4v va = {0.0f, 0.0f, 0.0f, 0.0f};
+      if (m < M) {
+        if (k + 3 < K) {
+          va = *(const __attribute__((address_space(1))) f4v*)(A + m * K + k);
+        } else {
+#pragma unroll
+          for (int e = 0; e < 4; ++e) va[e] = k + e < K ? A[m * K + k + e] : 0.0f;
+        }
+      }
+      ra[q] = va;
+      const int kb = idx / 32, j4 = idx % 32;
+      const int32_t kx = k0 + kb;
+      const int64_t c = c0 + 4 * j4;
+      f4v vb = {0.0f, 0.0f, 0.0f, 0.0f};
+      if (kx < K) {
+        if (c + 3 < N) {
+          vb = *(const f4v*)(X + (int64_t)kx * w.vs + c);
+        } else {
+#pragma unroll
+          for (int e = 0; e < 4; ++e) vb[e] = c + e < N ? X[(int64_t)kx * w.vs + c + e] : 0.0f;
+        }
+      }
+      rb[q] = vb;
+    }
+  };
+  auto stash = [&](int buf) {
+#pragma unroll
+    for (int q = 0; q < 2; ++q) {
+      const int idx = tid + q * 256;
+      const int mm = idx / 4, k4 = idx % 4;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) As[buf][4 * k4 + e][mm] = ra[q][e];
+      const int kb = idx / 32, j4 = idx % 32;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) Bs[buf][kb][4 * j4 + e] = rb[q][e];
+    }
+  };
+  mfma_f16x acc[2][2];
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int j = 0; j < 2; ++j)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.0f;
+  fetch(0);
+  stash(0);
+  __syncthreads();
+  int buf = 0;
+  for (int32_t k0 = 0; k0 < K; k0 += kG2K) {
+    const bool more = k0 + kG2K < K;
+    if (more) fetch(k0 + kG2K);
+#pragma unroll
+    for (int kk = 0; kk < kG2K; kk += 2) {
+      float a[2], b[2];
+#pragma unroll
+      for (int i = 0; i < 2; ++i) a[i] = As[buf][kk + lane / 32][wm * 64 + i * 32 + lane % 32];
+#pragma unroll
+      for (int j = 0; j < 2; ++j) b[j] = Bs[buf][kk + lane / 32][wn * 64 + j * 32 + lane % 32];
+#pragma unroll
+      for (int i = 0; i < 2; ++i)
+#pragma unroll
+        for (int j = 0; j < 2; ++j) acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(a[i], b[j], acc[i][j], 0, 0, 0);
+    }
+    if (more) stash(buf ^ 1);
+    __syncthreads();
+    buf ^= 1;
+  }
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int j = 0; j < 2; ++j)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) {
+        const int64_t m = m0 + wm * 64 + i * 32 + 8 * (v / 4) + 4 * (lane / 32) + (v % 4);
+        const int64_t c = c0 + wn * 64 + j * 32 + lane % 32;
+        if (m < M && c < N) C[m * w.vs + c] += acc[i][j][v];
+      }
+}
+
+// Reset of a contiguous block of rows to per-row values (or zeros), four
+// consecutive (step, column) entries per thread; needs T*B % 4 == 0.
+__global__ void k_w_reset4(WView w, int64_t rows, int64_t start, const float* values) {
+  typedef float f4v __attribute__((ext_vector_type(4)));
+  const uint32_t i = blockIdx.x * blockDim.x + threadIdx.x;
+  const uint32_t q = ((uint32_t)w.T * (uint32_t)w.B) / 4;
+  if (i >= (uint32_t)rows * q) return;
+  const uint32_t r = i / q, c4 = i - r * q;
+  const float v = values ? G(values)[r] : 0.0f;
+  const f4v vv = {v, v, v, v};
+  *(f4v*)(w.va + (start + r) * w.vs + w.B + 4 * (int64_t)c4) = vv;
+}

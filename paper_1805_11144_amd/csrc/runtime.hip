@@ -545,9 +545,12 @@ void stage_feeds(ms_sim* s, int64_t n_steps, const ms_feed* feeds, int32_t n_fee
       HIPCHECK(hipMemcpyAsync(s->feed_tmp, f.data, elems * 4, hipMemcpyHostToDevice, s->stream));
       src = s->feed_tmp;
     }
-    const int64_t n = (int64_t)elems;
-    hipLaunchKernelGGL(k_stage_feed, dim3(grid_for(n)), dim3(kBlock), 0, s->stream, src, B, n_steps,
-                       nsize, s->feed_stage, fr, ir.feed_row_of_node[f.node_id]);
+    for (int64_t t_off = 0; t_off < n_steps; t_off += 65535) {   // grid z is at most 65535
+      const int64_t nt = std::min<int64_t>(65535, n_steps - t_off);
+      hipLaunchKernelGGL(k_stage_feed, dim3((unsigned)((nsize + 31) / 32), (unsigned)((B + 31) / 32), (unsigned)nt),
+                         dim3(32, 8), 0, s->stream, src, B, n_steps, nsize, s->feed_stage, fr,
+                         ir.feed_row_of_node[f.node_id], t_off);
+    }
     if (!f.on_device) HIPCHECK(hipStreamSynchronize(s->stream));   // feed_tmp reused
   }
 }
@@ -766,7 +769,11 @@ void launch_phase(ms_sim* s, const Launch& l, int32_t T, int64_t t0, hipStream_t
                          (const float*)s->feed_stage, s->plan->ir.feed_rows, t0);
       break;
     case OP_RESET:
-      hipLaunchKernelGGL(k_w_reset, dim3(grid_items(l.rows * tb)), dim3(kBlock), 0, q, w, l.rows, l.dst, l.values);
+      if (!l.dst.idx && s->B % 4 == 0)   // contiguous rows, 16-byte aligned rows of every block
+        hipLaunchKernelGGL(k_w_reset4, dim3(grid_items(l.rows * tb / 4)), dim3(kBlock), 0, q, w, l.rows, l.dst.start,
+                           l.values);
+      else
+        hipLaunchKernelGGL(k_w_reset, dim3(grid_items(l.rows * tb)), dim3(kBlock), 0, q, w, l.rows, l.dst, l.values);
       break;
     case OP_COPY:
       hipLaunchKernelGGL(k_w_copy, dim3(grid_items(l.rows * tb)), dim3(kBlock), 0, q, w, l.rows, l.dst,
@@ -782,7 +789,14 @@ void launch_phase(ms_sim* s, const Launch& l, int32_t T, int64_t t0, hipStream_t
                          l.ptr);
       break;
     case OP_DOT_INC:
-      if (l.K >= 16) {
+      if (l.K >= 16 && l.M >= 64 && l.K % 4 == 0 && s->B % 4 == 0) {
+        const int32_t mtiles = (l.M + kG2M - 1) / kG2M;
+        const double ntiles = std::ceil(tb / kG2N);
+        if (ntiles >= 2147483648.0 || (double)mtiles * l.rows > 65535.0)
+          fail(MS_E_INVALID, "window product too large for the GEMM grid");
+        hipLaunchKernelGGL(k_w_gemm2, dim3((unsigned)ntiles, (unsigned)(mtiles * l.rows)), dim3(256), 0, q, w, l.M,
+                           l.K, mtiles, l.a_base, l.w_row, l.x_row, l.d_row, l.src_blk);
+      } else if (l.K >= 16) {
         const int32_t mtiles = (l.M + kGemmBM - 1) / kGemmBM;
         const double ntiles = std::ceil(tb / kGemmBN);
         if (ntiles >= 2147483648.0 || (double)mtiles * l.rows > 65535.0)
