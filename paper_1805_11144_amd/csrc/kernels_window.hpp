@@ -545,15 +545,43 @@ __global__ void __launch_bounds__(256) k_w_gemm2(WView w, int32_t M, int32_t K, 
       }
 }
 
-// Reset of a contiguous block of rows to per-row values (or zeros), four
-// consecutive (step, column) entries per thread; needs T*B % 4 == 0.
-__global__ void k_w_reset4(WView w, int64_t rows, int64_t start, const float* values) {
-  typedef float f4v __attribute__((ext_vector_type(4)));
-  const uint32_t i = blockIdx.x * blockDim.x + threadIdx.x;
-  const uint32_t q = ((uint32_t)w.T * (uint32_t)w.B) / 4;
-  if (i >= (uint32_t)rows * q) return;
-  const uint32_t r = i / q, c4 = i - r * q;
-  const float v = values ? G(values)[r] : 0.0f;
-  const f4v vv = {v, v, v, v};
-  *(f4v*)(w.va + (start + r) * w.vs + w.B + 4 * (int64_t)c4) = vv;
+// Four consecutive (step, column) entries per thread (needs T*B % 4 == 0 and
+// B % 4 == 0, so every row of every block is 16-byte aligned).
+typedef float w_f4 __attribute__((ext_vector_type(4)));
+#define W_ITEM4(rows)                                                          \
+  const uint32_t _i = blockIdx.x * blockDim.x + threadIdx.x;                   \
+  const uint32_t _q = ((uint32_t)w.T * (uint32_t)w.B) / 4;                     \
+  if (_i >= (uint32_t)(rows) * _q) return;                                     \
+  const uint32_t _r = _i / _q, _c = 4 * (_i - _r * _q);
+
+__device__ __forceinline__ w_f4& w4(const WView& w, int64_t row, int64_t c) {
+  return *(w_f4*)(w.va + row * w.vs + c);
+}
+
+__global__ void k_w_reset4(WView w, int64_t rows, Opnd dst, const float* values) {
+  W_ITEM4(rows);
+  const float v = values ? G(values)[_r] : 0.0f;
+  w4(w, rowof(dst, _r), w.B + _c) = w_f4{v, v, v, v};
+}
+
+__device__ __forceinline__ w_f4 w_src4(const WView& w, const float* param, int bcast, int64_t row, int blk,
+                                       uint32_t c) {
+  if (bcast) {
+    const float v = G(param)[row];
+    return w_f4{v, v, v, v};
+  }
+  return w4(w, row, (int64_t)blk * w.B + c);
+}
+
+__global__ void k_w_copy_inc4(WView w, int64_t rows, Opnd dst, const float* param, Opnd src, int bcast, int sblk,
+                              const int32_t* ptr) {
+  W_ITEM4(rows);
+  w_f4& d = w4(w, rowof(dst, _r), w.B + _c);
+  w_f4 acc = d;
+  if (ptr) {
+    for (int32_t e = G(ptr)[_r]; e < G(ptr)[_r + 1]; ++e) acc += w_src4(w, param, bcast, rowof(src, e), sblk, _c);
+  } else {
+    acc += w_src4(w, param, bcast, rowof(src, _r), sblk, _c);
+  }
+  d = acc;
 }

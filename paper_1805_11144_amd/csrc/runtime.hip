@@ -769,8 +769,8 @@ void launch_phase(ms_sim* s, const Launch& l, int32_t T, int64_t t0, hipStream_t
                          (const float*)s->feed_stage, s->plan->ir.feed_rows, t0);
       break;
     case OP_RESET:
-      if (!l.dst.idx && s->B % 4 == 0)   // contiguous rows, 16-byte aligned rows of every block
-        hipLaunchKernelGGL(k_w_reset4, dim3(grid_items(l.rows * tb / 4)), dim3(kBlock), 0, q, w, l.rows, l.dst.start,
+      if (s->B % 4 == 0)   // 16-byte aligned rows of every block: four entries per thread
+        hipLaunchKernelGGL(k_w_reset4, dim3(grid_items(l.rows * tb / 4)), dim3(kBlock), 0, q, w, l.rows, l.dst,
                            l.values);
       else
         hipLaunchKernelGGL(k_w_reset, dim3(grid_items(l.rows * tb)), dim3(kBlock), 0, q, w, l.rows, l.dst, l.values);
@@ -780,8 +780,12 @@ void launch_phase(ms_sim* s, const Launch& l, int32_t T, int64_t t0, hipStream_t
                          l.src_base, l.src, (int)l.src_bcast, l.src_blk);
       break;
     case OP_COPY_INC:
-      hipLaunchKernelGGL(k_w_copy_inc, dim3(grid_items(l.rows * tb)), dim3(kBlock), 0, q, w, l.rows, l.dst,
-                         l.src_base, l.src, (int)l.src_bcast, l.src_blk, l.ptr);
+      if (s->B % 4 == 0)
+        hipLaunchKernelGGL(k_w_copy_inc4, dim3(grid_items(l.rows * tb / 4)), dim3(kBlock), 0, q, w, l.rows, l.dst,
+                           l.src_base, l.src, (int)l.src_bcast, l.src_blk, l.ptr);
+      else
+        hipLaunchKernelGGL(k_w_copy_inc, dim3(grid_items(l.rows * tb)), dim3(kBlock), 0, q, w, l.rows, l.dst,
+                           l.src_base, l.src, (int)l.src_bcast, l.src_blk, l.ptr);
       break;
     case OP_ELEM_INC:
       hipLaunchKernelGGL(k_w_elem_inc, dim3(grid_items(l.rows * tb)), dim3(kBlock), 0, q, w, l.rows, l.dst,
