@@ -83,6 +83,7 @@ def gemm_flops_per_step(w):
 LIF_FLOPS = 21    # exact-integration LIF step, operations per neuron-step
 RATE_FLOPS = 7    # rate LIF
 FP32_MFMA_PEAK_TFLOPS = 157.3
+BF16_MFMA_PEAK_TFLOPS = 2500.0   # dense
 
 
 def ensemble_work_per_step(w):
@@ -137,7 +138,7 @@ def cpu_baseline(w, budget_s=15.0):
                       f"float64 numpy, {dt:.1f} s"}
 
 
-def measure_roofline(M, model, w, sim, info, feeds):
+def measure_roofline(M, model, w, sim, info, feeds, bf16=False):
     """Roofline of the dominant kernel, timed with HIP events on the stream it
     runs on (one extra run with per-launch timing; the plain-launch driver
     stands in for the hipGraph driver, whose kernels are the same)."""
@@ -160,6 +161,8 @@ def measure_roofline(M, model, w, sim, info, feeds):
     if tsim is not sim:
         tsim.close()
     top = max(times, key=lambda t: times[t][0])
+    if bf16:      # the bf16 variant reports its products against the bf16 peak
+        top = M.mergesim.OP_DOT_INC
     ms, n = times[top]
     window = drv == M.DRIVER_WINDOW
     if top == M.mergesim.OP_ENSEMBLE:
@@ -174,6 +177,8 @@ def measure_roofline(M, model, w, sim, info, feeds):
         work = dot_flops_per_step(M.Plan(model, minibatch=w.minibatch).json(), w.minibatch) * T
         bound, peak, unit = "mfma", FP32_MFMA_PEAK_TFLOPS, "TFLOP/s"
         kernel = "k_w_gemm" if window else "k_dot_inc"
+        if bf16:
+            peak, kernel = BF16_MFMA_PEAK_TFLOPS, "k_w_gemm_bf16"
     else:
         work, bound, peak, unit = compulsory_bytes_per_step(w) * T, "hbm", HBM_PEAK_GBS, "GB/s"
         kernel = f"op type {top}"
@@ -266,6 +271,8 @@ def main():
     ap.add_argument("--config", default="c2", choices=sorted(WORKLOADS))
     ap.add_argument("--driver", default="auto", choices=["auto", "steps", "graph", "persistent", "window"])
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--gemm-dtype", default="f32", choices=["f32", "bf16"],
+                    help="input precision of the large window products (bf16: fp32 accumulation)")
     ap.add_argument("--cpu-budget", type=float, default=15.0)
     ap.add_argument("--copy-probe", action="store_true",
                     help="copy 256 MiB device to device before timing (calibrates HBM counters)")
@@ -298,7 +305,7 @@ def main():
     dev = torch.device("cuda:0")
     t_build = time.perf_counter()
     sim = M.Simulator(model, minibatch=w.minibatch, driver=driver, unroll=20,
-                      probe_capacity_steps=w.n_steps)
+                      probe_capacity_steps=w.n_steps, gemm_dtype=args.gemm_dtype)
     t_build = time.perf_counter() - t_build
     feeds = {i: torch.from_numpy(f).to(dev) for i, f in w.feeds.items()}
     if args.copy_probe:
@@ -334,17 +341,19 @@ def main():
     neuron_steps = w.n_neurons * w.n_steps * w.minibatch
     value = neuron_steps / (elapsed / args.steps)
     info = sim.info()
-    roofline = measure_roofline(M, model, w, sim, info, feeds)
+    bf16 = args.gemm_dtype == "bf16"
+    roofline = measure_roofline(M, model, w, sim, info, feeds, bf16)
     out = {
         "metric": "neuron-timesteps/sec (x minibatch) on 1 MI355X",
         "value": value, "unit": "neuron-timesteps/s", "n_gpus": 1, "steps": args.steps,
         "warmup": args.warmup, "ms_per_step": ms_per_step, "higher_is_better": True,
-        "scaling": "weak", "vs_baseline": None, "dtype": "f32", "data": "synthetic",
+        "scaling": "weak", "vs_baseline": None, "dtype": "bf16/f32" if bf16 else "f32", "data": "synthetic",
         "config": {"workload": WORKLOADS[args.config], "name": args.config, "neurons": w.n_neurons,
                    "timesteps": w.n_steps, "minibatch": w.minibatch,
                    "driver": {1: "steps", 2: "graph", 3: "persistent", 4: "window"}.get(info["driver"]),
                    "launches_per_window" if info["driver"] == M.DRIVER_WINDOW else "groups_per_step":
-                       info["groups_per_step"], "build_s": round(t_build, 2)},
+                       info["groups_per_step"], "build_s": round(t_build, 2),
+                   "gemm_dtype": args.gemm_dtype},
         "roofline": roofline,
     }
     if not args.no_cpu_baseline:

@@ -156,6 +156,18 @@ ms_status ms_model_add_probe(ms_model* model, const ms_probe_desc* desc, int32_t
                                  as the time-major drivers: every operator still sees
                                  exactly the values of its own step (Sec. 4.1). */
 
+/* Input precision of the dense window products (Sec. 3.1 lets the user pick the
+ * simulation dtype; the paper's choices are float32/float64, bf16 is this
+ * library's addition for matrix cores).  MS_GEMM_BF16 makes the window driver
+ * run every merged DotInc group with constant weights, M >= 64, K >= 16,
+ * K % 8 == 0 and minibatch % 4 == 0 on bf16 MFMA: the weights are rounded to
+ * bf16 (nearest even) once at creation, the signal operand as it is read,
+ * products accumulate in fp32 and are added to the fp32 destination.  All
+ * other operators stay fp32.  Any other driver with MS_GEMM_BF16 is
+ * MS_E_INVALID. */
+#define MS_GEMM_F32 0
+#define MS_GEMM_BF16 1
+
 typedef struct {
   double dt;                  /* seconds, default 0.001 */
   int32_t minibatch;          /* B >= 1, default 1 */
@@ -172,6 +184,7 @@ typedef struct {
   int32_t device;             /* HIP device ordinal */
   void* stream;               /* hipStream_t to run on, NULL = library-owned */
   int64_t probe_capacity_steps; /* initial probe/feed staging capacity */
+  int32_t gemm_dtype;         /* MS_GEMM_F32 (default) or MS_GEMM_BF16 */
 } ms_sim_opts;
 
 /* Fill `opts` with the defaults listed above. */

@@ -6,8 +6,8 @@ Python binding: argument marshalling only.
 """
 from .mergesim import (Model, Plan, Simulator, MergesimError, load_library, model_from_spec,
                        DRIVER_AUTO, DRIVER_STEPS, DRIVER_GRAPH, DRIVER_PERSISTENT, DRIVER_WINDOW,
-                       PLANNER_GREEDY, PLANNER_TREE)
+                       GEMM_F32, GEMM_BF16, PLANNER_GREEDY, PLANNER_TREE)
 
 __all__ = ["Model", "Plan", "Simulator", "MergesimError", "load_library", "model_from_spec",
            "DRIVER_AUTO", "DRIVER_STEPS", "DRIVER_GRAPH", "DRIVER_PERSISTENT", "DRIVER_WINDOW",
-           "PLANNER_GREEDY", "PLANNER_TREE"]
+           "GEMM_F32", "GEMM_BF16", "PLANNER_GREEDY", "PLANNER_TREE"]

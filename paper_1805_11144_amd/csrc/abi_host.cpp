@@ -79,6 +79,7 @@ void ms_sim_opts_default(ms_sim_opts* o) {
   o->device = 0;
   o->stream = nullptr;
   o->probe_capacity_steps = 1000;
+  o->gemm_dtype = MS_GEMM_F32;
 }
 
 ms_status ms_model_create(ms_model** out) {

@@ -545,6 +545,105 @@ __global__ void __launch_bounds__(256) k_w_gemm2(WView w, int32_t M, int32_t K, 
       }
 }
 
+// The same products with bf16 inputs and fp32 accumulation (v_mfma_f32_32x32x16_bf16):
+// W arrives already rounded to bf16, one [M][K] block per op (op k at k*M*K);
+// x is rounded to nearest even as it is staged.  Workgroup tile 128 x 128, K in
+// slices of 32, double-buffered; LDS keeps both operands k-contiguous ([m][k]
+// and [column][k], rows padded to 40 values) so that each lane reads its eight
+// k values of a fragment as one 16-byte word.  A lane l supplies row (or
+// column) l%32 and k values 8(l/32) .. 8(l/32)+7 of each 16-wide k step; the
+// result layout is that of the fp32 32 x 32 products.  Needs K % 8 == 0 and
+// B % 4 == 0.
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+constexpr int kGbM = 128, kGbN = 128, kGbK = 32, kGbP = 40;
+
+__global__ void __launch_bounds__(256) k_w_gemm_bf16(WView w, int32_t M, int32_t K, int32_t mtiles,
+                                                     const uint16_t* W16, const int32_t* x_row,
+                                                     const int32_t* d_row, int xblk) {
+  __shared__ __attribute__((aligned(16))) __bf16 As[2][kGbM][kGbP];
+  __shared__ __attribute__((aligned(16))) __bf16 Bs[2][kGbN][kGbP];
+  const int64_t N = (int64_t)w.T * w.B;
+  const int op = blockIdx.y / mtiles, mt = blockIdx.y - op * mtiles;
+  const int64_t m0 = (int64_t)mt * kGbM, c0 = (int64_t)blockIdx.x * kGbN;
+  const int tid = threadIdx.x, lane = tid % 64, wave = tid / 64;
+  const int wm = wave / 2, wn = wave % 2;
+  const uint16_t* A = W16 + (int64_t)op * M * K;
+  const float* X = w.va + (int64_t)G(x_row)[op] * w.vs + (int64_t)xblk * w.B;
+  float* C = w.va + (int64_t)G(d_row)[op] * w.vs + w.B;
+  // fetch assignment: A slice 128 x 32 and B slice 32 x 128 are 512 units of
+  // eight k values each; thread tid takes units tid and tid + 256 of both
+  bf16x8 ra[2], rb[2];
+  auto fetch = [&](int32_t k0) {
+#pragma unroll
+    for (int q = 0; q < 2; ++q) {
+      const int idx = tid + q * 256;
+      const int mm = idx / 4, k8 = idx % 4;
+      const int64_t m = m0 + mm;
+      const int32_t k = k0 + 8 * k8;
+      bf16x8 va = {};
+      if (m < M && k < K) va = *(const bf16x8*)(A + m * K + k);
+      ra[q] = va;
+      const int cc = idx % kGbN, kb = idx / kGbN;
+      const int64_t c = c0 + cc;
+      const int32_t kx = k0 + 8 * kb;
+      bf16x8 vb = {};
+      if (c < N && kx < K) {
+#pragma unroll
+        for (int e = 0; e < 8; ++e) vb[e] = (__bf16)X[(int64_t)(kx + e) * w.vs + c];
+      }
+      rb[q] = vb;
+    }
+  };
+  auto stash = [&](int buf) {
+#pragma unroll
+    for (int q = 0; q < 2; ++q) {
+      const int idx = tid + q * 256;
+      *(bf16x8*)&As[buf][idx / 4][8 * (idx % 4)] = ra[q];
+      *(bf16x8*)&Bs[buf][idx % kGbN][8 * (idx / kGbN)] = rb[q];
+    }
+  };
+  mfma_f16x acc[2][2];
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int j = 0; j < 2; ++j)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.0f;
+  fetch(0);
+  stash(0);
+  __syncthreads();
+  int buf = 0;
+  for (int32_t k0 = 0; k0 < K; k0 += kGbK) {
+    const bool more = k0 + kGbK < K;
+    if (more) fetch(k0 + kGbK);
+#pragma unroll
+    for (int ks = 0; ks < kGbK; ks += 16) {
+      bf16x8 a[2], b[2];
+#pragma unroll
+      for (int i = 0; i < 2; ++i) a[i] = *(const bf16x8*)&As[buf][wm * 64 + i * 32 + lane % 32][ks + 8 * (lane / 32)];
+#pragma unroll
+      for (int j = 0; j < 2; ++j) b[j] = *(const bf16x8*)&Bs[buf][wn * 64 + j * 32 + lane % 32][ks + 8 * (lane / 32)];
+#pragma unroll
+      for (int i = 0; i < 2; ++i)
+#pragma unroll
+        for (int j = 0; j < 2; ++j) acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[i], b[j], acc[i][j], 0, 0, 0);
+    }
+    if (more) stash(buf ^ 1);
+    __syncthreads();
+    buf ^= 1;
+  }
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int j = 0; j < 2; ++j)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) {
+        const int64_t m = m0 + wm * 64 + i * 32 + 8 * (v / 4) + 4 * (lane / 32) + (v % 4);
+        const int64_t c = c0 + wn * 64 + j * 32 + lane % 32;
+        if (m < M && c < N) C[m * w.vs + c] += acc[i][j][v];
+      }
+}
+
 // Four consecutive (step, column) entries per thread (needs T*B % 4 == 0 and
 // B % 4 == 0, so every row of every block is 16-byte aligned).
 typedef float w_f4 __attribute__((ext_vector_type(4)));

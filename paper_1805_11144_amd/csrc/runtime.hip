@@ -65,6 +65,7 @@ struct Launch {
   int32_t nmax = 0, npt = 1, nthr = 64, ts = 16, cpw = 1, kch = 1;   // fused-ensemble launch shape
   int32_t enc_lds = 0, dec_lds = 0;
   size_t lds = 0;
+  const uint16_t* w16 = nullptr;     // DOT_INC on bf16 MFMA: W rounded to bf16, op k at k*M*K
 };
 
 }  // namespace
@@ -77,6 +78,7 @@ struct ms_sim {
   bool own_stream = false;
   int32_t driver = MS_DRIVER_STEPS;
   int32_t unroll = 10;
+  int32_t gemm_dtype = MS_GEMM_F32;
   float dt = 0.001f;
   // device memory
   std::vector<float*> base_ptr;      // per base id
@@ -723,6 +725,22 @@ void ensure_window(ms_sim* s, int64_t n_steps) {
   s->vs = vs;
 }
 
+// fp32 -> bf16, round to nearest even (NaN stays NaN)
+uint16_t bf16_rne(float f) {
+  uint32_t u;
+  std::memcpy(&u, &f, 4);
+  if ((u & 0x7f800000u) == 0x7f800000u && (u & 0x7fffffu)) return (uint16_t)((u >> 16) | 0x40);
+  u += 0x7fffu + ((u >> 16) & 1u);
+  return (uint16_t)(u >> 16);
+}
+
+// Products that run on bf16 MFMA when the simulator asks for bf16 GEMMs: merged
+// DotInc groups with constant weights, M >= 64, K >= 16, K % 8 == 0 and
+// B % 4 == 0 (the others keep fp32).
+bool bf16_product(const ms_sim* s, const Launch& l) {
+  return l.type == OP_DOT_INC && l.a_bcast && l.M >= 64 && l.K >= 16 && l.K % 8 == 0 && s->B % 4 == 0;
+}
+
 void setup_window(ms_sim* s) {
   WindowPlan& w = *s->wplan;
   const int32_t B = s->B;
@@ -743,6 +761,19 @@ void setup_window(ms_sim* s) {
     l.a_blk = w.phases[k].a_blk;
     if (l.type == OP_ENS) {
       ens_shape(s, l, w.phases[k].g);
+    }
+    if (s->gemm_dtype == MS_GEMM_BF16 && bf16_product(s, l)) {
+      // each op's [M][K] block of W, rounded to nearest even, packed op after op
+      const LGroup& g = w.phases[k].g;
+      const std::vector<float>& hw = host_param_base(s, g.a.base);
+      std::vector<uint16_t> w16((size_t)l.rows * l.M * l.K);
+      for (int64_t op = 0; op < l.rows; ++op)
+        for (int64_t e = 0; e < (int64_t)l.M * l.K; ++e)
+          w16[(size_t)(op * l.M * l.K + e)] = bf16_rne(hw[(size_t)((int64_t)g.w_row[op] * l.K + e)]);
+      uint16_t* d = dev_alloc<uint16_t>(w16.size());
+      s->extra_allocs.push_back(d);
+      HIPCHECK(hipMemcpy(d, w16.data(), w16.size() * sizeof(uint16_t), hipMemcpyHostToDevice));
+      l.w16 = d;
     }
   }
   if (s->lds_limit > 65536) {
@@ -793,7 +824,14 @@ void launch_phase(ms_sim* s, const Launch& l, int32_t T, int64_t t0, hipStream_t
                          l.ptr);
       break;
     case OP_DOT_INC:
-      if (l.K >= 16 && l.M >= 64 && l.K % 4 == 0 && s->B % 4 == 0) {
+      if (l.w16) {
+        const int32_t mtiles = (l.M + kGbM - 1) / kGbM;
+        const double ntiles = std::ceil(tb / kGbN);
+        if (ntiles >= 2147483648.0 || (double)mtiles * l.rows > 65535.0)
+          fail(MS_E_INVALID, "window product too large for the GEMM grid");
+        hipLaunchKernelGGL(k_w_gemm_bf16, dim3((unsigned)ntiles, (unsigned)(mtiles * l.rows)), dim3(256), 0, q, w,
+                           l.M, l.K, mtiles, l.w16, l.x_row, l.d_row, l.src_blk);
+      } else if (l.K >= 16 && l.M >= 64 && l.K % 4 == 0 && s->B % 4 == 0) {
         const int32_t mtiles = (l.M + kG2M - 1) / kG2M;
         const double ntiles = std::ceil(tb / kG2N);
         if (ntiles >= 2147483648.0 || (double)mtiles * l.rows > 65535.0)
@@ -901,6 +939,7 @@ ms_status ms_sim_create(const ms_model* model, const ms_sim_opts* opts, ms_sim**
     if (o->minibatch < 1) fail(MS_E_INVALID, "minibatch must be >= 1");
     if (o->unroll < 1) fail(MS_E_INVALID, "unroll must be >= 1");
     if (o->driver < MS_DRIVER_AUTO || o->driver > MS_DRIVER_WINDOW) fail(MS_E_INVALID, "unknown driver");
+    if (o->gemm_dtype != MS_GEMM_F32 && o->gemm_dtype != MS_GEMM_BF16) fail(MS_E_INVALID, "unknown gemm_dtype");
     int ndev = 0;
     HIPCHECK(hipGetDeviceCount(&ndev));
     if (o->device < 0 || o->device >= ndev) fail(MS_E_INVALID, "device ordinal out of range");
@@ -910,6 +949,7 @@ ms_status ms_sim_create(const ms_model* model, const ms_sim_opts* opts, ms_sim**
       s->device = o->device;
       s->unroll = o->unroll;
       s->dt = (float)o->dt;
+      s->gemm_dtype = o->gemm_dtype;
       s->plan = make_plan(model_of(model), o->dt, plan_opts_from(o));
       DeviceGuard dg(s->device);
       if (o->stream) {
@@ -921,6 +961,8 @@ ms_status ms_sim_create(const ms_model* model, const ms_sim_opts* opts, ms_sim**
       HIPCHECK(hipEventCreate(&s->ev0));
       HIPCHECK(hipEventCreate(&s->ev1));
       s->driver = choose_driver(*s->plan, s->B, o->driver);
+      if (s->gemm_dtype == MS_GEMM_BF16 && s->driver != MS_DRIVER_WINDOW)
+        fail(MS_E_INVALID, "bf16 products run on the window driver only");
       // persistent: one workgroup per batch column -> column-major state
       s->S = s->driver == MS_DRIVER_PERSISTENT ? Strides{1, (int64_t)std::max<int64_t>(1, s->plan->base_rows.empty() ? 1 : s->plan->base_rows[0])}
                                                : Strides{(int64_t)s->B, 1};
