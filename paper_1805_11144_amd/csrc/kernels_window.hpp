@@ -436,6 +436,80 @@ __global__ void __launch_bounds__(256) k_w_gemm(WView w, int32_t M, int32_t K, i
   }
 }
 
+// Products with few rows and a deep K (M <= 16, K >= 256): one lane per
+// (step, column) of the window, all M rows per lane.  The eight wavefronts of
+// a workgroup take eight contiguous ranges of K and meet in LDS, where their
+// partial sums are added in wavefront order (the result does not depend on
+// timing).  W is read at wave-uniform addresses.
+constexpr int kSkM = 16, kSkW = 8;
+
+__global__ void __launch_bounds__(512) k_w_skinny(WView w, int32_t M, int32_t K, int32_t ctiles, const float* Wt,
+                                                  const int32_t* w_row, const int32_t* x_row, const int32_t* d_row,
+                                                  int xblk) {
+  __shared__ float red[kSkW][kSkM][64];
+  const int64_t N = (int64_t)w.T * w.B;
+  const int op = blockIdx.x / ctiles;
+  const int64_t c0 = (int64_t)(blockIdx.x - op * ctiles) * 64;
+  const int lane = threadIdx.x % 64, wave = threadIdx.x / 64;
+  const int64_t c = c0 + lane;
+  const bool live = c < N;
+  const int32_t kper = (K + kSkW - 1) / kSkW;
+  const int32_t kb = min(K, wave * kper), ke = min(K, kb + kper);
+  gptr<float> A = G(Wt) + (int64_t)G(w_row)[op] * K;
+  const float* X = w.va + (int64_t)G(x_row)[op] * w.vs + (int64_t)xblk * w.B;
+  float acc[kSkM];
+#pragma unroll
+  for (int m = 0; m < kSkM; ++m) acc[m] = 0.0f;
+  int32_t k = kb;
+  for (; k + 8 <= ke; k += 8) {
+    float xv[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) xv[u] = live ? X[(int64_t)(k + u) * w.vs + c] : 0.0f;
+#pragma unroll
+    for (int m = 0; m < kSkM; ++m)
+      if (m < M) {
+#pragma unroll
+        for (int u = 0; u < 8; ++u) acc[m] += A[(int64_t)m * K + k + u] * xv[u];
+      }
+  }
+  for (; k < ke; ++k) {
+    const float x = live ? X[(int64_t)k * w.vs + c] : 0.0f;
+#pragma unroll
+    for (int m = 0; m < kSkM; ++m)
+      if (m < M) acc[m] += A[(int64_t)m * K + k] * x;
+  }
+#pragma unroll
+  for (int m = 0; m < kSkM; ++m) red[wave][m][lane] = acc[m];
+  __syncthreads();
+  float* C = w.va + (int64_t)G(d_row)[op] * w.vs + w.B;
+  for (int i = threadIdx.x; i < M * 64; i += blockDim.x) {
+    const int m = i / 64, l = i % 64;
+    float sum = 0.0f;
+#pragma unroll
+    for (int v = 0; v < kSkW; ++v) sum += red[v][m][l];
+    if (c0 + l < N) C[(int64_t)m * w.vs + c0 + l] += sum;
+  }
+}
+
+// Tile order of the large products.  Workgroups are handed to the eight XCDs
+// round robin (workgroup g to XCD g % 8); renumbering g so that XCD x receives
+// the contiguous run x*chunk .. of (op, column tile, row tile), row tile
+// fastest, lets the row tiles that share a column tile of x run back to back
+// on one XCD and read that tile from its L2.  The grid is padded to a multiple
+// of eight; the padding workgroups return at once.
+struct TileIdx { int op, mt, nt; bool live; };
+__device__ __forceinline__ TileIdx xcd_tile(uint32_t mtiles, uint32_t ntiles, uint32_t nops) {
+  const uint32_t total = mtiles * ntiles * nops, chunk = (total + 7) / 8;
+  const uint32_t L = (blockIdx.x % 8) * chunk + blockIdx.x / 8;
+  TileIdx t{0, 0, 0, L < total};
+  if (!t.live) return t;
+  t.mt = (int)(L % mtiles);
+  const uint32_t rest = L / mtiles;
+  t.nt = (int)(rest % ntiles);
+  t.op = (int)(rest / ntiles);
+  return t;
+}
+
 // Larger products: workgroup tile 128 x 128, K in slices of 16, double-buffered
 // LDS; each of the four wavefronts owns a 64 x 64 quarter as 2 x 2 blocks of
 // v_mfma_f32_32x32x2f32.  The next slice is fetched into registers (four
@@ -443,15 +517,17 @@ __global__ void __launch_bounds__(256) k_w_gemm(WView w, int32_t M, int32_t K, i
 // are multiples of 4 (so rows of W and of x are 16-byte aligned).
 constexpr int kG2M = 128, kG2N = 128, kG2K = 16;
 
-__global__ void __launch_bounds__(256) k_w_gemm2(WView w, int32_t M, int32_t K, int32_t mtiles, const float* Wt,
-                                                 const int32_t* w_row, const int32_t* x_row, const int32_t* d_row,
-                                                 int xblk) {
+__global__ void __launch_bounds__(256) k_w_gemm2(WView w, int32_t M, int32_t K, int32_t mtiles, int32_t ntiles,
+                                                 int32_t nops, const float* Wt, const int32_t* w_row,
+                                                 const int32_t* x_row, const int32_t* d_row, int xblk) {
   typedef float f4v __attribute__((ext_vector_type(4)));
   __shared__ float As[2][kG2K][kG2M + 4];
   __shared__ float Bs[2][kG2K][kG2N + 4];
+  const TileIdx ti = xcd_tile(mtiles, ntiles, nops);
+  if (!ti.live) return;
   const int64_t N = (int64_t)w.T * w.B;
-  const int op = blockIdx.y / mtiles, mt = blockIdx.y - op * mtiles;
-  const int64_t m0 = (int64_t)mt * kG2M, c0 = (int64_t)blockIdx.x * kG2N;
+  const int op = ti.op, mt = ti.mt;
+  const int64_t m0 = (int64_t)mt * kG2M, c0 = (int64_t)ti.nt * kG2N;
   const int tid = threadIdx.x, lane = tid % 64, wave = tid / 64;
   const int wm = wave / 2, wn = wave % 2;
   gptr<float> A = G(Wt) + (int64_t)G(w_row)[op] * K;
@@ -548,36 +624,39 @@ __global__ void __launch_bounds__(256) k_w_gemm2(WView w, int32_t M, int32_t K, 
 // The same products with bf16 inputs and fp32 accumulation (v_mfma_f32_32x32x16_bf16):
 // W arrives already rounded to bf16, one [M][K] block per op (op k at k*M*K);
 // x is rounded to nearest even as it is staged.  Workgroup tile 128 x 128, K in
-// slices of 32, double-buffered; LDS keeps both operands k-contiguous ([m][k]
-// and [column][k], rows padded to 40 values) so that each lane reads its eight
+// slices of 64, double-buffered; LDS keeps both operands k-contiguous ([m][k]
+// and [column][k], rows padded to 72 values) so that each lane reads its eight
 // k values of a fragment as one 16-byte word.  A lane l supplies row (or
 // column) l%32 and k values 8(l/32) .. 8(l/32)+7 of each 16-wide k step; the
 // result layout is that of the fp32 32 x 32 products.  Needs K % 8 == 0 and
 // B % 4 == 0.
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
-constexpr int kGbM = 128, kGbN = 128, kGbK = 32, kGbP = 40;
+constexpr int kGbM = 128, kGbN = 128, kGbK = 64, kGbP = 72, kGbU = kGbK / 16;
+static_assert(kGbM == kG2M && kGbN == kG2N, "the two large-product kernels share their tile grid");
 
 __global__ void __launch_bounds__(256) k_w_gemm_bf16(WView w, int32_t M, int32_t K, int32_t mtiles,
-                                                     const uint16_t* W16, const int32_t* x_row,
-                                                     const int32_t* d_row, int xblk) {
+                                                     int32_t ntiles, int32_t nops, const uint16_t* W16,
+                                                     const int32_t* x_row, const int32_t* d_row, int xblk) {
   __shared__ __attribute__((aligned(16))) __bf16 As[2][kGbM][kGbP];
   __shared__ __attribute__((aligned(16))) __bf16 Bs[2][kGbN][kGbP];
+  const TileIdx ti = xcd_tile(mtiles, ntiles, nops);
+  if (!ti.live) return;
   const int64_t N = (int64_t)w.T * w.B;
-  const int op = blockIdx.y / mtiles, mt = blockIdx.y - op * mtiles;
-  const int64_t m0 = (int64_t)mt * kGbM, c0 = (int64_t)blockIdx.x * kGbN;
+  const int op = ti.op, mt = ti.mt;
+  const int64_t m0 = (int64_t)mt * kGbM, c0 = (int64_t)ti.nt * kGbN;
   const int tid = threadIdx.x, lane = tid % 64, wave = tid / 64;
   const int wm = wave / 2, wn = wave % 2;
   const uint16_t* A = W16 + (int64_t)op * M * K;
   const float* X = w.va + (int64_t)G(x_row)[op] * w.vs + (int64_t)xblk * w.B;
   float* C = w.va + (int64_t)G(d_row)[op] * w.vs + w.B;
-  // fetch assignment: A slice 128 x 32 and B slice 32 x 128 are 512 units of
-  // eight k values each; thread tid takes units tid and tid + 256 of both
-  bf16x8 ra[2], rb[2];
+  // fetch assignment: A slice 128 x 64 and B slice 64 x 128 are 1024 units of
+  // eight k values each; thread tid takes units tid + 256 q (q < 4) of both
+  bf16x8 ra[kGbU], rb[kGbU];
   auto fetch = [&](int32_t k0) {
 #pragma unroll
-    for (int q = 0; q < 2; ++q) {
+    for (int q = 0; q < kGbU; ++q) {
       const int idx = tid + q * 256;
-      const int mm = idx / 4, k8 = idx % 4;
+      const int mm = idx / (kGbK / 8), k8 = idx % (kGbK / 8);
       const int64_t m = m0 + mm;
       const int32_t k = k0 + 8 * k8;
       bf16x8 va = {};
@@ -596,9 +675,9 @@ __global__ void __launch_bounds__(256) k_w_gemm_bf16(WView w, int32_t M, int32_t
   };
   auto stash = [&](int buf) {
 #pragma unroll
-    for (int q = 0; q < 2; ++q) {
+    for (int q = 0; q < kGbU; ++q) {
       const int idx = tid + q * 256;
-      *(bf16x8*)&As[buf][idx / 4][8 * (idx % 4)] = ra[q];
+      *(bf16x8*)&As[buf][idx / (kGbK / 8)][8 * (idx % (kGbK / 8))] = ra[q];
       *(bf16x8*)&Bs[buf][idx % kGbN][8 * (idx / kGbN)] = rb[q];
     }
   };

@@ -824,20 +824,24 @@ void launch_phase(ms_sim* s, const Launch& l, int32_t T, int64_t t0, hipStream_t
                          l.ptr);
       break;
     case OP_DOT_INC:
-      if (l.w16) {
-        const int32_t mtiles = (l.M + kGbM - 1) / kGbM;
-        const double ntiles = std::ceil(tb / kGbN);
-        if (ntiles >= 2147483648.0 || (double)mtiles * l.rows > 65535.0)
-          fail(MS_E_INVALID, "window product too large for the GEMM grid");
-        hipLaunchKernelGGL(k_w_gemm_bf16, dim3((unsigned)ntiles, (unsigned)(mtiles * l.rows)), dim3(256), 0, q, w,
-                           l.M, l.K, mtiles, l.w16, l.x_row, l.d_row, l.src_blk);
-      } else if (l.K >= 16 && l.M >= 64 && l.K % 4 == 0 && s->B % 4 == 0) {
+      if (l.w16 || (l.K >= 16 && l.M >= 64 && l.K % 4 == 0 && s->B % 4 == 0)) {
+        // 128 x 128 tiles in XCD order: one flat grid padded to a multiple of 8
         const int32_t mtiles = (l.M + kG2M - 1) / kG2M;
         const double ntiles = std::ceil(tb / kG2N);
-        if (ntiles >= 2147483648.0 || (double)mtiles * l.rows > 65535.0)
-          fail(MS_E_INVALID, "window product too large for the GEMM grid");
-        hipLaunchKernelGGL(k_w_gemm2, dim3((unsigned)ntiles, (unsigned)(mtiles * l.rows)), dim3(256), 0, q, w, l.M,
-                           l.K, mtiles, l.a_base, l.w_row, l.x_row, l.d_row, l.src_blk);
+        const double total = ntiles * mtiles * (double)l.rows;
+        if (total >= 2147483648.0 - 8) fail(MS_E_INVALID, "window product too large for the GEMM grid");
+        const unsigned grid = (unsigned)(8 * (((int64_t)total + 7) / 8));
+        if (l.w16)
+          hipLaunchKernelGGL(k_w_gemm_bf16, dim3(grid), dim3(256), 0, q, w, l.M, l.K, mtiles, (int32_t)ntiles,
+                             (int32_t)l.rows, l.w16, l.x_row, l.d_row, l.src_blk);
+        else
+          hipLaunchKernelGGL(k_w_gemm2, dim3(grid), dim3(256), 0, q, w, l.M, l.K, mtiles, (int32_t)ntiles,
+                             (int32_t)l.rows, l.a_base, l.w_row, l.x_row, l.d_row, l.src_blk);
+      } else if (l.M <= kSkM && l.K >= 256) {
+        const double ctiles = std::ceil(tb / 64);
+        if (ctiles * l.rows >= 2147483648.0) fail(MS_E_INVALID, "window product too large for the grid");
+        hipLaunchKernelGGL(k_w_skinny, dim3((unsigned)(ctiles * l.rows)), dim3(64 * kSkW), 0, q, w, l.M, l.K,
+                           (int32_t)ctiles, l.a_base, l.w_row, l.x_row, l.d_row, l.src_blk);
       } else if (l.K >= 16) {
         const int32_t mtiles = (l.M + kGemmBM - 1) / kGemmBM;
         const double ntiles = std::ceil(tb / kGemmBN);

@@ -84,3 +84,36 @@ def test_window_driver_refuses_recurrent_models(name):
     w = make_workload(name, **SMALL[name])
     with pytest.raises(M.MergesimError, match="cycle"):
         M.Simulator(M.model_from_spec(w.spec), minibatch=w.minibatch, driver=M.DRIVER_WINDOW)
+
+
+@pytest.mark.parametrize("neuron_type", ["lif_rate", "lif"])
+def test_window_product_kernels(neuron_type):
+    """A classifier sized so that every window product kernel runs with ragged
+    edges: the 128 x 128 MFMA tiles (M = 300 rows: three row tiles; K = 136
+    and 300: partial last slices; 12 x 20 columns: two column tiles) and the
+    split-K kernel of the 10-row readout (K = 300 over eight wavefronts).
+    Rate-mode neuron probes take the backward-error check of the full-size
+    tests: a 300-wide layer has neurons close enough to threshold that float32
+    rounding of their current moves their rate by more than 1e-5 of the peak."""
+    w = make_workload("c3", neuron_type=neuron_type, n_steps=20, minibatch=12, n_hidden=300, n_in=136)
+    got = run_gpu(w, driver=M.DRIVER_WINDOW, unroll=7)
+    if neuron_type == "lif_rate":
+        from tests.test_gpu_fullsize import check, oracle_run
+        out = oracle_run(w)
+        for pi, (g, e) in enumerate(zip(got, out[0])):
+            if w.spec.probes[pi].target[0] != "neurons":
+                r = rel_err(g, e)
+                print(f"probe {pi}: rel {r:.2e}")
+                assert r <= 1e-5, (pi, r)
+        check(w, got, out, False)
+        return
+    exp = run_oracle(w)
+    for pi, (g, e) in enumerate(zip(got, exp)):
+        if w.spec.probes[pi].target[0] == "neurons":
+            f, u = flip_fraction(g, e), unpaired_flips(g, e)
+            print(f"probe {pi}: flips {f:.2e} of {int((e > 0).sum())} spikes, unpaired {u}")
+            assert u == 0 and f <= 2e-3, (pi, f, u)
+        else:
+            d = float(np.abs(g - e).max())
+            print(f"probe {pi}: abs {d:.2e}")
+            assert d <= 1e-3, (pi, d)
