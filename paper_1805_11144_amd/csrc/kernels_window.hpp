@@ -152,9 +152,20 @@ __global__ void k_w_lowpass(WView w, int64_t rows, Opnd y, Opnd v, FilterParams 
   const int64_t yr = rowof(y, _r) * w.vs + _b;
   const int64_t vr = rowof(v, _r) * w.vs + (int64_t)vblk * w.B + _b;
   float yv = w.va[yr];
-  // inputs of 8 steps are loaded before they are consumed, so the loads of a
-  // chunk are in flight together; the recurrence itself is one FMA per step
+  // inputs of 32 (then 8) steps are loaded before they are consumed, so the
+  // loads of a chunk are in flight together; the recurrence itself is one FMA
+  // per step, in step order, whatever the window length
   int32_t t = 0;
+  for (; t + 32 <= w.T; t += 32) {
+    float vin[32];
+#pragma unroll
+    for (int u = 0; u < 32; ++u) vin[u] = w.va[vr + (int64_t)(t + u) * w.B];
+#pragma unroll
+    for (int u = 0; u < 32; ++u) {
+      yv = a * yv + c * vin[u];
+      w.va[yr + (int64_t)(t + u + 1) * w.B] = yv;
+    }
+  }
   for (; t + 8 <= w.T; t += 8) {
     float vin[8];
 #pragma unroll
