@@ -824,8 +824,10 @@ void launch_phase(ms_sim* s, const Launch& l, int32_t T, int64_t t0, hipStream_t
                          l.ptr);
       break;
     case OP_DOT_INC:
-      if (l.w16 || (l.K >= 16 && l.M >= 64 && l.K % 4 == 0 && s->B % 4 == 0)) {
-        // 128 x 128 tiles in XCD order: one flat grid padded to a multiple of 8
+      if (l.w16 || (l.K > 128 && l.M >= 64 && l.K % 4 == 0 && s->B % 4 == 0)) {
+        // 128 x 128 tiles in XCD order: one flat grid padded to a multiple of 8.
+        // Products with K <= 128 are bound by their output traffic and run
+        // faster on the 64 x 64 tiles below (more workgroups in flight).
         const int32_t mtiles = (l.M + kG2M - 1) / kG2M;
         const double ntiles = std::ceil(tb / kG2N);
         const double total = ntiles * mtiles * (double)l.rows;
