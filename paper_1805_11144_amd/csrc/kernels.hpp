@@ -588,25 +588,27 @@ __global__ void __launch_bounds__(256) k_ens_tile(float* st, Strides S, int32_t 
   }
 }
 
-// node output <- feed staging [step][feed_rows][B] at the run-relative step ctr[1]
+// node output <- feed staging [step][feed_rows][B] at the run-relative step
+// ctr[1] + du (du: the step's place among the steps launched since the counter
+// last advanced)
 __global__ void k_feed(float* st, Strides S, int32_t B, int64_t rows, Opnd dst, const int32_t* feed_row,
-                       const float* stage, int32_t feed_rows, const int64_t* ctr) {
+                       const float* stage, int32_t feed_rows, const int64_t* ctr, int32_t du) {
   GRID_ITEM(rows * B);
-  const int64_t t = ctr[1];
+  const int64_t t = ctr[1] + du;
   st[at(S, rowof(dst, _r), _b)] = stage[(t * feed_rows + feed_row[_r]) * B + _b];
 }
 
-// probe buffer [step][probe_rows][B] at the absolute step ctr[0]
+// probe buffer [step][probe_rows][B] at the absolute step ctr[0] + du
 __global__ void k_probe(const float* st, Strides S, int32_t B, int32_t rows, const int32_t* src, float* buf,
-                        const int64_t* ctr) {
+                        const int64_t* ctr, int32_t du) {
   GRID_ITEM((int64_t)rows * B);
-  buf[(ctr[0] * rows + _r) * B + _b] = st[at(S, src[_r], _b)];
+  buf[((ctr[0] + du) * rows + _r) * B + _b] = st[at(S, src[_r], _b)];
 }
 
-__global__ void k_advance(int64_t* ctr) {
+__global__ void k_advance(int64_t* ctr, int32_t n) {
   if (threadIdx.x == 0 && blockIdx.x == 0) {
-    ctr[0] += 1;
-    ctr[1] += 1;
+    ctr[0] += n;
+    ctr[1] += n;
   }
 }
 

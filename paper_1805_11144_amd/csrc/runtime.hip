@@ -398,7 +398,7 @@ void time_end(ms_sim* s, hipStream_t q) {
   ++s->tn;
 }
 
-void launch_group(ms_sim* s, const Launch& l) {
+void launch_group(ms_sim* s, const Launch& l, int32_t du) {
   const int32_t B = s->B;
   if ((double)l.rows * (l.type == OP_DOT_INC ? l.M : 1) * B >= 4294967296.0)
     fail(MS_E_INVALID, "merged group too large for 32-bit work-item indexing");
@@ -410,7 +410,7 @@ void launch_group(ms_sim* s, const Launch& l) {
   switch (l.type) {
     case OP_FEED:
       hipLaunchKernelGGL(k_feed, dim3(grid_for(n)), dim3(kBlock), 0, q, st, S, B, l.rows, l.dst,
-                         l.feed_rows, (const float*)s->feed_stage, s->plan->ir.feed_rows, s->ctr);
+                         l.feed_rows, (const float*)s->feed_stage, s->plan->ir.feed_rows, s->ctr, du);
       break;
     case OP_RESET:
       hipLaunchKernelGGL(k_reset, dim3(grid_for(n)), dim3(kBlock), 0, q, st, S, B, l.rows, l.dst, l.values);
@@ -463,18 +463,22 @@ void launch_group(ms_sim* s, const Launch& l) {
   }
 }
 
-void launch_step(ms_sim* s) {
+// One timestep: the groups in plan order, then the probes.  The step is the
+// du-th after the last advance of the device step counter; with advance set,
+// the counter moves past this step afterwards (so a hipGraph of U steps
+// advances it once, by U).
+void launch_step(ms_sim* s, int32_t du = 0, bool advance = true) {
   for (const Launch& l : s->launches) {
     const bool t = s->driver == MS_DRIVER_STEPS && l.rows > 0;
     if (t) time_begin(s, l.type, s->stream);
-    launch_group(s, l);
+    launch_group(s, l, du);
     if (t) time_end(s, s->stream);
   }
   const int64_t n = (int64_t)s->probe_rows * s->B;
   if (n > 0)
     hipLaunchKernelGGL(k_probe, dim3(grid_for(n)), dim3(kBlock), 0, s->stream, (const float*)s->state,
-                       s->S, s->B, s->probe_rows, s->probe_src, s->probe_buf, s->ctr);
-  hipLaunchKernelGGL(k_advance, dim3(1), dim3(64), 0, s->stream, s->ctr);
+                       s->S, s->B, s->probe_rows, s->probe_src, s->probe_buf, s->ctr, du);
+  if (advance) hipLaunchKernelGGL(k_advance, dim3(1), dim3(64), 0, s->stream, s->ctr, du + 1);
 }
 
 void ensure_graph(ms_sim* s) {
@@ -482,7 +486,7 @@ void ensure_graph(ms_sim* s) {
   destroy_graph(s);
   HIPCHECK(hipStreamBeginCapture(s->stream, hipStreamCaptureModeThreadLocal));
   try {
-    for (int32_t u = 0; u < s->unroll; ++u) launch_step(s);
+    for (int32_t u = 0; u < s->unroll; ++u) launch_step(s, u, u + 1 == s->unroll);
   } catch (...) {
     hipGraph_t g = nullptr;
     (void)hipStreamEndCapture(s->stream, &g);
