@@ -176,7 +176,7 @@ def measure_roofline(M, model, w, sim, info, feeds, bf16=False):
     elif top == M.mergesim.OP_DOT_INC:
         work = dot_flops_per_step(M.Plan(model, minibatch=w.minibatch).json(), w.minibatch) * T
         bound, peak, unit = "mfma", FP32_MFMA_PEAK_TFLOPS, "TFLOP/s"
-        kernel = "k_w_gemm" if window else "k_dot_inc"
+        kernel = "k_w_gemm2" if window else "k_dot_inc"
         if bf16:
             peak, kernel = BF16_MFMA_PEAK_TFLOPS, "k_w_gemm_bf16"
     else:
@@ -184,10 +184,11 @@ def measure_roofline(M, model, w, sim, info, feeds, bf16=False):
         kernel = f"op type {top}"
     scale = 1e12 if unit == "TFLOP/s" else 1e9
     ach = work / (ms * 1e-3) / scale
+    op_names = {M.mergesim.OP_ENSEMBLE: "Ensemble", M.mergesim.OP_DOT_INC: "DotInc"}
     return {"bound": bound, "achieved": round(ach, 3), "peak": peak, "unit": unit,
             "frac": round(ach / peak, 4), "traffic": stored_traffic(kernel, w.name),
-            "kernel": kernel, "launch_ms": round(ms / max(n, 1), 4), "launches": n,
-            "work_per_launch": int(work / max(n, 1))}
+            "kernel": kernel, "op": op_names.get(top, str(top)), "launch_ms": round(ms / max(n, 1), 4),
+            "launches": n, "work_per_launch": int(work / max(n, 1))}
 
 
 def stored_traffic(kernel, workload):
@@ -248,13 +249,17 @@ def summarize_traffic(args):
         if not copies:
             raise SystemExit("calibration copy not found (run the profiled bench with --copy-probe)")
         scale = COPY_PROBE_BYTES / max(copies)
-        vals = [v for k, vs in per.items() if k.split("(")[0].split("<")[0].strip().endswith(args.kernel) or
-                k.startswith(args.kernel) or (" " + args.kernel) in k for v in vs]
+        names = [n for n in (args.match or args.kernel).split(",") if n]
+
+        def hit(k):
+            base = k.split("(")[0].split("<")[0].strip().split(" ")[-1]
+            return any(base == n for n in names)
+        vals = [v for k, vs in per.items() if hit(k) for v in vs]
         if not vals:
-            raise SystemExit(f"kernel {args.kernel} not found in {d}")
+            raise SystemExit(f"kernels {names} not found in {d}")
         res[kind] = {"raw_bytes_per_launch": sum(vals) / len(vals), "scale": scale, "launches": len(vals),
                      "bytes_per_launch": scale * sum(vals) / len(vals)}
-    rec = {"kernel": args.kernel, "workload": args.config,
+    rec = {"kernel": args.kernel, "kernels_counted": names, "workload": args.config,
            "bytes_per_launch": int(res["fetch"]["bytes_per_launch"] + res["write"]["bytes_per_launch"]),
            "fetch": res["fetch"], "write": res["write"], "source_sha": source_sha(), "command": args.command}
     path = os.path.join(ROOT, "profiles", f"{args.kernel}_{args.config}_traffic.json")
@@ -280,6 +285,9 @@ def main():
                     help="turn two rocprofv3 --pmc runs (FETCH_SIZE, WRITE_SIZE) into profiles/<kernel>_<config>_traffic.json")
     ap.add_argument("--kernel", default="k_w_ens", help="kernel name prefix for --summarize-traffic")
     ap.add_argument("--command", default="", help="profiling command recorded by --summarize-traffic")
+    ap.add_argument("--match", default="",
+                    help="comma-separated kernel names counted by --summarize-traffic (default: --kernel); "
+                         "list every kernel of the operator type the roofline times")
     ap.add_argument("--timesteps", type=int, default=0,
                     help="override the workload's timesteps (counter passes: per-launch traffic of a "
                          "time-major kernel does not depend on the run length)")
