@@ -217,13 +217,20 @@ __global__ void k_w_carry(WView w, int64_t rows) {
 typedef float mfma_f4x __attribute__((ext_vector_type(4)));
 constexpr int kEnsXPre = 4;        // prefetched input values per thread
 
+// Workgroups are numbered for the XCDs (workgroup g runs on XCD g % 8): XCD x
+// takes a contiguous run of (op, column group), column group fastest, so the
+// column groups of one op share their input and output lines in one L2.  The
+// grid is padded to a multiple of eight; padding workgroups return at once.
 template <int NPT>
 __global__ void __launch_bounds__(512) k_w_ens(WView w, float* pa, EnsDesc E, float dt, int32_t nmax,
                                                int32_t ts, int32_t cpw, int32_t kch, int xblk, int enc_lds,
-                                               int dec_lds) {
+                                               int dec_lds, int32_t nops) {
   extern __shared__ float lds[];
-  const int op = blockIdx.x;
-  const int b0 = blockIdx.y * cpw;
+  const uint32_t ncg = ((uint32_t)w.B + cpw - 1) / cpw, total = (uint32_t)nops * ncg, chunk = (total + 7) / 8;
+  const uint32_t L = (blockIdx.x % 8) * chunk + blockIdx.x / 8;
+  if (L >= total) return;
+  const int op = (int)(L / ncg);
+  const int b0 = (int)(L - (uint32_t)op * ncg) * cpw;
   const int tid = threadIdx.x, nthr = blockDim.x, lane = tid % 64, wave = tid / 64, nw = nthr / 64;
   const EnsOp o = load_op(E.ops, op);
   const int n = o.n;

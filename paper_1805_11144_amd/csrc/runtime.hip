@@ -873,15 +873,19 @@ void launch_phase(ms_sim* s, const Launch& l, int32_t T, int64_t t0, hipStream_t
                          l.dst, l.src, l.fp, l.src_blk);
       break;
     case OP_ENS: {
-      const dim3 grid((unsigned)l.rows, (unsigned)((s->B + l.cpw - 1) / l.cpw));
+      // one flat grid in XCD order, padded to a multiple of 8
+      const int64_t total = l.rows * ((s->B + l.cpw - 1) / l.cpw);
+      if (total >= 2147483648LL - 8) fail(MS_E_INVALID, "too many ensemble workgroups");
+      const dim3 grid((unsigned)(8 * ((total + 7) / 8)));
+      const int32_t nops = (int32_t)l.rows;
       if (l.npt == 1)
-        hipLaunchKernelGGL(k_w_ens<1>, grid, dim3(l.nthr), l.lds, q, w, s->pa, l.ens, s->dt, l.nmax, l.ts, l.cpw, l.kch, l.src_blk, l.enc_lds, l.dec_lds);
+        hipLaunchKernelGGL(k_w_ens<1>, grid, dim3(l.nthr), l.lds, q, w, s->pa, l.ens, s->dt, l.nmax, l.ts, l.cpw, l.kch, l.src_blk, l.enc_lds, l.dec_lds, nops);
       else if (l.npt == 2)
-        hipLaunchKernelGGL(k_w_ens<2>, grid, dim3(l.nthr), l.lds, q, w, s->pa, l.ens, s->dt, l.nmax, l.ts, l.cpw, l.kch, l.src_blk, l.enc_lds, l.dec_lds);
+        hipLaunchKernelGGL(k_w_ens<2>, grid, dim3(l.nthr), l.lds, q, w, s->pa, l.ens, s->dt, l.nmax, l.ts, l.cpw, l.kch, l.src_blk, l.enc_lds, l.dec_lds, nops);
       else if (l.npt == 4)
-        hipLaunchKernelGGL(k_w_ens<4>, grid, dim3(l.nthr), l.lds, q, w, s->pa, l.ens, s->dt, l.nmax, l.ts, l.cpw, l.kch, l.src_blk, l.enc_lds, l.dec_lds);
+        hipLaunchKernelGGL(k_w_ens<4>, grid, dim3(l.nthr), l.lds, q, w, s->pa, l.ens, s->dt, l.nmax, l.ts, l.cpw, l.kch, l.src_blk, l.enc_lds, l.dec_lds, nops);
       else
-        hipLaunchKernelGGL(k_w_ens<8>, grid, dim3(l.nthr), l.lds, q, w, s->pa, l.ens, s->dt, l.nmax, l.ts, l.cpw, l.kch, l.src_blk, l.enc_lds, l.dec_lds);
+        hipLaunchKernelGGL(k_w_ens<8>, grid, dim3(l.nthr), l.lds, q, w, s->pa, l.ens, s->dt, l.nmax, l.ts, l.cpw, l.kch, l.src_blk, l.enc_lds, l.dec_lds, nops);
       break;
     }
     default: fail(MS_E_INVALID, "unknown group type");
