@@ -535,7 +535,7 @@ __device__ __forceinline__ TileIdx xcd_tile(uint32_t mtiles, uint32_t ntiles, ui
 // are multiples of 4 (so rows of W and of x are 16-byte aligned).
 constexpr int kG2M = 128, kG2N = 128, kG2K = 16;
 
-__global__ void __launch_bounds__(256) k_w_gemm2(WView w, int32_t M, int32_t K, int32_t mtiles, int32_t ntiles,
+__global__ void __launch_bounds__(256, 4) k_w_gemm2(WView w, int32_t M, int32_t K, int32_t mtiles, int32_t ntiles,
                                                  int32_t nops, const float* Wt, const int32_t* w_row,
                                                  const int32_t* x_row, const int32_t* d_row, int xblk) {
   typedef float f4v __attribute__((ext_vector_type(4)));
@@ -649,10 +649,10 @@ __global__ void __launch_bounds__(256) k_w_gemm2(WView w, int32_t M, int32_t K, 
 // result layout is that of the fp32 32 x 32 products.  Needs K % 8 == 0 and
 // B % 4 == 0.
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
-constexpr int kGbM = 128, kGbN = 128, kGbK = 64, kGbP = 72, kGbU = kGbK / 16;
+constexpr int kGbM = 128, kGbN = 128, kGbK = 32, kGbP = 40, kGbU = kGbK / 16;
 static_assert(kGbM == kG2M && kGbN == kG2N, "the two large-product kernels share their tile grid");
 
-__global__ void __launch_bounds__(256) k_w_gemm_bf16(WView w, int32_t M, int32_t K, int32_t mtiles,
+__global__ void __launch_bounds__(256, 3) k_w_gemm_bf16(WView w, int32_t M, int32_t K, int32_t mtiles,
                                                      int32_t ntiles, int32_t nops, const uint16_t* W16,
                                                      const int32_t* x_row, const int32_t* d_row, int xblk) {
   __shared__ __attribute__((aligned(16))) __bf16 As[2][kGbM][kGbP];
