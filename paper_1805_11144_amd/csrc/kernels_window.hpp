@@ -760,6 +760,15 @@ __global__ void k_w_reset4(WView w, int64_t rows, Opnd dst, const float* values)
   w4(w, rowof(dst, _r), w.B + _c) = w_f4{v, v, v, v};
 }
 
+// k_w_probe, four entries per thread; the probe buffer is not read again
+// before the host copies it out, so its stores bypass the caches
+__global__ void k_w_probe4(WView w, const int32_t* src, int32_t probe_rows, float* buf, int64_t step0) {
+  W_ITEM4(probe_rows);
+  const uint32_t t = _c / (uint32_t)w.B, b = _c - t * (uint32_t)w.B;
+  const w_f4 v = w4(w, G(src)[_r], w.B + _c);
+  __builtin_nontemporal_store(v, (w_f4*)(buf + ((step0 + t) * probe_rows + _r) * w.B + b));
+}
+
 __device__ __forceinline__ w_f4 w_src4(const WView& w, const float* param, int bcast, int64_t row, int blk,
                                        uint32_t c) {
   if (bcast) {

@@ -929,7 +929,10 @@ void run_window(ms_sim* s, int64_t n_steps) {
     }
     const WView v{s->va, s->vs, s->B, T};
     const int32_t pr = (int32_t)w.probe_rows.size();
-    if (pr > 0)
+    if (pr > 0 && s->B % 4 == 0)
+      hipLaunchKernelGGL(k_w_probe4, dim3(grid_items((double)pr * T * s->B / 4)), dim3(kBlock), 0, s->stream, v,
+                         s->wprobe_src, pr, s->probe_buf, s->steps_total + t0);
+    else if (pr > 0)
       hipLaunchKernelGGL(k_w_probe, dim3(grid_items((double)pr * T * s->B)), dim3(kBlock), 0, s->stream, v,
                          s->wprobe_src, pr, s->probe_buf, s->steps_total + t0);
     if (w.rows_v > 0)
