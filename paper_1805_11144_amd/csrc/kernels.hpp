@@ -321,7 +321,7 @@ __device__ __forceinline__ float input_current(float j, gptr<float> enc, const f
 template <int NDEC>
 __device__ __forceinline__ void ens_op_wave_t(float* st, const Strides& S, int64_t b, const EnsDesc& E,
                                               const EnsOp& o, int lane, float dt) {
-  const int d = E.d, ndec = E.ndec, df0 = E.df[0];
+  const int d = o.x >= 0 ? E.d : 0, ndec = E.ndec, df0 = E.df[0];   // ops without input: J = bias
   gptr<float> enc = G(E.enc) + (int64_t)o.enc * d;
   gptr<float> bias = G(E.bias) + o.bias;
   gptr<float> D0 = G(E.D[0]) + (int64_t)o.D[0] * E.Dcols[0];
@@ -453,7 +453,7 @@ __device__ __forceinline__ void ens_wg_t(float* st, const Strides& S, const EnsD
   const int64_t b = blockIdx.y;
   const int lane = threadIdx.x % 64, wave = threadIdx.x / 64;
   const EnsOp o = load_op(E.ops, op);
-  const int d = E.d, ndec = E.ndec, df0 = E.df[0];
+  const int d = o.x >= 0 ? E.d : 0, ndec = E.ndec, df0 = E.df[0];   // ops without input: J = bias
   gptr<float> enc = G(E.enc) + (int64_t)o.enc * d;
   gptr<float> bias = G(E.bias) + o.bias;
   gptr<float> D0 = G(E.D[0]) + (int64_t)o.D[0] * E.Dcols[0];
@@ -466,7 +466,7 @@ __device__ __forceinline__ void ens_wg_t(float* st, const Strides& S, const EnsD
   load_input(xr, st, S, o.x, b, d);
   // with the transposed copy, encoder k of adjacent neurons is adjacent in memory
   gptr<float> encT = G(E.encT) + (int64_t)o.enc * d;
-  const bool tr = E.encT != nullptr && d <= kMaxXReg;
+  const bool tr = E.encT != nullptr && d > 0 && d <= kMaxXReg;
   for (int r = threadIdx.x; r < o.n; r += 256) {
     // every load of this neuron is issued before any arithmetic or store: the
     // encoders with the index clamped to d - 1 (the extra terms meet xr[k] = 0),
@@ -537,7 +537,7 @@ __device__ __forceinline__ void ens_tile_t(float* st, const Strides& S, int32_t 
   const int64_t b = (int64_t)blockIdx.y * 64 + lane;
   const bool live = b < B;
   const EnsOp o = load_op(E.ops, op);
-  const int d = E.d, ndec = E.ndec, df0 = E.df[0];
+  const int d = o.x >= 0 ? E.d : 0, ndec = E.ndec, df0 = E.df[0];   // ops without input: J = bias
   gptr<float> enc = G(E.enc) + (int64_t)o.enc * d;
   gptr<float> bias = G(E.bias) + o.bias;
   gptr<float> D0 = G(E.D[0]) + (int64_t)o.D[0] * E.Dcols[0];

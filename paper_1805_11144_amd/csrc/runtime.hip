@@ -318,6 +318,7 @@ void build_launches(ms_sim* s, const std::vector<LGroup>& groups, std::vector<La
         std::vector<float> t(he.size(), 0.0f);
         const int64_t d = g.ens_d;
         for (size_t k = 0; k < g.ens_n.size(); ++k) {
+          if (g.ens_x[k] < 0 || g.ens_enc[k] < 0) continue;   // no input, no encoders
           const int64_t e0 = g.ens_enc[k], n = g.ens_n[k];
           for (int64_t r = 0; r < n; ++r)
             for (int64_t q = 0; q < d; ++q) t[(size_t)(e0 * d + q * n + r)] = he[(size_t)((e0 + r) * d + q)];
@@ -332,6 +333,82 @@ void build_launches(ms_sim* s, const std::vector<LGroup>& groups, std::vector<La
     }
     out.push_back(l);
   }
+}
+
+// Row ranges [first, last) of the state array that a fused-ensemble group
+// reads (inputs) and writes (spikes, decoded outputs; voltage and refractory
+// time count as both).
+void ens_rows(const LGroup& g, std::vector<std::pair<int64_t, int64_t>>& rd,
+              std::vector<std::pair<int64_t, int64_t>>& wr) {
+  for (size_t k = 0; k < g.ens_n.size(); ++k) {
+    const int64_t n = g.ens_n[k];
+    if (g.ens_x[k] >= 0) rd.push_back({g.ens_x[k], g.ens_x[k] + g.ens_d});
+    if (g.ens_V[k] >= 0) { wr.push_back({g.ens_V[k], g.ens_V[k] + n}); wr.push_back({g.ens_ref[k], g.ens_ref[k] + n}); }
+    if (g.ens_s[k] >= 0) wr.push_back({g.ens_s[k], g.ens_s[k] + n});
+    for (size_t f = 0; f < g.ens_dd.size(); ++f) wr.push_back({g.ens_dd[f][k], g.ens_dd[f][k] + g.ens_df[f]});
+  }
+}
+
+bool ranges_meet(std::vector<std::pair<int64_t, int64_t>> a, std::vector<std::pair<int64_t, int64_t>> b) {
+  std::sort(a.begin(), a.end());
+  std::sort(b.begin(), b.end());
+  size_t i = 0, j = 0;
+  while (i < a.size() && j < b.size()) {
+    if (a[i].second <= b[j].first) ++i;
+    else if (b[j].second <= a[i].first) ++j;
+    else return true;
+  }
+  return false;
+}
+
+// Two consecutive fused-ensemble groups can run as one launch when they share
+// neuron type, decoded functions and parameter bases, their inputs (if both
+// have any) have one width and encoder base, and neither touches a row the
+// other writes.  The planner keeps them apart because their operator
+// signatures differ (ensembles without input, ensembles whose spikes are
+// stored), which would otherwise cost a launch each per step.
+bool can_merge_ens(const LGroup& A, const LGroup& B) {
+  if (A.type != OP_ENS || B.type != OP_ENS) return false;
+  if (A.ens_type != B.ens_type || A.ens_df != B.ens_df || A.ens_Dbase != B.ens_Dbase ||
+      A.ens_bias_base != B.ens_bias_base)
+    return false;
+  const bool ia = A.a.base >= 0 && A.ens_d > 0, ib = B.a.base >= 0 && B.ens_d > 0;
+  if (ia && ib && (A.ens_d != B.ens_d || A.a.base != B.a.base)) return false;
+  for (int32_t x : A.ens_x) if (x >= 0 && !ia) return false;
+  for (int32_t x : B.ens_x) if (x >= 0 && !ib) return false;
+  std::vector<std::pair<int64_t, int64_t>> ra, wa, rb, wb;
+  ens_rows(A, ra, wa);
+  ens_rows(B, rb, wb);
+  return !ranges_meet(wa, rb) && !ranges_meet(wb, ra) && !ranges_meet(wa, wb);
+}
+
+void append_ens(LGroup& A, const LGroup& B) {
+  const size_t na = A.ens_n.size(), nb = B.ens_n.size();
+  auto params = [&](std::vector<float>& a, const std::vector<float>& b) {
+    if (a.size() == 1 && b.size() == 1 && a[0] == b[0]) return;
+    if (a.size() == 1) a.assign(na, a[0]);
+    if (b.size() == 1) a.insert(a.end(), nb, b[0]);
+    else a.insert(a.end(), b.begin(), b.end());
+  };
+  params(A.tau_rc, B.tau_rc);
+  params(A.tau_ref, B.tau_ref);
+  params(A.amp, B.amp);
+  if (!(A.a.base >= 0 && A.ens_d > 0)) { A.ens_d = B.ens_d; A.a = B.a; A.src = B.src; }
+  auto cat = [](std::vector<int32_t>& a, const std::vector<int32_t>& b) { a.insert(a.end(), b.begin(), b.end()); };
+  cat(A.ops, B.ops);
+  cat(A.ens_n, B.ens_n); cat(A.ens_x, B.ens_x); cat(A.ens_enc, B.ens_enc); cat(A.ens_bias, B.ens_bias);
+  cat(A.ens_V, B.ens_V); cat(A.ens_ref, B.ens_ref); cat(A.ens_s, B.ens_s);
+  for (size_t f = 0; f < A.ens_D.size(); ++f) { cat(A.ens_D[f], B.ens_D[f]); cat(A.ens_dd[f], B.ens_dd[f]); }
+  A.rows += B.rows;
+}
+
+std::vector<LGroup> merge_ens_groups(const std::vector<LGroup>& in) {
+  std::vector<LGroup> out;
+  for (const LGroup& g : in) {
+    if (!out.empty() && can_merge_ens(out.back(), g)) append_ens(out.back(), g);
+    else out.push_back(g);
+  }
+  return out;
 }
 
 void setup_device(ms_sim* s) {
@@ -364,7 +441,12 @@ void setup_device(ms_sim* s) {
   if (!s->state) {
     s->state = dev_alloc<float>(B);
   }
-  build_launches(s, p.lowered, s->launches, p.probe_src_rows, &s->probe_src);
+  // the persistent driver interprets the plan's groups one to one; the launch
+  // drivers run consecutive independent ensemble groups as one launch
+  if (s->driver == MS_DRIVER_STEPS || s->driver == MS_DRIVER_GRAPH)
+    build_launches(s, merge_ens_groups(p.lowered), s->launches, p.probe_src_rows, &s->probe_src);
+  else
+    build_launches(s, p.lowered, s->launches, p.probe_src_rows, &s->probe_src);
   s->probe_rows = (int32_t)p.probe_src_rows.size();
   s->ctr = dev_alloc<int64_t>(2);
   HIPCHECK(hipMemset(s->ctr, 0, 2 * sizeof(int64_t)));
