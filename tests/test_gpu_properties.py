@@ -135,3 +135,25 @@ def test_injected_state_window_driver(name, K):
             assert unpaired_flips(g, e) == 0 and flip_fraction(g, e) <= 1e-4
         elif p.synapse is not None:
             assert float(np.abs(g - e).max()) <= 1e-3
+
+
+@pytest.mark.parametrize("driver", ["steps", "graph"])
+def test_independent_ensemble_groups_share_a_launch(driver):
+    """The sparse-graph model's plan keeps its ensembles without input and its
+    spike-recorded ensemble in groups of their own; the launch drivers run
+    these independent groups as one launch, with the oracle's results (rate
+    mode, 1e-5 relative)."""
+    w = make_workload("c5", neuron_type="lif_rate", n_steps=30, n_ens=12, n_neurons=40, n_eval=200,
+                      n_input_targets=4, n_probed=3)
+    model = M.model_from_spec(w.spec)
+    plan_groups = [g["type"] for g in M.Plan(model, minibatch=1).json()["groups"]]
+    assert plan_groups.count("Ensemble") == 2
+    drv = {"steps": M.DRIVER_STEPS, "graph": M.DRIVER_GRAPH}[driver]
+    with M.Simulator(model, minibatch=1, driver=drv, unroll=7) as sim:
+        assert sim.info()["groups_per_step"] == len(plan_groups) - 1
+        sim.run_steps(w.n_steps, w.feeds)
+        got = [sim.data(p) for p in range(len(w.spec.probes))]
+    ref = OracleSim(w.spec, minibatch=1, param_dtype=np.float32)
+    ref.run_steps(w.n_steps, w.feeds)
+    for p, g in enumerate(got):
+        assert rel_err(g, ref.data(p)) <= 1e-5, p
