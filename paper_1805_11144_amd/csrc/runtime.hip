@@ -745,7 +745,7 @@ void run_persistent(ms_sim* s, int64_t n_steps) {
 }
 
 // ------------------------------------------------------------ window driver
-constexpr double kWindowBytes = 8.0 * (1 << 30);   // budget for the versioned signals
+constexpr double kWindowBytes = 16.0 * (1 << 30);  // budget for the versioned signals (of 288 GB HBM)
 constexpr int32_t kMaxWindow = 1024;
 
 // Launch shape of a fused-ensemble phase: threads cover the largest op's
