@@ -221,7 +221,18 @@ constexpr int kEnsXPre = 4;        // prefetched input values per thread
 // takes a contiguous run of (op, column group), column group fastest, so the
 // column groups of one op share their input and output lines in one L2.  The
 // grid is padded to a multiple of eight; padding workgroups return at once.
-template <int NPT>
+//
+// RW (weights in registers): each wavefront keeps, for the whole window, the
+// encoder fragments of its neuron tiles (tiles wave, wave + nw, ..., at most 4
+// tiles of k <= 16) and the decoder fragments of its neuron chunk (chunk
+// wave % kch, at most 16 k steps), loaded once from global memory.  The units
+// of both products are then assigned so that a wavefront only meets its own
+// fragments; every unit accumulates in the same order as without RW, so the
+// results are the same bit for bit.  Used when encoders and decoders are too
+// large to stage in LDS.
+constexpr int kRwTiles = 4, kRwKd = 4, kRwKs = 16;
+
+template <int NPT, bool RW>
 __global__ void __launch_bounds__(512) k_w_ens(WView w, float* pa, EnsDesc E, float dt, int32_t nmax,
                                                int32_t ts, int32_t cpw, int32_t kch, int xblk, int enc_lds,
                                                int dec_lds, int32_t nops) {
@@ -286,6 +297,22 @@ __global__ void __launch_bounds__(512) k_w_ens(WView w, float* pa, EnsDesc E, fl
   const int qa = lane % 16;
   gptr<float> drow = qa < df0 ? D0 + (int64_t)qa * s0 : D1 + (int64_t)(qa - df0) * s1;
   const int ksteps = (n + 4 * kch - 1) / (4 * kch);
+  float ae[RW ? kRwTiles : 1][RW ? kRwKd : 1], ad[RW ? kRwKs : 1];
+  if constexpr (RW) {
+#pragma unroll
+    for (int i = 0; i < kRwTiles; ++i)
+#pragma unroll
+      for (int kk = 0; kk < kRwKd; ++kk) {
+        const int ra = 16 * (wave + nw * i) + lane % 16, k = 4 * kk + lane / 16;
+        ae[i][kk] = (ra < n && k < d) ? enc[(int64_t)ra * E.d + k] : 0.0f;
+      }
+    const int kc = wave % kch;
+#pragma unroll
+    for (int ks = 0; ks < kRwKs; ++ks) {
+      const int r = 4 * (kc + kch * ks) + lane / 16;
+      ad[ks] = (qa < ndec && r < n && ks < ksteps) ? drow[r] : 0.0f;
+    }
+  }
   for (int32_t t0 = 0; t0 < w.T; t0 += ts) {
     const int tsv = min(ts, w.T - t0);
     // 0. fetch the next sub-window's inputs
@@ -298,6 +325,31 @@ __global__ void __launch_bounds__(512) k_w_ens(WView w, float* pa, EnsDesc E, fl
       xpre[c] = (tsn > 0 && i < ncol * d) ? stage_x(i, t1, tsn) : 0.0f;
     }
     // 1. J = E x + bias
+    if constexpr (RW) {
+#pragma unroll
+      for (int i = 0; i < kRwTiles; ++i) {
+        const int nt = wave + nw * i;
+        if (nt < ntile) {
+          for (int ct = 0; ct < ctiles; ++ct) {
+            const int col = 16 * ct + lane % 16;
+            mfma_f4x acc = {0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll
+            for (int kk = 0; kk < kRwKd; ++kk) {
+              if (kk < kd) {
+                const int k = 4 * kk + lane / 16;
+                const float xb = k < d ? X[col * dp + k] : 0.0f;
+                acc = __builtin_amdgcn_mfma_f32_16x16x4f32(ae[i][kk], xb, acc, 0, 0, 0);
+              }
+            }
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+              const int r = 16 * nt + 4 * (lane / 16) + q;
+              if (r < n) Jb[col * nmax + r] = acc[q] + Bl[r];
+            }
+          }
+        }
+      }
+    } else
     for (int u = wave; u < ntile * ctiles; u += nw) {
       const int nt = u / ctiles, ct = u - nt * ctiles;
       const int col = 16 * ct + lane % 16;
@@ -349,7 +401,23 @@ __global__ void __launch_bounds__(512) k_w_ens(WView w, float* pa, EnsDesc E, fl
     }
     __syncthreads();
     // 3. decoded outputs
-    if (ndec > 0) {
+    if constexpr (RW) {
+      for (int u = wave; ndec > 0 && u < ctiles * kch; u += nw) {
+        const int ct = u / kch, kc = u - ct * kch;   // kc == wave % kch
+        const int col = 16 * ct + lane % 16;
+        mfma_f4x acc = {0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll
+        for (int ks = 0; ks < kRwKs; ++ks) {
+          if (ks < ksteps) {
+            const int r = 4 * (kc + kch * ks) + lane / 16;
+            const float sb = r < n ? Jb[col * nmax + r] : 0.0f;
+            acc = __builtin_amdgcn_mfma_f32_16x16x4f32(ad[ks], sb, acc, 0, 0, 0);
+          }
+        }
+#pragma unroll
+        for (int q = 0; q < 4; ++q) red[(u * 16 + 4 * (lane / 16) + q) * 16 + lane % 16] = acc[q];
+      }
+    } else if (ndec > 0) {
       for (int u = wave; u < ctiles * kch; u += nw) {
         const int ct = u / kch, kc = u - ct * kch;
         const int col = 16 * ct + lane % 16;
@@ -408,14 +476,13 @@ typedef float mfma_f16x __attribute__((ext_vector_type(16)));
 
 constexpr int kGemmBM = 64, kGemmBN = 64, kGemmBK = 16;
 
-__global__ void __launch_bounds__(256) k_w_gemm(WView w, int32_t M, int32_t K, int32_t mtiles, const float* Wt,
-                                                const int32_t* w_row, const int32_t* x_row, const int32_t* d_row,
-                                                int xblk) {
-  __shared__ float As[kGemmBK][kGemmBM + 4];
-  __shared__ float Bs[kGemmBK][kGemmBN + 4];
+// One 64 x 64 tile (rows m0.., columns c0.. of the window) of op's product,
+// by a workgroup of 256 threads, staging through As and Bs.
+__device__ __forceinline__ void gemm64_tile(const WView& w, int32_t M, int32_t K, const float* Wt,
+                                            const int32_t* w_row, const int32_t* x_row, const int32_t* d_row,
+                                            int xblk, int op, int64_t m0, int64_t c0,
+                                            float (*As)[kGemmBM + 4], float (*Bs)[kGemmBN + 4]) {
   const int64_t N = (int64_t)w.T * w.B;
-  const int op = blockIdx.y / mtiles, mt = blockIdx.y - op * mtiles;
-  const int64_t m0 = (int64_t)mt * kGemmBM, c0 = (int64_t)blockIdx.x * kGemmBN;
   const int tid = threadIdx.x, lane = tid % 64, wave = tid / 64;
   const int wm = wave / 2, wn = wave % 2;
   gptr<float> A = G(Wt) + (int64_t)G(w_row)[op] * K;
@@ -454,6 +521,16 @@ __global__ void __launch_bounds__(256) k_w_gemm(WView w, int32_t M, int32_t K, i
   }
 }
 
+__global__ void __launch_bounds__(256) k_w_gemm(WView w, int32_t M, int32_t K, int32_t mtiles, const float* Wt,
+                                                const int32_t* w_row, const int32_t* x_row, const int32_t* d_row,
+                                                int xblk) {
+  __shared__ float As[kGemmBK][kGemmBM + 4];
+  __shared__ float Bs[kGemmBK][kGemmBN + 4];
+  const int op = blockIdx.y / mtiles, mt = blockIdx.y - op * mtiles;
+  gemm64_tile(w, M, K, Wt, w_row, x_row, d_row, xblk, op, (int64_t)mt * kGemmBM, (int64_t)blockIdx.x * kGemmBN,
+              As, Bs);
+}
+
 // Products with few rows and a deep K (M <= 16, K >= 256): one lane per
 // (step, column) of the window, all M rows per lane.  The eight wavefronts of
 // a workgroup take eight contiguous ranges of K and meet in LDS, where their
@@ -479,6 +556,19 @@ __global__ void __launch_bounds__(512) k_w_skinny(WView w, int32_t M, int32_t K,
 #pragma unroll
   for (int m = 0; m < kSkM; ++m) acc[m] = 0.0f;
   int32_t k = kb;
+  // 32 (then 8) input rows are loaded before they are used, so that their
+  // loads are in flight together; each sum still runs over k in order
+  for (; k + 32 <= ke; k += 32) {
+    float xv[32];
+#pragma unroll
+    for (int u = 0; u < 32; ++u) xv[u] = live ? X[(int64_t)(k + u) * w.vs + c] : 0.0f;
+#pragma unroll
+    for (int m = 0; m < kSkM; ++m)
+      if (m < M) {
+#pragma unroll
+        for (int u = 0; u < 32; ++u) acc[m] += A[(int64_t)m * K + k + u] * xv[u];
+      }
+  }
   for (; k + 8 <= ke; k += 8) {
     float xv[8];
 #pragma unroll
@@ -516,9 +606,9 @@ __global__ void __launch_bounds__(512) k_w_skinny(WView w, int32_t M, int32_t K,
 // on one XCD and read that tile from its L2.  The grid is padded to a multiple
 // of eight; the padding workgroups return at once.
 struct TileIdx { int op, mt, nt; bool live; };
-__device__ __forceinline__ TileIdx xcd_tile(uint32_t mtiles, uint32_t ntiles, uint32_t nops) {
+__device__ __forceinline__ TileIdx xcd_tile(uint32_t mtiles, uint32_t ntiles, uint32_t nops, uint32_t g) {
   const uint32_t total = mtiles * ntiles * nops, chunk = (total + 7) / 8;
-  const uint32_t L = (blockIdx.x % 8) * chunk + blockIdx.x / 8;
+  const uint32_t L = (g % 8) * chunk + g / 8;
   TileIdx t{0, 0, 0, L < total};
   if (!t.live) return t;
   t.mt = (int)(L % mtiles);
@@ -535,15 +625,36 @@ __device__ __forceinline__ TileIdx xcd_tile(uint32_t mtiles, uint32_t ntiles, ui
 // are multiples of 4 (so rows of W and of x are 16-byte aligned).
 constexpr int kG2M = 128, kG2N = 128, kG2K = 16;
 
+//
+// Tail split: when the 128 x 128 tiles number a little more than a whole
+// multiple of the CUs, the last column tiles would leave most CUs idle while
+// a few finish one extra tile.  The launch then covers only the first ntiles
+// column tiles with 128 x 128 tiles (workgroups 0 .. gbig-1) and the columns
+// after them with 64 x 64 tiles (workgroups gbig ..), a quarter of the work
+// each, which the CUs take up beside their large tiles.  Both tile sizes add
+// k in the same order (slices of 16, pairs on v_mfma_f32_32x32x2f32), so the
+// split does not change any result.
 __global__ void __launch_bounds__(256, 4) k_w_gemm2(WView w, int32_t M, int32_t K, int32_t mtiles, int32_t ntiles,
                                                  int32_t nops, const float* Wt, const int32_t* w_row,
-                                                 const int32_t* x_row, const int32_t* d_row, int xblk) {
+                                                 const int32_t* x_row, const int32_t* d_row, int xblk,
+                                                 uint32_t gbig) {
   typedef float f4v __attribute__((ext_vector_type(4)));
   __shared__ float As[2][kG2K][kG2M + 4];
   __shared__ float Bs[2][kG2K][kG2N + 4];
-  const TileIdx ti = xcd_tile(mtiles, ntiles, nops);
-  if (!ti.live) return;
   const int64_t N = (int64_t)w.T * w.B;
+  if (blockIdx.x >= gbig) {   // 64 x 64 tiles of the columns after the large tiles
+    const int64_t cs = (int64_t)ntiles * kG2N;
+    const uint32_t mt2 = (uint32_t)((M + kGemmBM - 1) / kGemmBM);
+    const uint32_t nt2 = (uint32_t)((N - cs + kGemmBN - 1) / kGemmBN);
+    const TileIdx st = xcd_tile(mt2, nt2, nops, blockIdx.x - gbig);
+    if (!st.live) return;
+    gemm64_tile(w, M, K, Wt, w_row, x_row, d_row, xblk, st.op, (int64_t)st.mt * kGemmBM,
+                cs + (int64_t)st.nt * kGemmBN, (float(*)[kGemmBM + 4]) & As[0][0][0],
+                (float(*)[kGemmBN + 4]) & Bs[0][0][0]);
+    return;
+  }
+  const TileIdx ti = xcd_tile(mtiles, ntiles, nops, blockIdx.x);
+  if (!ti.live) return;
   const int op = ti.op, mt = ti.mt;
   const int64_t m0 = (int64_t)mt * kG2M, c0 = (int64_t)ti.nt * kG2N;
   const int tid = threadIdx.x, lane = tid % 64, wave = tid / 64;
@@ -650,6 +761,9 @@ __global__ void __launch_bounds__(256, 4) k_w_gemm2(WView w, int32_t M, int32_t 
 // B % 4 == 0.
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 constexpr int kGbM = 128, kGbN = 128, kGbK = 32, kGbP = 40, kGbU = kGbK / 16;
+static_assert(kGemmBK == kG2K && kGemmBK * (kGemmBM + 4) <= 2 * kG2K * (kG2M + 4) &&
+                  kGemmBK * (kGemmBN + 4) <= 2 * kG2K * (kG2N + 4),
+              "the tail tiles of k_w_gemm2 add k in the same slices and fit its LDS arrays");
 static_assert(kGbM == kG2M && kGbN == kG2N, "the two large-product kernels share their tile grid");
 
 __global__ void __launch_bounds__(256, 3) k_w_gemm_bf16(WView w, int32_t M, int32_t K, int32_t mtiles,
@@ -657,7 +771,7 @@ __global__ void __launch_bounds__(256, 3) k_w_gemm_bf16(WView w, int32_t M, int3
                                                      const int32_t* x_row, const int32_t* d_row, int xblk) {
   __shared__ __attribute__((aligned(16))) __bf16 As[2][kGbM][kGbP];
   __shared__ __attribute__((aligned(16))) __bf16 Bs[2][kGbN][kGbP];
-  const TileIdx ti = xcd_tile(mtiles, ntiles, nops);
+  const TileIdx ti = xcd_tile(mtiles, ntiles, nops, blockIdx.x);
   if (!ti.live) return;
   const int64_t N = (int64_t)w.T * w.B;
   const int op = ti.op, mt = ti.mt;

@@ -63,7 +63,7 @@ struct Launch {
   // window driver
   int32_t src_blk = 1, a_blk = 1;    // block offsets of src / a (1: this step, 0: previous step)
   int32_t nmax = 0, npt = 1, nthr = 64, ts = 16, cpw = 1, kch = 1;   // fused-ensemble launch shape
-  int32_t enc_lds = 0, dec_lds = 0;
+  int32_t enc_lds = 0, dec_lds = 0, rw = 0;   // rw: encoder/decoder fragments held in registers
   size_t lds = 0;
   const uint16_t* w16 = nullptr;     // DOT_INC on bf16 MFMA: W rounded to bf16, op k at k*M*K
 };
@@ -108,6 +108,7 @@ struct ms_sim {
   PersistentProgram prog{};
   bool persistent_ok = false;
   size_t lds_limit = 0;              // dynamic LDS bytes one workgroup may use
+  int32_t n_cu = 256;                // compute units of the device
   int32_t persistent_threads = 256;  // workgroup size of the persistent kernel
   int64_t scratch_n = 0;             // per-column scratch floats of the persistent kernel
   float* scratch = nullptr;          // global scratch when state is not LDS-resident
@@ -784,6 +785,17 @@ void ens_shape(ms_sim* s, Launch& l, const LGroup& g) {
   l.ts = (int32_t)ts;
   l.kch = (int32_t)kch_of(ts);
   l.lds = (size_t)bytes(ts);
+  // weights too large for LDS: keep each wavefront's encoder and decoder
+  // fragments in registers for the whole window, when they fit the kernel's
+  // register arrays (at most 4 neuron tiles of 16 per wavefront, d <= 16, at
+  // most 16 k steps of 4 per decoder chunk, each wavefront on one chunk)
+  const int64_t ntile = ((int64_t)nmax + 15) / 16, ksteps = ((int64_t)nmax + 4 * l.kch - 1) / (4 * l.kch);
+  if (l.npt == 1 && !(l.enc_lds && l.dec_lds) && ntile <= 4 * nw && dp <= 16 && l.ens.ndec <= 16 &&
+      nw % l.kch == 0 && ksteps <= 16) {
+    l.rw = 1;
+    l.enc_lds = l.dec_lds = 0;
+    l.lds = (size_t)((l.cpw * ts * (dp + nmax) + (l.cpw * ts / 16) * l.kch * 256 + nmax) * (int64_t)sizeof(float));
+  }
 }
 
 // Steps per window for a run of n_steps: as many as the run needs, up to the
@@ -834,6 +846,7 @@ void setup_window(ms_sim* s) {
   int lds_max = 0;
   HIPCHECK(hipDeviceGetAttribute(&lds_max, hipDeviceAttributeMaxSharedMemoryPerBlock, s->device));
   s->lds_limit = (size_t)lds_max;
+  HIPCHECK(hipDeviceGetAttribute(&s->n_cu, hipDeviceAttributeMultiprocessorCount, s->device));
   s->pa = dev_alloc<float>((size_t)std::max<int64_t>(1, w.rows_p) * B);
   ensure_window(s, 1);
   for (int k = 0; k < ms_sim::kSide; ++k) HIPCHECK(hipStreamCreateWithFlags(&s->side[k], hipStreamNonBlocking));
@@ -863,10 +876,11 @@ void setup_window(ms_sim* s) {
     }
   }
   if (s->lds_limit > 65536) {
-    HIPCHECK(hipFuncSetAttribute((const void*)k_w_ens<1>, hipFuncAttributeMaxDynamicSharedMemorySize, (int)s->lds_limit));
-    HIPCHECK(hipFuncSetAttribute((const void*)k_w_ens<2>, hipFuncAttributeMaxDynamicSharedMemorySize, (int)s->lds_limit));
-    HIPCHECK(hipFuncSetAttribute((const void*)k_w_ens<4>, hipFuncAttributeMaxDynamicSharedMemorySize, (int)s->lds_limit));
-    HIPCHECK(hipFuncSetAttribute((const void*)k_w_ens<8>, hipFuncAttributeMaxDynamicSharedMemorySize, (int)s->lds_limit));
+    HIPCHECK(hipFuncSetAttribute((const void*)k_w_ens<1, false>, hipFuncAttributeMaxDynamicSharedMemorySize, (int)s->lds_limit));
+    HIPCHECK(hipFuncSetAttribute((const void*)k_w_ens<2, false>, hipFuncAttributeMaxDynamicSharedMemorySize, (int)s->lds_limit));
+    HIPCHECK(hipFuncSetAttribute((const void*)k_w_ens<4, false>, hipFuncAttributeMaxDynamicSharedMemorySize, (int)s->lds_limit));
+    HIPCHECK(hipFuncSetAttribute((const void*)k_w_ens<8, false>, hipFuncAttributeMaxDynamicSharedMemorySize, (int)s->lds_limit));
+    HIPCHECK(hipFuncSetAttribute((const void*)k_w_ens<1, true>, hipFuncAttributeMaxDynamicSharedMemorySize, (int)s->lds_limit));
   }
   HIPCHECK(hipMemset(s->pa, 0, (size_t)std::max<int64_t>(1, w.rows_p) * B * sizeof(float)));
 }
@@ -918,13 +932,30 @@ void launch_phase(ms_sim* s, const Launch& l, int32_t T, int64_t t0, hipStream_t
         const double ntiles = std::ceil(tb / kG2N);
         const double total = ntiles * mtiles * (double)l.rows;
         if (total >= 2147483648.0 - 8) fail(MS_E_INVALID, "window product too large for the GEMM grid");
-        const unsigned grid = (unsigned)(8 * (((int64_t)total + 7) / 8));
-        if (l.w16)
+        if (l.w16) {
+          const unsigned grid = (unsigned)(8 * (((int64_t)total + 7) / 8));
           hipLaunchKernelGGL(k_w_gemm_bf16, dim3(grid), dim3(256), 0, q, w, l.M, l.K, mtiles, (int32_t)ntiles,
                              (int32_t)l.rows, l.w16, l.x_row, l.d_row, l.src_blk);
-        else
-          hipLaunchKernelGGL(k_w_gemm2, dim3(grid), dim3(256), 0, q, w, l.M, l.K, mtiles, (int32_t)ntiles,
-                             (int32_t)l.rows, l.a_base, l.w_row, l.x_row, l.d_row, l.src_blk);
+        } else {
+          // tail split: when every tile is resident at once (at most 4 per CU)
+          // and the count is not a whole multiple of the CUs, the column tiles
+          // beyond the last whole multiple run as 64 x 64 tiles
+          const int64_t ncu = std::max<int32_t>(1, s->n_cu), tiles = (int64_t)total;
+          const int64_t per_col = (int64_t)mtiles * l.rows;
+          int64_t nbig = (int64_t)ntiles, small = 0;
+          if (tiles > ncu && tiles <= 4 * ncu && tiles % ncu != 0) {
+            const int64_t nb = (tiles / ncu) * ncu / per_col;
+            if (nb >= 1 && nb < nbig) {
+              nbig = nb;
+              small = (int64_t)((l.M + kGemmBM - 1) / kGemmBM) * l.rows *
+                      (((int64_t)tb - nb * kG2N + kGemmBN - 1) / kGemmBN);
+            }
+          }
+          const int64_t gbig = 8 * ((nbig * per_col + 7) / 8);
+          const unsigned grid = (unsigned)(gbig + 8 * ((small + 7) / 8));
+          hipLaunchKernelGGL(k_w_gemm2, dim3(grid), dim3(256), 0, q, w, l.M, l.K, mtiles, (int32_t)nbig,
+                             (int32_t)l.rows, l.a_base, l.w_row, l.x_row, l.d_row, l.src_blk, (uint32_t)gbig);
+        }
       } else if (l.M <= kSkM && l.K >= 256) {
         const double ctiles = std::ceil(tb / 64);
         if (ctiles * l.rows >= 2147483648.0) fail(MS_E_INVALID, "window product too large for the grid");
@@ -960,14 +991,16 @@ void launch_phase(ms_sim* s, const Launch& l, int32_t T, int64_t t0, hipStream_t
       if (total >= 2147483648LL - 8) fail(MS_E_INVALID, "too many ensemble workgroups");
       const dim3 grid((unsigned)(8 * ((total + 7) / 8)));
       const int32_t nops = (int32_t)l.rows;
-      if (l.npt == 1)
-        hipLaunchKernelGGL(k_w_ens<1>, grid, dim3(l.nthr), l.lds, q, w, s->pa, l.ens, s->dt, l.nmax, l.ts, l.cpw, l.kch, l.src_blk, l.enc_lds, l.dec_lds, nops);
+      if (l.rw)
+        hipLaunchKernelGGL((k_w_ens<1, true>), grid, dim3(l.nthr), l.lds, q, w, s->pa, l.ens, s->dt, l.nmax, l.ts, l.cpw, l.kch, l.src_blk, l.enc_lds, l.dec_lds, nops);
+      else if (l.npt == 1)
+        hipLaunchKernelGGL((k_w_ens<1, false>), grid, dim3(l.nthr), l.lds, q, w, s->pa, l.ens, s->dt, l.nmax, l.ts, l.cpw, l.kch, l.src_blk, l.enc_lds, l.dec_lds, nops);
       else if (l.npt == 2)
-        hipLaunchKernelGGL(k_w_ens<2>, grid, dim3(l.nthr), l.lds, q, w, s->pa, l.ens, s->dt, l.nmax, l.ts, l.cpw, l.kch, l.src_blk, l.enc_lds, l.dec_lds, nops);
+        hipLaunchKernelGGL((k_w_ens<2, false>), grid, dim3(l.nthr), l.lds, q, w, s->pa, l.ens, s->dt, l.nmax, l.ts, l.cpw, l.kch, l.src_blk, l.enc_lds, l.dec_lds, nops);
       else if (l.npt == 4)
-        hipLaunchKernelGGL(k_w_ens<4>, grid, dim3(l.nthr), l.lds, q, w, s->pa, l.ens, s->dt, l.nmax, l.ts, l.cpw, l.kch, l.src_blk, l.enc_lds, l.dec_lds, nops);
+        hipLaunchKernelGGL((k_w_ens<4, false>), grid, dim3(l.nthr), l.lds, q, w, s->pa, l.ens, s->dt, l.nmax, l.ts, l.cpw, l.kch, l.src_blk, l.enc_lds, l.dec_lds, nops);
       else
-        hipLaunchKernelGGL(k_w_ens<8>, grid, dim3(l.nthr), l.lds, q, w, s->pa, l.ens, s->dt, l.nmax, l.ts, l.cpw, l.kch, l.src_blk, l.enc_lds, l.dec_lds, nops);
+        hipLaunchKernelGGL((k_w_ens<8, false>), grid, dim3(l.nthr), l.lds, q, w, s->pa, l.ens, s->dt, l.nmax, l.ts, l.cpw, l.kch, l.src_blk, l.enc_lds, l.dec_lds, nops);
       break;
     }
     default: fail(MS_E_INVALID, "unknown group type");

@@ -117,3 +117,75 @@ def test_window_product_kernels(neuron_type):
             d = float(np.abs(g - e).max())
             print(f"probe {pi}: abs {d:.2e}")
             assert d <= 1e-3, (pi, d)
+
+
+@pytest.mark.parametrize("neuron_type", ["lif_rate", "lif"])
+def test_window_ensembles_weights_in_registers(neuron_type):
+    """Ensembles whose encoders and decoders (300 x 16 each) are too large to
+    stage in LDS: the fused window kernel keeps each wavefront's fragments in
+    registers (neuron tiles 300 = 18 3/4 x 16: a ragged last tile; decoder
+    chunks of 15 k steps).  Checked against the oracle like the other
+    window-driver runs."""
+    w = make_workload("c4", neuron_type=neuron_type, n_steps=40, minibatch=2, n_ens=3, n_neurons=300,
+                      n_eval=300)
+    got = run_gpu(w, driver=M.DRIVER_WINDOW)
+    exp = run_oracle(w)
+    for pi, (g, e) in enumerate(zip(got, exp)):
+        if neuron_type == "lif_rate":
+            if w.spec.probes[pi].target[0] != "neurons":
+                r = rel_err(g, e)
+                print(f"probe {pi}: rel {r:.2e}")
+                assert r <= 1e-5, (pi, r)
+        elif w.spec.probes[pi].target[0] == "neurons":
+            f, u = flip_fraction(g, e), unpaired_flips(g, e)
+            print(f"probe {pi}: flips {f:.2e} of {int((e > 0).sum())} spikes, unpaired {u}")
+            assert u == 0 and f <= 2e-3, (pi, f, u)
+        else:
+            d = float(np.abs(g - e).max())
+            print(f"probe {pi}: abs {d:.2e}")
+            assert d <= 1e-3, (pi, d)
+
+
+@pytest.mark.parametrize("neuron_type", ["lif_rate", "lif"])
+def test_window_product_tail_split(neuron_type):
+    """A product with more 128 x 128 tiles than CUs but not a whole multiple
+    of them (300 rows = 3 row tiles, 64 x 180 = 11520 columns = 90 column
+    tiles: 270 tiles): the columns beyond the last whole multiple of the CUs
+    run as 64 x 64 tiles in the same launch (ragged in rows and columns).
+    The split leaves every sum in the same order: in rate mode the hidden
+    layers equal those of the time-major driver bit for bit.
+
+    Rate mode: the hidden layers take the backward-error check of the
+    full-size tests.  The 10-D readout sums 300 rates, some of neurons so
+    close to threshold that float32 rounding of their current moves the
+    readout by 2.5e-4 of its peak in the first steps, on every driver alike;
+    it is held to 1e-3 against the oracle and to 1e-5 against the time-major
+    driver, whose products run on other kernels.  Spiking mode: the bounds of
+    the other window-driver runs."""
+    from tests.test_gpu_fullsize import check, oracle_run
+    w = make_workload("c3", neuron_type=neuron_type, n_steps=180, minibatch=64, n_hidden=300, n_in=136)
+    got = run_gpu(w, driver=M.DRIVER_WINDOW)
+    if neuron_type == "lif":
+        # whole-run spiking protocol of test_spiking_mode_parity: a one-step
+        # spike shift moves the readout by a whole spike, so the filtered
+        # readout is reported here and bounded in the injected-state tests
+        exp = run_oracle(w)
+        for pi, (g, e) in enumerate(zip(got, exp)):
+            if w.spec.probes[pi].target[0] == "neurons":
+                f, u = flip_fraction(g, e), unpaired_flips(g, e)
+                print(f"probe {pi}: flips {f:.2e} of {int((e > 0).sum())} spikes, unpaired {u}")
+                assert u == 0 and f <= 2e-3, (pi, f, u)
+            else:
+                print(f"probe {pi}: abs {float(np.abs(g - e).max()):.2e}")
+        return
+    ref = run_gpu(w, driver=M.DRIVER_STEPS)
+    out = oracle_run(w)
+    dec = [pi for pi, p in enumerate(w.spec.probes) if p.target[0] != "neurons"]
+    for pi in dec:
+        r, rs = rel_err(got[pi], out[0][pi]), rel_err(got[pi], ref[pi])
+        print(f"probe {pi}: rel {r:.2e} against the oracle, {rs:.2e} against the time-major driver")
+        assert r <= 1e-3 and rs <= 1e-5, (pi, r, rs)
+    neu = [pi for pi in range(len(got)) if pi not in dec]
+    for pi in neu:
+        assert np.array_equal(got[pi], ref[pi]), pi
+    check(w, [got[pi] if pi in neu else out[0][pi] for pi in range(len(got))], out, False)
