@@ -238,15 +238,19 @@ __device__ __forceinline__ float neuron_update(int ntype, float j, float& v, flo
 // wavefront.  Returns the neuron output (amp_dt = amplitude / dt or 0).
 __device__ __forceinline__ float lif_update_bf(float j, float& v, float& rf, float tau_rc, float tau_ref,
                                                float amp_dt, float full, float dt, float inv_tau) {
-  const float integ = fminf(fmaxf(dt - rf, 0.0f), dt);
+  const float integ = __builtin_amdgcn_fmed3f(dt - rf, 0.0f, dt);   // clamp to [0, dt] (v_med3_f32)
   const float ep = expm1_small(-integ * inv_tau);
   const float e = rf > 0.0f ? ep : full;
   v = v - (j - v) * e;
   rf = fmaxf(rf - dt, 0.0f);
   const float drive = j - 1.0f;
   const float q = (v - 1.0f) * __builtin_amdgcn_rcpf(drive);
-  const float lg = fminf(-tau_rc * kLn2 * __builtin_amdgcn_logf(1.0f - q), integ);
-  const float since = drive > 0.0f ? (q >= 1.0f ? integ : lg) : 0.0f;
+  const float lg = -tau_rc * kLn2 * __builtin_amdgcn_logf(1.0f - q);
+  float since = drive > 0.0f ? (q >= 1.0f || lg > integ ? integ : lg) : 0.0f;
+  // an empty asm statement that takes the crossing time as an operand: it is
+  // computed on every lane, so the compiler selects instead of branching on
+  // the spike (a branch runs both sides anyway when the lanes disagree)
+  __asm__ volatile("" : "+v"(since));
   const bool spk = v > 1.0f;
   v = spk ? 0.0f : fmaxf(v, 0.0f);
   rf = spk ? tau_ref - since : rf;

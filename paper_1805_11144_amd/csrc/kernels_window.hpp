@@ -297,6 +297,29 @@ __global__ void __launch_bounds__(512) k_w_ens(WView w, float* pa, EnsDesc E, fl
   const int qa = lane % 16;
   gptr<float> drow = qa < df0 ? D0 + (int64_t)qa * s0 : D1 + (int64_t)(qa - df0) * s1;
   const int ksteps = (n + 4 * kch - 1) / (4 * kch);
+  // Slots that stay fixed for the whole window, so that the sub-window loop
+  // does no integer division: input value tid + c*nthr of a sub-window (its
+  // LDS index, as dp == d whenever d > 0) is step st, column cc, dimension k,
+  // packed st | cc << 7 | k << 16, st = 127 for a column beyond B, -1 past the
+  // inputs; output tid is step st, column c, decoded dimension q, packed the
+  // same way (st | c << 7 | q << 16), -1 past the outputs.  The host keeps
+  // ts <= 64, cpw <= 512 and d, ndec < 32768.
+  int32_t xslot[kEnsXPre];
+#pragma unroll
+  for (int c = 0; c < kEnsXPre; ++c) {
+    const int i = tid + c * nthr;
+    if (i < ncol * d) {
+      const int col = i / d, k = i - col * d, cc = col / ts, st = col - cc * ts;
+      xslot[c] = (b0 + cc < w.B ? st : 127) | (cc << 7) | (k << 16);
+    } else {
+      xslot[c] = -1;
+    }
+  }
+  int32_t oslot = -1;
+  if (tid < ndec * ncol) {
+    const int q = tid / ncol, col = tid - q * ncol, c = col / ts;
+    oslot = (col - c * ts) | (c << 7) | (q << 16);
+  }
   float ae[RW ? kRwTiles : 1][RW ? kRwKd : 1], ad[RW ? kRwKs : 1];
   if constexpr (RW) {
 #pragma unroll
@@ -321,8 +344,10 @@ __global__ void __launch_bounds__(512) k_w_ens(WView w, float* pa, EnsDesc E, fl
     float xpre[kEnsXPre];
 #pragma unroll
     for (int c = 0; c < kEnsXPre; ++c) {
-      const int i = tid + c * nthr;
-      xpre[c] = (tsn > 0 && i < ncol * d) ? stage_x(i, t1, tsn) : 0.0f;
+      const int32_t ps = xslot[c], st = ps & 127;
+      xpre[c] = (ps >= 0 && st < tsn)
+                    ? xsrc[(int64_t)(ps >> 16) * w.vs + (int64_t)(t1 + st) * w.B + b0 + ((ps >> 7) & 511)]
+                    : 0.0f;
     }
     // 1. J = E x + bias
     if constexpr (RW) {
@@ -369,13 +394,8 @@ __global__ void __launch_bounds__(512) k_w_ens(WView w, float* pa, EnsDesc E, fl
     __syncthreads();
     // next inputs into LDS (every read of this sub-window's X is done)
 #pragma unroll
-    for (int c = 0; c < kEnsXPre; ++c) {
-      const int i = tid + c * nthr;
-      if (tsn > 0 && i < ncol * d) {
-        const int col = i / d, k = i - col * d;
-        X[col * dp + k] = xpre[c];
-      }
-    }
+    for (int c = 0; c < kEnsXPre; ++c)
+      if (tsn > 0 && xslot[c] >= 0) X[tid + c * nthr] = xpre[c];
     if (tsn > 0) {   // inputs beyond the prefetch registers
       for (int i = tid + kEnsXPre * nthr; i < ncol * d; i += nthr) {
         const int col = i / d, k = i - col * d;
@@ -434,7 +454,14 @@ __global__ void __launch_bounds__(512) k_w_ens(WView w, float* pa, EnsDesc E, fl
     }
     __syncthreads();
     for (int i = tid; i < ndec * ncol; i += nthr) {
-      const int q = i / ncol, col = i - q * ncol, c = col / ts, st = col - c * ts;
+      int q, c, st;
+      if (i == tid) {
+        st = oslot & 127, c = (oslot >> 7) & 511, q = oslot >> 16;
+      } else {
+        const int cl = i - (q = i / ncol) * ncol;
+        c = cl / ts, st = cl - c * ts;
+      }
+      const int col = c * ts + st;
       if (st < tsv && b0 + c < w.B) {
         float sum = 0.0f;
         for (int kc = 0; kc < kch; ++kc) sum += red[(((col / 16) * kch + kc) * 16 + q) * 16 + col % 16];

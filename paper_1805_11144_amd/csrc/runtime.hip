@@ -760,6 +760,7 @@ void ens_shape(ms_sim* s, Launch& l, const LGroup& g) {
   l.nthr = (int32_t)std::min<int64_t>(512, ((int64_t)nmax * l.cpw + 63) / 64 * 64);
   l.npt = (int32_t)(((int64_t)nmax * l.cpw + l.nthr - 1) / l.nthr);
   if (l.npt > 8) fail(MS_E_INVALID, "ensemble too large for the window driver (more than 4096 neurons)");
+  if (l.ens.d >= 32768 || l.ens.ndec >= 32768) fail(MS_E_INVALID, "ensemble dimensions too large for the window driver");
   l.npt = l.npt <= 1 ? 1 : l.npt <= 2 ? 2 : l.npt <= 4 ? 4 : 8;
   const int64_t nw = l.nthr / 64, dp = std::max<int32_t>(1, l.ens.d);
   // sub-window: the longest (a multiple of 16, at most 64 steps) that keeps
