@@ -138,7 +138,7 @@ def cpu_baseline(w, budget_s=15.0):
                       f"float64 numpy, {dt:.1f} s"}
 
 
-def measure_roofline(M, model, w, sim, info, feeds, bf16=False):
+def measure_roofline(M, model, w, sim, info, feeds, bf16=False, plan_opts=None, default_plan=True):
     """Roofline of the dominant kernel, timed with HIP events on the stream it
     runs on (one extra run with per-launch timing; the plain-launch driver
     stands in for the hipGraph driver, whose kernels are the same)."""
@@ -152,7 +152,8 @@ def measure_roofline(M, model, w, sim, info, feeds, bf16=False):
                 "frac": round(ach / HBM_PEAK_GBS, 4), "traffic": None, "kernel": "k_persistent",
                 "launch_ms": round(ms, 4), "launches": 1, "work_per_launch": int(b)}
     tsim = sim if drv in (M.DRIVER_WINDOW, M.DRIVER_STEPS) else \
-        M.Simulator(model, minibatch=w.minibatch, driver=M.DRIVER_STEPS, probe_capacity_steps=T)
+        M.Simulator(model, minibatch=w.minibatch, driver=M.DRIVER_STEPS, probe_capacity_steps=T,
+                    **(plan_opts or {}))
     tsim.set_timing(True)
     tsim.reset()
     tsim.run_steps(T, feeds)
@@ -174,7 +175,7 @@ def measure_roofline(M, model, w, sim, info, feeds, bf16=False):
             work, bound, peak, unit = byts * T, "hbm", HBM_PEAK_GBS, "GB/s"
             kernel = "k_ens_wg" if w.minibatch < 32 else "k_ens_tile"
     elif top == M.mergesim.OP_DOT_INC:
-        work = dot_flops_per_step(M.Plan(model, minibatch=w.minibatch).json(), w.minibatch) * T
+        work = dot_flops_per_step(M.Plan(model, minibatch=w.minibatch, **(plan_opts or {})).json(), w.minibatch) * T
         bound, peak, unit = "mfma", FP32_MFMA_PEAK_TFLOPS, "TFLOP/s"
         kernel = "k_w_gemm2" if window else "k_dot_inc"
         if bf16:
@@ -186,7 +187,7 @@ def measure_roofline(M, model, w, sim, info, feeds, bf16=False):
     ach = work / (ms * 1e-3) / scale
     op_names = {M.mergesim.OP_ENSEMBLE: "Ensemble", M.mergesim.OP_DOT_INC: "DotInc"}
     return {"bound": bound, "achieved": round(ach, 3), "peak": peak, "unit": unit,
-            "frac": round(ach / peak, 4), "traffic": stored_traffic(kernel, w.name),
+            "frac": round(ach / peak, 4), "traffic": stored_traffic(kernel, w.name) if default_plan else None,
             "kernel": kernel, "op": op_names.get(top, str(top)), "launch_ms": round(ms / max(n, 1), 4),
             "launches": n, "work_per_launch": int(work / max(n, 1))}
 
@@ -291,6 +292,13 @@ def main():
     ap.add_argument("--timesteps", type=int, default=0,
                     help="override the workload's timesteps (counter passes: per-launch traffic of a "
                          "time-major kernel does not depend on the run length)")
+    ap.add_argument("--planner", default="tree", choices=["tree", "greedy"],
+                    help="operator-merging planner (ablation; default: tree search, depth 3)")
+    ap.add_argument("--planner-depth", type=int, default=3)
+    ap.add_argument("--no-merge", action="store_true", help="ablation: one group per operator")
+    ap.add_argument("--no-sort", action="store_true", help="ablation: signals and operators in build order")
+    ap.add_argument("--no-simplify", action="store_true", help="ablation: skip simplification")
+    ap.add_argument("--no-fuse", action="store_true", help="ablation: no fused ensemble operators")
     ap.add_argument("--counters-run", action="store_true",
                     help="one untimed run for a rocprofv3 --pmc pass (with --copy-probe); prints no JSON")
     args = ap.parse_args()
@@ -312,8 +320,11 @@ def main():
               "persistent": M.DRIVER_PERSISTENT, "window": M.DRIVER_WINDOW}[args.driver]
     dev = torch.device("cuda:0")
     t_build = time.perf_counter()
+    plan_opts = dict(planner=M.PLANNER_TREE if args.planner == "tree" else M.PLANNER_GREEDY,
+                     planner_depth=args.planner_depth, merge=not args.no_merge, sort=not args.no_sort,
+                     simplify=not args.no_simplify, fuse=not args.no_fuse)
     sim = M.Simulator(model, minibatch=w.minibatch, driver=driver, unroll=20,
-                      probe_capacity_steps=w.n_steps, gemm_dtype=args.gemm_dtype)
+                      probe_capacity_steps=w.n_steps, gemm_dtype=args.gemm_dtype, **plan_opts)
     t_build = time.perf_counter() - t_build
     feeds = {i: torch.from_numpy(f).to(dev) for i, f in w.feeds.items()}
     if args.copy_probe:
@@ -350,7 +361,9 @@ def main():
     value = neuron_steps / (elapsed / args.steps)
     info = sim.info()
     bf16 = args.gemm_dtype == "bf16"
-    roofline = measure_roofline(M, model, w, sim, info, feeds, bf16)
+    default_plan = (args.planner, args.planner_depth, args.no_merge, args.no_sort, args.no_simplify,
+                    args.no_fuse) == ("tree", 3, False, False, False, False)
+    roofline = measure_roofline(M, model, w, sim, info, feeds, bf16, plan_opts, default_plan)
     out = {
         "metric": "neuron-timesteps/sec (x minibatch) on 1 MI355X",
         "value": value, "unit": "neuron-timesteps/s", "n_gpus": 1, "steps": args.steps,
@@ -361,7 +374,10 @@ def main():
                    "driver": {1: "steps", 2: "graph", 3: "persistent", 4: "window"}.get(info["driver"]),
                    "launches_per_window" if info["driver"] == M.DRIVER_WINDOW else "groups_per_step":
                        info["groups_per_step"], "build_s": round(t_build, 2),
-                   "gemm_dtype": args.gemm_dtype},
+                   "gemm_dtype": args.gemm_dtype,
+                   "plan": {"planner": args.planner, "depth": args.planner_depth, "merge": not args.no_merge,
+                            "sort": not args.no_sort, "simplify": not args.no_simplify,
+                            "fuse": not args.no_fuse}},
         "roofline": roofline,
     }
     if not args.no_cpu_baseline:
