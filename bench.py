@@ -138,7 +138,7 @@ def cpu_baseline(w, budget_s=15.0):
                       f"float64 numpy, {dt:.1f} s"}
 
 
-def measure_roofline(M, model, w, sim, info, feeds, bf16=False, plan_opts=None, default_plan=True):
+def measure_roofline(M, model, w, sim, info, feeds, bf16=False, plan_opts=None, default_plan=True, event=False):
     """Roofline of the dominant kernel, timed with HIP events on the stream it
     runs on (one extra run with per-launch timing; the plain-launch driver
     stands in for the hipGraph driver, whose kernels are the same)."""
@@ -183,11 +183,24 @@ def measure_roofline(M, model, w, sim, info, feeds, bf16=False, plan_opts=None, 
     else:
         work, bound, peak, unit = compulsory_bytes_per_step(w) * T, "hbm", HBM_PEAK_GBS, "GB/s"
         kernel = f"op type {top}"
+    basis = "algorithmic"
+    if event and top == M.mergesim.OP_ENSEMBLE and not window:
+        # event-driven decoding moves fewer bytes than the method's dense
+        # work: its rate is reported from measured counter bytes, if taken
+        rec = stored_traffic(kernel, w.name + "event")
+        basis = "counter bytes"
+        if rec is None:
+            return {"bound": bound, "achieved": None, "peak": peak, "unit": unit, "frac": None,
+                    "traffic": None, "basis": basis, "kernel": kernel, "op": "Ensemble",
+                    "launch_ms": round(ms / max(n, 1), 4), "launches": n}
+        work = rec * n
     scale = 1e12 if unit == "TFLOP/s" else 1e9
     ach = work / (ms * 1e-3) / scale
     op_names = {M.mergesim.OP_ENSEMBLE: "Ensemble", M.mergesim.OP_DOT_INC: "DotInc"}
     return {"bound": bound, "achieved": round(ach, 3), "peak": peak, "unit": unit,
-            "frac": round(ach / peak, 4), "traffic": stored_traffic(kernel, w.name) if default_plan else None,
+            "frac": round(ach / peak, 4),
+            "traffic": stored_traffic(kernel, w.name + ("event" if event else "")) if default_plan else None,
+            "basis": basis,
             "kernel": kernel, "op": op_names.get(top, str(top)), "launch_ms": round(ms / max(n, 1), 4),
             "launches": n, "work_per_launch": int(work / max(n, 1))}
 
@@ -260,10 +273,11 @@ def summarize_traffic(args):
             raise SystemExit(f"kernels {names} not found in {d}")
         res[kind] = {"raw_bytes_per_launch": sum(vals) / len(vals), "scale": scale, "launches": len(vals),
                      "bytes_per_launch": scale * sum(vals) / len(vals)}
-    rec = {"kernel": args.kernel, "kernels_counted": names, "workload": args.config,
+    workload = args.config + ("event" if args.event_decode else "")
+    rec = {"kernel": args.kernel, "kernels_counted": names, "workload": workload,
            "bytes_per_launch": int(res["fetch"]["bytes_per_launch"] + res["write"]["bytes_per_launch"]),
            "fetch": res["fetch"], "write": res["write"], "source_sha": source_sha(), "command": args.command}
-    path = os.path.join(ROOT, "profiles", f"{args.kernel}_{args.config}_traffic.json")
+    path = os.path.join(ROOT, "profiles", f"{args.kernel}_{workload}_traffic.json")
     with open(path, "w") as f:
         json.dump(rec, f, indent=1)
     print(json.dumps(rec))
@@ -299,6 +313,9 @@ def main():
     ap.add_argument("--no-sort", action="store_true", help="ablation: signals and operators in build order")
     ap.add_argument("--no-simplify", action="store_true", help="ablation: skip simplification")
     ap.add_argument("--no-fuse", action="store_true", help="ablation: no fused ensemble operators")
+    ap.add_argument("--event-decode", action="store_true",
+                    help="event-driven decoding (reads the decoders of spiking neurons only); not the "
+                         "method's dense work, so the roofline uses measured counter bytes")
     ap.add_argument("--counters-run", action="store_true",
                     help="one untimed run for a rocprofv3 --pmc pass (with --copy-probe); prints no JSON")
     args = ap.parse_args()
@@ -322,7 +339,8 @@ def main():
     t_build = time.perf_counter()
     plan_opts = dict(planner=M.PLANNER_TREE if args.planner == "tree" else M.PLANNER_GREEDY,
                      planner_depth=args.planner_depth, merge=not args.no_merge, sort=not args.no_sort,
-                     simplify=not args.no_simplify, fuse=not args.no_fuse)
+                     simplify=not args.no_simplify, fuse=not args.no_fuse,
+                     decode="event" if args.event_decode else "dense")
     sim = M.Simulator(model, minibatch=w.minibatch, driver=driver, unroll=20,
                       probe_capacity_steps=w.n_steps, gemm_dtype=args.gemm_dtype, **plan_opts)
     t_build = time.perf_counter() - t_build
@@ -363,7 +381,8 @@ def main():
     bf16 = args.gemm_dtype == "bf16"
     default_plan = (args.planner, args.planner_depth, args.no_merge, args.no_sort, args.no_simplify,
                     args.no_fuse) == ("tree", 3, False, False, False, False)
-    roofline = measure_roofline(M, model, w, sim, info, feeds, bf16, plan_opts, default_plan)
+    roofline = measure_roofline(M, model, w, sim, info, feeds, bf16, plan_opts, default_plan,
+                                event=args.event_decode)
     out = {
         "metric": "neuron-timesteps/sec (x minibatch) on 1 MI355X",
         "value": value, "unit": "neuron-timesteps/s", "n_gpus": 1, "steps": args.steps,
@@ -377,7 +396,8 @@ def main():
                    "gemm_dtype": args.gemm_dtype,
                    "plan": {"planner": args.planner, "depth": args.planner_depth, "merge": not args.no_merge,
                             "sort": not args.no_sort, "simplify": not args.no_simplify,
-                            "fuse": not args.no_fuse}},
+                            "fuse": not args.no_fuse},
+                   "decode": "event" if args.event_decode else "dense"},
         "roofline": roofline,
     }
     if not args.no_cpu_baseline:

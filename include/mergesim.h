@@ -168,6 +168,20 @@ ms_status ms_model_add_probe(ms_model* model, const ms_probe_desc* desc, int32_t
 #define MS_GEMM_F32 0
 #define MS_GEMM_BF16 1
 
+/* Decoding of spiking ensembles (the `decode` option).  MS_DECODE_DENSE, the
+ * method as the paper merges it, computes every decoded output as the full
+ * product of the decoders with the ensemble's output vector (Sec. 2, the
+ * decoder DotInc of each connection).  MS_DECODE_EVENT reads only the decoder
+ * columns of neurons that spiked in the step, from a neuron-major copy of the
+ * decoders made at creation (as much device memory again as the decoders):
+ * a neuron that does not spike contributes an exact zero, so the outputs are
+ * equal to the dense ones (up to the sign of a zero sum).  It applies to the
+ * small-minibatch fused-ensemble kernel of the time-major drivers (steps and
+ * graph, minibatch < 32) and to spiking ensembles; elsewhere decoding stays
+ * dense.  Other values are MS_E_INVALID. */
+#define MS_DECODE_DENSE 0
+#define MS_DECODE_EVENT 1
+
 typedef struct {
   double dt;                  /* seconds, default 0.001 */
   int32_t minibatch;          /* B >= 1, default 1 */
@@ -185,6 +199,7 @@ typedef struct {
   void* stream;               /* hipStream_t to run on, NULL = library-owned */
   int64_t probe_capacity_steps; /* initial probe/feed staging capacity */
   int32_t gemm_dtype;         /* MS_GEMM_F32 (default) or MS_GEMM_BF16 */
+  int32_t decode;             /* MS_DECODE_DENSE (default) or MS_DECODE_EVENT */
 } ms_sim_opts;
 
 /* Fill `opts` with the defaults listed above. */

@@ -6,8 +6,8 @@ Python binding: argument marshalling only.
 """
 from .mergesim import (Model, Plan, Simulator, MergesimError, load_library, model_from_spec,
                        DRIVER_AUTO, DRIVER_STEPS, DRIVER_GRAPH, DRIVER_PERSISTENT, DRIVER_WINDOW,
-                       GEMM_F32, GEMM_BF16, PLANNER_GREEDY, PLANNER_TREE)
+                       GEMM_F32, GEMM_BF16, PLANNER_GREEDY, PLANNER_TREE, DECODE_DENSE, DECODE_EVENT)
 
 __all__ = ["Model", "Plan", "Simulator", "MergesimError", "load_library", "model_from_spec",
            "DRIVER_AUTO", "DRIVER_STEPS", "DRIVER_GRAPH", "DRIVER_PERSISTENT", "DRIVER_WINDOW",
-           "GEMM_F32", "GEMM_BF16", "PLANNER_GREEDY", "PLANNER_TREE"]
+           "GEMM_F32", "GEMM_BF16", "PLANNER_GREEDY", "PLANNER_TREE", "DECODE_DENSE", "DECODE_EVENT"]

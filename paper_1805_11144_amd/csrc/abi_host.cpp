@@ -80,6 +80,7 @@ void ms_sim_opts_default(ms_sim_opts* o) {
   o->stream = nullptr;
   o->probe_capacity_steps = 1000;
   o->gemm_dtype = MS_GEMM_F32;
+  o->decode = MS_DECODE_DENSE;
 }
 
 ms_status ms_model_create(ms_model** out) {

@@ -178,6 +178,12 @@ struct EnsDesc {
   const float* bias;     // bias base (vector)
   const float* D[kMaxFns];  // decoder bases [rows][n]
   int32_t Dcols[kMaxFns];   // row stride of each decoder base
+  // event-driven decoding (spiking, or null): op k's decoders neuron-major,
+  // neuron r's decoded outputs at decT[k * dT_op + r * dT_row + q], rows padded
+  // with zeros to dT_row = dec_bucket(ndec) values
+  const float* decT;
+  int64_t dT_op;
+  int32_t dT_row;
 };
 
 constexpr float kLn2 = 0.6931471805599453f;
@@ -450,7 +456,7 @@ __global__ void k_lowpass(float* st, Strides S, int32_t B, int64_t rows, Opnd y,
 // Fused ensembles, small minibatch: one workgroup of 256 threads per (op,
 // batch column); threads over neurons.  Decoded partial sums are reduced
 // within each wavefront, then across the four wavefronts in LDS.
-template <int NDEC>
+template <int NDEC, bool EVD>
 __device__ __forceinline__ void ens_wg_t(float* st, const Strides& S, const EnsDesc& E, float dt,
                                          float (*red)[kMaxDec]) {
   const int op = blockIdx.x;
@@ -471,10 +477,14 @@ __device__ __forceinline__ void ens_wg_t(float* st, const Strides& S, const EnsD
   // with the transposed copy, encoder k of adjacent neurons is adjacent in memory
   gptr<float> encT = G(E.encT) + (int64_t)o.enc * d;
   const bool tr = E.encT != nullptr && d > 0 && d <= kMaxXReg;
+  // event-driven decoding (EVD, E.decT set) reads a neuron's decoders only
+  // when it spikes
+  constexpr bool evd = EVD;
+  gptr<float> dT = G(E.decT) + (int64_t)op * E.dT_op;
   for (int r = threadIdx.x; r < o.n; r += 256) {
     // every load of this neuron is issued before any arithmetic or store: the
     // encoders with the index clamped to d - 1 (the extra terms meet xr[k] = 0),
-    // the bias, the state and the decoder entries
+    // the bias, the state and (dense decoding) the decoder entries
     float ev[kMaxXReg], dv[NDEC > 0 ? NDEC : 1];
     if (tr) {
 #pragma unroll
@@ -483,11 +493,13 @@ __device__ __forceinline__ void ens_wg_t(float* st, const Strides& S, const EnsD
     const float bj = bias[r];
     float v = 0.0f, rf = 0.0f;
     if (E.ntype == 0) { v = st[at(S, o.V + r, b)]; rf = st[at(S, o.ref + r, b)]; }
+    if constexpr (!evd) {
 #pragma unroll
-    for (int q = 0; q < NDEC; ++q) {
-      const int qq = q < ndec ? q : ndec - 1;
-      gptr<float> row = qq < df0 ? D0 + (int64_t)qq * s0 : D1 + (int64_t)(qq - df0) * s1;
-      dv[q] = row[r];
+      for (int q = 0; q < NDEC; ++q) {
+        const int qq = q < ndec ? q : ndec - 1;
+        gptr<float> row = qq < df0 ? D0 + (int64_t)qq * s0 : D1 + (int64_t)(qq - df0) * s1;
+        dv[q] = row[r];
+      }
     }
     float j;
     if (tr) {
@@ -500,6 +512,25 @@ __device__ __forceinline__ void ens_wg_t(float* st, const Strides& S, const EnsD
     const float sp = neuron_update(E.ntype, j, v, rf, o.tau_rc, o.tau_ref, o.amp, o.full, dt, o.inv_tau);
     if (E.ntype == 0) { st[at(S, o.V + r, b)] = v; st[at(S, o.ref + r, b)] = rf; }
     if (o.s >= 0) st[at(S, o.s + r, b)] = sp;
+    if constexpr (evd) {   // a silent neuron adds exact zeros, as in the dense sum
+      if (sp != 0.0f) {
+        if constexpr (NDEC >= 4) {
+          typedef float f4v __attribute__((ext_vector_type(4)));
+#pragma unroll
+          for (int q4 = 0; q4 < NDEC / 4; ++q4) {
+            const f4v t = *(const __attribute__((address_space(1))) f4v*)(dT + (int64_t)r * NDEC + 4 * q4);
+#pragma unroll
+            for (int e = 0; e < 4; ++e) dv[4 * q4 + e] = t[e];
+          }
+        } else {
+#pragma unroll
+          for (int q = 0; q < NDEC; ++q) dv[q] = dT[(int64_t)r * NDEC + q];
+        }
+      } else {
+#pragma unroll
+        for (int q = 0; q < NDEC; ++q) dv[q] = 0.0f;
+      }
+    }
 #pragma unroll
     for (int q = 0; q < NDEC; ++q) acc[q] += dv[q] * sp;
   }
@@ -517,15 +548,16 @@ __device__ __forceinline__ void ens_wg_t(float* st, const Strides& S, const EnsD
   }
 }
 
+template <bool EVD>
 __global__ void __launch_bounds__(256) k_ens_wg(float* st, Strides S, EnsDesc E, float dt) {
   __shared__ float red[4][kMaxDec];
   switch (dec_bucket(E.ndec)) {
-    case 0: ens_wg_t<0>(st, S, E, dt, red); break;
-    case 1: ens_wg_t<1>(st, S, E, dt, red); break;
-    case 2: ens_wg_t<2>(st, S, E, dt, red); break;
-    case 4: ens_wg_t<4>(st, S, E, dt, red); break;
-    case 8: ens_wg_t<8>(st, S, E, dt, red); break;
-    default: ens_wg_t<16>(st, S, E, dt, red); break;
+    case 0: ens_wg_t<0, EVD>(st, S, E, dt, red); break;
+    case 1: ens_wg_t<1, EVD>(st, S, E, dt, red); break;
+    case 2: ens_wg_t<2, EVD>(st, S, E, dt, red); break;
+    case 4: ens_wg_t<4, EVD>(st, S, E, dt, red); break;
+    case 8: ens_wg_t<8, EVD>(st, S, E, dt, red); break;
+    default: ens_wg_t<16, EVD>(st, S, E, dt, red); break;
   }
 }
 

@@ -79,6 +79,7 @@ struct ms_sim {
   int32_t driver = MS_DRIVER_STEPS;
   int32_t unroll = 10;
   int32_t gemm_dtype = MS_GEMM_F32;
+  int32_t decode = MS_DECODE_DENSE;
   float dt = 0.001f;
   // device memory
   std::vector<float*> base_ptr;      // per base id
@@ -329,6 +330,31 @@ void build_launches(ms_sim* s, const std::vector<LGroup>& groups, std::vector<La
         s->extra_allocs.push_back(dt_);
         E.encT = dt_;
       }
+      if (s->decode == MS_DECODE_EVENT && g.ens_type == 0 && E.ndec > 0 && s->B < 32 &&
+          (s->driver == MS_DRIVER_STEPS || s->driver == MS_DRIVER_GRAPH)) {
+        // neuron-major decoders for event-driven decoding: op k's neuron r
+        // holds its decoded outputs (function 0's rows, then function 1's) in
+        // one row of dec_bucket(ndec) values, zero-padded
+        const int64_t row = dec_bucket(E.ndec);
+        int64_t nmax = 1;
+        for (int32_t n : g.ens_n) nmax = std::max<int64_t>(nmax, n);
+        std::vector<float> t((size_t)(g.ens_n.size() * nmax * row), 0.0f);
+        for (int f = 0, q0 = 0; f < E.nf; q0 += E.df[f], ++f) {
+          const std::vector<float>& hd = host_param_base(s, g.ens_Dbase[f]);
+          const int64_t cols = E.Dcols[f];
+          for (size_t k = 0; k < g.ens_n.size(); ++k)
+            for (int32_t q = 0; q < E.df[f]; ++q)
+              for (int64_t r = 0; r < g.ens_n[k]; ++r)
+                t[(size_t)(((int64_t)k * nmax + r) * row + q0 + q)] =
+                    hd[(size_t)(((int64_t)g.ens_D[f][k] + q) * cols + r)];
+        }
+        float* dd = dev_alloc<float>(t.size());
+        HIPCHECK(hipMemcpy(dd, t.data(), t.size() * 4, hipMemcpyHostToDevice));
+        s->extra_allocs.push_back(dd);
+        E.decT = dd;
+        E.dT_op = nmax * row;
+        E.dT_row = (int32_t)row;
+      }
       E.bias = s->base_ptr[g.ens_bias_base];
       E.ops = reinterpret_cast<const EnsOp*>(ipool + ens_off[gi]);
     }
@@ -539,7 +565,10 @@ void launch_group(ms_sim* s, const Launch& l, int32_t du) {
         hipLaunchKernelGGL(k_ens_tile, dim3((unsigned)l.rows, (unsigned)((B + 63) / 64)), dim3(256), 0, q, st, S,
                            B, l.ens, s->dt);
       } else {
-        hipLaunchKernelGGL(k_ens_wg, dim3((unsigned)l.rows, (unsigned)B), dim3(256), 0, q, st, S, l.ens, s->dt);
+        if (l.ens.decT)
+          hipLaunchKernelGGL(k_ens_wg<true>, dim3((unsigned)l.rows, (unsigned)B), dim3(256), 0, q, st, S, l.ens, s->dt);
+        else
+          hipLaunchKernelGGL(k_ens_wg<false>, dim3((unsigned)l.rows, (unsigned)B), dim3(256), 0, q, st, S, l.ens, s->dt);
       }
       break;
     default: fail(MS_E_INVALID, "unknown group type");
@@ -1073,6 +1102,7 @@ ms_status ms_sim_create(const ms_model* model, const ms_sim_opts* opts, ms_sim**
     if (o->unroll < 1) fail(MS_E_INVALID, "unroll must be >= 1");
     if (o->driver < MS_DRIVER_AUTO || o->driver > MS_DRIVER_WINDOW) fail(MS_E_INVALID, "unknown driver");
     if (o->gemm_dtype != MS_GEMM_F32 && o->gemm_dtype != MS_GEMM_BF16) fail(MS_E_INVALID, "unknown gemm_dtype");
+    if (o->decode != MS_DECODE_DENSE && o->decode != MS_DECODE_EVENT) fail(MS_E_INVALID, "unknown decode");
     int ndev = 0;
     HIPCHECK(hipGetDeviceCount(&ndev));
     if (o->device < 0 || o->device >= ndev) fail(MS_E_INVALID, "device ordinal out of range");
@@ -1083,6 +1113,7 @@ ms_status ms_sim_create(const ms_model* model, const ms_sim_opts* opts, ms_sim**
       s->unroll = o->unroll;
       s->dt = (float)o->dt;
       s->gemm_dtype = o->gemm_dtype;
+      s->decode = o->decode;
       s->plan = make_plan(model_of(model), o->dt, plan_opts_from(o));
       DeviceGuard dg(s->device);
       if (o->stream) {

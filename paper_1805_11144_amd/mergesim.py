@@ -19,6 +19,7 @@ FN_IDENTITY, FN_PRODUCT = 0, 1
 PLANNER_GREEDY, PLANNER_TREE = 0, 1
 DRIVER_AUTO, DRIVER_STEPS, DRIVER_GRAPH, DRIVER_PERSISTENT, DRIVER_WINDOW = 0, 1, 2, 3, 4
 GEMM_F32, GEMM_BF16 = 0, 1
+DECODE_DENSE, DECODE_EVENT = 0, 1
 PARAM_GAIN, PARAM_BIAS, PARAM_DECODERS = 0, 1, 2
 STATE_VOLTAGE, STATE_REFRACTORY, STATE_SYNAPSE, STATE_PROBE_SYNAPSE = 0, 1, 2, 3
 (OP_FEED, OP_RESET, OP_COPY, OP_COPY_INC, OP_ELEMENTWISE_INC, OP_DOT_INC, OP_LIF, OP_LIF_RATE, OP_LOWPASS,
@@ -55,7 +56,7 @@ class SimOpts(C.Structure):
                 ("planner_depth", _i32), ("merge", _i32), ("sort", _i32), ("simplify", _i32),
                 ("fuse", _i32),
                 ("driver", _i32), ("device", _i32), ("stream", C.c_void_p),
-                ("probe_capacity_steps", _i64), ("gemm_dtype", _i32)]
+                ("probe_capacity_steps", _i64), ("gemm_dtype", _i32), ("decode", _i32)]
 
 
 class Feed(C.Structure):
@@ -239,7 +240,7 @@ def model_from_spec(spec) -> Model:
 
 def make_opts(dt=0.001, minibatch=1, unroll=10, planner=PLANNER_TREE, planner_depth=3, merge=True,
               sort=True, simplify=True, fuse=True, driver=DRIVER_AUTO, device=0, stream=None,
-              probe_capacity_steps=1000, gemm_dtype=None) -> SimOpts:
+              probe_capacity_steps=1000, gemm_dtype=None, decode=None) -> SimOpts:
     o = SimOpts()
     load_library().ms_sim_opts_default(C.byref(o))
     o.dt, o.minibatch, o.unroll = float(dt), int(minibatch), int(unroll)
@@ -251,6 +252,8 @@ def make_opts(dt=0.001, minibatch=1, unroll=10, planner=PLANNER_TREE, planner_de
     o.probe_capacity_steps = int(probe_capacity_steps)
     if gemm_dtype is not None:
         o.gemm_dtype = {"f32": GEMM_F32, "bf16": GEMM_BF16}.get(gemm_dtype, gemm_dtype)
+    if decode is not None:
+        o.decode = {"dense": DECODE_DENSE, "event": DECODE_EVENT}.get(decode, decode)
     return o
 
 

@@ -103,3 +103,11 @@ def test_sim_creation_without_gpu_fails_cleanly():
     w = make_workload("c1", n_steps=5)
     code, msg = _status_of(lambda: M.Simulator(M.model_from_spec(w.spec)))
     assert code in (-1, -4)
+
+
+def test_sim_opts_defaults_and_decode_field():
+    """ms_sim_opts_default fills the decode option (dense) at the offset the
+    binding's structure declares; the event value marshals through."""
+    o = MS.make_opts()
+    assert o.decode == M.DECODE_DENSE and o.gemm_dtype == M.GEMM_F32
+    assert MS.make_opts(decode="event").decode == M.DECODE_EVENT
