@@ -4,7 +4,8 @@ operators; Sec. 3.2: decoders come from a least-squares optimisation over the
 ensemble's evaluation points).
 
 Readings where the paper is silent:
-  * gain/bias from (max rate, intercept) by the LIF rate curve (neurons.gain_bias)
+  * gain/bias from (max rate, intercept) by the LIF rate curve (neurons.gain_bias),
+    or by the rectified-linear line for ReLU neurons (neurons.relu_gain_bias)
   * scaled encoders E_hat = diag(gain) E (radius 1)
   * activities A[m, i] = amplitude * r(gain_i e_i . x_m + bias_i) on the
     ensemble's eval points
@@ -23,7 +24,7 @@ from typing import Dict, Optional, Tuple
 import numpy as np
 import scipy.linalg
 
-from .neurons import gain_bias, lif_rate
+from .neurons import gain_bias, rate_output, relu_gain_bias
 
 
 def function_targets(function: str, X: np.ndarray) -> np.ndarray:
@@ -51,13 +52,15 @@ def apply_function(function: str, x: np.ndarray) -> np.ndarray:
 def ensemble_gain_bias(ens):
     if ens.gains is not None:
         return np.asarray(ens.gains, np.float64), np.asarray(ens.biases, np.float64)
+    if ens.neuron_type == "relu":
+        return relu_gain_bias(ens.max_rates, ens.intercepts)
     return gain_bias(ens.max_rates, ens.intercepts, ens.tau_rc, ens.tau_ref)
 
 
 def ensemble_activities(ens, gain, bias, X):
     """Rate-mode outputs [M, n] of the ensemble's neurons at represented values X."""
     J = (X @ np.asarray(ens.encoders, np.float64).T) * gain[None, :] + bias[None, :]
-    return ens.amplitude * lif_rate(J, ens.tau_rc, ens.tau_ref)
+    return rate_output(ens.neuron_type, J, ens.tau_rc, ens.tau_ref, ens.amplitude)
 
 
 def ridge_decoders(A: np.ndarray, Y: np.ndarray, reg: float) -> np.ndarray:

@@ -7,6 +7,12 @@ Pins (tests/test_oracle_neurons.py):
   lif_rate        closed form 1/(tau_ref - tau_rc ln(1 - 1/J)); printed values
   lif_step        exact spike steps ceil(t_j / dt) for constant J; long-run rate
   gain_bias       r(g + b) == max_rate and g * intercept + b == 1
+  relu_rate       max(J, 0) by definition; relu_gain_bias: g + b == max_rate and
+                  g * intercept + b == 0 (tests/test_oracle_neurons.py)
+
+A rectified-linear rate neuron (the ReLU type of the memory model the paper
+lists among its benchmarks) is also defined here: its output is amplitude *
+max(J, 0), with no state.
 """
 import numpy as np
 
@@ -68,6 +74,29 @@ def lif_step(J, V, ref, dt, tau_rc, tau_ref, amplitude):
     ref = np.where(spiked, tau_ref - since, ref)
     s = np.where(spiked, amplitude / dt, 0.0)
     return s, V, ref
+
+
+def relu_rate(J):
+    """Rectified-linear rate: J above 0, else 0."""
+    J = np.asarray(J, dtype=np.float64)
+    return np.maximum(J, 0.0)
+
+
+def relu_gain_bias(max_rates, intercepts):
+    """Gain and bias of a rectified-linear neuron: J(x) = gain * x + bias is 0 at
+    x = intercept (where it starts to respond) and max_rate at x = 1."""
+    max_rates = np.asarray(max_rates, dtype=np.float64)
+    intercepts = np.asarray(intercepts, dtype=np.float64)
+    gain = max_rates / (1.0 - intercepts)
+    bias = -gain * intercepts
+    return gain, bias
+
+
+def rate_output(neuron_type, J, tau_rc, tau_ref, amplitude):
+    """Output of a rate neuron: amplitude * r(J) with the LIF or the ReLU curve."""
+    if neuron_type == "relu":
+        return amplitude * relu_rate(J)
+    return amplitude * lif_rate(J, tau_rc, tau_ref)
 
 
 def lif_rate_output(J, tau_rc, tau_ref, amplitude):

@@ -43,7 +43,7 @@ from typing import Dict, List, Optional
 import numpy as np
 
 from .build import apply_function, build_params, function_size
-from .neurons import lif_rate_output, lif_step
+from .neurons import lif_step, rate_output
 
 
 class CycleError(ValueError):
@@ -237,7 +237,7 @@ class OracleSim:
                     s, self.V[i], self.ref[i] = lif_step(J, self.V[i], self.ref[i], self.dt,
                                                          ens.tau_rc, ens.tau_ref, ens.amplitude)
                 else:
-                    s = lif_rate_output(J, ens.tau_rc, ens.tau_ref, ens.amplitude)
+                    s = rate_output(self.neuron_type[i], J, ens.tau_rc, ens.tau_ref, ens.amplitude)
                 out[obj] = s
         # filter updates run after every reader of the old filter state
         for ci, c in enumerate(spec.connections):

@@ -95,3 +95,21 @@ def test_gain_bias_invariants():
     np.testing.assert_allclose(g * c + b, 1.0, rtol=0, atol=1e-12 * np.abs(g).max())
     np.testing.assert_allclose(lif_rate(g + b, TAU_RC, TAU_REF), m, rtol=1e-12)
     assert np.all(g > 0)
+
+
+def test_relu_rate_and_gain_bias():
+    """Rectified-linear neuron: r(J) = max(J, 0); gain and bias put J = 0 at the
+    intercept and J = max_rate at x = 1.  Hand values: max_rate 200 Hz at
+    intercept 0.5 gives gain 400 and bias -200."""
+    from oracle.neurons import rate_output, relu_gain_bias, relu_rate
+    assert list(relu_rate(np.array([-1.0, 0.0, 2.5]))) == [0.0, 0.0, 2.5]
+    g, b = relu_gain_bias(np.array([200.0]), np.array([0.5]))
+    assert g[0] == 400.0 and b[0] == -200.0
+    rng = np.random.default_rng(7)
+    m, c = rng.uniform(200, 400, 1000), rng.uniform(-1, 1, 1000)
+    g, b = relu_gain_bias(m, c)
+    np.testing.assert_allclose(relu_rate(g + b), m, rtol=1e-12)          # x = 1 fires at max_rate
+    np.testing.assert_allclose(g * c + b, 0.0, atol=1e-9 * np.abs(g).max())  # x = intercept: J = 0
+    assert np.all(relu_rate(g * (c - 1e-3) + b) == 0.0)                   # silent below the intercept
+    np.testing.assert_array_equal(rate_output("relu", np.array([3.0, -2.0]), 0.02, 0.002, 0.5),
+                                  [1.5, 0.0])

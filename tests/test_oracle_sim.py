@@ -267,3 +267,40 @@ def test_rate_backward_check_accepts_oracle_and_rejects_offsets():
     off = e.amplitude * lif_rate(J + 1e-3 * S, e.tau_rc, e.tau_ref)
     nf, bad = lif_rate_inverse_ok(off, exp, J, S, e.amplitude, e.tau_rc, e.tau_ref)
     assert bad > 0
+
+
+def test_relu_ensemble_matches_closed_form():
+    """ReLU neurons fed by a constant node through a lowpass synapse: the
+    ensemble reads the filter state left by the previous step (R4), so at step
+    k (1-based) x_k = 0.7 (1 - a^(k-1)), and each output is
+    amplitude * max(gain * encoder * x_k + bias, 0)."""
+    gains, biases, enc = np.array([2.0, 1.5, 3.0]), np.array([0.1, -0.8, -1.5]), np.array([1.0, -1.0, 1.0])
+    m = ModelSpec(dt=DT)
+    m.add_node(Node(size=1, value=np.array([0.7])))
+    m.add_ensemble(Ensemble(n_neurons=3, dims=1, encoders=enc[:, None], eval_points=np.zeros((1, 1)),
+                            gains=gains, biases=biases, neuron_type="relu", amplitude=0.5))
+    m.connect(Connection(pre=("node", 0), post=("ens", 0), transform=1.0, synapse=0.01))
+    m.probe(Probe(target=("neurons", 0)))
+    sim = OracleSim(m)
+    sim.run_steps(50)
+    a = math.exp(-DT / 0.01)
+    k = np.arange(1, 51)[:, None]
+    x = 0.7 * (1.0 - a ** (k - 1))
+    expect = 0.5 * np.maximum(gains * enc * x + biases, 0.0)
+    np.testing.assert_allclose(sim.data(0)[0], expect, rtol=1e-13, atol=1e-15)
+    assert (expect[:, 2] == 0).sum() > 0 and (expect[:, 2] > 0).sum() > 0   # neuron 2 crosses 0
+
+
+def test_relu_decoders_solve_the_normal_equations():
+    from oracle.build import ensemble_activities, ensemble_gain_bias, ridge_decoders
+    rng = np.random.default_rng(11)
+    e = Ensemble(n_neurons=60, dims=2, encoders=rng.normal(size=(60, 2)), eval_points=rng.uniform(-1, 1, (300, 2)),
+                 max_rates=rng.uniform(200, 400, 60), intercepts=rng.uniform(-1, 1, 60), neuron_type="relu")
+    e.encoders /= np.linalg.norm(e.encoders, axis=1, keepdims=True)
+    g, b = ensemble_gain_bias(e)
+    A = ensemble_activities(e, g, b, e.eval_points)
+    np.testing.assert_allclose(A, np.maximum((e.eval_points @ e.encoders.T) * g + b, 0.0), rtol=1e-13, atol=1e-9)
+    D = ridge_decoders(A, e.eval_points, 0.1)
+    lam = 300 * (0.1 * A.max()) ** 2
+    resid = (A.T @ A + lam * np.eye(60)) @ D - A.T @ e.eval_points
+    assert np.abs(resid).max() <= 1e-8 * np.abs(A.T @ e.eval_points).max()
