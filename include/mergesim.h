@@ -61,6 +61,9 @@ typedef struct ms_sim ms_sim;
 
 #define MS_NEURON_LIF 0       /* spiking LIF, exact integration */
 #define MS_NEURON_LIF_RATE 1  /* LIF rate curve amplitude * r(J) */
+#define MS_NEURON_RELU 2      /* rectified linear: amplitude * max(J, 0); gain and bias
+                                 from max_rates/intercepts put J = 0 at the intercept
+                                 and J = max_rate at x = 1 (no state) */
 
 #define MS_FN_IDENTITY 0  /* decode x (d outputs) */
 #define MS_FN_PRODUCT 1   /* decode x0 * x1 (1 output, needs dims >= 2) */

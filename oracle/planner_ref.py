@@ -69,6 +69,7 @@ class Op:
     bias: Optional[Ref] = None                 # fused ensemble: bias parameter
     decs: list = field(default_factory=list)   # fused ensemble: [(D param, d output)]
     lif: bool = True
+    kind: int = 0                              # neuron type: 0 LIF, 1 LIF rate, 2 ReLU
 
 
 @dataclass
@@ -179,7 +180,8 @@ def build_ir(spec) -> IR:
         if lif:
             op(LIF, f"e{e}.neurons", src=whole(J), dst=whole(S), V=whole(V), ref=whole(R))
         else:
-            op(LIF_RATE, f"e{e}.neurons", src=whole(J), dst=whole(S))
+            op(LIF_RATE, f"e{e}.neurons", src=whole(J), dst=whole(S),
+               kind=2 if E.neuron_type == "relu" else 1)
         for fn, d, D in decs:
             op(RESET, f"e{e}.reset{_fn_tag(fn)}", dst=whole(d))
             op(DOT_INC, f"e{e}.dec{_fn_tag(fn)}", dst=whole(d), a=whole(D), src=whole(S))
@@ -291,7 +293,7 @@ def fuse_ensembles(ir: IR) -> None:
                     total += ir.ops[by_name[p + ".dec" + tag]].dst.length
             dec_ops.sort(key=lambda kk: kk[1])
             fuse_dec = total <= MAX_FUSED_DECODED
-            f = Op(ENS, p + ".ens", V=neu.V, ref=neu.ref, lif=neu.type == LIF,
+            f = Op(ENS, p + ".ens", V=neu.V, ref=neu.ref, lif=neu.type == LIF, kind=neu.kind,
                    bias=Ref(sig_by_name[p + ".bias"], 0, neu.src.length))
             if ke is not None:
                 f.src, f.a = ir.ops[ke].src, ir.ops[ke].a
@@ -396,10 +398,10 @@ def merge_key(ir: IR, o: Op):
     if t == LIF:
         return (t, b(o.src), b(o.dst), b(o.V), b(o.ref))
     if t == LIF_RATE:
-        return (t, b(o.src), b(o.dst))
+        return (t, b(o.src), b(o.dst), o.kind)
     if t == ENS:
         bb = lambda r: -1 if r is None else ir.sigs[r.sig].base
-        key = (t, 0 if o.lif else 1, bb(o.src), bb(o.a), 0 if o.src is None else o.src.length,
+        key = (t, o.kind, bb(o.src), bb(o.a), 0 if o.src is None else o.src.length,
                bb(o.bias), bb(o.dst), bb(o.V), bb(o.ref))
         for D, d in o.decs:
             key += (bb(D), d.length, bb(d))
@@ -695,13 +697,15 @@ def lower_group(ir: IR, offset: Dict[int, int], g: List[int]) -> dict:
                 if t == LIF:
                     V.append(row(o.V, i)); R.append(row(o.ref, i))
         out.update(rows=len(J), dst=_operand(base(o0.dst), S), src=_operand(base(o0.src), J))
+        if t == LIF_RATE and o0.kind == 2:
+            out["neuron"] = 2
         if t == LIF:
             out.update(V=_operand(base(o0.V), V), ref=_operand(base(o0.ref), R))
     elif t == ENS:
         ops = [ir.ops[oi] for oi in g]
         rr = lambda r: -1 if r is None else row(r, 0)
         bb = lambda r: -1 if r is None else ir.sigs[r.sig].base
-        out.update(rows=len(g), d=0 if o0.src is None else o0.src.length, neuron=0 if o0.lif else 1,
+        out.update(rows=len(g), d=0 if o0.src is None else o0.src.length, neuron=o0.kind,
                    enc_base=bb(o0.a), bias_base=bb(o0.bias), D_base=[bb(D) for D, _ in o0.decs],
                    n=[o.bias.length for o in ops], x_row=[rr(o.src) for o in ops],
                    enc_row=[-1 if o.a is None else offset[o.a.sig] for o in ops],

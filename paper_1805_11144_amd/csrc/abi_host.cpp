@@ -111,7 +111,8 @@ ms_status ms_model_add_ensemble(ms_model* m, const ms_ensemble_desc* d, int32_t*
   return guarded([&] {
     need(m && d && id_out, "NULL argument");
     need(d->n_neurons > 0 && d->dims > 0, "ensemble needs n_neurons > 0 and dims > 0");
-    need(d->neuron_type == MS_NEURON_LIF || d->neuron_type == MS_NEURON_LIF_RATE, "unknown neuron type");
+    need(d->neuron_type == MS_NEURON_LIF || d->neuron_type == MS_NEURON_LIF_RATE || d->neuron_type == MS_NEURON_RELU,
+         "unknown neuron type");
     need(d->tau_rc > 0 && d->tau_ref >= 0, "tau_rc must be > 0 and tau_ref >= 0");
     need(d->encoders != nullptr, "encoders are required");
     const size_t n = (size_t)d->n_neurons;

@@ -24,6 +24,12 @@ double lif_rate(double J, double tau_rc, double tau_ref) {
   return 1.0 / (tau_ref + tau_rc * std::log1p(1.0 / (J - 1.0)));
 }
 
+// rate curve of the ensemble's neuron type (spiking LIF decodes from its rates)
+double rate_of(const EnsembleDesc& e, double J) {
+  if (e.neuron_type == MS_NEURON_RELU) return J > 0.0 ? J : 0.0;
+  return lif_rate(J, e.tau_rc, e.tau_ref);
+}
+
 // G = A^T A (lower triangle filled, then mirrored), A is [M][n] row-major.
 void gram(const std::vector<double>& A, int M, int n, std::vector<double>& G) {
   // transpose so every entry is a contiguous dot product of length M
@@ -91,7 +97,7 @@ std::vector<double> solve_decoders(const EnsembleDesc& e, const std::vector<doub
       const double* en = &e.encoders[(size_t)i * d];
       double dot = 0.0;
       for (int k = 0; k < d; ++k) dot += en[k] * x[k];
-      double v = e.amplitude * lif_rate(gain[i] * dot + bias[i], e.tau_rc, e.tau_ref);
+      double v = e.amplitude * rate_of(e, gain[i] * dot + bias[i]);
       A[(size_t)m * n + i] = v;
       amax = std::max(amax, v);
     }
@@ -155,7 +161,13 @@ Built build_params(const Model& m) {
     }
     b.gain[i].resize(e.n);
     b.bias[i].resize(e.n);
-    for (int k = 0; k < e.n; ++k) {
+    for (int k = 0; k < e.n && e.neuron_type == MS_NEURON_RELU; ++k) {
+      // rectified linear: J = 0 at the intercept, J = max_rate at x = 1
+      const double g = e.max_rates[k] / (1.0 - e.intercepts[k]);
+      b.gain[i][k] = g;
+      b.bias[i][k] = -g * e.intercepts[k];
+    }
+    for (int k = 0; k < e.n && e.neuron_type != MS_NEURON_RELU; ++k) {
       const double jmax = 1.0 / -std::expm1((e.tau_ref - 1.0 / e.max_rates[k]) / e.tau_rc);
       const double g = (jmax - 1.0) / (1.0 - e.intercepts[k]);
       b.gain[i][k] = g;

@@ -127,7 +127,7 @@ struct Op {
   std::vector<double> reset_value;  // RESET: [dst.len] (empty = zeros)
   SRef bias;                        // ENS: bias parameter [n]
   std::vector<std::pair<SRef, SRef>> decs;  // ENS: (decoder param [d_f x n], output d_f)
-  int32_t ntype = 0;                // ENS: MS_NEURON_*
+  int32_t ntype = 0;                // ENS, LIF_RATE: MS_NEURON_*
   int32_t n = 0;                    // ENS: neurons
   double tau_rc = 0, tau_ref = 0, amp = 0;  // LIF params
   double coef_a = 0, coef_b = 0;            // LOWPASS y = coef_a y + coef_b v

@@ -237,6 +237,7 @@ IR build_ir(const Model& m, const Built& bp, double dt) {
     }
     {
       Op& o = B.add(lif ? OP_LIF : OP_LIF_RATE, p + ".neurons");
+      o.ntype = E.neuron_type;
       o.src = B.whole(eJ[e]);
       o.dst = B.whole(eS[e]);
       if (lif) { o.V = B.whole(V); o.ref = B.whole(R); }
@@ -420,7 +421,7 @@ void fuse_ensembles(IR& ir) {
     Op f;
     f.type = OP_ENS;
     f.name = p + ".ens";
-    f.ntype = nop.type == OP_LIF ? MS_NEURON_LIF : MS_NEURON_LIF_RATE;
+    f.ntype = nop.type == OP_LIF ? MS_NEURON_LIF : nop.ntype;
     f.n = nop.src.len;
     f.tau_rc = nop.tau_rc; f.tau_ref = nop.tau_ref; f.amp = nop.amp;
     f.V = nop.V; f.ref = nop.ref;

@@ -39,6 +39,7 @@ struct NeuronParams {
   float full;                                     // expm1(-dt / tau_rc), uniform
   const float *tau_rc_r, *tau_ref_r, *amp_r;      // per-row values or null
   const float* full_r;                            // per-row expm1(-dt / tau_rc) or null
+  int32_t relu;                                   // rate neurons: 1 = rectified linear
 };
 
 struct FilterParams {
@@ -83,7 +84,8 @@ __device__ __forceinline__ void lif_rate_item(float* st, const Strides& S, int64
   const float amp = np.amp_r ? G(np.amp_r)[r] : np.amp;
   const float j = st[at(S, rowof(J, r), b)];
   float out = 0.0f;
-  if (j > 1.0f) out = amp / (tau_ref + tau_rc * log1pf(1.0f / (j - 1.0f)));
+  if (np.relu) out = amp * fmaxf(j, 0.0f);
+  else if (j > 1.0f) out = amp / (tau_ref + tau_rc * log1pf(1.0f / (j - 1.0f)));
   st[at(S, rowof(s, r), b)] = out;
 }
 
@@ -211,6 +213,7 @@ __device__ __forceinline__ float expm1_small(float x) {
 __device__ __forceinline__ float neuron_update(int ntype, float j, float& v, float& rf, float tau_rc,
                                                float tau_ref, float amp, float full, float dt,
                                                float inv_tau) {
+  if (ntype == 2) return amp * fmaxf(j, 0.0f);   // rectified linear
   if (ntype != 0) {
     return j > 1.0f ? amp / (tau_ref + tau_rc * log1pf(1.0f / (j - 1.0f))) : 0.0f;
   }

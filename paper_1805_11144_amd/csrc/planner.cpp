@@ -98,7 +98,7 @@ std::vector<int32_t> merge_key(const IR& ir, const Op& o) {
     case OP_ELEM_INC: return {OP_ELEM_INC, b(o.dst), b(o.a), b(o.src)};
     case OP_DOT_INC: return {OP_DOT_INC, b(o.dst), b(o.a), b(o.src), o.a.len, o.src.len};
     case OP_LIF: return {OP_LIF, b(o.src), b(o.dst), b(o.V), b(o.ref)};
-    case OP_LIF_RATE: return {OP_LIF_RATE, b(o.src), b(o.dst)};
+    case OP_LIF_RATE: return {OP_LIF_RATE, b(o.src), b(o.dst), o.ntype};   // rate curve: LIF or ReLU
     case OP_LOWPASS: return {OP_LOWPASS, b(o.dst), b(o.src)};
     case OP_ENS: {
       std::vector<int32_t> k = {OP_ENS, o.ntype, b(o.src), b(o.a), o.src.len, b(o.bias),
@@ -592,6 +592,7 @@ LGroup lower_group_at(const IR& ir, const std::vector<int64_t>& sig_offset, cons
           J.push_back(row(o.src, i));
           s.push_back(row(o.dst, i));
           if (g.type == OP_LIF) { V.push_back(row(o.V, i)); R.push_back(row(o.ref, i)); }
+          if (g.type == OP_LIF_RATE) g.ens_type = o.ntype;   // same in every op of the group (key)
           trc.push_back(o.tau_rc); tref.push_back(o.tau_ref); amp.push_back(o.amp);
         }
       }

@@ -298,6 +298,7 @@ void build_launches(ms_sim* s, const std::vector<LGroup>& groups, std::vector<La
       l.np.full = (float)std::expm1(-p.dt / (double)g.tau_rc[0]);
       l.np.tau_rc_r = fp(o.trc); l.np.tau_ref_r = fp(o.tref); l.np.amp_r = fp(o.amp);
       l.np.full_r = fp(o.full);
+      l.np.relu = g.type == OP_LIF_RATE && g.ens_type == MS_NEURON_RELU ? 1 : 0;
     }
     if (g.type == OP_LOWPASS) {
       l.fp.a = g.ca[0]; l.fp.b = g.cb[0];

@@ -14,7 +14,7 @@ LIB_PATH = os.path.join(_HERE, "libmergesim.so")
 
 MS_OK = 0
 REF_NODE, REF_ENS, REF_NEURONS = 0, 1, 2
-NEURON_LIF, NEURON_LIF_RATE = 0, 1
+NEURON_LIF, NEURON_LIF_RATE, NEURON_RELU = 0, 1, 2
 FN_IDENTITY, FN_PRODUCT = 0, 1
 PLANNER_GREEDY, PLANNER_TREE = 0, 1
 DRIVER_AUTO, DRIVER_STEPS, DRIVER_GRAPH, DRIVER_PERSISTENT, DRIVER_WINDOW = 0, 1, 2, 3, 4
@@ -171,7 +171,7 @@ class Model:
             return _dptr(a)
         d = EnsembleDesc()
         d.n_neurons, d.dims = int(ens.n_neurons), int(ens.dims)
-        d.neuron_type = NEURON_LIF if ens.neuron_type == "lif" else NEURON_LIF_RATE
+        d.neuron_type = {"lif": NEURON_LIF, "lif_rate": NEURON_LIF_RATE, "relu": NEURON_RELU}[ens.neuron_type]
         d.tau_rc, d.tau_ref, d.amplitude = float(ens.tau_rc), float(ens.tau_ref), float(ens.amplitude)
         d.encoders = arr(ens.encoders)
         if ens.gains is not None:

@@ -198,7 +198,7 @@ class PlanExecutor:
             tref = _vec(g["tau_ref"], n)[:, None]
             amp = _vec(g["amp"], n)[:, None]
             if t == "SimLIFRate":
-                out = _rate(J, trc, tref, amp)
+                out = amp * np.maximum(J, 0.0) if g.get("neuron") == 2 else _rate(J, trc, tref, amp)
             else:
                 vr, rr = _rows(g["V"], n), _rows(g["ref"], n)
                 out, pa[vr], pa[rr] = _lif(J, pa[vr].copy(), pa[rr].copy(), self.dt, trc, tref, amp)
@@ -219,6 +219,8 @@ class PlanExecutor:
                     s_, pa[v0:v0 + nn], pa[r0:r0 + nn] = _lif(J, pa[v0:v0 + nn].copy(),
                                                               pa[r0:r0 + nn].copy(), self.dt,
                                                               trc_all[k], tref_all[k], amp_all[k])
+                elif g["neuron"] == 2:
+                    s_ = amp_all[k] * np.maximum(J, 0.0)
                 else:
                     s_ = _rate(J, trc_all[k], tref_all[k], amp_all[k])
                 if g["s_row"][k] >= 0:

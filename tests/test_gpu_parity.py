@@ -56,6 +56,22 @@ def test_rate_mode_parity(name, driver, fuse):
         assert r <= 1e-5, (name, driver, pi, r)
 
 
+@pytest.mark.parametrize("fuse", [True, False])
+@pytest.mark.parametrize("driver", list(DRIVERS))
+@pytest.mark.parametrize("name", list(SMALL))
+def test_relu_parity(name, driver, fuse):
+    """Rectified-linear rate neurons (fused ensembles and the unfused rate
+    operator) on every driver: the rate-mode bound, 1e-5 of each probe's peak."""
+    skip_unsupported(name, driver)
+    w = make_workload(name, neuron_type="relu", **SMALL[name])
+    got = run_gpu(w, driver=DRIVERS[driver], unroll=7, fuse=fuse)
+    exp = run_oracle(w)
+    for pi, (g, e) in enumerate(zip(got, exp)):
+        r = rel_err(g, e)
+        print(f"{name} {driver} probe {pi}: rel {r:.2e}")
+        assert r <= 1e-5, (name, driver, pi, r)
+
+
 @pytest.mark.parametrize("driver", list(DRIVERS))
 @pytest.mark.parametrize("name", list(SMALL))
 def test_spiking_mode_parity(name, driver):

@@ -58,3 +58,16 @@ def test_plans_identical(name, opt):
     assert got["probe_rows"] == exp["probe_rows"]
     assert got["probe_offsets"] == exp["probe_offsets"]
     assert got["feed_rows"] == exp["feed_rows"]
+
+
+@pytest.mark.parametrize("opt", ["tree3", "nofuse", "nomerge"])
+@pytest.mark.parametrize("name", ["c2", "c4", "c5"])
+def test_relu_plans_identical(name, opt):
+    """ReLU ensembles: rate operators keyed and exported with their neuron type."""
+    w = make_workload(name, neuron_type="relu", **CASES[name])
+    lib_opts, ref_opts = OPTS[opt]
+    got = _strip(M.Plan(M.model_from_spec(w.spec), **lib_opts).json())
+    exp = P.make_plan(w.spec, **ref_opts)
+    assert got == {**exp, "groups": exp["groups"]}
+    kinds = [g.get("neuron") for g in got["groups"] if g["type"] in ("SimLIFRate", "Ensemble")]
+    assert kinds and all(k == 2 for k in kinds)

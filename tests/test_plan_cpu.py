@@ -19,9 +19,10 @@ SMALL = {
 }
 
 
+@pytest.mark.parametrize("neuron_type", ["lif", "relu"])
 @pytest.mark.parametrize("name", ["c1", "c2", "c4", "c5"])
-def test_build_params_match_oracle(name):
-    w = make_workload(name, **SMALL[name])
+def test_build_params_match_oracle(name, neuron_type):
+    w = make_workload(name, neuron_type=neuron_type, **SMALL[name])
     plan = M.Plan(M.model_from_spec(w.spec), minibatch=w.minibatch)
     P = build_params(w.spec)
     for e in range(len(w.spec.ensembles)):
@@ -34,7 +35,7 @@ def test_build_params_match_oracle(name):
 
 
 @pytest.mark.parametrize("name", list(SMALL))
-@pytest.mark.parametrize("neuron_type", ["lif_rate", "lif"])
+@pytest.mark.parametrize("neuron_type", ["lif_rate", "lif", "relu"])
 @pytest.mark.parametrize("opts", [dict(), dict(planner=M.PLANNER_GREEDY), dict(sort=False),
                                   dict(simplify=False), dict(merge=False), dict(fuse=False)])
 def test_plan_execution_matches_oracle(name, neuron_type, opts):

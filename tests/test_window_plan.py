@@ -49,7 +49,7 @@ def test_chain_levels_follow_the_chain():
 
 
 @pytest.mark.parametrize("name", ["c2", "c3", "c4"])
-@pytest.mark.parametrize("neuron_type", ["lif_rate", "lif"])
+@pytest.mark.parametrize("neuron_type", ["lif_rate", "lif", "relu"])
 @pytest.mark.parametrize("window", [1, 7, 1000])
 @pytest.mark.parametrize("opts", [dict(), dict(fuse=False), dict(merge=False)])
 def test_window_execution_matches_oracle(name, neuron_type, window, opts):
