@@ -10,8 +10,8 @@ Pins (tests/test_oracle_neurons.py):
   relu_rate       max(J, 0) by definition; relu_gain_bias: g + b == max_rate and
                   g * intercept + b == 0 (tests/test_oracle_neurons.py)
 
-A rectified-linear rate neuron (the ReLU type of the memory model the paper
-lists among its benchmarks) is also defined here: its output is amplitude *
+A rectified-linear rate neuron (the neuron type of the memory storage and
+retrieval example, Sec. 5.2) is also defined here: its output is amplitude *
 max(J, 0), with no state.
 """
 import numpy as np
