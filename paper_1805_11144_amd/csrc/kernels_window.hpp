@@ -920,6 +920,19 @@ __device__ __forceinline__ w_f4 w_src4(const WView& w, const float* param, int b
   return w4(w, row, (int64_t)blk * w.B + c);
 }
 
+// k_w_feed, four entries per thread (B a multiple of 4: the staged rows are
+// 16-byte aligned as well)
+__global__ void k_w_feed4(WView w, int64_t rows, Opnd dst, const int32_t* feed_row, const float* stage,
+                          int32_t feed_rows, int64_t t0) {
+  W_ITEM4(rows);
+  const uint32_t t = _c / (uint32_t)w.B, b = _c - t * (uint32_t)w.B;
+  w4(w, rowof(dst, _r), w.B + _c) = *(const w_f4*)(stage + ((t0 + t) * feed_rows + G(feed_row)[_r]) * w.B + b);
+}
+
+// k_w_elem_inc, four entries per thread (each entry the same sum, in the same order)
+__global__ void k_w_elem_inc4(WView w, int64_t rows, Opnd dst, const float* a_param, Opnd a, int a_bcast, int ablk,
+                              const float* x_param, Opnd x, int x_bcast, int xblk, const int32_t* ptr);
+
 __global__ void k_w_copy_inc4(WView w, int64_t rows, Opnd dst, const float* param, Opnd src, int bcast, int sblk,
                               const int32_t* ptr) {
   W_ITEM4(rows);
@@ -929,6 +942,20 @@ __global__ void k_w_copy_inc4(WView w, int64_t rows, Opnd dst, const float* para
     for (int32_t e = G(ptr)[_r]; e < G(ptr)[_r + 1]; ++e) acc += w_src4(w, param, bcast, rowof(src, e), sblk, _c);
   } else {
     acc += w_src4(w, param, bcast, rowof(src, _r), sblk, _c);
+  }
+  d = acc;
+}
+
+__global__ void k_w_elem_inc4(WView w, int64_t rows, Opnd dst, const float* a_param, Opnd a, int a_bcast, int ablk,
+                              const float* x_param, Opnd x, int x_bcast, int xblk, const int32_t* ptr) {
+  W_ITEM4(rows);
+  w_f4& d = w4(w, rowof(dst, _r), w.B + _c);
+  w_f4 acc = d;
+  if (ptr) {
+    for (int32_t e = G(ptr)[_r]; e < G(ptr)[_r + 1]; ++e)
+      acc += w_src4(w, a_param, a_bcast, rowof(a, e), ablk, _c) * w_src4(w, x_param, x_bcast, rowof(x, e), xblk, _c);
+  } else {
+    acc += w_src4(w, a_param, a_bcast, rowof(a, _r), ablk, _c) * w_src4(w, x_param, x_bcast, rowof(x, _r), xblk, _c);
   }
   d = acc;
 }

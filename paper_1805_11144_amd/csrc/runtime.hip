@@ -931,8 +931,12 @@ void launch_phase(ms_sim* s, const Launch& l, int32_t T, int64_t t0, hipStream_t
   const double tb = (double)T * s->B;
   switch (l.type) {
     case OP_FEED:
-      hipLaunchKernelGGL(k_w_feed, dim3(grid_items(l.rows * tb)), dim3(kBlock), 0, q, w, l.rows, l.dst, l.feed_rows,
-                         (const float*)s->feed_stage, s->plan->ir.feed_rows, t0);
+      if (s->B % 4 == 0)
+        hipLaunchKernelGGL(k_w_feed4, dim3(grid_items(l.rows * tb / 4)), dim3(kBlock), 0, q, w, l.rows, l.dst,
+                           l.feed_rows, (const float*)s->feed_stage, s->plan->ir.feed_rows, t0);
+      else
+        hipLaunchKernelGGL(k_w_feed, dim3(grid_items(l.rows * tb)), dim3(kBlock), 0, q, w, l.rows, l.dst,
+                           l.feed_rows, (const float*)s->feed_stage, s->plan->ir.feed_rows, t0);
       break;
     case OP_RESET:
       if (s->B % 4 == 0)   // 16-byte aligned rows of every block: four entries per thread
@@ -954,9 +958,14 @@ void launch_phase(ms_sim* s, const Launch& l, int32_t T, int64_t t0, hipStream_t
                            l.src_base, l.src, (int)l.src_bcast, l.src_blk, l.ptr);
       break;
     case OP_ELEM_INC:
-      hipLaunchKernelGGL(k_w_elem_inc, dim3(grid_items(l.rows * tb)), dim3(kBlock), 0, q, w, l.rows, l.dst,
-                         l.a_base, l.a, (int)l.a_bcast, l.a_blk, l.src_base, l.src, (int)l.src_bcast, l.src_blk,
-                         l.ptr);
+      if (s->B % 4 == 0)
+        hipLaunchKernelGGL(k_w_elem_inc4, dim3(grid_items(l.rows * tb / 4)), dim3(kBlock), 0, q, w, l.rows, l.dst,
+                           l.a_base, l.a, (int)l.a_bcast, l.a_blk, l.src_base, l.src, (int)l.src_bcast, l.src_blk,
+                           l.ptr);
+      else
+        hipLaunchKernelGGL(k_w_elem_inc, dim3(grid_items(l.rows * tb)), dim3(kBlock), 0, q, w, l.rows, l.dst,
+                           l.a_base, l.a, (int)l.a_bcast, l.a_blk, l.src_base, l.src, (int)l.src_bcast, l.src_blk,
+                           l.ptr);
       break;
     case OP_DOT_INC:
       if (l.w16 || (l.K > 128 && l.M >= 64 && l.K % 4 == 0 && s->B % 4 == 0)) {
