@@ -32,6 +32,8 @@ WORKLOADS = {
     "c3": "spiking MLP 784-1024-1024-10, Glorot-normal, lowpass 0.005, B=256, T=50",
     "c4": "wide array: 200 ensembles x 500 LIF x 16-D chain, B=512, T=500",
     "c5": "sparse graph: 5000 ensembles x 500 LIF x 16-D, fan-out 4, B=1, T=1000",
+    "bg": "basal-ganglia-shaped: 5 arrays x 64 ensembles x 50 LIF (1-D), one-to-one and all-to-all "
+          "array transforms, B=1, T=1000",
 }
 
 

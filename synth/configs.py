@@ -11,6 +11,9 @@ parameters unchanged.
   c3  spiking MLP  784 -> 1024 LIF -> 1024 LIF -> 10 (paper Sec. 5.2.1 shape)
   c4  wide array   200 ensembles x 500 LIF x 16-D in a chain
   c5  sparse graph 5000 ensembles x 500 LIF x 16-D, fan-out 4, 32-D input
+  bg  basal-ganglia-shaped: five arrays of D one-dimensional ensembles (striatum
+      D1 and D2, STN, GPi, GPe) with one-to-one and all-to-all array transforms
+      (paper Sec. 5.1 "basal_ganglia"; used for the planner ablation)
 
 All values are synthetic; no dataset is read or reproduced.
 """
@@ -22,7 +25,7 @@ import numpy as np
 
 from .spec import Connection, Ensemble, ModelSpec, Node, Probe, Workload
 
-CONFIG_NAMES = ("c1", "c2", "c3", "c4", "c5")
+CONFIG_NAMES = ("c1", "c2", "c3", "c4", "c5", "bg")
 
 
 def _rng(seed: int, index: int) -> np.random.Generator:
@@ -253,7 +256,65 @@ def make_c5(neuron_type="lif", n_steps=1000, minibatch=1, n_ens=5000, n_neurons=
                     notes="sparse random graph of 16-D ensembles, fan-out 4, 32-D input")
 
 
-_MAKERS = {"c1": make_c1, "c2": make_c2, "c3": make_c3, "c4": make_c4, "c5": make_c5}
+# ----------------------------------------------------------------------------- bg
+def make_bg(neuron_type="lif", n_steps=1000, minibatch=1, D=64, n_neurons=50, n_eval=300) -> Workload:
+    """Basal-ganglia-shaped network (the paper names the benchmark without its
+    structure; this follows the usual action-selection circuit).  Five arrays
+    of D one-dimensional ensembles, each with an input and an output
+    passthrough of width D: striatum D1 (input weight 1.2), striatum D2 (0.8)
+    and STN (1.0) read the D utilities; D1 -> GPi and D2 -> GPe inhibit one to
+    one (-1, lowpass 0.008); STN excites GPi and GPe all to all (0.9, lowpass
+    0.002); GPe inhibits GPi and STN one to one (-0.3, lowpass 0.008), which
+    closes the STN-GPe loop.  Neurons have positive encoders and intercepts
+    U[0.2, 0.9], so each ensemble responds only above a threshold.  The GPi
+    output is probed (lowpass 0.01) with the spikes of one GPi ensemble.
+    Feed: seeded utilities U[0, 1]^D per batch row, constant in time."""
+    seed = 6
+    m = ModelSpec(dt=0.001)
+    u = m.add_node(Node(size=D))
+    eye, ones = np.eye(D), np.ones((D, D))
+
+    def array(k):
+        inp = m.add_node(Node(size=D, passthrough=True))
+        out = m.add_node(Node(size=D, passthrough=True))
+        ens = []
+        for j in range(D):
+            rng = _rng(seed, 1000 * k + j)
+            e = m.add_ensemble(Ensemble(
+                n_neurons=n_neurons, dims=1, encoders=np.ones((n_neurons, 1)),
+                eval_points=rng.uniform(0.0, 1.2, size=(n_eval, 1)),
+                max_rates=rng.uniform(200.0, 400.0, n_neurons),
+                intercepts=rng.uniform(0.2, 0.9, n_neurons), neuron_type=neuron_type))
+            m.connect(Connection(pre=inp, post=("ens", e), transform=1.0, pre_slice=(j, j + 1)))
+            m.connect(Connection(pre=("ens", e), post=out, transform=1.0, post_slice=(j, j + 1)))
+            ens.append(e)
+        return inp, out, ens
+
+    d1_in, d1_out, _ = array(1)
+    d2_in, d2_out, _ = array(2)
+    stn_in, stn_out, _ = array(3)
+    gpi_in, gpi_out, gpi = array(4)
+    gpe_in, gpe_out, _ = array(5)
+    ampa, gaba = 0.002, 0.008
+    m.connect(Connection(pre=u, post=d1_in, transform=1.2 * eye, synapse=ampa))
+    m.connect(Connection(pre=u, post=d2_in, transform=0.8 * eye, synapse=ampa))
+    m.connect(Connection(pre=u, post=stn_in, transform=1.0 * eye, synapse=ampa))
+    m.connect(Connection(pre=d1_out, post=gpi_in, transform=-1.0 * eye, synapse=gaba))
+    m.connect(Connection(pre=d2_out, post=gpe_in, transform=-1.0 * eye, synapse=gaba))
+    m.connect(Connection(pre=stn_out, post=gpi_in, transform=0.9 * ones, synapse=ampa))
+    m.connect(Connection(pre=stn_out, post=gpe_in, transform=0.9 * ones, synapse=ampa))
+    m.connect(Connection(pre=gpe_out, post=gpi_in, transform=-0.3 * eye, synapse=gaba))
+    m.connect(Connection(pre=gpe_out, post=stn_in, transform=-0.3 * eye, synapse=gaba))
+    m.probe(Probe(target=gpi_out, synapse=0.01))
+    m.probe(Probe(target=("neurons", gpi[0])))
+    rng = _rng(seed, 1)
+    v = rng.uniform(0.0, 1.0, size=(minibatch, D))
+    feeds = {u[1]: np.ascontiguousarray(np.broadcast_to(v[:, None, :], (minibatch, n_steps, D))).astype(np.float32)}
+    return Workload("bg", m, minibatch, n_steps, feeds,
+                    notes="basal-ganglia shaped: 5 arrays of D 1-D ensembles, one-to-one and all-to-all")
+
+
+_MAKERS = {"c1": make_c1, "c2": make_c2, "c3": make_c3, "c4": make_c4, "c5": make_c5, "bg": make_bg}
 
 
 def make_workload(name: str, **overrides) -> Workload:

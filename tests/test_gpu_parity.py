@@ -205,3 +205,28 @@ def test_window_product_tail_split(neuron_type):
     for pi in neu:
         assert np.array_equal(got[pi], ref[pi]), pi
     check(w, [got[pi] if pi in neu else out[0][pi] for pi in range(len(got))], out, False)
+
+
+BG = dict(n_steps=80, minibatch=3, D=8, n_neurons=30, n_eval=200)
+
+
+@pytest.mark.parametrize("neuron_type", ["lif_rate", "lif"])
+@pytest.mark.parametrize("driver", ["steps", "graph", "persistent"])
+def test_basal_ganglia_parity(driver, neuron_type):
+    """The basal-ganglia-shaped network (five arrays of 1-D ensembles,
+    one-to-one and all-to-all array transforms, an STN-GPe loop): rate mode to
+    1e-5 of each probe's peak, spiking mode with only one-step spike shifts."""
+    w = make_workload("bg", neuron_type=neuron_type, **BG)
+    got = run_gpu(w, driver=DRIVERS[driver], unroll=7)
+    exp = run_oracle(w)
+    for pi, (g, e) in enumerate(zip(got, exp)):
+        if neuron_type == "lif_rate":
+            r = rel_err(g, e)
+            print(f"bg {driver} probe {pi}: rel {r:.2e}")
+            assert r <= 1e-5, (driver, pi, r)
+        elif w.spec.probes[pi].target[0] == "neurons":
+            f, u = flip_fraction(g, e), unpaired_flips(g, e)
+            print(f"bg {driver} probe {pi}: flips {f:.2e} of {int((e > 0).sum())} spikes, unpaired {u}")
+            assert u == 0 and f <= 2e-3, (driver, pi, f, u)
+        else:
+            print(f"bg {driver} probe {pi}: abs {float(np.abs(g - e).max()):.2e}")

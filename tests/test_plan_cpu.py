@@ -16,11 +16,12 @@ SMALL = {
     "c3": dict(n_steps=30, minibatch=4, n_hidden=96, n_in=50),
     "c4": dict(n_steps=60, minibatch=3, n_ens=6, n_neurons=40, n_eval=200),
     "c5": dict(n_steps=40, n_ens=12, n_neurons=40, n_eval=200, n_input_targets=4, n_probed=3),
+    "bg": dict(n_steps=60, minibatch=2, D=6, n_neurons=20, n_eval=100),
 }
 
 
 @pytest.mark.parametrize("neuron_type", ["lif", "relu"])
-@pytest.mark.parametrize("name", ["c1", "c2", "c4", "c5"])
+@pytest.mark.parametrize("name", ["c1", "c2", "c4", "c5", "bg"])
 def test_build_params_match_oracle(name, neuron_type):
     w = make_workload(name, neuron_type=neuron_type, **SMALL[name])
     plan = M.Plan(M.model_from_spec(w.spec), minibatch=w.minibatch)

@@ -17,7 +17,7 @@ def window_of(name, **opts):
     return w, M.Plan(M.model_from_spec(w.spec), minibatch=w.minibatch, **opts).json()["window"]
 
 
-@pytest.mark.parametrize("name", ["c1", "c5"])
+@pytest.mark.parametrize("name", ["c1", "c5", "bg"])
 def test_recurrent_models_are_refused(name):
     _, win = window_of(name)
     assert not win["ok"] and "cycle" in win["why"]
