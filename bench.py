@@ -308,6 +308,8 @@ def main():
     ap.add_argument("--timesteps", type=int, default=0,
                     help="override the workload's timesteps (counter passes: per-launch traffic of a "
                          "time-major kernel does not depend on the run length)")
+    ap.add_argument("--unroll", type=int, default=20,
+                    help="steps per hipGraph launch (the paper's unroll_simulation)")
     ap.add_argument("--planner", default="tree", choices=["tree", "greedy"],
                     help="operator-merging planner (ablation; default: tree search, depth 3)")
     ap.add_argument("--planner-depth", type=int, default=3)
@@ -343,7 +345,7 @@ def main():
                      planner_depth=args.planner_depth, merge=not args.no_merge, sort=not args.no_sort,
                      simplify=not args.no_simplify, fuse=not args.no_fuse,
                      decode="event" if args.event_decode else "dense")
-    sim = M.Simulator(model, minibatch=w.minibatch, driver=driver, unroll=20,
+    sim = M.Simulator(model, minibatch=w.minibatch, driver=driver, unroll=args.unroll,
                       probe_capacity_steps=w.n_steps, gemm_dtype=args.gemm_dtype, **plan_opts)
     t_build = time.perf_counter() - t_build
     feeds = {i: torch.from_numpy(f).to(dev) for i, f in w.feeds.items()}
@@ -395,7 +397,7 @@ def main():
                    "driver": {1: "steps", 2: "graph", 3: "persistent", 4: "window"}.get(info["driver"]),
                    "launches_per_window" if info["driver"] == M.DRIVER_WINDOW else "groups_per_step":
                        info["groups_per_step"], "build_s": round(t_build, 2),
-                   "gemm_dtype": args.gemm_dtype,
+                   "gemm_dtype": args.gemm_dtype, "unroll": args.unroll,
                    "plan": {"planner": args.planner, "depth": args.planner_depth, "merge": not args.no_merge,
                             "sort": not args.no_sort, "simplify": not args.no_simplify,
                             "fuse": not args.no_fuse},
