@@ -788,8 +788,8 @@ void ens_shape(ms_sim* s, Launch& l, const LGroup& g) {
   // batch columns per workgroup: fill up to 256 threads (4 wavefronts) with
   // whole columns; an ensemble of more neurons takes one column and up to 512
   // threads.  Small workgroups let a CU interleave more of them around each
-  // one's barriers (C2's 100-neuron ensembles: 2 columns per workgroup ran
-  // 1.45 ms against 1.76 ms with 5)
+  // one's barriers (128 product ensembles of 100 neurons, minibatch 64, 1000
+  // steps: 2 columns per workgroup ran 1.47 ms against 1.76 ms with 5)
   l.cpw = (int32_t)std::max<int64_t>(1, std::min<int64_t>(s->B, 256 / nmax));
   l.nthr = (int32_t)std::min<int64_t>(512, ((int64_t)nmax * l.cpw + 63) / 64 * 64);
   l.npt = (int32_t)(((int64_t)nmax * l.cpw + l.nthr - 1) / l.nthr);
