@@ -5,9 +5,11 @@ n_steps timesteps for all B batch rows (every merged operator of the hot path:
 feeds, encoders, LIF, decoders, transforms, lowpass synapses, copies/scatters,
 probes).  Inputs are resident in HBM (torch CUDA tensors) before timing.
 
-Metric: neuron-timesteps/s = N_neurons * T * B / wall time per run.
-Default workload: the circular-convolution-shaped net (128 product ensembles of
-100 LIF neurons, 2-D, D = 64, B = 64, T = 1000).
+Metric: neuron-timesteps/s = N_neurons * T * B / wall time per run (the mean
+over the timed runs, with a 95% confidence interval as in the paper's speed
+measurements, Sec. 5.1).
+Default workload: the wide ensemble array (200 ensembles x 500 LIF x 16-D in a
+chain, B = 512, T = 500), the largest of the five workloads.
 
 Prints one JSON line.  --gpus > 1 is not supported (single-GPU build).
 """
@@ -24,6 +26,9 @@ sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0
 FP32_VALU_PEAK_TFLOPS = 78.6   # 256 CU x 4 SIMD x 16 lanes x 2 flop x 2.4 GHz, no packed FP32
+# VALU issue peak in wavefront instructions per second: a full-rate wave64
+# instruction occupies a 16-lane SIMD for 4 cycles; 256 CU x 4 SIMD x 2.4 GHz / 4
+VALU_ISSUE_PEAK = 256 * 4 * 2.4e9 / 4
 
 WORKLOADS = {
     "c1": "integrator: 1 ensemble x 100 LIF, 1-D, recurrent lowpass 0.1, B=1, T=1000",
@@ -82,7 +87,8 @@ def gemm_flops_per_step(w):
     return f
 
 
-LIF_FLOPS = 21    # exact-integration LIF step, operations per neuron-step
+LIF_FLOPS = 21    # exact-integration LIF step: clamp 3, factor 2, voltage 3, refractory 2, threshold 1,
+                  # overshoot 3, crossing time 4, resets 3 operations per neuron-step
 RATE_FLOPS = 7    # rate LIF
 FP32_MFMA_PEAK_TFLOPS = 157.3
 BF16_MFMA_PEAK_TFLOPS = 2500.0   # dense
@@ -114,30 +120,72 @@ def ensemble_work_per_step(w):
     return flops, byts
 
 
+def ensemble_gemm_flops_per_step(w):
+    """Matrix-product flops of the fused ensemble operators in one timestep:
+    per neuron and batch row 2 d for the encoders (ensembles with a
+    represented input) and 2 per decoded output for the decoders -- the
+    products that run on the matrix cores."""
+    spec, B = w.spec, w.minibatch
+    ndec = {}
+    fed = set()
+    for c in spec.connections:
+        if c.pre[0] == "ens" and c.decoders is None:
+            e = spec.ensembles[c.pre[1]]
+            ndec.setdefault(c.pre[1], {})[c.function] = 1 if c.function == "product" else e.dims
+        if c.post[0] == "ens":
+            fed.add(c.post[1])
+    for p in spec.probes:
+        if p.target[0] == "ens":
+            ndec.setdefault(p.target[1], {})["identity"] = spec.ensembles[p.target[1]].dims
+    f = 0
+    for i, e in enumerate(spec.ensembles):
+        nd = sum(ndec.get(i, {}).values())
+        f += 2 * e.n_neurons * B * ((e.dims if i in fed else 0) + nd)
+    return f
+
+
 def dot_flops_per_step(plan_json, B):
     """GEMM flops of the merged DotInc groups (2 M K per op and batch row)."""
     return sum(2 * g["M"] * g["K"] * len(g["w_row"]) * B for g in plan_json["groups"] if g["type"] == "DotInc")
 
 
-def cpu_baseline(w, budget_s=15.0):
-    """Time the float64 oracle on a bounded sample of the same workload."""
+def _oracle_leg(w, budget_s):
+    """Oracle timesteps run within budget_s (after building it), and the time."""
     from oracle.sim import OracleSim
-    try:
-        import threadpoolctl
-        cores = max(i.get("num_threads", 1) for i in threadpoolctl.threadpool_info()) or 1
-    except Exception:
-        cores = os.cpu_count() or 1
     sim = OracleSim(w.spec, minibatch=w.minibatch, param_dtype=np.float32)
     t0 = time.perf_counter()
     k = 0
     while k < w.n_steps and time.perf_counter() - t0 < budget_s:
         sim.run_steps(1, {i: f[:, k:k + 1] for i, f in w.feeds.items()})
         k += 1
-    dt = time.perf_counter() - t0
-    value = w.n_neurons * k * w.minibatch / dt
-    return {"value": value, "unit": "neuron-timesteps/s", "cores": int(cores), "kind": "oracle",
+    return k, time.perf_counter() - t0
+
+
+def cpu_baseline(w, budget_s=12.0):
+    """Time the float64 oracle on a bounded sample of the same workload: the
+    first timesteps that fit in budget_s, all batch rows, extrapolated per
+    timestep; once with the BLAS threads the host offers, once with one."""
+    import threadpoolctl
+    cores = max([i.get("num_threads", 1) for i in threadpoolctl.threadpool_info()] or [1])
+    k, dt = _oracle_leg(w, budget_s)
+    with threadpoolctl.threadpool_limits(limits=1):
+        k1, dt1 = _oracle_leg(w, budget_s)
+    per = w.n_neurons * w.minibatch
+    return {"value": per * k / dt, "unit": "neuron-timesteps/s", "cores": int(cores), "kind": "oracle",
             "sample": f"first {k} of {w.n_steps} timesteps, all {w.minibatch} batch rows, "
-                      f"float64 numpy, {dt:.1f} s"}
+                      f"float64 numpy, {dt:.1f} s, {cores} BLAS threads",
+            "single_thread": {"value": per * k1 / dt1, "cores": 1,
+                              "sample": f"first {k1} of {w.n_steps} timesteps, {dt1:.1f} s, 1 thread"}}
+
+
+def mean_ci95(xs):
+    """Mean and half-width of the 95% confidence interval (Student t)."""
+    xs = np.asarray(xs, np.float64)
+    if xs.size < 2:
+        return float(xs.mean()), None
+    from scipy import stats
+    h = stats.t.ppf(0.975, xs.size - 1) * xs.std(ddof=1) / np.sqrt(xs.size)
+    return float(xs.mean()), float(h)
 
 
 def measure_roofline(M, model, w, sim, info, feeds, bf16=False, plan_opts=None, default_plan=True, event=False):
@@ -159,7 +207,7 @@ def measure_roofline(M, model, w, sim, info, feeds, bf16=False, plan_opts=None, 
     tsim.set_timing(True)
     tsim.reset()
     tsim.run_steps(T, feeds)
-    times = {t: tsim.kernel_time(t) for t in range(10)}
+    times = {t: tsim.kernel_time(t) for t in range(11)}
     tsim.set_timing(False)
     if tsim is not sim:
         tsim.close()
@@ -170,8 +218,9 @@ def measure_roofline(M, model, w, sim, info, feeds, bf16=False, plan_opts=None, 
     window = drv == M.DRIVER_WINDOW
     if top == M.mergesim.OP_ENSEMBLE:
         flops, byts = ensemble_work_per_step(w)
-        if window:    # state stays on chip across the window: arithmetic bounds it
-            work, bound, peak, unit = flops * T, "alu", FP32_VALU_PEAK_TFLOPS, "TFLOP/s"
+        if window:    # state stays on chip across the window: the products bound it
+            work, bound, peak, unit = ensemble_gemm_flops_per_step(w) * T, "mfma", FP32_MFMA_PEAK_TFLOPS, \
+                "TFLOP/s"
             kernel = "k_w_ens"
         else:
             work, bound, peak, unit = byts * T, "hbm", HBM_PEAK_GBS, "GB/s"
@@ -199,12 +248,31 @@ def measure_roofline(M, model, w, sim, info, feeds, bf16=False, plan_opts=None, 
     scale = 1e12 if unit == "TFLOP/s" else 1e9
     ach = work / (ms * 1e-3) / scale
     op_names = {M.mergesim.OP_ENSEMBLE: "Ensemble", M.mergesim.OP_DOT_INC: "DotInc"}
-    return {"bound": bound, "achieved": round(ach, 3), "peak": peak, "unit": unit,
-            "frac": round(ach / peak, 4),
-            "traffic": stored_traffic(kernel, w.name + ("event" if event else "")) if default_plan else None,
-            "basis": basis,
-            "kernel": kernel, "op": op_names.get(top, str(top)), "launch_ms": round(ms / max(n, 1), 4),
-            "launches": n, "work_per_launch": int(work / max(n, 1))}
+    out = {"bound": bound, "achieved": round(ach, 3), "peak": peak, "unit": unit,
+           "frac": round(ach / peak, 4),
+           "traffic": stored_traffic(kernel, w.name + ("event" if event else "")) if default_plan else None,
+           "basis": basis,
+           "kernel": kernel, "op": op_names.get(top, str(top)), "launch_ms": round(ms / max(n, 1), 4),
+           "launches": n, "busy_ms": round(ms, 4), "work_per_launch": int(work / max(n, 1))}
+    sq = stored_sq(kernel, w.name) if default_plan else None
+    if sq is not None and "SQ_INSTS_VALU" in sq:
+        # VALU issue rate of the same kernel: wavefront instructions per launch
+        # from the committed counter pass, over the launch time measured here
+        rate = sq["SQ_INSTS_VALU"] / (ms * 1e-3 / max(n, 1))
+        out["valu"] = {"insts_per_launch": int(sq["SQ_INSTS_VALU"]), "issue_per_s": rate,
+                       "peak_per_s": VALU_ISSUE_PEAK, "frac": round(rate / VALU_ISSUE_PEAK, 4)}
+    return out
+
+
+def stored_sq(kernel, workload):
+    """Per-launch shader counters of a kernel and workload from the committed
+    counter summary, if it was taken from the current kernel sources."""
+    path = os.path.join(ROOT, "profiles", f"{kernel}_{workload}_sq.json")
+    if not os.path.exists(path):
+        return None
+    with open(path) as f:
+        rec = json.load(f)
+    return rec["per_launch"] if rec.get("source_sha") == source_sha() else None
 
 
 def stored_traffic(kernel, workload):
@@ -285,21 +353,49 @@ def summarize_traffic(args):
     print(json.dumps(rec))
 
 
+def summarize_sq(args):
+    """Per-launch shader (SQ_*) counters of a kernel from one or more rocprofv3
+    --pmc runs, averaged over its dispatches."""
+    names = [n for n in (args.match or args.kernel).split(",") if n]
+
+    def hit(k):
+        base = k.split("(")[0].split("<")[0].strip().split(" ")[-1]
+        return any(base == n for n in names)
+    per = {}
+    for d in args.summarize_sq:
+        for r in _counter_rows(d):
+            if hit(r["Kernel_Name"]):
+                per.setdefault(r["Counter_Name"], []).append(float(r["Counter_Value"]))
+    if not per:
+        raise SystemExit(f"kernels {names} not found")
+    rec = {"kernel": args.kernel, "kernels_counted": names, "workload": args.config,
+           "per_launch": {k: sum(v) / len(v) for k, v in sorted(per.items())},
+           "launches": {k: len(v) for k, v in sorted(per.items())},
+           "source_sha": source_sha(), "command": args.command}
+    path = os.path.join(ROOT, "profiles", f"{args.kernel}_{args.config}_sq.json")
+    with open(path, "w") as f:
+        json.dump(rec, f, indent=1)
+    print(json.dumps(rec))
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=5)
     ap.add_argument("--warmup", type=int, default=2)
-    ap.add_argument("--config", default="c2", choices=sorted(WORKLOADS))
+    ap.add_argument("--config", default="c4", choices=sorted(WORKLOADS))
     ap.add_argument("--driver", default="auto", choices=["auto", "steps", "graph", "persistent", "window"])
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--gemm-dtype", default="f32", choices=["f32", "bf16"],
                     help="input precision of the large window products (bf16: fp32 accumulation)")
-    ap.add_argument("--cpu-budget", type=float, default=15.0)
+    ap.add_argument("--cpu-budget", type=float, default=12.0,
+                    help="seconds of oracle stepping per leg of the CPU baseline (two legs)")
     ap.add_argument("--copy-probe", action="store_true",
                     help="copy 256 MiB device to device before timing (calibrates HBM counters)")
     ap.add_argument("--summarize-traffic", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
                     help="turn two rocprofv3 --pmc runs (FETCH_SIZE, WRITE_SIZE) into profiles/<kernel>_<config>_traffic.json")
+    ap.add_argument("--summarize-sq", nargs="+", metavar="PMC_DIR",
+                    help="turn rocprofv3 --pmc runs of SQ_* counters into profiles/<kernel>_<config>_sq.json")
     ap.add_argument("--kernel", default="k_w_ens", help="kernel name prefix for --summarize-traffic")
     ap.add_argument("--command", default="", help="profiling command recorded by --summarize-traffic")
     ap.add_argument("--match", default="",
@@ -325,6 +421,9 @@ def main():
     args = ap.parse_args()
     if args.summarize_traffic:
         summarize_traffic(args)
+        return
+    if args.summarize_sq:
+        summarize_sq(args)
         return
     if args.gpus != 1:
         print(json.dumps({"error": "this build runs on one GPU; --gpus must be 1"}))
@@ -369,11 +468,11 @@ def main():
         one_run()
     sim.sync()
     torch.cuda.synchronize()
-    kernel_ms = []
+    run_ms = []
     t0 = time.perf_counter()
     for _ in range(args.steps):
         one_run()
-        kernel_ms.append(sim.last_run_ms())
+        run_ms.append(sim.last_run_ms())   # HIP events around the run on its stream
     sim.sync()
     torch.cuda.synchronize()
     elapsed = time.perf_counter() - t0
@@ -381,6 +480,7 @@ def main():
     ms_per_step = 1000.0 * elapsed / args.steps
     neuron_steps = w.n_neurons * w.n_steps * w.minibatch
     value = neuron_steps / (elapsed / args.steps)
+    run_mean, run_ci = mean_ci95(run_ms)
     info = sim.info()
     bf16 = args.gemm_dtype == "bf16"
     default_plan = (args.planner, args.planner_depth, args.no_merge, args.no_sort, args.no_simplify,
@@ -402,6 +502,10 @@ def main():
                             "sort": not args.no_sort, "simplify": not args.no_simplify,
                             "fuse": not args.no_fuse},
                    "decode": "event" if args.event_decode else "dense"},
+        "runs": {"device_ms": [round(x, 4) for x in run_ms], "mean_ms": round(run_mean, 4),
+                 "ci95_ms": None if run_ci is None else round(run_ci, 4),
+                 "value_ci95": None if run_ci is None else
+                 [neuron_steps / ((run_mean + run_ci) * 1e-3), neuron_steps / ((run_mean - run_ci) * 1e-3)]},
         "roofline": roofline,
     }
     if not args.no_cpu_baseline:

@@ -185,6 +185,23 @@ ms_status ms_model_add_probe(ms_model* model, const ms_probe_desc* desc, int32_t
 #define MS_DECODE_DENSE 0
 #define MS_DECODE_EVENT 1
 
+/* Operator fusion (the `fuse` option).  The paper merges operators of one type
+ * (Sec. 4.2.1); these fuse operators of different types that always run
+ * together, with the same results:
+ *   MS_FUSE_ENSEMBLES: each ensemble's bias reset, encoder DotInc, neuron
+ *     update and decoder DotIncs become one operator (J is never stored);
+ *   MS_FUSE_SYNAPSES: in the time-major launch drivers (STEPS, GRAPH), the
+ *     tail of the connections of Fig. 2 -- transform DotInc, synaptic filter
+ *     and the Copy of the filtered value into the post input (with that
+ *     input's reset) -- becomes one launch at the filter's place at the end of
+ *     the step, which also sums the filtered values into the post inputs of
+ *     the next step (every run starts with a launch that sums them from the
+ *     filter state).  Applied to the connections whose signals allow it (each
+ *     filtered value copied once, post inputs touched by nothing else before
+ *     the copy, no probe on them); the others keep their separate operators. */
+#define MS_FUSE_ENSEMBLES 1
+#define MS_FUSE_SYNAPSES 2
+
 typedef struct {
   double dt;                  /* seconds, default 0.001 */
   int32_t minibatch;          /* B >= 1, default 1 */
@@ -194,9 +211,9 @@ typedef struct {
   int32_t merge;              /* 0: one operator per group (no merging) */
   int32_t sort;               /* 0: keep signals/operators in build order */
   int32_t simplify;           /* 0: skip simplification */
-  int32_t fuse;               /* 0: keep each ensemble's bias, encoder, neuron and
-                                 decoder operators separate (default 1: fuse them
-                                 into one operator per ensemble) */
+  int32_t fuse;               /* operator fusion, a set of MS_FUSE_* bits (default
+                                 both; 0 keeps every operator of the lowered model
+                                 separate) */
   int32_t driver;             /* MS_DRIVER_* */
   int32_t device;             /* HIP device ordinal */
   void* stream;               /* hipStream_t to run on, NULL = library-owned */
@@ -304,14 +321,18 @@ ms_status ms_sim_info(const ms_sim* sim, int32_t* driver_out, int32_t* groups_pe
 #define MS_OP_LIF_RATE 7
 #define MS_OP_LOWPASS 8
 #define MS_OP_ENSEMBLE 9  /* fused bias + encoders + neurons + decoders of an ensemble */
+#define MS_OP_SYNAPSE_SCATTER 10  /* fused transform + lowpass + copy into post inputs */
 
 /* Per-kernel timing for measurement.  With timing on (on != 0), every kernel
  * launch of a merged group is bracketed by HIP events recorded on the stream
- * the launch runs on; ms_sim_kernel_time then returns the summed duration in
- * ms and the number of launches of operator type `op_type` (MS_OP_*) during
- * the last ms_sim_run_steps call (it waits for that call to finish).  Only the
- * WINDOW and STEPS drivers time individual launches (MS_E_STATE otherwise).
- * Timing adds event records to every launch: leave it off for throughput runs. */
+ * the launch runs on; ms_sim_kernel_time then returns, for operator type
+ * `op_type` (MS_OP_*) during the last ms_sim_run_steps call (it waits for that
+ * call to finish), the busy time in ms -- the length of the union of those
+ * launches' intervals, so that launches running at once on different streams
+ * count once (it equals the summed durations when they do not overlap) -- and
+ * the number of launches.  Only the WINDOW and STEPS drivers time individual
+ * launches (MS_E_STATE otherwise).  Timing adds event records to every
+ * launch: leave it off for throughput runs. */
 ms_status ms_sim_set_timing(ms_sim* sim, int32_t on);
 ms_status ms_sim_kernel_time(ms_sim* sim, int32_t op_type, double* ms_out, int64_t* launches_out);
 

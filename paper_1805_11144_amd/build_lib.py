@@ -11,7 +11,7 @@ INCLUDE = os.path.join(ROOT, "include")
 OUT = os.path.join(HERE, "libmergesim.so")
 BUILD = os.path.join(HERE, "_build")
 
-HOST_SOURCES = ["build.cpp", "ir.cpp", "planner.cpp", "plan_json.cpp", "abi_host.cpp"]
+HOST_SOURCES = ["build.cpp", "ir.cpp", "planner.cpp", "launch_plan.cpp", "plan_json.cpp", "abi_host.cpp"]
 HIP_SOURCES = ["runtime.hip"]
 ROCM = os.environ.get("ROCM_PATH", "/opt/rocm")
 HIPCC = os.path.join(ROCM, "bin", "hipcc")

@@ -50,7 +50,10 @@ PlanOpts plan_opts_from(const ms_sim_opts* o) {
     p.merge = o->merge != 0;
     p.sort = o->sort != 0;
     p.simplify = o->simplify != 0;
-    p.fuse = o->fuse != 0;
+    p.fuse = (o->fuse & MS_FUSE_ENSEMBLES) != 0;
+    p.fuse_synapse = (o->fuse & MS_FUSE_SYNAPSES) != 0;
+    need(o->minibatch >= 1, "minibatch must be >= 1");
+    p.minibatch = o->minibatch;
     need(p.planner == MS_PLANNER_GREEDY || p.planner == MS_PLANNER_TREE, "unknown planner");
     need(p.depth >= 1 && p.depth <= 8, "planner depth must be in [1, 8]");
   }
@@ -74,7 +77,7 @@ void ms_sim_opts_default(ms_sim_opts* o) {
   o->merge = 1;
   o->sort = 1;
   o->simplify = 1;
-  o->fuse = 1;
+  o->fuse = MS_FUSE_ENSEMBLES | MS_FUSE_SYNAPSES;
   o->driver = MS_DRIVER_AUTO;
   o->device = 0;
   o->stream = nullptr;

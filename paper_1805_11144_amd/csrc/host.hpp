@@ -101,7 +101,9 @@ enum OpType : int32_t {
   OP_LIF_RATE = 7,
   OP_LOWPASS = 8,
   OP_ENS = 9,           // fused ensemble: J = bias + enc x; LIF; d_f = D_f s
-  OP_NTYPES = 10
+  OP_SYN_SCATTER = 10,  // fused connection tail (launch drivers only, never in a plan's
+                        // groups): transform, lowpass update, pull into the post inputs
+  OP_NTYPES = 11
 };
 
 // Fused decoders of one ensemble operator are limited to this many outputs in
@@ -165,6 +167,8 @@ struct PlanOpts {
   int32_t planner = MS_PLANNER_TREE;
   int32_t depth = 3;
   bool merge = true, sort = true, simplify = true, fuse = true;
+  bool fuse_synapse = true;    // time-major step program: fused synapse filter + scatter
+  int32_t minibatch = 1;       // B, which picks the product kernel of a launch
 };
 
 // One operand of a lowered group: rows in its base array, either a contiguous
@@ -204,7 +208,23 @@ struct LGroup {
   std::vector<std::vector<int32_t>> ens_D, ens_dd;   // [function][op]
   std::vector<int32_t> ens_Dbase;                    // per function
   int32_t ens_bias_base = -1;
+  // SYN_SCATTER: segments of at most kSynSeg consecutive rows, 4 ints each
+  // (first destination row or -1 for none, length, first connection, number of
+  // connections); connections 8 ints each (first filter row y, first value row v
+  // or -1 when the value is computed here or -2 for a probe copy of row y,
+  // first input row x, K, weight slot, first weight row, first probe row or -1,
+  // 1 when the inputs are rows of the feed staging buffer)
+  // plus 2 floats (a, b: y <- a y + b v); weight bases per slot; syn_update 0:
+  // pull only (no filter update, no probe); syn_probe 1: the group records
+  // every probe row of the step (the separate probe copy is dropped)
+  std::vector<int32_t> syn_seg, syn_conn, syn_wbase;
+  std::vector<float> syn_ab;
+  int32_t syn_update = 1;
+  int32_t syn_probe = 0;
 };
+
+constexpr int32_t kSynSeg = 16;   // rows per segment of a fused synapse group
+constexpr int32_t kSynSlots = 4;  // weight bases one fused synapse group may read
 
 struct Plan {
   PlanOpts opts;
@@ -252,6 +272,27 @@ struct WindowPlan {
 };
 
 WindowPlan make_window_plan(const Plan& p);
+
+// ------------------------------------------------- time-major step program
+// The groups one timestep of the launch drivers (plain launches, hipGraph)
+// runs, in order.  Consecutive independent fused-ensemble groups share a
+// launch.  With fuse_synapse, the connections' tail of Fig. 2 -- transform
+// (DotInc), synaptic filter (Lowpass, last in the step) and the copy of the
+// filtered value into the post input at the start of the next step (Reset +
+// CopyInc) -- becomes one SYN_SCATTER group at the filter's place: per post
+// input row it computes each incoming connection's value, updates the filter
+// and sums the filtered values, in the CopyInc's order.  The pull thereby
+// moves from the start of step k + 1 to the end of step k; nothing reads those
+// rows in between, and `prologue` (pull only) sets them at the start of every
+// run from the filter state.
+struct LaunchPlan {
+  std::vector<LGroup> step;
+  bool has_prologue = false;
+  LGroup prologue;
+  std::string why;   // why no fusion took place (empty when it did or was off)
+};
+LaunchPlan make_launch_plan(const Plan& p);
+std::vector<LGroup> merge_ens_groups(const std::vector<LGroup>& in);
 
 std::unique_ptr<Plan> make_plan(const Model& m, double dt, const PlanOpts& o);
 std::string plan_to_json(const Plan& p);

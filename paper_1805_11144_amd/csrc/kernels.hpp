@@ -627,6 +627,162 @@ __global__ void __launch_bounds__(256) k_ens_tile(float* st, Strides S, int32_t 
   }
 }
 
+// ------------------------------------------- fused synapse filter + scatter
+// The connection tail of Fig. 2 for a merged set of connections, at the end
+// of a timestep: for every post input row, each incoming connection's value
+// (a state row, or weight row . input rows computed here), its lowpass update
+// y <- a y + b v, and the sum of the updated y in the order of the CopyInc it
+// replaces, stored as the post input of the next step.  Segment: {post row or
+// -1, rows, first connection, connections}; a connection record is 8 words
+// {y, v, x, K | slot << 16 | staged << 20, w, probe row, a, b}: segment row i
+// reads or updates row y + i and takes its value from row v + i (v >= 0), or
+// computes it from weight row w + i of slot `slot` and the K inputs from row
+// x on (v == -1; rows of the state, or with `staged` rows of this step's feed
+// staging buffer), or only records row y + i (v == -2, a probe copy); with a
+// probe row p >= 0 the updated (or copied) value of row i also goes to probe
+// row p + i of this step.  update == 0 only sums (the pull at the start of a
+// run).
+//
+// One wavefront per (segment, batch column): lane 16 j + i takes row i and,
+// in chunk q, connections 8 q + j and 8 q + j + 4, whose loads are all issued
+// before their arithmetic; the next chunk's records are fetched meanwhile.
+// Row i's sum adds the chunk's values in connection order, read from lanes
+// i, i + 16, i + 32, i + 48 (first and second connection of each lane).
+struct SynConn {
+  int32_t y, v, x, kw, w, p;
+  float a, b;
+};
+struct SynW {
+  const float* w[4];
+};
+constexpr int kSynRows = 16, kSynLanes = 4, kSynPerLane = 2, kSynChunk = kSynLanes * kSynPerLane;
+
+// sum_k w[k] x[k] in k order (the DotInc kernel's order); x[k] at xp[k * xs]
+template <int KK>
+__device__ __forceinline__ float syn_dot_fixed(gptr<float> wr, const float* xp, int64_t xs) {
+  typedef float f4v __attribute__((ext_vector_type(4)));
+  const __attribute__((address_space(1))) f4v* w4 = (const __attribute__((address_space(1))) f4v*)wr;
+  f4v wv[KK / 4];
+  float xv[KK];
+#pragma unroll
+  for (int k4 = 0; k4 < KK / 4; ++k4) wv[k4] = w4[k4];
+#pragma unroll
+  for (int k = 0; k < KK; ++k) xv[k] = xp[k * xs];
+  float d = 0.0f;
+#pragma unroll
+  for (int k4 = 0; k4 < KK / 4; ++k4) {
+    d += wv[k4][0] * xv[4 * k4];
+    d += wv[k4][1] * xv[4 * k4 + 1];
+    d += wv[k4][2] * xv[4 * k4 + 2];
+    d += wv[k4][3] * xv[4 * k4 + 3];
+  }
+  return d;
+}
+
+__device__ __forceinline__ float syn_dot(gptr<float> wr, const float* xp, int64_t xs, int32_t K) {
+  if (K == 16) return syn_dot_fixed<16>(wr, xp, xs);
+  if (K == 32) return syn_dot_fixed<32>(wr, xp, xs);
+  float d = 0.0f;
+  if ((K & 3) == 0) {
+    typedef float f4v __attribute__((ext_vector_type(4)));
+    const __attribute__((address_space(1))) f4v* w4 = (const __attribute__((address_space(1))) f4v*)wr;
+    for (int32_t k4 = 0; k4 < K / 4; ++k4) {
+      const f4v wq = w4[k4];
+      const int64_t k = 4 * (int64_t)k4;
+      d += wq[0] * xp[k * xs];
+      d += wq[1] * xp[(k + 1) * xs];
+      d += wq[2] * xp[(k + 2) * xs];
+      d += wq[3] * xp[(k + 3) * xs];
+    }
+  } else {
+    for (int32_t k = 0; k < K; ++k) d += wr[k] * xp[(int64_t)k * xs];
+  }
+  return d;
+}
+
+struct SynRec {
+  int32_t y, v, x, kw, w, p, a, b;
+};
+
+__device__ __forceinline__ SynRec syn_rec(const SynConn* conn, int32_t c, bool live) {
+  SynRec r{-3, -3, 0, 0, 0, -1, 0, 0};
+  if (live) {
+    typedef int i4v __attribute__((ext_vector_type(4)));
+    const __attribute__((address_space(1))) i4v* q = (const __attribute__((address_space(1))) i4v*)(conn + c);
+    const i4v u = q[0], w = q[1];
+    r = SynRec{u[0], u[1], u[2], u[3], w[0], w[1], w[2], w[3]};
+  }
+  return r;
+}
+
+__global__ void __launch_bounds__(256) k_syn_scatter(float* st, Strides S, int32_t B, int32_t nseg,
+                                                     const int32_t* seg, const SynConn* conn, SynW W,
+                                                     int32_t update, float* probe, int32_t probe_rows,
+                                                     const float* stage, int32_t feed_rows, const int64_t* ctr,
+                                                     int32_t du) {
+  const uint32_t wv = (blockIdx.x * blockDim.x + threadIdx.x) / 64;
+  const int lane = threadIdx.x % 64, i = lane % kSynRows, j = lane / kSynRows;
+  const uint32_t sg = wv / (uint32_t)B, b = wv - sg * (uint32_t)B;
+  if (sg >= (uint32_t)nseg) return;   // the whole wavefront leaves together
+  typedef int i4v __attribute__((ext_vector_type(4)));
+  const i4v sd = *(const __attribute__((address_space(1))) i4v*)(G(seg) + 4 * (int64_t)sg);
+  const bool row = i < sd[1];
+  const int32_t c0 = sd[2], nc = sd[3];
+  // run-relative step (feed staging) and absolute step (probe record)
+  const int64_t tr = update ? ctr[1] + du : 0, ta = update ? ctr[0] + du : 0;
+  SynRec nxt[kSynPerLane];
+#pragma unroll
+  for (int h = 0; h < kSynPerLane; ++h) nxt[h] = syn_rec(conn, c0 + j + kSynLanes * h, row && j + kSynLanes * h < nc);
+  float acc = 0.0f;
+  for (int32_t q0 = 0; q0 < nc; q0 += kSynChunk) {
+    SynRec cur[kSynPerLane];
+#pragma unroll
+    for (int h = 0; h < kSynPerLane; ++h) cur[h] = nxt[h];
+#pragma unroll
+    for (int h = 0; h < kSynPerLane; ++h) {
+      const int32_t q = q0 + kSynChunk + j + kSynLanes * h;
+      nxt[h] = syn_rec(conn, c0 + q, row && q < nc);
+    }
+    // values (loads of both connections first, then the products)
+    float y[kSynPerLane], v[kSynPerLane];
+#pragma unroll
+    for (int h = 0; h < kSynPerLane; ++h) {
+      const SynRec& r = cur[h];
+      y[h] = 0.0f;
+      v[h] = 0.0f;
+      if (r.y == -3) continue;   // no connection in this slot
+      y[h] = st[at(S, (int64_t)r.y + i, b)];
+      if (!update || r.v == -2) continue;
+      if (r.v >= 0) {
+        v[h] = st[at(S, (int64_t)r.v + i, b)];
+      } else {
+        const int32_t K = r.kw & 0xffff, ws = (r.kw >> 16) & 15, staged = r.kw >> 20;
+        gptr<float> wr = G(W.w[ws]) + ((int64_t)r.w + i) * K;
+        const float* xp = staged ? stage + (tr * feed_rows + r.x) * B + b : st + at(S, r.x, b);
+        const int64_t xs = staged ? (int64_t)B : S.rs;
+        v[h] = 0.0f + syn_dot(wr, xp, xs, K);   // the DotInc adds into a reset row
+      }
+    }
+#pragma unroll
+    for (int h = 0; h < kSynPerLane; ++h) {
+      const SynRec& r = cur[h];
+      if (r.y == -3 || !update) continue;
+      if (r.v != -2) {
+        y[h] = __builtin_bit_cast(float, r.a) * y[h] + __builtin_bit_cast(float, r.b) * v[h];
+        st[at(S, (int64_t)r.y + i, b)] = y[h];
+      }
+      if (probe && r.p >= 0) probe[(ta * probe_rows + r.p + i) * B + b] = y[h];
+    }
+    // every lane takes part in the exchange; only lanes j == 0 keep a sum
+#pragma unroll
+    for (int jj = 0; jj < kSynChunk; ++jj) {
+      const float u = __shfl(y[jj / kSynLanes], i + kSynRows * (jj % kSynLanes), 64);
+      if (q0 + jj < nc) acc += u;
+    }
+  }
+  if (j == 0 && row && sd[0] >= 0) st[at(S, (int64_t)sd[0] + i, b)] = acc;
+}
+
 // node output <- feed staging [step][feed_rows][B] at the run-relative step
 // ctr[1] + du (du: the step's place among the steps launched since the counter
 // last advanced)

@@ -66,6 +66,15 @@ void jgroup(std::ostringstream& o, const Plan& p, const LGroup& L) {
     o << ",\"tau_rc\":"; jarr(o, L.tau_rc);
     o << ",\"tau_ref\":"; jarr(o, L.tau_ref);
     o << ",\"amp\":"; jarr(o, L.amp);
+  } else if (L.type == OP_SYN_SCATTER) {
+    o << ",\"update\":" << L.syn_update << ",\"probe\":" << L.syn_probe << ",\"seg\":";
+    jarr(o, L.syn_seg);
+    o << ",\"conn\":";
+    jarr(o, L.syn_conn);
+    o << ",\"ab\":";
+    jarr(o, L.syn_ab);
+    o << ",\"wbase\":";
+    jarr(o, L.syn_wbase);
   } else if (L.type == OP_DOT_INC) {
     o << ",\"M\":" << L.M << ",\"K\":" << L.K << ",\"w_row\":";
     jarr(o, L.w_row);
@@ -148,6 +157,19 @@ std::string plan_to_json(const Plan& p) {
     }
     o << ']';
   }
+  o << '}';
+  // the time-major step program of the launch drivers
+  const LaunchPlan lp = make_launch_plan(p);
+  o << ",\"launch\":{\"why\":";
+  jstr(o, lp.why);
+  o << ",\"groups\":[";
+  for (size_t g = 0; g < lp.step.size(); ++g) {
+    if (g) o << ',';
+    jgroup(o, p, lp.step[g]);
+  }
+  o << "],\"prologue\":";
+  if (lp.has_prologue) jgroup(o, p, lp.prologue);
+  else o << "null";
   o << "}}";
   return o.str();
 }

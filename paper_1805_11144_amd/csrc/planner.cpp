@@ -35,7 +35,8 @@ namespace ms {
 
 const char* op_type_name(int32_t t) {
   static const char* n[] = {"Feed", "Reset", "Copy", "CopyInc", "ElementwiseInc",
-                            "DotInc", "SimLIF", "SimLIFRate", "Lowpass", "Ensemble"};
+                            "DotInc", "SimLIF", "SimLIFRate", "Lowpass", "Ensemble",
+                            "SynapseScatter"};
   return (t >= 0 && t < OP_NTYPES) ? n[t] : "?";
 }
 

@@ -66,6 +66,12 @@ struct Launch {
   int32_t enc_lds = 0, dec_lds = 0, rw = 0;   // rw: encoder/decoder fragments held in registers
   size_t lds = 0;
   const uint16_t* w16 = nullptr;     // DOT_INC on bf16 MFMA: W rounded to bf16, op k at k*M*K
+  // SYN_SCATTER
+  const int32_t* syn_seg = nullptr;
+  const SynConn* syn_conn = nullptr;
+  SynW syn_w{};
+  int32_t syn_update = 1;
+  int32_t syn_probe = 0;
 };
 
 }  // namespace
@@ -89,6 +95,9 @@ struct ms_sim {
   int32_t* ipool = nullptr;
   float* fpool = nullptr;
   std::vector<Launch> launches;
+  bool has_prologue = false;         // launch drivers: pull of the post inputs before each run
+  Launch prologue;
+  bool probe_folded = false;         // the step's fused synapse launch records the probes
   int64_t* ctr = nullptr;            // [0] steps recorded since reset, [1] step within run
   float* feed_stage = nullptr;       // [cap][feed_rows][B]
   int64_t feed_cap = 0;
@@ -256,6 +265,27 @@ void build_launches(ms_sim* s, const std::vector<LGroup>& groups, std::vector<La
     }
     ens_off[gi] = pb.add_i(rec);
   }
+  // fused synapse groups: segments, then connection records of 8 words
+  static_assert(sizeof(SynConn) == 8 * 4, "SynConn layout");
+  std::vector<int64_t> seg_off(groups.size(), -1), conn_off(groups.size(), -1);
+  for (size_t gi = 0; gi < groups.size(); ++gi) {
+    const LGroup& g = groups[gi];
+    if (g.type != OP_SYN_SCATTER) continue;
+    seg_off[gi] = pb.add_i(g.syn_seg);
+    std::vector<int32_t> rec;
+    const size_t nc = g.syn_conn.size() / 8;
+    for (size_t c = 0; c < nc; ++c) {
+      const int32_t* q = &g.syn_conn[8 * c];
+      if (q[0] < 0 || q[3] < 0 || q[3] > 0xffff || q[4] > 3) fail(MS_E_INVALID, "fused synapse connection out of range");
+      SynConn r{};
+      r.y = q[0]; r.v = q[1]; r.x = q[2]; r.kw = q[3] | (std::max(q[4], 0) << 16) | (q[7] ? 1 << 20 : 0);
+      r.w = q[5]; r.p = q[6];
+      r.a = g.syn_ab[2 * c]; r.b = g.syn_ab[2 * c + 1];
+      const int32_t* w = reinterpret_cast<const int32_t*>(&r);
+      rec.insert(rec.end(), w, w + 8);
+    }
+    conn_off[gi] = pb.add_i(rec);
+  }
   const int64_t extra_off = pb.add_i(extra_ints);
   int32_t* ipool = dev_alloc<int32_t>(std::max<size_t>(1, pb.ints.size()));
   float* fpool = dev_alloc<float>(std::max<size_t>(1, pb.floats.size()));
@@ -359,84 +389,16 @@ void build_launches(ms_sim* s, const std::vector<LGroup>& groups, std::vector<La
       E.bias = s->base_ptr[g.ens_bias_base];
       E.ops = reinterpret_cast<const EnsOp*>(ipool + ens_off[gi]);
     }
+    if (g.type == OP_SYN_SCATTER) {
+      if ((int)g.syn_wbase.size() > 4) fail(MS_E_INVALID, "fused synapse group with too many weight bases");
+      l.syn_seg = ip(seg_off[gi]);
+      l.syn_conn = reinterpret_cast<const SynConn*>(ip(conn_off[gi]));
+      for (size_t k = 0; k < g.syn_wbase.size(); ++k) l.syn_w.w[k] = s->base_ptr[g.syn_wbase[k]];
+      l.syn_update = g.syn_update;
+      l.syn_probe = g.syn_probe;
+    }
     out.push_back(l);
   }
-}
-
-// Row ranges [first, last) of the state array that a fused-ensemble group
-// reads (inputs) and writes (spikes, decoded outputs; voltage and refractory
-// time count as both).
-void ens_rows(const LGroup& g, std::vector<std::pair<int64_t, int64_t>>& rd,
-              std::vector<std::pair<int64_t, int64_t>>& wr) {
-  for (size_t k = 0; k < g.ens_n.size(); ++k) {
-    const int64_t n = g.ens_n[k];
-    if (g.ens_x[k] >= 0) rd.push_back({g.ens_x[k], g.ens_x[k] + g.ens_d});
-    if (g.ens_V[k] >= 0) { wr.push_back({g.ens_V[k], g.ens_V[k] + n}); wr.push_back({g.ens_ref[k], g.ens_ref[k] + n}); }
-    if (g.ens_s[k] >= 0) wr.push_back({g.ens_s[k], g.ens_s[k] + n});
-    for (size_t f = 0; f < g.ens_dd.size(); ++f) wr.push_back({g.ens_dd[f][k], g.ens_dd[f][k] + g.ens_df[f]});
-  }
-}
-
-bool ranges_meet(std::vector<std::pair<int64_t, int64_t>> a, std::vector<std::pair<int64_t, int64_t>> b) {
-  std::sort(a.begin(), a.end());
-  std::sort(b.begin(), b.end());
-  size_t i = 0, j = 0;
-  while (i < a.size() && j < b.size()) {
-    if (a[i].second <= b[j].first) ++i;
-    else if (b[j].second <= a[i].first) ++j;
-    else return true;
-  }
-  return false;
-}
-
-// Two consecutive fused-ensemble groups can run as one launch when they share
-// neuron type, decoded functions and parameter bases, their inputs (if both
-// have any) have one width and encoder base, and neither touches a row the
-// other writes.  The planner keeps them apart because their operator
-// signatures differ (ensembles without input, ensembles whose spikes are
-// stored), which would otherwise cost a launch each per step.
-bool can_merge_ens(const LGroup& A, const LGroup& B) {
-  if (A.type != OP_ENS || B.type != OP_ENS) return false;
-  if (A.ens_type != B.ens_type || A.ens_df != B.ens_df || A.ens_Dbase != B.ens_Dbase ||
-      A.ens_bias_base != B.ens_bias_base)
-    return false;
-  const bool ia = A.a.base >= 0 && A.ens_d > 0, ib = B.a.base >= 0 && B.ens_d > 0;
-  if (ia && ib && (A.ens_d != B.ens_d || A.a.base != B.a.base)) return false;
-  for (int32_t x : A.ens_x) if (x >= 0 && !ia) return false;
-  for (int32_t x : B.ens_x) if (x >= 0 && !ib) return false;
-  std::vector<std::pair<int64_t, int64_t>> ra, wa, rb, wb;
-  ens_rows(A, ra, wa);
-  ens_rows(B, rb, wb);
-  return !ranges_meet(wa, rb) && !ranges_meet(wb, ra) && !ranges_meet(wa, wb);
-}
-
-void append_ens(LGroup& A, const LGroup& B) {
-  const size_t na = A.ens_n.size(), nb = B.ens_n.size();
-  auto params = [&](std::vector<float>& a, const std::vector<float>& b) {
-    if (a.size() == 1 && b.size() == 1 && a[0] == b[0]) return;
-    if (a.size() == 1) a.assign(na, a[0]);
-    if (b.size() == 1) a.insert(a.end(), nb, b[0]);
-    else a.insert(a.end(), b.begin(), b.end());
-  };
-  params(A.tau_rc, B.tau_rc);
-  params(A.tau_ref, B.tau_ref);
-  params(A.amp, B.amp);
-  if (!(A.a.base >= 0 && A.ens_d > 0)) { A.ens_d = B.ens_d; A.a = B.a; A.src = B.src; }
-  auto cat = [](std::vector<int32_t>& a, const std::vector<int32_t>& b) { a.insert(a.end(), b.begin(), b.end()); };
-  cat(A.ops, B.ops);
-  cat(A.ens_n, B.ens_n); cat(A.ens_x, B.ens_x); cat(A.ens_enc, B.ens_enc); cat(A.ens_bias, B.ens_bias);
-  cat(A.ens_V, B.ens_V); cat(A.ens_ref, B.ens_ref); cat(A.ens_s, B.ens_s);
-  for (size_t f = 0; f < A.ens_D.size(); ++f) { cat(A.ens_D[f], B.ens_D[f]); cat(A.ens_dd[f], B.ens_dd[f]); }
-  A.rows += B.rows;
-}
-
-std::vector<LGroup> merge_ens_groups(const std::vector<LGroup>& in) {
-  std::vector<LGroup> out;
-  for (const LGroup& g : in) {
-    if (!out.empty() && can_merge_ens(out.back(), g)) append_ens(out.back(), g);
-    else out.push_back(g);
-  }
-  return out;
 }
 
 void setup_device(ms_sim* s) {
@@ -470,11 +432,21 @@ void setup_device(ms_sim* s) {
     s->state = dev_alloc<float>(B);
   }
   // the persistent driver interprets the plan's groups one to one; the launch
-  // drivers run consecutive independent ensemble groups as one launch
-  if (s->driver == MS_DRIVER_STEPS || s->driver == MS_DRIVER_GRAPH)
-    build_launches(s, merge_ens_groups(p.lowered), s->launches, p.probe_src_rows, &s->probe_src);
-  else
+  // drivers run the step program (merged ensemble launches, fused synapses)
+  if (s->driver == MS_DRIVER_STEPS || s->driver == MS_DRIVER_GRAPH) {
+    LaunchPlan lp = make_launch_plan(p);
+    std::vector<LGroup> gs = std::move(lp.step);
+    if (lp.has_prologue) gs.push_back(lp.prologue);
+    build_launches(s, gs, s->launches, p.probe_src_rows, &s->probe_src);
+    if (lp.has_prologue) {
+      s->prologue = s->launches.back();
+      s->launches.pop_back();
+      s->has_prologue = true;
+    }
+    for (const Launch& l : s->launches) s->probe_folded |= l.type == OP_SYN_SCATTER && l.syn_probe;
+  } else {
     build_launches(s, p.lowered, s->launches, p.probe_src_rows, &s->probe_src);
+  }
   s->probe_rows = (int32_t)p.probe_src_rows.size();
   s->ctr = dev_alloc<int64_t>(2);
   HIPCHECK(hipMemset(s->ctr, 0, 2 * sizeof(int64_t)));
@@ -561,6 +533,16 @@ void launch_group(ms_sim* s, const Launch& l, int32_t du) {
       hipLaunchKernelGGL(k_lowpass, dim3(grid_for(n)), dim3(kBlock), 0, q, st, S, B, l.rows, l.dst,
                          l.src, l.fp);
       break;
+    case OP_SYN_SCATTER: {
+      // one wavefront per (segment, batch column)
+      const double items = (double)l.rows * 64 * B;
+      if (items >= 4294967296.0) fail(MS_E_INVALID, "fused synapse group too large for 32-bit indexing");
+      hipLaunchKernelGGL(k_syn_scatter, dim3(grid_for((int64_t)items)), dim3(kBlock), 0, q, st, S, B,
+                         (int32_t)l.rows, l.syn_seg, l.syn_conn, l.syn_w, l.syn_update,
+                         l.syn_probe ? s->probe_buf : nullptr, s->probe_rows, (const float*)s->feed_stage,
+                         s->plan->ir.feed_rows, (const int64_t*)s->ctr, du);
+      break;
+    }
     case OP_ENS:
       if (B >= 32) {
         hipLaunchKernelGGL(k_ens_tile, dim3((unsigned)l.rows, (unsigned)((B + 63) / 64)), dim3(256), 0, q, st, S,
@@ -588,7 +570,7 @@ void launch_step(ms_sim* s, int32_t du = 0, bool advance = true) {
     if (t) time_end(s, s->stream);
   }
   const int64_t n = (int64_t)s->probe_rows * s->B;
-  if (n > 0)
+  if (n > 0 && !s->probe_folded)
     hipLaunchKernelGGL(k_probe, dim3(grid_for(n)), dim3(kBlock), 0, s->stream, (const float*)s->state,
                        s->S, s->B, s->probe_rows, s->probe_src, s->probe_buf, s->ctr, du);
   if (advance) hipLaunchKernelGGL(k_advance, dim3(1), dim3(64), 0, s->stream, s->ctr, du + 1);
@@ -1191,10 +1173,16 @@ ms_status ms_sim_run_steps(ms_sim* s, int64_t n_steps, const ms_feed* feeds, int
       run_window(s, n_steps);
     } else if (s->driver == MS_DRIVER_GRAPH) {
       ensure_graph(s);
+      if (s->has_prologue) launch_group(s, s->prologue, 0);
       int64_t k = 0;
       for (; k + s->unroll <= n_steps; k += s->unroll) HIPCHECK(hipGraphLaunch(s->graph_exec, s->stream));
       for (; k < n_steps; ++k) launch_step(s);
     } else {
+      if (s->has_prologue) {
+        time_begin(s, OP_SYN_SCATTER, s->stream);
+        launch_group(s, s->prologue, 0);
+        time_end(s, s->stream);
+      }
       for (int64_t k = 0; k < n_steps; ++k) launch_step(s);
     }
     HIPCHECK(hipGetLastError());
@@ -1237,17 +1225,29 @@ ms_status ms_sim_kernel_time(ms_sim* s, int32_t op_type, double* ms_out, int64_t
       fail(MS_E_STATE, "per-kernel timing needs the WINDOW or STEPS driver");
     DeviceGuard dg(s->device);
     HIPCHECK(hipEventSynchronize(s->ev1));
-    double total = 0.0;
-    int64_t count = 0;
+    // launch intervals relative to the start of the run, then their union
+    std::vector<std::pair<double, double>> iv;
     for (size_t k = 0; k < s->tn; ++k) {
       if (s->ttype[k] != op_type) continue;
-      float ms = 0.f;
-      HIPCHECK(hipEventElapsedTime(&ms, s->tev[2 * k], s->tev[2 * k + 1]));
-      total += ms;
-      ++count;
+      float a = 0.f, b = 0.f;
+      HIPCHECK(hipEventElapsedTime(&a, s->ev0, s->tev[2 * k]));
+      HIPCHECK(hipEventElapsedTime(&b, s->ev0, s->tev[2 * k + 1]));
+      iv.push_back({a, std::max(a, b)});
     }
-    *ms_out = total;
-    if (launches_out) *launches_out = count;
+    std::sort(iv.begin(), iv.end());
+    double busy = 0.0, lo = 0.0, hi = -1.0;
+    for (const auto& x : iv) {
+      if (x.first > hi) {
+        if (hi > lo) busy += hi - lo;
+        lo = x.first;
+        hi = x.second;
+      } else {
+        hi = std::max(hi, x.second);
+      }
+    }
+    if (hi > lo) busy += hi - lo;
+    *ms_out = busy;
+    if (launches_out) *launches_out = (int64_t)iv.size();
   });
 }
 

@@ -19,11 +19,12 @@ FN_IDENTITY, FN_PRODUCT = 0, 1
 PLANNER_GREEDY, PLANNER_TREE = 0, 1
 DRIVER_AUTO, DRIVER_STEPS, DRIVER_GRAPH, DRIVER_PERSISTENT, DRIVER_WINDOW = 0, 1, 2, 3, 4
 GEMM_F32, GEMM_BF16 = 0, 1
+FUSE_ENSEMBLES, FUSE_SYNAPSES = 1, 2
 DECODE_DENSE, DECODE_EVENT = 0, 1
 PARAM_GAIN, PARAM_BIAS, PARAM_DECODERS = 0, 1, 2
 STATE_VOLTAGE, STATE_REFRACTORY, STATE_SYNAPSE, STATE_PROBE_SYNAPSE = 0, 1, 2, 3
 (OP_FEED, OP_RESET, OP_COPY, OP_COPY_INC, OP_ELEMENTWISE_INC, OP_DOT_INC, OP_LIF, OP_LIF_RATE, OP_LOWPASS,
- OP_ENSEMBLE) = range(10)
+ OP_ENSEMBLE, OP_SYNAPSE_SCATTER) = range(11)
 
 _dp = C.POINTER(C.c_double)
 _fp = C.POINTER(C.c_float)
@@ -246,7 +247,9 @@ def make_opts(dt=0.001, minibatch=1, unroll=10, planner=PLANNER_TREE, planner_de
     o.dt, o.minibatch, o.unroll = float(dt), int(minibatch), int(unroll)
     o.planner, o.planner_depth = int(planner), int(planner_depth)
     o.merge, o.sort, o.simplify = int(bool(merge)), int(bool(sort)), int(bool(simplify))
-    o.fuse = int(bool(fuse))
+    # True: every fusion (MS_FUSE_ENSEMBLES | MS_FUSE_SYNAPSES); False: none; an
+    # int: the MS_FUSE_* bits
+    o.fuse = (FUSE_ENSEMBLES | FUSE_SYNAPSES) if fuse is True else 0 if fuse is False else int(fuse)
     o.driver, o.device = int(driver), int(device)
     o.stream = stream
     o.probe_capacity_steps = int(probe_capacity_steps)

@@ -303,3 +303,91 @@ class WindowExecutor(PlanExecutor):
                 self.records.append(self.va[pr, t + 1].copy())
             self.va[:, 0] = self.va[:, tw]
             t0 += tw
+
+
+class LaunchExecutor(PlanExecutor):
+    """Runs the time-major step program of the launch drivers (the plan's
+    "launch" section): merged ensemble groups and fused synapse groups, with
+    the fused groups' pull-only prologue at the start of every run."""
+
+    def __init__(self, plan, spec, minibatch, params_from=None):
+        super().__init__(plan, spec, minibatch, params_from)
+        self.lp = self.j["launch"]
+        if params_from is not None:
+            self._replace_constants(params_from, [g for g in self.lp["groups"] if g["type"] != "Reset"])
+            # resets may have lost rows: their values row by row from the plan's
+            reset_val = {}
+            for g in self.j["groups"]:
+                if g["type"] == "Reset":
+                    n = g["rows"]
+                    vals = _vec(g["values"], n) if "values" in g else np.zeros(n)
+                    reset_val.update({int(r): float(v) for r, v in zip(_rows(g["dst"], n), vals)})
+            for g in self.lp["groups"]:
+                if g["type"] == "Reset" and "values" in g:
+                    g["values"] = [reset_val[int(r)] for r in _rows(g["dst"], g["rows"])]
+            # fused groups take each connection's coefficients from its first
+            # filter row, as set in the plan's (oracle-valued) Lowpass groups
+            coef = {}
+            for g in self.j["groups"]:
+                if g["type"] == "Lowpass":
+                    n = g["rows"]
+                    for y, a, b in zip(_rows(g["dst"], n), _vec(g["ca"], n), _vec(g["cb"], n)):
+                        coef[int(y)] = (float(a), float(b))
+            for g in self.lp["groups"] + ([self.lp["prologue"]] if self.lp["prologue"] else []):
+                if g["type"] == "SynapseScatter":
+                    conn = np.asarray(g["conn"], np.int64).reshape(-1, 8)
+                    g["ab"] = [x for y0, v0 in conn[:, :2] for x in (coef[int(y0)] if v0 != -2 else (0.0, 0.0))]
+
+    def step(self, feed_rows_values):
+        st = self.st
+        rec = None
+        for g in self.lp["groups"]:
+            if g["type"] == "SynapseScatter":
+                r = self.exec_synapse(g, st, feed_rows_values)
+                if g["probe"]:
+                    rec = r
+            else:
+                self.exec_group(g, st, st, st, st, feed_rows_values)
+        if rec is None:
+            rec = st[np.asarray(self.j["probe_rows"], np.int64)].copy()
+        else:   # a folded probe must have recorded every probe row
+            assert not np.isnan(rec).any(), "probe rows the fused group did not record"
+        self.records.append(rec)
+
+    def run(self, n_steps, feeds):
+        if self.lp["prologue"] is not None:
+            self.exec_synapse(self.lp["prologue"], self.st)
+        super().run(n_steps, feeds)
+
+    def exec_synapse(self, g, st, feed_rows_values=None):
+        """Per segment row i: for each connection in order, v (state row or
+        weight row . inputs, the inputs from the state or from this step's
+        feed values), y <- a y + b v (when updating), sum of the y; the sum is
+        stored in the post row.  Returns the probe rows it recorded."""
+        seg = np.asarray(g["seg"], np.int64).reshape(-1, 4)
+        conn = np.asarray(g["conn"], np.int64).reshape(-1, 8)
+        ab = np.asarray(g["ab"], np.float64).reshape(-1, 2)
+        rec = np.full((len(self.j["probe_rows"]), self.B), np.nan)
+        for dst, ln, c0, nc in seg:
+            i = np.arange(ln)
+            acc = np.zeros((ln, self.B))
+            for c in range(c0, c0 + nc):
+                y0, v0, x0, K, ws, w0, pr, staged = conn[c]
+                y = st[y0 + i]
+                if g["update"]:
+                    if v0 != -2:
+                        if v0 >= 0:
+                            v = st[v0 + i]
+                        else:
+                            W = self.bases[g["wbase"][ws]]
+                            xin = feed_rows_values[x0:x0 + K] if staged else st[x0:x0 + K]
+                            v = W[w0 + i, :K] @ xin
+                        y = ab[c, 0] * y + ab[c, 1] * v
+                        st[y0 + i] = y
+                    if pr >= 0:
+                        assert np.isnan(rec[pr + i]).all(), "probe row recorded twice"
+                        rec[pr + i] = y
+                acc = acc + y
+            if dst >= 0:
+                st[dst + i] = acc
+        return rec

@@ -37,3 +37,20 @@ def test_c2_c4_magnitudes(name, mb, mflop):
     w = make_workload(name)
     assert bench.compulsory_bytes_per_step(w) / 1e6 == pytest.approx(mb, rel=0.01)
     assert bench.gemm_flops_per_step(w) / 1e6 == pytest.approx(mflop, rel=0.01)
+
+
+def test_c4_ensemble_gemm_flops_by_hand():
+    """The matrix-core work of C4's fused ensembles: 200 ensembles x 500
+    neurons x 512 batch rows, 16-D encoders (every ensemble has an input: the
+    chain and the input node) and 16 decoded outputs, 2 flops per
+    multiply-add."""
+    w = make_workload("c4")
+    assert bench.ensemble_gemm_flops_per_step(w) == 200 * 500 * 512 * 2 * (16 + 16)
+
+
+def test_mean_ci95_matches_student_t():
+    """95% interval of five values by hand: mean 2, sample sd 1.5811, t(0.975, 4)
+    = 2.7764 -> half-width 1.9632."""
+    m, h = bench.mean_ci95([0.0, 1.0, 2.0, 3.0, 4.0])
+    assert m == pytest.approx(2.0)
+    assert h == pytest.approx(2.7764451 * 1.5811388 / 5 ** 0.5, rel=1e-6)

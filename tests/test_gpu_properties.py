@@ -149,7 +149,7 @@ def test_independent_ensemble_groups_share_a_launch(driver):
     plan_groups = [g["type"] for g in M.Plan(model, minibatch=1).json()["groups"]]
     assert plan_groups.count("Ensemble") == 2
     drv = {"steps": M.DRIVER_STEPS, "graph": M.DRIVER_GRAPH}[driver]
-    with M.Simulator(model, minibatch=1, driver=drv, unroll=7) as sim:
+    with M.Simulator(model, minibatch=1, driver=drv, unroll=7, fuse=M.mergesim.FUSE_ENSEMBLES) as sim:
         assert sim.info()["groups_per_step"] == len(plan_groups) - 1
         sim.run_steps(w.n_steps, w.feeds)
         got = [sim.data(p) for p in range(len(w.spec.probes))]
