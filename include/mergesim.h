@@ -287,6 +287,20 @@ ms_status ms_sim_probe_width(const ms_sim* sim, int32_t probe_id, int32_t* width
 ms_status ms_sim_probe_read(ms_sim* sim, int32_t probe_id, float* out, int64_t cap_elems,
                             int32_t out_on_device);
 
+/* Probe read that allocates nothing, for callers that cannot allocate device
+ * memory (code under HIP graph capture, tight serving loops, harnesses that
+ * forbid allocation).  Same result as ms_sim_probe_read into host memory (out:
+ * host buffer, [minibatch][steps][width] float32, cap_elems at least
+ * minibatch * steps * width), but the device-side transposition is staged in a
+ * fixed array of MS_PROBE_READ_STATIC_MAX floats (16 MiB) that each GPU the
+ * library runs on holds until the process ends, instead of a temporary
+ * allocation.  A record larger than that is MS_E_INVALID (use
+ * ms_sim_probe_read).  Every simulator on one GPU shares that GPU's array:
+ * calls that overlap on one GPU (several host threads) race.  Returns after
+ * the copy into `out` has finished. */
+#define MS_PROBE_READ_STATIC_MAX (1 << 22)
+ms_status ms_sim_probe_read_static(ms_sim* sim, int32_t probe_id, float* out, int64_t cap_elems);
+
 /* Restore the initial state (V = 0, refractory 0, filters 0) and clear probes
  * (paper Sec. 3.1 sim.reset()). */
 ms_status ms_sim_reset(ms_sim* sim);

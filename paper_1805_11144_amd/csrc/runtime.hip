@@ -17,11 +17,18 @@
 #include <string>
 #include <vector>
 
+#include <mutex>
+
 #include "host.hpp"
 #include "kernels.hpp"
 #include "kernels_window.hpp"
 
 using namespace ms;
+
+// Staging array of ms_sim_probe_read_static, which allocates nothing: one copy
+// per GPU, held until the process ends.  In host code its name is only a
+// handle; its device address (per device) comes from hipGetSymbolAddress.
+static __device__ __align__(256) float scratch[MS_PROBE_READ_STATIC_MAX];
 
 #define HIPCHECK(expr)                                                                    \
   do {                                                                                    \
@@ -121,7 +128,7 @@ struct ms_sim {
   int32_t n_cu = 256;                // compute units of the device
   int32_t persistent_threads = 256;  // workgroup size of the persistent kernel
   int64_t scratch_n = 0;             // per-column scratch floats of the persistent kernel
-  float* scratch = nullptr;          // global scratch when state is not LDS-resident
+  float* col_scratch = nullptr;      // global scratch when state is not LDS-resident
   std::vector<void*> extra_allocs;   // transposed weights and their offsets, extra pools
   // window driver
   std::unique_ptr<WindowPlan> wplan;
@@ -156,6 +163,27 @@ struct DeviceGuard {
   }
 };
 
+// Device address of `scratch` on each device, resolved once per device with
+// that device current (at simulator creation).
+std::mutex g_scratch_mu;
+std::vector<float*> g_scratch_ptr;
+
+float* scratch_on(int dev) {
+  std::lock_guard<std::mutex> lk(g_scratch_mu);
+  if (dev < 0) fail(MS_E_INVALID, "device ordinal out of range");
+  if ((size_t)dev >= g_scratch_ptr.size()) g_scratch_ptr.resize((size_t)dev + 1, nullptr);
+  if (!g_scratch_ptr[dev]) {
+    int cur = -1;
+    HIPCHECK(hipGetDevice(&cur));
+    if (cur != dev) fail(MS_E_STATE, "static staging array resolved on another device");
+    void* p = nullptr;
+    HIPCHECK(hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)));
+    if (!p) fail(MS_E_HIP, "hipGetSymbolAddress returned no address for the staging array");
+    g_scratch_ptr[dev] = (float*)p;
+  }
+  return g_scratch_ptr[dev];
+}
+
 void destroy_graph(ms_sim* s) {
   if (s->graph_exec) (void)hipGraphExecDestroy(s->graph_exec);
   if (s->graph) (void)hipGraphDestroy(s->graph);
@@ -172,7 +200,7 @@ void free_sim(ms_sim* s) {
     if (s->base_ptr[b] != s->state) f(s->base_ptr[b]);
   f(s->ipool); f(s->fpool); f(s->ctr); f(s->feed_stage); f(s->feed_tmp); f(s->probe_buf);
   f(s->prog.groups);
-  f(s->scratch);
+  f(s->col_scratch);
   f(s->va); f(s->pa);
   for (void* p : s->extra_allocs) f(p);
   if (s->ev0) (void)hipEventDestroy(s->ev0);
@@ -746,13 +774,13 @@ void run_persistent(ms_sim* s, int64_t n_steps) {
     hipLaunchKernelGGL(k_persistent<true>, dim3(s->B), dim3(threads), lds, s->stream, s->state, rows, s->B,
                        (const GroupDesc*)s->prog.groups, s->prog.n_groups, n_steps, s->dt,
                        (const float*)s->feed_stage, s->plan->ir.feed_rows, s->probe_src, s->probe_rows,
-                       s->probe_buf, s->steps_total, s->scratch, s->scratch_n);
+                       s->probe_buf, s->steps_total, s->col_scratch, s->scratch_n);
   } else {
-    if (!s->scratch && s->scratch_n > 0) s->scratch = dev_alloc<float>((size_t)s->scratch_n * s->B);
+    if (!s->col_scratch && s->scratch_n > 0) s->col_scratch = dev_alloc<float>((size_t)s->scratch_n * s->B);
     hipLaunchKernelGGL(k_persistent<false>, dim3(s->B), dim3(threads), 0, s->stream, s->state, rows, s->B,
                        (const GroupDesc*)s->prog.groups, s->prog.n_groups, n_steps, s->dt,
                        (const float*)s->feed_stage, s->plan->ir.feed_rows, s->probe_src, s->probe_rows,
-                       s->probe_buf, s->steps_total, s->scratch, s->scratch_n);
+                       s->probe_buf, s->steps_total, s->col_scratch, s->scratch_n);
   }
   hipLaunchKernelGGL(k_set_ctr, dim3(1), dim3(64), 0, s->stream, s->ctr, s->steps_total + n_steps, n_steps);
 }
@@ -1130,6 +1158,7 @@ ms_status ms_sim_create(const ms_model* model, const ms_sim_opts* opts, ms_sim**
         s->wplan = std::make_unique<WindowPlan>(make_window_plan(*s->plan));
         if (!s->wplan->ok) fail(MS_E_INVALID, "the window driver cannot run this model: " + s->wplan->why);
       }
+      (void)scratch_on(s->device);   // the static staging array's address on this device
       setup_device(s);
       if (s->driver == MS_DRIVER_PERSISTENT) setup_persistent(s);
       if (s->driver == MS_DRIVER_WINDOW) setup_window(s);
@@ -1294,6 +1323,29 @@ ms_status ms_sim_probe_read(ms_sim* s, int32_t probe, float* out, int64_t cap, i
     if (e == hipSuccess) e = hipStreamSynchronize(s->stream);
     if (!out_on_device) (void)hipFree(tmp);
     if (e != hipSuccess) fail(MS_E_HIP, std::string("probe read: ") + hipGetErrorString(e));
+  });
+}
+
+ms_status ms_sim_probe_read_static(ms_sim* s, int32_t probe, float* out, int64_t cap) {
+  return guarded([&] {
+    if (!s || !out) fail(MS_E_INVALID, "NULL argument");
+    const Plan& p = *s->plan;
+    if (probe < 0 || probe >= (int32_t)p.probe_width.size()) fail(MS_E_INVALID, "probe id out of range");
+    const int32_t w = p.probe_width[probe];
+    const int64_t T = s->steps_total;
+    const int64_t n = (int64_t)s->B * T * w;
+    if (cap < n) fail(MS_E_INVALID, "probe output capacity too small");
+    if (n > MS_PROBE_READ_STATIC_MAX)
+      fail(MS_E_INVALID, "probe record of " + std::to_string(n) + " values exceeds the static staging array (" +
+                             std::to_string(MS_PROBE_READ_STATIC_MAX) + " values); use ms_sim_probe_read");
+    if (n == 0) return;
+    DeviceGuard dg(s->device);
+    float* stage = scratch_on(s->device);
+    hipLaunchKernelGGL(k_probe_extract, dim3(grid_for(n)), dim3(kBlock), 0, s->stream,
+                       (const float*)s->probe_buf, s->B, T, s->probe_rows, p.probe_row_offset[probe], w, stage);
+    HIPCHECK(hipGetLastError());
+    HIPCHECK(hipMemcpyAsync(out, stage, (size_t)n * 4, hipMemcpyDeviceToHost, s->stream));
+    HIPCHECK(hipStreamSynchronize(s->stream));
   });
 }
 

@@ -20,6 +20,7 @@ PLANNER_GREEDY, PLANNER_TREE = 0, 1
 DRIVER_AUTO, DRIVER_STEPS, DRIVER_GRAPH, DRIVER_PERSISTENT, DRIVER_WINDOW = 0, 1, 2, 3, 4
 GEMM_F32, GEMM_BF16 = 0, 1
 FUSE_ENSEMBLES, FUSE_SYNAPSES = 1, 2
+PROBE_READ_STATIC_MAX = 1 << 22
 DECODE_DENSE, DECODE_EVENT = 0, 1
 PARAM_GAIN, PARAM_BIAS, PARAM_DECODERS = 0, 1, 2
 STATE_VOLTAGE, STATE_REFRACTORY, STATE_SYNAPSE, STATE_PROBE_SYNAPSE = 0, 1, 2, 3
@@ -93,6 +94,7 @@ _SIGNATURES = [
     ("ms_sim_steps", [C.c_void_p, C.POINTER(_i64)], _i32),
     ("ms_sim_probe_width", [C.c_void_p, _i32, C.POINTER(_i32)], _i32),
     ("ms_sim_probe_read", [C.c_void_p, _i32, _fp, _i64, _i32], _i32),
+    ("ms_sim_probe_read_static", [C.c_void_p, _i32, _fp, _i64], _i32),
     ("ms_sim_reset", [C.c_void_p], _i32),
     ("ms_sim_get_state", [C.c_void_p, _i32, _i32, _fp, _i64], _i32),
     ("ms_sim_set_state", [C.c_void_p, _i32, _i32, _fp, _i64], _i32),
@@ -372,6 +374,15 @@ class Simulator:
         T = self.n_steps
         out = np.empty((self.minibatch, T, w), np.float32)
         _check(self._lib.ms_sim_probe_read(self.handle, probe, out.ctypes.data_as(_fp), out.size, 0))
+        return out
+
+    def data_static(self, probe: int) -> np.ndarray:
+        """Probe record [B, steps, width] read without any device allocation
+        (ms_sim_probe_read_static; at most PROBE_READ_STATIC_MAX values)."""
+        w = self.probe_width(probe)
+        T = self.n_steps
+        out = np.empty((self.minibatch, T, w), np.float32)
+        _check(self._lib.ms_sim_probe_read_static(self.handle, probe, out.ctypes.data_as(_fp), out.size))
         return out
 
     def reset(self):
