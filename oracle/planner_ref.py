@@ -528,43 +528,101 @@ def read_blocks(ir: IR, groups: List[List[int]]) -> List[ReadBlock]:
 
 
 def sort_metablocks(metas: List[frozenset], block_size: Dict[int, int]) -> List[int]:
-    """Alg. 1: order meta-blocks (sets of read-block ids, listed in id order)
-    so that large read blocks end up contiguous.  Returns meta-block ids."""
-    remaining = list(range(len(metas)))
+    """Order meta-blocks (sets of read-block ids) so that large read blocks end
+    up contiguous (Sec. 4.2.3, Alg. 1).  Meta-blocks are appended one at a
+    time; the next one is the remaining meta-block that best matches the last
+    one appended, by the section's four criteria in order of precedence:
+
+      1. it contains the active read block (the block being laid out: at
+         first the largest; once no remaining meta-block contains it, the
+         largest block of the last meta-block takes over for later choices);
+      2. it contains every read block of the last meta-block;
+      3. its Hamming distance to the last meta-block is smallest;
+      4. it contains the last meta-block's read blocks, the larger the better
+         (compared block by block, largest first);
+
+    then the lowest id.  Returns meta-block ids in layout order."""
+    left = list(range(len(metas)))
     if not block_size:
-        return remaining
-    def order(bs):   # larger first, then lower id
-        return sorted(bs, key=lambda b: (-block_size[b], b))
-    a = order(block_size)[0]
-    c = next(m for m in remaining if a in metas[m])
-    out = []
-    while remaining:
-        X = [m for m in remaining if a in metas[m]]
-        if not X:
-            X = list(remaining)
-            if metas[c]:
-                a = order(metas[c])[0]
-        Y = [x for x in X if metas[c] <= metas[x]] or X
-        dist = {y: len(metas[y] ^ metas[c]) for y in Y}
-        dmin = min(dist.values())
-        Z = [y for y in Y if dist[y] == dmin]
-        if len(Z) > 1:
-            for b in order(metas[c]):
-                Z2 = [z for z in Z if b in metas[z]]
-                if Z2:
-                    Z = Z2
-                if len(Z) == 1:
-                    break
-        z = min(Z)
-        remaining.remove(z)
-        out.append(z)
-        c = z
-    return out
+        return left
+    def size_order(blocks):
+        return sorted(blocks, key=lambda bid: (-block_size[bid], bid))
+    active = size_order(block_size)[0]
+    # before anything is placed, a meta-block holding the active block plays
+    # the part of the last one
+    last = metas[next(m for m in left if active in metas[m])]
+    placed = []
+    while left:
+        active_left = any(active in metas[m] for m in left)
+        ranked_blocks = size_order(last)
+
+        def rank(m):
+            s = metas[m]
+            return (active_left and active not in s,
+                    not last <= s,
+                    len(s ^ last),
+                    tuple(bid not in s for bid in ranked_blocks),
+                    m)
+        best = min(left, key=rank)
+        if not active_left and last:
+            active = ranked_blocks[0]
+        left.remove(best)
+        placed.append(best)
+        last = metas[best]
+    return placed
+
+
+def _settle(ir: IR, groups: List[List[int]], blocks: List[ReadBlock], meta_sigs: List[List[int]],
+            meta_sets: List[frozenset], order: Dict[int, List[int]], passes: int) -> None:
+    """Order operators and signals inside meta-blocks (Sec. 4.2.3, Alg. 2).
+    For one read block b: (1) b's group takes the order in which b's signals
+    lie in memory; (2) every read block c of that group has its signals
+    rearranged, each meta-block within its own positions (so the meta-block
+    layout of Alg. 1 stays), into the group's new operator order.  Blocks are
+    taken from the smallest to the largest, so larger blocks settle last and
+    win conflicts; passes repeat until one leaves everything as it was, at
+    most `passes` of them."""
+    pos = {s: i for base in order for i, s in enumerate(order[base])}
+    visit = sorted(range(len(blocks)), key=lambda bid: (blocks[bid].size, bid))
+    of_group: Dict[int, List[int]] = {}
+    for bid, blk in enumerate(blocks):
+        of_group.setdefault(blk.group, []).append(bid)
+    metas_of = {bid: [m for m in range(len(meta_sets)) if bid in meta_sets[m]] for bid in range(len(blocks))}
+
+    def read(op, slot):
+        r = read_refs(ir.ops[op])[slot]
+        return r.sig, r.start
+
+    def ops_follow_layout(blk):
+        groups[blk.group] = sorted(groups[blk.group], key=lambda op: (pos[read(op, blk.slot)[0]],
+                                                                       read(op, blk.slot)[1]))
+
+    def signals_follow_ops(bid):
+        blk = blocks[bid]
+        rank: Dict[int, int] = {}
+        for op in groups[blk.group]:
+            rank.setdefault(read(op, blk.slot)[0], len(rank))
+        for m in metas_of[bid]:
+            spots = sorted(pos[s] for s in meta_sigs[m])
+            for spot, sig in zip(spots, sorted(meta_sigs[m], key=rank.__getitem__)):
+                order[blk.base][spot] = sig
+                pos[sig] = spot
+
+    for _ in range(passes):
+        before = ([list(g) for g in groups], {b: list(o) for b, o in order.items()})
+        for bid in visit:
+            ops_follow_layout(blocks[bid])
+            for other in of_group[blocks[bid].group]:
+                signals_follow_ops(other)
+        if before == ([list(g) for g in groups], order):
+            break
 
 
 def sort_signals_ops(ir: IR, groups: List[List[int]], passes: int = 10):
-    """Meta-block sort per base array (Alg. 1), then Alg. 2.  Returns the
-    signal order of every base array; reorders the operators inside groups."""
+    """Signal layout of every base array (meta-blocks ordered by Alg. 1, then
+    operators and signals settled by Alg. 2); reorders the operators inside
+    groups in place.  Meta-blocks: the signals of one base array that take
+    part in exactly the same read blocks, numbered by first appearance."""
     blocks = read_blocks(ir, groups)
     member: Dict[int, List[int]] = {}
     for bi, b in enumerate(blocks):
@@ -588,43 +646,7 @@ def sort_signals_ops(ir: IR, groups: List[List[int]], passes: int = 10):
         sizes = {bi: b.size for bi, b in enumerate(blocks) if b.base == base}
         local = sort_metablocks([meta_sets[m] for m in ids], sizes)
         order[base] = [s for li in local for s in meta_sigs[ids[li]]]
-    pos = {s: i for base in order for i, s in enumerate(order[base])}
-
-    by_size = sorted(range(len(blocks)), key=lambda bi: (blocks[bi].size, bi))
-    blocks_of_group: Dict[int, List[int]] = {}
-    for bi, b in enumerate(blocks):
-        blocks_of_group.setdefault(b.group, []).append(bi)
-    for _ in range(passes):
-        changed = False
-        for bi in by_size:
-            b = blocks[bi]
-            g = groups[b.group]
-            new = sorted(g, key=lambda oi: (pos[read_refs(ir.ops[oi])[b.slot].sig],
-                                            read_refs(ir.ops[oi])[b.slot].start))
-            if new != g:
-                changed = True
-                groups[b.group] = g = new
-            for ci in blocks_of_group[b.group]:
-                c = blocks[ci]
-                seq = []
-                for oi in g:
-                    s = read_refs(ir.ops[oi])[c.slot].sig
-                    if s not in seq:
-                        seq.append(s)
-                rank = {s: i for i, s in enumerate(seq)}
-                for m in range(len(meta_sigs)):
-                    if ci not in meta_sets[m]:
-                        continue
-                    slots = sorted(pos[s] for s in meta_sigs[m])
-                    now = [order[c.base][p] for p in slots]
-                    want = sorted(now, key=lambda s: rank[s])
-                    if want != now:
-                        changed = True
-                        for p, s in zip(slots, want):
-                            order[c.base][p] = s
-                            pos[s] = p
-        if not changed:
-            break
+    _settle(ir, groups, blocks, meta_sigs, meta_sets, order, passes)
     return order
 
 

@@ -17,11 +17,11 @@
 //    larger first group, then the lower key id (key ids in order of first
 //    appearance in the operator list)
 //  * read blocks: signals read by one group in one operand slot; block size =
-//    total elements; ties go to the lower id.  Alg. 1 filters keep the previous
-//    candidate set if a filter would empty it, and fall back to the lowest
-//    meta-block id.  Alg. 2 sorts operators by (position of the read signal,
-//    slice start), permutes signals only inside their meta-block, and makes at
-//    most 10 passes.
+//    total elements; ties go to the lower id.  Alg. 1 ranks the candidate
+//    meta-blocks by the four criteria of Sec. 4.2.3 (a criterion no candidate
+//    meets does not separate them), then by the lowest id.  Alg. 2 sorts
+//    operators by (position of the read signal, slice start), permutes
+//    signals only inside their meta-block, and makes at most 10 passes.
 #include <algorithm>
 #include <array>
 #include <climits>
@@ -327,129 +327,117 @@ void sort_plan(const IR& ir, std::vector<std::vector<int32_t>>& groups, SortStat
     meta_sigs[id].push_back(sig);
     meta_of[sig] = id;
   }
-  auto bigger = [&](int32_t x, int32_t y) {   // block order: size desc, id asc
+  auto larger_first = [&](int32_t x, int32_t y) {   // read blocks: size desc, id asc
     if (blocks[x].size != blocks[y].size) return blocks[x].size > blocks[y].size;
     return x < y;
   };
-  auto contains = [&](int32_t m, int32_t b) {
-    return std::binary_search(meta_set[m].begin(), meta_set[m].end(), b);
-  };
-  auto subset = [&](int32_t c, int32_t x) {   // set(c) within set(x)
-    return std::includes(meta_set[x].begin(), meta_set[x].end(), meta_set[c].begin(), meta_set[c].end());
-  };
-  auto hamming = [&](int32_t x, int32_t y) {
-    std::vector<int32_t> d;
-    std::set_symmetric_difference(meta_set[x].begin(), meta_set[x].end(), meta_set[y].begin(),
-                                  meta_set[y].end(), std::back_inserter(d));
-    return (int64_t)d.size();
+  auto holds = [&](int32_t m, int32_t blk) {
+    return std::binary_search(meta_set[m].begin(), meta_set[m].end(), blk);
   };
 
-  // ---- Alg. 1, per base array
+  // ---- meta-block layout (Alg. 1), per base array.  Meta-blocks are placed
+  // one after another; the next is the remaining one that best matches the
+  // last placed, ranked by the four criteria of Sec. 4.2.3 in order of
+  // precedence: holds the active read block; holds every read block of the
+  // last; smallest Hamming distance to the last; holds the last's read blocks,
+  // the larger the better (block by block, largest first); then lowest id.
+  // The active block is the largest at first; once no remaining meta-block
+  // holds it, the largest block of the last placed takes over for later
+  // choices.
   st.order.assign(nb, {});
   st.pos.assign(ns, -1);
   for (int32_t base = 0; base < nb; ++base) {
-    std::vector<int32_t> M;
-    for (int32_t m = 0; m < (int32_t)meta_sigs.size(); ++m) if (meta_base[m] == base) M.push_back(m);
-    std::vector<int32_t> bblocks;
-    for (int32_t bi = 0; bi < nblk; ++bi) if (blocks[bi].base == base) bblocks.push_back(bi);
-    std::vector<int32_t> S;
-    if (bblocks.empty()) {
-      S = M;
+    std::vector<int32_t> left;
+    for (int32_t m = 0; m < (int32_t)meta_sigs.size(); ++m) if (meta_base[m] == base) left.push_back(m);
+    std::vector<int32_t> base_blocks;
+    for (int32_t bi = 0; bi < nblk; ++bi) if (blocks[bi].base == base) base_blocks.push_back(bi);
+    std::vector<int32_t> placed;
+    if (base_blocks.empty()) {
+      placed = left;
     } else {
-      int32_t a = *std::min_element(bblocks.begin(), bblocks.end(), bigger);
-      int32_t c = -1;
-      for (int32_t m : M) if (contains(m, a)) { c = m; break; }
-      while (!M.empty()) {
-        std::vector<int32_t> X;
-        for (int32_t m : M) if (contains(m, a)) X.push_back(m);
-        if (X.empty()) {
-          X = M;
-          if (!meta_set[c].empty())
-            a = *std::min_element(meta_set[c].begin(), meta_set[c].end(), bigger);
+      int32_t active = *std::min_element(base_blocks.begin(), base_blocks.end(), larger_first);
+      int32_t last = -1;   // before anything is placed: a meta-block holding the active block
+      for (int32_t m : left) if (holds(m, active)) { last = m; break; }
+      while (!left.empty()) {
+        bool active_left = false;
+        for (int32_t m : left) active_left = active_left || holds(m, active);
+        std::vector<int32_t> last_blocks = meta_set[last];
+        std::sort(last_blocks.begin(), last_blocks.end(), larger_first);
+        // rank key: criteria 1-4 as small integers, then the id
+        auto key = [&](int32_t m) {
+          std::vector<int64_t> k;
+          k.push_back(active_left && !holds(m, active) ? 1 : 0);
+          k.push_back(std::includes(meta_set[m].begin(), meta_set[m].end(), meta_set[last].begin(),
+                                    meta_set[last].end()) ? 0 : 1);
+          std::vector<int32_t> diff;
+          std::set_symmetric_difference(meta_set[m].begin(), meta_set[m].end(), meta_set[last].begin(),
+                                        meta_set[last].end(), std::back_inserter(diff));
+          k.push_back((int64_t)diff.size());
+          for (int32_t blk : last_blocks) k.push_back(holds(m, blk) ? 0 : 1);
+          k.push_back(m);
+          return k;
+        };
+        int32_t best = left[0];
+        std::vector<int64_t> best_key = key(best);
+        for (size_t i = 1; i < left.size(); ++i) {
+          std::vector<int64_t> k = key(left[i]);
+          if (k < best_key) { best_key.swap(k); best = left[i]; }
         }
-        std::vector<int32_t> Y;
-        for (int32_t x : X) if (subset(c, x)) Y.push_back(x);
-        if (Y.empty()) Y = X;
-        int64_t dmin = INT64_MAX;
-        for (int32_t y : Y) dmin = std::min(dmin, hamming(y, c));
-        std::vector<int32_t> Z;
-        for (int32_t y : Y) if (hamming(y, c) == dmin) Z.push_back(y);
-        if (Z.size() > 1) {
-          std::vector<int32_t> cb = meta_set[c];
-          std::sort(cb.begin(), cb.end(), bigger);
-          for (int32_t mb : cb) {
-            std::vector<int32_t> Z2;
-            for (int32_t z : Z) if (contains(z, mb)) Z2.push_back(z);
-            if (!Z2.empty()) Z.swap(Z2);
-            if (Z.size() == 1) break;
-          }
-        }
-        int32_t z = *std::min_element(Z.begin(), Z.end());
-        M.erase(std::find(M.begin(), M.end(), z));
-        S.push_back(z);
-        c = z;
+        if (!active_left && !last_blocks.empty()) active = last_blocks[0];
+        left.erase(std::find(left.begin(), left.end(), best));
+        placed.push_back(best);
+        last = best;
       }
     }
-    for (int32_t m : S)
+    for (int32_t m : placed)
       for (int32_t sig : meta_sigs[m]) st.order[base].push_back(sig);
     st.reindex(base);
   }
 
-  // ---- Alg. 2
-  std::vector<int32_t> sorted_blocks(nblk);
-  std::iota(sorted_blocks.begin(), sorted_blocks.end(), 0);
-  std::stable_sort(sorted_blocks.begin(), sorted_blocks.end(), [&](int32_t x, int32_t y) {
-    return blocks[x].size < blocks[y].size;
-  });
-  // meta-blocks containing each block
-  std::vector<std::vector<int32_t>> metas_of_block(nblk);
+  // ---- operators and signals inside meta-blocks (Alg. 2).  For one read
+  // block: its group's operators take the order in which the block's signals
+  // lie in memory; then every read block of that group has its signals
+  // rearranged into the new operator order, each meta-block within its own
+  // positions (the meta-block layout stays).  Blocks are visited smallest
+  // first so that larger blocks settle last; passes repeat until one changes
+  // nothing, at most 10.
+  std::vector<int32_t> visit(nblk);
+  std::iota(visit.begin(), visit.end(), 0);
+  std::stable_sort(visit.begin(), visit.end(), [&](int32_t x, int32_t y) { return blocks[x].size < blocks[y].size; });
+  std::vector<std::vector<int32_t>> metas_of(nblk);
   for (int32_t m = 0; m < (int32_t)meta_sigs.size(); ++m)
-    for (int32_t bi : meta_set[m]) metas_of_block[bi].push_back(m);
-  for (int pass = 0; pass < 10; ++pass) {
-    bool changed = false;
-    for (int32_t bi : sorted_blocks) {
-      const Block& b = blocks[bi];
-      std::vector<int32_t>& O = groups[b.group];
-      std::vector<int32_t> before = O;
-      std::stable_sort(O.begin(), O.end(), [&](int32_t x, int32_t y) {
-        const SRef rx = read_slots(ir.ops[x])[b.slot], ry = read_slots(ir.ops[y])[b.slot];
-        const int32_t px = st.pos[rx.sig], py = st.pos[ry.sig];
-        if (px != py) return px < py;
-        return rx.start < ry.start;
-      });
-      if (O != before) changed = true;
-      for (int32_t cbi : group_blocks[b.group]) {
-        const Block& cb = blocks[cbi];
-        // signals of cb in the new operator order
-        std::vector<int32_t> seq;
-        std::set<int32_t> seen;
-        for (int32_t oi : O) {
-          int32_t sig = read_slots(ir.ops[oi])[cb.slot].sig;
-          if (seen.insert(sig).second) seq.push_back(sig);
-        }
-        std::vector<int32_t> rank(0);
-        std::map<int32_t, int32_t> rk;
-        for (int32_t i = 0; i < (int32_t)seq.size(); ++i) rk[seq[i]] = i;
-        for (int32_t m : metas_of_block[cbi]) {
-          const auto& msigs = meta_sigs[m];
-          std::vector<int32_t> positions;
-          for (int32_t sig : msigs) positions.push_back(st.pos[sig]);
-          std::sort(positions.begin(), positions.end());
-          std::vector<int32_t> now(msigs.size());
-          for (size_t i = 0; i < positions.size(); ++i) now[i] = st.order[cb.base][positions[i]];
-          std::vector<int32_t> want = now;
-          std::stable_sort(want.begin(), want.end(), [&](int32_t x, int32_t y) { return rk[x] < rk[y]; });
-          if (want != now) {
-            changed = true;
-            for (size_t i = 0; i < positions.size(); ++i) {
-              st.order[cb.base][positions[i]] = want[i];
-              st.pos[want[i]] = positions[i];
-            }
-          }
-        }
+    for (int32_t bi : meta_set[m]) metas_of[bi].push_back(m);
+  auto read_of = [&](int32_t op, int32_t slot) { return read_slots(ir.ops[op])[slot]; };
+  auto ops_follow_layout = [&](const Block& b) {
+    std::vector<int32_t>& ops = groups[b.group];
+    std::stable_sort(ops.begin(), ops.end(), [&](int32_t x, int32_t y) {
+      const SRef rx = read_of(x, b.slot), ry = read_of(y, b.slot);
+      return std::make_pair(st.pos[rx.sig], rx.start) < std::make_pair(st.pos[ry.sig], ry.start);
+    });
+  };
+  auto signals_follow_ops = [&](int32_t bi) {
+    const Block& c = blocks[bi];
+    std::map<int32_t, int32_t> rank;   // signal -> first operator (in group order) reading it
+    for (int32_t op : groups[c.group]) rank.emplace(read_of(op, c.slot).sig, (int32_t)rank.size());
+    for (int32_t m : metas_of[bi]) {
+      std::vector<int32_t> spots, sigs = meta_sigs[m];
+      for (int32_t sig : sigs) spots.push_back(st.pos[sig]);
+      std::sort(spots.begin(), spots.end());
+      std::sort(sigs.begin(), sigs.end(), [&](int32_t x, int32_t y) { return rank.at(x) < rank.at(y); });
+      for (size_t i = 0; i < spots.size(); ++i) {
+        st.order[c.base][spots[i]] = sigs[i];
+        st.pos[sigs[i]] = spots[i];
       }
     }
-    if (!changed) break;
+  };
+  for (int pass = 0; pass < 10; ++pass) {
+    const auto groups_before = groups;
+    const auto order_before = st.order;
+    for (int32_t bi : visit) {
+      ops_follow_layout(blocks[bi]);
+      for (int32_t other : group_blocks[blocks[bi].group]) signals_follow_ops(other);
+    }
+    if (groups == groups_before && st.order == order_before) break;
   }
 }
 
