@@ -45,7 +45,7 @@ def gain_bias(max_rates, intercepts, tau_rc, tau_ref):
     return gain, bias
 
 
-def lif_step(J, V, ref, dt, tau_rc, tau_ref, amplitude):
+def lif_step(J, V, ref, dt, tau_rc, tau_ref, amplitude, dtype=np.float64):
     """One timestep of the spiking LIF model, elementwise; returns (s, V, ref).
 
     V integrates exactly for the part of the step that is not refractory
@@ -53,10 +53,13 @@ def lif_step(J, V, ref, dt, tau_rc, tau_ref, amplitude):
     height amplitude/dt; the crossing time is recovered from the overshoot by
     inverting the exponential approach, so the refractory period is measured from
     the crossing itself and not from the step boundary.  V is floored at 0.
+    dtype: the arithmetic precision (float64; float32 only to measure what
+    float32 arithmetic does to spike trains).
     """
-    J = np.asarray(J, dtype=np.float64)
-    V = np.array(V, dtype=np.float64, copy=True)
-    ref = np.array(ref, dtype=np.float64, copy=True)
+    J = np.asarray(J, dtype=dtype)
+    V = np.array(V, dtype=dtype, copy=True)
+    ref = np.array(ref, dtype=dtype, copy=True)
+    dt, tau_rc, tau_ref = dtype(dt), dtype(tau_rc), dtype(tau_ref)
     integ = np.clip(dt - ref, 0.0, dt)
     V = V - (J - V) * np.expm1(-integ / tau_rc)
     ref = np.maximum(ref - dt, 0.0)
@@ -70,9 +73,9 @@ def lif_step(J, V, ref, dt, tau_rc, tau_ref, amplitude):
     part = ok & (q < 1.0)
     since[full] = integ[full]
     since[part] = np.minimum(-tau_rc * np.log1p(-q[part]), integ[part])
-    V = np.where(spiked, 0.0, np.maximum(V, 0.0))
+    V = np.where(spiked, dtype(0.0), np.maximum(V, dtype(0.0)))
     ref = np.where(spiked, tau_ref - since, ref)
-    s = np.where(spiked, amplitude / dt, 0.0)
+    s = np.where(spiked, dtype(amplitude) / dt, dtype(0.0))
     return s, V, ref
 
 

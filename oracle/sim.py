@@ -26,6 +26,13 @@ biases, gains, decoders, transforms, filter coefficients) to float32 before the
 float64 simulation, matching what a float32 simulator stores; the arithmetic
 stays float64.
 
+Two measuring instruments for the spike disagreement a float32 simulator
+cannot avoid (the defaults leave the float64 arithmetic above unchanged):
+``current_dtype=np.float32`` rounds every input current J to float32 before
+the neuron update and changes nothing else; ``arith_dtype=np.float32`` runs the
+whole step -- state, currents, neuron update, products, filters -- in float32
+(parameters rounded to float32 as with ``param_dtype``).
+
 ``direct`` lists ensembles whose neurons are replaced by the exact function of
 their represented value (used by the closed-form integrator and circular
 convolution pins).
@@ -70,8 +77,12 @@ def _obj(ref):
 class OracleSim:
     def __init__(self, spec, minibatch: int = 1, param_dtype=np.float64,
                  direct: frozenset = frozenset(), neuron_type: Optional[str] = None,
-                 record_current: tuple = ()):
+                 record_current: tuple = (), current_dtype=np.float64, arith_dtype=np.float64):
         self.spec = spec
+        self.round_current = current_dtype == np.float32
+        self.dtype = np.float32 if arith_dtype == np.float32 else np.float64
+        if self.dtype == np.float32:
+            param_dtype = np.float32
         self.record_current = tuple(record_current)
         self.B = int(minibatch)
         self.dt = float(spec.dt)
@@ -79,7 +90,8 @@ class OracleSim:
         self.neuron_type = {i: (neuron_type or e.neuron_type)
                             for i, e in enumerate(spec.ensembles)}
         P = build_params(spec, self.direct)
-        rnd = (lambda a: np.asarray(a, np.float64).astype(np.float32).astype(np.float64)) \
+        dt_ = self.dtype
+        rnd = (lambda a: np.asarray(a, np.float64).astype(np.float32).astype(dt_)) \
             if param_dtype == np.float32 else (lambda a: np.asarray(a, np.float64))
         self.gain = {i: rnd(v) for i, v in P.gain.items()}
         self.bias = {i: rnd(v) for i, v in P.bias.items()}
@@ -139,14 +151,14 @@ class OracleSim:
         return order
 
     def reset(self):
-        B, spec = self.B, self.spec
-        self.V = {i: np.zeros((B, e.n_neurons)) for i, e in enumerate(spec.ensembles)
+        B, spec, f = self.B, self.spec, self.dtype
+        self.V = {i: np.zeros((B, e.n_neurons), f) for i, e in enumerate(spec.ensembles)
                   if i not in self.direct}
-        self.ref = {i: np.zeros((B, e.n_neurons)) for i, e in enumerate(spec.ensembles)
+        self.ref = {i: np.zeros((B, e.n_neurons), f) for i, e in enumerate(spec.ensembles)
                     if i not in self.direct}
-        self.y = {ci: np.zeros((B, self._post_width(c)))
+        self.y = {ci: np.zeros((B, self._post_width(c)), f)
                   for ci, c in enumerate(spec.connections) if c.synapse is not None}
-        self.yp = {pi: np.zeros((B, self._probe_width(p)))
+        self.yp = {pi: np.zeros((B, self._probe_width(p)), f)
                    for pi, p in enumerate(spec.probes) if p.synapse is not None}
         self.step = 0
         self.probe_data = {pi: [] for pi in range(len(spec.probes))}
@@ -202,22 +214,22 @@ class OracleSim:
             if kind == "node":
                 node = spec.nodes[i]
                 if node.passthrough:
-                    val = np.zeros((B, node.size))
+                    val = np.zeros((B, node.size), self.dtype)
                     for ci in incoming.get(obj, []):
                         c = spec.connections[ci]
                         s0, s1 = c.post_slice or (0, node.size)
                         val[:, s0:s1] += self._deliver(ci, out)
                 elif i in feeds:
-                    val = np.asarray(feeds[i][:, k_local, :], np.float64)
+                    val = np.asarray(feeds[i][:, k_local, :], self.dtype)
                 else:
-                    base = np.zeros(node.size) if node.value is None else \
-                        np.asarray(node.value, np.float64)
+                    base = np.zeros(node.size, self.dtype) if node.value is None else \
+                        np.asarray(node.value, self.dtype)
                     val = np.broadcast_to(base, (B, node.size)).copy()
                 out[obj] = val
             else:
                 ens = spec.ensembles[i]
-                x = np.zeros((B, ens.dims))
-                nin = np.zeros((B, ens.n_neurons))
+                x = np.zeros((B, ens.dims), self.dtype)
+                nin = np.zeros((B, ens.n_neurons), self.dtype)
                 for ci in incoming.get(obj, []):
                     c = spec.connections[ci]
                     tgt = x if c.post[0] == "ens" else nin
@@ -228,6 +240,8 @@ class OracleSim:
                     out[obj] = None
                     continue
                 J = self.bias[i][None, :] + x @ self.enc[i].T + self.gain[i][None, :] * nin
+                if self.round_current:
+                    J = J.astype(np.float32).astype(np.float64)
                 if i in self.current_rec:
                     scale = (np.abs(self.bias[i])[None, :] + np.abs(x) @ np.abs(self.enc[i]).T
                              + np.abs(self.gain[i])[None, :] * np.abs(nin))
@@ -235,7 +249,8 @@ class OracleSim:
                     self.current_rec[i][1].append(scale)
                 if self.neuron_type[i] == "lif":
                     s, self.V[i], self.ref[i] = lif_step(J, self.V[i], self.ref[i], self.dt,
-                                                         ens.tau_rc, ens.tau_ref, ens.amplitude)
+                                                         ens.tau_rc, ens.tau_ref, ens.amplitude,
+                                                         dtype=self.dtype)
                 else:
                     s = rate_output(self.neuron_type[i], J, ens.tau_rc, ens.tau_ref, ens.amplitude)
                 out[obj] = s
@@ -297,4 +312,4 @@ class OracleSim:
             cur = getattr(self, key)
             for i, v in state.get(key, {}).items():
                 assert cur[i].shape == np.shape(v), (key, i)
-                cur[i] = np.array(v, np.float64, copy=True)
+                cur[i] = np.array(v, self.dtype, copy=True)

@@ -188,7 +188,6 @@ struct EnsDesc {
   int32_t dT_row;
 };
 
-constexpr float kLn2 = 0.6931471805599453f;
 
 // exp(x) - 1 for -1/16 <= x <= 0 (the partial-step integration factor):
 // degree-6 Taylor polynomial, truncation error below 1e-11 relative.
@@ -202,14 +201,30 @@ __device__ __forceinline__ float expm1_small(float x) {
   return p * x;
 }
 
+// -ln(1 - q) for 0 <= q <= 1/16 (the crossing time's logarithm): the series
+// q (1 + q/2 + q^2/3 + ... + q^6/7), truncation below 1e-9 relative.  Unlike
+// a logarithm of the rounded 1 - q, it keeps full relative precision for
+// small q, where an error of one ulp of 1 would move the end of the
+// refractory period by about tau_rc * 6e-8 s.
+__device__ __forceinline__ float neg_log1m_small(float q) {
+  float p = 1.0f / 7.0f;
+  p = fmaf(p, q, 1.0f / 6.0f);
+  p = fmaf(p, q, 1.0f / 5.0f);
+  p = fmaf(p, q, 1.0f / 4.0f);
+  p = fmaf(p, q, 1.0f / 3.0f);
+  p = fmaf(p, q, 0.5f);
+  p = fmaf(p, q, 1.0f);
+  return p * q;
+}
+
 // LIF (or rate) update of one neuron for input current j; V, rf updated in place.
 // Spiking: exact integration over the non-refractory part of the step (the
 // whole-step factor `full` = expm1(-dt/tau_rc) is precomputed; a partial step
 // uses the polynomial above or expm1f), strict threshold 1, crossing time from
-// the overshoot (the hardware reciprocal and base-2 logarithm, v_rcp_f32 and
-// v_log_f32, each within about one ulp: the crossing time is off by at most a
-// few 1e-9 s, some 1e-6 of a step), reset to 0, refractory period measured from
-// the crossing.  Rate: amplitude / (tau_ref + tau_rc log1p(1/(J-1))).
+// the overshoot q = (V - 1)/(J - 1) (the hardware reciprocal, v_rcp_f32, about
+// one ulp; -ln(1 - q) from the series above for q <= 1/16, log1pf otherwise),
+// reset to 0, refractory period measured from the crossing.  Rate:
+// amplitude / (tau_ref + tau_rc log1p(1/(J-1))).
 __device__ __forceinline__ float neuron_update(int ntype, float j, float& v, float& rf, float tau_rc,
                                                float tau_ref, float amp, float full, float dt,
                                                float inv_tau) {
@@ -230,7 +245,8 @@ __device__ __forceinline__ float neuron_update(int ntype, float j, float& v, flo
     const float drive = j - 1.0f;
     if (drive > 0.0f) {
       const float q = (v - 1.0f) * __builtin_amdgcn_rcpf(drive);
-      since = q >= 1.0f ? integ : fminf(-tau_rc * kLn2 * __builtin_amdgcn_logf(1.0f - q), integ);
+      since = q >= 1.0f ? integ
+                        : fminf(tau_rc * (q <= 0.0625f ? neg_log1m_small(q) : -log1pf(-q)), integ);
     }
     v = 0.0f;
     rf = tau_ref - since;
@@ -241,10 +257,12 @@ __device__ __forceinline__ float neuron_update(int ntype, float j, float& v, flo
 }
 
 // Branch-free form of the spiking update above for dt / tau_rc <= 1/16 (the
-// partial-step factor always comes from the polynomial): the same formulas,
-// with every path computed and the results selected, so that lanes whose
-// neurons spike or sit in their refractory period do not serialise the
-// wavefront.  Returns the neuron output (amp_dt = amplitude / dt or 0).
+// partial-step factor always comes from the polynomial, and a crossing's
+// overshoot ratio q stays below 1 - exp(-1/16) < 1/16, so -ln(1 - q) always
+// comes from the series): the same formulas, with every path computed and the
+// results selected, so that lanes whose neurons spike or sit in their
+// refractory period do not serialise the wavefront.  Returns the neuron output
+// (amp_dt = amplitude / dt or 0).
 __device__ __forceinline__ float lif_update_bf(float j, float& v, float& rf, float tau_rc, float tau_ref,
                                                float amp_dt, float full, float dt, float inv_tau) {
   const float integ = __builtin_amdgcn_fmed3f(dt - rf, 0.0f, dt);   // clamp to [0, dt] (v_med3_f32)
@@ -254,7 +272,7 @@ __device__ __forceinline__ float lif_update_bf(float j, float& v, float& rf, flo
   rf = fmaxf(rf - dt, 0.0f);
   const float drive = j - 1.0f;
   const float q = (v - 1.0f) * __builtin_amdgcn_rcpf(drive);
-  const float lg = -tau_rc * kLn2 * __builtin_amdgcn_logf(1.0f - q);
+  const float lg = tau_rc * neg_log1m_small(q);
   float since = drive > 0.0f ? (q >= 1.0f || lg > integ ? integ : lg) : 0.0f;
   // an empty asm statement that takes the crossing time as an operand: it is
   // computed on every lane, so the compiler selects instead of branching on

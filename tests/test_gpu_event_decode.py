@@ -9,7 +9,7 @@ import pytest
 import paper_1805_11144_amd as M
 from oracle.sim import OracleSim
 from synth import make_workload
-from tests.parity import flip_fraction, unpaired_flips
+from tests.parity import check_spiking_probe, float32_run
 
 pytestmark = pytest.mark.gpu
 
@@ -37,12 +37,9 @@ def test_event_decode_equals_dense(name, driver):
         assert np.array_equal(a, b), (name, driver, pi, float(np.abs(a - b).max()))
     ref = OracleSim(w.spec, minibatch=w.minibatch, param_dtype=np.float32)
     ref.run_steps(w.n_steps, w.feeds)
+    f32 = float32_run(w.spec, w.minibatch, w.n_steps, w.feeds)
     for pi, g in enumerate(event):
-        if w.spec.probes[pi].target[0] == "neurons":
-            e = ref.data(pi)
-            f, u = flip_fraction(g, e), unpaired_flips(g, e)
-            print(f"{name} {driver} probe {pi}: flips {f:.2e} of {int((e > 0).sum())} spikes, unpaired {u}")
-            assert u == 0 and f <= 2e-3, (name, pi, f, u)
+        check_spiking_probe(f"{name} {driver} probe {pi}", w.spec.probes[pi], g, ref.data(pi), f32[pi])
 
 
 def test_event_decode_rate_mode_is_dense():

@@ -2,29 +2,31 @@
 benchmark times (driver chosen by the library).  C4 compares a sample of batch
 rows (batch rows are independent); C5 the first steps of the full network.
 
+Over a whole run, float32 arithmetic by itself makes results drift from the
+float64 oracle: a spike moved across threshold shifts every downstream
+filtered value by a spike, and near-threshold rate neurons (gains of 1e4-1e5)
+turn float32 rounding of their input into large rate changes.  The oracle run
+in float32 arithmetic on the same inputs measures that floor (measured on the
+CPU: circular convolution 1.3e-4 of spikes flipped and 1.1e-2 on the output
+probe; classifier 4.1e-4 flips in layer 2 and 0.69 on the readout, of a 9.2
+peak; wide array 8 rows x 200 steps 11% flips at the chain's end, none in
+the first 100 steps).  So spiking probes are held to the stated bound -- 1e-4 of
+the spikes flipped, 1e-3 absolute on decoded and filtered probes -- or to twice
+the float32 floor, whichever is larger (tests/parity.py).  Rate-mode decoded
+and node probes are held to 1e-5 of the peak plus the running error band of
+float32 evaluation (tests/error_band.py: the float32 rounding of every current,
+rate, product, filter and sum, propagated through the run); rate-mode neuron
+probes take the backward-error test.
 Strict per-step parity at these sizes is asserted along the GPU's own
-trajectory (one oracle step from the GPU's state at sampled steps).  Over a
-whole run two effects of float32 evaluation accumulate and are bounded here
-instead:
-  * rate mode: neurons with intercepts close to the radius have gains of 1e4
-    to 1e5, so float32 rounding of their input moves their rate by far more
-    than 1e-5 of the peak rate.  Neuron probes are checked with the
-    backward-error test (exact rate of a current within 1e-4 of its term
-    scale: one step holds 1e-5, but a second layer's current also carries the
-    first layer's rate errors through a 1024-wide sum); decoded probes are
-    held to 1e-4 relative (measured: 4.5e-5 for the circular-convolution net,
-    5.9e-5 for the classifier).
-  * spiking: a spike moved across threshold by rounding perturbs every
-    downstream ensemble by a whole spike, so spike trains of large networks
-    diverge (chaos).  Whole runs check validity (every output is 0 or
-    amplitude/dt) and population rates within 2%; flips are reported."""
+trajectory (tests/test_gpu_shadow.py)."""
 import numpy as np
 import pytest
 
 import paper_1805_11144_amd as M
 from oracle.sim import OracleSim
 from synth import make_workload
-from tests.parity import flip_fraction, lif_rate_inverse_ok, rel_err, unpaired_flips
+from tests.parity import (check_rate_probe, check_spiking_probe, flip_fraction, float32_run,
+                          lif_rate_inverse_ok, rel_err, unpaired_flips)
 
 pytestmark = pytest.mark.gpu
 
@@ -51,18 +53,49 @@ def oracle_run(w, n_steps=None, rows=None):
     return [ref.data(p) for p in range(len(w.spec.probes))], cur
 
 
-def check(w, got, oracle_out, spiking):
+def floor_run(w, n_steps=None, rows=None):
+    """The oracle run in float32 arithmetic on the same inputs."""
+    n = n_steps or w.n_steps
+    feeds = {k: (f if rows is None else f[rows]) for k, f in w.feeds.items()}
+    return float32_run(w.spec, w.minibatch if rows is None else len(rows), n, feeds)
+
+
+def band_run(w, n_steps=None, rows=None):
+    """Rate-mode error band of every probe on the same inputs (BandSim)."""
+    from tests.error_band import BandSim
+    n = n_steps or w.n_steps
+    feeds = {k: (f if rows is None else f[rows])[:, :n] for k, f in w.feeds.items()}
+    b = BandSim(w.spec, minibatch=w.minibatch if rows is None else len(rows))
+    b.run_steps(n, feeds)
+    return [b.band(p) for p in range(len(w.spec.probes))]
+
+
+def check_band(tag, got, exp, band):
+    """|gpu - oracle| within the error band plus 1e-5 of the probe's peak."""
+    dev = np.abs(np.asarray(got, np.float64) - exp)
+    lim = band + 1e-5 * np.abs(exp).max(initial=0.0)
+    print(f"{tag}: rel {rel_err(got, exp):.2e}; deviation / (band + 1e-5 peak) at most "
+          f"{float((dev / np.maximum(lim, 1e-300)).max()):.2e}")
+    assert np.all(dev <= lim), (tag, float((dev - lim).max()))
+
+
+def check(w, got, oracle_out, spiking, f32=None, bounded=True, band=None):
+    """bounded: hold spiking runs to the whole-run bounds (feedforward models);
+    otherwise (recurrent, chaotic) report them and check validity only."""
     exp, cur = oracle_out
     for pi, (g, e) in enumerate(zip(got, exp)):
         p = w.spec.probes[pi]
         if spiking and p.target[0] == "neurons":
-            f, u = flip_fraction(g, e), unpaired_flips(g, e)
             height = np.float32(w.spec.ensembles[p.target[1]].amplitude / w.spec.dt)
             ng, ne = int((g > 0).sum()), int((e > 0).sum())
-            print(f"{w.name} probe {pi}: flips {f:.2e} of {ne} spikes, unpaired {u}, "
-                  f"spike count {ng} vs {ne}")
             assert np.all((g == 0) | np.isclose(g, height, rtol=1e-6, atol=0))
-            assert abs(ng - ne) <= 0.02 * ne
+            if bounded:
+                check_spiking_probe(f"{w.name} probe {pi}", p, g, e, f32[pi])
+            else:
+                print(f"{w.name} probe {pi}: flips {flip_fraction(g, e):.2e} of {ne} spikes "
+                      f"(float32 floor {flip_fraction(f32[pi], e):.2e}), unpaired {unpaired_flips(g, e)}, "
+                      f"spike count {ng} vs {ne}")
+                assert abs(ng - ne) <= 0.02 * ne
         elif not spiking and p.target[0] == "neurons" and p.synapse is None:
             ens = w.spec.ensembles[p.target[1]]
             J, S = cur[p.target[1]]
@@ -74,41 +107,55 @@ def check(w, got, oracle_out, spiking):
             print(f"{w.name} probe {pi}: rel {rel_err(g, e):.2e}; {nf} elements outside the forward "
                   f"bound, {bad5} / {bad} outside the backward bound at 1e-5 / 1e-4")
             assert bad == 0
+        elif not spiking and band is not None:
+            check_band(f"{w.name} probe {pi}", g, e, band[pi])
         elif not spiking:
-            r = rel_err(g, e)
-            print(f"{w.name} probe {pi}: rel {r:.2e}")
-            assert r <= 1e-4
+            check_rate_probe(f"{w.name} probe {pi}", g, e, f32[pi])
+        elif bounded:
+            check_spiking_probe(f"{w.name} probe {pi}", p, g, e, f32[pi])
         else:
-            print(f"{w.name} probe {pi}: abs {float(np.abs(g - e).max()):.2e} (after spike flips)")
+            print(f"{w.name} probe {pi}: abs {float(np.abs(g - e).max()):.2e} (float32 floor "
+                  f"{float(np.abs(f32[pi] - e).max()):.2e})")
             assert np.all(np.isfinite(g))
+
+
+def _full(name, neuron_type, n=None, rows=None):
+    """The whole benchmark run on the GPU; the oracle (and, in rate mode, the
+    error band) on the given batch rows (batch rows are independent)."""
+    w = make_workload(name, neuron_type=neuron_type)
+    spiking = neuron_type == "lif"
+    got = gpu_run(w, n, rows)
+    check(w, got, oracle_run(w, n, rows), spiking, floor_run(w, n, rows) if spiking else None,
+          band=None if spiking else band_run(w, n, rows))
 
 
 @pytest.mark.timeout(600)
 @pytest.mark.parametrize("neuron_type", ["lif_rate", "lif"])
 def test_c2_full(neuron_type):
-    w = make_workload("c2", neuron_type=neuron_type)
-    check(w, gpu_run(w), oracle_run(w), neuron_type == "lif")
+    _full("c2", neuron_type, rows=None if neuron_type == "lif" else np.arange(0, 64, 9)[:8])
 
 
 @pytest.mark.timeout(600)
 @pytest.mark.parametrize("neuron_type", ["lif_rate", "lif"])
 def test_c3_full(neuron_type):
-    w = make_workload("c3", neuron_type=neuron_type)
-    check(w, gpu_run(w), oracle_run(w), neuron_type == "lif")
+    _full("c3", neuron_type, rows=None if neuron_type == "lif" else np.arange(0, 256, 37)[:8])
 
 
 @pytest.mark.timeout(900)
+@pytest.mark.parametrize("n", [100, 500])
 @pytest.mark.parametrize("neuron_type", ["lif_rate", "lif"])
-def test_c4_full_batch_sampled_rows(neuron_type):
-    w = make_workload("c4", neuron_type=neuron_type)
-    rows = np.arange(0, 512, 73)[:8]
-    n = 200
-    check(w, gpu_run(w, n, rows), oracle_run(w, n, rows), neuron_type == "lif")
+def test_c4_full_batch_sampled_rows(neuron_type, n):
+    """8 of the 512 batch rows, the first 100 steps (no spike moves in the
+    float32 oracle there: the stated spiking bounds apply as they are) and
+    the whole 500-step run."""
+    _full("c4", neuron_type, n, np.arange(0, 512, 73)[:8])
 
 
 @pytest.mark.timeout(1200)
 def test_c5_full_first_steps():
+    """Recurrent (chaotic once a spike moves): whole-run flips are reported
+    with the float32 floor, and outputs checked for validity."""
     w = make_workload("c5", neuron_type="lif")
     n = 40
     got, exp = gpu_run(w, n), oracle_run(w, n)
-    check(w, got, exp, True)
+    check(w, got, exp, True, floor_run(w, n), bounded=False)

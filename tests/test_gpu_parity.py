@@ -1,14 +1,16 @@
 """GPU parity: the HIP simulator against the float64 oracle on the same seeded
 inputs, through the C ABI.  Tolerances: rate mode max|gpu - oracle| /
 max|oracle| <= 1e-5 per probe; spiking mode spike flips <= 1e-4 of oracle spikes
-and filtered decoded probes within 1e-3 absolute."""
+and decoded / filtered probes within 1e-3 absolute -- or, where float32
+arithmetic itself moves spikes over a run, twice what the oracle run in float32
+arithmetic deviates (tests/parity.py: check_spiking_probe)."""
 import numpy as np
 import pytest
 
 import paper_1805_11144_amd as M
 from oracle.sim import OracleSim
 from synth import make_workload
-from tests.parity import flip_fraction, rel_err, unpaired_flips
+from tests.parity import check_spiking_probe, float32_run, rel_err
 
 pytestmark = pytest.mark.gpu
 
@@ -75,24 +77,24 @@ def test_relu_parity(name, driver, fuse):
 @pytest.mark.parametrize("driver", list(DRIVERS))
 @pytest.mark.parametrize("name", list(SMALL))
 def test_spiking_mode_parity(name, driver):
-    """Small models: every spike disagreement must be a one-step shift (the
-    signature of float32-vs-float64 rounding at the threshold) and rare; the
-    1e-4 flip bound itself is asserted at full sizes, where the spike count can
-    resolve it."""
+    """Whole runs of the small models: spike flips and every decoded or
+    filtered probe held to the benchmark spec bounds (1e-4 of the spikes, 1e-3
+    absolute), or to twice the float32-arithmetic oracle's deviation where
+    that is larger (at these sizes it is zero: no spike moves)."""
     skip_unsupported(name, driver)
     w = make_workload(name, neuron_type="lif", **SMALL[name])
     got = run_gpu(w, driver=DRIVERS[driver], unroll=7)
     exp = run_oracle(w)
-    for pi, (g, e) in enumerate(zip(got, exp)):
-        p = w.spec.probes[pi]
-        if p.target[0] == "neurons":
-            f = flip_fraction(g, e)
-            u = unpaired_flips(g, e)
-            print(f"{name} {driver} probe {pi}: flips {f:.2e} of {int((e > 0).sum())} spikes, unpaired {u}")
-            assert u == 0 and f <= 2e-3, (name, driver, pi, f, u)
-        else:
-            d = float(np.abs(g - e).max())
-            print(f"{name} {driver} probe {pi}: abs {d:.2e}")
+    f32 = float32_run(w.spec, w.minibatch, w.n_steps, w.feeds)
+    for pi, (g, e, f) in enumerate(zip(got, exp, f32)):
+        check_spiking_probe(f"{name} {driver} probe {pi}", w.spec.probes[pi], g, e, f)
+
+
+def _spiking_whole_run(w, got):
+    exp = run_oracle(w)
+    f32 = float32_run(w.spec, w.minibatch, w.n_steps, w.feeds)
+    for pi, (g, e, f) in enumerate(zip(got, exp, f32)):
+        check_spiking_probe(f"{w.name} probe {pi}", w.spec.probes[pi], g, e, f)
 
 
 @pytest.mark.parametrize("name", sorted(RECURRENT))
@@ -114,25 +116,16 @@ def test_window_product_kernels(neuron_type):
     w = make_workload("c3", neuron_type=neuron_type, n_steps=20, minibatch=12, n_hidden=300, n_in=136)
     got = run_gpu(w, driver=M.DRIVER_WINDOW, unroll=7)
     if neuron_type == "lif_rate":
-        from tests.test_gpu_fullsize import check, oracle_run
+        from tests.test_gpu_fullsize import check, floor_run, oracle_run
         out = oracle_run(w)
         for pi, (g, e) in enumerate(zip(got, out[0])):
             if w.spec.probes[pi].target[0] != "neurons":
                 r = rel_err(g, e)
                 print(f"probe {pi}: rel {r:.2e}")
                 assert r <= 1e-5, (pi, r)
-        check(w, got, out, False)
+        check(w, got, out, False, floor_run(w))
         return
-    exp = run_oracle(w)
-    for pi, (g, e) in enumerate(zip(got, exp)):
-        if w.spec.probes[pi].target[0] == "neurons":
-            f, u = flip_fraction(g, e), unpaired_flips(g, e)
-            print(f"probe {pi}: flips {f:.2e} of {int((e > 0).sum())} spikes, unpaired {u}")
-            assert u == 0 and f <= 2e-3, (pi, f, u)
-        else:
-            d = float(np.abs(g - e).max())
-            print(f"probe {pi}: abs {d:.2e}")
-            assert d <= 1e-3, (pi, d)
+    _spiking_whole_run(w, got)
 
 
 @pytest.mark.parametrize("neuron_type", ["lif_rate", "lif"])
@@ -145,21 +138,15 @@ def test_window_ensembles_weights_in_registers(neuron_type):
     w = make_workload("c4", neuron_type=neuron_type, n_steps=40, minibatch=2, n_ens=3, n_neurons=300,
                       n_eval=300)
     got = run_gpu(w, driver=M.DRIVER_WINDOW)
+    if neuron_type == "lif":
+        _spiking_whole_run(w, got)
+        return
     exp = run_oracle(w)
     for pi, (g, e) in enumerate(zip(got, exp)):
-        if neuron_type == "lif_rate":
-            if w.spec.probes[pi].target[0] != "neurons":
-                r = rel_err(g, e)
-                print(f"probe {pi}: rel {r:.2e}")
-                assert r <= 1e-5, (pi, r)
-        elif w.spec.probes[pi].target[0] == "neurons":
-            f, u = flip_fraction(g, e), unpaired_flips(g, e)
-            print(f"probe {pi}: flips {f:.2e} of {int((e > 0).sum())} spikes, unpaired {u}")
-            assert u == 0 and f <= 2e-3, (pi, f, u)
-        else:
-            d = float(np.abs(g - e).max())
-            print(f"probe {pi}: abs {d:.2e}")
-            assert d <= 1e-3, (pi, d)
+        if w.spec.probes[pi].target[0] != "neurons":
+            r = rel_err(g, e)
+            print(f"probe {pi}: rel {r:.2e}")
+            assert r <= 1e-5, (pi, r)
 
 
 @pytest.mark.parametrize("neuron_type", ["lif_rate", "lif"])
@@ -177,22 +164,12 @@ def test_window_product_tail_split(neuron_type):
     readout by 2.5e-4 of its peak in the first steps, on every driver alike;
     it is held to 1e-3 against the oracle and to 1e-5 against the time-major
     driver, whose products run on other kernels.  Spiking mode: the bounds of
-    the other window-driver runs."""
-    from tests.test_gpu_fullsize import check, oracle_run
+    the whole-run bounds of the other spiking runs."""
+    from tests.test_gpu_fullsize import check, floor_run, oracle_run
     w = make_workload("c3", neuron_type=neuron_type, n_steps=180, minibatch=64, n_hidden=300, n_in=136)
     got = run_gpu(w, driver=M.DRIVER_WINDOW)
     if neuron_type == "lif":
-        # whole-run spiking protocol of test_spiking_mode_parity: a one-step
-        # spike shift moves the readout by a whole spike, so the filtered
-        # readout is reported here and bounded in the injected-state tests
-        exp = run_oracle(w)
-        for pi, (g, e) in enumerate(zip(got, exp)):
-            if w.spec.probes[pi].target[0] == "neurons":
-                f, u = flip_fraction(g, e), unpaired_flips(g, e)
-                print(f"probe {pi}: flips {f:.2e} of {int((e > 0).sum())} spikes, unpaired {u}")
-                assert u == 0 and f <= 2e-3, (pi, f, u)
-            else:
-                print(f"probe {pi}: abs {float(np.abs(g - e).max()):.2e}")
+        _spiking_whole_run(w, got)
         return
     ref = run_gpu(w, driver=M.DRIVER_STEPS)
     out = oracle_run(w)
@@ -204,7 +181,7 @@ def test_window_product_tail_split(neuron_type):
     neu = [pi for pi in range(len(got)) if pi not in dec]
     for pi in neu:
         assert np.array_equal(got[pi], ref[pi]), pi
-    check(w, [got[pi] if pi in neu else out[0][pi] for pi in range(len(got))], out, False)
+    check(w, [got[pi] if pi in neu else out[0][pi] for pi in range(len(got))], out, False, floor_run(w))
 
 
 BG = dict(n_steps=80, minibatch=3, D=8, n_neurons=30, n_eval=200)
@@ -215,18 +192,14 @@ BG = dict(n_steps=80, minibatch=3, D=8, n_neurons=30, n_eval=200)
 def test_basal_ganglia_parity(driver, neuron_type):
     """The basal-ganglia-shaped network (five arrays of 1-D ensembles,
     one-to-one and all-to-all array transforms, an STN-GPe loop): rate mode to
-    1e-5 of each probe's peak, spiking mode with only one-step spike shifts."""
+    1e-5 of each probe's peak, spiking mode to the whole-run spiking bounds."""
     w = make_workload("bg", neuron_type=neuron_type, **BG)
     got = run_gpu(w, driver=DRIVERS[driver], unroll=7)
+    if neuron_type == "lif":
+        _spiking_whole_run(w, got)
+        return
     exp = run_oracle(w)
     for pi, (g, e) in enumerate(zip(got, exp)):
-        if neuron_type == "lif_rate":
-            r = rel_err(g, e)
-            print(f"bg {driver} probe {pi}: rel {r:.2e}")
-            assert r <= 1e-5, (driver, pi, r)
-        elif w.spec.probes[pi].target[0] == "neurons":
-            f, u = flip_fraction(g, e), unpaired_flips(g, e)
-            print(f"bg {driver} probe {pi}: flips {f:.2e} of {int((e > 0).sum())} spikes, unpaired {u}")
-            assert u == 0 and f <= 2e-3, (driver, pi, f, u)
-        else:
-            print(f"bg {driver} probe {pi}: abs {float(np.abs(g - e).max()):.2e}")
+        r = rel_err(g, e)
+        print(f"bg {driver} probe {pi}: rel {r:.2e}")
+        assert r <= 1e-5, (driver, pi, r)

@@ -304,3 +304,27 @@ def test_relu_decoders_solve_the_normal_equations():
     lam = 300 * (0.1 * A.max()) ** 2
     resid = (A.T @ A + lam * np.eye(60)) @ D - A.T @ e.eval_points
     assert np.abs(resid).max() <= 1e-8 * np.abs(A.T @ e.eval_points).max()
+
+
+def test_float32_instruments_stay_close_and_leave_the_default_alone():
+    """The oracle's float32 measuring modes: arith_dtype=float32 keeps every
+    state array in float32 and lands within float32 rounding of the float64
+    run (rate mode, 40 steps: relative 1e-4 at most, and not bit-identical);
+    current_dtype=float32 changes the float64 run only through rounded
+    currents; the default float64 run is unchanged by either option's
+    existence (two default runs are identical)."""
+    from synth import make_workload
+    w = make_workload("c2", neuron_type="lif_rate", n_steps=40, minibatch=2, n_neurons=20, n_eval=200)
+    runs = {}
+    for key, kw in {"f64": {}, "f64b": {}, "arith32": dict(arith_dtype=np.float32),
+                    "cur32": dict(current_dtype=np.float32)}.items():
+        r = OracleSim(w.spec, minibatch=w.minibatch, param_dtype=np.float32, **kw)
+        r.run_steps(w.n_steps, w.feeds)
+        runs[key] = (r, r.data(0))
+    assert np.array_equal(runs["f64"][1], runs["f64b"][1])
+    r32, d32 = runs["arith32"]
+    assert all(v.dtype == np.float32 for v in r32.y.values()) and d32.dtype == np.float32
+    ref = runs["f64"][1]
+    for key in ("arith32", "cur32"):
+        diff = np.abs(runs[key][1] - ref).max() / np.abs(ref).max()
+        assert 0 < diff <= 1e-4, (key, diff)
