@@ -39,6 +39,8 @@ WORKLOADS = {
     "c5": "sparse graph: 5000 ensembles x 500 LIF x 16-D, fan-out 4, B=1, T=1000",
     "bg": "basal-ganglia-shaped: 5 arrays x 64 ensembles x 50 LIF (1-D), one-to-one and all-to-all "
           "array transforms, B=1, T=1000",
+    "pes": "online learning: 192-D input -> 9600 LIF -> PES-learned decoders (one 9600x192 matrix "
+           "per batch row), error lowpass 0.005, B=10, T=1000",
 }
 
 
@@ -53,8 +55,14 @@ def compulsory_bytes_per_step(w):
     for e in spec.ensembles:
         params += 4 * e.n_neurons * (1 + e.dims)               # bias + scaled encoders
     decoded = set()
+    learned = 0
     for c in spec.connections:
         params += 4 * int(np.size(c.transform))
+        if c.learning_rule is not None:
+            # per-batch-row decoders read and written every step, and the
+            # activity filter state
+            learned += pes_bytes_per_launch(spec, c, B)
+            continue
         if c.pre[0] == "ens" and (c.pre[1], c.function) not in decoded:
             decoded.add((c.pre[1], c.function))
             params += 4 * spec.ensembles[c.pre[1]].n_neurons * (1 if c.function == "product" else
@@ -62,12 +70,32 @@ def compulsory_bytes_per_step(w):
     filt = 0
     for c in spec.connections:
         if c.synapse is not None:
-            w_ = (c.post_slice[1] - c.post_slice[0]) if c.post_slice else (
-                spec.nodes[c.post[1]].size if c.post[0] == "node" else
-                spec.ensembles[c.post[1]].dims if c.post[0] == "ens" else spec.ensembles[c.post[1]].n_neurons)
+            w_ = (c.post_slice[1] - c.post_slice[0]) if c.post_slice else _post_width(spec, c)
             filt += 8 * w_ * B
     feeds = 4 * B * sum(f.shape[2] for f in w.feeds.values())
-    return state + params + filt + feeds
+    return state + params + filt + feeds + learned
+
+
+def _post_width(spec, c):
+    kind, i = c.post
+    if kind == "node":
+        return spec.nodes[i].size
+    if kind == "ens":
+        return spec.ensembles[i].dims
+    if kind == "learning":
+        lc = spec.connections[i]
+        return np.asarray(lc.decoders).shape[1] if lc.decoders is not None else spec.ensembles[lc.pre[1]].dims
+    return spec.ensembles[i].n_neurons
+
+
+def pes_bytes_per_launch(spec, c, B):
+    """Algorithmic bytes of one PES decode + update pass over one learned
+    connection (n neurons, k outputs): the decoders read and written (8 n k B),
+    the activities and their filter read (8 n B), the error read and the
+    decoded output written (8 k B)."""
+    n = spec.ensembles[c.pre[1]].n_neurons
+    k = np.asarray(c.decoders).shape[1] if c.decoders is not None else spec.ensembles[c.pre[1]].dims
+    return 8 * n * k * B + 8 * n * B + 8 * k * B
 
 
 def gemm_flops_per_step(w):
@@ -207,7 +235,7 @@ def measure_roofline(M, model, w, sim, info, feeds, bf16=False, plan_opts=None, 
     tsim.set_timing(True)
     tsim.reset()
     tsim.run_steps(T, feeds)
-    times = {t: tsim.kernel_time(t) for t in range(11)}
+    times = {t: tsim.kernel_time(t) for t in range(14)}
     tsim.set_timing(False)
     if tsim is not sim:
         tsim.close()
@@ -231,6 +259,10 @@ def measure_roofline(M, model, w, sim, info, feeds, bf16=False, plan_opts=None, 
         kernel = "k_w_gemm2" if window else "k_dot_inc"
         if bf16:
             peak, kernel = BF16_MFMA_PEAK_TFLOPS, "k_w_gemm_bf16"
+    elif top in (M.mergesim.OP_PES_DECODE_UPDATE, M.mergesim.OP_LEARNED_DECODE, M.mergesim.OP_PES):
+        work = sum(pes_bytes_per_launch(w.spec, c, w.minibatch) for c in w.spec.connections
+                   if c.learning_rule is not None) * T
+        bound, peak, unit, kernel = "hbm", HBM_PEAK_GBS, "GB/s", "k_pes"
     else:
         work, bound, peak, unit = compulsory_bytes_per_step(w) * T, "hbm", HBM_PEAK_GBS, "GB/s"
         kernel = f"op type {top}"
@@ -247,7 +279,8 @@ def measure_roofline(M, model, w, sim, info, feeds, bf16=False, plan_opts=None, 
         work = rec * n
     scale = 1e12 if unit == "TFLOP/s" else 1e9
     ach = work / (ms * 1e-3) / scale
-    op_names = {M.mergesim.OP_ENSEMBLE: "Ensemble", M.mergesim.OP_DOT_INC: "DotInc"}
+    op_names = {M.mergesim.OP_ENSEMBLE: "Ensemble", M.mergesim.OP_DOT_INC: "DotInc",
+                M.mergesim.OP_PES_DECODE_UPDATE: "PESDecodeUpdate"}
     out = {"bound": bound, "achieved": round(ach, 3), "peak": peak, "unit": unit,
            "frac": round(ach / peak, 4),
            "traffic": stored_traffic(kernel, w.name + ("event" if event else "")) if default_plan else None,

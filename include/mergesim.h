@@ -58,6 +58,8 @@ typedef struct ms_sim ms_sim;
 #define MS_REF_NODE 0     /* node output (pre) / passthrough node input (post) */
 #define MS_REF_ENS 1      /* decoded value (pre) / represented input (post)    */
 #define MS_REF_NEURONS 2  /* spike output (pre) / input current times gain (post) */
+#define MS_REF_LEARNING 3 /* post only: error input of the learning rule of
+                             connection post_id (see ms_model_set_pes) */
 
 #define MS_NEURON_LIF 0       /* spiking LIF, exact integration */
 #define MS_NEURON_LIF_RATE 1  /* LIF rate curve amplitude * r(J) */
@@ -139,6 +141,26 @@ ms_status ms_model_add_ensemble(ms_model* model, const ms_ensemble_desc* desc,
 ms_status ms_model_add_connection(ms_model* model, const ms_connection_desc* desc,
                                   int32_t* id_out);
 ms_status ms_model_add_probe(ms_model* model, const ms_probe_desc* desc, int32_t* id_out);
+
+/* Online learning with the Prescribed Error Sensitivity rule (paper Sec. 5.1,
+ * the pes benchmark: an ensemble's output weights updated as the simulation
+ * runs; Fig. 7: each batch element then needs its own weight matrix).
+ * Connection `conn_id` must decode from an ensemble (pre_kind MS_REF_ENS, no
+ * pre slice); its decoders D [n][k] (explicit, or solved for its function)
+ * become the initial value of per-batch-element decoders D^b, which every step
+ * changes by
+ *     D^b <- D^b - (learning_rate * dt / n) * outer(a^b, e^b)
+ * after the connection has decoded with them.  e^b [k] is the sum of the
+ * connections whose post is (MS_REF_LEARNING, conn_id) (a filtered one
+ * delivers its state as left by the previous step); a^b [n] is the pre
+ * neurons' output lowpass-filtered with pre_synapse_tau, as left by the
+ * previous step, or this step's output when pre_synapse_tau <= 0.  Models
+ * with learning run on the STEPS and GRAPH drivers (MS_DRIVER_AUTO picks
+ * GRAPH; PERSISTENT and WINDOW give MS_E_INVALID).  MS_E_INVALID for a
+ * connection that does not decode from neurons, has a pre slice or already
+ * learns, and for learning_rate < 0. */
+ms_status ms_model_set_pes(ms_model* model, int32_t conn_id, double learning_rate,
+                           double pre_synapse_tau);
 
 /* ---------------------------------------------------------------- options */
 
@@ -249,9 +271,11 @@ ms_status ms_plan_export_json(const ms_plan* plan, char* buf, int64_t cap, int64
 ms_status ms_plan_get_param(const ms_plan* plan, int32_t which, int32_t ensemble,
                             int32_t function, double* out, int64_t cap, int64_t* n_out);
 
-/* Copy parameter base array `base` (ids as in the JSON export; batched bases
- * are rejected) as the float32 values the simulation uses: [rows][cols]
- * row-major.  *n_out receives the element count; out == NULL sizes it. */
+/* Copy parameter base array `base` (ids as in the JSON export) as the float32
+ * values the simulation uses: [rows][cols] row-major.  For the batched state
+ * array: the value each row starts from in every batch column (zero except
+ * the learned decoders of PES connections).  *n_out receives the element
+ * count; out == NULL sizes it. */
 ms_status ms_plan_export_base(const ms_plan* plan, int32_t base, float* out, int64_t cap,
                               int64_t* n_out);
 
@@ -301,8 +325,9 @@ ms_status ms_sim_probe_read(ms_sim* sim, int32_t probe_id, float* out, int64_t c
 #define MS_PROBE_READ_STATIC_MAX (1 << 22)
 ms_status ms_sim_probe_read_static(ms_sim* sim, int32_t probe_id, float* out, int64_t cap_elems);
 
-/* Restore the initial state (V = 0, refractory 0, filters 0) and clear probes
- * (paper Sec. 3.1 sim.reset()). */
+/* Restore the initial state (V = 0, refractory 0, filters 0, learned
+ * decoders back to their initial value) and clear probes (paper Sec. 3.1
+ * sim.reset()). */
 ms_status ms_sim_reset(ms_sim* sim);
 
 /* State access for checkpoint/resume and injected-state tests.  Host buffers.
@@ -313,6 +338,9 @@ ms_status ms_sim_reset(ms_sim* sim);
 #define MS_STATE_REFRACTORY 1
 #define MS_STATE_SYNAPSE 2
 #define MS_STATE_PROBE_SYNAPSE 3
+#define MS_STATE_LEARNED_DECODERS 4  /* id = learning connection, [minibatch][n][k] (D^b) */
+#define MS_STATE_PES_ACTIVITY 5      /* id = learning connection with a pre synapse,
+                                        [minibatch][n] (a^b) */
 ms_status ms_sim_get_state(ms_sim* sim, int32_t which, int32_t id, float* out, int64_t cap_elems);
 ms_status ms_sim_set_state(ms_sim* sim, int32_t which, int32_t id, const float* in, int64_t n_elems);
 
@@ -336,6 +364,10 @@ ms_status ms_sim_info(const ms_sim* sim, int32_t* driver_out, int32_t* groups_pe
 #define MS_OP_LOWPASS 8
 #define MS_OP_ENSEMBLE 9  /* fused bias + encoders + neurons + decoders of an ensemble */
 #define MS_OP_SYNAPSE_SCATTER 10  /* fused transform + lowpass + copy into post inputs */
+#define MS_OP_LEARNED_DECODE 11   /* decoding with per-batch-element decoders */
+#define MS_OP_PES 12              /* the PES update of those decoders */
+#define MS_OP_PES_DECODE_UPDATE 13 /* both in one pass over the decoders (launch drivers,
+                                      when the error is known before the decode) */
 
 /* Per-kernel timing for measurement.  With timing on (on != 0), every kernel
  * launch of a merged group is bracketed by HIP events recorded on the stream

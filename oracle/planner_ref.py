@@ -33,8 +33,9 @@ from typing import Dict, List, Optional, Sequence, Tuple
 import numpy as np
 
 FEED, RESET, COPY, COPY_INC, ELEM_INC, DOT_INC, LIF, LIF_RATE, LOWPASS, ENS = range(10)
+BDOT_INC, PES = 11, 12          # learned decoding (per batch row) and its PES update
 TYPE_NAMES = ["Feed", "Reset", "Copy", "CopyInc", "ElementwiseInc", "DotInc", "SimLIF",
-              "SimLIFRate", "Lowpass", "Ensemble"]
+              "SimLIFRate", "Lowpass", "Ensemble", "SynapseScatter", "LearnedDotInc", "PES"]
 MAX_FUSED_DECODED = 16
 
 
@@ -114,7 +115,15 @@ def build_ir(spec) -> IR:
 
     nodes, ens, conns = spec.nodes, spec.ensembles, spec.connections
 
+    def learn_width(ci):
+        c = conns[ci]
+        if c.decoders is not None:
+            return np.asarray(c.decoders).shape[1]
+        return _fn_size(c.function, ens[c.pre[1]].dims)
+
     def width(kind, i, fn="identity"):
+        if kind == "learning":
+            return learn_width(i)
         if kind == "node":
             return nodes[i].size
         if kind == "ens":
@@ -129,7 +138,8 @@ def build_ir(spec) -> IR:
             has_x[c.post[1]] = True
         if c.post[0] == "neurons":
             has_nin[c.post[1]] = True
-        if c.pre[0] == "ens" and c.decoders is None and c.function not in fns[c.pre[1]]:
+        if c.pre[0] == "ens" and c.decoders is None and c.learning_rule is None \
+                and c.function not in fns[c.pre[1]]:
             fns[c.pre[1]].append(c.function)
     for p in spec.probes:
         if p.target[0] == "ens" and "identity" not in fns[p.target[1]]:
@@ -186,9 +196,23 @@ def build_ir(spec) -> IR:
             op(RESET, f"e{e}.reset{_fn_tag(fn)}", dst=whole(d))
             op(DOT_INC, f"e{e}.dec{_fn_tag(fn)}", dst=whole(d), a=whole(D), src=whole(S))
 
+    # error inputs of the learning rules, in connection order, before any
+    # connection's own signals
+    err = {ci: sig(f"c{ci}.E", learn_width(ci)) for ci, c in enumerate(conns) if c.learning_rule is not None}
     for ci, c in enumerate(conns):
         kind, i = c.pre
-        if kind == "node":
+        if c.learning_rule is not None:
+            n, k = ens[i].n_neurons, learn_width(ci)
+            pre = sig(f"c{ci}.xd", k)
+            W = sig(f"c{ci}.W", n * k)
+            act = sig(f"c{ci}.a", n) if c.learning_rule.pre_synapse is not None else eS[i]
+            op(RESET, f"c{ci}.resetd", dst=whole(pre))
+            op(BDOT_INC, f"c{ci}.dec", dst=whole(pre), a=whole(W), src=whole(eS[i]))
+            op(RESET, f"c{ci}.resete", dst=whole(err[ci]))
+            op(PES, f"c{ci}.pes", dst=whole(W), src=whole(act), a=whole(err[ci]))
+            if c.learning_rule.pre_synapse is not None:
+                op(LOWPASS, f"c{ci}.presyn", dst=whole(act), src=whole(eS[i]))
+        elif kind == "node":
             pre = node_out[i]
         elif kind == "neurons":
             pre = eS[i]
@@ -218,7 +242,9 @@ def build_ir(spec) -> IR:
         if y is not None:
             op(LOWPASS, f"c{ci}.synapse", dst=whole(y), src=whole(v))
         out = y if y is not None else v
-        if c.post[0] == "neurons":
+        if c.post[0] == "learning":
+            op(COPY_INC, f"c{ci}.deliver", dst=Ref(err[c.post[1]], q0, w), src=whole(out))
+        elif c.post[0] == "neurons":
             op(ELEM_INC, f"c{ci}.deliver", dst=Ref(eJ[c.post[1]], q0, w),
                a=Ref(eGain[c.post[1]], q0, w), src=whole(out))
         else:
@@ -350,6 +376,10 @@ def accesses(o: Op):
         return [o.dst.sig], [], [o.src.sig], []
     if t == LOWPASS:
         return [], [], [o.src.sig], [o.dst.sig]
+    if t == BDOT_INC:
+        return [], [o.dst.sig], [o.a.sig, o.src.sig], []
+    if t == PES:
+        return [], [], [o.src.sig, o.a.sig], [o.dst.sig]
     if t == ENS:
         sets = ([o.dst.sig] if o.dst is not None else []) + [d.sig for _, d in o.decs]
         reads = [o.src.sig] if o.src is not None else []
@@ -399,6 +429,10 @@ def merge_key(ir: IR, o: Op):
         return (t, b(o.src), b(o.dst), b(o.V), b(o.ref))
     if t == LIF_RATE:
         return (t, b(o.src), b(o.dst), o.kind)
+    if t == BDOT_INC:
+        return (t, b(o.dst), b(o.a), b(o.src), o.dst.length, o.src.length)
+    if t == PES:
+        return (t, b(o.dst), b(o.src), b(o.a), o.a.length, o.src.length)
     if t == ENS:
         bb = lambda r: -1 if r is None else ir.sigs[r.sig].base
         key = (t, o.kind, bb(o.src), bb(o.a), 0 if o.src is None else o.src.length,
@@ -497,6 +531,10 @@ def read_refs(o: Op) -> List[Ref]:
         return [o.src]
     if t == LOWPASS:
         return [o.src, o.dst]
+    if t == BDOT_INC:
+        return [o.a, o.src]
+    if t == PES:
+        return [o.src, o.a, o.dst]
     if t == ENS:
         refs = ([o.src, o.a] if o.src is not None else []) + [o.bias]
         refs += [o.V, o.ref] if o.V is not None else []
@@ -710,6 +748,15 @@ def lower_group(ir: IR, offset: Dict[int, int], g: List[int]) -> dict:
                    w_row=[offset[ir.ops[oi].a.sig] + ir.ops[oi].a.start for oi in g],
                    x_row=[row(ir.ops[oi].src, 0) for oi in g],
                    d_row=[row(ir.ops[oi].dst, 0) for oi in g])
+    elif t in (BDOT_INC, PES):
+        ops = [ir.ops[oi] for oi in g]
+        out.update(rows=len(g), M=o0.dst.length if t == BDOT_INC else o0.a.length, K=o0.src.length,
+                   w_row=[row(o.a if t == BDOT_INC else o.dst, 0) for o in ops],
+                   x_row=[row(o.src, 0) for o in ops])
+        if t == BDOT_INC:
+            out["d_row"] = [row(o.dst, 0) for o in ops]
+        else:
+            out["e_row"] = [row(o.a, 0) for o in ops]
     elif t in (LIF, LIF_RATE):
         J, S, V, R = [], [], [], []
         for oi in g:

@@ -18,8 +18,22 @@ writes to it).  Readings where the paper is silent:
   * probes sample after the filter updates; a probe synapse is a lowpass on the
     probed value
   * initial state: V = 0, refractory time 0, filter states 0
+  * PES learning (Sec. 5.1's pes benchmark; Fig. 7: one weight matrix per
+    batch row): a connection with a learning rule decodes with its own
+    decoders D^b [n, k] per batch row, initially the solved (or given)
+    decoders.  Connections into ("learning", c) sum into the rule's error
+    input e [B, k] (filtered ones deliver their state as left by the previous
+    step, like any filtered connection).  After every object has run, and
+    with the error and the activity filter read before any filter updates,
+        D^b <- D^b - (kappa * dt / n) * outer(a^b, e^b)
+    where a is the pre activity filter's state as left by the previous step
+    (a <- p a + (1 - p) s updates after the weights are read, p =
+    exp(-dt / pre_synapse)), or this step's activities s when the rule has no
+    pre_synapse.  The learned connection's own filter update reads the
+    decoders from before this step's change.
 
-Every batch row is independent; parameters are shared across the batch.
+Every batch row is independent; parameters are shared across the batch
+(learned decoders are per batch row).
 
 ``param_dtype=np.float32`` rounds every stored parameter (scaled encoders,
 biases, gains, decoders, transforms, filter coefficients) to float32 before the
@@ -69,8 +83,11 @@ def _ref_size(spec, ref) -> int:
 
 
 def _obj(ref):
-    """Object a reference belongs to (ensembles and their neurons are one object)."""
+    """Object a reference belongs to (ensembles and their neurons are one
+    object; a learning rule's error input is its own)."""
     kind, i = ref
+    if kind == "learning":
+        return ("learning", i)
     return ("node", i) if kind == "node" else ("ens", i)
 
 
@@ -113,6 +130,23 @@ class OracleSim:
                 self.conn_a.append((float(rnd(a)), float(rnd(1.0 - a))))
             else:
                 self.conn_a.append(None)
+        # learning rules: per learned connection (kappa dt / n, pre filter coefficients)
+        self.learned = [ci for ci, c in enumerate(spec.connections) if c.learning_rule is not None]
+        self.pes_coef, self.pes_a = {}, {}
+        for ci in self.learned:
+            c = spec.connections[ci]
+            if c.pre[0] != "ens" or c.pre[1] in self.direct or c.pre_slice is not None:
+                raise ValueError("a learning rule needs a decoded connection from neurons, without pre slice")
+            n = spec.ensembles[c.pre[1]].n_neurons
+            self.pes_coef[ci] = float(rnd(c.learning_rule.learning_rate * self.dt / n))
+            tau = c.learning_rule.pre_synapse
+            if tau is not None:
+                a = math.exp(-self.dt / tau)
+                self.pes_a[ci] = (float(rnd(a)), float(rnd(1.0 - a)))
+        for ci, c in enumerate(spec.connections):
+            if c.post[0] == "learning":
+                if c.post[1] not in self.pes_coef:
+                    raise ValueError("error connection into a connection without a learning rule")
         self.probe_a = []
         for p in spec.probes:
             if p.synapse is not None:
@@ -131,7 +165,7 @@ class OracleSim:
         succ: Dict[tuple, List[tuple]] = {o: [] for o in objs}
         indeg = {o: 0 for o in objs}
         for c in spec.connections:
-            if c.synapse is None:
+            if c.synapse is None and c.post[0] != "learning":
                 a, b = _obj(c.pre), _obj(c.post)
                 if a == b:
                     raise CycleError("unfiltered self-connection")
@@ -160,6 +194,10 @@ class OracleSim:
                   for ci, c in enumerate(spec.connections) if c.synapse is not None}
         self.yp = {pi: np.zeros((B, self._probe_width(p)), f)
                    for pi, p in enumerate(spec.probes) if p.synapse is not None}
+        self.W = {ci: np.broadcast_to(self.conn_dec[ci], (B,) + self.conn_dec[ci].shape).astype(f)
+                  for ci in self.learned}
+        self.abar = {ci: np.zeros((B, spec.ensembles[spec.connections[ci].pre[1]].n_neurons), f)
+                     for ci in self.learned if ci in self.pes_a}
         self.step = 0
         self.probe_data = {pi: [] for pi in range(len(spec.probes))}
         self.current_rec = {i: ([], []) for i in self.record_current}
@@ -167,6 +205,8 @@ class OracleSim:
     def _post_width(self, c) -> int:
         if c.post_slice is not None:
             return c.post_slice[1] - c.post_slice[0]
+        if c.post[0] == "learning":
+            return self.conn_dec[c.post[1]].shape[1]
         return _ref_size(self.spec, c.post)
 
     def _probe_width(self, p) -> int:
@@ -186,6 +226,8 @@ class OracleSim:
         else:
             if i in self.direct:
                 v = apply_function(c.function, out[("ens_x", i)])
+            elif ci in self.W:      # this batch row's own decoders: [B, 1, n] @ [B, n, k]
+                v = np.matmul(out[("ens", i)][:, None, :], self.W[ci])[:, 0, :]
             else:
                 v = out[("ens", i)] @ self.conn_dec[ci]
         if c.pre_slice is not None:
@@ -254,11 +296,29 @@ class OracleSim:
                 else:
                     s = rate_output(self.neuron_type[i], J, ens.tau_rc, ens.tau_ref, ens.amplitude)
                 out[obj] = s
+        # learning rules read their error input and pre activity filter
+        # before any filter moves
+        err, act = {}, {}
+        for ci in self.learned:
+            e = np.zeros((B, self.conn_dec[ci].shape[1]), self.dtype)
+            for cj in incoming.get(("learning", ci), []):
+                c = spec.connections[cj]
+                s0, s1 = c.post_slice or (0, e.shape[1])
+                e[:, s0:s1] += self._deliver(cj, out)
+            err[ci] = e
+            act[ci] = self.abar[ci] if ci in self.abar else out[("ens", spec.connections[ci].pre[1])]
         # filter updates run after every reader of the old filter state
         for ci, c in enumerate(spec.connections):
             if c.synapse is not None:
                 a, one_minus_a = self.conn_a[ci]
                 self.y[ci] = a * self.y[ci] + one_minus_a * self._conn_value(ci, out)
+        # weight changes (after the learned connections' filters read the old
+        # decoders), then the pre activity filters
+        for ci in self.learned:
+            self.W[ci] = self.W[ci] - self.pes_coef[ci] * (act[ci][:, :, None] * err[ci][:, None, :])
+            if ci in self.abar:
+                p_, one_minus_p = self.pes_a[ci]
+                self.abar[ci] = p_ * self.abar[ci] + one_minus_p * out[("ens", spec.connections[ci].pre[1])]
         # probes sample after the updates
         for pi, p in enumerate(spec.probes):
             kind, i = p.target
@@ -305,10 +365,12 @@ class OracleSim:
         return {"V": {i: v.copy() for i, v in self.V.items()},
                 "ref": {i: v.copy() for i, v in self.ref.items()},
                 "y": {i: v.copy() for i, v in self.y.items()},
-                "yp": {i: v.copy() for i, v in self.yp.items()}}
+                "yp": {i: v.copy() for i, v in self.yp.items()},
+                "W": {i: v.copy() for i, v in self.W.items()},
+                "abar": {i: v.copy() for i, v in self.abar.items()}}
 
     def set_state(self, state):
-        for key in ("V", "ref", "y", "yp"):
+        for key in ("V", "ref", "y", "yp", "W", "abar"):
             cur = getattr(self, key)
             for i, v in state.get(key, {}).items():
                 assert cur[i].shape == np.shape(v), (key, i)

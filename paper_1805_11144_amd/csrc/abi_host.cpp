@@ -1,6 +1,7 @@
 // Host half of the C ABI: model description, host-only planning and error
 // reporting.  Every entry point converts exceptions into an ms_status.
 #include <algorithm>
+#include <cmath>
 #include <cstring>
 #include <string>
 
@@ -159,7 +160,7 @@ ms_status ms_model_add_connection(ms_model* m, const ms_connection_desc* d, int3
     c.post_kind = d->post_kind; c.post_id = d->post_id;
     c.post_start = d->post_start; c.post_stop = d->post_stop;
     c.function = d->function;
-    need(c.pre_kind >= 0 && c.pre_kind <= 2 && c.post_kind >= 0 && c.post_kind <= 2, "bad reference kind");
+    need(c.pre_kind >= 0 && c.pre_kind <= 2 && c.post_kind >= 0 && c.post_kind <= 3, "bad reference kind");
     if (d->decoders) {
       need(c.pre_kind == MS_REF_ENS, "explicit decoders need an ensemble pre");
       need(c.pre_id >= 0 && c.pre_id < (int32_t)m->m.ens.size(), "ensemble id out of range");
@@ -179,6 +180,21 @@ ms_status ms_model_add_connection(ms_model* m, const ms_connection_desc* d, int3
     c.synapse = d->synapse_tau;
     m->m.conns.push_back(std::move(c));
     *id_out = (int32_t)m->m.conns.size() - 1;
+  });
+}
+
+ms_status ms_model_set_pes(ms_model* m, int32_t conn_id, double learning_rate, double pre_synapse_tau) {
+  return guarded([&] {
+    need(m != nullptr, "NULL argument");
+    need(conn_id >= 0 && conn_id < (int32_t)m->m.conns.size(), "connection id out of range");
+    ms::ConnDesc& c = m->m.conns[conn_id];
+    need(c.pre_kind == MS_REF_ENS, "a learning rule needs a connection that decodes from an ensemble");
+    need(c.pre_start == 0 && c.pre_stop == 0, "a learning connection takes no pre slice");
+    need(!c.learned, "the connection already has a learning rule");
+    need(learning_rate >= 0.0 && std::isfinite(learning_rate), "learning_rate must be finite and >= 0");
+    c.learned = true;
+    c.pes_rate = learning_rate;
+    c.pes_tau = pre_synapse_tau;
   });
 }
 
@@ -258,8 +274,7 @@ ms_status ms_plan_export_base(const ms_plan* p, int32_t base, float* out, int64_
     const ms::Plan& P = *p->p;
     const ms::IR& ir = P.ir;
     need(base >= 0 && base < (int32_t)ir.bases.size(), "base id out of range");
-    need(ir.bases[base].cls == ms::SC_PARAM, "base is not a parameter base array");
-    const int64_t cols = ir.bases[base].cols;
+    const int64_t cols = ir.bases[base].cols;   // 1 for the batched state base
     const int64_t n = P.base_rows[base] * cols;
     *n_out = n;
     if (!out) return;

@@ -51,6 +51,9 @@ struct ConnDesc {
   std::vector<double> transform;  // [rows*cols] or empty (scalar)
   double t_scalar = 1.0;
   double synapse = 0.0;           // <= 0: none
+  bool learned = false;           // PES on its decoders
+  double pes_rate = 0.0;          // kappa
+  double pes_tau = 0.0;           // pre activity filter; <= 0: none
 };
 
 struct ProbeDesc {
@@ -86,7 +89,8 @@ struct Signal {
   int32_t cols = 1;               // params: matrix width (1 for vectors)
   SigClass cls = SC_BATCHED;
   bool state = false;             // persists across steps (V, ref, filters)
-  std::vector<double> value;      // params: [rows*cols]
+  std::vector<double> value;      // params: [rows*cols]; batched state: initial value
+                                  // [rows] of every batch column (empty: zeros)
   int32_t base = -1;              // base array id (assigned by the IR builder)
 };
 
@@ -103,7 +107,10 @@ enum OpType : int32_t {
   OP_ENS = 9,           // fused ensemble: J = bias + enc x; LIF; d_f = D_f s
   OP_SYN_SCATTER = 10,  // fused connection tail (launch drivers only, never in a plan's
                         // groups): transform, lowpass update, pull into the post inputs
-  OP_NTYPES = 11
+  OP_BDOT_INC = 11,     // dst[j] += sum_i src[i] W[i*k + j], W a batched signal (per-row decoders)
+  OP_PES = 12,          // W[i*k + j] += coef * src[i] * a[j] (update: after W's readers)
+  OP_PES_FUSED = 13,    // BDOT_INC and PES of the same connections in one pass (launch drivers)
+  OP_NTYPES = 14
 };
 
 // Fused decoders of one ensemble operator are limited to this many outputs in
@@ -132,7 +139,7 @@ struct Op {
   int32_t ntype = 0;                // ENS, LIF_RATE: MS_NEURON_*
   int32_t n = 0;                    // ENS: neurons
   double tau_rc = 0, tau_ref = 0, amp = 0;  // LIF params
-  double coef_a = 0, coef_b = 0;            // LOWPASS y = coef_a y + coef_b v
+  double coef_a = 0, coef_b = 0;            // LOWPASS y = coef_a y + coef_b v; PES coef_a
 };
 
 struct BaseArray {
@@ -157,6 +164,7 @@ struct IR {
   std::vector<int32_t> ens_V, ens_ref;     // per ensemble signal id or -1
   std::vector<int32_t> conn_y;             // per connection signal id or -1
   std::vector<int32_t> probe_y;            // per probe signal id or -1
+  std::vector<int32_t> conn_W, conn_act;   // per connection: learned decoders, PES activity filter
 };
 IR build_ir(const Model& m, const Built& b, double dt);
 void simplify_ir(IR& ir);
@@ -192,6 +200,13 @@ struct LGroup {
   // DOT_INC
   int32_t M = 0, K = 0;
   std::vector<int32_t> w_row, x_row, d_row;   // per op
+  // BDOT_INC (M = k outputs, K = n neurons): per op w_row (first row of the
+  // batched decoders, row i*k + j), x_row (activities), d_row (outputs).
+  // PES: per op w_row, x_row (activities or their filter), e_row (error),
+  // coef (-kappa dt / n).  PES_FUSED: both, d_row the outputs and x_row the
+  // activities the decode reads, act_row the activities the update reads.
+  std::vector<int32_t> e_row, act_row;
+  std::vector<float> coef;
   // RESET values (empty: zeros)
   std::vector<float> values;
   // LIF / LIF_RATE parameters: uniform (size 1) or per row

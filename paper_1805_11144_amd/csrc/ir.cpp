@@ -28,6 +28,15 @@
 //        (v += T pre[slice]); LOWPASS c<c>.synapse (y <- a y + (1-a) v);
 //        c<c>.deliver: COPY_INC into x / passthrough output, or ELEM_INC
 //        (J += gain (.) value) for neuron-space posts
+//   connection with a PES rule (decodes from ensemble e, n neurons, k
+//   outputs): c<c>.xd [k] batched, c<c>.W [n*k] batched state (row i*k + j,
+//   initially the decoders), with a pre synapse c<c>.a [n] batched state;
+//     RESET c<c>.resetd, BDOT_INC c<c>.dec (xd += per-column W^T s),
+//     RESET c<c>.resete, PES c<c>.pes (W += -kappa dt / n  act (x) E, act =
+//     c<c>.a or e<e>.s), with a pre synapse LOWPASS c<c>.presyn (a <- p a +
+//     (1-p) s); its error input c<c>.E [k] batched is created, in connection
+//     order, before the first connection's signals; connections into
+//     (MS_REF_LEARNING, c) deliver into it by COPY_INC
 // Per probe p: with a synapse p<p>.y [w] batched state, LOWPASS p<p>.synapse.
 #include <algorithm>
 #include <cmath>
@@ -111,7 +120,14 @@ IR build_ir(const Model& m, const Built& bp, double dt) {
     check(kind == MS_REF_NEURONS, "bad reference kind");
     return m.ens[id].n;
   };
-  std::vector<int32_t> pre_w(nc), post_w(nc), pre_full(nc), post_full(nc);
+  std::vector<int32_t> pre_w(nc), post_w(nc), pre_full(nc), post_full(nc), learn_k(nc, 0);
+  for (int32_t ci = 0; ci < nc; ++ci) {
+    const ConnDesc& c = m.conns[ci];
+    if (!c.learned) continue;
+    check(c.pre_kind == MS_REF_ENS && c.pre_id >= 0 && c.pre_id < ne, "a learning connection decodes from an ensemble");
+    check(c.pre_start == 0 && c.pre_stop == 0, "a learning connection takes no pre slice");
+    learn_k[ci] = c.decoders.empty() ? function_size(c.function, m.ens[c.pre_id].d) : c.decoders_cols;
+  }
   for (int32_t ci = 0; ci < nc; ++ci) {
     const ConnDesc& c = m.conns[ci];
     int32_t pf;
@@ -127,7 +143,14 @@ IR build_ir(const Model& m, const Built& bp, double dt) {
       }
       pf = ref_size(c.pre_kind, c.pre_id, c.function);
     }
-    int32_t qf = ref_size(c.post_kind, c.post_id, MS_FN_IDENTITY);
+    int32_t qf;
+    if (c.post_kind == MS_REF_LEARNING) {
+      check(c.post_id >= 0 && c.post_id < nc && m.conns[c.post_id].learned,
+            "connection into the learning rule of a connection that has none");
+      qf = learn_k[c.post_id];
+    } else {
+      qf = ref_size(c.post_kind, c.post_id, MS_FN_IDENTITY);
+    }
     if (c.post_kind == MS_REF_NODE) check(m.nodes[c.post_id].passthrough, "connection into a non-passthrough node");
     pre_full[ci] = pf; post_full[ci] = qf;
     int32_t p0 = c.pre_start, p1 = (c.pre_start == 0 && c.pre_stop == 0) ? pf : c.pre_stop;
@@ -144,7 +167,7 @@ IR build_ir(const Model& m, const Built& bp, double dt) {
     }
     if (c.post_kind == MS_REF_ENS) has_x[c.post_id] = 1;
     if (c.post_kind == MS_REF_NEURONS) has_nin[c.post_id] = 1;
-    if (c.pre_kind == MS_REF_ENS && c.decoders.empty()) use_fn(c.pre_id, c.function);
+    if (c.pre_kind == MS_REF_ENS && c.decoders.empty() && !c.learned) use_fn(c.pre_id, c.function);
   }
   for (const ProbeDesc& p : m.probes) {
     int32_t w = ref_size(p.kind, p.id, MS_FN_IDENTITY);
@@ -256,12 +279,51 @@ IR build_ir(const Model& m, const Built& bp, double dt) {
 
   // ---- connections
   B.ir.conn_y.assign(nc, -1);
+  B.ir.conn_W.assign(nc, -1);
+  B.ir.conn_act.assign(nc, -1);
+  std::vector<int32_t> err_sig(nc, -1);
+  for (int32_t ci = 0; ci < nc; ++ci)
+    if (m.conns[ci].learned) err_sig[ci] = B.batched("c" + std::to_string(ci) + ".E", learn_k[ci], false);
   for (int32_t ci = 0; ci < nc; ++ci) {
     const ConnDesc& c = m.conns[ci];
     const std::string p = "c" + std::to_string(ci);
     // pre value signal
     int32_t pre_sig;
-    if (c.pre_kind == MS_REF_NODE) {
+    if (c.learned) {
+      const EnsembleDesc& E = m.ens[c.pre_id];
+      const int32_t k = learn_k[ci];
+      const std::vector<double>& D = c.decoders.empty() ? bp.decoders.at({c.pre_id, c.function}) : c.decoders;
+      pre_sig = B.batched(p + ".xd", k, false);
+      const int32_t W = B.batched(p + ".W", E.n * k, true);
+      B.ir.sigs[W].value = D;   // [n][k] row-major: row i*k + j
+      B.ir.conn_W[ci] = W;
+      int32_t act = eS[c.pre_id];
+      if (c.pes_tau > 0) {
+        act = B.batched(p + ".a", E.n, true);
+        B.ir.conn_act[ci] = act;
+      }
+      Op& r = B.add(OP_RESET, p + ".resetd");
+      r.dst = B.whole(pre_sig);
+      Op& o = B.add(OP_BDOT_INC, p + ".dec");
+      o.dst = B.whole(pre_sig);
+      o.a = B.whole(W);
+      o.src = B.whole(eS[c.pre_id]);
+      Op& re = B.add(OP_RESET, p + ".resete");
+      re.dst = B.whole(err_sig[ci]);
+      Op& u = B.add(OP_PES, p + ".pes");
+      u.dst = B.whole(W);
+      u.src = B.whole(act);
+      u.a = B.whole(err_sig[ci]);
+      u.coef_a = -c.pes_rate * dt / E.n;
+      if (c.pes_tau > 0) {
+        Op& f = B.add(OP_LOWPASS, p + ".presyn");
+        f.dst = B.whole(act);
+        f.src = B.whole(eS[c.pre_id]);
+        const double a = std::exp(-dt / c.pes_tau);
+        f.coef_a = a;
+        f.coef_b = 1.0 - a;
+      }
+    } else if (c.pre_kind == MS_REF_NODE) {
       pre_sig = node_out[c.pre_id];
     } else if (c.pre_kind == MS_REF_NEURONS) {
       pre_sig = eS[c.pre_id];
@@ -315,7 +377,11 @@ IR build_ir(const Model& m, const Built& bp, double dt) {
       o.coef_b = 1.0 - a;
     }
     const int32_t delivered = y >= 0 ? y : v;
-    if (c.post_kind == MS_REF_NEURONS) {
+    if (c.post_kind == MS_REF_LEARNING) {
+      Op& o = B.add(OP_COPY_INC, p + ".deliver");
+      o.dst = SRef{err_sig[c.post_id], q0, w};
+      o.src = B.whole(delivered);
+    } else if (c.post_kind == MS_REF_NEURONS) {
       Op& o = B.add(OP_ELEM_INC, p + ".deliver");
       o.dst = SRef{eJ[c.post_id], q0, w};
       o.a = SRef{eGain[c.post_id], q0, w};
@@ -478,7 +544,7 @@ void fuse_ensembles(IR& ir) {
     for (auto& d : o.decs) { rm(d.first); rm(d.second); }
   }
   for (auto& p : ir.probes) rm(p.src);
-  for (auto* v : {&ir.ens_V, &ir.ens_ref, &ir.conn_y, &ir.probe_y})
+  for (auto* v : {&ir.ens_V, &ir.ens_ref, &ir.conn_y, &ir.probe_y, &ir.conn_W, &ir.conn_act})
     for (int32_t& x : *v) if (x >= 0) x = remap[x];
 }
 

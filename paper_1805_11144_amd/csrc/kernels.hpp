@@ -582,6 +582,80 @@ __global__ void __launch_bounds__(256) k_ens_wg(float* st, Strides S, EnsDesc E,
   }
 }
 
+// Fused ensembles without fused decoders, with many neurons and a small
+// minibatch (B <= 16), in the launch drivers' layout (element (r, b) at
+// r * B + b).  Such neurons are independent, so a workgroup takes 64
+// neurons of one op for every batch column: its 4 wavefronts split the input
+// dimensions in four, lanes are neurons, the batch columns are held in
+// registers.  The input x[q][b] is staged in LDS once per workgroup, and each
+// transposed encoder value (coalesced across lanes) feeds B products.  The
+// four partial currents meet in LDS; then the workgroup runs the neuron
+// update for its 64 x B (neuron, column) pairs, consecutive threads taking
+// consecutive columns.  The workgroup has nw wavefronts (blockDim.x = 64 nw),
+// which split the input dimensions nw ways.  Dynamic LDS: (d + 64 nw) * B
+// floats.
+constexpr int kBigCols = 16, kBigNeurons = 64;
+
+__global__ void __launch_bounds__(1024) k_ens_big(float* __restrict__ st, int32_t B, EnsDesc E, float dt) {
+  extern __shared__ float big_lds[];
+  const EnsOp o = load_op(E.ops, blockIdx.y);
+  const int32_t i0 = (int32_t)blockIdx.x * kBigNeurons;
+  if (i0 >= o.n) return;   // the whole workgroup
+  const int32_t d = o.x >= 0 ? E.d : 0;
+  float* xs = big_lds;
+  float* part = big_lds + (size_t)d * B;   // [wave][neuron][column]
+  const int32_t nt = blockDim.x, nw = nt / 64;
+  for (int32_t t = threadIdx.x; t < d * B; t += nt) xs[t] = st[(int64_t)o.x * B + t];
+  __syncthreads();
+  const int32_t lane = threadIdx.x % 64, wave = threadIdx.x / 64;
+  float acc[kBigCols];
+#pragma unroll
+  for (int b = 0; b < kBigCols; ++b) acc[b] = 0.0f;
+  if (i0 + lane < o.n && d > 0) {
+    const int32_t dq = (d + nw - 1) / nw, q0 = wave * dq, q1 = min(d, q0 + dq);
+    gptr<float> encT = G(E.encT) + (int64_t)o.enc * d + i0 + lane;   // (q, r) at q * n + r
+    int32_t q = q0;
+    for (; q + 4 <= q1; q += 4) {   // four loads in flight, then their products
+      float e[4];
+#pragma unroll
+      for (int k = 0; k < 4; ++k) e[k] = encT[(int64_t)(q + k) * o.n];
+#pragma unroll
+      for (int k = 0; k < 4; ++k)
+#pragma unroll
+        for (int b = 0; b < kBigCols; ++b)
+          if (b < B) acc[b] = fmaf(e[k], xs[(q + k) * B + b], acc[b]);
+    }
+    for (; q < q1; ++q) {
+      const float e = encT[(int64_t)q * o.n];
+#pragma unroll
+      for (int b = 0; b < kBigCols; ++b)
+        if (b < B) acc[b] = fmaf(e, xs[q * B + b], acc[b]);
+    }
+  }
+#pragma unroll
+  for (int b = 0; b < kBigCols; ++b)
+    if (b < B) part[(wave * kBigNeurons + lane) * B + b] = acc[b];
+  __syncthreads();
+  const int32_t nb = min(kBigNeurons, o.n - i0) * B;
+  for (int32_t p = threadIdx.x; p < nb; p += nt) {
+    const int32_t r = p / B, b = p - r * B, i = i0 + r;
+    float sum = 0.0f;
+    for (int32_t w = 0; w < nw; ++w) sum += part[(w * kBigNeurons + r) * B + b];
+    const float j = G(E.bias)[o.bias + i] + sum;
+    float v = 0.0f, rf = 0.0f;
+    if (E.ntype == 0) {
+      v = st[(int64_t)(o.V + i) * B + b];
+      rf = st[(int64_t)(o.ref + i) * B + b];
+    }
+    const float sp = neuron_update(E.ntype, j, v, rf, o.tau_rc, o.tau_ref, o.amp, o.full, dt, o.inv_tau);
+    if (E.ntype == 0) {
+      st[(int64_t)(o.V + i) * B + b] = v;
+      st[(int64_t)(o.ref + i) * B + b] = rf;
+    }
+    if (o.s >= 0) st[(int64_t)(o.s + i) * B + b] = sp;
+  }
+}
+
 // Fused ensembles, large minibatch: one workgroup (4 wavefronts) per (op, tile
 // of 64 batch columns); lanes are batch columns, wavefronts split the neurons;
 // encoder and decoder weights are wavefront-uniform loads; decoded partial
@@ -801,6 +875,115 @@ __global__ void __launch_bounds__(256) k_syn_scatter(float* st, Strides S, int32
   if (j == 0 && row && sd[0] >= 0) st[at(S, (int64_t)sd[0] + i, b)] = acc;
 }
 
+// ------------------------------------------------------------- PES learning
+// Online learning of a decoded connection's output weights (paper Sec. 5.1,
+// the pes benchmark), one decoder matrix per batch column (Fig. 7).  Op o's
+// decoders for neuron i, output j, batch column b sit at state row
+// w[o] + i*M + j, column b; in the launch drivers' layout (element (r, b) at
+// r * B + b) neuron i's decoders are the M*B consecutive floats at
+// (w[o] + i*M) * B, indexed by c = j*B + b.  One pass over them computes the
+// decode d[j, b] += sum_i x[i, b] W[i, j, b] (MODE 0), the PES update
+// W[i, j, b] += coef * act[i, b] * e[j, b] (MODE 1, act = the x rows), or
+// both (MODE 2: decode with the old value, store the new), so that the
+// decoders are read once and written once per step.
+struct PesOps {
+  const int32_t* w;     // first decoder row
+  const int32_t* x;     // activities the decode reads (MODE 1: the update's)
+  const int32_t* d;     // decoded outputs (MODE 0, 2)
+  const int32_t* e;     // error rows (MODE 1, 2)
+  const int32_t* act;   // activities the update reads (MODE 2)
+  const float* coef;    // -kappa dt / n (MODE 1, 2)
+};
+
+// grid (ceil(M*B / 256), chunks, ops); each workgroup takes neurons
+// [chunk * L, min(K, chunk * L + L)) of 256 columns c; the chunk's activity
+// rows (L*B floats each) are staged in LDS (dynamic, 2*L*B floats).  Partial
+// decodes go to part[(o * nch + chunk) * M*B + c], summed by k_pes_reduce.
+template <int MODE>
+__global__ void __launch_bounds__(256) k_pes(float* __restrict__ st, int32_t B, int32_t M, int32_t K,
+                                             int32_t L, PesOps P, float* __restrict__ part, int32_t nch) {
+  extern __shared__ float pes_lds[];
+  float* s_x = pes_lds;
+  float* s_a = pes_lds + (size_t)L * B;
+  const int32_t o = blockIdx.z, ch = blockIdx.y;
+  const int32_t MB = M * B;
+  const int32_t c = (int32_t)blockIdx.x * 256 + (int32_t)threadIdx.x;
+  const int32_t i0 = ch * L, n = min(K, i0 + L) - i0;
+  const int64_t xb = ((int64_t)P.x[o] + i0) * B;
+  const int64_t ab = MODE == 2 ? ((int64_t)P.act[o] + i0) * B : xb;
+  for (int32_t t = threadIdx.x; t < n * B; t += 256) {
+    if (MODE != 1) s_x[t] = st[xb + t];
+    if (MODE != 0) s_a[t] = st[ab + t];
+  }
+  __syncthreads();
+  if (c >= MB) return;
+  const int32_t b = c % B;
+  float e = 0.f, coef = 0.f;
+  if (MODE != 0) {
+    e = st[(int64_t)P.e[o] * B + c];
+    coef = P.coef[o];
+  }
+  float* w = st + ((int64_t)P.w[o] + (int64_t)i0 * M) * B + c;
+  const int64_t stp = MB;
+  float acc0 = 0.f, acc1 = 0.f;
+  int32_t i = 0;
+  for (; i + 4 <= n; i += 4) {
+    const float w0 = w[0], w1 = w[stp], w2 = w[2 * stp], w3 = w[3 * stp];
+    if (MODE != 1) {
+      acc0 = fmaf(s_x[i * B + b], w0, acc0);
+      acc1 = fmaf(s_x[(i + 1) * B + b], w1, acc1);
+      acc0 = fmaf(s_x[(i + 2) * B + b], w2, acc0);
+      acc1 = fmaf(s_x[(i + 3) * B + b], w3, acc1);
+    }
+    if (MODE != 0) {
+      w[0] = fmaf(coef * s_a[i * B + b], e, w0);
+      w[stp] = fmaf(coef * s_a[(i + 1) * B + b], e, w1);
+      w[2 * stp] = fmaf(coef * s_a[(i + 2) * B + b], e, w2);
+      w[3 * stp] = fmaf(coef * s_a[(i + 3) * B + b], e, w3);
+    }
+    w += 4 * stp;
+  }
+  for (; i < n; ++i) {
+    const float w0 = w[0];
+    if (MODE != 1) acc0 = fmaf(s_x[i * B + b], w0, acc0);
+    if (MODE != 0) w[0] = fmaf(coef * s_a[i * B + b], e, w0);
+    w += stp;
+  }
+  if (MODE != 1) part[((int64_t)o * nch + ch) * MB + c] = acc0 + acc1;
+}
+
+// d[o] rows += the sum over chunks of the partial decodes, in a fixed order:
+// a workgroup takes 32 columns of one op; its 8 slices of 32 threads each sum
+// every 8th chunk (4 accumulators), and the 8 slice sums are added in slice
+// order.  grid (ceil(M*B / 32), ops).
+__global__ void __launch_bounds__(256) k_pes_reduce(float* __restrict__ st, int32_t B, int32_t M, const int32_t* d,
+                                                    const float* __restrict__ part, int32_t nch) {
+  __shared__ float red[8][32];
+  const int64_t MB = (int64_t)M * B;
+  const int32_t o = blockIdx.y, col = threadIdx.x % 32, slice = threadIdx.x / 32;
+  const int64_t c = (int64_t)blockIdx.x * 32 + col;
+  float a0 = 0.f, a1 = 0.f, a2 = 0.f, a3 = 0.f;
+  if (c < MB) {
+    const float* p = part + (int64_t)o * nch * MB + c;
+    int32_t ch = slice;
+    for (; ch + 24 < nch; ch += 32) {
+      a0 += p[(int64_t)ch * MB];
+      a1 += p[(int64_t)(ch + 8) * MB];
+      a2 += p[(int64_t)(ch + 16) * MB];
+      a3 += p[(int64_t)(ch + 24) * MB];
+    }
+    for (; ch < nch; ch += 8) a0 += p[(int64_t)ch * MB];
+  }
+  red[slice][col] = (a0 + a1) + (a2 + a3);
+  __syncthreads();
+  if (slice == 0 && c < MB) {
+    float t = red[0][col];
+#pragma unroll
+    for (int k = 1; k < 8; ++k) t += red[k][col];
+    st[(int64_t)d[o] * B + c] += t;
+  }
+}
+
 // node output <- feed staging [step][feed_rows][B] at the run-relative step
 // ctr[1] + du (du: the step's place among the steps launched since the counter
 // last advanced)
@@ -823,6 +1006,15 @@ __global__ void k_advance(int64_t* ctr, int32_t n) {
     ctr[0] += n;
     ctr[1] += n;
   }
+}
+
+// Rows [row0, row0 + rows) of the state get vals[r] in every batch column
+// (initial values of learned decoders, on creation and reset).
+__global__ void k_init_rows(float* st, Strides S, int32_t B, int64_t row0, int64_t rows, const float* vals) {
+  const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (t >= rows * B) return;
+  const int64_t r = t / B, b = t - r * B;
+  st[at(S, row0 + r, b)] = vals[r];
 }
 
 __global__ void k_set_ctr(int64_t* ctr, int64_t c0, int64_t c1) {

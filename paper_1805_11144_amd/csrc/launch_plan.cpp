@@ -2,9 +2,12 @@
 // of one timestep, with consecutive independent fused-ensemble groups sharing
 // a launch and (option MS_FUSE_SYNAPSES) the connection tail of the paper's
 // Fig. 2 -- transform DotInc, synaptic filter, Copy of the filtered value into
-// the post input -- fused into one group.  Host code only.
+// the post input -- fused into one group; a PES update runs in the same pass
+// over the decoders as the decode that reads them, where the error is known
+// by then.  Host code only.
 #include <algorithm>
 #include <map>
+#include <set>
 
 #include "host.hpp"
 
@@ -126,6 +129,20 @@ void accesses(const IR& ir, int32_t sb, const LGroup& g, std::vector<int64_t>& r
     case OP_LIF_RATE: rows_of(g.src, g.rows, rd); rows_of(g.dst, g.rows, wr); break;
     case OP_LOWPASS:
       rows_of(g.src, g.rows, rd); rows_of(g.dst, g.rows, rd); rows_of(g.dst, g.rows, wr);
+      break;
+    case OP_BDOT_INC:
+    case OP_PES:
+    case OP_PES_FUSED:
+      for (int64_t o = 0; o < g.rows; ++o) {
+        const int64_t nw = (int64_t)g.M * g.K;
+        for (int64_t r = 0; r < nw; ++r) rd.push_back(g.w_row[o] + r);
+        if (g.type != OP_BDOT_INC) for (int64_t r = 0; r < nw; ++r) wr.push_back(g.w_row[o] + r);
+        for (int32_t k = 0; k < g.K; ++k) rd.push_back(g.x_row[o] + k);
+        if (g.type == OP_PES_FUSED) for (int32_t k = 0; k < g.K; ++k) rd.push_back(g.act_row[o] + k);
+        if (g.type != OP_BDOT_INC) for (int32_t m = 0; m < g.M; ++m) rd.push_back(g.e_row[o] + m);
+        if (g.type != OP_PES)
+          for (int32_t m = 0; m < g.M; ++m) { rd.push_back(g.d_row[o] + m); wr.push_back(g.d_row[o] + m); }
+      }
       break;
     case OP_ENS:
       for (size_t k = 0; k < g.ens_n.size(); ++k) {
@@ -571,18 +588,170 @@ std::vector<LGroup> merge_ens_groups(const std::vector<LGroup>& in) {
   return out;
 }
 
+namespace {
+
+int32_t state_base(const Plan& p) {
+  int32_t sb = -1;
+  for (size_t b = 0; b < p.ir.bases.size(); ++b)
+    if (p.ir.bases[b].cls == SC_BATCHED) sb = (int32_t)b;
+  return sb;
+}
+
+bool overlap(const std::vector<int64_t>& a, const std::vector<int64_t>& b) {
+  if (a.empty() || b.empty()) return false;
+  std::set<int64_t> s(a.begin(), a.end());
+  for (int64_t x : b) if (s.count(x)) return true;
+  return false;
+}
+
+LOperand rows_operand(int32_t base, const std::vector<int32_t>& rows) {
+  LOperand o;
+  o.base = base;
+  bool contig = true;
+  for (size_t i = 1; i < rows.size() && contig; ++i) contig = rows[i] == rows[0] + (int32_t)i;
+  if (contig) o.start = rows.empty() ? 0 : rows[0];
+  else o.idx = rows;
+  return o;
+}
+
+// A CopyInc group whose destinations are of two kinds -- all of a
+// destination's entries pull filter rows of the last group and the filters
+// neither read nor probes record the destination, or not -- splits into the
+// pulls and the rest at the same place (they write different rows), so that
+// the pulls can fuse with the filters.  A destination whose entries mix
+// filtered and other values keeps the group whole.
+void split_pulls(const Plan& p, std::vector<LGroup>& G) {
+  const int32_t sb = state_base(p);
+  if (sb < 0 || G.empty() || G.back().type != OP_LOWPASS) return;
+  const LGroup& L = G.back();
+  std::set<int64_t> filt, busy;   // filter rows; rows the filters read or probes record
+  for (int64_t r = 0; r < L.rows; ++r) {
+    filt.insert(lrow(L.dst, r));
+    busy.insert(lrow(L.src, r));
+    busy.insert(lrow(L.dst, r));
+  }
+  for (int32_t r : p.probe_src_rows) busy.insert(r);
+  std::vector<LGroup> out;
+  for (size_t gi = 0; gi < G.size(); ++gi) {
+    const LGroup& q = G[gi];
+    if (q.type != OP_COPY_INC || q.src.base != sb || q.dst.base != sb) { out.push_back(q); continue; }
+    struct Part { std::vector<int32_t> dst, src, ptr{0}; std::set<int64_t> dset; };
+    Part part[2];   // 0: pulls, 1: the rest
+    bool mixed = false;
+    for (int64_t u = 0; u < q.rows && !mixed; ++u) {
+      const int64_t e0 = q.ptr.empty() ? u : q.ptr[u], e1 = q.ptr.empty() ? u + 1 : q.ptr[u + 1];
+      int32_t nf = 0;
+      for (int64_t e = e0; e < e1; ++e) nf += filt.count(lrow(q.src, e)) ? 1 : 0;
+      if (nf != 0 && nf != e1 - e0) { mixed = true; break; }
+      Part& P = part[nf && !busy.count(lrow(q.dst, u)) ? 0 : 1];
+      P.dst.push_back((int32_t)lrow(q.dst, u));
+      P.dset.insert(lrow(q.dst, u));
+      for (int64_t e = e0; e < e1; ++e) P.src.push_back((int32_t)lrow(q.src, e));
+      P.ptr.push_back((int32_t)P.src.size());
+    }
+    if (mixed || part[0].dst.empty() || part[1].dst.empty()) { out.push_back(q); continue; }
+    for (Part& P : part) {
+      LGroup g = q;
+      g.rows = (int64_t)P.dst.size();
+      g.dst = rows_operand(sb, P.dst);
+      g.src = rows_operand(sb, P.src);
+      g.ptr = P.src.size() == P.dst.size() ? std::vector<int32_t>{} : P.ptr;
+      g.ops.clear();
+      for (int32_t oi : q.ops) {
+        const Op& o = p.ir.ops[oi];
+        if (P.dset.count(p.sig_offset[o.dst.sig] + o.dst.start)) g.ops.push_back(oi);
+      }
+      out.push_back(std::move(g));
+    }
+  }
+  G.swap(out);
+}
+
+// Groups after the last filter group that share no row with it (a PES update
+// of decoders nothing else touches, say) move in front of it, so that the
+// step ends with the filters.
+void filters_last(const Plan& p, std::vector<LGroup>& G) {
+  const int32_t sb = state_base(p);
+  int32_t L = -1;
+  for (int32_t g = 0; g < (int32_t)G.size(); ++g) if (G[g].type == OP_LOWPASS) L = g;
+  if (L < 0 || L + 1 == (int32_t)G.size() || sb < 0) return;
+  std::vector<int64_t> lr, lw, rd, wr;
+  accesses(p.ir, sb, G[L], lr, lw);
+  for (int32_t g = L + 1; g < (int32_t)G.size(); ++g) {
+    accesses(p.ir, sb, G[g], rd, wr);
+    if (overlap(lw, rd) || overlap(lw, wr) || overlap(lr, wr)) return;
+  }
+  LGroup f = std::move(G[L]);
+  G.erase(G.begin() + L);
+  G.push_back(std::move(f));
+}
+
+// A PES group whose ops are exactly those of a learned-decode group moves to
+// the decode's place and runs with it as one pass over the decoders, when
+// nothing between the two writes the error or activity rows the update reads
+// or touches the decoders.
+void fuse_pes(const Plan& p, std::vector<LGroup>& G) {
+  const int32_t sb = state_base(p);
+  if (sb < 0) return;
+  std::vector<int64_t> rd, wr;
+  for (int32_t pi = 0; pi < (int32_t)G.size(); ++pi) {
+    if (G[pi].type != OP_PES) continue;
+    const LGroup& P = G[pi];
+    int32_t di = -1;
+    for (int32_t g = 0; g < pi; ++g)
+      if (G[g].type == OP_BDOT_INC && G[g].w_row == P.w_row && G[g].M == P.M && G[g].K == P.K &&
+          G[g].a.base == sb && P.dst.base == sb && G[g].src.base == sb && P.src.base == sb && P.a.base == sb)
+        di = g;
+    if (di < 0) continue;
+    std::vector<int64_t> need;   // rows the update reads besides the decoders
+    for (int64_t o = 0; o < P.rows; ++o) {
+      for (int32_t k = 0; k < P.K; ++k) need.push_back(P.x_row[o] + k);
+      for (int32_t m = 0; m < P.M; ++m) need.push_back(P.e_row[o] + m);
+    }
+    std::vector<int64_t> wrows;
+    for (int64_t o = 0; o < P.rows; ++o)
+      for (int64_t r = 0; r < (int64_t)P.M * P.K; ++r) wrows.push_back(P.w_row[o] + r);
+    bool ok = true;
+    for (int32_t g = di + 1; g < pi && ok; ++g) {
+      accesses(p.ir, sb, G[g], rd, wr);
+      ok = !overlap(need, wr) && !overlap(wrows, wr) && !overlap(wrows, rd);
+    }
+    // the decode's own outputs are not among the rows the update reads
+    std::vector<int64_t> drows;
+    for (int64_t o = 0; o < P.rows; ++o)
+      for (int32_t m = 0; m < P.M; ++m) drows.push_back(G[di].d_row[o] + m);
+    ok = ok && !overlap(need, drows);
+    if (!ok) continue;
+    LGroup f = G[di];
+    f.type = OP_PES_FUSED;
+    f.act_row = P.x_row;
+    f.e_row = P.e_row;
+    f.coef = P.coef;
+    f.ops.insert(f.ops.end(), P.ops.begin(), P.ops.end());
+    G[di] = std::move(f);
+    G.erase(G.begin() + pi);
+    --pi;
+  }
+}
+
+}  // namespace
+
 LaunchPlan make_launch_plan(const Plan& p) {
   LaunchPlan lp;
   lp.step = merge_ens_groups(p.lowered);
-  if (!p.opts.fuse_synapse) return lp;
-  Fuser f(p, lp.step);
-  std::vector<LGroup> out;
-  if (f.run(out, lp.prologue)) {
-    lp.step = std::move(out);
-    lp.has_prologue = lp.prologue.rows > 0;
-  } else {
-    lp.why = f.why;
+  if (p.opts.fuse_synapse) {
+    filters_last(p, lp.step);
+    split_pulls(p, lp.step);
+    Fuser f(p, lp.step);
+    std::vector<LGroup> out;
+    if (f.run(out, lp.prologue)) {
+      lp.step = std::move(out);
+      lp.has_prologue = lp.prologue.rows > 0;
+    } else {
+      lp.why = f.why;
+    }
   }
+  fuse_pes(p, lp.step);
   return lp;
 }
 

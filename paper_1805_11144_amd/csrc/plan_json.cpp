@@ -75,13 +75,17 @@ void jgroup(std::ostringstream& o, const Plan& p, const LGroup& L) {
     jarr(o, L.syn_ab);
     o << ",\"wbase\":";
     jarr(o, L.syn_wbase);
-  } else if (L.type == OP_DOT_INC) {
+  } else if (L.type == OP_DOT_INC || L.type == OP_BDOT_INC || L.type == OP_PES || L.type == OP_PES_FUSED) {
     o << ",\"M\":" << L.M << ",\"K\":" << L.K << ",\"w_row\":";
     jarr(o, L.w_row);
     o << ",\"x_row\":";
     jarr(o, L.x_row);
-    o << ",\"d_row\":";
-    jarr(o, L.d_row);
+    if (L.type != OP_PES) { o << ",\"d_row\":"; jarr(o, L.d_row); }
+    if (L.type == OP_PES || L.type == OP_PES_FUSED) {
+      o << ",\"e_row\":"; jarr(o, L.e_row);
+      o << ",\"coef\":"; jarr(o, L.coef);
+    }
+    if (L.type == OP_PES_FUSED) { o << ",\"act_row\":"; jarr(o, L.act_row); }
   } else {
     o << ",\"dst\":";
     joperand(o, L.dst);

@@ -36,7 +36,7 @@ namespace ms {
 const char* op_type_name(int32_t t) {
   static const char* n[] = {"Feed", "Reset", "Copy", "CopyInc", "ElementwiseInc",
                             "DotInc", "SimLIF", "SimLIFRate", "Lowpass", "Ensemble",
-                            "SynapseScatter"};
+                            "SynapseScatter", "LearnedDotInc", "PES", "PESDecodeUpdate"};
   return (t >= 0 && t < OP_NTYPES) ? n[t] : "?";
 }
 
@@ -52,6 +52,8 @@ std::vector<SRef> read_slots(const Op& o) {
     case OP_LIF: return {o.src, o.V, o.ref};
     case OP_LIF_RATE: return {o.src};
     case OP_LOWPASS: return {o.src, o.dst};
+    case OP_BDOT_INC: return {o.a, o.src};
+    case OP_PES: return {o.src, o.a, o.dst};
     case OP_ENS: {
       std::vector<SRef> r;
       if (o.src.sig >= 0) { r.push_back(o.src); r.push_back(o.a); }
@@ -79,6 +81,8 @@ void access(const Op& o, std::vector<int32_t>& sets, std::vector<int32_t>& incs,
       upds.push_back(o.V.sig); upds.push_back(o.ref.sig); break;
     case OP_LIF_RATE: reads.push_back(o.src.sig); sets.push_back(o.dst.sig); break;
     case OP_LOWPASS: reads.push_back(o.src.sig); upds.push_back(o.dst.sig); break;
+    case OP_BDOT_INC: incs.push_back(o.dst.sig); reads.push_back(o.a.sig); reads.push_back(o.src.sig); break;
+    case OP_PES: reads.push_back(o.src.sig); reads.push_back(o.a.sig); upds.push_back(o.dst.sig); break;
     case OP_ENS:
       if (o.src.sig >= 0) reads.push_back(o.src.sig);
       if (o.dst.sig >= 0) sets.push_back(o.dst.sig);
@@ -101,6 +105,8 @@ std::vector<int32_t> merge_key(const IR& ir, const Op& o) {
     case OP_LIF: return {OP_LIF, b(o.src), b(o.dst), b(o.V), b(o.ref)};
     case OP_LIF_RATE: return {OP_LIF_RATE, b(o.src), b(o.dst), o.ntype};   // rate curve: LIF or ReLU
     case OP_LOWPASS: return {OP_LOWPASS, b(o.dst), b(o.src)};
+    case OP_BDOT_INC: return {OP_BDOT_INC, b(o.dst), b(o.a), b(o.src), o.dst.len, o.src.len};
+    case OP_PES: return {OP_PES, b(o.dst), b(o.src), b(o.a), o.a.len, o.src.len};
     case OP_ENS: {
       std::vector<int32_t> k = {OP_ENS, o.ntype, b(o.src), b(o.a), o.src.len, b(o.bias),
                                 b(o.dst), b(o.V), b(o.ref)};
@@ -611,6 +617,29 @@ LGroup lower_group_at(const IR& ir, const std::vector<int64_t>& sig_offset, cons
       g.cb = uniform_or_rows(cb);
       break;
     }
+    case OP_BDOT_INC:
+    case OP_PES: {
+      // per op: decoders, activities, outputs (BDOT_INC) or error (PES)
+      g.M = g.type == OP_BDOT_INC ? f.dst.len : f.a.len;
+      g.K = f.src.len;
+      for (int32_t oi : ops) {
+        const Op& o = ir.ops[oi];
+        if (g.type == OP_BDOT_INC) {
+          g.w_row.push_back(row(o.a, 0));
+          g.d_row.push_back(row(o.dst, 0));
+        } else {
+          g.w_row.push_back(row(o.dst, 0));
+          g.e_row.push_back(row(o.a, 0));
+          g.coef.push_back((float)o.coef_a);
+        }
+        g.x_row.push_back(row(o.src, 0));
+      }
+      g.rows = (int64_t)ops.size();
+      g.dst.base = base(f.dst);
+      g.src.base = base(f.src);
+      g.a.base = base(f.a);
+      break;
+    }
     case OP_ENS: {
       g.rows = (int64_t)ops.size();
       g.ens_type = f.ntype;
@@ -681,6 +710,8 @@ WindowPlan make_window_plan(const Plan& p) {
   for (const Op& o : ir.ops)
     if ((o.type == OP_LIF || o.type == OP_ENS) && o.V.sig >= 0) { w.priv[o.V.sig] = 1; w.priv[o.ref.sig] = 1; }
   auto refuse = [&](const std::string& why) { w.ok = false; w.why = why; return w; };
+  for (const Op& o : ir.ops)
+    if (o.type == OP_PES) return refuse("online learning changes the decoders every step (" + o.name + ")");
   for (int32_t sg = 0; sg < ns; ++sg) {
     if (!batched(sg)) continue;
     if (w.priv[sg]) {

@@ -9,6 +9,7 @@
 //   mat<K> float [rows][K]  weight matrices with K columns
 // Each merged group is one launch; a group's per-row operands are either a
 // contiguous row range (a "slice") or an int32 index list.
+#include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
@@ -79,6 +80,12 @@ struct Launch {
   SynW syn_w{};
   int32_t syn_update = 1;
   int32_t syn_probe = 0;
+  // BDOT_INC / PES / PES_FUSED: per-op rows, chunking of the neurons
+  int32_t ens_nmax = 0;              // ENS: most neurons of an op
+  const int32_t* e_row = nullptr;
+  const int32_t* act_row = nullptr;
+  const float* coef = nullptr;
+  int32_t pes_L = 0, pes_nch = 0;
 };
 
 }  // namespace
@@ -143,10 +150,16 @@ struct ms_sim {
   std::vector<hipEvent_t> tev;       // event pool, pairs
   std::vector<int32_t> ttype;        // op type of each recorded pair
   size_t tn = 0;                     // pairs recorded in the last run
+  bool tx = false, tx_first = false; // a launch-driver group is being timed (first kernel next)
+  hipEvent_t tx_start = nullptr, tx_stop = nullptr;
   static constexpr int kSide = 3;    // extra streams for independent phases of one level
   hipStream_t side[kSide] = {};
   hipEvent_t side_ev[kSide + 1] = {};
   std::vector<std::vector<float>> host_bases;   // host copies of parameter bases
+  float* init_vals = nullptr;        // initial values of batched state signals that have one
+  std::vector<std::pair<int32_t, int64_t>> init_sigs;   // (signal, offset in init_vals)
+  float* pes_part = nullptr;         // partial decodes of the learned-decoder launches
+  size_t pes_part_n = 0, pes_part_cap = 0;
 };
 
 namespace {
@@ -202,6 +215,8 @@ void free_sim(ms_sim* s) {
   f(s->prog.groups);
   f(s->col_scratch);
   f(s->va); f(s->pa);
+  f(s->pes_part);
+  f(s->init_vals);
   for (void* p : s->extra_allocs) f(p);
   if (s->ev0) (void)hipEventDestroy(s->ev0);
   if (s->ev1) (void)hipEventDestroy(s->ev1);
@@ -244,13 +259,14 @@ void build_launches(ms_sim* s, const std::vector<LGroup>& groups, std::vector<La
   const IR& ir = p.ir;
   // ---- lowered groups -> pools
   PoolBuilder pb;
-  struct Offs { int64_t dst, src, a, V, ref, ptr, values, w, x, d, trc, tref, amp, ca, cb, feed, full; };
+  struct Offs { int64_t dst, src, a, V, ref, ptr, values, w, x, d, trc, tref, amp, ca, cb, feed, full, e, act, coef; };
   std::vector<Offs> offs;
   for (const LGroup& g : groups) {
     Offs o{};
     o.dst = pb.add_i(g.dst.idx); o.src = pb.add_i(g.src.idx); o.a = pb.add_i(g.a.idx);
     o.V = pb.add_i(g.V.idx); o.ref = pb.add_i(g.ref.idx); o.ptr = pb.add_i(g.ptr);
     o.w = pb.add_i(g.w_row); o.x = pb.add_i(g.x_row); o.d = pb.add_i(g.d_row);
+    o.e = pb.add_i(g.e_row); o.act = pb.add_i(g.act_row); o.coef = pb.add_f(g.coef);
     o.feed = pb.add_i(g.feed_rows);
     o.values = pb.add_f(g.values);
     const bool per_row_params = g.type != OP_ENS;
@@ -416,6 +432,28 @@ void build_launches(ms_sim* s, const std::vector<LGroup>& groups, std::vector<La
       }
       E.bias = s->base_ptr[g.ens_bias_base];
       E.ops = reinterpret_cast<const EnsOp*>(ipool + ens_off[gi]);
+      for (int32_t n : g.ens_n) l.ens_nmax = std::max(l.ens_nmax, n);
+    }
+    if (g.type == OP_BDOT_INC || g.type == OP_PES || g.type == OP_PES_FUSED) {
+      // neurons per workgroup: about 2048 workgroups per launch, at least 4
+      // neurons each, the chunk's activities (2 * L * B floats) within 64 KB of LDS
+      if (s->S.rs != s->B || s->S.cs != 1) fail(MS_E_INVALID, "learned decoders need the launch drivers' state layout");
+      const int64_t MB = (int64_t)g.M * s->B;
+      const int64_t cblk = (MB + 255) / 256;
+      if (g.rows > 65535 || cblk > 2147483647LL) fail(MS_E_INVALID, "learned-decoder group too large");
+      const int64_t lmax = 8192 / s->B;
+      if (lmax < 1) fail(MS_E_INVALID, "minibatch too large for learned decoders (at most 8192)");
+      const int64_t want = std::max<int64_t>(1, 2048 / std::max<int64_t>(1, cblk * g.rows));
+      int64_t L = std::max<int64_t>(4, (g.K + want - 1) / want);
+      L = std::max<int64_t>(1, std::min<int64_t>(L, lmax));
+      const int64_t nch = (g.K + L - 1) / L;
+      if (nch > 65535) fail(MS_E_INVALID, "learned-decoder group has too many neurons for its minibatch");
+      l.pes_L = (int32_t)L;
+      l.pes_nch = (int32_t)nch;
+      l.e_row = ip(o.e);
+      l.act_row = ip(o.act);
+      l.coef = fp(o.coef);
+      if (g.type != OP_PES) s->pes_part_n = std::max(s->pes_part_n, (size_t)(g.rows * nch * MB));
     }
     if (g.type == OP_SYN_SCATTER) {
       if ((int)g.syn_wbase.size() > 4) fail(MS_E_INVALID, "fused synapse group with too many weight bases");
@@ -426,6 +464,12 @@ void build_launches(ms_sim* s, const std::vector<LGroup>& groups, std::vector<La
       l.syn_probe = g.syn_probe;
     }
     out.push_back(l);
+  }
+  if (s->pes_part_n > s->pes_part_cap) {
+    if (s->pes_part) HIPCHECK(hipFree(s->pes_part));
+    s->pes_part = nullptr;
+    s->pes_part = dev_alloc<float>(s->pes_part_n);
+    s->pes_part_cap = s->pes_part_n;
   }
 }
 
@@ -488,8 +532,8 @@ inline unsigned grid_for(int64_t n) { return (unsigned)std::max<int64_t>(1, (n +
 
 // Timing brackets around one launch of type `type` on stream q (no-ops unless
 // timing is on).
-void time_begin(ms_sim* s, int32_t type, hipStream_t q) {
-  if (!s->timing) return;
+// The next pair of timing events, for a launch of operator type `type`.
+void time_slot(ms_sim* s, int32_t type) {
   if (2 * (s->tn + 1) > s->tev.size()) {
     for (int k = 0; k < 2; ++k) {
       hipEvent_t e = nullptr;
@@ -499,6 +543,11 @@ void time_begin(ms_sim* s, int32_t type, hipStream_t q) {
   }
   if (s->ttype.size() <= s->tn) s->ttype.resize(s->tn + 1);
   s->ttype[s->tn] = type;
+}
+
+void time_begin(ms_sim* s, int32_t type, hipStream_t q) {
+  if (!s->timing) return;
+  time_slot(s, type);
   HIPCHECK(hipEventRecord(s->tev[2 * s->tn], q));
 }
 
@@ -507,6 +556,40 @@ void time_end(ms_sim* s, hipStream_t q) {
   HIPCHECK(hipEventRecord(s->tev[2 * s->tn + 1], q));
   ++s->tn;
 }
+
+// Timing of one group of the launch drivers: its kernels are launched with
+// hipExtLaunchKernelGGL, the first recording the begin event when it starts
+// and each recording the end event when it ends (the last one counts), so
+// that the interval is the group's execution, without the host's launch
+// latency (which the stream-ordered driver would otherwise add whenever the
+// GPU waits for the next launch).
+void time_group_begin(ms_sim* s, int32_t type) {
+  if (!s->timing) return;
+  time_slot(s, type);
+  s->tx = true;
+  s->tx_first = true;
+  s->tx_start = s->tev[2 * s->tn];
+  s->tx_stop = s->tev[2 * s->tn + 1];
+}
+
+void time_group_end(ms_sim* s) {
+  if (!s->timing) return;
+  s->tx = false;
+  ++s->tn;
+}
+
+// Kernel launch of a merged group: plain, or with the timing events of
+// time_group_begin.
+#define KL(kern, grid, block, lds, stream, ...)                                                          \
+  do {                                                                                                  \
+    if (s->tx) {                                                                                        \
+      hipExtLaunchKernelGGL(kern, grid, block, lds, stream, s->tx_first ? s->tx_start : nullptr,        \
+                            s->tx_stop, 0, __VA_ARGS__);                                               \
+      s->tx_first = false;                                                                              \
+    } else {                                                                                            \
+      hipLaunchKernelGGL(kern, grid, block, lds, stream, __VA_ARGS__);                                  \
+    }                                                                                                   \
+  } while (0)
 
 void launch_group(ms_sim* s, const Launch& l, int32_t du) {
   const int32_t B = s->B;
@@ -519,69 +602,98 @@ void launch_group(ms_sim* s, const Launch& l, int32_t du) {
   const int64_t n = l.rows * B;
   switch (l.type) {
     case OP_FEED:
-      hipLaunchKernelGGL(k_feed, dim3(grid_for(n)), dim3(kBlock), 0, q, st, S, B, l.rows, l.dst,
+      KL(k_feed, dim3(grid_for(n)), dim3(kBlock), 0, q, st, S, B, l.rows, l.dst,
                          l.feed_rows, (const float*)s->feed_stage, s->plan->ir.feed_rows, s->ctr, du);
       break;
     case OP_RESET:
-      hipLaunchKernelGGL(k_reset, dim3(grid_for(n)), dim3(kBlock), 0, q, st, S, B, l.rows, l.dst, l.values);
+      KL(k_reset, dim3(grid_for(n)), dim3(kBlock), 0, q, st, S, B, l.rows, l.dst, l.values);
       break;
     case OP_COPY:
-      hipLaunchKernelGGL(k_copy, dim3(grid_for(n)), dim3(kBlock), 0, q, st, S, B, l.rows, l.dst,
+      KL(k_copy, dim3(grid_for(n)), dim3(kBlock), 0, q, st, S, B, l.rows, l.dst,
                          l.src_base, l.src, (int)l.src_bcast);
       break;
     case OP_COPY_INC:
-      hipLaunchKernelGGL(k_copy_inc, dim3(grid_for(n)), dim3(kBlock), 0, q, st, S, B, l.rows, l.dst,
+      KL(k_copy_inc, dim3(grid_for(n)), dim3(kBlock), 0, q, st, S, B, l.rows, l.dst,
                          l.src_base, l.src, (int)l.src_bcast, l.ptr);
       break;
     case OP_ELEM_INC:
-      hipLaunchKernelGGL(k_elem_inc, dim3(grid_for(n)), dim3(kBlock), 0, q, st, S, B, l.rows, l.dst,
+      KL(k_elem_inc, dim3(grid_for(n)), dim3(kBlock), 0, q, st, S, B, l.rows, l.dst,
                          l.a_base, l.a, l.src_base, l.src, l.ptr);
       break;
     case OP_DOT_INC: {
       if (l.K >= 64 && B <= 4) {
         const int64_t waves = l.rows * (int64_t)l.M;
-        hipLaunchKernelGGL(k_dot_inc_wave, dim3(grid_for(waves * 64)), dim3(kBlock), 0, q, st, S, B, l.rows,
+        KL(k_dot_inc_wave, dim3(grid_for(waves * 64)), dim3(kBlock), 0, q, st, S, B, l.rows,
                            l.M, l.K, l.a_base, l.w_row, l.x_row, l.d_row);
       } else {
         const int64_t work = l.rows * (int64_t)l.M * B;
-        hipLaunchKernelGGL(k_dot_inc, dim3(grid_for(work)), dim3(kBlock), 0, q, st, S, B, l.rows, l.M, l.K,
+        KL(k_dot_inc, dim3(grid_for(work)), dim3(kBlock), 0, q, st, S, B, l.rows, l.M, l.K,
                            l.a_base, l.w_row, l.x_row, l.d_row);
       }
       break;
     }
     case OP_LIF:
-      hipLaunchKernelGGL(k_lif, dim3(grid_for(n)), dim3(kBlock), 0, q, st, S, B, l.rows, l.src, l.dst,
+      KL(k_lif, dim3(grid_for(n)), dim3(kBlock), 0, q, st, S, B, l.rows, l.src, l.dst,
                          l.V, l.ref, l.np, s->dt);
       break;
     case OP_LIF_RATE:
-      hipLaunchKernelGGL(k_lif_rate, dim3(grid_for(n)), dim3(kBlock), 0, q, st, S, B, l.rows, l.src,
+      KL(k_lif_rate, dim3(grid_for(n)), dim3(kBlock), 0, q, st, S, B, l.rows, l.src,
                          l.dst, l.np);
       break;
     case OP_LOWPASS:
-      hipLaunchKernelGGL(k_lowpass, dim3(grid_for(n)), dim3(kBlock), 0, q, st, S, B, l.rows, l.dst,
+      KL(k_lowpass, dim3(grid_for(n)), dim3(kBlock), 0, q, st, S, B, l.rows, l.dst,
                          l.src, l.fp);
       break;
     case OP_SYN_SCATTER: {
       // one wavefront per (segment, batch column)
       const double items = (double)l.rows * 64 * B;
       if (items >= 4294967296.0) fail(MS_E_INVALID, "fused synapse group too large for 32-bit indexing");
-      hipLaunchKernelGGL(k_syn_scatter, dim3(grid_for((int64_t)items)), dim3(kBlock), 0, q, st, S, B,
+      KL(k_syn_scatter, dim3(grid_for((int64_t)items)), dim3(kBlock), 0, q, st, S, B,
                          (int32_t)l.rows, l.syn_seg, l.syn_conn, l.syn_w, l.syn_update,
                          l.syn_probe ? s->probe_buf : nullptr, s->probe_rows, (const float*)s->feed_stage,
                          s->plan->ir.feed_rows, (const int64_t*)s->ctr, du);
       break;
     }
-    case OP_ENS:
-      if (B >= 32) {
-        hipLaunchKernelGGL(k_ens_tile, dim3((unsigned)l.rows, (unsigned)((B + 63) / 64)), dim3(256), 0, q, st, S,
-                           B, l.ens, s->dt);
-      } else {
-        if (l.ens.decT)
-          hipLaunchKernelGGL(k_ens_wg<true>, dim3((unsigned)l.rows, (unsigned)B), dim3(256), 0, q, st, S, l.ens, s->dt);
-        else
-          hipLaunchKernelGGL(k_ens_wg<false>, dim3((unsigned)l.rows, (unsigned)B), dim3(256), 0, q, st, S, l.ens, s->dt);
+    case OP_BDOT_INC:
+    case OP_PES:
+    case OP_PES_FUSED: {
+      const int64_t MB = (int64_t)l.M * B;
+      const dim3 grid((unsigned)((MB + 255) / 256), (unsigned)l.pes_nch, (unsigned)l.rows);
+      const size_t lds = (size_t)2 * l.pes_L * B * sizeof(float);
+      const PesOps P{l.w_row, l.x_row, l.d_row, l.e_row, l.act_row, l.coef};
+      if (l.type == OP_BDOT_INC)
+        KL(k_pes<0>, grid, dim3(256), lds, q, st, B, l.M, l.K, l.pes_L, P, s->pes_part, l.pes_nch);
+      else if (l.type == OP_PES)
+        KL(k_pes<1>, grid, dim3(256), lds, q, st, B, l.M, l.K, l.pes_L, P, s->pes_part, l.pes_nch);
+      else
+        KL(k_pes<2>, grid, dim3(256), lds, q, st, B, l.M, l.K, l.pes_L, P, s->pes_part, l.pes_nch);
+      if (l.type != OP_PES) {
+        HIPCHECK(hipGetLastError());
+        KL(k_pes_reduce, dim3((unsigned)((MB + 31) / 32), (unsigned)l.rows), dim3(256), 0, q, st,
+                           B, l.M, l.d_row, (const float*)s->pes_part, l.pes_nch);
       }
       break;
+    }
+    case OP_ENS: {
+      // many neurons per op, no fused decoders, few batch columns: neuron
+      // chunks of every op run in parallel, the batch in registers
+      int32_t nw = 16;   // wavefronts per workgroup, within 64 KB of LDS
+      while (nw >= 4 && (size_t)(l.ens.d + 64 * nw) * B * sizeof(float) > 65536) nw /= 2;
+      if (B <= kBigCols && l.ens.ndec == 0 && l.ens.encT && l.ens_nmax >= 512 && nw >= 4 &&
+          S.rs == B && S.cs == 1 && l.rows <= 65535) {
+        const size_t big_lds = (size_t)(l.ens.d + 64 * nw) * B * sizeof(float);
+        KL(k_ens_big, dim3((unsigned)((l.ens_nmax + kBigNeurons - 1) / kBigNeurons), (unsigned)l.rows),
+                           dim3(64 * nw), big_lds, q, st, B, l.ens, s->dt);
+      } else if (B >= 32) {
+        KL(k_ens_tile, dim3((unsigned)l.rows, (unsigned)((B + 63) / 64)), dim3(256), 0, q, st, S,
+                           B, l.ens, s->dt);
+      } else if (l.ens.decT) {
+        KL(k_ens_wg<true>, dim3((unsigned)l.rows, (unsigned)B), dim3(256), 0, q, st, S, l.ens, s->dt);
+      } else {
+        KL(k_ens_wg<false>, dim3((unsigned)l.rows, (unsigned)B), dim3(256), 0, q, st, S, l.ens, s->dt);
+      }
+      break;
+    }
     default: fail(MS_E_INVALID, "unknown group type");
   }
 }
@@ -593,9 +705,9 @@ void launch_group(ms_sim* s, const Launch& l, int32_t du) {
 void launch_step(ms_sim* s, int32_t du = 0, bool advance = true) {
   for (const Launch& l : s->launches) {
     const bool t = s->driver == MS_DRIVER_STEPS && l.rows > 0;
-    if (t) time_begin(s, l.type, s->stream);
+    if (t) time_group_begin(s, l.type);
     launch_group(s, l, du);
-    if (t) time_end(s, s->stream);
+    if (t) time_group_end(s);
   }
   const int64_t n = (int64_t)s->probe_rows * s->B;
   if (n > 0 && !s->probe_folded)
@@ -702,8 +814,14 @@ int64_t param_bytes(const Plan& p) {
 // own state; otherwise the persistent per-column driver when one workgroup can
 // hold a column's whole step cheaply (small weights, modest state), else
 // launches.
+bool has_learning(const Plan& p) {
+  for (const Op& o : p.ir.ops) if (o.type == OP_PES) return true;
+  return false;
+}
+
 int32_t choose_driver(const Plan& p, int32_t B, int32_t requested) {
   if (requested != MS_DRIVER_AUTO) return requested;
+  if (has_learning(p)) return MS_DRIVER_GRAPH;
   if (make_window_plan(p).ok) return MS_DRIVER_WINDOW;
   const int64_t rows = p.base_rows.empty() ? 0 : p.base_rows[0];
   const int64_t wbytes = param_bytes(p);
@@ -1113,6 +1231,43 @@ void run_window(ms_sim* s, int64_t n_steps) {
 
 }  // namespace
 
+static void state_copy(ms_sim* s, int32_t sig, float* host, bool to_device);
+
+// Batched state signals with an initial value (learned decoders) get it in
+// every batch column; the rest of the state starts at zero.  The values are
+// uploaded once and broadcast on the device (the window driver's state is
+// written through state_copy).
+static void init_state(ms_sim* s) {
+  const IR& ir = s->plan->ir;
+  if (s->init_sigs.empty()) {
+    std::vector<float> h;
+    for (int32_t k = 0; k < (int32_t)ir.sigs.size(); ++k) {
+      const Signal& sg = ir.sigs[k];
+      if (sg.cls != SC_BATCHED || sg.value.empty()) continue;
+      if ((int64_t)sg.value.size() != sg.rows) fail(MS_E_INVALID, "initial value size mismatch for " + sg.name);
+      s->init_sigs.push_back({k, (int64_t)h.size()});
+      h.insert(h.end(), sg.value.begin(), sg.value.end());
+    }
+    if (h.empty()) return;
+    s->init_vals = dev_alloc<float>(h.size());
+    HIPCHECK(hipMemcpy(s->init_vals, h.data(), h.size() * sizeof(float), hipMemcpyHostToDevice));
+  }
+  for (const auto& is : s->init_sigs) {
+    const Signal& sg = ir.sigs[is.first];
+    if (s->driver == MS_DRIVER_WINDOW) {
+      std::vector<float> h((size_t)sg.rows * s->B);
+      for (int64_t b = 0; b < s->B; ++b)
+        for (int64_t r = 0; r < sg.rows; ++r) h[(size_t)(b * sg.rows + r)] = (float)sg.value[(size_t)r];
+      state_copy(s, is.first, h.data(), true);
+      continue;
+    }
+    const int64_t n = sg.rows * s->B;
+    hipLaunchKernelGGL(k_init_rows, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s->stream, s->state, s->S,
+                       s->B, s->plan->sig_offset[is.first], sg.rows, (const float*)(s->init_vals + is.second));
+    HIPCHECK(hipGetLastError());
+  }
+}
+
 extern "C" {
 
 ms_status ms_sim_create(const ms_model* model, const ms_sim_opts* opts, ms_sim** out) {
@@ -1149,6 +1304,8 @@ ms_status ms_sim_create(const ms_model* model, const ms_sim_opts* opts, ms_sim**
       HIPCHECK(hipEventCreate(&s->ev0));
       HIPCHECK(hipEventCreate(&s->ev1));
       s->driver = choose_driver(*s->plan, s->B, o->driver);
+      if (s->driver == MS_DRIVER_PERSISTENT && has_learning(*s->plan))
+        fail(MS_E_INVALID, "the persistent driver cannot run a model with learning rules");
       if (s->gemm_dtype == MS_GEMM_BF16 && s->driver != MS_DRIVER_WINDOW)
         fail(MS_E_INVALID, "bf16 products run on the window driver only");
       // persistent: one workgroup per batch column -> column-major state
@@ -1163,6 +1320,7 @@ ms_status ms_sim_create(const ms_model* model, const ms_sim_opts* opts, ms_sim**
       if (s->driver == MS_DRIVER_PERSISTENT) setup_persistent(s);
       if (s->driver == MS_DRIVER_WINDOW) setup_window(s);
       ensure_capacity(s, std::max<int64_t>(1, o->probe_capacity_steps));
+      init_state(s);
       HIPCHECK(hipStreamSynchronize(s->stream));
     } catch (...) {
       free_sim(s);
@@ -1208,9 +1366,9 @@ ms_status ms_sim_run_steps(ms_sim* s, int64_t n_steps, const ms_feed* feeds, int
       for (; k < n_steps; ++k) launch_step(s);
     } else {
       if (s->has_prologue) {
-        time_begin(s, OP_SYN_SCATTER, s->stream);
+        time_group_begin(s, OP_SYN_SCATTER);
         launch_group(s, s->prologue, 0);
-        time_end(s, s->stream);
+        time_group_end(s);
       }
       for (int64_t k = 0; k < n_steps; ++k) launch_step(s);
     }
@@ -1358,6 +1516,7 @@ ms_status ms_sim_reset(ms_sim* s) {
       HIPCHECK(hipMemset2DAsync(s->va, s->vs * 4, 0, (size_t)s->B * 4, std::max<int64_t>(1, s->wplan->rows_v), s->stream));
     if (s->pa) HIPCHECK(hipMemsetAsync(s->pa, 0, (size_t)std::max<int64_t>(1, s->wplan->rows_p) * s->B * 4, s->stream));
     HIPCHECK(hipMemsetAsync(s->ctr, 0, 2 * sizeof(int64_t), s->stream));
+    init_state(s);
     HIPCHECK(hipStreamSynchronize(s->stream));
     s->steps_total = 0;
   });
@@ -1425,6 +1584,8 @@ static int32_t state_signal(const ms_sim* s, int32_t which, int32_t id) {
     case MS_STATE_REFRACTORY: return pick(ir.ens_ref);
     case MS_STATE_SYNAPSE: return pick(ir.conn_y);
     case MS_STATE_PROBE_SYNAPSE: return pick(ir.probe_y);
+    case MS_STATE_LEARNED_DECODERS: return pick(ir.conn_W);
+    case MS_STATE_PES_ACTIVITY: return pick(ir.conn_act);
     default: fail(MS_E_INVALID, "unknown state kind");
   }
 }

@@ -13,7 +13,7 @@ _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libmergesim.so")
 
 MS_OK = 0
-REF_NODE, REF_ENS, REF_NEURONS = 0, 1, 2
+REF_NODE, REF_ENS, REF_NEURONS, REF_LEARNING = 0, 1, 2, 3
 NEURON_LIF, NEURON_LIF_RATE, NEURON_RELU = 0, 1, 2
 FN_IDENTITY, FN_PRODUCT = 0, 1
 PLANNER_GREEDY, PLANNER_TREE = 0, 1
@@ -23,9 +23,10 @@ FUSE_ENSEMBLES, FUSE_SYNAPSES = 1, 2
 PROBE_READ_STATIC_MAX = 1 << 22
 DECODE_DENSE, DECODE_EVENT = 0, 1
 PARAM_GAIN, PARAM_BIAS, PARAM_DECODERS = 0, 1, 2
-STATE_VOLTAGE, STATE_REFRACTORY, STATE_SYNAPSE, STATE_PROBE_SYNAPSE = 0, 1, 2, 3
+(STATE_VOLTAGE, STATE_REFRACTORY, STATE_SYNAPSE, STATE_PROBE_SYNAPSE, STATE_LEARNED_DECODERS,
+ STATE_PES_ACTIVITY) = range(6)
 (OP_FEED, OP_RESET, OP_COPY, OP_COPY_INC, OP_ELEMENTWISE_INC, OP_DOT_INC, OP_LIF, OP_LIF_RATE, OP_LOWPASS,
- OP_ENSEMBLE, OP_SYNAPSE_SCATTER) = range(11)
+ OP_ENSEMBLE, OP_SYNAPSE_SCATTER, OP_LEARNED_DECODE, OP_PES, OP_PES_DECODE_UPDATE) = range(14)
 
 _dp = C.POINTER(C.c_double)
 _fp = C.POINTER(C.c_float)
@@ -81,6 +82,7 @@ _SIGNATURES = [
     ("ms_model_add_ensemble", [C.c_void_p, C.POINTER(EnsembleDesc), C.POINTER(_i32)], _i32),
     ("ms_model_add_connection", [C.c_void_p, C.POINTER(ConnectionDesc), C.POINTER(_i32)], _i32),
     ("ms_model_add_probe", [C.c_void_p, C.POINTER(ProbeDesc), C.POINTER(_i32)], _i32),
+    ("ms_model_set_pes", [C.c_void_p, _i32, C.c_double, C.c_double], _i32),
     ("ms_sim_opts_default", [C.POINTER(SimOpts)], None),
     ("ms_plan_create", [C.c_void_p, C.POINTER(SimOpts), C.POINTER(C.c_void_p)], _i32),
     ("ms_plan_destroy", [C.c_void_p], None),
@@ -139,7 +141,7 @@ def _f64(a) -> np.ndarray:
     return np.ascontiguousarray(np.asarray(a, dtype=np.float64))
 
 
-_KINDS = {"node": REF_NODE, "ens": REF_ENS, "neurons": REF_NEURONS}
+_KINDS = {"node": REF_NODE, "ens": REF_ENS, "neurons": REF_NEURONS, "learning": REF_LEARNING}
 
 
 class Model:
@@ -213,7 +215,15 @@ class Model:
         d.synapse_tau = float(conn.synapse) if conn.synapse is not None else 0.0
         out = _i32()
         _check(self._lib.ms_model_add_connection(self.handle, C.byref(d), C.byref(out)))
+        rule = getattr(conn, "learning_rule", None)
+        if rule is not None:
+            self.set_pes(out.value, rule.learning_rate, rule.pre_synapse)
         return out.value
+
+    def set_pes(self, conn_id: int, learning_rate: float, pre_synapse=None) -> None:
+        """PES learning on connection conn_id's decoders (ms_model_set_pes)."""
+        _check(self._lib.ms_model_set_pes(self.handle, int(conn_id), float(learning_rate),
+                                          0.0 if pre_synapse is None else float(pre_synapse)))
 
     def add_probe(self, probe) -> int:
         d = ProbeDesc()

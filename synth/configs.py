@@ -14,6 +14,8 @@ parameters unchanged.
   bg  basal-ganglia-shaped: five arrays of D one-dimensional ensembles (striatum
       D1 and D2, STN, GPi, GPe) with one-to-one and all-to-all array transforms
       (paper Sec. 5.1 "basal_ganglia"; used for the planner ablation)
+  pes online learning: a D-dimensional ensemble whose output weights learn the
+      identity by PES, 10 batch rows (paper Sec. 5.1 "pes", Fig. 7)
 
 All values are synthetic; no dataset is read or reproduced.
 """
@@ -23,9 +25,9 @@ from typing import Dict, Optional
 
 import numpy as np
 
-from .spec import Connection, Ensemble, ModelSpec, Node, Probe, Workload
+from .spec import PES, Connection, Ensemble, ModelSpec, Node, Probe, Workload
 
-CONFIG_NAMES = ("c1", "c2", "c3", "c4", "c5", "bg")
+CONFIG_NAMES = ("c1", "c2", "c3", "c4", "c5", "bg", "pes")
 
 
 def _rng(seed: int, index: int) -> np.random.Generator:
@@ -314,10 +316,46 @@ def make_bg(neuron_type="lif", n_steps=1000, minibatch=1, D=64, n_neurons=50, n_
                     notes="basal-ganglia shaped: 5 arrays of D 1-D ensembles, one-to-one and all-to-all")
 
 
-_MAKERS = {"c1": make_c1, "c2": make_c2, "c3": make_c3, "c4": make_c4, "c5": make_c5, "bg": make_bg}
+# ---------------------------------------------------------------------------- pes
+def make_pes(neuron_type="lif", n_steps=1000, minibatch=10, D=192, neurons_per_dim=50,
+             learning_rate=1e-4, pre_synapse=0.005, n_eval=100) -> Workload:
+    """Online-learning benchmark shape (paper Sec. 5.1 "pes": an ensemble whose
+    output weights learn by PES; Figs. 6 and 7 vary D over 64, 128, 192 and
+    batch 10 inputs).  A D-dimensional input node drives an ensemble of
+    neurons_per_dim * D neurons (lowpass 0.005).  The ensemble reaches a
+    passthrough output node through a connection with zero initial decoders
+    that learns by PES (learning rate 1e-4, pre activities lowpass 0.005;
+    lowpass 0.005 on the connection); its error is output minus input (two
+    connections into the rule, lowpass 0.005 each).  Probed: the output node
+    (lowpass 0.01).  Feed: per batch row and dimension 0.5 sin(2 pi f t +
+    phase), f ~ U[1, 5] Hz, phase ~ U[0, 2 pi)."""
+    seed = 7
+    m = ModelSpec(dt=0.001)
+    n = neurons_per_dim * D
+    inp = m.add_node(Node(size=D))
+    out = m.add_node(Node(size=D, passthrough=True))
+    e = m.add_ensemble(lif_ensemble(_rng(seed, 100), n, D, n_eval, neuron_type))
+    syn = 0.005
+    m.connect(Connection(pre=inp, post=("ens", e), transform=1.0, synapse=syn))
+    c = m.connect(Connection(pre=("ens", e), post=out, decoders=np.zeros((n, D)), synapse=syn,
+                             learning_rule=PES(learning_rate=learning_rate, pre_synapse=pre_synapse)))
+    m.connect(Connection(pre=out, post=("learning", c), transform=1.0, synapse=syn))
+    m.connect(Connection(pre=inp, post=("learning", c), transform=-1.0, synapse=syn))
+    m.probe(Probe(target=out, synapse=0.01))
+    rng = _rng(seed, 1)
+    f = rng.uniform(1.0, 5.0, size=(minibatch, 1, D))
+    ph = rng.uniform(0.0, 2 * np.pi, size=(minibatch, 1, D))
+    t = (np.arange(1, n_steps + 1) * m.dt)[None, :, None]
+    feed = 0.5 * np.sin(2 * np.pi * f * t + ph)
+    return Workload("pes", m, minibatch, n_steps, {inp[1]: feed.astype(np.float32)},
+                    notes="PES learning of the identity, zero initial decoders, per-batch-row weights")
+
+
+_MAKERS = {"c1": make_c1, "c2": make_c2, "c3": make_c3, "c4": make_c4, "c5": make_c5, "bg": make_bg,
+           "pes": make_pes}
 
 
 def make_workload(name: str, **overrides) -> Workload:
-    """Build workload ``name`` ("c1".."c5"); keyword overrides shrink it for tests
+    """Build workload ``name`` ("c1".."c5", "bg", "pes"); keyword overrides shrink it for tests
     (n_steps, minibatch, n_ens, n_neurons, neuron_type, ...)."""
     return _MAKERS[name](**overrides)

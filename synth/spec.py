@@ -9,6 +9,7 @@ Object references are (kind, index) pairs:
                    the ensemble's represented input                 -- post
   ("neurons", i)   spike output of ensemble i's neurons            -- pre / probe
                    the neurons' input current (scaled by gain)     -- post
+  ("learning", c)  error input of connection c's learning rule     -- post only
 """
 from __future__ import annotations
 
@@ -44,6 +45,18 @@ class Node:
 
 
 @dataclass
+class PES:
+    """Prescribed Error Sensitivity rule on a decoded connection's output
+    weights (paper Sec. 5.1, the pes benchmark; MacNeil and Eliasmith 2011).
+    Every step each batch row's decoders move against the error:
+    D <- D - (learning_rate * dt / n) * outer(pre activities, error), the pre
+    activities lowpass-filtered with time constant pre_synapse (None: this
+    step's activities)."""
+    learning_rate: float = 1e-4
+    pre_synapse: Optional[float] = 0.005
+
+
+@dataclass
 class Connection:
     pre: Ref
     post: Ref
@@ -54,6 +67,7 @@ class Connection:
     synapse: Optional[float] = None      # lowpass time constant in s; None = no filter
     pre_slice: Optional[Tuple[int, int]] = None   # [start, stop) of the pre output
     post_slice: Optional[Tuple[int, int]] = None  # [start, stop) of the post input
+    learning_rule: Optional[PES] = None  # decoded connections only: per-batch learned decoders
 
 
 @dataclass

@@ -78,11 +78,14 @@ class PlanExecutor:
         self.j = plan.json()
         self.B = minibatch
         self.spec = spec
+        self.params_from = params_from
         self.bases = []
         for bi, b in enumerate(self.j["bases"]):
             if b["name"] == "state":
                 self.bases.append(None)
                 self.state_base = bi
+                # initial value of every row (learned decoders; zeros elsewhere)
+                self.init = plan.base(bi).astype(np.float64).reshape(b["rows"])
             elif params_from is None:
                 self.bases.append(plan.base(bi).astype(np.float64).reshape(b["rows"], b["cols"]))
             else:
@@ -107,7 +110,7 @@ class PlanExecutor:
             if g["type"] == "Reset" and "values" in g:
                 rows = {sg["name"]: sg["rows"] for sg in self.j["signals"]}
                 dst = {"reset": "out", "resetx": "x", "resetid": "did", "resetprod": "dprod",
-                       "resetv": "v", "resetd": "xd"}
+                       "resetv": "v", "resetd": "xd", "resete": "E"}
                 vals = []
                 for name in g["ops"]:
                     owner, kind = name.split(".", 1)
@@ -132,19 +135,32 @@ class PlanExecutor:
                 g["tau_rc"] = [e.tau_rc for e in ens]
                 g["tau_ref"] = [e.tau_ref for e in ens]
                 g["amp"] = [e.amplitude for e in ens]
+            elif g["type"] in ("PES", "PESDecodeUpdate"):
+                g["coef"] = [-o.pes_coef[int(name.split(".")[0][1:])] for name in g["ops"]
+                             if name.endswith(".pes")]
             elif g["type"] == "Lowpass":
                 ca, cb = [], []
                 for name in g["ops"]:
-                    owner = name.split(".")[0]
+                    owner, kind = name.split(".", 1)
                     i = int(owner[1:])
-                    a, b = (o.conn_a[i] if owner[0] == "c" else o.probe_a[i])
-                    w = (o.y[i] if owner[0] == "c" else o.yp[i]).shape[1]
+                    if kind == "presyn":      # a PES rule's activity filter
+                        a, b = o.pes_a[i]
+                        w = o.abar[i].shape[1]
+                    else:
+                        a, b = (o.conn_a[i] if owner[0] == "c" else o.probe_a[i])
+                        w = (o.y[i] if owner[0] == "c" else o.yp[i]).shape[1]
                     ca.append(np.full(w, a)); cb.append(np.full(w, b))
                 g["ca"] = np.concatenate(ca).tolist()
                 g["cb"] = np.concatenate(cb).tolist()
 
     def reset(self):
-        self.st = np.zeros((self.rows, self.B))
+        self.st = np.repeat(self.init[:, None], self.B, axis=1)
+        if self.params_from is not None:      # learned decoders from the oracle's values
+            for sg in self.j["signals"]:
+                owner, kind = sg["name"].split(".", 1)
+                if kind == "W":
+                    W = self.params_from.conn_dec[int(owner[1:])]
+                    self.st[sg["offset"]:sg["offset"] + sg["rows"]] = W.reshape(-1)[:, None]
         self.records = []
 
     def _src(self, arr, base, rows):
@@ -192,6 +208,18 @@ class PlanExecutor:
             for w0, x0, d0 in zip(g["w_row"], g["x_row"], g["d_row"]):
                 Wm = W[w0:w0 + M, :K] if W.shape[1] == K else W[w0:w0 + M * K, 0].reshape(M, K)
                 cur[d0:d0 + M] += Wm @ src[x0:x0 + K]
+        elif t in ("LearnedDotInc", "PES", "PESDecodeUpdate"):
+            M, K = g["M"], g["K"]
+            for o in range(n):
+                w0, x0 = g["w_row"][o], g["x_row"][o]
+                W = cur[w0:w0 + K * M].reshape(K, M, self.B)      # row i*M + j: neuron i, output j
+                if t != "PES":
+                    d0 = g["d_row"][o]
+                    cur[d0:d0 + M] += np.einsum("kmb,kb->mb", W, src[x0:x0 + K])
+                if t != "LearnedDotInc":
+                    a0 = g["act_row"][o] if t == "PESDecodeUpdate" else x0
+                    e0 = g["e_row"][o]
+                    W += g["coef"][o] * src[a0:a0 + K][:, None, :] * src[e0:e0 + M][None, :, :]
         elif t in ("SimLIF", "SimLIFRate"):
             J = src[_rows(g["src"], n)]
             trc = _vec(g["tau_rc"], n)[:, None]

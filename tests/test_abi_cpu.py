@@ -97,8 +97,9 @@ def test_plan_json_sizes_with_zero_capacity():
 
 
 def test_sim_creation_without_gpu_fails_cleanly():
-    import torch
-    if torch.cuda.is_available():
+    # the GPU driver's device node, checked without starting a GPU runtime in
+    # this process (torch brings its own HIP runtime besides the library's)
+    if os.path.exists("/dev/kfd"):
         pytest.skip("a GPU is present")
     w = make_workload("c1", n_steps=5)
     code, msg = _status_of(lambda: M.Simulator(M.model_from_spec(w.spec)))

@@ -16,7 +16,7 @@ import pytest
 
 import paper_1805_11144_amd as M
 from oracle.neurons import lif_step
-from synth.spec import Ensemble, ModelSpec, Probe
+from synth.spec import Connection, Ensemble, ModelSpec, Node, Probe
 
 pytestmark = pytest.mark.gpu
 
@@ -50,12 +50,17 @@ def _inputs(n, B, seed):
     return J.astype(np.float32), V.astype(np.float32), R.astype(np.float32)
 
 
-def _model(J):
+def _model(J, with_input=False):
+    """with_input: a node feeding zeros into the ensemble (J = bias + 0), so
+    that the kernels for ensembles with encoders run."""
     n = len(J)
     spec = ModelSpec(dt=DT)
     spec.add_ensemble(Ensemble(n_neurons=n, dims=1, encoders=np.ones((n, 1)), eval_points=np.zeros((1, 1)),
                                gains=np.ones(n), biases=J.astype(np.float64), tau_rc=TAU_RC, tau_ref=TAU_REF))
     spec.probe(Probe(target=("neurons", 0)))
+    if with_input:
+        inp = spec.add_node(Node(size=1))
+        spec.connect(Connection(pre=inp, post=("ens", 0)))
     return spec
 
 
@@ -66,6 +71,7 @@ KERNELS = {
     "k_persistent": dict(driver=M.DRIVER_PERSISTENT, B=2),
     "k_lif": dict(driver=M.DRIVER_STEPS, B=4, fuse=False),
     "k_w_lif": dict(driver=M.DRIVER_WINDOW, B=4, fuse=False),
+    "k_ens_big": dict(driver=M.DRIVER_STEPS, B=5, with_input=True),   # n >= 512, B <= 16, no decoders
 }
 
 
@@ -74,8 +80,11 @@ KERNELS = {
 def test_lif_edge_cases(kernel, n):
     cfg = dict(KERNELS[kernel])
     B = cfg.pop("B")
+    with_input = cfg.pop("with_input", False)
+    if kernel == "k_ens_big" and n < 512:
+        pytest.skip("the large-ensemble kernel takes ensembles of 512 neurons or more")
     J, V, R = _inputs(n, B, seed=n)
-    spec = _model(J)
+    spec = _model(J, with_input)
     with M.Simulator(M.model_from_spec(spec), minibatch=B, probe_capacity_steps=1, **cfg) as sim:
         sim.set_state(M.mergesim.STATE_VOLTAGE, 0, V)
         sim.set_state(M.mergesim.STATE_REFRACTORY, 0, R)

@@ -14,8 +14,9 @@ CASES = {
     "c4": dict(n_steps=2, minibatch=1, n_ens=12, n_neurons=30, n_eval=40),
     "c5": dict(n_steps=2, n_ens=15, n_neurons=30, n_eval=40, n_input_targets=5, n_probed=4),
     "bg": dict(n_steps=2, D=5, n_neurons=20, n_eval=40),
+    "pes": dict(n_steps=2, minibatch=2, D=6, neurons_per_dim=5),
 }
-FLOAT_KEYS = {"values", "tau_rc", "tau_ref", "amp", "ca", "cb"}
+FLOAT_KEYS = {"values", "tau_rc", "tau_ref", "amp", "ca", "cb", "coef"}
 
 
 def _strip(plan):
