@@ -297,12 +297,17 @@ typedef struct {
  * listed read zeros.  Asynchronous with respect to the host unless a probe or
  * state read follows; ms_sim_sync waits. */
 ms_status ms_sim_run_steps(ms_sim* sim, int64_t n_steps, const ms_feed* feeds, int32_t n_feeds);
+/* Wait until every launch of earlier ms_sim_run_steps calls has finished (the
+ * paper's run_steps returns with the steps done, Sec. 3.1; here the wait is
+ * explicit so that runs can be queued). */
 ms_status ms_sim_sync(ms_sim* sim);
 
-/* Number of steps recorded since creation or the last reset. */
+/* Number of steps recorded since creation or the last reset (the time axis of
+ * the probe data, Sec. 3.1). */
 ms_status ms_sim_steps(const ms_sim* sim, int64_t* n_steps_out);
 
-/* Probe width (values per batch row per step). */
+/* Probe width: values per batch row per step, the last axis of the probe data
+ * [batch, steps, width] (Sec. 3.1). */
 ms_status ms_sim_probe_width(const ms_sim* sim, int32_t probe_id, int32_t* width_out);
 
 /* Copy probe `probe_id`'s record, [minibatch][steps][width] float32, into `out`
@@ -345,11 +350,14 @@ ms_status ms_sim_get_state(ms_sim* sim, int32_t which, int32_t id, float* out, i
 ms_status ms_sim_set_state(ms_sim* sim, int32_t which, int32_t id, const float* in, int64_t n_elems);
 
 /* Per-run timing of the last ms_sim_run_steps (HIP events on the simulator's
- * stream around the simulation launches, excluding feed staging); ms. */
+ * stream around the simulation launches, excluding feed staging); ms.  The
+ * quantity behind the speed comparisons of Sec. 5.1 (simulation time of a
+ * run, repeated and averaged). */
 ms_status ms_sim_last_run_ms(ms_sim* sim, double* ms_out);
 
 /* The driver actually used (MS_DRIVER_STEPS/GRAPH/PERSISTENT/WINDOW) and the
- * number of merged groups executed per step (WINDOW: launches per window). */
+ * number of merged groups executed per step (WINDOW: launches per window) --
+ * the count that operator merging reduces (Sec. 4.2, Fig. 8). */
 ms_status ms_sim_info(const ms_sim* sim, int32_t* driver_out, int32_t* groups_per_step_out);
 
 /* Merged operator types (the groups a plan is made of, paper Sec. 4.2). */
@@ -369,16 +377,20 @@ ms_status ms_sim_info(const ms_sim* sim, int32_t* driver_out, int32_t* groups_pe
 #define MS_OP_PES_DECODE_UPDATE 13 /* both in one pass over the decoders (launch drivers,
                                       when the error is known before the decode) */
 
-/* Per-kernel timing for measurement.  With timing on (on != 0), every kernel
- * launch of a merged group is bracketed by HIP events recorded on the stream
- * the launch runs on; ms_sim_kernel_time then returns, for operator type
- * `op_type` (MS_OP_*) during the last ms_sim_run_steps call (it waits for that
- * call to finish), the busy time in ms -- the length of the union of those
- * launches' intervals, so that launches running at once on different streams
- * count once (it equals the summed durations when they do not overlap) -- and
- * the number of launches.  Only the WINDOW and STEPS drivers time individual
- * launches (MS_E_STATE otherwise).  Timing adds event records to every
- * launch: leave it off for throughput runs. */
+/* Per-kernel timing for measurement (the cost of each kind of merged operator
+ * group, Sec. 4.2 and 5.1).  With timing on (on != 0), every merged group's
+ * launch is timed: on the STEPS driver its kernels are launched with
+ * hipExtLaunchKernelGGL, the first recording the group's begin event when it
+ * starts executing and each recording the end event when it finishes, so that
+ * host launch latency is not counted; on the WINDOW driver HIP events are
+ * recorded on the stream the launch runs on.  ms_sim_kernel_time then returns,
+ * for operator type `op_type` (MS_OP_*) during the last ms_sim_run_steps call
+ * (it waits for that call to finish), the busy time in ms -- the length of the
+ * union of those launches' intervals, so that launches running at once on
+ * different streams count once (it equals the summed durations when they do
+ * not overlap) -- and the number of launches.  Only the WINDOW and STEPS
+ * drivers time individual launches (MS_E_STATE otherwise).  Timing adds event
+ * records to every launch: leave it off for throughput runs. */
 ms_status ms_sim_set_timing(ms_sim* sim, int32_t on);
 ms_status ms_sim_kernel_time(ms_sim* sim, int32_t op_type, double* ms_out, int64_t* launches_out);
 
