@@ -256,24 +256,51 @@ __device__ __forceinline__ float neuron_update(int ntype, float j, float& v, flo
   return 0.0f;
 }
 
-// Branch-free form of the spiking update above for dt / tau_rc <= 1/16 (the
-// partial-step factor always comes from the polynomial, and a crossing's
-// overshoot ratio q stays below 1 - exp(-1/16) < 1/16, so -ln(1 - q) always
-// comes from the series): the same formulas, with every path computed and the
-// results selected, so that lanes whose neurons spike or sit in their
-// refractory period do not serialise the wavefront.  Returns the neuron output
-// (amp_dt = amplitude / dt or 0).
+// Shorter polynomials for the branch-free update below, where |x| <= 1/16 and
+// 0 <= q <= 1/16: expm1 to degree 5 (truncation below 2e-9 relative) and
+// -ln(1 - q) = q (1 + q/2 + ... + q^5/6) (truncation below 1e-8 relative),
+// both well under float32 rounding.
+__device__ __forceinline__ float expm1_bf(float x) {
+  float p = 1.0f / 120.0f;
+  p = fmaf(p, x, 1.0f / 24.0f);
+  p = fmaf(p, x, 1.0f / 6.0f);
+  p = fmaf(p, x, 0.5f);
+  p = fmaf(p, x, 1.0f);
+  return p * x;
+}
+
+__device__ __forceinline__ float neg_log1m_bf(float q) {
+  float p = 1.0f / 6.0f;
+  p = fmaf(p, q, 1.0f / 5.0f);
+  p = fmaf(p, q, 1.0f / 4.0f);
+  p = fmaf(p, q, 1.0f / 3.0f);
+  p = fmaf(p, q, 0.5f);
+  p = fmaf(p, q, 1.0f);
+  return p * q;
+}
+
+// Branch-free form of the spiking update above for dt / tau_rc <= 1/16, with
+// every path computed and the results selected, so that lanes whose neurons
+// spike or sit in their refractory period do not serialise the wavefront:
+//   * the partial-step factor comes from the polynomial on every lane (at a
+//     whole step it is expm1(-dt / tau_rc) to within rounding, so the
+//     refractory state needs no select);
+//   * a crossing's overshoot ratio q stays below 1 - exp(-1/16) < 1/16 on any
+//     trajectory from V <= 1, so -ln(1 - q) comes from the series;
+//   * the crossing time is min(tau_rc (-ln(1 - q)), integ) when J > 1: the
+//     series grows with q, and for q >= 1 (a voltage above threshold set from
+//     outside) it exceeds tau_rc >= 16 dt >= integ, so the clamp of the
+//     crossing to the start of the step needs no test of its own.
+// Returns the neuron output (amp_dt = amplitude / dt or 0).
 __device__ __forceinline__ float lif_update_bf(float j, float& v, float& rf, float tau_rc, float tau_ref,
-                                               float amp_dt, float full, float dt, float inv_tau) {
+                                               float amp_dt, float dt, float inv_tau) {
   const float integ = __builtin_amdgcn_fmed3f(dt - rf, 0.0f, dt);   // clamp to [0, dt] (v_med3_f32)
-  const float ep = expm1_small(-integ * inv_tau);
-  const float e = rf > 0.0f ? ep : full;
+  const float e = expm1_bf(-integ * inv_tau);
   v = v - (j - v) * e;
   rf = fmaxf(rf - dt, 0.0f);
   const float drive = j - 1.0f;
   const float q = (v - 1.0f) * __builtin_amdgcn_rcpf(drive);
-  const float lg = tau_rc * neg_log1m_small(q);
-  float since = drive > 0.0f ? (q >= 1.0f || lg > integ ? integ : lg) : 0.0f;
+  float since = drive > 0.0f ? fminf(tau_rc * neg_log1m_bf(q), integ) : 0.0f;
   // an empty asm statement that takes the crossing time as an operand: it is
   // computed on every lane, so the compiler selects instead of branching on
   // the spike (a branch runs both sides anyway when the lanes disagree)

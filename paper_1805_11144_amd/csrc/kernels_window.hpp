@@ -133,7 +133,7 @@ __global__ void k_w_lif(WView w, int64_t rows, Opnd J, Opnd s, Opnd V, Opnd R, f
     const float amp_dt = amp / dt;
     for (int32_t t = 0; t < w.T; ++t) {
       const float j = w.va[jr + (int64_t)t * w.B];
-      w.va[sr + (int64_t)t * w.B] = lif_update_bf(j, v, rf, tau_rc, tau_ref, amp_dt, full, dt, inv_tau);
+      w.va[sr + (int64_t)t * w.B] = lif_update_bf(j, v, rf, tau_rc, tau_ref, amp_dt, dt, inv_tau);
     }
   } else {
     for (int32_t t = 0; t < w.T; ++t) {
@@ -233,10 +233,15 @@ constexpr int kEnsXPre = 4;        // prefetched input values per thread
 // large to stage in LDS.
 constexpr int kRwTiles = 4, kRwKd = 4, kRwKs = 16;
 
+// Smallest stride >= x that is 2 mod 4: rows of that stride put lanes i and
+// i + 1 of a 16-lane group (rows i, i + 1; two adjacent columns per group)
+// in 32 different banks.
+__host__ __device__ inline int32_t stride2mod4(int32_t x) { return x + ((6 - x % 4) % 4); }
+
 template <int NPT, bool RW>
 __global__ void __launch_bounds__(512) k_w_ens(WView w, float* pa, EnsDesc E, float dt, int32_t nmax,
                                                int32_t ts, int32_t cpw, int32_t kch, int xblk, int enc_lds,
-                                               int dec_lds, int32_t nops) {
+                                               int dec_lds, int32_t nops, int32_t xs, int32_t js) {
   extern __shared__ float lds[];
   const uint32_t ncg = ((uint32_t)w.B + cpw - 1) / cpw, total = (uint32_t)nops * ncg, chunk = (total + 7) / 8;
   const uint32_t L = (blockIdx.x % 8) * chunk + blockIdx.x / 8;
@@ -249,12 +254,15 @@ __global__ void __launch_bounds__(512) k_w_ens(WView w, float* pa, EnsDesc E, fl
   const int d = o.x >= 0 ? E.d : 0, ndec = E.ndec, df0 = E.df[0];
   const int dp = E.d > 0 ? E.d : 1;
   const int ncol = cpw * ts, ctiles = ncol / 16;
-  float* X = lds;                                   // [ncol][dp]
-  float* Jb = X + ncol * dp;                        // [ncol][nmax]: currents, then outputs
-  float* red = Jb + (int64_t)ncol * nmax;           // [ctiles][kch][16][16]
+  // LDS rows are padded (xs >= dp, js >= nmax) so that the products' lanes,
+  // 16 columns apart, fall into different banks
+  float* X = lds;                                   // [ncol][xs]
+  float* Jb = X + ncol * xs;                        // [ncol][js]: currents, then outputs
+  float* red = Jb + (int64_t)ncol * js;             // [ctiles][kch][16][16]
   float* Bl = red + ctiles * kch * 256;             // [nmax] biases, [nmax][dp] encoders (enc_lds)
-  float* El = Bl + nmax;
-  float* Dl = El + (enc_lds ? nmax * dp : 0);       // [ndec][nmax] decoders (dec_lds)
+  float* El = Bl + nmax;                            // rows of stride xs
+  const int ds = stride2mod4(nmax);
+  float* Dl = El + (enc_lds ? nmax * xs : 0);       // [ndec][ds] decoders (dec_lds)
   gptr<float> enc = G(E.enc) + (int64_t)o.enc * E.d;
   gptr<float> bias = G(E.bias) + o.bias;
   gptr<float> D0 = G(E.D[0]) + (int64_t)o.D[0] * E.Dcols[0];
@@ -281,17 +289,17 @@ __global__ void __launch_bounds__(512) k_w_ens(WView w, float* pa, EnsDesc E, fl
     const int tsv = min(ts, w.T);
     for (int i = tid; i < ncol * d; i += nthr) {
       const int col = i / d, k = i - col * d;
-      X[col * dp + k] = stage_x(i, 0, tsv);
+      X[col * xs + k] = stage_x(i, 0, tsv);
     }
   }
   // per-op constants: biases always, encoders and decoders when they fit
   for (int r = tid; r < n; r += nthr) Bl[r] = bias[r];
   if (enc_lds)
-    for (int i = tid; i < n * d; i += nthr) El[(i / d) * dp + i % d] = enc[(int64_t)i];
+    for (int i = tid; i < n * d; i += nthr) El[(i / d) * xs + i % d] = enc[(int64_t)i];
   if (dec_lds)
     for (int i = tid; i < ndec * n; i += nthr) {
       const int q = i / n, r = i - q * n;
-      Dl[q * nmax + r] = (q < df0 ? D0 + (int64_t)q * s0 : D1 + (int64_t)(q - df0) * s1)[r];
+      Dl[q * ds + r] = (q < df0 ? D0 + (int64_t)q * s0 : D1 + (int64_t)(q - df0) * s1)[r];
     }
   __syncthreads();
   const int ntile = (n + 15) / 16, kd = (d + 3) / 4;
@@ -299,21 +307,23 @@ __global__ void __launch_bounds__(512) k_w_ens(WView w, float* pa, EnsDesc E, fl
   gptr<float> drow = qa < df0 ? D0 + (int64_t)qa * s0 : D1 + (int64_t)(qa - df0) * s1;
   const int ksteps = (n + 4 * kch - 1) / (4 * kch);
   // Slots that stay fixed for the whole window, so that the sub-window loop
-  // does no integer division: input value tid + c*nthr of a sub-window (its
-  // LDS index, as dp == d whenever d > 0) is step st, column cc, dimension k,
-  // packed st | cc << 7 | k << 16, st = 127 for a column beyond B, -1 past the
-  // inputs; output tid is step st, column c, decoded dimension q, packed the
-  // same way (st | c << 7 | q << 16), -1 past the outputs.  The host keeps
-  // ts <= 64, cpw <= 512 and d, ndec < 32768.
-  int32_t xslot[kEnsXPre];
+  // does no integer division: input value tid + c*nthr of a sub-window is
+  // step st, column cc, dimension k, packed st | cc << 7 | k << 16, -1 past the
+  // inputs or for a column beyond B (which keeps the zeros staged above), with
+  // its LDS index in xlds; output tid is step st, column c, decoded dimension
+  // q, packed the same way (st | c << 7 | q << 16), -1 past the outputs.  The
+  // host keeps ts <= 64, cpw <= 512 and d, ndec < 32768.
+  int32_t xslot[kEnsXPre], xlds[kEnsXPre];
 #pragma unroll
   for (int c = 0; c < kEnsXPre; ++c) {
     const int i = tid + c * nthr;
     if (i < ncol * d) {
       const int col = i / d, k = i - col * d, cc = col / ts, st = col - cc * ts;
-      xslot[c] = (b0 + cc < w.B ? st : 127) | (cc << 7) | (k << 16);
+      xslot[c] = b0 + cc < w.B ? st | (cc << 7) | (k << 16) : -1;
+      xlds[c] = col * xs + k;
     } else {
       xslot[c] = -1;
+      xlds[c] = 0;
     }
   }
   int32_t oslot = -1;
@@ -363,14 +373,14 @@ __global__ void __launch_bounds__(512) k_w_ens(WView w, float* pa, EnsDesc E, fl
             for (int kk = 0; kk < kRwKd; ++kk) {
               if (kk < kd) {
                 const int k = 4 * kk + lane / 16;
-                const float xb = k < d ? X[col * dp + k] : 0.0f;
+                const float xb = k < d ? X[col * xs + k] : 0.0f;
                 acc = __builtin_amdgcn_mfma_f32_16x16x4f32(ae[i][kk], xb, acc, 0, 0, 0);
               }
             }
 #pragma unroll
             for (int q = 0; q < 4; ++q) {
               const int r = 16 * nt + 4 * (lane / 16) + q;
-              if (r < n) Jb[col * nmax + r] = acc[q] + Bl[r];
+              if (r < n) Jb[col * js + r] = acc[q] + Bl[r];
             }
           }
         }
@@ -382,25 +392,25 @@ __global__ void __launch_bounds__(512) k_w_ens(WView w, float* pa, EnsDesc E, fl
       mfma_f4x acc = {0.0f, 0.0f, 0.0f, 0.0f};
       for (int kk = 0; kk < kd; ++kk) {
         const int ra = 16 * nt + lane % 16, k = 4 * kk + lane / 16;
-        const float a = (ra < n && k < d) ? (enc_lds ? El[ra * dp + k] : enc[(int64_t)ra * E.d + k]) : 0.0f;
-        const float xb = k < d ? X[col * dp + k] : 0.0f;
+        const float a = (ra < n && k < d) ? (enc_lds ? El[ra * xs + k] : enc[(int64_t)ra * E.d + k]) : 0.0f;
+        const float xb = k < d ? X[col * xs + k] : 0.0f;
         acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a, xb, acc, 0, 0, 0);
       }
 #pragma unroll
       for (int q = 0; q < 4; ++q) {
         const int r = 16 * nt + 4 * (lane / 16) + q;
-        if (r < n) Jb[col * nmax + r] = acc[q] + Bl[r];
+        if (r < n) Jb[col * js + r] = acc[q] + Bl[r];
       }
     }
     __syncthreads();
     // next inputs into LDS (every read of this sub-window's X is done)
 #pragma unroll
     for (int c = 0; c < kEnsXPre; ++c)
-      if (tsn > 0 && xslot[c] >= 0) X[tid + c * nthr] = xpre[c];
+      if (tsn > 0 && xslot[c] >= 0) X[xlds[c]] = xpre[c];
     if (tsn > 0) {   // inputs beyond the prefetch registers
       for (int i = tid + kEnsXPre * nthr; i < ncol * d; i += nthr) {
         const int col = i / d, k = i - col * d;
-        X[col * dp + k] = stage_x(i, t1, tsn);
+        X[col * xs + k] = stage_x(i, t1, tsn);
       }
     }
     // 2. neurons through the sub-window
@@ -408,14 +418,13 @@ __global__ void __launch_bounds__(512) k_w_ens(WView w, float* pa, EnsDesc E, fl
     for (int j = 0; j < NPT; ++j) {
       const int g = tid + j * nthr, c = g / nmax, r = g - c * nmax;
       if (c < cpw && b0 + c < w.B && r < n) {
-        float* cell = Jb + (int64_t)c * ts * nmax + r;
+        float* cell = Jb + (int64_t)c * ts * js + r;
         if (bf) {
           for (int st = 0; st < tsv; ++st)
-            cell[st * nmax] = lif_update_bf(cell[st * nmax], v[j], rf[j], o.tau_rc, o.tau_ref, amp_dt, o.full, dt,
-                                            o.inv_tau);
+            cell[st * js] = lif_update_bf(cell[st * js], v[j], rf[j], o.tau_rc, o.tau_ref, amp_dt, dt, o.inv_tau);
         } else {
           for (int st = 0; st < tsv; ++st)
-            cell[st * nmax] = neuron_update(E.ntype, cell[st * nmax], v[j], rf[j], o.tau_rc, o.tau_ref, o.amp,
+            cell[st * js] = neuron_update(E.ntype, cell[st * js], v[j], rf[j], o.tau_rc, o.tau_ref, o.amp,
                                             o.full, dt, o.inv_tau);
         }
       }
@@ -431,7 +440,7 @@ __global__ void __launch_bounds__(512) k_w_ens(WView w, float* pa, EnsDesc E, fl
         for (int ks = 0; ks < kRwKs; ++ks) {
           if (ks < ksteps) {
             const int r = 4 * (kc + kch * ks) + lane / 16;
-            const float sb = r < n ? Jb[col * nmax + r] : 0.0f;
+            const float sb = r < n ? Jb[col * js + r] : 0.0f;
             acc = __builtin_amdgcn_mfma_f32_16x16x4f32(ad[ks], sb, acc, 0, 0, 0);
           }
         }
@@ -445,8 +454,8 @@ __global__ void __launch_bounds__(512) k_w_ens(WView w, float* pa, EnsDesc E, fl
         mfma_f4x acc = {0.0f, 0.0f, 0.0f, 0.0f};
         for (int ks = 0; ks < ksteps; ++ks) {
           const int r = 4 * (kc + kch * ks) + lane / 16;
-          const float a = (qa < ndec && r < n) ? (dec_lds ? Dl[qa * nmax + r] : drow[r]) : 0.0f;
-          const float sb = r < n ? Jb[col * nmax + r] : 0.0f;
+          const float a = (qa < ndec && r < n) ? (dec_lds ? Dl[qa * ds + r] : drow[r]) : 0.0f;
+          const float sb = r < n ? Jb[col * js + r] : 0.0f;
           acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a, sb, acc, 0, 0, 0);
         }
 #pragma unroll
@@ -476,7 +485,7 @@ __global__ void __launch_bounds__(512) k_w_ens(WView w, float* pa, EnsDesc E, fl
       for (int i = tid; i < ncol * n; i += nthr) {
         const int r = i / ncol, rem = i - r * ncol, st = rem / cpw, c = rem - st * cpw;
         if (st < tsv && b0 + c < w.B)
-          w.va[(int64_t)(o.s + r) * w.vs + (int64_t)(t0 + st + 1) * w.B + b0 + c] = Jb[(c * ts + st) * nmax + r];
+          w.va[(int64_t)(o.s + r) * w.vs + (int64_t)(t0 + st + 1) * w.B + b0 + c] = Jb[(c * ts + st) * js + r];
       }
     }
     __syncthreads();

@@ -72,6 +72,7 @@ struct Launch {
   int32_t src_blk = 1, a_blk = 1;    // block offsets of src / a (1: this step, 0: previous step)
   int32_t nmax = 0, npt = 1, nthr = 64, ts = 16, cpw = 1, kch = 1;   // fused-ensemble launch shape
   int32_t enc_lds = 0, dec_lds = 0, rw = 0;   // rw: encoder/decoder fragments held in registers
+  int32_t xs = 1, js = 1;            // LDS row strides of the inputs and currents (padded)
   size_t lds = 0;
   const uint16_t* w16 = nullptr;     // DOT_INC on bf16 MFMA: W rounded to bf16, op k at k*M*K
   // SYN_SCATTER
@@ -925,6 +926,10 @@ void ens_shape(ms_sim* s, Launch& l, const LGroup& g) {
   if (l.ens.d >= 32768 || l.ens.ndec >= 32768) fail(MS_E_INVALID, "ensemble dimensions too large for the window driver");
   l.npt = l.npt <= 1 ? 1 : l.npt <= 2 ? 2 : l.npt <= 4 ? 4 : 8;
   const int64_t nw = l.nthr / 64, dp = std::max<int32_t>(1, l.ens.d);
+  // LDS row strides: inputs and currents are read and written by lanes 16
+  // columns apart; padding the rows spreads those lanes over the banks
+  l.xs = stride2mod4((int32_t)dp);
+  l.js = nmax % 2 == 0 ? nmax + 1 : nmax;
   // sub-window: the longest (a multiple of 16, at most 64 steps) that keeps
   // about 32 wavefronts per CU resident within the CU's LDS and whose inputs
   // fit the per-thread prefetch registers (if none does, 16 steps, the rest of
@@ -935,10 +940,11 @@ void ens_shape(ms_sim* s, Launch& l, const LGroup& g) {
   // small (otherwise they are read through the caches)
   l.enc_lds = (int64_t)nmax * dp * 4 <= 16384 ? 1 : 0;
   l.dec_lds = (int64_t)l.ens.ndec * nmax * 4 <= 16384 ? 1 : 0;
-  const int64_t consts = nmax + (l.enc_lds ? (int64_t)nmax * dp : 0) + (l.dec_lds ? (int64_t)l.ens.ndec * nmax : 0);
+  const int64_t consts = nmax + (l.enc_lds ? (int64_t)nmax * l.xs : 0) +
+                        (l.dec_lds ? (int64_t)l.ens.ndec * stride2mod4(nmax) : 0);
   auto bytes = [&](int64_t ts) {
     const int64_t ncol = l.cpw * ts;
-    return (ncol * (dp + nmax) + (ncol / 16) * kch_of(ts) * 256 + consts) * (int64_t)sizeof(float);
+    return (ncol * (l.xs + l.js) + (ncol / 16) * kch_of(ts) * 256 + consts) * (int64_t)sizeof(float);
   };
   const int64_t wgs = std::max<int64_t>(1, 32 / nw);
   int64_t ts = 64;
@@ -957,7 +963,7 @@ void ens_shape(ms_sim* s, Launch& l, const LGroup& g) {
       nw % l.kch == 0 && ksteps <= 16) {
     l.rw = 1;
     l.enc_lds = l.dec_lds = 0;
-    l.lds = (size_t)((l.cpw * ts * (dp + nmax) + (l.cpw * ts / 16) * l.kch * 256 + nmax) * (int64_t)sizeof(float));
+    l.lds = (size_t)((l.cpw * ts * (l.xs + l.js) + (l.cpw * ts / 16) * l.kch * 256 + nmax) * (int64_t)sizeof(float));
   }
 }
 
@@ -1164,15 +1170,15 @@ void launch_phase(ms_sim* s, const Launch& l, int32_t T, int64_t t0, hipStream_t
       const dim3 grid((unsigned)(8 * ((total + 7) / 8)));
       const int32_t nops = (int32_t)l.rows;
       if (l.rw)
-        hipLaunchKernelGGL((k_w_ens<1, true>), grid, dim3(l.nthr), l.lds, q, w, s->pa, l.ens, s->dt, l.nmax, l.ts, l.cpw, l.kch, l.src_blk, l.enc_lds, l.dec_lds, nops);
+        hipLaunchKernelGGL((k_w_ens<1, true>), grid, dim3(l.nthr), l.lds, q, w, s->pa, l.ens, s->dt, l.nmax, l.ts, l.cpw, l.kch, l.src_blk, l.enc_lds, l.dec_lds, nops, l.xs, l.js);
       else if (l.npt == 1)
-        hipLaunchKernelGGL((k_w_ens<1, false>), grid, dim3(l.nthr), l.lds, q, w, s->pa, l.ens, s->dt, l.nmax, l.ts, l.cpw, l.kch, l.src_blk, l.enc_lds, l.dec_lds, nops);
+        hipLaunchKernelGGL((k_w_ens<1, false>), grid, dim3(l.nthr), l.lds, q, w, s->pa, l.ens, s->dt, l.nmax, l.ts, l.cpw, l.kch, l.src_blk, l.enc_lds, l.dec_lds, nops, l.xs, l.js);
       else if (l.npt == 2)
-        hipLaunchKernelGGL((k_w_ens<2, false>), grid, dim3(l.nthr), l.lds, q, w, s->pa, l.ens, s->dt, l.nmax, l.ts, l.cpw, l.kch, l.src_blk, l.enc_lds, l.dec_lds, nops);
+        hipLaunchKernelGGL((k_w_ens<2, false>), grid, dim3(l.nthr), l.lds, q, w, s->pa, l.ens, s->dt, l.nmax, l.ts, l.cpw, l.kch, l.src_blk, l.enc_lds, l.dec_lds, nops, l.xs, l.js);
       else if (l.npt == 4)
-        hipLaunchKernelGGL((k_w_ens<4, false>), grid, dim3(l.nthr), l.lds, q, w, s->pa, l.ens, s->dt, l.nmax, l.ts, l.cpw, l.kch, l.src_blk, l.enc_lds, l.dec_lds, nops);
+        hipLaunchKernelGGL((k_w_ens<4, false>), grid, dim3(l.nthr), l.lds, q, w, s->pa, l.ens, s->dt, l.nmax, l.ts, l.cpw, l.kch, l.src_blk, l.enc_lds, l.dec_lds, nops, l.xs, l.js);
       else
-        hipLaunchKernelGGL((k_w_ens<8, false>), grid, dim3(l.nthr), l.lds, q, w, s->pa, l.ens, s->dt, l.nmax, l.ts, l.cpw, l.kch, l.src_blk, l.enc_lds, l.dec_lds, nops);
+        hipLaunchKernelGGL((k_w_ens<8, false>), grid, dim3(l.nthr), l.lds, q, w, s->pa, l.ens, s->dt, l.nmax, l.ts, l.cpw, l.kch, l.src_blk, l.enc_lds, l.dec_lds, nops, l.xs, l.js);
       break;
     }
     default: fail(MS_E_INVALID, "unknown group type");
