@@ -767,6 +767,8 @@ __global__ void __launch_bounds__(256) k_ens_tile(float* st, Strides S, int32_t 
 // before their arithmetic; the next chunk's records are fetched meanwhile.
 // Row i's sum adds the chunk's values in connection order, read from lanes
 // i, i + 16, i + 32, i + 48 (first and second connection of each lane).
+// kw: K | weight slot << 16 | staged inputs << 20 | elementwise << 21 (then w
+// holds the float bits of the scale)
 struct SynConn {
   int32_t y, v, x, kw, w, p;
   float a, b;
@@ -874,8 +876,11 @@ __global__ void __launch_bounds__(256) k_syn_scatter(float* st, Strides S, int32
       if (!update || r.v == -2) continue;
       if (r.v >= 0) {
         v[h] = st[at(S, (int64_t)r.v + i, b)];
+      } else if (r.kw & (1 << 21)) {   // elementwise transform: scale (bits in w) times input row x + i
+        const float xi = (r.kw >> 20) & 1 ? stage[(tr * feed_rows + r.x + i) * B + b] : st[at(S, (int64_t)r.x + i, b)];
+        v[h] = 0.0f + __builtin_bit_cast(float, r.w) * xi;   // the increment adds into a reset row
       } else {
-        const int32_t K = r.kw & 0xffff, ws = (r.kw >> 16) & 15, staged = r.kw >> 20;
+        const int32_t K = r.kw & 0xffff, ws = (r.kw >> 16) & 15, staged = (r.kw >> 20) & 1;
         gptr<float> wr = G(W.w[ws]) + ((int64_t)r.w + i) * K;
         const float* xp = staged ? stage + (tr * feed_rows + r.x) * B + b : st + at(S, r.x, b);
         const int64_t xs = staged ? (int64_t)B : S.rs;

@@ -88,6 +88,17 @@ void append_ens(LGroup& A, const LGroup& B) {
 
 int64_t lrow(const LOperand& o, int64_t r) { return o.idx.empty() ? o.start + r : (int64_t)o.idx[r]; }
 
+LOperand rows_operand(int32_t base, const std::vector<int32_t>& rows) {
+  LOperand o;
+  o.base = base;
+  bool contig = true;
+  for (size_t i = 1; i < rows.size() && contig; ++i) contig = rows[i] == rows[0] + (int32_t)i;
+  if (contig) o.start = rows.empty() ? 0 : rows[0];
+  else o.idx = rows;
+  return o;
+}
+
+
 // Entries of an increment group (COPY_INC / ELEM_INC): ptr gives the entries of
 // unique destination u, or one entry per destination without ptr.
 int64_t n_entries(const LGroup& g) { return g.ptr.empty() ? g.rows : (int64_t)g.ptr.back(); }
@@ -163,8 +174,9 @@ void accesses(const IR& ir, int32_t sb, const LGroup& g, std::vector<int64_t>& r
 }
 
 // One connection of a fused segment: its value v for row i of the segment is
-// either state row v + i or the product of weight row w + i (slot ws, K wide)
-// with input rows x .. x + K - 1; its filter row is y + i.
+// either state row v + i, or the product of weight row w + i (slot ws, K wide)
+// with input rows x .. x + K - 1, or (ws == -2, an elementwise transform) the
+// scale whose float bits are w times input row x + i; its filter row is y + i.
 // v == -2 marks a probe copy: row y is read and recorded, nothing updated.
 // pr: the probe row that records row y (-1: none).
 // stage: the inputs x .. x + K - 1 are rows of the step's feed staging
@@ -177,6 +189,7 @@ struct Conn {
     if ((pr < 0) != (p.pr < 0) || (pr >= 0 && pr != p.pr + 1)) return false;
     if (v == -2 || p.v == -2) return v == p.v;
     if (v >= 0) return v == p.v + 1;
+    if (ws == -2 || p.ws == -2) return ws == p.ws && x == p.x + 1 && w == p.w;
     return ws == p.ws && x == p.x && K == p.K && w == p.w + 1;
   }
 };
@@ -198,6 +211,23 @@ struct Fuser {
   std::vector<int32_t> vcount;   // how often the filter group reads each row as its input
 
   bool no(const std::string& w) { why = w; return false; }
+
+  // value of row `row` of a one-column parameter base (the plan's float32 values)
+  std::map<int32_t, std::vector<float>> pbase;
+  float param_value(int32_t base, int64_t row) {
+    auto it = pbase.find(base);
+    if (it == pbase.end()) {
+      std::vector<float> v((size_t)p.base_rows[base] * p.ir.bases[base].cols, 0.0f);
+      for (size_t k = 0; k < p.ir.sigs.size(); ++k) {
+        const Signal& sg = p.ir.sigs[k];
+        if (sg.base != base) continue;
+        const size_t off = (size_t)p.sig_offset[k] * p.ir.bases[base].cols;
+        for (size_t j = 0; j < sg.value.size(); ++j) v[off + j] = (float)sg.value[j];
+      }
+      it = pbase.emplace(base, std::move(v)).first;
+    }
+    return it->second[(size_t)row * p.ir.bases[base].cols];
+  }
 
   bool run(std::vector<LGroup>& out, LGroup& prologue);
   bool fuse_with(int32_t ci, std::vector<LGroup>& out, LGroup& prologue);
@@ -277,7 +307,12 @@ bool Fuser::fuse_with(int32_t ci, std::vector<LGroup>& out, LGroup& prologue) {
   // product) and by one row of one DotInc op with constant weights, read only
   // by the filter, not probed, and with inputs that nothing rewrites before
   // the filter's place
-  struct Src { int32_t g = -1; int32_t op = -1; int32_t m = -1; int32_t writers = 0; int32_t first_reset = -1; };
+  // el: the row is the single entry of a CopyInc / ElementwiseInc (input row
+  // ex times scale) rather than a row of a DotInc op
+  struct Src {
+    int32_t g = -1; int32_t op = -1; int32_t m = -1; int32_t writers = 0; int32_t first_reset = -1;
+    bool el = false; int64_t ex = -1; float scale = 1.0f;
+  };
   std::vector<Src> vs((size_t)nrows);
   std::vector<int32_t> readers((size_t)nrows, 0), last_writer((size_t)nrows, -1);
   for (int32_t g = 0; g + 1 < n; ++g) {
@@ -297,6 +332,31 @@ bool Fuser::fuse_with(int32_t ci, std::vector<LGroup>& out, LGroup& prologue) {
       for (int64_t o = 0; o < q.rows; ++o)
         if (q.src.base == sb) for (int32_t k = 0; k < q.K; ++k) rd2.push_back(q.x_row[o] + k);
       rd.swap(rd2);
+    } else if ((q.type == OP_COPY_INC || q.type == OP_ELEM_INC) && q.dst.base == sb && q.src.base == sb && g != ci) {
+      // single-entry destinations that are filter inputs may fold (v = scale
+      // x); the accumulation's read of its own destination is not a read
+      const bool a_param = q.type == OP_COPY_INC || (q.a.base >= 0 && p.ir.bases[q.a.base].cls != SC_BATCHED);
+      std::vector<int64_t> rd2;
+      for (int64_t u = 0; u < q.rows; ++u) {
+        const int64_t e0 = q.ptr.empty() ? u : q.ptr[u], e1 = q.ptr.empty() ? u + 1 : q.ptr[u + 1];
+        const int64_t x = lrow(q.dst, u);
+        for (int64_t e = e0; e < e1; ++e) {
+          rd2.push_back(lrow(q.src, e));
+          if (q.type == OP_ELEM_INC && !a_param) rd2.push_back(lrow(q.a, e));
+        }
+        if (vcount[x] == 0) continue;
+        Src& sx = vs[x];
+        if (e1 - e0 == 1 && a_param) {
+          ++sx.writers;
+          sx.g = g;
+          sx.el = true;
+          sx.ex = lrow(q.src, e0);
+          sx.scale = q.type == OP_COPY_INC ? 1.0f : param_value(q.a.base, lrow(q.a, e0));
+        } else {
+          sx.writers += 2;
+        }
+      }
+      rd.swap(rd2);
     } else {
       for (int64_t x : wr) if (vcount[x] > 0) vs[x].writers += 2;   // any other writer disqualifies
     }
@@ -310,6 +370,8 @@ bool Fuser::fuse_with(int32_t ci, std::vector<LGroup>& out, LGroup& prologue) {
     const Src& s = vs[v];
     if (s.writers != 1 || s.g < 0 || vcount[v] != 1 || readers[v] != 0 || probed[v]) return false;
     if (s.first_reset < 0 || s.first_reset > s.g) return false;
+    if (s.el)   // input not rewritten after the copy, not written by the fused group
+      return last_writer[s.ex] <= s.g && lidx[s.ex] < 0 && !isdst[s.ex];
     const LGroup& D = G[s.g];
     if (D.a.base < 0 || p.ir.bases[D.a.base].cls == SC_BATCHED) return false;
     if (D.src.base != sb) return false;
@@ -321,10 +383,15 @@ bool Fuser::fuse_with(int32_t ci, std::vector<LGroup>& out, LGroup& prologue) {
     }
     return true;
   };
+  std::vector<char> el_fold((size_t)nrows, 0);   // elementwise rows that fold, one by one
   for (int64_t r = 0; r < nl; ++r) {
     const int64_t v = lrow(L.src, r);
     const Src& s = vs[v];
     if (s.g < 0) continue;
+    if (s.el) {
+      el_fold[v] = eligible(v) ? 1 : 0;
+      continue;
+    }
     const auto key = std::make_pair(s.g, s.op);
     const bool ok = eligible(v);
     auto it = op_ok.find(key);
@@ -341,6 +408,7 @@ bool Fuser::fuse_with(int32_t ci, std::vector<LGroup>& out, LGroup& prologue) {
   auto folded = [&](int64_t v) {
     const Src& s = vs[v];
     if (s.g < 0) return false;
+    if (s.el) return el_fold[v] != 0;
     auto it = op_ok.find({s.g, s.op});
     return it != op_ok.end() && it->second;
   };
@@ -393,7 +461,17 @@ bool Fuser::fuse_with(int32_t ci, std::vector<LGroup>& out, LGroup& prologue) {
     c.a = L.ca.size() > 1 ? L.ca[r] : L.ca[0];
     c.b = L.cb.size() > 1 ? L.cb[r] : L.cb[0];
     const int64_t v = lrow(L.src, r);
-    if (folded(v)) {
+    if (folded(v) && vs[v].el) {
+      const Src& s = vs[v];
+      c.ws = -2;
+      c.K = 0;
+      c.x = (int32_t)s.ex;
+      c.w = __builtin_bit_cast(int32_t, s.scale);
+      if (staged(c.x, 1)) {
+        c.stage = 1;
+        c.x = feed_of[c.x];
+      }
+    } else if (folded(v)) {
       const Src& s = vs[v];
       const LGroup& D = G[s.g];
       c.x = D.x_row[s.op];
@@ -530,6 +608,38 @@ bool Fuser::fuse_with(int32_t ci, std::vector<LGroup>& out, LGroup& prologue) {
       out.push_back(k);
       continue;
     }
+    if ((q.type == OP_COPY_INC || q.type == OP_ELEM_INC) && q.dst.base == sb && q.src.base == sb) {
+      // without the entries of folded rows (each the single entry of its row)
+      std::vector<int32_t> dst, src, av, ptr{0};
+      bool any = false;
+      for (int64_t u = 0; u < q.rows; ++u) {
+        const int64_t x = lrow(q.dst, u);
+        if (drop_row[x]) { any = true; continue; }
+        const int64_t e0 = q.ptr.empty() ? u : q.ptr[u], e1 = q.ptr.empty() ? u + 1 : q.ptr[u + 1];
+        dst.push_back((int32_t)x);
+        for (int64_t e = e0; e < e1; ++e) {
+          src.push_back((int32_t)lrow(q.src, e));
+          if (q.type == OP_ELEM_INC) av.push_back((int32_t)lrow(q.a, e));
+        }
+        ptr.push_back((int32_t)src.size());
+      }
+      if (!any) { out.push_back(q); continue; }
+      if (dst.empty()) continue;
+      LGroup k = q;
+      k.ops.clear();
+      for (int32_t oi : q.ops) {
+        const Op& o = p.ir.ops[oi];
+        if (!drop_row[p.sig_offset[o.dst.sig] + o.dst.start]) k.ops.push_back(oi);
+      }
+      if (k.ops.empty()) k.ops.push_back(q.ops[0]);
+      k.rows = (int64_t)dst.size();
+      k.dst = rows_operand(sb, dst);
+      k.src = rows_operand(sb, src);
+      if (q.type == OP_ELEM_INC) k.a = rows_operand(q.a.base, av);
+      k.ptr = src.size() == dst.size() ? std::vector<int32_t>{} : ptr;
+      out.push_back(k);
+      continue;
+    }
     if (q.type == OP_DOT_INC) {
       LGroup k = q;
       k.ops.clear(); k.w_row.clear(); k.x_row.clear(); k.d_row.clear();
@@ -562,7 +672,8 @@ bool Fuser::fuse_with(int32_t ci, std::vector<LGroup>& out, LGroup& prologue) {
           if (q.v >= 0) read[q.v + i] = 1;
           if (q.v == -2) read[q.y + i] = 1;
         }
-        if (q.v == -1 && !q.stage) for (int32_t k = 0; k < q.K; ++k) read[q.x + k] = 1;
+        if (q.v == -1 && !q.stage && q.ws == -2) for (int32_t i = 0; i < len; ++i) read[q.x + i] = 1;
+        if (q.v == -1 && !q.stage && q.ws != -2) for (int32_t k = 0; k < q.K; ++k) read[q.x + k] = 1;
       }
     }
     std::vector<LGroup> kept;
@@ -604,15 +715,6 @@ bool overlap(const std::vector<int64_t>& a, const std::vector<int64_t>& b) {
   return false;
 }
 
-LOperand rows_operand(int32_t base, const std::vector<int32_t>& rows) {
-  LOperand o;
-  o.base = base;
-  bool contig = true;
-  for (size_t i = 1; i < rows.size() && contig; ++i) contig = rows[i] == rows[0] + (int32_t)i;
-  if (contig) o.start = rows.empty() ? 0 : rows[0];
-  else o.idx = rows;
-  return o;
-}
 
 // A CopyInc group whose destinations are of two kinds -- all of a
 // destination's entries pull filter rows of the last group and the filters

@@ -321,9 +321,10 @@ void build_launches(ms_sim* s, const std::vector<LGroup>& groups, std::vector<La
     const size_t nc = g.syn_conn.size() / 8;
     for (size_t c = 0; c < nc; ++c) {
       const int32_t* q = &g.syn_conn[8 * c];
-      if (q[0] < 0 || q[3] < 0 || q[3] > 0xffff || q[4] > 3) fail(MS_E_INVALID, "fused synapse connection out of range");
+      if (q[0] < 0 || q[3] < 0 || q[3] > 0xffff || q[4] > 3 || q[4] < -2) fail(MS_E_INVALID, "fused synapse connection out of range");
       SynConn r{};
-      r.y = q[0]; r.v = q[1]; r.x = q[2]; r.kw = q[3] | (std::max(q[4], 0) << 16) | (q[7] ? 1 << 20 : 0);
+      r.y = q[0]; r.v = q[1]; r.x = q[2];
+      r.kw = q[3] | (std::max(q[4], 0) << 16) | (q[7] ? 1 << 20 : 0) | (q[4] == -2 ? 1 << 21 : 0);
       r.w = q[5]; r.p = q[6];
       r.a = g.syn_ab[2 * c]; r.b = g.syn_ab[2 * c + 1];
       const int32_t* w = reinterpret_cast<const int32_t*>(&r);

@@ -406,6 +406,9 @@ class LaunchExecutor(PlanExecutor):
                     if v0 != -2:
                         if v0 >= 0:
                             v = st[v0 + i]
+                        elif ws == -2:      # elementwise: scale (float bits in w0) times input row x0 + i
+                            scale = float(np.array([w0], np.int32).view(np.float32)[0])
+                            v = scale * (feed_rows_values[x0 + i] if staged else st[x0 + i])
                         else:
                             W = self.bases[g["wbase"][ws]]
                             xin = feed_rows_values[x0:x0 + K] if staged else st[x0:x0 + K]
