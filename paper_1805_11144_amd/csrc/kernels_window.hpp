@@ -256,10 +256,13 @@ __global__ void __launch_bounds__(512) k_w_ens(WView w, float* pa, EnsDesc E, fl
   const int ncol = cpw * ts, ctiles = ncol / 16;
   // LDS rows are padded (xs >= dp, js >= nmax) so that the products' lanes,
   // 16 columns apart, fall into different banks
+  // RW keeps a second input buffer (the next sub-window's) and two sets of
+  // per-wavefront partial decodes, so that a sub-window needs one barrier
   float* X = lds;                                   // [ncol][xs]
-  float* Jb = X + ncol * xs;                        // [ncol][js]: currents, then outputs
-  float* red = Jb + (int64_t)ncol * js;             // [ctiles][kch][16][16]
-  float* Bl = red + ctiles * kch * 256;             // [nmax] biases, [nmax][dp] encoders (enc_lds)
+  float* Xn = X + (RW ? ncol * xs : 0);             // RW: the other input buffer
+  float* Jb = Xn + ncol * xs;                       // [ncol][js]: currents, then outputs
+  float* red = Jb + (int64_t)ncol * js;             // [ctiles][kch][16][16]; RW: [2][nw][ctiles][16][16]
+  float* Bl = red + (RW ? 2 * nw * ctiles * 256 : ctiles * kch * 256);   // [nmax] biases, [nmax][xs] encoders
   float* El = Bl + nmax;                            // rows of stride xs
   const int ds = stride2mod4(nmax);
   float* Dl = El + (enc_lds ? nmax * xs : 0);       // [ndec][ds] decoders (dec_lds)
@@ -333,20 +336,127 @@ __global__ void __launch_bounds__(512) k_w_ens(WView w, float* pa, EnsDesc E, fl
   }
   float ae[RW ? kRwTiles : 1][RW ? kRwKd : 1], ad[RW ? kRwKs : 1];
   if constexpr (RW) {
+    // one column per workgroup, slot tid = neuron tid: wavefront `wave` owns
+    // neurons 64 wave .. 64 wave + 63, i.e. encoder tiles 4 wave .. 4 wave + 3
+    // and the decoder entries of those neurons
 #pragma unroll
     for (int i = 0; i < kRwTiles; ++i)
 #pragma unroll
       for (int kk = 0; kk < kRwKd; ++kk) {
-        const int ra = 16 * (wave + nw * i) + lane % 16, k = 4 * kk + lane / 16;
+        const int ra = 16 * (kRwTiles * wave + i) + lane % 16, k = 4 * kk + lane / 16;
         ae[i][kk] = (ra < n && k < d) ? enc[(int64_t)ra * E.d + k] : 0.0f;
       }
-    const int kc = wave % kch;
 #pragma unroll
     for (int ks = 0; ks < kRwKs; ++ks) {
-      const int r = 4 * (kc + kch * ks) + lane / 16;
-      ad[ks] = (qa < ndec && r < n && ks < ksteps) ? drow[r] : 0.0f;
+      const int r = 64 * wave + 4 * ks + lane / 16;
+      ad[ks] = (qa < ndec && r < n) ? drow[r] : 0.0f;
     }
   }
+  (void)ksteps;
+  if constexpr (RW) {
+    // Per sub-window, each wavefront alone: the currents of its own neurons
+    // (MFMA) into LDS, their updates through the sub-window, their share of
+    // the decoded outputs (MFMA) into its partial buffer, and its share of the
+    // next inputs into the other input buffer; then one barrier, after which
+    // the partials of every wavefront are added in wavefront order.  A
+    // wavefront reads only LDS rows it wrote itself until that barrier.
+    int xb = 0;
+    for (int32_t t0 = 0; t0 < w.T; t0 += ts) {
+      const int tsv = min(ts, w.T - t0);
+      const int32_t t1 = t0 + ts;
+      const int tsn = t1 < w.T ? min(ts, w.T - t1) : 0;
+      float xpre[kEnsXPre];
+#pragma unroll
+      for (int c = 0; c < kEnsXPre; ++c) {
+        const int32_t ps = xslot[c], st = ps & 127;
+        xpre[c] = (ps >= 0 && st < tsn)
+                      ? xsrc[(int64_t)(ps >> 16) * w.vs + (int64_t)(t1 + st) * w.B + b0 + ((ps >> 7) & 511)]
+                      : 0.0f;
+      }
+      const float* Xc = xb ? Xn : X;
+      float* Xo = xb ? X : Xn;
+      float* rb = red + xb * nw * ctiles * 256;
+      // 1. currents of this wavefront's neurons
+#pragma unroll
+      for (int i = 0; i < kRwTiles; ++i) {
+        const int nt = kRwTiles * wave + i;
+        if (nt < ntile) {
+          for (int ct = 0; ct < ctiles; ++ct) {
+            const int col = 16 * ct + lane % 16;
+            mfma_f4x acc = {0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll
+            for (int kk = 0; kk < kRwKd; ++kk) {
+              if (kk < kd) {
+                const int k = 4 * kk + lane / 16;
+                const float xv = k < d ? Xc[col * xs + k] : 0.0f;
+                acc = __builtin_amdgcn_mfma_f32_16x16x4f32(ae[i][kk], xv, acc, 0, 0, 0);
+              }
+            }
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+              const int r = 16 * nt + 4 * (lane / 16) + q;
+              if (r < n) Jb[col * js + r] = acc[q] + Bl[r];
+            }
+          }
+        }
+      }
+      // 2. its neurons through the sub-window (slot tid: neuron tid, column 0)
+      if (tid < n && b0 < w.B) {
+        float* cell = Jb + tid;
+        if (bf) {
+          for (int st = 0; st < tsv; ++st)
+            cell[st * js] = lif_update_bf(cell[st * js], v[0], rf[0], o.tau_rc, o.tau_ref, amp_dt, dt, o.inv_tau);
+        } else {
+          for (int st = 0; st < tsv; ++st)
+            cell[st * js] = neuron_update(E.ntype, cell[st * js], v[0], rf[0], o.tau_rc, o.tau_ref, o.amp, o.full,
+                                          dt, o.inv_tau);
+        }
+      }
+      // 3. its neurons' share of the decoded outputs
+      for (int ct = 0; ndec > 0 && ct < ctiles; ++ct) {
+        const int col = 16 * ct + lane % 16;
+        mfma_f4x acc = {0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll
+        for (int ks = 0; ks < kRwKs; ++ks) {
+          const int r = 64 * wave + 4 * ks + lane / 16;
+          const float sb = r < n ? Jb[col * js + r] : 0.0f;
+          acc = __builtin_amdgcn_mfma_f32_16x16x4f32(ad[ks], sb, acc, 0, 0, 0);
+        }
+#pragma unroll
+        for (int q = 0; q < 4; ++q) rb[((wave * ctiles + ct) * 16 + 4 * (lane / 16) + q) * 16 + lane % 16] = acc[q];
+      }
+      // 4. the next sub-window's inputs into the other buffer
+#pragma unroll
+      for (int c = 0; c < kEnsXPre; ++c)
+        if (tsn > 0 && xslot[c] >= 0) Xo[xlds[c]] = xpre[c];
+      if (tsn > 0) {
+        for (int i = tid + kEnsXPre * nthr; i < ncol * d; i += nthr) {
+          const int col = i / d, k = i - col * d;
+          Xo[col * xs + k] = stage_x(i, t1, tsn);
+        }
+      }
+      __syncthreads();
+      // 5. decoded outputs: the wavefronts' partials in wavefront order
+      for (int i = tid; i < ndec * ncol; i += nthr) {
+        const int q = i / ncol, col = i - q * ncol;
+        if (col < tsv && b0 < w.B) {
+          float sum = 0.0f;
+          for (int ww = 0; ww < nw; ++ww) sum += rb[((ww * ctiles + col / 16) * 16 + q) * 16 + col % 16];
+          const int dr = q < df0 ? o.d[0] + q : o.d[1] + (q - df0);
+          w.va[(int64_t)dr * w.vs + (int64_t)(t0 + col + 1) * w.B + b0] = sum;
+        }
+      }
+      if (o.s >= 0) {   // neuron outputs of every wavefront, then a barrier before they are overwritten
+        for (int i = tid; i < ncol * n; i += nthr) {
+          const int r = i / ncol, st = i - r * ncol;
+          if (st < tsv && b0 < w.B)
+            w.va[(int64_t)(o.s + r) * w.vs + (int64_t)(t0 + st + 1) * w.B + b0] = Jb[st * js + r];
+        }
+        __syncthreads();
+      }
+      xb ^= 1;
+    }
+  } else
   for (int32_t t0 = 0; t0 < w.T; t0 += ts) {
     const int tsv = min(ts, w.T - t0);
     // 0. fetch the next sub-window's inputs
@@ -361,31 +471,6 @@ __global__ void __launch_bounds__(512) k_w_ens(WView w, float* pa, EnsDesc E, fl
                     : 0.0f;
     }
     // 1. J = E x + bias
-    if constexpr (RW) {
-#pragma unroll
-      for (int i = 0; i < kRwTiles; ++i) {
-        const int nt = wave + nw * i;
-        if (nt < ntile) {
-          for (int ct = 0; ct < ctiles; ++ct) {
-            const int col = 16 * ct + lane % 16;
-            mfma_f4x acc = {0.0f, 0.0f, 0.0f, 0.0f};
-#pragma unroll
-            for (int kk = 0; kk < kRwKd; ++kk) {
-              if (kk < kd) {
-                const int k = 4 * kk + lane / 16;
-                const float xb = k < d ? X[col * xs + k] : 0.0f;
-                acc = __builtin_amdgcn_mfma_f32_16x16x4f32(ae[i][kk], xb, acc, 0, 0, 0);
-              }
-            }
-#pragma unroll
-            for (int q = 0; q < 4; ++q) {
-              const int r = 16 * nt + 4 * (lane / 16) + q;
-              if (r < n) Jb[col * js + r] = acc[q] + Bl[r];
-            }
-          }
-        }
-      }
-    } else
     for (int u = wave; u < ntile * ctiles; u += nw) {
       const int nt = u / ctiles, ct = u - nt * ctiles;
       const int col = 16 * ct + lane % 16;
@@ -431,23 +516,7 @@ __global__ void __launch_bounds__(512) k_w_ens(WView w, float* pa, EnsDesc E, fl
     }
     __syncthreads();
     // 3. decoded outputs
-    if constexpr (RW) {
-      for (int u = wave; ndec > 0 && u < ctiles * kch; u += nw) {
-        const int ct = u / kch, kc = u - ct * kch;   // kc == wave % kch
-        const int col = 16 * ct + lane % 16;
-        mfma_f4x acc = {0.0f, 0.0f, 0.0f, 0.0f};
-#pragma unroll
-        for (int ks = 0; ks < kRwKs; ++ks) {
-          if (ks < ksteps) {
-            const int r = 4 * (kc + kch * ks) + lane / 16;
-            const float sb = r < n ? Jb[col * js + r] : 0.0f;
-            acc = __builtin_amdgcn_mfma_f32_16x16x4f32(ad[ks], sb, acc, 0, 0, 0);
-          }
-        }
-#pragma unroll
-        for (int q = 0; q < 4; ++q) red[(u * 16 + 4 * (lane / 16) + q) * 16 + lane % 16] = acc[q];
-      }
-    } else if (ndec > 0) {
+    if (ndec > 0) {
       for (int u = wave; u < ctiles * kch; u += nw) {
         const int ct = u / kch, kc = u - ct * kch;
         const int col = 16 * ct + lane % 16;

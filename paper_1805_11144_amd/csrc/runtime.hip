@@ -959,12 +959,16 @@ void ens_shape(ms_sim* s, Launch& l, const LGroup& g) {
   // fragments in registers for the whole window, when they fit the kernel's
   // register arrays (at most 4 neuron tiles of 16 per wavefront, d <= 16, at
   // most 16 k steps of 4 per decoder chunk, each wavefront on one chunk)
-  const int64_t ntile = ((int64_t)nmax + 15) / 16, ksteps = ((int64_t)nmax + 4 * l.kch - 1) / (4 * l.kch);
-  if (l.npt == 1 && !(l.enc_lds && l.dec_lds) && ntile <= 4 * nw && dp <= 16 && l.ens.ndec <= 16 &&
-      nw % l.kch == 0 && ksteps <= 16) {
+  // (one column per workgroup; wavefront w owns neurons 64 w .. 64 w + 63 and
+  // their 4 encoder tiles; two input buffers and two sets of per-wavefront
+  // partial decodes)
+  const int64_t ntile = ((int64_t)nmax + 15) / 16;
+  const int64_t rw_lds = (2 * ts * l.xs + ts * l.js + 2 * nw * (ts / 16) * 256 + nmax) * (int64_t)sizeof(float);
+  if (l.npt == 1 && l.cpw == 1 && !(l.enc_lds && l.dec_lds) && ntile <= 4 * nw && dp <= 16 && l.ens.ndec <= 16 &&
+      rw_lds <= (int64_t)s->lds_limit) {
     l.rw = 1;
     l.enc_lds = l.dec_lds = 0;
-    l.lds = (size_t)((l.cpw * ts * (l.xs + l.js) + (l.cpw * ts / 16) * l.kch * 256 + nmax) * (int64_t)sizeof(float));
+    l.lds = (size_t)rw_lds;
   }
 }
 
