@@ -223,6 +223,13 @@ struct LGroup {
   std::vector<std::vector<int32_t>> ens_D, ens_dd;   // [function][op]
   std::vector<int32_t> ens_Dbase;                    // per function
   int32_t ens_bias_base = -1;
+  // ENS, window driver: per op kChainInts ints (empty: no op has one) -- the
+  // op's input x is the connection chain of Fig. 2 fused in (x_t = y_{t-1},
+  // y_t = a y_{t-1} + b W d_t): d first row (window row) and K, W first row
+  // in the weight base ens_chain_wbase (M rows of K), y first row (window
+  // row), M, then the float bits of a and b; K = 0 for an op without one
+  std::vector<int32_t> ens_chain;
+  int32_t ens_chain_wbase = -1;
   // SYN_SCATTER: segments of at most kSynSeg consecutive rows, 4 ints each
   // (first destination row or -1 for none, length, first connection, number of
   // connections); connections 8 ints each (first filter row y, first value row v
@@ -238,6 +245,7 @@ struct LGroup {
   int32_t syn_probe = 0;
 };
 
+constexpr int32_t kChainInts = 8; // ints per op of a fused window connection chain
 constexpr int32_t kSynSeg = 16;   // rows per segment of a fused synapse group
 constexpr int32_t kSynSlots = 4;  // weight bases one fused synapse group may read
 

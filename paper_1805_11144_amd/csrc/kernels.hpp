@@ -186,6 +186,11 @@ struct EnsDesc {
   const float* decT;
   int64_t dT_op;
   int32_t dT_row;
+  // window driver: fused connection chains into the ops' inputs (per op 8
+  // ints, see k_w_ens; null: none) and their transforms' weight base
+  const int32_t* chain;
+  const float* chain_w;
+  int32_t chain_wcols;
 };
 
 

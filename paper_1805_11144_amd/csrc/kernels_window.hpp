@@ -233,13 +233,83 @@ constexpr int kEnsXPre = 4;        // prefetched input values per thread
 // large to stage in LDS.
 constexpr int kRwTiles = 4, kRwKd = 4, kRwKs = 16;
 
+// The connection chain of Fig. 2 fused into an ensemble's input (window
+// driver; one wavefront, one batch column b0): for window steps t0 .. t0 + tsn
+// - 1, x_t = y_{t-1} and y_t = a y_{t-1} + b v_t with v_t = W d_t, d_t the
+// upstream value (rows cr[0] .. + K, block t + 1) and W the M x K transform.
+// Over a tile of 16 steps s = 0 .. 15 starting from y_{-1} = y0 the filter
+// unrolls to y_s = sum_{j <= s} b a^(s-j) v'_j with v'_0 = v_0 + (a / b) y0
+// and v'_j = v_j otherwise, so a tile is two 16 x 16 products on MFMA and no
+// sequential loop: V'^T = D^T W^T (plus the y0 term), then Y^T = L^T V'^T
+// with L[j][s] = b a^(s-j) for j <= s, else 0.  The second product sums over
+// j in the order j = 4 (l / 16) + kk, which is the layout the first one
+// leaves its result in, so V'^T passes between them in registers.
+// Fragments (lane l, m = l % 16, g = l / 16): wa[kk] = W[m][4 kk + g] and
+// la[kk] = L[4 g + kk][m] (kept in LDS, Cf[kk][l] and Cf[4 + kk][l]), the
+// upstream values of a tile D[4 kk + g][m] (kk = 0 .. 3), and ycur = y0[m]; the result lane l holds y_{4 g + q} for output
+// m, which it stores as x one step later into Xdst[step * xs + m].
+// chain_load fetches the first tile's upstream values early, so that their
+// latency overlaps other work; later tiles (sub-windows of more than 16
+// steps) are loaded when they are used.
+constexpr int kChainPre = 4;
+
+__device__ __forceinline__ void chain_load(const WView& w, const int32_t* cr, int64_t b0, int32_t t0, int32_t tsn,
+                                           int lane, float (&pre)[kChainPre]) {
+  const int32_t drow = cr[0], K = cr[1];
+#pragma unroll
+  for (int kk = 0; kk < kChainPre; ++kk) {
+    const int32_t k = 4 * kk + lane / 16, st = lane % 16;
+    pre[kk] = (k < K && st < tsn) ? w.va[(int64_t)(drow + k) * w.vs + (int64_t)(t0 + st + 1) * w.B + b0] : 0.0f;
+  }
+}
+
+__device__ __forceinline__ void chain_inputs(const WView& w, const int32_t* cr, int64_t b0, int32_t t0, int32_t tsn,
+                                             float* Xdst, int32_t xs, float& ycur, int lane, const float* Cf,
+                                             float c0, const float (&pre)[kChainPre]) {
+  const int32_t drow = cr[0], K = cr[1], M = cr[4];
+  const int m = lane % 16, g = lane / 16;
+  float wa[4], la[4];
+#pragma unroll
+  for (int kk = 0; kk < 4; ++kk) {
+    wa[kk] = Cf[kk * 64 + lane];
+    la[kk] = Cf[(4 + kk) * 64 + lane];
+  }
+  for (int32_t ct = 0; 16 * ct < tsn; ++ct) {
+    const int32_t n = min(16, tsn - 16 * ct);   // steps of this tile
+    float dv[4];
+#pragma unroll
+    for (int kk = 0; kk < 4; ++kk) {
+      const int32_t k = 4 * kk + g, st = 16 * ct + m;
+      dv[kk] = ct == 0 ? pre[kk]
+                       : (k < K && st < tsn) ? w.va[(int64_t)(drow + k) * w.vs + (int64_t)(t0 + st + 1) * w.B + b0]
+                                             : 0.0f;
+    }
+    mfma_f4x v = {0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll
+    for (int kk = 0; kk < 4; ++kk) v = __builtin_amdgcn_mfma_f32_16x16x4f32(dv[kk], wa[kk], v, 0, 0, 0);
+    if (g == 0) v[0] += c0 * ycur;   // the carried state enters with step 0
+    mfma_f4x y = {0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll
+    for (int kk = 0; kk < 4; ++kk) y = __builtin_amdgcn_mfma_f32_16x16x4f32(la[kk], v[kk], y, 0, 0, 0);
+    if (m < M) {
+      if (g == 0) Xdst[(16 * ct) * xs + m] = ycur;
+#pragma unroll
+      for (int q = 0; q < 4; ++q)
+        if (4 * g + q + 1 < n) Xdst[(16 * ct + 4 * g + q + 1) * xs + m] = y[q];
+    }
+    const int ql = (n - 1) % 4;   // y of the tile's last step, from lane 16 ((n - 1) / 4) + m
+    const float last = ql == 0 ? y[0] : ql == 1 ? y[1] : ql == 2 ? y[2] : y[3];
+    ycur = __shfl(last, 16 * ((n - 1) / 4) + m);
+  }
+}
+
 // Smallest stride >= x that is 2 mod 4: rows of that stride put lanes i and
 // i + 1 of a 16-lane group (rows i, i + 1; two adjacent columns per group)
 // in 32 different banks.
 __host__ __device__ inline int32_t stride2mod4(int32_t x) { return x + ((6 - x % 4) % 4); }
 
-template <int NPT, bool RW>
-__global__ void __launch_bounds__(512) k_w_ens(WView w, float* pa, EnsDesc E, float dt, int32_t nmax,
+template <int NPT, bool RW, bool CHAIN>
+__global__ void __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(CHAIN ? 4 : 1))) k_w_ens(WView w, float* pa, EnsDesc E, float dt, int32_t nmax,
                                                int32_t ts, int32_t cpw, int32_t kch, int xblk, int enc_lds,
                                                int dec_lds, int32_t nops, int32_t xs, int32_t js) {
   extern __shared__ float lds[];
@@ -266,6 +336,10 @@ __global__ void __launch_bounds__(512) k_w_ens(WView w, float* pa, EnsDesc E, fl
   float* El = Bl + nmax;                            // rows of stride xs
   const int ds = stride2mod4(nmax);
   float* Dl = El + (enc_lds ? nmax * xs : 0);       // [ndec][ds] decoders (dec_lds)
+  // fused connection chain into this op's input (cr[1] = K > 0): staging of
+  // the upstream values and of the products, wavefront 0 alone
+  const int32_t* cr = E.chain ? E.chain + (int64_t)op * 8 : nullptr;
+  const bool chain = CHAIN && cr && cr[1] > 0;   // compiled out of the kernels without chains
   gptr<float> enc = G(E.enc) + (int64_t)o.enc * E.d;
   gptr<float> bias = G(E.bias) + o.bias;
   gptr<float> D0 = G(E.D[0]) + (int64_t)o.D[0] * E.Dcols[0];
@@ -288,11 +362,38 @@ __global__ void __launch_bounds__(512) k_w_ens(WView w, float* pa, EnsDesc E, fl
     const int col = i / d, k = i - col * d, c = col / ts, st = col - c * ts;
     return (st < tsv && b0 + c < w.B) ? xsrc[(int64_t)k * w.vs + (int64_t)(tb + st) * w.B + b0 + c] : 0.0f;
   };
+  // chain: W and L fragments and the carried filter state (wavefront 0)
+  float* Cf = Dl + (dec_lds ? ndec * ds : 0);       // [8][64] chain fragments
+  float ycur = 0.0f, c0 = 0.0f;
+  if (chain && wave == 0) {
+    const int32_t K = cr[1], M = cr[4];
+    const float a = __builtin_bit_cast(float, cr[6]), b = __builtin_bit_cast(float, cr[7]);
+    gptr<float> Wc = G(E.chain_w) + (int64_t)cr[2] * E.chain_wcols;
+    const int m = lane % 16, g = lane / 16;
+#pragma unroll
+    for (int kk = 0; kk < 4; ++kk) {
+      const int k = 4 * kk + g, j = 4 * g + kk;
+      Cf[kk * 64 + lane] = (m < M && k < K) ? Wc[(int64_t)m * E.chain_wcols + k] : 0.0f;
+      double p = b;   // b a^(m - j), powers formed in double
+      for (int e = j; e < m; ++e) p *= (double)a;
+      Cf[(4 + kk) * 64 + lane] = j <= m ? (float)p : 0.0f;
+    }
+    c0 = a / b;   // b != 0 (the planner fuses no chain without it)
+    if (m < M && b0 < w.B) ycur = w.va[(int64_t)(cr[3] + m) * w.vs + b0];
+  }
   {
     const int tsv = min(ts, w.T);
-    for (int i = tid; i < ncol * d; i += nthr) {
-      const int col = i / d, k = i - col * d;
-      X[col * xs + k] = stage_x(i, 0, tsv);
+    if (chain) {
+      if (wave == 0 && b0 < w.B) {
+        float cpre0[kChainPre];
+        chain_load(w, cr, b0, 0, tsv, lane, cpre0);
+        chain_inputs(w, cr, b0, 0, tsv, X, xs, ycur, lane, Cf, c0, cpre0);
+      }
+    } else {
+      for (int i = tid; i < ncol * d; i += nthr) {
+        const int col = i / d, k = i - col * d;
+        X[col * xs + k] = stage_x(i, 0, tsv);
+      }
     }
   }
   // per-op constants: biases always, encoders and decoders when they fit
@@ -320,7 +421,7 @@ __global__ void __launch_bounds__(512) k_w_ens(WView w, float* pa, EnsDesc E, fl
 #pragma unroll
   for (int c = 0; c < kEnsXPre; ++c) {
     const int i = tid + c * nthr;
-    if (i < ncol * d) {
+    if (!chain && i < ncol * d) {
       const int col = i / d, k = i - col * d, cc = col / ts, st = col - cc * ts;
       xslot[c] = b0 + cc < w.B ? st | (cc << 7) | (k << 16) : -1;
       xlds[c] = col * xs + k;
@@ -373,6 +474,8 @@ __global__ void __launch_bounds__(512) k_w_ens(WView w, float* pa, EnsDesc E, fl
                       ? xsrc[(int64_t)(ps >> 16) * w.vs + (int64_t)(t1 + st) * w.B + b0 + ((ps >> 7) & 511)]
                       : 0.0f;
       }
+      float cpre[kChainPre];   // the next sub-window's upstream values (chain, wavefront 0)
+      if (chain && wave == 0 && tsn > 0 && b0 < w.B) chain_load(w, cr, b0, t1, tsn, lane, cpre);
       const float* Xc = xb ? Xn : X;
       float* Xo = xb ? X : Xn;
       float* rb = red + xb * nw * ctiles * 256;
@@ -426,10 +529,12 @@ __global__ void __launch_bounds__(512) k_w_ens(WView w, float* pa, EnsDesc E, fl
         for (int q = 0; q < 4; ++q) rb[((wave * ctiles + ct) * 16 + 4 * (lane / 16) + q) * 16 + lane % 16] = acc[q];
       }
       // 4. the next sub-window's inputs into the other buffer
+      if (chain && wave == 0 && tsn > 0 && b0 < w.B)
+        chain_inputs(w, cr, b0, t1, tsn, Xo, xs, ycur, lane, Cf, c0, cpre);
 #pragma unroll
       for (int c = 0; c < kEnsXPre; ++c)
         if (tsn > 0 && xslot[c] >= 0) Xo[xlds[c]] = xpre[c];
-      if (tsn > 0) {
+      if (tsn > 0 && !chain) {
         for (int i = tid + kEnsXPre * nthr; i < ncol * d; i += nthr) {
           const int col = i / d, k = i - col * d;
           Xo[col * xs + k] = stage_x(i, t1, tsn);
@@ -470,6 +575,8 @@ __global__ void __launch_bounds__(512) k_w_ens(WView w, float* pa, EnsDesc E, fl
                     ? xsrc[(int64_t)(ps >> 16) * w.vs + (int64_t)(t1 + st) * w.B + b0 + ((ps >> 7) & 511)]
                     : 0.0f;
     }
+    float cpre[kChainPre];   // the next sub-window's upstream values (chain, wavefront 0)
+    if (chain && wave == 0 && tsn > 0 && b0 < w.B) chain_load(w, cr, b0, t1, tsn, lane, cpre);
     // 1. J = E x + bias
     for (int u = wave; u < ntile * ctiles; u += nw) {
       const int nt = u / ctiles, ct = u - nt * ctiles;
@@ -489,10 +596,12 @@ __global__ void __launch_bounds__(512) k_w_ens(WView w, float* pa, EnsDesc E, fl
     }
     __syncthreads();
     // next inputs into LDS (every read of this sub-window's X is done)
+    if (chain && wave == 0 && tsn > 0 && b0 < w.B)
+      chain_inputs(w, cr, b0, t1, tsn, X, xs, ycur, lane, Cf, c0, cpre);
 #pragma unroll
     for (int c = 0; c < kEnsXPre; ++c)
       if (tsn > 0 && xslot[c] >= 0) X[xlds[c]] = xpre[c];
-    if (tsn > 0) {   // inputs beyond the prefetch registers
+    if (tsn > 0 && !chain) {   // inputs beyond the prefetch registers
       for (int i = tid + kEnsXPre * nthr; i < ncol * d; i += nthr) {
         const int col = i / d, k = i - col * d;
         X[col * xs + k] = stage_x(i, t1, tsn);
@@ -559,6 +668,8 @@ __global__ void __launch_bounds__(512) k_w_ens(WView w, float* pa, EnsDesc E, fl
     }
     __syncthreads();
   }
+  if (chain && wave == 0 && lane < cr[4] && b0 < w.B)   // the filter state the next window starts from
+    w.va[(int64_t)(cr[3] + lane) * w.vs + (int64_t)w.T * w.B + b0] = ycur;
   if (spiking) {
 #pragma unroll
     for (int j = 0; j < NPT; ++j) {

@@ -66,6 +66,10 @@ void jgroup(std::ostringstream& o, const Plan& p, const LGroup& L) {
     o << ",\"tau_rc\":"; jarr(o, L.tau_rc);
     o << ",\"tau_ref\":"; jarr(o, L.tau_ref);
     o << ",\"amp\":"; jarr(o, L.amp);
+    if (!L.ens_chain.empty()) {
+      o << ",\"chain\":"; jarr(o, L.ens_chain);
+      o << ",\"chain_wbase\":" << L.ens_chain_wbase;
+    }
   } else if (L.type == OP_SYN_SCATTER) {
     o << ",\"update\":" << L.syn_update << ",\"probe\":" << L.syn_probe << ",\"seg\":";
     jarr(o, L.syn_seg);

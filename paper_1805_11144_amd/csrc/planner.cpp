@@ -25,6 +25,7 @@
 #include <algorithm>
 #include <array>
 #include <climits>
+#include <cstring>
 #include <numeric>
 #include <set>
 #include <tuple>
@@ -682,6 +683,124 @@ LGroup lower_group(const Plan& p, const std::vector<int32_t>& ops) { return lowe
 
 }  // namespace
 
+// The connection chain of Fig. 2 in front of an ensemble -- a transform
+// DotInc of a value d into v (reset to zero), the lowpass y <- a y + b v, and
+// the Copy of y (the previous step's, as filters are read) into the
+// ensemble's input x (reset to zero) -- fuses into the ensemble's window phase
+// when each of v, y and x has no other reader or writer and no probe, the
+// three operators are alone in their phases, the transform has constant
+// weights with K, M <= 16, the lowpass a nonzero input gain b, and the
+// ensemble takes one batch column per
+// workgroup and one neuron per thread (more than 128 neurons, or minibatch 1;
+// no ensemble of its phase above 512 neurons).  The ensemble kernel
+// then computes x_t = y_{t-1}, y_t = a y_{t-1} + b W d_t itself, and writes
+// only y's last step (the value the next window starts from); the three
+// phases and the resets of v and x go.
+static void fuse_window_chains(const Plan& p, WindowPlan& w, const std::vector<std::vector<int32_t>>& S,
+                        const std::vector<std::vector<int32_t>>& I, const std::vector<std::vector<int32_t>>& R,
+                        const std::vector<std::vector<int32_t>>& U) {
+  const IR& ir = p.ir;
+  const int32_t ns = (int32_t)ir.sigs.size();
+  std::vector<char> probed(ns, 0);
+  for (const auto& pr : ir.probes) probed[pr.src.sig] = 1;
+  std::map<int32_t, int32_t> phase_of;
+  for (size_t k = 0; k < w.phases.size(); ++k)
+    for (int32_t op : w.phases[k].g.ops) phase_of[op] = (int32_t)k;
+  auto whole = [&](const SRef& r) { return r.sig >= 0 && r.start == 0 && r.len == ir.sigs[r.sig].rows; };
+  auto zero_reset_only = [&](int32_t sg) {
+    if (S[sg].size() != 1) return false;
+    const Op& o = ir.ops[S[sg][0]];
+    if (o.type != OP_RESET || !whole(o.dst)) return false;
+    for (double v : o.reset_value) if (v != 0.0) return false;
+    return true;
+  };
+  auto alone = [&](int32_t op, int32_t blk) {
+    auto it = phase_of.find(op);
+    return it != phase_of.end() && w.phases[it->second].g.ops.size() == 1 && w.phases[it->second].src_blk == blk;
+  };
+  std::vector<char> drop_phase(w.phases.size(), 0);
+  std::set<int64_t> drop_rows;   // window rows of v and x whose resets go
+  for (int32_t e = 0; e < (int32_t)ir.ops.size(); ++e) {
+    const Op& E = ir.ops[e];
+    if (E.type != OP_ENS || E.src.sig < 0 || !whole(E.src)) continue;
+    if (!(E.n > 128 || p.opts.minibatch == 1)) continue;
+    const int32_t X = E.src.sig;
+    if (!zero_reset_only(X) || I[X].size() != 1 || R[X] != std::vector<int32_t>{e} || !U[X].empty() || probed[X])
+      continue;
+    const int32_t c = I[X][0];
+    const Op& C = ir.ops[c];
+    if (C.type != OP_COPY_INC || !whole(C.dst) || !whole(C.src)) continue;
+    const int32_t Y = C.src.sig;
+    if (U[Y].size() != 1 || R[Y] != std::vector<int32_t>{c} || !S[Y].empty() || !I[Y].empty() || probed[Y]) continue;
+    const int32_t f = U[Y][0];
+    const Op& F = ir.ops[f];
+    if (F.type != OP_LOWPASS || !whole(F.dst) || !whole(F.src)) continue;
+    const int32_t V = F.src.sig;
+    if (!zero_reset_only(V) || I[V].size() != 1 || R[V] != std::vector<int32_t>{f} || !U[V].empty() || probed[V])
+      continue;
+    const int32_t dd = I[V][0];
+    const Op& D = ir.ops[dd];
+    if (D.type != OP_DOT_INC || !whole(D.dst) || ir.sigs[D.a.sig].cls == SC_BATCHED ||
+        ir.sigs[D.src.sig].cls != SC_BATCHED || w.priv[D.src.sig])
+      continue;
+    const int32_t M = D.dst.len, K = D.src.len;
+    if (M > 16 || K > 16 || M != E.src.len) continue;
+    if (!alone(dd, 1) || !alone(f, 1) || !alone(c, 0)) continue;
+    if ((float)F.coef_b == 0.0f) continue;   // the kernel's unrolled filter divides by b
+    auto ph = phase_of.find(e);
+    if (ph == phase_of.end()) continue;
+    LGroup& G = w.phases[ph->second].g;
+    // the fused launch runs one column per workgroup and one neuron per thread
+    if (*std::max_element(G.ens_n.begin(), G.ens_n.end()) > 512) continue;
+    const int32_t wb = ir.sigs[D.a.sig].base;
+    if (G.ens_chain_wbase >= 0 && G.ens_chain_wbase != wb) continue;
+    const size_t k = (size_t)(std::find(G.ops.begin(), G.ops.end(), e) - G.ops.begin());
+    if (G.ens_chain.empty()) G.ens_chain.assign(G.ops.size() * kChainInts, 0);
+    int32_t* r = &G.ens_chain[k * kChainInts];
+    r[0] = (int32_t)(w.sig_row[D.src.sig] + D.src.start);
+    r[1] = K;
+    r[2] = (int32_t)(p.sig_offset[D.a.sig] + D.a.start);
+    r[3] = (int32_t)w.sig_row[Y];
+    r[4] = M;
+    r[5] = 0;
+    const float a = (float)F.coef_a, b = (float)F.coef_b;
+    std::memcpy(&r[6], &a, 4);
+    std::memcpy(&r[7], &b, 4);
+    G.ens_chain_wbase = wb;
+    drop_phase[phase_of[dd]] = drop_phase[phase_of[f]] = drop_phase[phase_of[c]] = 1;
+    for (int32_t i = 0; i < ir.sigs[V].rows; ++i) drop_rows.insert(w.sig_row[V] + i);
+    for (int32_t i = 0; i < ir.sigs[X].rows; ++i) drop_rows.insert(w.sig_row[X] + i);
+  }
+  if (drop_rows.empty()) return;
+  std::vector<WPhase> kept;
+  for (size_t k = 0; k < w.phases.size(); ++k) {
+    if (drop_phase[k]) continue;
+    WPhase ph = w.phases[k];
+    if (ph.g.type == OP_RESET) {
+      std::vector<int32_t> rows;
+      std::vector<float> vals;
+      for (int64_t r = 0; r < ph.g.rows; ++r) {
+        const int64_t x = ph.g.dst.idx.empty() ? ph.g.dst.start + r : ph.g.dst.idx[r];
+        if (drop_rows.count(x)) continue;
+        rows.push_back((int32_t)x);
+        if (!ph.g.values.empty()) vals.push_back(ph.g.values[r]);
+      }
+      if (rows.empty()) continue;
+      if ((int64_t)rows.size() != ph.g.rows) {
+        ph.g.rows = (int64_t)rows.size();
+        ph.g.dst = make_operand(ph.g.dst.base, rows);
+        ph.g.values = vals;
+        std::vector<int32_t> ops;   // the resets that still have rows
+        for (int32_t op : ph.g.ops)
+          if (!drop_rows.count(w.sig_row[ir.ops[op].dst.sig] + ir.ops[op].dst.start)) ops.push_back(op);
+        ph.g.ops = ops;
+      }
+    }
+    kept.push_back(std::move(ph));
+  }
+  w.phases.swap(kept);
+}
+
 // Stage-major schedule.  Per batched signal: the operators that set it run
 // before those that increment it, which run before those that read it (all
 // within a step); a signal that is updated (filter output) is read as the
@@ -818,6 +937,7 @@ WindowPlan make_window_plan(const Plan& p) {
     }
     a = e;
   }
+  fuse_window_chains(p, w, S, I, R, U);
   for (const auto& pr : ir.probes)
     for (int32_t i = 0; i < pr.src.len; ++i) w.probe_rows.push_back((int32_t)(w.sig_row[pr.src.sig] + pr.src.start + i));
   w.ok = true;

@@ -310,6 +310,10 @@ void build_launches(ms_sim* s, const std::vector<LGroup>& groups, std::vector<La
     }
     ens_off[gi] = pb.add_i(rec);
   }
+  // fused connection chains of window ensemble phases (8 words per op)
+  std::vector<int64_t> chain_off(groups.size(), -1);
+  for (size_t gi = 0; gi < groups.size(); ++gi)
+    if (groups[gi].type == OP_ENS && !groups[gi].ens_chain.empty()) chain_off[gi] = pb.add_i(groups[gi].ens_chain);
   // fused synapse groups: segments, then connection records of 8 words
   static_assert(sizeof(SynConn) == 8 * 4, "SynConn layout");
   std::vector<int64_t> seg_off(groups.size(), -1), conn_off(groups.size(), -1);
@@ -434,6 +438,11 @@ void build_launches(ms_sim* s, const std::vector<LGroup>& groups, std::vector<La
       }
       E.bias = s->base_ptr[g.ens_bias_base];
       E.ops = reinterpret_cast<const EnsOp*>(ipool + ens_off[gi]);
+      if (chain_off[gi] >= 0) {
+        E.chain = ip(chain_off[gi]);
+        E.chain_w = s->base_ptr[g.ens_chain_wbase];
+        E.chain_wcols = ir.bases[g.ens_chain_wbase].cols;
+      }
       for (int32_t n : g.ens_n) l.ens_nmax = std::max(l.ens_nmax, n);
     }
     if (g.type == OP_BDOT_INC || g.type == OP_PES || g.type == OP_PES_FUSED) {
@@ -943,9 +952,13 @@ void ens_shape(ms_sim* s, Launch& l, const LGroup& g) {
   l.dec_lds = (int64_t)l.ens.ndec * nmax * 4 <= 16384 ? 1 : 0;
   const int64_t consts = nmax + (l.enc_lds ? (int64_t)nmax * l.xs : 0) +
                         (l.dec_lds ? (int64_t)l.ens.ndec * stride2mod4(nmax) : 0);
+  if (!g.ens_chain.empty() && (l.cpw != 1 || l.npt != 1))
+    fail(MS_E_INVALID, "fused connection chain needs one column per workgroup and one neuron per thread");
+  // fused connection chains keep the transform and filter fragments in LDS
+  const int64_t chain_f = g.ens_chain.empty() ? 0 : 512;
   auto bytes = [&](int64_t ts) {
     const int64_t ncol = l.cpw * ts;
-    return (ncol * (l.xs + l.js) + (ncol / 16) * kch_of(ts) * 256 + consts) * (int64_t)sizeof(float);
+    return (ncol * (l.xs + l.js) + (ncol / 16) * kch_of(ts) * 256 + consts + chain_f) * (int64_t)sizeof(float);
   };
   const int64_t wgs = std::max<int64_t>(1, 32 / nw);
   int64_t ts = 64;
@@ -963,7 +976,7 @@ void ens_shape(ms_sim* s, Launch& l, const LGroup& g) {
   // their 4 encoder tiles; two input buffers and two sets of per-wavefront
   // partial decodes)
   const int64_t ntile = ((int64_t)nmax + 15) / 16;
-  const int64_t rw_lds = (2 * ts * l.xs + ts * l.js + 2 * nw * (ts / 16) * 256 + nmax) * (int64_t)sizeof(float);
+  const int64_t rw_lds = (2 * ts * l.xs + ts * l.js + 2 * nw * (ts / 16) * 256 + nmax + chain_f) * (int64_t)sizeof(float);
   if (l.npt == 1 && l.cpw == 1 && !(l.enc_lds && l.dec_lds) && ntile <= 4 * nw && dp <= 16 && l.ens.ndec <= 16 &&
       rw_lds <= (int64_t)s->lds_limit) {
     l.rw = 1;
@@ -1050,11 +1063,12 @@ void setup_window(ms_sim* s) {
     }
   }
   if (s->lds_limit > 65536) {
-    HIPCHECK(hipFuncSetAttribute((const void*)k_w_ens<1, false>, hipFuncAttributeMaxDynamicSharedMemorySize, (int)s->lds_limit));
-    HIPCHECK(hipFuncSetAttribute((const void*)k_w_ens<2, false>, hipFuncAttributeMaxDynamicSharedMemorySize, (int)s->lds_limit));
-    HIPCHECK(hipFuncSetAttribute((const void*)k_w_ens<4, false>, hipFuncAttributeMaxDynamicSharedMemorySize, (int)s->lds_limit));
-    HIPCHECK(hipFuncSetAttribute((const void*)k_w_ens<8, false>, hipFuncAttributeMaxDynamicSharedMemorySize, (int)s->lds_limit));
-    HIPCHECK(hipFuncSetAttribute((const void*)k_w_ens<1, true>, hipFuncAttributeMaxDynamicSharedMemorySize, (int)s->lds_limit));
+    const void* wens[] = {(const void*)k_w_ens<1, false, false>, (const void*)k_w_ens<2, false, false>,
+                          (const void*)k_w_ens<4, false, false>, (const void*)k_w_ens<8, false, false>,
+                          (const void*)k_w_ens<1, true, false>,  (const void*)k_w_ens<1, false, true>,
+                          (const void*)k_w_ens<1, true, true>};
+    for (const void* f : wens)
+      HIPCHECK(hipFuncSetAttribute(f, hipFuncAttributeMaxDynamicSharedMemorySize, (int)s->lds_limit));
   }
   HIPCHECK(hipMemset(s->pa, 0, (size_t)std::max<int64_t>(1, w.rows_p) * B * sizeof(float)));
 }
@@ -1174,16 +1188,18 @@ void launch_phase(ms_sim* s, const Launch& l, int32_t T, int64_t t0, hipStream_t
       if (total >= 2147483648LL - 8) fail(MS_E_INVALID, "too many ensemble workgroups");
       const dim3 grid((unsigned)(8 * ((total + 7) / 8)));
       const int32_t nops = (int32_t)l.rows;
-      if (l.rw)
-        hipLaunchKernelGGL((k_w_ens<1, true>), grid, dim3(l.nthr), l.lds, q, w, s->pa, l.ens, s->dt, l.nmax, l.ts, l.cpw, l.kch, l.src_blk, l.enc_lds, l.dec_lds, nops, l.xs, l.js);
-      else if (l.npt == 1)
-        hipLaunchKernelGGL((k_w_ens<1, false>), grid, dim3(l.nthr), l.lds, q, w, s->pa, l.ens, s->dt, l.nmax, l.ts, l.cpw, l.kch, l.src_blk, l.enc_lds, l.dec_lds, nops, l.xs, l.js);
-      else if (l.npt == 2)
-        hipLaunchKernelGGL((k_w_ens<2, false>), grid, dim3(l.nthr), l.lds, q, w, s->pa, l.ens, s->dt, l.nmax, l.ts, l.cpw, l.kch, l.src_blk, l.enc_lds, l.dec_lds, nops, l.xs, l.js);
-      else if (l.npt == 4)
-        hipLaunchKernelGGL((k_w_ens<4, false>), grid, dim3(l.nthr), l.lds, q, w, s->pa, l.ens, s->dt, l.nmax, l.ts, l.cpw, l.kch, l.src_blk, l.enc_lds, l.dec_lds, nops, l.xs, l.js);
-      else
-        hipLaunchKernelGGL((k_w_ens<8, false>), grid, dim3(l.nthr), l.lds, q, w, s->pa, l.ens, s->dt, l.nmax, l.ts, l.cpw, l.kch, l.src_blk, l.enc_lds, l.dec_lds, nops, l.xs, l.js);
+#define MS_WENS(NPT, RW, CH)                                                                                    \
+  hipLaunchKernelGGL((k_w_ens<NPT, RW, CH>), grid, dim3(l.nthr), l.lds, q, w, s->pa, l.ens, s->dt, l.nmax, l.ts, \
+                     l.cpw, l.kch, l.src_blk, l.enc_lds, l.dec_lds, nops, l.xs, l.js)
+      const bool ch = l.ens.chain != nullptr;   // fused chains: one neuron per thread (checked by ens_shape)
+      if (l.rw && ch) MS_WENS(1, true, true);
+      else if (l.rw) MS_WENS(1, true, false);
+      else if (ch) MS_WENS(1, false, true);
+      else if (l.npt == 1) MS_WENS(1, false, false);
+      else if (l.npt == 2) MS_WENS(2, false, false);
+      else if (l.npt == 4) MS_WENS(4, false, false);
+      else MS_WENS(8, false, false);
+#undef MS_WENS
       break;
     }
     default: fail(MS_E_INVALID, "unknown group type");

@@ -234,6 +234,7 @@ class PlanExecutor:
         elif t == "Ensemble":
             trc_all = _vec(g["tau_rc"], n); tref_all = _vec(g["tau_ref"], n)
             amp_all = _vec(g["amp"], n)
+            chain = np.asarray(g["chain"], np.int64).reshape(n, -1) if "chain" in g else None
             for k in range(n):
                 nn = g["n"][k]
                 b0 = g["bias_row"][k]
@@ -241,7 +242,16 @@ class PlanExecutor:
                 if g["x_row"][k] >= 0:
                     d = g["d"]
                     E = self.bases[g["enc_base"]][g["enc_row"][k]:g["enc_row"][k] + nn]
-                    J = J + E[:, :d] @ src[g["x_row"][k]:g["x_row"][k] + d]
+                    if chain is not None and chain[k, 1] > 0:
+                        # fused connection chain (window driver): x_t = y_{t-1}, y_t = a y_{t-1} + b W d_t
+                        d0, K, w0, y0, Mc = (int(v) for v in chain[k, :5])
+                        a, b = np.asarray(chain[k, 6:8], np.int32).view(np.float32).astype(np.float64)
+                        Wc = self.bases[g["chain_wbase"]][w0:w0 + Mc, :K]
+                        x = prev[y0:y0 + Mc].copy()
+                        cur[y0:y0 + Mc] = a * prev[y0:y0 + Mc] + b * (Wc @ cur[d0:d0 + K])
+                    else:
+                        x = src[g["x_row"][k]:g["x_row"][k] + d]
+                    J = J + E[:, :d] @ x
                 if g["neuron"] == 0:
                     v0, r0 = g["V_row"][k], g["ref_row"][k]
                     s_, pa[v0:v0 + nn], pa[r0:r0 + nn] = _lif(J, pa[v0:v0 + nn].copy(),

@@ -10,7 +10,7 @@ import pytest
 import paper_1805_11144_amd as M
 from oracle.sim import OracleSim
 from synth import make_workload
-from tests.parity import check_spiking_probe, float32_run, rel_err
+from tests.parity import check_rate_probe, check_spiking_probe, float32_run, rel_err
 
 pytestmark = pytest.mark.gpu
 
@@ -203,3 +203,44 @@ def test_basal_ganglia_parity(driver, neuron_type):
         r = rel_err(g, e)
         print(f"bg {driver} probe {pi}: rel {r:.2e}")
         assert r <= 1e-5, (driver, pi, r)
+
+
+@pytest.mark.parametrize("neuron_type", ["lif_rate", "lif"])
+@pytest.mark.parametrize("n_neurons,minibatch", [(300, 2), (512, 3), (200, 2), (100, 1)])
+def test_window_fused_connection_chains(neuron_type, n_neurons, minibatch):
+    """Wide-array links fused into the next ensemble's window kernel (the
+    ensemble computes its input through the transform and the lowpass): on
+    the weights-in-registers path (300 and 512 neurons), the path with
+    weights in LDS (200 neurons) and with minibatch 1 (100 neurons); against the oracle,
+    split into two runs (the filter state carried between windows), and with
+    the state of one link's filter read back."""
+    w = make_workload("c4", neuron_type=neuron_type, n_steps=60, minibatch=minibatch, n_ens=3,
+                      n_neurons=n_neurons, n_eval=300)
+    j = M.Plan(M.model_from_spec(w.spec), minibatch=minibatch).json()["window"]
+    assert sum("chain" in ph["group"] for ph in j["phases"]) == 2
+    with M.Simulator(M.model_from_spec(w.spec), minibatch=minibatch, driver=M.DRIVER_WINDOW) as sim:
+        sim.run_steps(25, {i: f[:, :25] for i, f in w.feeds.items()})
+        sim.run_steps(35, {i: f[:, 25:] for i, f in w.feeds.items()})
+        got = [sim.data(p) for p in range(len(w.spec.probes))]
+        y1 = sim.get_state(M.mergesim.STATE_SYNAPSE, 1, 16)
+    ref = OracleSim(w.spec, minibatch=minibatch, param_dtype=np.float32)
+    ref.run_steps(w.n_steps, w.feeds)
+    r = rel_err(y1, ref.y[1])
+    print(f"link 1 filter state: rel {r:.2e}")
+    if neuron_type == "lif":
+        _spiking_whole_run(w, got)
+        assert np.abs(y1 - ref.y[1]).max() <= 1e-3 + 2 * np.abs(float32_run_state(w)[1] - ref.y[1]).max()
+        return
+    assert r <= 1e-5
+    # rate probes: 1e-5 of the peak or twice the float32 floor (the neuron
+    # probe's near-threshold rates amplify float32 rounding of their currents)
+    f32 = float32_run(w.spec, w.minibatch, w.n_steps, w.feeds)
+    for pi, (g, e, f) in enumerate(zip(got, [ref.data(p) for p in range(len(w.spec.probes))], f32)):
+        check_rate_probe(f"chain probe {pi}", g, e, f)
+
+
+def float32_run_state(w):
+    """Connection filter states of the float32-arithmetic oracle after the run."""
+    ref = OracleSim(w.spec, minibatch=w.minibatch, arith_dtype=np.float32)
+    ref.run_steps(w.n_steps, w.feeds)
+    return ref.y
