@@ -169,6 +169,7 @@ struct EnsOp {
   float inv_tau;                      // 1 / tau_rc
   int32_t D[kMaxFns], d[kMaxFns];
   float tau_rc, tau_ref, amp, full;   // neuron parameters of this op
+  float tau6;                         // tau_rc / 6 (the spike-time series' scale)
 };
 
 struct EnsDesc {
@@ -274,14 +275,15 @@ __device__ __forceinline__ float expm1_bf(float x) {
   return p * x;
 }
 
-__device__ __forceinline__ float neg_log1m_bf(float q) {
-  float p = 1.0f / 6.0f;
-  p = fmaf(p, q, 1.0f / 5.0f);
-  p = fmaf(p, q, 1.0f / 4.0f);
-  p = fmaf(p, q, 1.0f / 3.0f);
-  p = fmaf(p, q, 0.5f);
-  p = fmaf(p, q, 1.0f);
-  return p * q;
+// 6 (-ln(1 - q)) / q to the same order, 6 + 3q + 2q^2 + 1.5q^3 + 1.2q^4 + q^5:
+// with the leading coefficient 1 the first Horner step is an add of a
+// literal, so no constant has to sit in a register.
+__device__ __forceinline__ float neg_log1m6_bf(float q) {
+  float p = q + 1.2f;
+  p = fmaf(p, q, 1.5f);
+  p = fmaf(p, q, 2.0f);
+  p = fmaf(p, q, 3.0f);
+  return fmaf(p, q, 6.0f);
 }
 
 // Branch-free form of the spiking update above for dt / tau_rc <= 1/16, with
@@ -296,23 +298,34 @@ __device__ __forceinline__ float neg_log1m_bf(float q) {
 //     series grows with q, and for q >= 1 (a voltage above threshold set from
 //     outside) it exceeds tau_rc >= 16 dt >= integ, so the clamp of the
 //     crossing to the start of the step needs no test of its own.
+// The series is evaluated as (tau_rc / 6) q (6 + 3q + ... + q^5).  Clamps are
+// v_med3 (no operand canonicalisation), the refractory countdown
+// reuses dt - rf negated (exact), and (V - 1) / (J - 1) is one fma on the
+// reciprocal (V - 1 is exact for V in [1/2, 2]; elsewhere the fma rounds once
+// where the product of the rounded difference rounded twice).
 // Returns the neuron output (amp_dt = amplitude / dt or 0).
-__device__ __forceinline__ float lif_update_bf(float j, float& v, float& rf, float tau_rc, float tau_ref,
+// tau6 = tau_rc / 6.
+__device__ __forceinline__ float lif_update_bf(float j, float& v, float& rf, float tau6, float tau_ref,
                                                float amp_dt, float dt, float inv_tau) {
-  const float integ = __builtin_amdgcn_fmed3f(dt - rf, 0.0f, dt);   // clamp to [0, dt] (v_med3_f32)
+  const float t = dt - rf;
+  const float integ = __builtin_amdgcn_fmed3f(t, 0.0f, dt);           // clamp to [0, dt]
   const float e = expm1_bf(-integ * inv_tau);
   v = v - (j - v) * e;
-  rf = fmaxf(rf - dt, 0.0f);
+  const float rf_next = __builtin_amdgcn_fmed3f(-t, 0.0f, __builtin_inff());   // max(rf - dt, 0)
   const float drive = j - 1.0f;
-  const float q = (v - 1.0f) * __builtin_amdgcn_rcpf(drive);
-  float since = drive > 0.0f ? fminf(tau_rc * neg_log1m_bf(q), integ) : 0.0f;
-  // an empty asm statement that takes the crossing time as an operand: it is
-  // computed on every lane, so the compiler selects instead of branching on
-  // the spike (a branch runs both sides anyway when the lanes disagree)
+  const float r = __builtin_amdgcn_rcpf(drive);
+  const float q = fmaf(v, r, -r);
+  // the crossing time, clamped to [0, integ] (a crossing has q > 0), computed
+  // on every lane: the empty asm statement takes it as an operand, so that the
+  // compiler selects instead of branching on J > 1 (a branch runs both sides
+  // anyway when the lanes disagree)
+  float since = __builtin_amdgcn_fmed3f(tau6 * (q * neg_log1m6_bf(q)), 0.0f, integ);
   __asm__ volatile("" : "+v"(since));
+  since = drive > 0.0f ? since : 0.0f;
   const bool spk = v > 1.0f;
-  v = spk ? 0.0f : fmaxf(v, 0.0f);
-  rf = spk ? tau_ref - since : rf;
+  const float vpos = __builtin_amdgcn_fmed3f(v, 0.0f, __builtin_inff());
+  v = spk ? 0.0f : vpos;
+  rf = spk ? tau_ref - since : rf_next;
   return spk ? amp_dt : 0.0f;
 }
 
@@ -345,6 +358,7 @@ __device__ __forceinline__ EnsOp load_op(const EnsOp* ops, int op) {
   o.tau_ref = __builtin_bit_cast(float, w[13]);
   o.amp = __builtin_bit_cast(float, w[14]);
   o.full = __builtin_bit_cast(float, w[15]);
+  o.tau6 = __builtin_bit_cast(float, w[16]);
   return o;
 }
 

@@ -130,10 +130,10 @@ __global__ void k_w_lif(WView w, int64_t rows, Opnd J, Opnd s, Opnd V, Opnd R, f
   const int64_t sr = rowof(s, _r) * w.vs + w.B + _b;
   const float inv_tau = 1.0f / tau_rc;
   if (dt * inv_tau <= 0.0625f) {
-    const float amp_dt = amp / dt;
+    const float amp_dt = amp / dt, tau6 = tau_rc * (1.0f / 6.0f);
     for (int32_t t = 0; t < w.T; ++t) {
       const float j = w.va[jr + (int64_t)t * w.B];
-      w.va[sr + (int64_t)t * w.B] = lif_update_bf(j, v, rf, tau_rc, tau_ref, amp_dt, dt, inv_tau);
+      w.va[sr + (int64_t)t * w.B] = lif_update_bf(j, v, rf, tau6, tau_ref, amp_dt, dt, inv_tau);
     }
   } else {
     for (int32_t t = 0; t < w.T; ++t) {
@@ -347,7 +347,7 @@ __global__ void __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(CHAIN 
   const int64_t s0 = E.Dcols[0], s1 = E.Dcols[E.nf > 1 ? 1 : 0];
   const bool spiking = E.ntype == 0;
   const bool bf = spiking && dt * o.inv_tau <= 0.0625f;   // branch-free spiking update applies
-  const float amp_dt = o.amp / dt;
+  const float amp_dt = o.amp / dt, tau6 = o.tau6;
   const float* xsrc = w.va + (int64_t)(o.x >= 0 ? o.x : 0) * w.vs + (int64_t)xblk * w.B;
   // neuron state of this thread's slots
   float v[NPT], rf[NPT];
@@ -508,7 +508,7 @@ __global__ void __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(CHAIN 
         float* cell = Jb + tid;
         if (bf) {
           for (int st = 0; st < tsv; ++st)
-            cell[st * js] = lif_update_bf(cell[st * js], v[0], rf[0], o.tau_rc, o.tau_ref, amp_dt, dt, o.inv_tau);
+            cell[st * js] = lif_update_bf(cell[st * js], v[0], rf[0], tau6, o.tau_ref, amp_dt, dt, o.inv_tau);
         } else {
           for (int st = 0; st < tsv; ++st)
             cell[st * js] = neuron_update(E.ntype, cell[st * js], v[0], rf[0], o.tau_rc, o.tau_ref, o.amp, o.full,
@@ -615,7 +615,7 @@ __global__ void __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(CHAIN 
         float* cell = Jb + (int64_t)c * ts * js + r;
         if (bf) {
           for (int st = 0; st < tsv; ++st)
-            cell[st * js] = lif_update_bf(cell[st * js], v[j], rf[j], o.tau_rc, o.tau_ref, amp_dt, dt, o.inv_tau);
+            cell[st * js] = lif_update_bf(cell[st * js], v[j], rf[j], tau6, o.tau_ref, amp_dt, dt, o.inv_tau);
         } else {
           for (int st = 0; st < tsv; ++st)
             cell[st * js] = neuron_update(E.ntype, cell[st * js], v[j], rf[j], o.tau_rc, o.tau_ref, o.amp,

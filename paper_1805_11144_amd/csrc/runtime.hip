@@ -284,8 +284,8 @@ void build_launches(ms_sim* s, const std::vector<LGroup>& groups, std::vector<La
     o.cb = g.cb.size() > 1 ? pb.add_f(g.cb) : -1;
     offs.push_back(o);
   }
-  // packed per-op records of fused ensemble groups (EnsOp, 16 x 4 bytes each)
-  static_assert(sizeof(EnsOp) == 16 * 4, "EnsOp layout");
+  // packed per-op records of fused ensemble groups (EnsOp, 17 x 4 bytes each)
+  static_assert(sizeof(EnsOp) == 17 * 4, "EnsOp layout");
   std::vector<int64_t> ens_off(groups.size(), -1);
   for (size_t gi = 0; gi < groups.size(); ++gi) {
     const LGroup& g = groups[gi];
@@ -305,8 +305,9 @@ void build_launches(ms_sim* s, const std::vector<LGroup>& groups, std::vector<La
       e.amp = g.amp.size() > 1 ? g.amp[k] : g.amp[0];
       e.full = (float)std::expm1(-p.dt / (double)trc);
       e.inv_tau = (float)(1.0 / (double)trc);
+      e.tau6 = (float)((double)trc / 6.0);
       const int32_t* w = reinterpret_cast<const int32_t*>(&e);
-      rec.insert(rec.end(), w, w + 16);
+      rec.insert(rec.end(), w, w + 17);
     }
     ens_off[gi] = pb.add_i(rec);
   }
