@@ -236,7 +236,7 @@ constexpr int kRwTiles = 4, kRwKd = 4, kRwKs = 16;
 // The connection chain of Fig. 2 fused into an ensemble's input (window
 // driver; one wavefront, one batch column b0): for window steps t0 .. t0 + tsn
 // - 1, x_t = y_{t-1} and y_t = a y_{t-1} + b v_t with v_t = W d_t, d_t the
-// upstream value (rows cr[0] .. + K, block t + 1) and W the M x K transform.
+// upstream value (K rows from drow, block t + 1) and W the M x K transform.
 // Over a tile of 16 steps s = 0 .. 15 starting from y_{-1} = y0 the filter
 // unrolls to y_s = sum_{j <= s} b a^(s-j) v'_j with v'_0 = v_0 + (a / b) y0
 // and v'_j = v_j otherwise, so a tile is two 16 x 16 products on MFMA and no
@@ -253,20 +253,25 @@ constexpr int kRwTiles = 4, kRwKd = 4, kRwKs = 16;
 // steps) are loaded when they are used.
 constexpr int kChainPre = 4;
 
-__device__ __forceinline__ void chain_load(const WView& w, const int32_t* cr, int64_t b0, int32_t t0, int32_t tsn,
-                                           int lane, float (&pre)[kChainPre]) {
-  const int32_t drow = cr[0], K = cr[1];
+// Per-lane view of a chain's upstream values: lane l reads rows drow + 4 kk +
+// l / 16 at window step l % 16 of a tile, from base (its value at block 1 of
+// row drow + l / 16) plus kk * kstride + t * B; K inputs, M outputs.
+struct ChainCtx {
+  const float* base;
+  int64_t kstride;
+  int32_t K, M;
+};
+
+__device__ __forceinline__ void chain_load(const WView& w, const ChainCtx& cc, int32_t t0, int32_t tsn, int lane,
+                                           float (&pre)[kChainPre]) {
 #pragma unroll
-  for (int kk = 0; kk < kChainPre; ++kk) {
-    const int32_t k = 4 * kk + lane / 16, st = lane % 16;
-    pre[kk] = (k < K && st < tsn) ? w.va[(int64_t)(drow + k) * w.vs + (int64_t)(t0 + st + 1) * w.B + b0] : 0.0f;
-  }
+  for (int kk = 0; kk < kChainPre; ++kk)
+    pre[kk] = (4 * kk + lane / 16 < cc.K && lane % 16 < tsn) ? cc.base[kk * cc.kstride + (int64_t)t0 * w.B] : 0.0f;
 }
 
-__device__ __forceinline__ void chain_inputs(const WView& w, const int32_t* cr, int64_t b0, int32_t t0, int32_t tsn,
-                                             float* Xdst, int32_t xs, float& ycur, int lane, const float* Cf,
-                                             float c0, const float (&pre)[kChainPre]) {
-  const int32_t drow = cr[0], K = cr[1], M = cr[4];
+__device__ __forceinline__ void chain_inputs(const WView& w, const ChainCtx& cc, int32_t t0, int32_t tsn, float* Xdst,
+                                             int32_t xs, float& ycur, int lane, const float* Cf, float c0,
+                                             const float (&pre)[kChainPre]) {
   const int m = lane % 16, g = lane / 16;
   float wa[4], la[4];
 #pragma unroll
@@ -278,12 +283,11 @@ __device__ __forceinline__ void chain_inputs(const WView& w, const int32_t* cr, 
     const int32_t n = min(16, tsn - 16 * ct);   // steps of this tile
     float dv[4];
 #pragma unroll
-    for (int kk = 0; kk < 4; ++kk) {
-      const int32_t k = 4 * kk + g, st = 16 * ct + m;
+    for (int kk = 0; kk < 4; ++kk)
       dv[kk] = ct == 0 ? pre[kk]
-                       : (k < K && st < tsn) ? w.va[(int64_t)(drow + k) * w.vs + (int64_t)(t0 + st + 1) * w.B + b0]
-                                             : 0.0f;
-    }
+                       : (4 * kk + g < cc.K && 16 * ct + m < tsn)
+                             ? cc.base[kk * cc.kstride + (int64_t)(t0 + 16 * ct) * w.B]
+                             : 0.0f;
     mfma_f4x v = {0.0f, 0.0f, 0.0f, 0.0f};
 #pragma unroll
     for (int kk = 0; kk < 4; ++kk) v = __builtin_amdgcn_mfma_f32_16x16x4f32(dv[kk], wa[kk], v, 0, 0, 0);
@@ -291,7 +295,7 @@ __device__ __forceinline__ void chain_inputs(const WView& w, const int32_t* cr, 
     mfma_f4x y = {0.0f, 0.0f, 0.0f, 0.0f};
 #pragma unroll
     for (int kk = 0; kk < 4; ++kk) y = __builtin_amdgcn_mfma_f32_16x16x4f32(la[kk], v[kk], y, 0, 0, 0);
-    if (m < M) {
+    if (m < cc.M) {
       if (g == 0) Xdst[(16 * ct) * xs + m] = ycur;
 #pragma unroll
       for (int q = 0; q < 4; ++q)
@@ -332,14 +336,21 @@ __global__ void __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(CHAIN 
   float* Xn = X + (RW ? ncol * xs : 0);             // RW: the other input buffer
   float* Jb = Xn + ncol * xs;                       // [ncol][js]: currents, then outputs
   float* red = Jb + (int64_t)ncol * js;             // [ctiles][kch][16][16]; RW: [2][nw][ctiles][16][16]
-  float* Bl = red + (RW ? 2 * nw * ctiles * 256 : ctiles * kch * 256);   // [nmax] biases, [nmax][xs] encoders
-  float* El = Bl + nmax;                            // rows of stride xs
+  // [nmax] biases (RW: [nthr], zero past n), then [nmax][xs] encoders
+  float* Bl = red + (RW ? 2 * nw * ctiles * 256 : ctiles * kch * 256);
+  float* El = Bl + (RW ? nthr : nmax);              // rows of stride xs
   const int ds = stride2mod4(nmax);
   float* Dl = El + (enc_lds ? nmax * xs : 0);       // [ndec][ds] decoders (dec_lds)
-  // fused connection chain into this op's input (cr[1] = K > 0): staging of
-  // the upstream values and of the products, wavefront 0 alone
-  const int32_t* cr = E.chain ? E.chain + (int64_t)op * 8 : nullptr;
-  const bool chain = CHAIN && cr && cr[1] > 0;   // compiled out of the kernels without chains
+  // fused connection chain into this op's input (K = crec[1] > 0), computed by
+  // wavefront 0 alone
+  // (its record is read once here: rows, sizes, coefficients)
+  int32_t crec[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+  if (CHAIN && E.chain) {
+    gptr<int32_t> cg = G(E.chain) + (int64_t)op * 8;
+#pragma unroll
+    for (int i = 0; i < 8; ++i) crec[i] = cg[i];
+  }
+  const bool chain = CHAIN && crec[1] > 0;   // compiled out of the kernels without chains
   gptr<float> enc = G(E.enc) + (int64_t)o.enc * E.d;
   gptr<float> bias = G(E.bias) + o.bias;
   gptr<float> D0 = G(E.D[0]) + (int64_t)o.D[0] * E.Dcols[0];
@@ -365,11 +376,13 @@ __global__ void __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(CHAIN 
   // chain: W and L fragments and the carried filter state (wavefront 0)
   float* Cf = Dl + (dec_lds ? ndec * ds : 0);       // [8][64] chain fragments
   float ycur = 0.0f, c0 = 0.0f;
+  ChainCtx cc{w.va, 4 * w.vs, crec[1], crec[4]};
   if (chain && wave == 0) {
-    const int32_t K = cr[1], M = cr[4];
-    const float a = __builtin_bit_cast(float, cr[6]), b = __builtin_bit_cast(float, cr[7]);
-    gptr<float> Wc = G(E.chain_w) + (int64_t)cr[2] * E.chain_wcols;
+    const int32_t K = crec[1], M = crec[4];
+    const float a = __builtin_bit_cast(float, crec[6]), b = __builtin_bit_cast(float, crec[7]);
+    gptr<float> Wc = G(E.chain_w) + (int64_t)crec[2] * E.chain_wcols;
     const int m = lane % 16, g = lane / 16;
+    cc.base = w.va + (int64_t)(crec[0] + g) * w.vs + (int64_t)(m + 1) * w.B + b0;
 #pragma unroll
     for (int kk = 0; kk < 4; ++kk) {
       const int k = 4 * kk + g, j = 4 * g + kk;
@@ -379,15 +392,15 @@ __global__ void __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(CHAIN 
       Cf[(4 + kk) * 64 + lane] = j <= m ? (float)p : 0.0f;
     }
     c0 = a / b;   // b != 0 (the planner fuses no chain without it)
-    if (m < M && b0 < w.B) ycur = w.va[(int64_t)(cr[3] + m) * w.vs + b0];
+    if (m < M && b0 < w.B) ycur = w.va[(int64_t)(crec[3] + m) * w.vs + b0];
   }
   {
     const int tsv = min(ts, w.T);
     if (chain) {
       if (wave == 0 && b0 < w.B) {
         float cpre0[kChainPre];
-        chain_load(w, cr, b0, 0, tsv, lane, cpre0);
-        chain_inputs(w, cr, b0, 0, tsv, X, xs, ycur, lane, Cf, c0, cpre0);
+        chain_load(w, cc, 0, tsv, lane, cpre0);
+        chain_inputs(w, cc, 0, tsv, X, xs, ycur, lane, Cf, c0, cpre0);
       }
     } else {
       for (int i = tid; i < ncol * d; i += nthr) {
@@ -397,7 +410,20 @@ __global__ void __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(CHAIN 
     }
   }
   // per-op constants: biases always, encoders and decoders when they fit
-  for (int r = tid; r < n; r += nthr) Bl[r] = bias[r];
+  if (RW) {
+    // every slot of the workgroup is a neuron row of the products: rows past
+    // n get zero bias (and zero encoder and decoder entries), so that they
+    // compute zeros and the sub-window loop needs no per-lane tests; the
+    // input columns past d up to the k steps' 4 kd are zero as well
+    Bl[tid] = tid < n ? bias[tid] : 0.0f;
+    const int dpad = 4 * ((d + 3) / 4) - d;
+    for (int i = tid; i < 2 * ncol * dpad; i += nthr) {
+      const int col = i / dpad, k = d + (i - col * dpad);
+      X[col * xs + k] = 0.0f;   // X and Xn, which follows it
+    }
+  } else {
+    for (int r = tid; r < n; r += nthr) Bl[r] = bias[r];
+  }
   if (enc_lds)
     for (int i = tid; i < n * d; i += nthr) El[(i / d) * xs + i % d] = enc[(int64_t)i];
   if (dec_lds)
@@ -467,44 +493,40 @@ __global__ void __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(CHAIN 
       const int32_t t1 = t0 + ts;
       const int tsn = t1 < w.T ? min(ts, w.T - t1) : 0;
       float xpre[kEnsXPre];
+      if (!chain) {
 #pragma unroll
-      for (int c = 0; c < kEnsXPre; ++c) {
-        const int32_t ps = xslot[c], st = ps & 127;
-        xpre[c] = (ps >= 0 && st < tsn)
-                      ? xsrc[(int64_t)(ps >> 16) * w.vs + (int64_t)(t1 + st) * w.B + b0 + ((ps >> 7) & 511)]
-                      : 0.0f;
+        for (int c = 0; c < kEnsXPre; ++c) {
+          const int32_t ps = xslot[c], st = ps & 127;
+          xpre[c] = (ps >= 0 && st < tsn)
+                        ? xsrc[(int64_t)(ps >> 16) * w.vs + (int64_t)(t1 + st) * w.B + b0 + ((ps >> 7) & 511)]
+                        : 0.0f;
+        }
       }
       float cpre[kChainPre];   // the next sub-window's upstream values (chain, wavefront 0)
-      if (chain && wave == 0 && tsn > 0 && b0 < w.B) chain_load(w, cr, b0, t1, tsn, lane, cpre);
+      if (chain && wave == 0 && tsn > 0 && b0 < w.B) chain_load(w, cc, t1, tsn, lane, cpre);
       const float* Xc = xb ? Xn : X;
       float* Xo = xb ? X : Xn;
       float* rb = red + xb * nw * ctiles * 256;
-      // 1. currents of this wavefront's neurons
+      // 1. currents of this wavefront's neurons (all four tiles: rows past n
+      // compute zeros), loads and stores at fixed offsets from one address
 #pragma unroll
       for (int i = 0; i < kRwTiles; ++i) {
-        const int nt = kRwTiles * wave + i;
-        if (nt < ntile) {
-          for (int ct = 0; ct < ctiles; ++ct) {
-            const int col = 16 * ct + lane % 16;
-            mfma_f4x acc = {0.0f, 0.0f, 0.0f, 0.0f};
+        const int r0 = 16 * (kRwTiles * wave + i) + 4 * (lane / 16);
+        for (int ct = 0; ct < ctiles; ++ct) {
+          const int col = 16 * ct + lane % 16;
+          const float* xr = Xc + col * xs + lane / 16;
+          mfma_f4x acc = {0.0f, 0.0f, 0.0f, 0.0f};
 #pragma unroll
-            for (int kk = 0; kk < kRwKd; ++kk) {
-              if (kk < kd) {
-                const int k = 4 * kk + lane / 16;
-                const float xv = k < d ? Xc[col * xs + k] : 0.0f;
-                acc = __builtin_amdgcn_mfma_f32_16x16x4f32(ae[i][kk], xv, acc, 0, 0, 0);
-              }
-            }
+          for (int kk = 0; kk < kRwKd; ++kk)
+            if (kk < kd) acc = __builtin_amdgcn_mfma_f32_16x16x4f32(ae[i][kk], xr[4 * kk], acc, 0, 0, 0);
+          float* jr = Jb + col * js + r0;
 #pragma unroll
-            for (int q = 0; q < 4; ++q) {
-              const int r = 16 * nt + 4 * (lane / 16) + q;
-              if (r < n) Jb[col * js + r] = acc[q] + Bl[r];
-            }
-          }
+          for (int q = 0; q < 4; ++q) jr[q] = acc[q] + Bl[r0 + q];
         }
       }
-      // 2. its neurons through the sub-window (slot tid: neuron tid, column 0)
-      if (tid < n && b0 < w.B) {
+      // 2. its neurons through the sub-window (slot tid: neuron tid, column 0;
+      // slots past n carry zero state and current, and output zeros)
+      if (b0 < w.B) {
         float* cell = Jb + tid;
         if (bf) {
           for (int st = 0; st < tsv; ++st)
@@ -519,21 +541,20 @@ __global__ void __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(CHAIN 
       for (int ct = 0; ndec > 0 && ct < ctiles; ++ct) {
         const int col = 16 * ct + lane % 16;
         mfma_f4x acc = {0.0f, 0.0f, 0.0f, 0.0f};
+        const float* sr = Jb + col * js + 64 * wave + lane / 16;
 #pragma unroll
-        for (int ks = 0; ks < kRwKs; ++ks) {
-          const int r = 64 * wave + 4 * ks + lane / 16;
-          const float sb = r < n ? Jb[col * js + r] : 0.0f;
-          acc = __builtin_amdgcn_mfma_f32_16x16x4f32(ad[ks], sb, acc, 0, 0, 0);
-        }
+        for (int ks = 0; ks < kRwKs; ++ks) acc = __builtin_amdgcn_mfma_f32_16x16x4f32(ad[ks], sr[4 * ks], acc, 0, 0, 0);
 #pragma unroll
         for (int q = 0; q < 4; ++q) rb[((wave * ctiles + ct) * 16 + 4 * (lane / 16) + q) * 16 + lane % 16] = acc[q];
       }
       // 4. the next sub-window's inputs into the other buffer
       if (chain && wave == 0 && tsn > 0 && b0 < w.B)
-        chain_inputs(w, cr, b0, t1, tsn, Xo, xs, ycur, lane, Cf, c0, cpre);
+        chain_inputs(w, cc, t1, tsn, Xo, xs, ycur, lane, Cf, c0, cpre);
+      if (!chain) {
 #pragma unroll
-      for (int c = 0; c < kEnsXPre; ++c)
-        if (tsn > 0 && xslot[c] >= 0) Xo[xlds[c]] = xpre[c];
+        for (int c = 0; c < kEnsXPre; ++c)
+          if (tsn > 0 && xslot[c] >= 0) Xo[xlds[c]] = xpre[c];
+      }
       if (tsn > 0 && !chain) {
         for (int i = tid + kEnsXPre * nthr; i < ncol * d; i += nthr) {
           const int col = i / d, k = i - col * d;
@@ -576,7 +597,7 @@ __global__ void __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(CHAIN 
                     : 0.0f;
     }
     float cpre[kChainPre];   // the next sub-window's upstream values (chain, wavefront 0)
-    if (chain && wave == 0 && tsn > 0 && b0 < w.B) chain_load(w, cr, b0, t1, tsn, lane, cpre);
+    if (chain && wave == 0 && tsn > 0 && b0 < w.B) chain_load(w, cc, t1, tsn, lane, cpre);
     // 1. J = E x + bias
     for (int u = wave; u < ntile * ctiles; u += nw) {
       const int nt = u / ctiles, ct = u - nt * ctiles;
@@ -597,7 +618,7 @@ __global__ void __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(CHAIN 
     __syncthreads();
     // next inputs into LDS (every read of this sub-window's X is done)
     if (chain && wave == 0 && tsn > 0 && b0 < w.B)
-      chain_inputs(w, cr, b0, t1, tsn, X, xs, ycur, lane, Cf, c0, cpre);
+      chain_inputs(w, cc, t1, tsn, X, xs, ycur, lane, Cf, c0, cpre);
 #pragma unroll
     for (int c = 0; c < kEnsXPre; ++c)
       if (tsn > 0 && xslot[c] >= 0) X[xlds[c]] = xpre[c];
@@ -668,8 +689,8 @@ __global__ void __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(CHAIN 
     }
     __syncthreads();
   }
-  if (chain && wave == 0 && lane < cr[4] && b0 < w.B)   // the filter state the next window starts from
-    w.va[(int64_t)(cr[3] + lane) * w.vs + (int64_t)w.T * w.B + b0] = ycur;
+  if (chain && wave == 0 && lane < crec[4] && b0 < w.B)   // the filter state the next window starts from
+    w.va[(int64_t)(crec[3] + lane) * w.vs + (int64_t)w.T * w.B + b0] = ycur;
   if (spiking) {
 #pragma unroll
     for (int j = 0; j < NPT; ++j) {

@@ -939,7 +939,7 @@ void ens_shape(ms_sim* s, Launch& l, const LGroup& g) {
   const int64_t nw = l.nthr / 64, dp = std::max<int32_t>(1, l.ens.d);
   // LDS row strides: inputs and currents are read and written by lanes 16
   // columns apart; padding the rows spreads those lanes over the banks
-  l.xs = stride2mod4((int32_t)dp);
+  l.xs = stride2mod4((int32_t)(4 * ((dp + 3) / 4)));   // whole k steps of 4
   l.js = nmax % 2 == 0 ? nmax + 1 : nmax;
   // sub-window: the longest (a multiple of 16, at most 64 steps) that keeps
   // about 32 wavefronts per CU resident within the CU's LDS and whose inputs
@@ -976,12 +976,15 @@ void ens_shape(ms_sim* s, Launch& l, const LGroup& g) {
   // (one column per workgroup; wavefront w owns neurons 64 w .. 64 w + 63 and
   // their 4 encoder tiles; two input buffers and two sets of per-wavefront
   // partial decodes)
-  const int64_t ntile = ((int64_t)nmax + 15) / 16;
-  const int64_t rw_lds = (2 * ts * l.xs + ts * l.js + 2 * nw * (ts / 16) * 256 + nmax + chain_f) * (int64_t)sizeof(float);
+  // (every slot a neuron row of the products: rows of nthr + 1 currents and
+  // nthr biases, zero past the op's neurons)
+  const int64_t ntile = ((int64_t)nmax + 15) / 16, rw_js = l.nthr + 1;
+  const int64_t rw_lds = (2 * ts * l.xs + ts * rw_js + 2 * nw * (ts / 16) * 256 + l.nthr + chain_f) * (int64_t)sizeof(float);
   if (l.npt == 1 && l.cpw == 1 && !(l.enc_lds && l.dec_lds) && ntile <= 4 * nw && dp <= 16 && l.ens.ndec <= 16 &&
       rw_lds <= (int64_t)s->lds_limit) {
     l.rw = 1;
     l.enc_lds = l.dec_lds = 0;
+    l.js = (int32_t)rw_js;
     l.lds = (size_t)rw_lds;
   }
 }
