@@ -17,6 +17,8 @@
 
 #include "kernels.hpp"
 
+#include <type_traits>
+
 struct WView {
   float* va;
   int64_t vs;      // row stride of va, (W + 1) * B
@@ -232,6 +234,24 @@ constexpr int kEnsXPre = 4;        // prefetched input values per thread
 // results are the same bit for bit.  Used when encoders and decoders are too
 // large to stage in LDS.
 constexpr int kRwTiles = 4, kRwKd = 4, kRwKs = 16;
+
+// One neuron's updates through tsv steps of its LDS column (stride js), each
+// current replaced by the neuron's output: blocks of 8 steps read their
+// currents first, so that one LDS wait covers a block and the addresses are
+// fixed offsets from one register.
+template <class F>
+__device__ __forceinline__ void sweep_cell(float* cell, int32_t js, int tsv, F&& upd) {
+  int st = 0;
+  for (; st + 8 <= tsv; st += 8) {
+    float* c = cell + st * js;
+    float jv[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) jv[u] = c[u * js];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) c[u * js] = upd(jv[u]);
+  }
+  for (; st < tsv; ++st) cell[st * js] = upd(cell[st * js]);
+}
 
 // The connection chain of Fig. 2 fused into an ensemble's input (window
 // driver; one wavefront, one batch column b0): for window steps t0 .. t0 + tsn
@@ -488,6 +508,10 @@ __global__ void __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(CHAIN 
     // the partials of every wavefront are added in wavefront order.  A
     // wavefront reads only LDS rows it wrote itself until that barrier.
     int xb = 0;
+    const int oq = tid / ncol, ocol = tid - oq * ncol;   // this thread's first decoded output
+    float* const odst = oq < ndec ? w.va + (int64_t)(oq < df0 ? o.d[0] + oq : o.d[1] + (oq - df0)) * w.vs +
+                                        (int64_t)(ocol + 1) * w.B + b0
+                                  : w.va;
     for (int32_t t0 = 0; t0 < w.T; t0 += ts) {
       const int tsv = min(ts, w.T - t0);
       const int32_t t1 = t0 + ts;
@@ -509,33 +533,41 @@ __global__ void __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(CHAIN 
       float* rb = red + xb * nw * ctiles * 256;
       // 1. currents of this wavefront's neurons (all four tiles: rows past n
       // compute zeros), loads and stores at fixed offsets from one address
+      // (all kRwKd k steps when d > 12: no test per step)
+      auto currents = [&](auto full) {
 #pragma unroll
-      for (int i = 0; i < kRwTiles; ++i) {
-        const int r0 = 16 * (kRwTiles * wave + i) + 4 * (lane / 16);
-        for (int ct = 0; ct < ctiles; ++ct) {
-          const int col = 16 * ct + lane % 16;
-          const float* xr = Xc + col * xs + lane / 16;
-          mfma_f4x acc = {0.0f, 0.0f, 0.0f, 0.0f};
+        for (int i = 0; i < kRwTiles; ++i) {
+          const int r0 = 16 * (kRwTiles * wave + i) + 4 * (lane / 16);
+          for (int ct = 0; ct < ctiles; ++ct) {
+            const int col = 16 * ct + lane % 16;
+            const float* xr = Xc + col * xs + lane / 16;
+            mfma_f4x acc = {0.0f, 0.0f, 0.0f, 0.0f};
 #pragma unroll
-          for (int kk = 0; kk < kRwKd; ++kk)
-            if (kk < kd) acc = __builtin_amdgcn_mfma_f32_16x16x4f32(ae[i][kk], xr[4 * kk], acc, 0, 0, 0);
-          float* jr = Jb + col * js + r0;
+            for (int kk = 0; kk < kRwKd; ++kk)
+              if (decltype(full)::value || kk < kd)
+                acc = __builtin_amdgcn_mfma_f32_16x16x4f32(ae[i][kk], xr[4 * kk], acc, 0, 0, 0);
+            float* jr = Jb + col * js + r0;
 #pragma unroll
-          for (int q = 0; q < 4; ++q) jr[q] = acc[q] + Bl[r0 + q];
+            for (int q = 0; q < 4; ++q) jr[q] = acc[q] + Bl[r0 + q];
+          }
         }
-      }
+      };
+      if (kd == kRwKd)
+        currents(std::true_type{});
+      else
+        currents(std::false_type{});
       // 2. its neurons through the sub-window (slot tid: neuron tid, column 0;
       // slots past n carry zero state and current, and output zeros)
       if (b0 < w.B) {
         float* cell = Jb + tid;
-        if (bf) {
-          for (int st = 0; st < tsv; ++st)
-            cell[st * js] = lif_update_bf(cell[st * js], v[0], rf[0], tau6, o.tau_ref, amp_dt, dt, o.inv_tau);
-        } else {
+        if (bf)
+          sweep_cell(cell, js, tsv, [&](float j) {
+            return lif_update_bf(j, v[0], rf[0], tau6, o.tau_ref, amp_dt, dt, o.inv_tau);
+          });
+        else
           for (int st = 0; st < tsv; ++st)
             cell[st * js] = neuron_update(E.ntype, cell[st * js], v[0], rf[0], o.tau_rc, o.tau_ref, o.amp, o.full,
                                           dt, o.inv_tau);
-        }
       }
       // 3. its neurons' share of the decoded outputs
       for (int ct = 0; ndec > 0 && ct < ctiles; ++ct) {
@@ -562,16 +594,23 @@ __global__ void __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(CHAIN 
         }
       }
       __syncthreads();
-      // 5. decoded outputs: the wavefronts' partials in wavefront order
-      for (int i = tid; i < ndec * ncol; i += nthr) {
-        const int q = i / ncol, col = i - q * ncol;
-        if (col < tsv && b0 < w.B) {
-          float sum = 0.0f;
-          for (int ww = 0; ww < nw; ++ww) sum += rb[((ww * ctiles + col / 16) * 16 + q) * 16 + col % 16];
-          const int dr = q < df0 ? o.d[0] + q : o.d[1] + (q - df0);
-          w.va[(int64_t)dr * w.vs + (int64_t)(t0 + col + 1) * w.B + b0] = sum;
+      // 5. decoded outputs: the wavefronts' partials in wavefront order (the
+      // first output of each thread from its precomputed slot)
+      if (b0 < w.B)
+        for (int i = tid; i < ndec * ncol; i += nthr) {
+          int q = oq, col = ocol;
+          float* dst = odst;
+          if (i != tid) {
+            q = i / ncol, col = i - q * ncol;
+            dst = w.va + (int64_t)(q < df0 ? o.d[0] + q : o.d[1] + (q - df0)) * w.vs + (int64_t)(col + 1) * w.B + b0;
+          }
+          if (col < tsv) {
+            const float* pr = rb + ((col / 16) * 16 + q) * 16 + col % 16;
+            float sum = 0.0f;
+            for (int ww = 0; ww < nw; ++ww) sum += pr[ww * ctiles * 256];
+            dst[(int64_t)t0 * w.B] = sum;
+          }
         }
-      }
       if (o.s >= 0) {   // neuron outputs of every wavefront, then a barrier before they are overwritten
         for (int i = tid; i < ncol * n; i += nthr) {
           const int r = i / ncol, st = i - r * ncol;
