@@ -541,14 +541,14 @@ __global__ void __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(CHAIN 
           for (int ct = 0; ct < ctiles; ++ct) {
             const int col = 16 * ct + lane % 16;
             const float* xr = Xc + col * xs + lane / 16;
-            mfma_f4x acc = {0.0f, 0.0f, 0.0f, 0.0f};
+            mfma_f4x acc = {Bl[r0], Bl[r0 + 1], Bl[r0 + 2], Bl[r0 + 3]};   // J = bias + E x
 #pragma unroll
             for (int kk = 0; kk < kRwKd; ++kk)
               if (decltype(full)::value || kk < kd)
                 acc = __builtin_amdgcn_mfma_f32_16x16x4f32(ae[i][kk], xr[4 * kk], acc, 0, 0, 0);
             float* jr = Jb + col * js + r0;
 #pragma unroll
-            for (int q = 0; q < 4; ++q) jr[q] = acc[q] + Bl[r0 + q];
+            for (int q = 0; q < 4; ++q) jr[q] = acc[q];
           }
         }
       };
@@ -641,7 +641,10 @@ __global__ void __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(CHAIN 
     for (int u = wave; u < ntile * ctiles; u += nw) {
       const int nt = u / ctiles, ct = u - nt * ctiles;
       const int col = 16 * ct + lane % 16;
-      mfma_f4x acc = {0.0f, 0.0f, 0.0f, 0.0f};
+      const int rb0 = 16 * nt + 4 * (lane / 16);
+      mfma_f4x acc;   // J = bias + E x (rows past n unused)
+#pragma unroll
+      for (int q = 0; q < 4; ++q) acc[q] = rb0 + q < n ? Bl[rb0 + q] : 0.0f;
       for (int kk = 0; kk < kd; ++kk) {
         const int ra = 16 * nt + lane % 16, k = 4 * kk + lane / 16;
         const float a = (ra < n && k < d) ? (enc_lds ? El[ra * xs + k] : enc[(int64_t)ra * E.d + k]) : 0.0f;
@@ -650,8 +653,8 @@ __global__ void __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(CHAIN 
       }
 #pragma unroll
       for (int q = 0; q < 4; ++q) {
-        const int r = 16 * nt + 4 * (lane / 16) + q;
-        if (r < n) Jb[col * js + r] = acc[q] + Bl[r];
+        const int r = rb0 + q;
+        if (r < n) Jb[col * js + r] = acc[q];
       }
     }
     __syncthreads();
