@@ -374,8 +374,20 @@ def summarize_traffic(args):
         vals = [v for k, vs in per.items() if hit(k) for v in vs]
         if not vals:
             raise SystemExit(f"kernels {names} not found in {d}")
-        res[kind] = {"raw_bytes_per_launch": sum(vals) / len(vals), "scale": scale, "launches": len(vals),
-                     "bytes_per_launch": scale * sum(vals) / len(vals)}
+        raw, launches = sum(vals) / len(vals), len(vals)
+        if args.sum_kernels:
+            # the kernels run together as one launch of the operator (one dispatch of
+            # each per launch): a launch moves the sum of their per-dispatch averages
+            by = {}
+            for k, vs in per.items():
+                if hit(k):
+                    by.setdefault(k.split("(")[0].split("<")[0].strip().split(" ")[-1], []).extend(vs)
+            counts = {len(vs) for vs in by.values()}
+            if len(counts) != 1:
+                raise SystemExit(f"--sum-kernels: dispatch counts differ {[(k, len(v)) for k, v in by.items()]}")
+            raw, launches = sum(sum(vs) / len(vs) for vs in by.values()), counts.pop()
+        res[kind] = {"raw_bytes_per_launch": raw, "scale": scale, "launches": launches,
+                     "bytes_per_launch": scale * raw}
     workload = args.config + ("event" if args.event_decode else "")
     rec = {"kernel": args.kernel, "kernels_counted": names, "workload": workload,
            "bytes_per_launch": int(res["fetch"]["bytes_per_launch"] + res["write"]["bytes_per_launch"]),
@@ -434,6 +446,9 @@ def main():
     ap.add_argument("--match", default="",
                     help="comma-separated kernel names counted by --summarize-traffic (default: --kernel); "
                          "list every kernel of the operator type the roofline times")
+    ap.add_argument("--sum-kernels", action="store_true",
+                    help="--summarize-traffic: the --match kernels are one operator launch (one dispatch "
+                         "each); count their sum per launch")
     ap.add_argument("--timesteps", type=int, default=0,
                     help="override the workload's timesteps (counter passes: per-launch traffic of a "
                          "time-major kernel does not depend on the run length)")
