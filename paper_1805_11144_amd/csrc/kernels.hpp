@@ -89,12 +89,17 @@ __device__ __forceinline__ void lif_rate_item(float* st, const Strides& S, int64
   st[at(S, rowof(s, r), b)] = out;
 }
 
+// One lowpass step y <- a y + c v with its rounding fixed (c v rounded, then
+// a y added in one fma), so that every kernel that runs a filter, fused or
+// not, gives the same bits.
+__device__ __forceinline__ float lowpass_step(float a, float y, float c, float v) { return fmaf(a, y, c * v); }
+
 __device__ __forceinline__ void lowpass_item(float* st, const Strides& S, int64_t r, int64_t b,
                                              const Opnd& y, const Opnd& v, const FilterParams& fp) {
   const float a = fp.a_r ? G(fp.a_r)[r] : fp.a;
   const float c = fp.b_r ? G(fp.b_r)[r] : fp.b;
   const int64_t yi = at(S, rowof(y, r), b);
-  st[yi] = a * st[yi] + c * st[at(S, rowof(v, r), b)];
+  st[yi] = lowpass_step(a, st[yi], c, st[at(S, rowof(v, r), b)]);
 }
 
 __device__ __forceinline__ float src_val(const float* base, const Strides& S, int bcast, int64_t row,
@@ -798,8 +803,9 @@ struct SynW {
 constexpr int kSynRows = 16, kSynLanes = 4, kSynPerLane = 2, kSynChunk = kSynLanes * kSynPerLane;
 
 // sum_k w[k] x[k] in k order (the DotInc kernel's order); x[k] at xp[k * xs]
-template <int KK>
-__device__ __forceinline__ float syn_dot_fixed(gptr<float> wr, const float* xp, int64_t xs) {
+// (UNIT: xs = 1, the inputs at fixed offsets from one address)
+template <int KK, bool UNIT>
+__device__ __forceinline__ float syn_dot_fixed(gptr<float> wr, const float* xp, int64_t xs, float d = 0.0f) {
   typedef float f4v __attribute__((ext_vector_type(4)));
   const __attribute__((address_space(1))) f4v* w4 = (const __attribute__((address_space(1))) f4v*)wr;
   f4v wv[KK / 4];
@@ -807,8 +813,7 @@ __device__ __forceinline__ float syn_dot_fixed(gptr<float> wr, const float* xp, 
 #pragma unroll
   for (int k4 = 0; k4 < KK / 4; ++k4) wv[k4] = w4[k4];
 #pragma unroll
-  for (int k = 0; k < KK; ++k) xv[k] = xp[k * xs];
-  float d = 0.0f;
+  for (int k = 0; k < KK; ++k) xv[k] = xp[UNIT ? k : k * xs];
 #pragma unroll
   for (int k4 = 0; k4 < KK / 4; ++k4) {
     d += wv[k4][0] * xv[4 * k4];
@@ -819,9 +824,13 @@ __device__ __forceinline__ float syn_dot_fixed(gptr<float> wr, const float* xp, 
   return d;
 }
 
+template <bool UNIT>
 __device__ __forceinline__ float syn_dot(gptr<float> wr, const float* xp, int64_t xs, int32_t K) {
-  if (K == 16) return syn_dot_fixed<16>(wr, xp, xs);
-  if (K == 32) return syn_dot_fixed<32>(wr, xp, xs);
+  if (K == 16) return syn_dot_fixed<16, UNIT>(wr, xp, xs);
+  if (K == 32) {   // two blocks of 16 (fewer registers), the sum still in k order
+    const float d0 = syn_dot_fixed<16, UNIT>(wr, xp, xs);
+    return syn_dot_fixed<16, UNIT>(wr + 16, xp + (UNIT ? 16 : 16 * xs), xs, d0);
+  }
   float d = 0.0f;
   if ((K & 3) == 0) {
     typedef float f4v __attribute__((ext_vector_type(4)));
@@ -855,12 +864,18 @@ __device__ __forceinline__ SynRec syn_rec(const SynConn* conn, int32_t c, bool l
   return r;
 }
 
-__global__ void __launch_bounds__(256) k_syn_scatter(float* st, Strides S, int32_t B, int32_t nseg,
+// UNIT: one batch column (B = 1, row stride 1), so a connection's inputs are
+// consecutive floats.
+template <bool UNIT>
+__global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(UNIT ? 5 : 1))) k_syn_scatter(float* st, Strides S, int32_t B, int32_t nseg,
                                                      const int32_t* seg, const SynConn* conn, SynW W,
                                                      int32_t update, float* probe, int32_t probe_rows,
                                                      const float* stage, int32_t feed_rows, const int64_t* ctr,
                                                      int32_t du) {
   const uint32_t wv = (blockIdx.x * blockDim.x + threadIdx.x) / 64;
+  // slots per lane: one when the inputs are consecutive (fewer registers, more
+  // wavefronts resident), kSynPerLane otherwise
+  constexpr int PL = UNIT ? 1 : kSynPerLane, CH = kSynLanes * PL;
   const int lane = threadIdx.x % 64, i = lane % kSynRows, j = lane / kSynRows;
   const uint32_t sg = wv / (uint32_t)B, b = wv - sg * (uint32_t)B;
   if (sg >= (uint32_t)nseg) return;   // the whole wavefront leaves together
@@ -870,23 +885,23 @@ __global__ void __launch_bounds__(256) k_syn_scatter(float* st, Strides S, int32
   const int32_t c0 = sd[2], nc = sd[3];
   // run-relative step (feed staging) and absolute step (probe record)
   const int64_t tr = update ? ctr[1] + du : 0, ta = update ? ctr[0] + du : 0;
-  SynRec nxt[kSynPerLane];
+  SynRec nxt[PL];
 #pragma unroll
-  for (int h = 0; h < kSynPerLane; ++h) nxt[h] = syn_rec(conn, c0 + j + kSynLanes * h, row && j + kSynLanes * h < nc);
+  for (int h = 0; h < PL; ++h) nxt[h] = syn_rec(conn, c0 + j + kSynLanes * h, row && j + kSynLanes * h < nc);
   float acc = 0.0f;
-  for (int32_t q0 = 0; q0 < nc; q0 += kSynChunk) {
-    SynRec cur[kSynPerLane];
+  for (int32_t q0 = 0; q0 < nc; q0 += CH) {
+    SynRec cur[PL];
 #pragma unroll
-    for (int h = 0; h < kSynPerLane; ++h) cur[h] = nxt[h];
+    for (int h = 0; h < PL; ++h) cur[h] = nxt[h];
 #pragma unroll
-    for (int h = 0; h < kSynPerLane; ++h) {
-      const int32_t q = q0 + kSynChunk + j + kSynLanes * h;
+    for (int h = 0; h < PL; ++h) {
+      const int32_t q = q0 + CH + j + kSynLanes * h;
       nxt[h] = syn_rec(conn, c0 + q, row && q < nc);
     }
     // values (loads of both connections first, then the products)
-    float y[kSynPerLane], v[kSynPerLane];
+    float y[PL], v[PL];
 #pragma unroll
-    for (int h = 0; h < kSynPerLane; ++h) {
+    for (int h = 0; h < PL; ++h) {
       const SynRec& r = cur[h];
       y[h] = 0.0f;
       v[h] = 0.0f;
@@ -903,22 +918,22 @@ __global__ void __launch_bounds__(256) k_syn_scatter(float* st, Strides S, int32
         gptr<float> wr = G(W.w[ws]) + ((int64_t)r.w + i) * K;
         const float* xp = staged ? stage + (tr * feed_rows + r.x) * B + b : st + at(S, r.x, b);
         const int64_t xs = staged ? (int64_t)B : S.rs;
-        v[h] = 0.0f + syn_dot(wr, xp, xs, K);   // the DotInc adds into a reset row
+        v[h] = 0.0f + syn_dot<UNIT>(wr, xp, xs, K);   // the DotInc adds into a reset row
       }
     }
 #pragma unroll
-    for (int h = 0; h < kSynPerLane; ++h) {
+    for (int h = 0; h < PL; ++h) {
       const SynRec& r = cur[h];
       if (r.y == -3 || !update) continue;
       if (r.v != -2) {
-        y[h] = __builtin_bit_cast(float, r.a) * y[h] + __builtin_bit_cast(float, r.b) * v[h];
+        y[h] = lowpass_step(__builtin_bit_cast(float, r.a), y[h], __builtin_bit_cast(float, r.b), v[h]);
         st[at(S, (int64_t)r.y + i, b)] = y[h];
       }
       if (probe && r.p >= 0) probe[(ta * probe_rows + r.p + i) * B + b] = y[h];
     }
     // every lane takes part in the exchange; only lanes j == 0 keep a sum
 #pragma unroll
-    for (int jj = 0; jj < kSynChunk; ++jj) {
+    for (int jj = 0; jj < CH; ++jj) {
       const float u = __shfl(y[jj / kSynLanes], i + kSynRows * (jj % kSynLanes), 64);
       if (q0 + jj < nc) acc += u;
     }

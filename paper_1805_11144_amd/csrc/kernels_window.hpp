@@ -165,7 +165,7 @@ __global__ void k_w_lowpass(WView w, int64_t rows, Opnd y, Opnd v, FilterParams 
     for (int u = 0; u < 32; ++u) vin[u] = w.va[vr + (int64_t)(t + u) * w.B];
 #pragma unroll
     for (int u = 0; u < 32; ++u) {
-      yv = a * yv + c * vin[u];
+      yv = lowpass_step(a, yv, c, vin[u]);
       w.va[yr + (int64_t)(t + u + 1) * w.B] = yv;
     }
   }
@@ -175,12 +175,12 @@ __global__ void k_w_lowpass(WView w, int64_t rows, Opnd y, Opnd v, FilterParams 
     for (int u = 0; u < 8; ++u) vin[u] = w.va[vr + (int64_t)(t + u) * w.B];
 #pragma unroll
     for (int u = 0; u < 8; ++u) {
-      yv = a * yv + c * vin[u];
+      yv = lowpass_step(a, yv, c, vin[u]);
       w.va[yr + (int64_t)(t + u + 1) * w.B] = yv;
     }
   }
   for (; t < w.T; ++t) {
-    yv = a * yv + c * w.va[vr + (int64_t)t * w.B];
+    yv = lowpass_step(a, yv, c, w.va[vr + (int64_t)t * w.B]);
     w.va[yr + (int64_t)(t + 1) * w.B] = yv;
   }
 }

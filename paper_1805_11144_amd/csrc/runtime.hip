@@ -660,10 +660,16 @@ void launch_group(ms_sim* s, const Launch& l, int32_t du) {
       // one wavefront per (segment, batch column)
       const double items = (double)l.rows * 64 * B;
       if (items >= 4294967296.0) fail(MS_E_INVALID, "fused synapse group too large for 32-bit indexing");
-      KL(k_syn_scatter, dim3(grid_for((int64_t)items)), dim3(kBlock), 0, q, st, S, B,
-                         (int32_t)l.rows, l.syn_seg, l.syn_conn, l.syn_w, l.syn_update,
-                         l.syn_probe ? s->probe_buf : nullptr, s->probe_rows, (const float*)s->feed_stage,
-                         s->plan->ir.feed_rows, (const int64_t*)s->ctr, du);
+      if (B == 1 && S.rs == 1)
+        KL(k_syn_scatter<true>, dim3(grid_for((int64_t)items)), dim3(kBlock), 0, q, st, S, B,
+                           (int32_t)l.rows, l.syn_seg, l.syn_conn, l.syn_w, l.syn_update,
+                           l.syn_probe ? s->probe_buf : nullptr, s->probe_rows, (const float*)s->feed_stage,
+                           s->plan->ir.feed_rows, (const int64_t*)s->ctr, du);
+      else
+        KL(k_syn_scatter<false>, dim3(grid_for((int64_t)items)), dim3(kBlock), 0, q, st, S, B,
+                           (int32_t)l.rows, l.syn_seg, l.syn_conn, l.syn_w, l.syn_update,
+                           l.syn_probe ? s->probe_buf : nullptr, s->probe_rows, (const float*)s->feed_stage,
+                           s->plan->ir.feed_rows, (const int64_t*)s->ctr, du);
       break;
     }
     case OP_BDOT_INC:
