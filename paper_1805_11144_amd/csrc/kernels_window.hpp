@@ -677,8 +677,9 @@ __global__ void __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(CHAIN 
       if (c < cpw && b0 + c < w.B && r < n) {
         float* cell = Jb + (int64_t)c * ts * js + r;
         if (bf) {
-          for (int st = 0; st < tsv; ++st)
-            cell[st * js] = lif_update_bf(cell[st * js], v[j], rf[j], tau6, o.tau_ref, amp_dt, dt, o.inv_tau);
+          sweep_cell(cell, js, tsv, [&](float jc) {
+            return lif_update_bf(jc, v[j], rf[j], tau6, o.tau_ref, amp_dt, dt, o.inv_tau);
+          });
         } else {
           for (int st = 0; st < tsv; ++st)
             cell[st * js] = neuron_update(E.ntype, cell[st * js], v[j], rf[j], o.tau_rc, o.tau_ref, o.amp,
