@@ -931,12 +931,17 @@ void ens_shape(ms_sim* s, Launch& l, const LGroup& g) {
   int32_t nmax = 1;
   for (int32_t n : g.ens_n) nmax = std::max(nmax, n);
   l.nmax = nmax;
-  // batch columns per workgroup: fill up to 256 threads (4 wavefronts) with
-  // whole columns; an ensemble of more neurons takes one column and up to 512
-  // threads.  Small workgroups let a CU interleave more of them around each
-  // one's barriers (128 product ensembles of 100 neurons, minibatch 64, 1000
-  // steps: 2 columns per workgroup ran 1.47 ms against 1.76 ms with 5)
-  l.cpw = (int32_t)std::max<int64_t>(1, std::min<int64_t>(s->B, 256 / nmax));
+  // batch columns per workgroup: one when the weights-in-registers kernel
+  // applies (at most 512 neurons, d and decoded dimensions at most 16: its
+  // sub-window needs one barrier; 128 product ensembles of 100 neurons,
+  // minibatch 64, 1000 steps: 2.0 ms per run against 2.5 with 2 columns per
+  // workgroup and weights in LDS); otherwise fill up to 256 threads (4
+  // wavefronts) with whole columns, and an ensemble of more neurons takes one
+  // column and up to 512 threads.  Small workgroups let a CU interleave more of
+  // them around each one's barriers (2 columns per workgroup ran 1.47 ms
+  // against 1.76 ms with 5)
+  const bool rw_shape = nmax <= 512 && std::max<int32_t>(1, l.ens.d) <= 16 && l.ens.ndec <= 16;
+  l.cpw = rw_shape ? 1 : (int32_t)std::max<int64_t>(1, std::min<int64_t>(s->B, 256 / nmax));
   l.nthr = (int32_t)std::min<int64_t>(512, ((int64_t)nmax * l.cpw + 63) / 64 * 64);
   l.npt = (int32_t)(((int64_t)nmax * l.cpw + l.nthr - 1) / l.nthr);
   if (l.npt > 8) fail(MS_E_INVALID, "ensemble too large for the window driver (more than 4096 neurons)");
@@ -975,10 +980,10 @@ void ens_shape(ms_sim* s, Launch& l, const LGroup& g) {
   l.ts = (int32_t)ts;
   l.kch = (int32_t)kch_of(ts);
   l.lds = (size_t)bytes(ts);
-  // weights too large for LDS: keep each wavefront's encoder and decoder
-  // fragments in registers for the whole window, when they fit the kernel's
-  // register arrays (at most 4 neuron tiles of 16 per wavefront, d <= 16, at
-  // most 16 k steps of 4 per decoder chunk, each wavefront on one chunk)
+  // keep each wavefront's encoder and decoder fragments in registers for the
+  // whole window when they fit the kernel's register arrays (at most 4 neuron
+  // tiles of 16 per wavefront, d <= 16, at most 16 k steps of 4 per decoder
+  // chunk, each wavefront on one chunk), also when they would fit in LDS
   // (one column per workgroup; wavefront w owns neurons 64 w .. 64 w + 63 and
   // their 4 encoder tiles; two input buffers and two sets of per-wavefront
   // partial decodes)
@@ -986,7 +991,7 @@ void ens_shape(ms_sim* s, Launch& l, const LGroup& g) {
   // nthr biases, zero past the op's neurons)
   const int64_t ntile = ((int64_t)nmax + 15) / 16, rw_js = l.nthr + 1;
   const int64_t rw_lds = (2 * ts * l.xs + ts * rw_js + 2 * nw * (ts / 16) * 256 + l.nthr + chain_f) * (int64_t)sizeof(float);
-  if (l.npt == 1 && l.cpw == 1 && !(l.enc_lds && l.dec_lds) && ntile <= 4 * nw && dp <= 16 && l.ens.ndec <= 16 &&
+  if (l.npt == 1 && l.cpw == 1 && ntile <= 4 * nw && dp <= 16 && l.ens.ndec <= 16 &&
       rw_lds <= (int64_t)s->lds_limit) {
     l.rw = 1;
     l.enc_lds = l.dec_lds = 0;

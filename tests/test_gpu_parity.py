@@ -150,6 +150,25 @@ def test_window_ensembles_weights_in_registers(neuron_type):
 
 
 @pytest.mark.parametrize("neuron_type", ["lif_rate", "lif"])
+@pytest.mark.parametrize("n_neurons,dims", [(60, 20), (600, 16)])
+def test_window_ensembles_weights_in_lds(neuron_type, n_neurons, dims):
+    """Ensembles the weights-in-registers kernel does not take (20-D: several
+    batch columns per workgroup, encoders and decoders staged in LDS; 600
+    neurons: two per thread): the window kernel with weights in LDS, checked
+    against the oracle like the other window-driver runs."""
+    w = make_workload("c4", neuron_type=neuron_type, n_steps=40, minibatch=3, n_ens=3, n_neurons=n_neurons,
+                      dims=dims, n_eval=300)
+    got = run_gpu(w, driver=M.DRIVER_WINDOW)
+    if neuron_type == "lif":
+        _spiking_whole_run(w, got)
+        return
+    exp = run_oracle(w)
+    f32 = float32_run(w.spec, w.minibatch, w.n_steps, w.feeds)
+    for pi, (g, e, f) in enumerate(zip(got, exp, f32)):
+        check_rate_probe(f"lds weights probe {pi}", g, e, f)
+
+
+@pytest.mark.parametrize("neuron_type", ["lif_rate", "lif"])
 def test_window_product_tail_split(neuron_type):
     """A product with more 128 x 128 tiles than CUs but not a whole multiple
     of them (300 rows = 3 row tiles, 64 x 180 = 11520 columns = 90 column
