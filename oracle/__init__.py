@@ -14,6 +14,8 @@ Contents
                   sim.py on tiny models
   planner_ref.py  independent implementation of operator merging, planning,
                   sorting and simplification (paper Sec. 4.2)
+  train.py        objective, gradients and gradient-descent steps of a
+                  rate-neuron model through the unrolled simulation (Sec. 3.2)
 
 Parity status of each function is stated in its docstring; anything not pinned
 by a closed form, a library routine or brute force says "parity unpinned".

@@ -351,6 +351,44 @@ def make_pes(neuron_type="lif", n_steps=1000, minibatch=10, D=192, neurons_per_d
                     notes="PES learning of the identity, zero initial decoders, per-batch-row weights")
 
 
+# ------------------------------------------------------------------------ training
+def make_train(kind="mlp", neuron_type="lif_rate", seed=7, **overrides):
+    """A rate-neuron model to train by gradient descent (paper Sec. 3.2) and
+    seeded targets for some of its probes: (Workload, {probe: [B, T, w]}).
+
+    kind "mlp": the spiking-classifier shape (784-1024-1024-10, filtered
+      hidden connections, 50 steps, minibatch 256) with rate neurons; each
+      batch row's target on the readout probe is a one-hot class vector drawn
+      from the seed, at every step.
+    kind "chain": the ensemble-array shape (a chain of d-dimensional
+      ensembles with orthogonal transforms and lowpass synapses); targets on
+      the filtered decoded output: the input vector rotated by a seeded
+      orthogonal matrix, at every step.
+    kind "cconv": the circular-convolution shape (product ensembles, DFT
+      transforms, decoded product function, slices); targets on the output
+      node: seeded values of magnitude 0.1."""
+    if kind == "mlp":
+        w = make_c3(neuron_type=neuron_type, **overrides)
+        rng = _rng(seed, 1)
+        n_out = w.spec.nodes[1].size
+        cls = rng.integers(0, n_out, size=w.minibatch)
+        tgt = np.zeros((w.minibatch, w.n_steps, n_out), np.float32)
+        tgt[np.arange(w.minibatch), :, cls] = 1.0
+        return w, {0: tgt}
+    if kind == "chain":
+        w = make_c4(neuron_type=neuron_type, **overrides)
+        d = w.spec.nodes[0].size
+        R = random_orthogonal(_rng(seed, 2), d)
+        tgt = np.einsum("btd,ed->bte", w.feeds[0].astype(np.float64), R).astype(np.float32)
+        return w, {0: tgt}
+    if kind == "cconv":
+        w = make_c2(neuron_type=neuron_type, **overrides)
+        D = w.spec.nodes[4].size
+        tgt = (0.1 * _rng(seed, 3).standard_normal((w.minibatch, 1, D))).astype(np.float32)
+        return w, {0: np.ascontiguousarray(np.broadcast_to(tgt, (w.minibatch, w.n_steps, D)))}
+    raise ValueError(f"unknown training workload {kind!r}")
+
+
 _MAKERS = {"c1": make_c1, "c2": make_c2, "c3": make_c3, "c4": make_c4, "c5": make_c5, "bg": make_bg,
            "pes": make_pes}
 
