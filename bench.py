@@ -41,7 +41,10 @@ WORKLOADS = {
           "array transforms, B=1, T=1000",
     "pes": "online learning: 192-D input -> 9600 LIF -> PES-learned decoders (one 9600x192 matrix "
            "per batch row), error lowpass 0.005, B=10, T=1000",
+    "train": "training step: rate classifier 784-1024-1024-10 (LIF rate), lowpass 0.005, mean squared error "
+             "on one-hot targets at every step, gradient through all T=50 steps, B=256, gradient-descent update",
 }
+TRAIN_LR = 1e-4
 
 
 def compulsory_bytes_per_step(w):
@@ -204,6 +207,132 @@ def cpu_baseline(w, budget_s=12.0):
                       f"float64 numpy, {dt:.1f} s, {cores} BLAS threads",
             "single_thread": {"value": per * k1 / dt1, "cores": 1,
                               "sample": f"first {k1} of {w.n_steps} timesteps, {dt1:.1f} s, 1 thread"}}
+
+
+def train_cpu_baseline(w, targets, budget_s=12.0):
+    """Time the training oracle (float64 forward and reverse-mode gradient of
+    the whole run, then the update) on a bounded sample: all steps of the
+    first b batch rows, b doubled from 2 while a leg stays under a quarter of
+    the budget; once with torch's CPU threads and once with one."""
+    import torch
+    from oracle.train import TrainOracle
+
+    def leg():
+        b, rate, dt = 2, 0.0, 0.0
+        while True:
+            sub = {i: f[:b] for i, f in w.feeds.items()}
+            tg = {p: t[:b] for p, t in targets.items()}
+            tr = TrainOracle(w.spec, b)
+            t0 = time.perf_counter()
+            _, g, _ = tr.loss_and_grads(w.n_steps, sub, tg)
+            tr.sgd(g, TRAIN_LR)
+            dt = time.perf_counter() - t0
+            rate = w.n_neurons * w.n_steps * b / dt
+            if dt > budget_s / 4 or 2 * b > w.minibatch:
+                return b, rate, dt
+            b *= 2
+    threads = torch.get_num_threads()
+    b, rate, dt = leg()
+    torch.set_num_threads(1)
+    try:
+        b1, rate1, dt1 = leg()
+    finally:
+        torch.set_num_threads(threads)
+    return {"value": rate, "unit": "neuron-timesteps/s", "cores": int(threads), "kind": "oracle",
+            "sample": f"one training step (all {w.n_steps} steps, gradient, update) of the first {b} of "
+                      f"{w.minibatch} batch rows, float64 torch, {dt:.1f} s, {threads} threads",
+            "single_thread": {"value": rate1, "cores": 1,
+                              "sample": f"first {b1} batch rows, {dt1:.1f} s, 1 thread"}}
+
+
+def train_roofline(M, sim, w, feeds, targets, plan_json):
+    """Roofline of the largest operator kind of a training step, from HIP
+    events with per-launch timing on (one extra step): the weight-gradient
+    products (2 M K flops per op, step and batch row) against the fp32
+    MFMA peak when they dominate."""
+    sim.set_timing(True)
+    sim.train_step(w.n_steps, feeds, targets, TRAIN_LR)
+    times = {t: sim.kernel_time(t) for t in range(17)}
+    sim.set_timing(False)
+    top = max(times, key=lambda t: times[t][0])
+    ms, n = times[top]
+    TB = w.n_steps * w.minibatch
+    dots = [g for g in plan_json["groups"] if g["type"] == "DotInc"]
+    if top == M.mergesim.OP_GRAD_WEIGHTS:
+        work, kernel, op = sum(2 * g["M"] * g["K"] * len(g["w_row"]) for g in dots) * TB, "k_t_dw", "weight gradients"
+    elif top == M.mergesim.OP_DOT_INC:
+        work, kernel, op = sum(2 * g["M"] * g["K"] * len(g["w_row"]) for g in dots) * TB, "k_w_gemm2", "DotInc"
+    else:
+        return {"bound": None, "achieved": None, "peak": None, "unit": None, "frac": None, "traffic": None,
+                "kernel": f"timing kind {top}", "launch_ms": round(ms / max(n, 1), 4), "launches": n,
+                "busy_ms": round(ms, 4), "kinds_ms": {str(t): round(v[0], 4) for t, v in times.items() if v[1]}}
+    ach = work / (ms * 1e-3) / 1e12
+    return {"bound": "mfma", "achieved": round(ach, 3), "peak": FP32_MFMA_PEAK_TFLOPS, "unit": "TFLOP/s",
+            "frac": round(ach / FP32_MFMA_PEAK_TFLOPS, 4), "traffic": stored_traffic(kernel, "train"),
+            "basis": "algorithmic", "kernel": kernel, "op": op, "launch_ms": round(ms / max(n, 1), 4),
+            "launches": n, "busy_ms": round(ms, 4), "work_per_launch": int(work / max(n, 1)),
+            "kinds_ms": {str(t): round(v[0], 4) for t, v in times.items() if v[1]}}
+
+
+def main_train(args):
+    """One bench step = one training step of the classifier (ms_sim_train_step):
+    a run from the initial state over the whole batch, the objective, its
+    gradient through every step, and the update."""
+    import torch
+
+    import paper_1805_11144_amd as M
+    from synth import make_train
+
+    w, targets = make_train("mlp", **({"n_steps": args.timesteps} if args.timesteps else {}))
+    model = M.model_from_spec(w.spec)
+    dev = torch.device("cuda:0")
+    opts = dict(driver=M.DRIVER_WINDOW, fuse=False, simplify=False)
+    t_build = time.perf_counter()
+    sim = M.Simulator(model, minibatch=w.minibatch, probe_capacity_steps=w.n_steps, **opts)
+    t_build = time.perf_counter() - t_build
+    feeds = {i: torch.from_numpy(f).to(dev) for i, f in w.feeds.items()}
+    tg = {p: torch.from_numpy(t).to(dev) for p, t in targets.items()}
+    if args.copy_probe:
+        src = torch.ones(COPY_PROBE_BYTES // 4, dtype=torch.float32, device=dev)
+        dst = torch.empty_like(src)
+        dst.copy_(src)
+        del src, dst
+    torch.cuda.synchronize()
+    if args.counters_run:
+        sim.train_step(w.n_steps, feeds, tg, TRAIN_LR)
+        torch.cuda.synchronize()
+        return
+    for _ in range(args.warmup):
+        sim.train_step(w.n_steps, feeds, tg, TRAIN_LR)
+    torch.cuda.synchronize()
+    run_ms, losses = [], []
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        losses.append(sim.train_step(w.n_steps, feeds, tg, TRAIN_LR))   # returns when the step is done
+        run_ms.append(sim.last_run_ms())
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+    neuron_steps = w.n_neurons * w.n_steps * w.minibatch
+    run_mean, run_ci = mean_ci95(run_ms)
+    plan_json = M.Plan(model, minibatch=w.minibatch, fuse=False, simplify=False).json()
+    roofline = train_roofline(M, sim, w, feeds, tg, plan_json)
+    out = {
+        "metric": "training neuron-timesteps/sec (x minibatch) on 1 MI355X",
+        "value": neuron_steps / (elapsed / args.steps), "unit": "neuron-timesteps/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": 1000.0 * elapsed / args.steps,
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "f32", "data": "synthetic",
+        "config": {"workload": WORKLOADS["train"], "name": "train", "neurons": w.n_neurons,
+                   "timesteps": w.n_steps, "minibatch": w.minibatch, "driver": "window",
+                   "learning_rate": TRAIN_LR, "build_s": round(t_build, 2),
+                   "plan": {"fuse": False, "simplify": False}},
+        "runs": {"device_ms": [round(x, 4) for x in run_ms], "mean_ms": round(run_mean, 4),
+                 "ci95_ms": None if run_ci is None else round(run_ci, 4), "objective": losses},
+        "roofline": roofline,
+    }
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = train_cpu_baseline(w, targets, args.cpu_budget)
+    print(json.dumps(out))
+    sim.close()
 
 
 def mean_ci95(xs):
@@ -476,6 +605,9 @@ def main():
     if args.gpus != 1:
         print(json.dumps({"error": "this build runs on one GPU; --gpus must be 1"}))
         sys.exit(2)
+    if args.config == "train":
+        main_train(args)
+        return
 
     import torch
 

@@ -66,6 +66,12 @@ typedef struct ms_sim ms_sim;
 #define MS_NEURON_RELU 2      /* rectified linear: amplitude * max(J, 0); gain and bias
                                  from max_rates/intercepts put J = 0 at the intercept
                                  and J = max_rate at x = 1 (no state) */
+#define MS_NEURON_SOFTLIF_RATE 3  /* smoothed LIF rate, the differentiable stand-in for
+                                 the spiking LIF in training (Sec. 3.2 trains spiking
+                                 models through a rate approximation): amplitude /
+                                 (tau_ref + tau_rc log(1 + 1/rho)), rho = sigma
+                                 log(1 + exp((J - 1) / sigma)); gain and bias as for
+                                 LIF; never fused (MS_FUSE_ENSEMBLES skips it) */
 
 #define MS_FN_IDENTITY 0  /* decode x (d outputs) */
 #define MS_FN_PRODUCT 1   /* decode x0 * x1 (1 output, needs dims >= 2) */
@@ -92,6 +98,7 @@ typedef struct {
   const double* biases;         /* [n] or NULL */
   int32_t n_eval_points;
   const double* eval_points;    /* [M][d] or NULL */
+  double sigma;                 /* smoothing of MS_NEURON_SOFTLIF_RATE (> 0); ignored otherwise */
 } ms_ensemble_desc;
 
 /* Connection description (paper Sec. 2.1.2 "Connection", Fig. 2).
@@ -393,6 +400,78 @@ ms_status ms_sim_info(const ms_sim* sim, int32_t* driver_out, int32_t* groups_pe
  * records to every launch: leave it off for throughput runs. */
 ms_status ms_sim_set_timing(ms_sim* sim, int32_t on);
 ms_status ms_sim_kernel_time(ms_sim* sim, int32_t op_type, double* ms_out, int64_t* launches_out);
+
+/* ------------------------------------------------------------- training */
+
+/* Training by gradient descent (paper Sec. 3.2: an objective on probe outputs
+ * minimised with a gradient-descent optimiser, the gradient taken through
+ * every step of the unrolled simulation).
+ *
+ * One call of ms_sim_train_step:
+ *   1. restores the initial state (as ms_sim_reset, probes cleared) and runs
+ *      n_steps with the feeds (as ms_sim_run_steps; the probes record them);
+ *   2. computes the objective: for each target, the mean over minibatch rows,
+ *      steps and probe dimensions of (probe value - target)^2, summed over
+ *      the targets (mean squared error);
+ *   3. computes dL/dp for every trained parameter, through all n_steps;
+ *   4. if learning_rate != 0, updates each trained parameter p <- p -
+ *      learning_rate * dL/dp.
+ * *loss_out (if not NULL) receives the objective of step 2 (double); the call
+ * returns after the step has finished.
+ *
+ * Trained parameters: each ensemble's gain-scaled encoders [n][d] and biases
+ * [n]; each (ensemble, function)'s solved decoders (shared by every
+ * connection and probe that decodes that function); each connection's
+ * explicit decoders and its transform (matrix or scalar).  Gains of
+ * neuron-space inputs, node constants and filter coefficients stay fixed.
+ *
+ * Requirements (MS_E_STATE otherwise, with the reason): the simulator runs on
+ * MS_DRIVER_WINDOW with fp32 products, was created with fuse = 0 and
+ * simplify = 0 (fusion and simplification turn parameters into parts of
+ * other operators or into constants), its ensembles use rate neurons
+ * (MS_NEURON_LIF_RATE or MS_NEURON_RELU: the spiking LIF has no useful
+ * derivative) and it has no learning rule; n_steps must fit in one window of
+ * the window driver (its versioned signals hold every step for the backward
+ * pass).  Memory: the backward pass holds one more array the size of the
+ * window's versioned signals, plus gradients the size of the trained
+ * parameter bases.
+ *
+ * Targets: data [minibatch][n_steps][probe width] float32, host memory
+ * unless on_device != 0. */
+typedef struct {
+  int32_t probe_id;
+  int32_t on_device;
+  const float* data;
+} ms_target;
+
+ms_status ms_sim_train_step(ms_sim* sim, int64_t n_steps, const ms_feed* feeds, int32_t n_feeds,
+                            const ms_target* targets, int32_t n_targets, double learning_rate,
+                            double* loss_out);
+
+#define MS_TRAIN_ENCODERS 0       /* id = ensemble: [n][d] gain-scaled encoders */
+#define MS_TRAIN_BIASES 1         /* id = ensemble: [n] */
+#define MS_TRAIN_DECODERS 2       /* id = ensemble, function = MS_FN_*: [n][d_fn] */
+#define MS_TRAIN_CONN_DECODERS 3  /* id = connection with explicit decoders: [n][cols] */
+#define MS_TRAIN_TRANSFORM 4      /* id = connection: [rows][cols], or [1] for a scalar */
+
+/* Read a trained parameter's current value (gradient == 0) or its gradient
+ * from the last ms_sim_train_step (gradient != 0; zeros before the first),
+ * as float32 in the layout listed above, into host memory `out` (capacity
+ * `cap` floats; out == NULL sizes it).  *n_out receives the element count.
+ * MS_E_INVALID if the model has no such parameter. */
+ms_status ms_sim_train_param(ms_sim* sim, int32_t which, int32_t id, int32_t function, int32_t gradient,
+                             float* out, int64_t cap, int64_t* n_out);
+/* Overwrite a trained parameter (checkpoint restore; n must equal its element
+ * count).  Later runs and training steps use the new values. */
+ms_status ms_sim_set_train_param(ms_sim* sim, int32_t which, int32_t id, int32_t function, const float* in,
+                                 int64_t n);
+
+/* Timing kinds of a training step's backward pass for ms_sim_kernel_time
+ * (with timing on, the forward groups are timed under their MS_OP_* types as
+ * in ms_sim_run_steps): */
+#define MS_OP_GRAD_WEIGHTS 14  /* weight gradients of the merged DotInc groups */
+#define MS_OP_GRAD_INPUTS 15   /* adjoints of the DotInc inputs (products with W^T) */
+#define MS_OP_GRAD_OTHER 16    /* objective, elementwise, neuron and filter reverses, update */
 
 const char* ms_last_error(void);
 

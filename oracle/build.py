@@ -60,7 +60,7 @@ def ensemble_gain_bias(ens):
 def ensemble_activities(ens, gain, bias, X):
     """Rate-mode outputs [M, n] of the ensemble's neurons at represented values X."""
     J = (X @ np.asarray(ens.encoders, np.float64).T) * gain[None, :] + bias[None, :]
-    return rate_output(ens.neuron_type, J, ens.tau_rc, ens.tau_ref, ens.amplitude)
+    return rate_output(ens.neuron_type, J, ens.tau_rc, ens.tau_ref, ens.amplitude, ens.sigma)
 
 
 def ridge_decoders(A: np.ndarray, Y: np.ndarray, reg: float) -> np.ndarray:

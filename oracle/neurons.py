@@ -9,6 +9,10 @@ Pins (tests/test_oracle_neurons.py):
   gain_bias       r(g + b) == max_rate and g * intercept + b == 1
   relu_rate       max(J, 0) by definition; relu_gain_bias: g + b == max_rate and
                   g * intercept + b == 0 (tests/test_oracle_neurons.py)
+  soft_lif_rate   at J = 1 the closed form 1/(tau_ref + tau_rc ln(1 + 1/(sigma ln 2)));
+                  equal to lif_rate where J - 1 >> sigma; tends to lif_rate as
+                  sigma -> 0; far below threshold 1/(tau_ref + tau_rc ((1 - J)/sigma
+                  - ln sigma)) (tests/test_oracle_neurons.py)
 
 A rectified-linear rate neuron (the neuron type of the memory storage and
 retrieval example, Sec. 5.2) is also defined here: its output is amplitude *
@@ -95,10 +99,37 @@ def relu_gain_bias(max_rates, intercepts):
     return gain, bias
 
 
-def rate_output(neuron_type, J, tau_rc, tau_ref, amplitude):
-    """Output of a rate neuron: amplitude * r(J) with the LIF or the ReLU curve."""
+def soft_lif_rate(J, tau_rc, tau_ref, sigma):
+    """Smoothed LIF rate curve, the differentiable stand-in for the spiking LIF
+    when a model is trained by gradient descent (paper Sec. 3.2 trains spiking
+    models through a rate approximation; the smoothing is Hunsberger and
+    Eliasmith's): the threshold nonlinearity max(J - 1, 0) inside the LIF rate
+    curve becomes rho = sigma log(1 + exp((J - 1) / sigma)), so that
+    r = 1 / (tau_ref + tau_rc log(1 + 1 / rho)) for every J.  Its slope stays
+    bounded at threshold, where the exact curve's grows without bound; below
+    threshold it decays slowly (log(1 + 1/rho) grows like (1 - J) / sigma).
+
+    Evaluated with x = (J - 1) / sigma as log1p(1 / rho), rho = sigma
+    softplus(x), for x >= -30; below, where softplus(x) = exp(x) to a relative
+    exp(x) / 2, as log1p(rho) - log(rho) with log(rho) = log(sigma) + x, so
+    that nothing overflows or underflows."""
+    J = np.asarray(J, dtype=np.float64)
+    x = (J - 1.0) / sigma
+    far = x < -30.0
+    rho = sigma * np.logaddexp(0.0, np.where(far, 0.0, x))
+    q_near = np.log1p(1.0 / rho)
+    q_far = np.log1p(sigma * np.exp(np.minimum(x, 0.0))) - (np.log(sigma) + x)
+    q = np.where(far, q_far, q_near)
+    return 1.0 / (tau_ref + tau_rc * q)
+
+
+def rate_output(neuron_type, J, tau_rc, tau_ref, amplitude, sigma=0.0):
+    """Output of a rate neuron: amplitude * r(J) with the LIF, the smoothed LIF
+    (smoothing sigma) or the ReLU curve."""
     if neuron_type == "relu":
         return amplitude * relu_rate(J)
+    if neuron_type == "softlif_rate":
+        return amplitude * soft_lif_rate(J, tau_rc, tau_ref, sigma)
     return amplitude * lif_rate(J, tau_rc, tau_ref)
 
 

@@ -191,7 +191,7 @@ def build_ir(spec) -> IR:
             op(LIF, f"e{e}.neurons", src=whole(J), dst=whole(S), V=whole(V), ref=whole(R))
         else:
             op(LIF_RATE, f"e{e}.neurons", src=whole(J), dst=whole(S),
-               kind=2 if E.neuron_type == "relu" else 1)
+               kind={"relu": 2, "softlif_rate": 3}.get(E.neuron_type, 1))
         for fn, d, D in decs:
             op(RESET, f"e{e}.reset{_fn_tag(fn)}", dst=whole(d))
             op(DOT_INC, f"e{e}.dec{_fn_tag(fn)}", dst=whole(d), a=whole(D), src=whole(S))
@@ -310,7 +310,9 @@ def fuse_ensembles(ir: IR) -> None:
         kb, kn = by_name[p + ".bias"], by_name[p + ".neurons"]
         ke = by_name.get(p + ".enc")
         neu = ir.ops[kn]
-        if writers.get(neu.src.sig, 0) == 1 + (ke is not None):
+        # the soft LIF rate is never fused (the fused kernels compute LIF, LIF rate and ReLU)
+        soft = neu.type == LIF_RATE and neu.kind == 3
+        if not soft and writers.get(neu.src.sig, 0) == 1 + (ke is not None):
             dec_ops = []
             total = 0
             for tag in ("id", "prod"):
@@ -766,8 +768,8 @@ def lower_group(ir: IR, offset: Dict[int, int], g: List[int]) -> dict:
                 if t == LIF:
                     V.append(row(o.V, i)); R.append(row(o.ref, i))
         out.update(rows=len(J), dst=_operand(base(o0.dst), S), src=_operand(base(o0.src), J))
-        if t == LIF_RATE and o0.kind == 2:
-            out["neuron"] = 2
+        if t == LIF_RATE and o0.kind in (2, 3):
+            out["neuron"] = o0.kind
         if t == LIF:
             out.update(V=_operand(base(o0.V), V), ref=_operand(base(o0.ref), R))
     elif t == ENS:

@@ -294,7 +294,7 @@ class OracleSim:
                                                          ens.tau_rc, ens.tau_ref, ens.amplitude,
                                                          dtype=self.dtype)
                 else:
-                    s = rate_output(self.neuron_type[i], J, ens.tau_rc, ens.tau_ref, ens.amplitude)
+                    s = rate_output(self.neuron_type[i], J, ens.tau_rc, ens.tau_ref, ens.amplitude, ens.sigma)
                 out[obj] = s
         # learning rules read their error input and pre activity filter
         # before any filter moves

@@ -115,8 +115,10 @@ ms_status ms_model_add_ensemble(ms_model* m, const ms_ensemble_desc* d, int32_t*
   return guarded([&] {
     need(m && d && id_out, "NULL argument");
     need(d->n_neurons > 0 && d->dims > 0, "ensemble needs n_neurons > 0 and dims > 0");
-    need(d->neuron_type == MS_NEURON_LIF || d->neuron_type == MS_NEURON_LIF_RATE || d->neuron_type == MS_NEURON_RELU,
+    need(d->neuron_type == MS_NEURON_LIF || d->neuron_type == MS_NEURON_LIF_RATE || d->neuron_type == MS_NEURON_RELU ||
+             d->neuron_type == MS_NEURON_SOFTLIF_RATE,
          "unknown neuron type");
+    need(d->neuron_type != MS_NEURON_SOFTLIF_RATE || d->sigma > 0, "the soft LIF rate needs sigma > 0");
     need(d->tau_rc > 0 && d->tau_ref >= 0, "tau_rc must be > 0 and tau_ref >= 0");
     need(d->encoders != nullptr, "encoders are required");
     const size_t n = (size_t)d->n_neurons;
@@ -127,6 +129,7 @@ ms_status ms_model_add_ensemble(ms_model* m, const ms_ensemble_desc* d, int32_t*
     e.tau_rc = d->tau_rc;
     e.tau_ref = d->tau_ref;
     e.amplitude = d->amplitude;
+    e.sigma = d->neuron_type == MS_NEURON_SOFTLIF_RATE ? d->sigma : 0.0;
     e.encoders.assign(d->encoders, d->encoders + n * d->dims);
     if (d->gains) {
       need(d->biases != nullptr, "gains given without biases");

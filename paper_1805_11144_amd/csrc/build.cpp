@@ -24,9 +24,26 @@ double lif_rate(double J, double tau_rc, double tau_ref) {
   return 1.0 / (tau_ref + tau_rc * std::log1p(1.0 / (J - 1.0)));
 }
 
+// Smoothed LIF rate: max(J - 1, 0) replaced by rho = sigma log(1 + exp(x)),
+// x = (J - 1) / sigma; log(1 + 1/rho) directly for x >= -30, and below (where
+// softplus(x) = exp(x) to a relative exp(x) / 2) as log1p(rho) - log(rho) with
+// log(rho) = log(sigma) + x.
+double soft_lif_rate(double J, double tau_rc, double tau_ref, double sigma) {
+  const double x = (J - 1.0) / sigma;
+  double q;
+  if (x < -30.0) {
+    q = std::log1p(sigma * std::exp(x)) - (std::log(sigma) + x);
+  } else {
+    const double sp = x > 30.0 ? x + std::log1p(std::exp(-x)) : std::log1p(std::exp(x));
+    q = std::log1p(1.0 / (sigma * sp));
+  }
+  return 1.0 / (tau_ref + tau_rc * q);
+}
+
 // rate curve of the ensemble's neuron type (spiking LIF decodes from its rates)
 double rate_of(const EnsembleDesc& e, double J) {
   if (e.neuron_type == MS_NEURON_RELU) return J > 0.0 ? J : 0.0;
+  if (e.neuron_type == MS_NEURON_SOFTLIF_RATE) return soft_lif_rate(J, e.tau_rc, e.tau_ref, e.sigma);
   return lif_rate(J, e.tau_rc, e.tau_ref);
 }
 

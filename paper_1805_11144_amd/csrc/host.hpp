@@ -35,6 +35,7 @@ struct NodeDesc {
 struct EnsembleDesc {
   int32_t n = 0, d = 0, neuron_type = MS_NEURON_LIF;
   double tau_rc = 0.02, tau_ref = 0.002, amplitude = 1.0;
+  double sigma = 0.0;             // smoothing of the soft LIF rate curve
   std::vector<double> encoders;   // [n*d]
   std::vector<double> max_rates, intercepts, gains, biases;
   int32_t n_eval = 0;
@@ -139,6 +140,7 @@ struct Op {
   int32_t ntype = 0;                // ENS, LIF_RATE: MS_NEURON_*
   int32_t n = 0;                    // ENS: neurons
   double tau_rc = 0, tau_ref = 0, amp = 0;  // LIF params
+  double sigma = 0;                         // LIF_RATE, soft LIF rate: smoothing
   double coef_a = 0, coef_b = 0;            // LOWPASS y = coef_a y + coef_b v; PES coef_a
 };
 
@@ -211,6 +213,7 @@ struct LGroup {
   std::vector<float> values;
   // LIF / LIF_RATE parameters: uniform (size 1) or per row
   std::vector<float> tau_rc, tau_ref, amp;
+  std::vector<float> sigma;     // LIF_RATE of soft LIF rate neurons: smoothing (uniform or per row)
   // LOWPASS coefficients: uniform (size 1) or per row
   std::vector<float> ca, cb;
   // FEED: staging rows per destination row

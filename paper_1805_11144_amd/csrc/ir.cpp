@@ -264,7 +264,7 @@ IR build_ir(const Model& m, const Built& bp, double dt) {
       o.src = B.whole(eJ[e]);
       o.dst = B.whole(eS[e]);
       if (lif) { o.V = B.whole(V); o.ref = B.whole(R); }
-      o.tau_rc = E.tau_rc; o.tau_ref = E.tau_ref; o.amp = E.amplitude;
+      o.tau_rc = E.tau_rc; o.tau_ref = E.tau_ref; o.amp = E.amplitude; o.sigma = E.sigma;
     }
     for (size_t k = 0; k < fns[e].size(); ++k) {
       const std::string tag = fn_tag(fns[e][k]);
@@ -481,6 +481,8 @@ void fuse_ensembles(IR& ir) {
     if (kb < 0 || kn < 0) break;
     const Op& nop = ir.ops[kn];
     const int32_t J = nop.src.sig;
+    // the fused kernels compute the LIF, LIF rate and ReLU curves only
+    if (nop.type == OP_LIF_RATE && nop.ntype == MS_NEURON_SOFTLIF_RATE) continue;
     // J must be written only by the bias op and the encoder op
     const int32_t ke = find(p + ".enc");
     if (writers[J] != 1 + (ke >= 0 ? 1 : 0)) continue;

@@ -40,7 +40,33 @@ struct NeuronParams {
   const float *tau_rc_r, *tau_ref_r, *amp_r;      // per-row values or null
   const float* full_r;                            // per-row expm1(-dt / tau_rc) or null
   int32_t relu;                                   // rate neurons: 1 = rectified linear
+  float sigma;                                    // rate neurons: > 0 = soft LIF rate, its smoothing
+  const float* sigma_r;                           // per-row smoothing or null
 };
+
+// Soft LIF rate curve r(J) (without amplitude): the LIF rate with max(J - 1, 0)
+// replaced by rho = s log(1 + exp(x)), x = (J - 1) / s.  For x >= -15,
+// log(1 + 1/rho) is evaluated directly from rho = s softplus(x); below, where
+// softplus(x) = exp(x) to a relative exp(x) / 2 < 2e-7, as log1p(rho) -
+// log(rho) with log(rho) = log(s) + x, so nothing overflows or underflows.
+// Also returns rho'/rho and rho for the derivative.
+__device__ __forceinline__ float soft_lif_rate(float j, float tau_rc, float tau_ref, float s, float* dlog,
+                                               float* rho_out) {
+  const float x = (j - 1.0f) / s;
+  float q, rho;
+  if (x < -15.0f) {
+    rho = s * expf(x);
+    q = log1pf(rho) - (logf(s) + x);
+    *dlog = 1.0f / s;   // sigmoid(x) / (s softplus(x)) = 1 / s to 2e-7
+  } else {
+    const float sp = x > 15.0f ? x + log1pf(expf(-x)) : log1pf(expf(x));
+    rho = s * sp;
+    q = log1pf(1.0f / rho);
+    *dlog = 1.0f / ((1.0f + expf(-x)) * rho);
+  }
+  *rho_out = rho;
+  return 1.0f / (tau_ref + tau_rc * q);
+}
 
 struct FilterParams {
   float a, b;                 // y = a y + b v (uniform)
@@ -84,8 +110,14 @@ __device__ __forceinline__ void lif_rate_item(float* st, const Strides& S, int64
   const float amp = np.amp_r ? G(np.amp_r)[r] : np.amp;
   const float j = st[at(S, rowof(J, r), b)];
   float out = 0.0f;
-  if (np.relu) out = amp * fmaxf(j, 0.0f);
-  else if (j > 1.0f) out = amp / (tau_ref + tau_rc * log1pf(1.0f / (j - 1.0f)));
+  if (np.relu) {
+    out = amp * fmaxf(j, 0.0f);
+  } else if (np.sigma > 0.0f) {
+    float dl, rho;
+    out = amp * soft_lif_rate(j, tau_rc, tau_ref, np.sigma_r ? G(np.sigma_r)[r] : np.sigma, &dl, &rho);
+  } else if (j > 1.0f) {
+    out = amp / (tau_ref + tau_rc * log1pf(1.0f / (j - 1.0f)));
+  }
   st[at(S, rowof(s, r), b)] = out;
 }
 

@@ -108,8 +108,14 @@ __global__ void k_w_lif_rate(WView w, int64_t rows, Opnd J, Opnd s, NeuronParams
   const float amp = np.amp_r ? G(np.amp_r)[_r] : np.amp;
   const float j = w.va[vat(w, rowof(J, _r), (int64_t)jblk * w.B + _c)];
   float out = 0.0f;
-  if (np.relu) out = amp * fmaxf(j, 0.0f);
-  else if (j > 1.0f) out = amp / (tau_ref + tau_rc * log1pf(1.0f / (j - 1.0f)));
+  if (np.relu) {
+    out = amp * fmaxf(j, 0.0f);
+  } else if (np.sigma > 0.0f) {
+    float dl, rho;
+    out = amp * soft_lif_rate(j, tau_rc, tau_ref, np.sigma_r ? G(np.sigma_r)[_r] : np.sigma, &dl, &rho);
+  } else if (j > 1.0f) {
+    out = amp / (tau_ref + tau_rc * log1pf(1.0f / (j - 1.0f)));
+  }
   w.va[vat(w, rowof(s, _r), w.B + _c)] = out;
 }
 

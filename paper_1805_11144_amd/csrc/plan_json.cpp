@@ -100,7 +100,8 @@ void jgroup(std::ostringstream& o, const Plan& p, const LGroup& L) {
     if (!L.ptr.empty()) { o << ",\"ptr\":"; jarr(o, L.ptr); }
     if (!L.feed_rows.empty()) { o << ",\"feed_rows\":"; jarr(o, L.feed_rows); }
     if (!L.values.empty()) { o << ",\"values\":"; jarr(o, L.values); }
-    if (L.type == OP_LIF_RATE && L.ens_type == MS_NEURON_RELU) o << ",\"neuron\":" << L.ens_type;
+    if (L.type == OP_LIF_RATE && L.ens_type != MS_NEURON_LIF_RATE) o << ",\"neuron\":" << L.ens_type;
+    if (!L.sigma.empty()) { o << ",\"sigma\":"; jarr(o, L.sigma); }
     if (!L.tau_rc.empty()) {
       o << ",\"tau_rc\":"; jarr(o, L.tau_rc);
       o << ",\"tau_ref\":"; jarr(o, L.tau_ref);

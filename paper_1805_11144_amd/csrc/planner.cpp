@@ -581,7 +581,7 @@ LGroup lower_group_at(const IR& ir, const std::vector<int64_t>& sig_offset, cons
     case OP_LIF:
     case OP_LIF_RATE: {
       std::vector<int32_t> J, s, V, R;
-      std::vector<double> trc, tref, amp;
+      std::vector<double> trc, tref, amp, sig;
       for (int32_t oi : ops) {
         const Op& o = ir.ops[oi];
         for (int32_t i = 0; i < o.src.len; ++i) {
@@ -589,9 +589,10 @@ LGroup lower_group_at(const IR& ir, const std::vector<int64_t>& sig_offset, cons
           s.push_back(row(o.dst, i));
           if (g.type == OP_LIF) { V.push_back(row(o.V, i)); R.push_back(row(o.ref, i)); }
           if (g.type == OP_LIF_RATE) g.ens_type = o.ntype;   // same in every op of the group (key)
-          trc.push_back(o.tau_rc); tref.push_back(o.tau_ref); amp.push_back(o.amp);
+          trc.push_back(o.tau_rc); tref.push_back(o.tau_ref); amp.push_back(o.amp); sig.push_back(o.sigma);
         }
       }
+      if (g.type == OP_LIF_RATE && g.ens_type == MS_NEURON_SOFTLIF_RATE) g.sigma = uniform_or_rows(sig);
       g.rows = (int64_t)J.size();
       g.src = make_operand(base(f.src), J);
       g.dst = make_operand(base(f.dst), s);

@@ -23,6 +23,7 @@
 #include "host.hpp"
 #include "kernels.hpp"
 #include "kernels_window.hpp"
+#include "kernels_train.hpp"
 
 using namespace ms;
 
@@ -87,6 +88,18 @@ struct Launch {
   const int32_t* act_row = nullptr;
   const float* coef = nullptr;
   int32_t pes_L = 0, pes_nch = 0;
+};
+
+// Backward work of one forward window phase (training, paper Sec. 3.2).
+struct TrainStep {
+  size_t phase = 0;                  // index into the window phases
+  int32_t type = 0;
+  TScatter sc{};                     // COPY / COPY_INC / ELEM_INC
+  int32_t atomic = 0;                // LOWPASS: inputs shared by several rows
+  bool dx = false, dw = false;       // DOT_INC: adjoint of the input, gradient of W
+  std::vector<Launch> dx_l;          // products on W^T, input rows disjoint within each launch
+  float* wt = nullptr;               // W^T, [nops * K][M]
+  float* gw = nullptr;               // gradient base of W
 };
 
 }  // namespace
@@ -161,6 +174,17 @@ struct ms_sim {
   std::vector<std::pair<int32_t, int64_t>> init_sigs;   // (signal, offset in init_vals)
   float* pes_part = nullptr;         // partial decodes of the learned-decoder launches
   size_t pes_part_n = 0, pes_part_cap = 0;
+  // training (window driver)
+  bool train_ready = false;
+  std::vector<TrainStep> tsteps;     // backward order
+  std::vector<int32_t> trained;      // trained parameter signals
+  float* ga = nullptr;               // adjoints, laid out like va
+  size_t ga_n = 0;
+  std::vector<float*> gbase;         // per base: parameter gradients (null: nothing trained there)
+  float* loss_part = nullptr;        // per-workgroup sums of squared differences
+  size_t loss_part_n = 0;
+  float* tgt_buf = nullptr;          // a target uploaded from the host
+  size_t tgt_n = 0;
 };
 
 namespace {
@@ -218,6 +242,8 @@ void free_sim(ms_sim* s) {
   f(s->va); f(s->pa);
   f(s->pes_part);
   f(s->init_vals);
+  f(s->ga); f(s->loss_part); f(s->tgt_buf);
+  for (float* g : s->gbase) f(g);
   for (void* p : s->extra_allocs) f(p);
   if (s->ev0) (void)hipEventDestroy(s->ev0);
   if (s->ev1) (void)hipEventDestroy(s->ev1);
@@ -260,7 +286,7 @@ void build_launches(ms_sim* s, const std::vector<LGroup>& groups, std::vector<La
   const IR& ir = p.ir;
   // ---- lowered groups -> pools
   PoolBuilder pb;
-  struct Offs { int64_t dst, src, a, V, ref, ptr, values, w, x, d, trc, tref, amp, ca, cb, feed, full, e, act, coef; };
+  struct Offs { int64_t dst, src, a, V, ref, ptr, values, w, x, d, trc, tref, amp, ca, cb, feed, full, e, act, coef, sig; };
   std::vector<Offs> offs;
   for (const LGroup& g : groups) {
     Offs o{};
@@ -279,6 +305,7 @@ void build_launches(ms_sim* s, const std::vector<LGroup>& groups, std::vector<La
       o.full = pb.add_f(full);
     }
     o.tref = per_row_params && g.tau_ref.size() > 1 ? pb.add_f(g.tau_ref) : -1;
+    o.sig = g.sigma.size() > 1 ? pb.add_f(g.sigma) : -1;
     o.amp = per_row_params && g.amp.size() > 1 ? pb.add_f(g.amp) : -1;
     o.ca = g.ca.size() > 1 ? pb.add_f(g.ca) : -1;
     o.cb = g.cb.size() > 1 ? pb.add_f(g.cb) : -1;
@@ -380,6 +407,8 @@ void build_launches(ms_sim* s, const std::vector<LGroup>& groups, std::vector<La
       l.np.tau_rc_r = fp(o.trc); l.np.tau_ref_r = fp(o.tref); l.np.amp_r = fp(o.amp);
       l.np.full_r = fp(o.full);
       l.np.relu = g.type == OP_LIF_RATE && g.ens_type == MS_NEURON_RELU ? 1 : 0;
+      l.np.sigma = g.sigma.empty() ? 0.0f : g.sigma[0];
+      l.np.sigma_r = fp(o.sig);
     }
     if (g.type == OP_LOWPASS) {
       l.fp.a = g.ca[0]; l.fp.b = g.cb[0];
@@ -539,6 +568,12 @@ void setup_device(ms_sim* s) {
 
 // -------------------------------------------------------------- launching
 constexpr int kBlock = 256;
+// Timing kinds beyond the operator types: the launches of a training step's
+// backward pass (weight gradients, adjoints of product inputs, the rest).
+constexpr int32_t kTimeGradW = OP_NTYPES, kTimeGradX = OP_NTYPES + 1, kTimeGradOther = OP_NTYPES + 2;
+constexpr int32_t kTimedTypes = OP_NTYPES + 3;
+static_assert(kTimeGradW == MS_OP_GRAD_WEIGHTS && kTimeGradX == MS_OP_GRAD_INPUTS &&
+                  kTimeGradOther == MS_OP_GRAD_OTHER, "timing kinds match the C ABI");
 
 inline unsigned grid_for(int64_t n) { return (unsigned)std::max<int64_t>(1, (n + kBlock - 1) / kBlock); }
 
@@ -1093,9 +1128,11 @@ inline unsigned grid_items(double n) {
   return (unsigned)std::max<int64_t>(1, ((int64_t)n + kBlock - 1) / kBlock);
 }
 
-void launch_phase(ms_sim* s, const Launch& l, int32_t T, int64_t t0, hipStream_t q) {
+// va: the versioned array the phase works on (null: the simulation's; the
+// training pass runs products on the adjoints)
+void launch_phase(ms_sim* s, const Launch& l, int32_t T, int64_t t0, hipStream_t q, float* va = nullptr) {
   if (l.rows == 0) return;
-  const WView w{s->va, s->vs, s->B, T};
+  const WView w{va ? va : s->va, s->vs, s->B, T};
   const double tb = (double)T * s->B;
   switch (l.type) {
     case OP_FEED:
@@ -1449,7 +1486,7 @@ ms_status ms_sim_set_timing(ms_sim* s, int32_t on) {
 ms_status ms_sim_kernel_time(ms_sim* s, int32_t op_type, double* ms_out, int64_t* launches_out) {
   return guarded([&] {
     if (!s || !ms_out) fail(MS_E_INVALID, "NULL argument");
-    if (op_type < 0 || op_type >= OP_NTYPES) fail(MS_E_INVALID, "unknown operator type");
+    if (op_type < 0 || op_type >= kTimedTypes) fail(MS_E_INVALID, "unknown operator type");
     if (s->driver != MS_DRIVER_WINDOW && s->driver != MS_DRIVER_STEPS)
       fail(MS_E_STATE, "per-kernel timing needs the WINDOW or STEPS driver");
     DeviceGuard dg(s->device);
@@ -1549,18 +1586,23 @@ ms_status ms_sim_probe_read_static(ms_sim* s, int32_t probe, float* out, int64_t
   });
 }
 
+// The initial state (ms_sim_reset), queued on the simulator's stream.
+static void reset_state(ms_sim* s) {
+  HIPCHECK(hipMemsetAsync(s->state, 0, std::max<size_t>(1, s->state_rows) * s->B * 4, s->stream));
+  if (s->va)   // block 0 (the carried state); the other blocks are written before they are read
+    HIPCHECK(hipMemset2DAsync(s->va, s->vs * 4, 0, (size_t)s->B * 4, std::max<int64_t>(1, s->wplan->rows_v), s->stream));
+  if (s->pa) HIPCHECK(hipMemsetAsync(s->pa, 0, (size_t)std::max<int64_t>(1, s->wplan->rows_p) * s->B * 4, s->stream));
+  HIPCHECK(hipMemsetAsync(s->ctr, 0, 2 * sizeof(int64_t), s->stream));
+  init_state(s);
+  s->steps_total = 0;
+}
+
 ms_status ms_sim_reset(ms_sim* s) {
   return guarded([&] {
     if (!s) fail(MS_E_INVALID, "NULL sim");
     DeviceGuard dg(s->device);
-    HIPCHECK(hipMemsetAsync(s->state, 0, std::max<size_t>(1, s->state_rows) * s->B * 4, s->stream));
-    if (s->va)   // block 0 (the carried state); the other blocks are written before they are read
-      HIPCHECK(hipMemset2DAsync(s->va, s->vs * 4, 0, (size_t)s->B * 4, std::max<int64_t>(1, s->wplan->rows_v), s->stream));
-    if (s->pa) HIPCHECK(hipMemsetAsync(s->pa, 0, (size_t)std::max<int64_t>(1, s->wplan->rows_p) * s->B * 4, s->stream));
-    HIPCHECK(hipMemsetAsync(s->ctr, 0, 2 * sizeof(int64_t), s->stream));
-    init_state(s);
+    reset_state(s);
     HIPCHECK(hipStreamSynchronize(s->stream));
-    s->steps_total = 0;
   });
 }
 
@@ -1651,3 +1693,5 @@ ms_status ms_sim_set_state(ms_sim* s, int32_t which, int32_t id, const float* in
 }
 
 }  // extern "C"
+
+#include "train_host.hpp"

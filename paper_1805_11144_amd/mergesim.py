@@ -14,7 +14,7 @@ LIB_PATH = os.path.join(_HERE, "libmergesim.so")
 
 MS_OK = 0
 REF_NODE, REF_ENS, REF_NEURONS, REF_LEARNING = 0, 1, 2, 3
-NEURON_LIF, NEURON_LIF_RATE, NEURON_RELU = 0, 1, 2
+NEURON_LIF, NEURON_LIF_RATE, NEURON_RELU, NEURON_SOFTLIF_RATE = 0, 1, 2, 3
 FN_IDENTITY, FN_PRODUCT = 0, 1
 PLANNER_GREEDY, PLANNER_TREE = 0, 1
 DRIVER_AUTO, DRIVER_STEPS, DRIVER_GRAPH, DRIVER_PERSISTENT, DRIVER_WINDOW = 0, 1, 2, 3, 4
@@ -27,6 +27,8 @@ PARAM_GAIN, PARAM_BIAS, PARAM_DECODERS = 0, 1, 2
  STATE_PES_ACTIVITY) = range(6)
 (OP_FEED, OP_RESET, OP_COPY, OP_COPY_INC, OP_ELEMENTWISE_INC, OP_DOT_INC, OP_LIF, OP_LIF_RATE, OP_LOWPASS,
  OP_ENSEMBLE, OP_SYNAPSE_SCATTER, OP_LEARNED_DECODE, OP_PES, OP_PES_DECODE_UPDATE) = range(14)
+OP_GRAD_WEIGHTS, OP_GRAD_INPUTS, OP_GRAD_OTHER = 14, 15, 16
+TRAIN_ENCODERS, TRAIN_BIASES, TRAIN_DECODERS, TRAIN_CONN_DECODERS, TRAIN_TRANSFORM = range(5)
 
 _dp = C.POINTER(C.c_double)
 _fp = C.POINTER(C.c_float)
@@ -38,7 +40,7 @@ class EnsembleDesc(C.Structure):
     _fields_ = [("n_neurons", _i32), ("dims", _i32), ("neuron_type", _i32),
                 ("tau_rc", C.c_double), ("tau_ref", C.c_double), ("amplitude", C.c_double),
                 ("encoders", _dp), ("max_rates", _dp), ("intercepts", _dp), ("gains", _dp),
-                ("biases", _dp), ("n_eval_points", _i32), ("eval_points", _dp)]
+                ("biases", _dp), ("n_eval_points", _i32), ("eval_points", _dp), ("sigma", C.c_double)]
 
 
 class ConnectionDesc(C.Structure):
@@ -64,6 +66,10 @@ class SimOpts(C.Structure):
 
 class Feed(C.Structure):
     _fields_ = [("node_id", _i32), ("on_device", _i32), ("data", _fp)]
+
+
+class Target(C.Structure):
+    _fields_ = [("probe_id", _i32), ("on_device", _i32), ("data", _fp)]
 
 
 class MergesimError(RuntimeError):
@@ -104,6 +110,10 @@ _SIGNATURES = [
     ("ms_sim_set_timing", [C.c_void_p, _i32], _i32),
     ("ms_sim_kernel_time", [C.c_void_p, _i32, C.POINTER(C.c_double), C.POINTER(_i64)], _i32),
     ("ms_sim_info", [C.c_void_p, C.POINTER(_i32), C.POINTER(_i32)], _i32),
+    ("ms_sim_train_step", [C.c_void_p, _i64, C.POINTER(Feed), _i32, C.POINTER(Target), _i32, C.c_double,
+                           _dp], _i32),
+    ("ms_sim_train_param", [C.c_void_p, _i32, _i32, _i32, _i32, _fp, _i64, C.POINTER(_i64)], _i32),
+    ("ms_sim_set_train_param", [C.c_void_p, _i32, _i32, _i32, _fp, _i64], _i32),
     ("ms_last_error", [], C.c_char_p),
 ]
 
@@ -176,7 +186,9 @@ class Model:
             return _dptr(a)
         d = EnsembleDesc()
         d.n_neurons, d.dims = int(ens.n_neurons), int(ens.dims)
-        d.neuron_type = {"lif": NEURON_LIF, "lif_rate": NEURON_LIF_RATE, "relu": NEURON_RELU}[ens.neuron_type]
+        d.neuron_type = {"lif": NEURON_LIF, "lif_rate": NEURON_LIF_RATE, "relu": NEURON_RELU,
+                         "softlif_rate": NEURON_SOFTLIF_RATE}[ens.neuron_type]
+        d.sigma = float(getattr(ens, "sigma", 0.0))
         d.tau_rc, d.tau_ref, d.amplitude = float(ens.tau_rc), float(ens.tau_ref), float(ens.amplitude)
         d.encoders = arr(ens.encoders)
         if ens.gains is not None:
@@ -341,14 +353,14 @@ class Simulator:
     def __exit__(self, *exc):
         self.close()
 
-    def run_steps(self, n_steps: int, feeds: Optional[Dict[int, object]] = None):
-        """Advance n_steps.  feeds: node id -> float32 [B, n_steps, size]
-        (numpy array, or a torch tensor on the simulator's device)."""
-        feeds = feeds or {}
-        arr = (Feed * max(1, len(feeds)))()
+    def _arrays(self, n_steps, items, Struct, key, what):
+        """ctypes array of Struct (Feed or Target) for {id: [B, n_steps, w]}
+        data (numpy, or torch tensors on the simulator's device), and the
+        objects that keep the data alive."""
+        arr = (Struct * max(1, len(items)))()
         keep = []
-        for i, (node, data) in enumerate(feeds.items()):
-            arr[i].node_id = int(node)
+        for i, (ident, data) in enumerate(items.items()):
+            setattr(arr[i], key, int(ident))
             if hasattr(data, "is_cuda") and data.is_cuda:
                 t = data.contiguous()
                 keep.append(t)
@@ -356,13 +368,54 @@ class Simulator:
                 arr[i].data = C.cast(C.c_void_p(t.data_ptr()), _fp)
             else:
                 a = np.ascontiguousarray(np.asarray(data, dtype=np.float32))
-                if a.shape[0] != self.minibatch or a.shape[1] < n_steps:
-                    raise ValueError(f"feed for node {node} has shape {a.shape}")
+                if a.ndim != 3 or a.shape[0] != self.minibatch or a.shape[1] < n_steps:
+                    raise ValueError(f"{what} for {ident} has shape {a.shape}")
                 a = np.ascontiguousarray(a[:, :n_steps])
                 keep.append(a)
                 arr[i].on_device = 0
                 arr[i].data = a.ctypes.data_as(_fp)
+        return arr, keep
+
+    def run_steps(self, n_steps: int, feeds: Optional[Dict[int, object]] = None):
+        """Advance n_steps.  feeds: node id -> float32 [B, n_steps, size]
+        (numpy array, or a torch tensor on the simulator's device)."""
+        feeds = feeds or {}
+        arr, keep = self._arrays(n_steps, feeds, Feed, "node_id", "feed")
         _check(self._lib.ms_sim_run_steps(self.handle, int(n_steps), arr, len(feeds)))
+        del keep
+
+    def train_step(self, n_steps: int, feeds: Optional[Dict[int, object]], targets: Dict[int, object],
+                   learning_rate: float = 0.0) -> float:
+        """One training step (ms_sim_train_step, paper Sec. 3.2): a run of
+        n_steps from the initial state, the mean-squared-error objective of
+        the probes in `targets` (probe id -> [B, n_steps, width]), its
+        gradient through the run, and p <- p - learning_rate * dL/dp.
+        Returns the objective.  Needs driver=DRIVER_WINDOW, fuse=False,
+        simplify=False and rate neurons."""
+        feeds = feeds or {}
+        farr, fkeep = self._arrays(n_steps, feeds, Feed, "node_id", "feed")
+        tarr, tkeep = self._arrays(n_steps, targets, Target, "probe_id", "target")
+        loss = C.c_double()
+        _check(self._lib.ms_sim_train_step(self.handle, int(n_steps), farr, len(feeds), tarr, len(targets),
+                                           float(learning_rate), C.byref(loss)))
+        del fkeep, tkeep
+        return loss.value
+
+    def train_param(self, which: int, ident: int, function: int = FN_IDENTITY, gradient: bool = False):
+        """A trained parameter (TRAIN_*) or its gradient from the last
+        train_step, float32, flat in the layout of ms_sim_train_param."""
+        n = _i64()
+        _check(self._lib.ms_sim_train_param(self.handle, which, ident, function, int(bool(gradient)), None, 0,
+                                            C.byref(n)))
+        out = np.empty(n.value, np.float32)
+        _check(self._lib.ms_sim_train_param(self.handle, which, ident, function, int(bool(gradient)),
+                                            out.ctypes.data_as(_fp), n.value, C.byref(n)))
+        return out
+
+    def set_train_param(self, which: int, ident: int, values, function: int = FN_IDENTITY) -> None:
+        a = np.ascontiguousarray(np.asarray(values, np.float32).ravel())
+        _check(self._lib.ms_sim_set_train_param(self.handle, which, ident, function, a.ctypes.data_as(_fp),
+                                                a.size))
 
     def sync(self):
         _check(self._lib.ms_sim_sync(self.handle))

@@ -352,14 +352,19 @@ def make_pes(neuron_type="lif", n_steps=1000, minibatch=10, D=192, neurons_per_d
 
 
 # ------------------------------------------------------------------------ training
-def make_train(kind="mlp", neuron_type="lif_rate", seed=7, **overrides):
+def make_train(kind="mlp", neuron_type="softlif_rate", seed=7, **overrides):
     """A rate-neuron model to train by gradient descent (paper Sec. 3.2) and
     seeded targets for some of its probes: (Workload, {probe: [B, T, w]}).
 
+    Rate neurons: the smoothed LIF rate by default (the differentiable
+    stand-in of a spiking LIF model; smoothing sigma 0.02 from Ensemble).
+
     kind "mlp": the spiking-classifier shape (784-1024-1024-10, filtered
-      hidden connections, 50 steps, minibatch 256) with rate neurons; each
-      batch row's target on the readout probe is a one-hot class vector drawn
-      from the seed, at every step.
+      hidden connections, 50 steps, minibatch 256) with rate neurons of one
+      maximum rate (100 Hz) and intercept (0), the usual set-up of a
+      classifier to be trained (every neuron gets the same moderate gain);
+      each batch row's target on the readout probe is a one-hot class vector
+      drawn from the seed, at every step.
     kind "chain": the ensemble-array shape (a chain of d-dimensional
       ensembles with orthogonal transforms and lowpass synapses); targets on
       the filtered decoded output: the input vector rotated by a seeded
@@ -369,6 +374,9 @@ def make_train(kind="mlp", neuron_type="lif_rate", seed=7, **overrides):
       node: seeded values of magnitude 0.1."""
     if kind == "mlp":
         w = make_c3(neuron_type=neuron_type, **overrides)
+        for e in w.spec.ensembles:
+            e.max_rates = np.full(e.n_neurons, 100.0)
+            e.intercepts = np.zeros(e.n_neurons)
         rng = _rng(seed, 1)
         n_out = w.spec.nodes[1].size
         cls = rng.integers(0, n_out, size=w.minibatch)

@@ -31,10 +31,11 @@ class Ensemble:
     intercepts: Optional[np.ndarray] = None  # [n]
     gains: Optional[np.ndarray] = None       # [n]; overrides max_rates/intercepts
     biases: Optional[np.ndarray] = None      # [n]
-    neuron_type: str = "lif"             # "lif" (spiking) | "lif_rate" | "relu"
+    neuron_type: str = "lif"             # "lif" (spiking) | "lif_rate" | "softlif_rate" | "relu"
     tau_rc: float = 0.02
     tau_ref: float = 0.002
     amplitude: float = 1.0
+    sigma: float = 0.02                  # smoothing of the "softlif_rate" curve (ignored otherwise)
 
 
 @dataclass

@@ -8,6 +8,8 @@ lowering do not change the model's output (paper Sec. 4.2), without a GPU.
 """
 import numpy as np
 
+from oracle.neurons import soft_lif_rate
+
 
 def _rows(op, n):
     if op is None:
@@ -130,6 +132,10 @@ class PlanExecutor:
                         cols[k].append(np.full(e.n_neurons, getattr(e, "amplitude" if k == "amp" else k)))
                 for k in cols:
                     g[k] = np.concatenate(cols[k]).tolist()
+                if "sigma" in g:
+                    g["sigma"] = np.concatenate([np.full(e.n_neurons, e.sigma) for e in
+                                                 (self.spec.ensembles[int(name.split(".")[0][1:])]
+                                                  for name in g["ops"])]).tolist()
             elif g["type"] == "Ensemble":
                 ens = [self.spec.ensembles[int(name.split(".")[0][1:])] for name in g["ops"]]
                 g["tau_rc"] = [e.tau_rc for e in ens]
@@ -226,7 +232,12 @@ class PlanExecutor:
             tref = _vec(g["tau_ref"], n)[:, None]
             amp = _vec(g["amp"], n)[:, None]
             if t == "SimLIFRate":
-                out = amp * np.maximum(J, 0.0) if g.get("neuron") == 2 else _rate(J, trc, tref, amp)
+                if g.get("neuron") == 2:
+                    out = amp * np.maximum(J, 0.0)
+                elif g.get("neuron") == 3:
+                    out = amp * soft_lif_rate(J, trc, tref, _vec(g["sigma"], n)[:, None])
+                else:
+                    out = _rate(J, trc, tref, amp)
             else:
                 vr, rr = _rows(g["V"], n), _rows(g["ref"], n)
                 out, pa[vr], pa[rr] = _lif(J, pa[vr].copy(), pa[rr].copy(), self.dt, trc, tref, amp)

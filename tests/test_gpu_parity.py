@@ -76,6 +76,21 @@ def test_relu_parity(name, driver, fuse):
 
 @pytest.mark.parametrize("driver", list(DRIVERS))
 @pytest.mark.parametrize("name", list(SMALL))
+def test_soft_lif_rate_parity(name, driver):
+    """Soft LIF rate neurons (always the unfused rate operator) on every
+    driver: the rate-mode bound, 1e-5 of each probe's peak."""
+    skip_unsupported(name, driver)
+    w = make_workload(name, neuron_type="softlif_rate", **SMALL[name])
+    got = run_gpu(w, driver=DRIVERS[driver], unroll=7)
+    exp = run_oracle(w)
+    for pi, (g, e) in enumerate(zip(got, exp)):
+        r = rel_err(g, e)
+        print(f"{name} {driver} probe {pi}: rel {r:.2e}")
+        assert r <= 1e-5, (name, driver, pi, r)
+
+
+@pytest.mark.parametrize("driver", list(DRIVERS))
+@pytest.mark.parametrize("name", list(SMALL))
 def test_spiking_mode_parity(name, driver):
     """Whole runs of the small models: spike flips and every decoded or
     filtered probe held to the benchmark spec bounds (1e-4 of the spikes, 1e-3

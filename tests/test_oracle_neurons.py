@@ -97,6 +97,39 @@ def test_gain_bias_invariants():
     assert np.all(g > 0)
 
 
+def test_soft_lif_rate_closed_forms():
+    """Soft LIF rate: at J = 1, rho = sigma ln 2 exactly, so r = 1/(tau_ref +
+    tau_rc ln(1 + 1/(sigma ln 2))); where J - 1 >> sigma, rho = J - 1 (to
+    exp(-(J-1)/sigma)) and the curve is the LIF rate; as sigma -> 0 it tends
+    to the LIF rate everywhere off threshold; far below threshold rho = sigma
+    exp((J-1)/sigma) (relative error exp((J-1)/sigma)), so r = 1/(tau_ref +
+    tau_rc ((1-J)/sigma - ln sigma)) up to that error; always positive and
+    increasing."""
+    from oracle.neurons import lif_rate, rate_output, soft_lif_rate
+    trc, tref = 0.02, 0.002
+    for s in (0.005, 0.02, 0.3):
+        exp = 1.0 / (tref + trc * np.log1p(1.0 / (s * np.log(2.0))))
+        assert soft_lif_rate(np.array([1.0]), trc, tref, s)[0] == pytest.approx(exp, rel=1e-13)
+    J = 1.0 + np.array([0.8, 1.5, 4.0, 40.0])
+    np.testing.assert_allclose(soft_lif_rate(J, trc, tref, 0.01), lif_rate(J, trc, tref), rtol=1e-13)
+    Jo = np.array([0.2, 0.9, 1.05, 1.3, 3.0])
+    prev = None
+    for s in (1e-2, 1e-3, 1e-4):
+        d = np.abs(soft_lif_rate(Jo, trc, tref, s) - lif_rate(Jo, trc, tref)).max()
+        assert prev is None or d < prev
+        prev = d
+    assert prev < 0.06   # Hz, against rates of tens of Hz (the tail below threshold shrinks like sigma)
+    far = np.array([-3.0, -0.5, 0.5])
+    s = 0.01
+    np.testing.assert_allclose(soft_lif_rate(far, trc, tref, s),
+                               1.0 / (tref + trc * ((1.0 - far) / s - np.log(s))), rtol=1e-12)
+    grid = np.linspace(-5, 5, 2001)
+    r = soft_lif_rate(grid, trc, tref, 0.02)
+    assert np.all(r > 0) and np.all(np.diff(r) > 0)
+    np.testing.assert_array_equal(rate_output("softlif_rate", J, trc, tref, 0.5, 0.01),
+                                  0.5 * soft_lif_rate(J, trc, tref, 0.01))
+
+
 def test_relu_rate_and_gain_bias():
     """Rectified-linear neuron: r(J) = max(J, 0); gain and bias put J = 0 at the
     intercept and J = max_rate at x = 1.  Hand values: max_rate 200 Hz at

@@ -29,10 +29,18 @@ SHAPES = {
 
 
 def _small(kind, neuron_type):
-    return make_train(kind, neuron_type=neuron_type, **SHAPES[kind])
+    """A small training model; intercepts drawn from [-0.9, 0.9] so that no
+    current sits exactly on a kink of the rate curves (the classifier's
+    default intercept 0 with zero filter states puts ReLU currents at exactly
+    0, where a central difference straddles the kink)."""
+    w, targets = make_train(kind, neuron_type=neuron_type, **SHAPES[kind])
+    rng = np.random.default_rng(5)
+    for e in w.spec.ensembles:
+        e.intercepts = rng.uniform(-0.9, 0.9, e.n_neurons)
+    return w, targets
 
 
-@pytest.mark.parametrize("neuron_type", ["lif_rate", "relu"])
+@pytest.mark.parametrize("neuron_type", ["lif_rate", "softlif_rate", "relu"])
 @pytest.mark.parametrize("kind", list(SHAPES))
 def test_forward_equals_oracle_sim(kind, neuron_type):
     w, targets = _small(kind, neuron_type)
@@ -52,9 +60,6 @@ def _fd_check(w, targets, tr, per_tensor=5, seed=0, h_rel=1e-6):
     """Central differences of objective_numpy at a few entries of every
     trained tensor against the oracle's gradient."""
     loss, grads, _ = tr.loss_and_grads(w.n_steps, w.feeds, targets)
-    # rounding of the two objective values limits a central difference to
-    # about eps |L| / h (h >= 1e-6): 1e-8 |L| covers it
-    noise = 1e-8 * abs(loss)
     rng = np.random.default_rng(seed)
     checked = 0
     for key, val in tr.params.items():
@@ -64,8 +69,13 @@ def _fd_check(w, targets, tr, per_tensor=5, seed=0, h_rel=1e-6):
         picks = rng.choice(flat, size=min(per_tensor, val.size), replace=False)
         # the largest entry too, so that every tensor is checked where it matters
         picks = np.unique(np.append(picks, np.argmax(np.abs(g).ravel())))
+        # steps relative to the tensor's size (decoders are ~1e-3), so that
+        # the truncation error (h^2 times the third derivative) stays small
+        size = max(np.abs(val).max(), 1e-6)
         for i in picks:
-            h = h_rel * max(1.0, abs(val.flat[i]))
+            h = h_rel * size
+            # rounding of the two objective values: about eps |L| / h
+            noise = 1e-15 * abs(loss) / h
             P = {k: v.copy() for k, v in tr.params.items()}
             P[key].flat[i] = val.flat[i] + h
             lp = objective_numpy(w.spec, w.minibatch, w.n_steps, w.feeds, targets, P)
@@ -77,7 +87,7 @@ def _fd_check(w, targets, tr, per_tensor=5, seed=0, h_rel=1e-6):
     return checked
 
 
-@pytest.mark.parametrize("neuron_type", ["lif_rate", "relu"])
+@pytest.mark.parametrize("neuron_type", ["lif_rate", "softlif_rate", "relu"])
 @pytest.mark.parametrize("kind", list(SHAPES))
 def test_gradients_equal_finite_differences(kind, neuron_type):
     w, targets = _small(kind, neuron_type)
@@ -123,6 +133,26 @@ def test_one_relu_neuron_by_hand():
     assert g[("enc", 0)][0, 0] == pytest.approx(0.56, rel=1e-12)
     assert g[("T", 1)][0] == pytest.approx(1.75 * 0.8 / 1.0, rel=1e-12)   # p = T d s: dL/dT = 2 (p - t) d s
     assert g[("T", 0)][0] == pytest.approx(1.12, rel=1e-12)   # x = T u: dL/dT = dL/dJ e u = 1.12 * 2 * 0.5
+
+
+def test_relu_derivative_at_zero_current_is_zero():
+    """The reading at the kink: a ReLU neuron whose current is exactly 0
+    (zero bias, zero input) passes no gradient to its bias, while one step
+    later with current 0.5 it passes d (p - t) * 2 / T (T = 2 steps)."""
+    m = ModelSpec(dt=0.001)
+    inp = m.add_node(Node(size=1))
+    e = m.add_ensemble(Ensemble(n_neurons=1, dims=1, encoders=np.ones((1, 1)), eval_points=np.zeros((1, 1)),
+                                gains=np.array([1.0]), biases=np.array([0.0]), neuron_type="relu"))
+    out = m.add_node(Node(size=1, passthrough=True))
+    m.connect(Connection(pre=inp, post=("ens", e)))
+    m.connect(Connection(pre=("ens", e), post=out, decoders=np.array([[0.8]])))
+    m.probe(Probe(target=out))
+    tr = TrainOracle(m, minibatch=1, param_dtype=np.float64)
+    feed = np.array([[[0.0], [0.5]]])   # J = 0, then J = 0.5
+    _, g, probes = tr.loss_and_grads(2, {0: feed}, {0: np.full((1, 2, 1), 0.3)})
+    assert probes[0][0, :, 0] == pytest.approx([0.0, 0.4], abs=1e-15)
+    # only step 1 contributes: dL/db = (2/2) (0.4 - 0.3) * 0.8
+    assert g[("bias", 0)][0] == pytest.approx(0.08, rel=1e-12)
 
 
 def test_filtered_scalar_connection_by_hand():

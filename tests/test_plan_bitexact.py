@@ -1,6 +1,7 @@
 """The library's C++ planner against the independent reference planner: the
 exported plans (signal layout, merged groups, operator order, index arrays)
 must be identical."""
+import numpy as np
 import pytest
 
 import paper_1805_11144_amd as M
@@ -16,7 +17,7 @@ CASES = {
     "bg": dict(n_steps=2, D=5, n_neurons=20, n_eval=40),
     "pes": dict(n_steps=2, minibatch=2, D=6, neurons_per_dim=5),
 }
-FLOAT_KEYS = {"values", "tau_rc", "tau_ref", "amp", "ca", "cb", "coef"}
+FLOAT_KEYS = {"values", "tau_rc", "tau_ref", "amp", "ca", "cb", "coef", "sigma"}
 
 
 def _strip(plan):
@@ -74,3 +75,20 @@ def test_relu_plans_identical(name, opt):
     assert got == {**exp, "groups": exp["groups"]}
     kinds = [g.get("neuron") for g in got["groups"] if g["type"] in ("SimLIFRate", "Ensemble")]
     assert kinds and all(k == 2 for k in kinds)
+
+
+@pytest.mark.parametrize("opt", ["tree3", "nofuse", "nomerge"])
+@pytest.mark.parametrize("name", ["c2", "c4", "c5"])
+def test_soft_lif_rate_plans_identical(name, opt):
+    """Soft LIF rate ensembles: never fused, their rate operators keyed and
+    exported with the neuron type (the smoothing travels per row)."""
+    w = make_workload(name, neuron_type="softlif_rate", **CASES[name])
+    lib_opts, ref_opts = OPTS[opt]
+    full = M.Plan(M.model_from_spec(w.spec), **lib_opts).json()
+    got = _strip(full)
+    exp = P.make_plan(w.spec, **ref_opts)
+    assert got == {**exp, "groups": exp["groups"]}
+    assert not [g for g in got["groups"] if g["type"] == "Ensemble"]
+    rate = [g for g in full["groups"] if g["type"] == "SimLIFRate"]
+    assert rate and all(g["neuron"] == 3 for g in rate)
+    assert all(np.allclose(g["sigma"], w.spec.ensembles[0].sigma) for g in rate)

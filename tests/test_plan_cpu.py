@@ -20,7 +20,7 @@ SMALL = {
 }
 
 
-@pytest.mark.parametrize("neuron_type", ["lif", "relu"])
+@pytest.mark.parametrize("neuron_type", ["lif", "relu", "softlif_rate"])
 @pytest.mark.parametrize("name", ["c1", "c2", "c4", "c5", "bg"])
 def test_build_params_match_oracle(name, neuron_type):
     w = make_workload(name, neuron_type=neuron_type, **SMALL[name])
@@ -36,7 +36,7 @@ def test_build_params_match_oracle(name, neuron_type):
 
 
 @pytest.mark.parametrize("name", list(SMALL))
-@pytest.mark.parametrize("neuron_type", ["lif_rate", "lif", "relu"])
+@pytest.mark.parametrize("neuron_type", ["lif_rate", "lif", "relu", "softlif_rate"])
 @pytest.mark.parametrize("opts", [dict(), dict(planner=M.PLANNER_GREEDY), dict(sort=False),
                                   dict(simplify=False), dict(merge=False), dict(fuse=False)])
 def test_plan_execution_matches_oracle(name, neuron_type, opts):
