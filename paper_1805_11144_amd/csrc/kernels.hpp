@@ -44,28 +44,42 @@ struct NeuronParams {
   const float* sigma_r;                           // per-row smoothing or null
 };
 
+// log(1 + y) for y >= 0 from the hardware log2 (v_log_f32, about 1 ulp):
+// with u = 1 + y rounded, log(u) * y / (u - 1) cancels the rounding of u
+// (Kahan's method; a few ulp), and y itself where u rounds to 1.
+__device__ __forceinline__ float log1p_hw(float y) {
+  const float u = 1.0f + y;
+  if (u == 1.0f) return y;
+  return __builtin_amdgcn_logf(u) * 0.69314718055994531f * (y / (u - 1.0f));
+}
+
 // Soft LIF rate curve r(J) (without amplitude): the LIF rate with max(J - 1, 0)
 // replaced by rho = s log(1 + exp(x)), x = (J - 1) / s.  For x >= -15,
 // log(1 + 1/rho) is evaluated directly from rho = s softplus(x); below, where
 // softplus(x) = exp(x) to a relative exp(x) / 2 < 2e-7, as log1p(rho) -
 // log(rho) with log(rho) = log(s) + x, so nothing overflows or underflows.
+// exp(x) comes from the hardware exp2 (v_exp_f32) of x log2(e), whose rounding
+// adds a relative |x| 2^-24 (at most 1e-6 here); reciprocals from v_rcp_f32.
 // Also returns rho'/rho and rho for the derivative.
 __device__ __forceinline__ float soft_lif_rate(float j, float tau_rc, float tau_ref, float s, float* dlog,
                                                float* rho_out) {
-  const float x = (j - 1.0f) / s;
+  constexpr float kLog2e = 1.44269504088896341f;
+  const float inv_s = __builtin_amdgcn_rcpf(s);
+  const float x = (j - 1.0f) * inv_s;
   float q, rho;
   if (x < -15.0f) {
-    rho = s * expf(x);
-    q = log1pf(rho) - (logf(s) + x);
-    *dlog = 1.0f / s;   // sigmoid(x) / (s softplus(x)) = 1 / s to 2e-7
+    rho = s * __builtin_amdgcn_exp2f(x * kLog2e);
+    q = log1p_hw(rho) - (__builtin_amdgcn_logf(s) * 0.69314718055994531f + x);
+    *dlog = inv_s;   // sigmoid(x) / (s softplus(x)) = 1 / s to 2e-7
   } else {
-    const float sp = x > 15.0f ? x + log1pf(expf(-x)) : log1pf(expf(x));
+    const float e = __builtin_amdgcn_exp2f(x * kLog2e);
+    const float sp = x > 15.0f ? x + __builtin_amdgcn_exp2f(-x * kLog2e) : log1p_hw(e);
     rho = s * sp;
-    q = log1pf(1.0f / rho);
-    *dlog = 1.0f / ((1.0f + expf(-x)) * rho);
+    q = log1p_hw(__builtin_amdgcn_rcpf(rho));
+    *dlog = x > 15.0f ? __builtin_amdgcn_rcpf(rho) : e * __builtin_amdgcn_rcpf((1.0f + e) * rho);
   }
   *rho_out = rho;
-  return 1.0f / (tau_ref + tau_rc * q);
+  return __builtin_amdgcn_rcpf(tau_ref + tau_rc * q);
 }
 
 struct FilterParams {

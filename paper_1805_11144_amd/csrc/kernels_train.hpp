@@ -278,6 +278,48 @@ __global__ void __launch_bounds__(256, 2) k_t_dw(WView w, const float* ga, int32
       }
 }
 
+// Weight gradients of skinny blocks, one side (M or K) at most kSkM: each
+// wavefront takes one row of the long side and cchunk columns; its lanes walk
+// the columns (coalesced), each keeping partial sums against every row of the
+// short side (those rows are shared by all wavefronts and stay in cache); the
+// wavefront then sums each partial over its lanes and adds it atomically.
+// long_m != 0: the long side is M (rows of the output adjoint).
+__global__ void __launch_bounds__(256) k_t_dw_skinny(WView w, const float* ga, int32_t M, int32_t K, int64_t nwaves,
+                                                     int32_t nch, int64_t cchunk, float* gW, const int32_t* w_row,
+                                                     const int32_t* x_row, const int32_t* d_row, int xblk,
+                                                     int long_m) {
+  const int64_t wv = (int64_t)blockIdx.x * 4 + threadIdx.x / 64;
+  const int lane = threadIdx.x % 64;
+  if (wv >= nwaves) return;   // whole wavefronts leave together
+  const int32_t L = long_m ? M : K, S = long_m ? K : M;
+  const int64_t ch = wv % nch, rest = wv / nch;
+  const int64_t l = rest % L, op = rest / L;
+  const int64_t N = (int64_t)w.T * w.B;
+  const int64_t c0 = ch * cchunk, c1 = min(N, c0 + cchunk);
+  const float* Y = ga + (int64_t)G(d_row)[op] * w.vs + w.B;
+  const float* X = w.va + (int64_t)G(x_row)[op] * w.vs + (int64_t)xblk * w.B;
+  const float* lrow = long_m ? Y + l * w.vs : X + l * w.vs;
+  const float* srow = long_m ? X : Y;
+  float acc[kSkM];
+#pragma unroll
+  for (int s = 0; s < kSkM; ++s) acc[s] = 0.0f;
+  for (int64_t c = c0 + lane; c < c1; c += 64) {
+    const float lv = lrow[c];
+#pragma unroll
+    for (int s = 0; s < kSkM; ++s)
+      if (s < S) acc[s] = fmaf(lv, srow[(int64_t)s * w.vs + c], acc[s]);
+  }
+  float* dW = gW + (int64_t)G(w_row)[op] * K;
+#pragma unroll
+  for (int s = 0; s < kSkM; ++s) {
+    if (s >= S) break;
+    float v = acc[s];
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
+    if (lane == 0) atomicAdd(&dW[long_m ? l * K + s : (int64_t)s * K + l], v);
+  }
+}
+
 // The same gradients for small blocks (M or K below a tile, or B % 4 != 0):
 // one work item per (op, m, k) and column chunk blockIdx.y of cchunk columns.
 __global__ void k_t_dw_small(WView w, const float* ga, int32_t M, int32_t K, int64_t nout, int64_t cchunk, float* gW,

@@ -252,6 +252,18 @@ void run_backward(ms_sim* s, int32_t T) {
             hipLaunchKernelGGL(k_t_dw, dim3((unsigned)(8 * ((total + 7) / 8))), dim3(256), 0, q, w,
                                (const float*)s->ga, l.M, l.K, mt, kt, (int32_t)nops, (int32_t)nsplit, cchunk,
                                st.gw, l.w_row, l.x_row, l.d_row, l.src_blk);
+          } else if (std::min(l.M, l.K) <= kSkM) {
+            const bool long_m = l.K <= kSkM && l.M > l.K;
+            const int64_t L = long_m ? l.M : l.K;
+            // column chunks: about 32 waves per CU over all (op, long row, chunk)
+            const int64_t want = std::max<int64_t>(1, (32 * (int64_t)s->n_cu + nops * L - 1) / (nops * L));
+            const int64_t nch = std::max<int64_t>(1, std::min<int64_t>(want, ((int64_t)tb + 255) / 256));
+            const int64_t cchunk = ((int64_t)tb + nch - 1) / nch;
+            const int64_t nwaves = nops * L * nch;
+            if ((nwaves + 3) / 4 >= 2147483647LL) fail(MS_E_INVALID, "weight gradient grid too large");
+            hipLaunchKernelGGL(k_t_dw_skinny, dim3((unsigned)((nwaves + 3) / 4)), dim3(256), 0, q, w,
+                               (const float*)s->ga, l.M, l.K, nwaves, (int32_t)nch, cchunk, st.gw, l.w_row, l.x_row,
+                               l.d_row, l.src_blk, long_m ? 1 : 0);
           } else {
             const int64_t nout = nops * l.M * l.K;
             const int64_t cchunk = 256;
