@@ -247,31 +247,37 @@ def train_cpu_baseline(w, targets, budget_s=12.0):
 
 def train_roofline(M, sim, w, feeds, targets, plan_json):
     """Roofline of the largest operator kind of a training step, from HIP
-    events with per-launch timing on (one extra step): the weight-gradient
-    products (2 M K flops per op, step and batch row) against the fp32
-    MFMA peak when they dominate."""
+    events with per-launch timing on (one extra step), and beside it the
+    weight-gradient products on the matrix cores (k_t_dw).  Products: 2 M K
+    flops per op, step and batch row, against the fp32 MFMA peak."""
+    MS = M.mergesim
     sim.set_timing(True)
     sim.train_step(w.n_steps, feeds, targets, TRAIN_LR)
-    times = {t: sim.kernel_time(t) for t in range(17)}
+    times = {t: sim.kernel_time(t) for t in range(18)}
     sim.set_timing(False)
-    top = max(times, key=lambda t: times[t][0])
-    ms, n = times[top]
     TB = w.n_steps * w.minibatch
     dots = [g for g in plan_json["groups"] if g["type"] == "DotInc"]
-    if top == M.mergesim.OP_GRAD_WEIGHTS:
-        work, kernel, op = sum(2 * g["M"] * g["K"] * len(g["w_row"]) for g in dots) * TB, "k_t_dw", "weight gradients"
-    elif top == M.mergesim.OP_DOT_INC:
-        work, kernel, op = sum(2 * g["M"] * g["K"] * len(g["w_row"]) for g in dots) * TB, "k_w_gemm2", "DotInc"
-    else:
-        return {"bound": None, "achieved": None, "peak": None, "unit": None, "frac": None, "traffic": None,
-                "kernel": f"timing kind {top}", "launch_ms": round(ms / max(n, 1), 4), "launches": n,
-                "busy_ms": round(ms, 4), "kinds_ms": {str(t): round(v[0], 4) for t, v in times.items() if v[1]}}
-    ach = work / (ms * 1e-3) / 1e12
-    return {"bound": "mfma", "achieved": round(ach, 3), "peak": FP32_MFMA_PEAK_TFLOPS, "unit": "TFLOP/s",
-            "frac": round(ach / FP32_MFMA_PEAK_TFLOPS, 4), "traffic": stored_traffic(kernel, "train"),
-            "basis": "algorithmic", "kernel": kernel, "op": op, "launch_ms": round(ms / max(n, 1), 4),
-            "launches": n, "busy_ms": round(ms, 4), "work_per_launch": int(work / max(n, 1)),
-            "kinds_ms": {str(t): round(v[0], 4) for t, v in times.items() if v[1]}}
+    flops = lambda gs: sum(2 * g["M"] * g["K"] * len(g["w_row"]) for g in gs) * TB
+    big = [g for g in dots if g["M"] >= 64 and g["K"] >= 64 and w.minibatch % 4 == 0]
+    kinds = {MS.OP_DOT_INC: (flops(dots), "k_w_gemm2", "DotInc (forward)"),
+             MS.OP_GRAD_WEIGHTS: (flops(big), "k_t_dw", "weight gradients")}
+
+    def line(t):
+        ms, n = times[t]
+        work, kernel, op = kinds[t]
+        ach = work / (ms * 1e-3) / 1e12
+        return {"bound": "mfma", "achieved": round(ach, 3), "peak": FP32_MFMA_PEAK_TFLOPS, "unit": "TFLOP/s",
+                "frac": round(ach / FP32_MFMA_PEAK_TFLOPS, 4), "traffic": stored_traffic(kernel, "train"),
+                "basis": "algorithmic", "kernel": kernel, "op": op, "launch_ms": round(ms / max(n, 1), 4),
+                "launches": n, "busy_ms": round(ms, 4), "work_per_launch": int(work / max(n, 1))}
+    top = max(times, key=lambda t: times[t][0])
+    out = line(top) if top in kinds else {
+        "bound": None, "achieved": None, "peak": None, "unit": None, "frac": None, "traffic": None,
+        "kernel": f"timing kind {top}", "launch_ms": round(times[top][0] / max(times[top][1], 1), 4)}
+    if top != MS.OP_GRAD_WEIGHTS and times[MS.OP_GRAD_WEIGHTS][1]:
+        out["weight_gradients"] = line(MS.OP_GRAD_WEIGHTS)
+    out["kinds_ms"] = {str(t): round(v[0], 4) for t, v in times.items() if v[1]}
+    return out
 
 
 def main_train(args):

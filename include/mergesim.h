@@ -469,9 +469,11 @@ ms_status ms_sim_set_train_param(ms_sim* sim, int32_t which, int32_t id, int32_t
 /* Timing kinds of a training step's backward pass for ms_sim_kernel_time
  * (with timing on, the forward groups are timed under their MS_OP_* types as
  * in ms_sim_run_steps): */
-#define MS_OP_GRAD_WEIGHTS 14  /* weight gradients of the merged DotInc groups */
+#define MS_OP_GRAD_WEIGHTS 14  /* weight gradients of merged DotInc groups with both sides
+                                  of W at least 64 (matrix-core products) */
 #define MS_OP_GRAD_INPUTS 15   /* adjoints of the DotInc inputs (products with W^T) */
 #define MS_OP_GRAD_OTHER 16    /* objective, elementwise, neuron and filter reverses, update */
+#define MS_OP_GRAD_WEIGHTS_SMALL 17  /* weight gradients of the other DotInc groups */
 
 const char* ms_last_error(void);
 

@@ -571,9 +571,11 @@ constexpr int kBlock = 256;
 // Timing kinds beyond the operator types: the launches of a training step's
 // backward pass (weight gradients, adjoints of product inputs, the rest).
 constexpr int32_t kTimeGradW = OP_NTYPES, kTimeGradX = OP_NTYPES + 1, kTimeGradOther = OP_NTYPES + 2;
-constexpr int32_t kTimedTypes = OP_NTYPES + 3;
+constexpr int32_t kTimeGradWSmall = OP_NTYPES + 3;
+constexpr int32_t kTimedTypes = OP_NTYPES + 4;
 static_assert(kTimeGradW == MS_OP_GRAD_WEIGHTS && kTimeGradX == MS_OP_GRAD_INPUTS &&
-                  kTimeGradOther == MS_OP_GRAD_OTHER, "timing kinds match the C ABI");
+                  kTimeGradOther == MS_OP_GRAD_OTHER && kTimeGradWSmall == MS_OP_GRAD_WEIGHTS_SMALL,
+              "timing kinds match the C ABI");
 
 inline unsigned grid_for(int64_t n) { return (unsigned)std::max<int64_t>(1, (n + kBlock - 1) / kBlock); }
 

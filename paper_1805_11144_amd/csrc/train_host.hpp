@@ -239,8 +239,9 @@ void run_backward(ms_sim* s, int32_t T) {
       case OP_DOT_INC: {
         const int64_t nops = l.rows;
         if (st.dw) {
-          time_begin(s, kTimeGradW, q);
-          if (l.M >= 64 && l.K >= 64 && s->B % 4 == 0) {
+          const bool mfma = l.M >= 64 && l.K >= 64 && s->B % 4 == 0;
+          time_begin(s, mfma ? kTimeGradW : kTimeGradWSmall, q);
+          if (mfma) {
             const int32_t mt = (l.M + kDwM - 1) / kDwM, kt = (l.K + kDwK - 1) / kDwK;
             const int64_t tiles = (int64_t)mt * kt * nops;
             // column chunks: enough workgroups for two per CU twice over, chunks of at least 256 columns

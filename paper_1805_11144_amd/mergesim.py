@@ -27,7 +27,7 @@ PARAM_GAIN, PARAM_BIAS, PARAM_DECODERS = 0, 1, 2
  STATE_PES_ACTIVITY) = range(6)
 (OP_FEED, OP_RESET, OP_COPY, OP_COPY_INC, OP_ELEMENTWISE_INC, OP_DOT_INC, OP_LIF, OP_LIF_RATE, OP_LOWPASS,
  OP_ENSEMBLE, OP_SYNAPSE_SCATTER, OP_LEARNED_DECODE, OP_PES, OP_PES_DECODE_UPDATE) = range(14)
-OP_GRAD_WEIGHTS, OP_GRAD_INPUTS, OP_GRAD_OTHER = 14, 15, 16
+OP_GRAD_WEIGHTS, OP_GRAD_INPUTS, OP_GRAD_OTHER, OP_GRAD_WEIGHTS_SMALL = 14, 15, 16, 17
 TRAIN_ENCODERS, TRAIN_BIASES, TRAIN_DECODERS, TRAIN_CONN_DECODERS, TRAIN_TRANSFORM = range(5)
 
 _dp = C.POINTER(C.c_double)
