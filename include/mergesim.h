@@ -362,6 +362,17 @@ ms_status ms_sim_set_state(ms_sim* sim, int32_t which, int32_t id, const float* 
  * run, repeated and averaged). */
 ms_status ms_sim_last_run_ms(ms_sim* sim, double* ms_out);
 
+/* Failure detection for the caller's data (not a part of the paper's method):
+ * with on != 0, every later ms_sim_run_steps and ms_sim_train_step first
+ * scans each feed for NaN and Inf (host feeds on the host, device feeds with
+ * a counting kernel and a wait) and returns MS_E_NUMERIC, naming the node and
+ * the count, before anything runs.  Off by default (the scan reads every feed
+ * once more).  Setting the environment variable MS_LOG (to anything but "0")
+ * prints a summary of the plan on stderr when a simulator is created: the
+ * driver, the merged groups launched per step (per window on the window
+ * driver) with their sizes, and the bytes of state and parameters. */
+ms_status ms_sim_set_check_feeds(ms_sim* sim, int32_t on);
+
 /* The driver actually used (MS_DRIVER_STEPS/GRAPH/PERSISTENT/WINDOW) and the
  * number of merged groups executed per step (WINDOW: launches per window) --
  * the count that operator merging reduces (Sec. 4.2, Fig. 8). */

@@ -1136,6 +1136,19 @@ __global__ void k_set_ctr(int64_t* ctr, int64_t c0, int64_t c1) {
   }
 }
 
+// count of non-finite values among x[0..n) (grid-stride; one atomic per workgroup)
+__global__ void __launch_bounds__(256) k_count_nonfinite(const float* x, int64_t n, unsigned int* count) {
+  __shared__ unsigned int c;
+  if (threadIdx.x == 0) c = 0;
+  __syncthreads();
+  unsigned int mine = 0;
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (int64_t)gridDim.x * blockDim.x)
+    mine += isfinite(x[i]) ? 0u : 1u;
+  if (mine) atomicAdd(&c, mine);
+  __syncthreads();
+  if (threadIdx.x == 0 && c) atomicAdd(count, c);
+}
+
 // feed [B][T][size] -> staging [T][feed_rows][B] rows [row0, row0+size)
 #define GRID_FLAT(n)                                                        \
   const int64_t _i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;        \

@@ -14,6 +14,8 @@
 
 #include <algorithm>
 #include <cmath>
+#include <cstdio>
+#include <cstdlib>
 #include <cstring>
 #include <string>
 #include <vector>
@@ -185,6 +187,9 @@ struct ms_sim {
   size_t loss_part_n = 0;
   float* tgt_buf = nullptr;          // a target uploaded from the host
   size_t tgt_n = 0;
+  // failure detection
+  bool check_feeds = false;          // scan every feed for NaN / Inf before a run
+  unsigned int* nonfinite = nullptr; // device count of non-finite feed values
 };
 
 namespace {
@@ -242,7 +247,7 @@ void free_sim(ms_sim* s) {
   f(s->va); f(s->pa);
   f(s->pes_part);
   f(s->init_vals);
-  f(s->ga); f(s->loss_part); f(s->tgt_buf);
+  f(s->ga); f(s->loss_part); f(s->tgt_buf); f(s->nonfinite);
   for (float* g : s->gbase) f(g);
   for (void* p : s->extra_allocs) f(p);
   if (s->ev0) (void)hipEventDestroy(s->ev0);
@@ -817,11 +822,40 @@ void ensure_capacity(ms_sim* s, int64_t n_steps) {
   }
 }
 
+// Failure detection (ms_sim_set_check_feeds): a feed holding NaN or Inf is
+// refused before anything runs; host feeds are scanned on the host, device
+// feeds by a counting kernel.
+void check_feed(ms_sim* s, const ms_feed& f, size_t elems) {
+  int64_t bad = 0;
+  if (!f.on_device) {
+    for (size_t k = 0; k < elems; ++k) bad += std::isfinite(f.data[k]) ? 0 : 1;
+  } else {
+    if (!s->nonfinite) s->nonfinite = dev_alloc<unsigned int>(1);
+    HIPCHECK(hipMemsetAsync(s->nonfinite, 0, sizeof(unsigned int), s->stream));
+    const unsigned blocks = (unsigned)std::min<size_t>(1024, (elems + kBlock - 1) / kBlock);
+    hipLaunchKernelGGL(k_count_nonfinite, dim3(std::max(1u, blocks)), dim3(kBlock), 0, s->stream, f.data,
+                       (int64_t)elems, s->nonfinite);
+    unsigned int h = 0;
+    HIPCHECK(hipMemcpyAsync(&h, s->nonfinite, sizeof(h), hipMemcpyDeviceToHost, s->stream));
+    HIPCHECK(hipStreamSynchronize(s->stream));
+    bad = h;
+  }
+  if (bad)
+    fail(MS_E_NUMERIC, "feed for node " + std::to_string(f.node_id) + " holds " + std::to_string(bad) +
+                           " non-finite values (NaN or Inf)");
+}
+
 void stage_feeds(ms_sim* s, int64_t n_steps, const ms_feed* feeds, int32_t n_feeds) {
   const IR& ir = s->plan->ir;
   const int32_t B = s->B;
   const int32_t fr = ir.feed_rows;
   if (fr == 0) return;
+  if (s->check_feeds)
+    for (int32_t i = 0; i < n_feeds; ++i) {
+      const ms_feed& f = feeds[i];
+      if (f.node_id < 0 || f.node_id >= (int32_t)ir.node_size.size() || !f.data) continue;   // refused below
+      check_feed(s, f, (size_t)B * n_steps * ir.node_size[f.node_id]);
+    }
   HIPCHECK(hipMemsetAsync(s->feed_stage, 0, (size_t)n_steps * fr * B * 4, s->stream));
   for (int32_t i = 0; i < n_feeds; ++i) {
     const ms_feed& f = feeds[i];
@@ -1351,6 +1385,36 @@ static void init_state(ms_sim* s) {
 
 extern "C" {
 
+// MS_LOG (any value but "0"): the plan summary on stderr when a simulator is
+// created: the driver, the merged groups it launches per step (per window for
+// the window driver) with their sizes and kernels' shapes, and the bytes of
+// state and parameters.
+static void log_sim(const ms_sim* s) {
+  const char* e = std::getenv("MS_LOG");
+  if (!e || !*e || std::strcmp(e, "0") == 0) return;
+  const Plan& p = *s->plan;
+  const bool win = s->driver == MS_DRIVER_WINDOW;
+  const std::vector<Launch>& ls = win ? s->wl : s->launches;
+  static const char* dn[] = {"auto", "steps", "graph", "persistent", "window"};
+  int64_t state_b = 0, param_b = 0;
+  for (size_t b = 0; b < p.ir.bases.size(); ++b)
+    (p.ir.bases[b].cls == SC_BATCHED ? state_b : param_b) += p.base_rows[b] * p.ir.bases[b].cols * 4;
+  std::fprintf(stderr, "mergesim: driver %s, minibatch %d, %zu signals, %zu operators in %zu merged groups; "
+               "%zu launches per %s; state %lld B per batch column, parameters %lld B\n",
+               dn[s->driver], s->B, p.ir.sigs.size(), p.ir.ops.size(), p.groups.size(), ls.size(),
+               win ? "window" : "step", (long long)state_b, (long long)param_b);
+  for (size_t k = 0; k < ls.size(); ++k) {
+    const Launch& l = ls[k];
+    std::fprintf(stderr, "mergesim:   %2zu %-16s rows %lld", k, op_type_name(l.type), (long long)l.rows);
+    if (l.type == OP_DOT_INC) std::fprintf(stderr, ", W %d x %d", l.M, l.K);
+    if (l.type == OP_ENS)
+      std::fprintf(stderr, ", <= %d neurons, %d threads, %d columns per workgroup%s%s", l.nmax, l.nthr, l.cpw,
+                   l.rw ? ", weights in registers" : "", l.ens.chain ? ", fused chain" : "");
+    if (win) std::fprintf(stderr, ", level %d", s->wplan->phases[k].level);
+    std::fprintf(stderr, "\n");
+  }
+}
+
 ms_status ms_sim_create(const ms_model* model, const ms_sim_opts* opts, ms_sim** out) {
   return guarded([&] {
     if (!model || !out) fail(MS_E_INVALID, "NULL argument");
@@ -1403,6 +1467,7 @@ ms_status ms_sim_create(const ms_model* model, const ms_sim_opts* opts, ms_sim**
       ensure_capacity(s, std::max<int64_t>(1, o->probe_capacity_steps));
       init_state(s);
       HIPCHECK(hipStreamSynchronize(s->stream));
+      log_sim(s);
     } catch (...) {
       free_sim(s);
       delete s;
@@ -1523,6 +1588,13 @@ ms_status ms_sim_steps(const ms_sim* s, int64_t* out) {
   return guarded([&] {
     if (!s || !out) fail(MS_E_INVALID, "NULL argument");
     *out = s->steps_total;
+  });
+}
+
+ms_status ms_sim_set_check_feeds(ms_sim* s, int32_t on) {
+  return guarded([&] {
+    if (!s) fail(MS_E_INVALID, "NULL sim");
+    s->check_feeds = on != 0;
   });
 }
 

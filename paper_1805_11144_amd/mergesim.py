@@ -110,6 +110,7 @@ _SIGNATURES = [
     ("ms_sim_set_timing", [C.c_void_p, _i32], _i32),
     ("ms_sim_kernel_time", [C.c_void_p, _i32, C.POINTER(C.c_double), C.POINTER(_i64)], _i32),
     ("ms_sim_info", [C.c_void_p, C.POINTER(_i32), C.POINTER(_i32)], _i32),
+    ("ms_sim_set_check_feeds", [C.c_void_p, _i32], _i32),
     ("ms_sim_train_step", [C.c_void_p, _i64, C.POINTER(Feed), _i32, C.POINTER(Target), _i32, C.c_double,
                            _dp], _i32),
     ("ms_sim_train_param", [C.c_void_p, _i32, _i32, _i32, _i32, _fp, _i64, C.POINTER(_i64)], _i32),
@@ -118,8 +119,10 @@ _SIGNATURES = [
 ]
 
 
-def load_library(path: str = LIB_PATH):
-    """Load libmergesim.so; raise loudly if it has not been built."""
+def load_library(path: str = LIB_PATH, host_only: bool = False):
+    """Load libmergesim.so; raise loudly if it has not been built.
+    host_only: the library holds the host part only (model, plan and JSON
+    calls; a sanitizer build of the planner), the simulator calls are absent."""
     global _LIB
     if _LIB is not None:
         return _LIB
@@ -128,7 +131,11 @@ def load_library(path: str = LIB_PATH):
                           "(run `python -c 'import __graft_entry__ as g; g.build()'`)")
     lib = C.CDLL(path)
     for name, args, res in _SIGNATURES:
-        fn = getattr(lib, name)
+        fn = getattr(lib, name, None)
+        if fn is None and host_only and name.startswith("ms_sim_") and name != "ms_sim_opts_default":
+            continue
+        if fn is None:
+            raise ImportError(f"{path} does not export {name}")
         fn.argtypes = args
         fn.restype = res
     _LIB = lib
@@ -473,6 +480,10 @@ class Simulator:
         ms, n = C.c_double(), _i64()
         _check(self._lib.ms_sim_kernel_time(self.handle, int(op_type), C.byref(ms), C.byref(n)))
         return ms.value, n.value
+
+    def set_check_feeds(self, on: bool) -> None:
+        """Refuse feeds that hold NaN or Inf (MS_E_NUMERIC) before each run."""
+        _check(self._lib.ms_sim_set_check_feeds(self.handle, 1 if on else 0))
 
     def info(self):
         d, g = _i32(), _i32()
