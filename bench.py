@@ -41,7 +41,7 @@ WORKLOADS = {
           "array transforms, B=1, T=1000",
     "pes": "online learning: 192-D input -> 9600 LIF -> PES-learned decoders (one 9600x192 matrix "
            "per batch row), error lowpass 0.005, B=10, T=1000",
-    "train": "training step: rate classifier 784-1024-1024-10 (LIF rate), lowpass 0.005, mean squared error "
+    "train": "training step: rate classifier 784-1024-1024-10 (smoothed LIF rate, sigma 0.02), lowpass 0.005, mean squared error "
              "on one-hot targets at every step, gradient through all T=50 steps, B=256, gradient-descent update",
 }
 TRAIN_LR = 1e-4
