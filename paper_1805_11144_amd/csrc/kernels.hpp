@@ -24,6 +24,25 @@ __device__ __forceinline__ gptr<T> G(const T* p) {
   return (gptr<T>)p;
 }
 
+// A record of a table that no kernel writes while it runs (group descriptors,
+// per-op records), read word by word through the constant address space.  At a
+// workgroup-uniform address the compiler then issues scalar loads; through a
+// generic pointer it must use vector loads in any kernel that also stores,
+// since it cannot prove the table unchanged.
+template <class T>
+using kptr = const __attribute__((address_space(4))) T*;
+template <class T>
+__device__ __forceinline__ T kload(const T* p) {
+  static_assert(sizeof(T) % 4 == 0, "records of whole 32-bit words");
+  struct Words {
+    int32_t v[sizeof(T) / 4];
+  } x;
+  kptr<int32_t> w = (kptr<int32_t>)p;
+#pragma unroll
+  for (int i = 0; i < (int)(sizeof(T) / 4); ++i) x.v[i] = w[i];
+  return __builtin_bit_cast(T, x);
+}
+
 // Row of the r-th work item of an operand: slice start + r, or idx[r].
 struct Opnd {
   const int32_t* idx;
@@ -399,8 +418,8 @@ __device__ __forceinline__ float wave_sum(float x) {
          __builtin_bit_cast(float, __builtin_amdgcn_readlane(xi, 48));
 }
 
-__device__ __forceinline__ EnsOp load_op(const EnsOp* ops, int op) {
-  gptr<int32_t> w = G(reinterpret_cast<const int32_t*>(ops + op));
+template <class P>
+__device__ __forceinline__ EnsOp op_from_words(P w) {
   EnsOp o;
   o.n = w[0]; o.x = w[1]; o.enc = w[2]; o.bias = w[3]; o.V = w[4]; o.ref = w[5]; o.s = w[6];
   o.inv_tau = __builtin_bit_cast(float, w[7]);
@@ -411,6 +430,15 @@ __device__ __forceinline__ EnsOp load_op(const EnsOp* ops, int op) {
   o.full = __builtin_bit_cast(float, w[15]);
   o.tau6 = __builtin_bit_cast(float, w[16]);
   return o;
+}
+
+__device__ __forceinline__ EnsOp load_op(const EnsOp* ops, int op) {
+  return op_from_words(G(reinterpret_cast<const int32_t*>(ops + op)));
+}
+
+// The same record at a wavefront-uniform index, through scalar loads (kload).
+__device__ __forceinline__ EnsOp load_op_uniform(const EnsOp* ops, int op) {
+  return op_from_words((kptr<int32_t>)reinterpret_cast<const int32_t*>(ops + op));
 }
 
 // Decoded-output bucket: the smallest of 0, 1, 2, 4, 8, 16 that holds n outputs.
@@ -485,7 +513,7 @@ __device__ __forceinline__ void ens_op_wave_t(float* st, const Strides& S, int64
 
 __device__ __forceinline__ void ens_op_wave(float* st, const Strides& S, int64_t b, const EnsDesc& E, int op,
                                             int lane, float dt) {
-  const EnsOp o = load_op(E.ops, op);
+  const EnsOp o = load_op_uniform(E.ops, op);
   switch (dec_bucket(E.ndec)) {
     case 0: ens_op_wave_t<0>(st, S, b, E, o, lane, dt); break;
     case 1: ens_op_wave_t<1>(st, S, b, E, o, lane, dt); break;
@@ -1240,64 +1268,85 @@ k_persistent(float* state, int64_t rows, int32_t B, const GroupDesc* groups, int
   }
   for (int64_t k = 0; k < n_steps; ++k) {
     for (int32_t g = 0; g < ng; ++g) {
-      const GroupDesc& G = groups[g];   // (::G is the address-space helper)
-      const int64_t nrow = G.rows;
-      switch (G.type) {
-        case ms::OP_FEED:
+      // descriptor fields through kload: scalar loads of a table the kernel never writes
+      const GroupDesc* gp = groups + g;
+      const int64_t nrow = kload(&gp->rows);
+      switch (kload(&gp->type)) {
+        case ms::OP_FEED: {
+          const Opnd dst = kload(&gp->dst);
+          gptr<int32_t> fr = ::G(kload(&gp->feed_row));
+          for (int64_t r = tid; r < nrow; r += nt) st[rowof(dst, r)] = stage[(k * feed_rows + fr[r]) * B + col];
+          break;
+        }
+        case ms::OP_RESET: {
+          const Opnd dst = kload(&gp->dst);
+          const float* values = kload(&gp->values);
+          for (int64_t r = tid; r < nrow; r += nt) st[rowof(dst, r)] = values ? ::G(values)[r] : 0.0f;
+          break;
+        }
+        case ms::OP_COPY: {
+          const Opnd dst = kload(&gp->dst), src = kload(&gp->src);
+          const int32_t bcast = kload(&gp->bcast);
+          gptr<float> sb = ::G(kload(&gp->src_base));
           for (int64_t r = tid; r < nrow; r += nt)
-            st[rowof(G.dst, r)] = stage[(k * feed_rows + ::G(G.feed_row)[r]) * B + col];
+            st[rowof(dst, r)] = bcast ? sb[rowof(src, r)] : st[rowof(src, r)];
           break;
-        case ms::OP_RESET:
-          for (int64_t r = tid; r < nrow; r += nt) st[rowof(G.dst, r)] = G.values ? ::G(G.values)[r] : 0.0f;
-          break;
-        case ms::OP_COPY:
-          for (int64_t r = tid; r < nrow; r += nt)
-            st[rowof(G.dst, r)] = G.bcast ? ::G(G.src_base)[rowof(G.src, r)] : st[rowof(G.src, r)];
-          break;
-        case ms::OP_COPY_INC:
+        }
+        case ms::OP_COPY_INC: {
+          const Opnd dst = kload(&gp->dst), src = kload(&gp->src);
+          const int32_t bcast = kload(&gp->bcast);
+          gptr<float> sb = ::G(kload(&gp->src_base));
+          const int32_t* ptr = kload(&gp->ptr);
           for (int64_t r = tid; r < nrow; r += nt) {
-            const int64_t di = rowof(G.dst, r);
+            const int64_t di = rowof(dst, r);
             float acc = st[di];
-            if (G.ptr) {
-              for (int32_t e = ::G(G.ptr)[r]; e < ::G(G.ptr)[r + 1]; ++e)
-                acc += G.bcast ? ::G(G.src_base)[rowof(G.src, e)] : st[rowof(G.src, e)];
+            if (ptr) {
+              for (int32_t e = ::G(ptr)[r]; e < ::G(ptr)[r + 1]; ++e)
+                acc += bcast ? sb[rowof(src, e)] : st[rowof(src, e)];
             } else {
-              acc += G.bcast ? ::G(G.src_base)[rowof(G.src, r)] : st[rowof(G.src, r)];
+              acc += bcast ? sb[rowof(src, r)] : st[rowof(src, r)];
             }
             st[di] = acc;
           }
           break;
-        case ms::OP_ELEM_INC:
+        }
+        case ms::OP_ELEM_INC: {
+          const Opnd dst = kload(&gp->dst), src = kload(&gp->src), a = kload(&gp->a);
+          gptr<float> ab = ::G(kload(&gp->a_base));
+          const int32_t* ptr = kload(&gp->ptr);
           for (int64_t r = tid; r < nrow; r += nt) {
-            const int64_t di = rowof(G.dst, r);
+            const int64_t di = rowof(dst, r);
             float acc = st[di];
-            if (G.ptr) {
-              for (int32_t e = ::G(G.ptr)[r]; e < ::G(G.ptr)[r + 1]; ++e)
-                acc += ::G(G.a_base)[rowof(G.a, e)] * st[rowof(G.src, e)];
+            if (ptr) {
+              for (int32_t e = ::G(ptr)[r]; e < ::G(ptr)[r + 1]; ++e) acc += ab[rowof(a, e)] * st[rowof(src, e)];
             } else {
-              acc += ::G(G.a_base)[rowof(G.a, r)] * st[rowof(G.src, r)];
+              acc += ab[rowof(a, r)] * st[rowof(src, r)];
             }
             st[di] = acc;
           }
           break;
+        }
         case ms::OP_DOT_INC: {
-          // Weights are stored transposed per op ([K][M], G.wt_base) so that
+          // Weights are stored transposed per op ([K][M], wt_base) so that
           // lanes over output rows read consecutive weights.  The K range is
-          // split into G.tpr parts; part-major work items keep lanes of a
+          // split into tpr parts; part-major work items keep lanes of a
           // wavefront on consecutive rows; parts > 1 add their partial sums
           // through the LDS scratch after the state.
-          const uint32_t M = (uint32_t)G.M, K = (uint32_t)G.K, tpr = (uint32_t)G.tpr;
+          const uint32_t M = (uint32_t)kload(&gp->M), K = (uint32_t)kload(&gp->K), tpr = (uint32_t)kload(&gp->tpr);
+          gptr<float> wt_base = ::G(kload(&gp->wt_base));
+          gptr<int64_t> wt_off = ::G(kload(&gp->wt_off));
+          gptr<int32_t> x_row = ::G(kload(&gp->x_row)), d_row = ::G(kload(&gp->d_row));
           const uint32_t total = (uint32_t)nrow * M;
           const uint32_t chunk = (K + tpr - 1) / tpr;
           for (uint32_t t = tid; t < total * tpr; t += (uint32_t)nt) {
             const uint32_t part = t / total, rowi = t - part * total;
             const uint32_t op = rowi / M, m = rowi - op * M;
-            gptr<float> w = ::G(G.wt_base) + (int64_t)::G(G.wt_off)[op];
-            const int64_t x0 = ::G(G.x_row)[op];
+            gptr<float> w = wt_base + wt_off[op];
+            const int64_t x0 = x_row[op];
             const uint32_t k0 = part * chunk, k1 = min(K, k0 + chunk);
             float acc = 0.0f;
             for (uint32_t kk = k0; kk < k1; ++kk) acc += w[(int64_t)kk * M + m] * st[x0 + kk];
-            if (tpr == 1) st[(int64_t)::G(G.d_row)[op] + m] += acc;
+            if (tpr == 1) st[(int64_t)d_row[op] + m] += acc;
             else scratch[t] = acc;
           }
           if (tpr > 1) {
@@ -1306,23 +1355,34 @@ k_persistent(float* state, int64_t rows, int32_t B, const GroupDesc* groups, int
               const uint32_t op = rowi / M, m = rowi - op * M;
               float acc = 0.0f;
               for (uint32_t p2 = 0; p2 < tpr; ++p2) acc += scratch[p2 * total + rowi];
-              st[(int64_t)::G(G.d_row)[op] + m] += acc;
+              st[(int64_t)d_row[op] + m] += acc;
             }
           }
           break;
         }
-        case ms::OP_LIF:
-          for (int64_t r = tid; r < nrow; r += nt) lif_item(st, S, r, b, G.src, G.dst, G.V, G.ref, G.np, dt);
+        case ms::OP_LIF: {
+          const Opnd src = kload(&gp->src), dst = kload(&gp->dst), V = kload(&gp->V), ref = kload(&gp->ref);
+          const NeuronParams np = kload(&gp->np);
+          for (int64_t r = tid; r < nrow; r += nt) lif_item(st, S, r, b, src, dst, V, ref, np, dt);
           break;
-        case ms::OP_LIF_RATE:
-          for (int64_t r = tid; r < nrow; r += nt) lif_rate_item(st, S, r, b, G.src, G.dst, G.np);
+        }
+        case ms::OP_LIF_RATE: {
+          const Opnd src = kload(&gp->src), dst = kload(&gp->dst);
+          const NeuronParams np = kload(&gp->np);
+          for (int64_t r = tid; r < nrow; r += nt) lif_rate_item(st, S, r, b, src, dst, np);
           break;
-        case ms::OP_LOWPASS:
-          for (int64_t r = tid; r < nrow; r += nt) lowpass_item(st, S, r, b, G.dst, G.src, G.fp);
+        }
+        case ms::OP_LOWPASS: {
+          const Opnd dst = kload(&gp->dst), src = kload(&gp->src);
+          const FilterParams fp = kload(&gp->fp);
+          for (int64_t r = tid; r < nrow; r += nt) lowpass_item(st, S, r, b, dst, src, fp);
           break;
-        case ms::OP_ENS:
-          for (int op = wave; op < nrow; op += nwaves) ens_op_wave(st, S, b, G.ens, op, lane, dt);
+        }
+        case ms::OP_ENS: {
+          const EnsDesc E = kload(&gp->ens);
+          for (int op = wave; op < nrow; op += nwaves) ens_op_wave(st, S, b, E, op, lane, dt);
           break;
+        }
         default: break;
       }
       __syncthreads();
