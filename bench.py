@@ -596,6 +596,8 @@ def main():
     ap.add_argument("--no-sort", action="store_true", help="ablation: signals and operators in build order")
     ap.add_argument("--no-simplify", action="store_true", help="ablation: skip simplification")
     ap.add_argument("--no-fuse", action="store_true", help="ablation: no fused ensemble operators")
+    ap.add_argument("--spike-bits", action="store_true",
+                    help="record spike probes as one bit per neuron and step (window driver)")
     ap.add_argument("--event-decode", action="store_true",
                     help="event-driven decoding (reads the decoders of spiking neurons only); not the "
                          "method's dense work, so the roofline uses measured counter bytes")
@@ -629,7 +631,8 @@ def main():
     plan_opts = dict(planner=M.PLANNER_TREE if args.planner == "tree" else M.PLANNER_GREEDY,
                      planner_depth=args.planner_depth, merge=not args.no_merge, sort=not args.no_sort,
                      simplify=not args.no_simplify, fuse=not args.no_fuse,
-                     decode="event" if args.event_decode else "dense")
+                     decode="event" if args.event_decode else "dense",
+                     spike_probe_bits=args.spike_bits)
     sim = M.Simulator(model, minibatch=w.minibatch, driver=driver, unroll=args.unroll,
                       probe_capacity_steps=w.n_steps, gemm_dtype=args.gemm_dtype, **plan_opts)
     t_build = time.perf_counter() - t_build
@@ -687,7 +690,7 @@ def main():
                    "plan": {"planner": args.planner, "depth": args.planner_depth, "merge": not args.no_merge,
                             "sort": not args.no_sort, "simplify": not args.no_simplify,
                             "fuse": not args.no_fuse},
-                   "decode": "event" if args.event_decode else "dense"},
+                   "decode": "event" if args.event_decode else "dense", "spike_probe_bits": args.spike_bits},
         "runs": {"device_ms": [round(x, 4) for x in run_ms], "mean_ms": round(run_mean, 4),
                  "ci95_ms": None if run_ci is None else round(run_ci, 4),
                  "value_ci95": None if run_ci is None else

@@ -249,6 +249,10 @@ typedef struct {
   int64_t probe_capacity_steps; /* initial probe/feed staging capacity */
   int32_t gemm_dtype;         /* MS_GEMM_F32 (default) or MS_GEMM_BF16 */
   int32_t decode;             /* MS_DECODE_DENSE (default) or MS_DECODE_EVENT */
+  int32_t spike_probe_bits;   /* 1: spike probes (MS_REF_NEURONS targets of
+                                 spiking LIF ensembles, no synapse) are recorded
+                                 as one bit per neuron and step (window driver
+                                 only; see ms_sim_probe_read_bits); default 0 */
 } ms_sim_opts;
 
 /* Fill `opts` with the defaults listed above. */
@@ -322,6 +326,18 @@ ms_status ms_sim_probe_width(const ms_sim* sim, int32_t probe_id, int32_t* width
  * minibatch * steps * width. */
 ms_status ms_sim_probe_read(ms_sim* sim, int32_t probe_id, float* out, int64_t cap_elems,
                             int32_t out_on_device);
+
+/* Spike probe record as bitmasks (paper Sec. 3.1 sim.data of a spike probe;
+ * a spiking neuron's output is 0 or amplitude / dt, so one bit per neuron and
+ * step holds it).  Only for a simulator created with spike_probe_bits = 1 and a
+ * probe recorded that way (else MS_E_INVALID); ms_sim_probe_read of such a
+ * probe expands the bits to the values.  out: [minibatch][steps][nw] uint32,
+ * nw = ceil(width / 32); bit j of word k is neuron 32 k + j of the probe (bits
+ * past the width are 0).  cap_words >= minibatch * steps * nw, else
+ * MS_E_INVALID.  out_on_device: out is device memory on the simulator's GPU;
+ * otherwise host memory (the call then allocates a device staging buffer). */
+ms_status ms_sim_probe_read_bits(ms_sim* sim, int32_t probe_id, uint32_t* out, int64_t cap_words,
+                                 int32_t out_on_device);
 
 /* Probe read that allocates nothing, for callers that cannot allocate device
  * memory (code under HIP graph capture, tight serving loops, harnesses that

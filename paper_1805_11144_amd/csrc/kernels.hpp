@@ -1214,6 +1214,31 @@ __global__ void k_probe_extract(const float* buf, int32_t B, int64_t T, int32_t 
   out[_i] = buf[(t * probe_rows + off + j) * B + b];
 }
 
+// A bit-recorded spike probe read out as values: out[b][t][i] (the layout of
+// every probe read) is `mag` (amplitude / dt) where bit i of step t, column b
+// is set, else 0.  The probe's words start at word row `off` of `words` per step.
+__global__ void k_bits_extract(const uint32_t* bits, int32_t B, int64_t T, int32_t words, int32_t off, int32_t width,
+                               float mag, float* out) {
+  const int64_t n = (int64_t)B * T * width;
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= n) return;
+  const int32_t j = (int32_t)(i % width);
+  const int64_t t = (i / width) % T, b = i / ((int64_t)width * T);
+  const uint32_t m = G(bits)[(t * words + off + j / 32) * B + b];
+  out[i] = ((m >> (j % 32)) & 1u) ? mag : 0.0f;
+}
+
+// The same probe's words, [b][t][k] for k < nw (bit j of word k: neuron 32 k + j).
+__global__ void k_bits_words(const uint32_t* bits, int32_t B, int64_t T, int32_t words, int32_t off, int32_t nw,
+                             uint32_t* out) {
+  const int64_t n = (int64_t)B * T * nw;
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= n) return;
+  const int32_t k = (int32_t)(i % nw);
+  const int64_t t = (i / nw) % T, b = i / ((int64_t)nw * T);
+  out[i] = G(bits)[(t * words + off + k) * B + b];
+}
+
 // ----------------------------------------------------- persistent interpreter
 // A merged group as the persistent kernel sees it (device-resident array).
 struct GroupDesc {

@@ -198,6 +198,33 @@ __global__ void k_w_probe(WView w, const int32_t* src, int32_t probe_rows, float
   buf[((step0 + t) * probe_rows + _r) * w.B + b] = w.va[vat(w, G(src)[_r], w.B + _c)];
 }
 
+// k_w_probe for a subset of the probe rows: entry i copies window row src[i]
+// into row dst[i] of the probe buffer, which holds `stride` rows per step.
+__global__ void k_w_probe_map(WView w, const int32_t* src, const int32_t* dst, int32_t n, int32_t stride, float* buf,
+                              int64_t step0) {
+  W_ITEM(n);
+  const uint32_t t = _c / (uint32_t)w.B, b = _c - t * (uint32_t)w.B;
+  buf[((step0 + t) * stride + G(dst)[_r]) * w.B + b] = w.va[vat(w, G(src)[_r], w.B + _c)];
+}
+
+// Spike probes as bitmasks (a spiking neuron's output is 0 or amplitude / dt):
+// word k of a step and batch column has bit j set when the neuron recorded at
+// src[32 k + j] spiked (a nonzero output); entries of -1 pad a probe to whole
+// words and stay 0.  Lanes run over batch columns, so each of the 32 reads of
+// a thread is one coalesced row segment across its wavefront.
+__global__ void k_w_probe_bits(WView w, const int32_t* src, int32_t words, uint32_t* bits, int64_t step0) {
+  W_ITEM(words);
+  const uint32_t t = _c / (uint32_t)w.B, b = _c - t * (uint32_t)w.B;
+  gptr<int32_t> rs = G(src) + (int64_t)_r * 32;
+  uint32_t m = 0;
+#pragma unroll 8
+  for (int j = 0; j < 32; ++j) {
+    const int32_t r = rs[j];
+    if (r >= 0 && w.va[vat(w, r, w.B + _c)] != 0.0f) m |= 1u << j;
+  }
+  bits[((step0 + t) * words + _r) * w.B + b] = m;
+}
+
 // block 0 <- block T for every row (the values the next window starts from)
 __global__ void k_w_carry(WView w, int64_t rows) {
   W_ROWCOL(rows);

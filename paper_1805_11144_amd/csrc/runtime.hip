@@ -134,6 +134,16 @@ struct ms_sim {
   float* feed_tmp = nullptr;         // [B][T][size] upload buffer for host feeds
   size_t feed_tmp_elems = 0;
   float* probe_buf = nullptr;        // [cap][probe_rows][B]
+  // spike probes recorded as bitmasks (window driver, opts spike_probe_bits):
+  // per probe the spike value amplitude / dt, or 0 for a probe recorded as floats
+  std::vector<float> spike_mag;
+  std::vector<int32_t> bit_off;      // per probe: first word row in bits_buf, or -1
+  int32_t bit_words = 0;             // word rows per step (0: no bit-recorded probe)
+  uint32_t* bits_buf = nullptr;      // [cap][bit_words][B]
+  int32_t* wbit_src = nullptr;       // [bit_words * 32]: window row of each bit, -1 pads
+  int32_t* wprobe_fsrc = nullptr;    // float-recorded probe rows: window source rows
+  int32_t* wprobe_fdst = nullptr;    // ... and their rows in probe_buf
+  int32_t pr_float = 0;
   int64_t probe_cap = 0;
   int32_t probe_rows = 0;
   const int32_t* probe_src = nullptr;
@@ -248,6 +258,7 @@ void free_sim(ms_sim* s) {
   f(s->pes_part);
   f(s->init_vals);
   f(s->ga); f(s->loss_part); f(s->tgt_buf); f(s->nonfinite);
+  f(s->bits_buf); f(s->wbit_src); f(s->wprobe_fsrc); f(s->wprobe_fdst);
   for (float* g : s->gbase) f(g);
   for (void* p : s->extra_allocs) f(p);
   if (s->ev0) (void)hipEventDestroy(s->ev0);
@@ -816,6 +827,18 @@ void ensure_capacity(ms_sim* s, int64_t n_steps) {
       HIPCHECK(hipFree(s->probe_buf));
     }
     s->probe_buf = nb;
+    if (s->bit_words > 0) {
+      const size_t words = (size_t)s->bit_words * B;
+      uint32_t* nbits = dev_alloc<uint32_t>((size_t)cap * words);
+      if (s->bits_buf) {
+        if (s->steps_total > 0)
+          HIPCHECK(hipMemcpyAsync(nbits, s->bits_buf, (size_t)s->steps_total * words * 4, hipMemcpyDeviceToDevice,
+                                  s->stream));
+        HIPCHECK(hipStreamSynchronize(s->stream));
+        HIPCHECK(hipFree(s->bits_buf));
+      }
+      s->bits_buf = nbits;
+    }
     s->probe_cap = cap;
     destroy_graph(s);
     s->persistent_ok = false;
@@ -1112,6 +1135,40 @@ bool bf16_product(const ms_sim* s, const Launch& l) {
   return l.type == OP_DOT_INC && l.a_bcast && l.M >= 64 && l.K >= 16 && l.K % 8 == 0 && s->B % 4 == 0;
 }
 
+// Bit-recorded spike probes: their rows leave the float record (the rows of the
+// other probes keep their places in probe_buf) and their bits go to bits_buf,
+// each probe padded to whole 32-neuron words.
+static void setup_spike_bits(ms_sim* s, const WindowPlan& w) {
+  const Plan& p = *s->plan;
+  const int32_t pr = (int32_t)w.probe_rows.size();
+  if (pr != s->probe_rows) fail(MS_E_INVALID, "window probe rows differ from the plan's");
+  std::vector<int32_t> src((size_t)std::max(1, pr));
+  if (pr > 0) HIPCHECK(hipMemcpy(src.data(), s->wprobe_src, (size_t)pr * 4, hipMemcpyDeviceToHost));
+  std::vector<int32_t> bsrc, fsrc, fdst;
+  s->bit_off.assign(p.probe_width.size(), -1);
+  for (size_t pi = 0; pi < p.probe_width.size(); ++pi) {
+    const int32_t off = p.probe_row_offset[pi], width = p.probe_width[pi];
+    if (s->spike_mag[pi] != 0.0f && width > 0) {
+      s->bit_off[pi] = (int32_t)(bsrc.size() / 32);
+      for (int32_t j = 0; j < width; ++j) bsrc.push_back(src[(size_t)(off + j)]);
+      while (bsrc.size() % 32) bsrc.push_back(-1);
+    } else {
+      for (int32_t j = 0; j < width; ++j) { fsrc.push_back(src[(size_t)(off + j)]); fdst.push_back(off + j); }
+    }
+  }
+  s->bit_words = (int32_t)(bsrc.size() / 32);
+  if (s->bit_words == 0) return;
+  s->pr_float = (int32_t)fsrc.size();
+  s->wbit_src = dev_alloc<int32_t>(bsrc.size());
+  HIPCHECK(hipMemcpy(s->wbit_src, bsrc.data(), bsrc.size() * 4, hipMemcpyHostToDevice));
+  s->wprobe_fsrc = dev_alloc<int32_t>(std::max<size_t>(1, fsrc.size()));
+  s->wprobe_fdst = dev_alloc<int32_t>(std::max<size_t>(1, fdst.size()));
+  if (!fsrc.empty()) {
+    HIPCHECK(hipMemcpy(s->wprobe_fsrc, fsrc.data(), fsrc.size() * 4, hipMemcpyHostToDevice));
+    HIPCHECK(hipMemcpy(s->wprobe_fdst, fdst.data(), fdst.size() * 4, hipMemcpyHostToDevice));
+  }
+}
+
 void setup_window(ms_sim* s) {
   WindowPlan& w = *s->wplan;
   const int32_t B = s->B;
@@ -1127,6 +1184,7 @@ void setup_window(ms_sim* s) {
   std::vector<LGroup> groups;
   for (const WPhase& ph : w.phases) groups.push_back(ph.g);
   build_launches(s, groups, s->wl, w.probe_rows, &s->wprobe_src);
+  if (!s->spike_mag.empty()) setup_spike_bits(s, w);
   for (size_t k = 0; k < s->wl.size(); ++k) {
     Launch& l = s->wl[k];
     l.src_blk = w.phases[k].src_blk;
@@ -1331,7 +1389,14 @@ void run_window(ms_sim* s, int64_t n_steps) {
     }
     const WView v{s->va, s->vs, s->B, T};
     const int32_t pr = (int32_t)w.probe_rows.size();
-    if (pr > 0 && s->B % 4 == 0)
+    if (s->bit_words > 0) {
+      if (s->pr_float > 0)
+        hipLaunchKernelGGL(k_w_probe_map, dim3(grid_items((double)s->pr_float * T * s->B)), dim3(kBlock), 0,
+                           s->stream, v, (const int32_t*)s->wprobe_fsrc, (const int32_t*)s->wprobe_fdst, s->pr_float,
+                           pr, s->probe_buf, s->steps_total + t0);
+      hipLaunchKernelGGL(k_w_probe_bits, dim3(grid_items((double)s->bit_words * T * s->B)), dim3(kBlock), 0,
+                         s->stream, v, (const int32_t*)s->wbit_src, s->bit_words, s->bits_buf, s->steps_total + t0);
+    } else if (pr > 0 && s->B % 4 == 0)
       hipLaunchKernelGGL(k_w_probe4, dim3(grid_items((double)pr * T * s->B / 4)), dim3(kBlock), 0, s->stream, v,
                          s->wprobe_src, pr, s->probe_buf, s->steps_total + t0);
     else if (pr > 0)
@@ -1439,6 +1504,15 @@ ms_status ms_sim_create(const ms_model* model, const ms_sim_opts* opts, ms_sim**
       s->gemm_dtype = o->gemm_dtype;
       s->decode = o->decode;
       s->plan = make_plan(model_of(model), o->dt, plan_opts_from(o));
+      if (o->spike_probe_bits) {
+        const Model& m = model_of(model);
+        s->spike_mag.assign(m.probes.size(), 0.0f);
+        for (size_t i = 0; i < m.probes.size(); ++i) {
+          const ProbeDesc& pd = m.probes[i];
+          if (pd.kind == MS_REF_NEURONS && pd.synapse <= 0.0 && m.ens[(size_t)pd.id].neuron_type == MS_NEURON_LIF)
+            s->spike_mag[i] = (float)m.ens[(size_t)pd.id].amplitude / (float)o->dt;
+        }
+      }
       DeviceGuard dg(s->device);
       if (o->stream) {
         s->stream = (hipStream_t)o->stream;
@@ -1453,6 +1527,8 @@ ms_status ms_sim_create(const ms_model* model, const ms_sim_opts* opts, ms_sim**
         fail(MS_E_INVALID, "the persistent driver cannot run a model with learning rules");
       if (s->gemm_dtype == MS_GEMM_BF16 && s->driver != MS_DRIVER_WINDOW)
         fail(MS_E_INVALID, "bf16 products run on the window driver only");
+      if (o->spike_probe_bits && s->driver != MS_DRIVER_WINDOW)
+        fail(MS_E_INVALID, "spike probes are recorded as bits by the window driver only");
       // persistent: one workgroup per batch column -> column-major state
       s->S = s->driver == MS_DRIVER_PERSISTENT ? Strides{1, (int64_t)std::max<int64_t>(1, s->plan->base_rows.empty() ? 1 : s->plan->base_rows[0])}
                                                : Strides{(int64_t)s->B, 1};
@@ -1626,8 +1702,13 @@ ms_status ms_sim_probe_read(ms_sim* s, int32_t probe, float* out, int64_t cap, i
     if (n == 0) return;
     DeviceGuard dg(s->device);
     float* tmp = out_on_device ? out : dev_alloc<float>((size_t)n);
-    hipLaunchKernelGGL(k_probe_extract, dim3(grid_for(n)), dim3(kBlock), 0, s->stream,
-                       (const float*)s->probe_buf, s->B, T, s->probe_rows, p.probe_row_offset[probe], w, tmp);
+    if (!s->bit_off.empty() && s->bit_off[probe] >= 0)
+      hipLaunchKernelGGL(k_bits_extract, dim3(grid_for(n)), dim3(kBlock), 0, s->stream,
+                         (const uint32_t*)s->bits_buf, s->B, T, s->bit_words, s->bit_off[probe], w,
+                         s->spike_mag[probe], tmp);
+    else
+      hipLaunchKernelGGL(k_probe_extract, dim3(grid_for(n)), dim3(kBlock), 0, s->stream,
+                         (const float*)s->probe_buf, s->B, T, s->probe_rows, p.probe_row_offset[probe], w, tmp);
     hipError_t e = hipGetLastError();
     if (e == hipSuccess && !out_on_device)
       e = hipMemcpyAsync(out, tmp, (size_t)n * 4, hipMemcpyDeviceToHost, s->stream);
@@ -1652,11 +1733,41 @@ ms_status ms_sim_probe_read_static(ms_sim* s, int32_t probe, float* out, int64_t
     if (n == 0) return;
     DeviceGuard dg(s->device);
     float* stage = scratch_on(s->device);
-    hipLaunchKernelGGL(k_probe_extract, dim3(grid_for(n)), dim3(kBlock), 0, s->stream,
-                       (const float*)s->probe_buf, s->B, T, s->probe_rows, p.probe_row_offset[probe], w, stage);
+    if (!s->bit_off.empty() && s->bit_off[probe] >= 0)
+      hipLaunchKernelGGL(k_bits_extract, dim3(grid_for(n)), dim3(kBlock), 0, s->stream,
+                         (const uint32_t*)s->bits_buf, s->B, T, s->bit_words, s->bit_off[probe], w,
+                         s->spike_mag[probe], stage);
+    else
+      hipLaunchKernelGGL(k_probe_extract, dim3(grid_for(n)), dim3(kBlock), 0, s->stream,
+                         (const float*)s->probe_buf, s->B, T, s->probe_rows, p.probe_row_offset[probe], w, stage);
     HIPCHECK(hipGetLastError());
     HIPCHECK(hipMemcpyAsync(out, stage, (size_t)n * 4, hipMemcpyDeviceToHost, s->stream));
     HIPCHECK(hipStreamSynchronize(s->stream));
+  });
+}
+
+ms_status ms_sim_probe_read_bits(ms_sim* s, int32_t probe, uint32_t* out, int64_t cap, int32_t out_on_device) {
+  return guarded([&] {
+    if (!s || !out) fail(MS_E_INVALID, "NULL argument");
+    const Plan& p = *s->plan;
+    if (probe < 0 || probe >= (int32_t)p.probe_width.size()) fail(MS_E_INVALID, "probe id out of range");
+    if (s->bit_off.empty() || s->bit_off[probe] < 0)
+      fail(MS_E_INVALID, "probe " + std::to_string(probe) + " is not recorded as spike bits");
+    const int32_t nw = (p.probe_width[probe] + 31) / 32;
+    const int64_t T = s->steps_total;
+    const int64_t n = (int64_t)s->B * T * nw;
+    if (cap < n) fail(MS_E_INVALID, "probe output capacity too small");
+    if (n == 0) return;
+    DeviceGuard dg(s->device);
+    uint32_t* tmp = out_on_device ? out : dev_alloc<uint32_t>((size_t)n);
+    hipLaunchKernelGGL(k_bits_words, dim3(grid_for(n)), dim3(kBlock), 0, s->stream, (const uint32_t*)s->bits_buf,
+                       s->B, T, s->bit_words, s->bit_off[probe], nw, tmp);
+    hipError_t e = hipGetLastError();
+    if (e == hipSuccess && !out_on_device)
+      e = hipMemcpyAsync(out, tmp, (size_t)n * 4, hipMemcpyDeviceToHost, s->stream);
+    if (e == hipSuccess) e = hipStreamSynchronize(s->stream);
+    if (!out_on_device) (void)hipFree(tmp);
+    if (e != hipSuccess) fail(MS_E_HIP, std::string("probe read: ") + hipGetErrorString(e));
   });
 }
 

@@ -61,7 +61,8 @@ class SimOpts(C.Structure):
                 ("planner_depth", _i32), ("merge", _i32), ("sort", _i32), ("simplify", _i32),
                 ("fuse", _i32),
                 ("driver", _i32), ("device", _i32), ("stream", C.c_void_p),
-                ("probe_capacity_steps", _i64), ("gemm_dtype", _i32), ("decode", _i32)]
+                ("probe_capacity_steps", _i64), ("gemm_dtype", _i32), ("decode", _i32),
+                ("spike_probe_bits", _i32)]
 
 
 class Feed(C.Structure):
@@ -103,6 +104,7 @@ _SIGNATURES = [
     ("ms_sim_probe_width", [C.c_void_p, _i32, C.POINTER(_i32)], _i32),
     ("ms_sim_probe_read", [C.c_void_p, _i32, _fp, _i64, _i32], _i32),
     ("ms_sim_probe_read_static", [C.c_void_p, _i32, _fp, _i64], _i32),
+    ("ms_sim_probe_read_bits", [C.c_void_p, _i32, C.POINTER(C.c_uint32), _i64, _i32], _i32),
     ("ms_sim_reset", [C.c_void_p], _i32),
     ("ms_sim_get_state", [C.c_void_p, _i32, _i32, _fp, _i64], _i32),
     ("ms_sim_set_state", [C.c_void_p, _i32, _i32, _fp, _i64], _i32),
@@ -272,7 +274,7 @@ def model_from_spec(spec) -> Model:
 
 def make_opts(dt=0.001, minibatch=1, unroll=10, planner=PLANNER_TREE, planner_depth=3, merge=True,
               sort=True, simplify=True, fuse=True, driver=DRIVER_AUTO, device=0, stream=None,
-              probe_capacity_steps=1000, gemm_dtype=None, decode=None) -> SimOpts:
+              probe_capacity_steps=1000, gemm_dtype=None, decode=None, spike_probe_bits=False) -> SimOpts:
     o = SimOpts()
     load_library().ms_sim_opts_default(C.byref(o))
     o.dt, o.minibatch, o.unroll = float(dt), int(minibatch), int(unroll)
@@ -288,6 +290,7 @@ def make_opts(dt=0.001, minibatch=1, unroll=10, planner=PLANNER_TREE, planner_de
         o.gemm_dtype = {"f32": GEMM_F32, "bf16": GEMM_BF16}.get(gemm_dtype, gemm_dtype)
     if decode is not None:
         o.decode = {"dense": DECODE_DENSE, "event": DECODE_EVENT}.get(decode, decode)
+    o.spike_probe_bits = int(bool(spike_probe_bits))
     return o
 
 
@@ -444,6 +447,15 @@ class Simulator:
         T = self.n_steps
         out = np.empty((self.minibatch, T, w), np.float32)
         _check(self._lib.ms_sim_probe_read(self.handle, probe, out.ctypes.data_as(_fp), out.size, 0))
+        return out
+
+    def data_bits(self, probe: int) -> np.ndarray:
+        """Spike probe record as bitmasks [B, steps, ceil(width / 32)] uint32
+        (simulators created with spike_probe_bits=True)."""
+        nw = (self.probe_width(probe) + 31) // 32
+        out = np.empty((self.minibatch, self.n_steps, nw), np.uint32)
+        _check(self._lib.ms_sim_probe_read_bits(self.handle, probe, out.ctypes.data_as(C.POINTER(C.c_uint32)),
+                                                out.size, 0))
         return out
 
     def data_static(self, probe: int) -> np.ndarray:
